@@ -1,0 +1,308 @@
+"""CPU oracle for sampling a weighted 3D-Gaussian scalar field (W-VEG).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the smoke check and by
+the benchmark's CPU-baseline leg, never by the product library. It is an
+independent float64 brute-force implementation (oracle.c) of the paper's
+Eq. 2 and Eq. 3 with the cutoff of Sec. 4.1.1 and the definedness rule of
+Sec. 4.1.3, their exact derivatives (Sec. 4.1.4), and the canonical float32
+cell index (Sec. 4.1.1, Sec. 4.1.2).
+
+Every function here is pinned by the tests in tests/test_oracle_*.py against
+closed forms, invariants, finite differences and brute-force recounts.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+from . import build as _build
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+c_i64 = ctypes.c_int64
+c_int = ctypes.c_int
+c_float = ctypes.c_float
+vp = ctypes.c_void_p
+
+
+def lib():
+    global _LIB
+    if _LIB is None:
+        path = os.path.join(_HERE, "liboracle.so")
+        if not os.path.exists(path):
+            _build.build()
+        L = ctypes.CDLL(path)
+        L.orc_forward.restype = c_int
+        L.orc_forward.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, c_int, c_int,
+                                  vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_backward.restype = c_int
+        L.orc_backward.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, vp, vp, vp, vp, vp,
+                                   c_i64, vp, c_int, c_int, vp, vp]
+        L.orc_support.restype = c_int
+        L.orc_support.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, c_i64, vp, c_int, vp]
+        L.orc_voxel_centers.restype = c_int
+        L.orc_voxel_centers.argtypes = [vp, vp, vp, c_i64, vp, vp]
+        L.orc_index_boxes.restype = c_i64
+        L.orc_index_boxes.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp]
+        L.orc_index.restype = c_int
+        L.orc_index.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp, c_i64, vp, vp]
+        L.orc_point_order.restype = c_int
+        L.orc_point_order.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp]
+        _LIB = L
+    return _LIB
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(vp)
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _gauss(g):
+    """float32 parameter arrays for the canonical index."""
+    return (_f32(g.mean).reshape(-1, 3), _f32(g.scale).reshape(-1, 3), _f32(g.rot).reshape(-1, 4),
+            _f32(g.value).reshape(-1), _f32(g.weight).reshape(-1))
+
+
+def _gauss64(g):
+    """float64 parameter arrays (exact copies of float32 inputs, or float64
+    values for finite-difference probes)."""
+    return (_f64(g.mean).reshape(-1, 3), _f64(g.scale).reshape(-1, 3), _f64(g.rot).reshape(-1, 4),
+            _f64(g.value).reshape(-1), _f64(g.weight).reshape(-1))
+
+
+def _box(lo, hi):
+    return _f32(np.asarray(lo, dtype=np.float32).reshape(3)), _f32(np.asarray(hi, dtype=np.float32).reshape(3))
+
+
+def default_threads() -> int:
+    v = os.environ.get("OMP_NUM_THREADS")
+    if v and v.isdigit() and int(v) > 0:
+        return int(v)
+    return max(1, os.cpu_count() or 1)
+
+
+class ForwardResult:
+    def __init__(self, n):
+        self.phi = np.zeros(n)
+        self.inf = np.zeros(n)
+        self.defined = np.zeros(n, dtype=np.int32)
+        self.ncontrib = np.zeros(n, dtype=np.int32)
+        self.namb = np.zeros(n, dtype=np.int32)
+        self.i_base = np.zeros(n)
+        self.v_base = np.zeros(n)
+        self.amb_a = np.zeros((n, 4))
+        self.amb_v = np.zeros((n, 4))
+        self.b_phi = np.zeros(n)
+        self.b_inf = np.zeros(n)
+
+
+def forward(g, points, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01, prune: bool = True,
+            threads: int = 0) -> ForwardResult:
+    """Eq. 2 at every point by brute force over all Gaussians (float64)."""
+    m, s, q, v, w = _gauss64(g)
+    pts = _f64(points).reshape(-1, 3)
+    lo_, hi_ = _box(lo, hi)
+    n = pts.shape[0]
+    r = ForwardResult(n)
+    rc = lib().orc_forward(m.shape[0], _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), tau, n, _p(pts),
+                           int(prune), threads or default_threads(),
+                           _p(r.phi), _p(r.inf), _p(r.defined), _p(r.ncontrib), _p(r.namb), _p(r.i_base),
+                           _p(r.v_base), _p(r.amb_a), _p(r.amb_v), _p(r.b_phi), _p(r.b_inf))
+    if rc != 0:
+        raise RuntimeError(f"orc_forward failed ({rc})")
+    return r
+
+
+def backward(g, points, phi, inf, g_phi, g_inf, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01,
+             zero_mask=None, select=None, prune: bool = True, threads: int = 0):
+    """Exact gradients (float64) of L = sum gPhi*Phi + gI*I with respect to
+    every parameter of the selected Gaussians (all when select is None).
+    Returns (grad, abs_sum), each [nsel, 12] = dmu(3), ds(3), dq(4), dv, dw."""
+    m, s, q, v, w = _gauss64(g)
+    pts = _f64(points).reshape(-1, 3)
+    n = pts.shape[0]
+    lo_, hi_ = _box(lo, hi)
+    phi = np.ascontiguousarray(phi, dtype=np.float64)
+    inf = np.ascontiguousarray(inf, dtype=np.float64)
+    gp = _f64(g_phi)
+    gi = _f64(g_inf)
+    zm = None if zero_mask is None else np.ascontiguousarray(zero_mask, dtype=np.uint8)
+    sel = None if select is None else np.ascontiguousarray(select, dtype=np.int64)
+    nsel = m.shape[0] if sel is None else sel.shape[0]
+    grad = np.zeros((nsel, 12))
+    ab = np.zeros((nsel, 12))
+    rc = lib().orc_backward(m.shape[0], _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), tau, n, _p(pts),
+                            _p(phi), _p(inf), _p(gp), _p(gi), _p(zm), nsel, _p(sel), int(prune),
+                            threads or default_threads(), _p(grad), _p(ab))
+    if rc != 0:
+        raise RuntimeError(f"orc_backward failed ({rc})")
+    return grad, ab
+
+
+def support(g, points, select, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01, threads: int = 0):
+    """Mask of points within the cutoff (plus ambiguity band) of any selected Gaussian."""
+    m, s, q, v, w = _gauss64(g)
+    pts = _f64(points).reshape(-1, 3)
+    lo_, hi_ = _box(lo, hi)
+    sel = np.ascontiguousarray(select, dtype=np.int64)
+    out = np.zeros(pts.shape[0], dtype=np.uint8)
+    rc = lib().orc_support(m.shape[0], _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), tau,
+                           pts.shape[0], _p(pts), sel.shape[0], _p(sel), threads or default_threads(), _p(out))
+    if rc != 0:
+        raise RuntimeError(f"orc_support failed ({rc})")
+    return out.astype(bool)
+
+
+def voxel_centers(dims, lo=(0, 0, 0), hi=(1, 1, 1), ids=None) -> np.ndarray:
+    """Canonical float32 voxel centres (x fastest ids); all voxels when ids is None."""
+    d = np.asarray(dims, dtype=np.int32).reshape(3)
+    lo_, hi_ = _box(lo, hi)
+    if ids is None:
+        n = int(d[0]) * int(d[1]) * int(d[2])
+        idp = None
+    else:
+        ids = np.ascontiguousarray(ids, dtype=np.uint32)
+        n = ids.shape[0]
+        idp = ids
+    out = np.zeros((n, 3), dtype=np.float32)
+    rc = lib().orc_voxel_centers(_p(d), _p(lo_), _p(hi_), n, _p(idp), _p(out))
+    if rc != 0:
+        raise RuntimeError("orc_voxel_centers failed")
+    return out
+
+
+def index_boxes(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01):
+    """Canonical float32 cell box per Gaussian ([n,6], -1 when empty) and pair counts."""
+    m, s, q, v, w = _gauss(g)
+    c = np.asarray(cells, dtype=np.int32).reshape(3)
+    lo_, hi_ = _box(lo, hi)
+    n = m.shape[0]
+    box = np.zeros((n, 6), dtype=np.int32)
+    cnt = np.zeros(n, dtype=np.int64)
+    P = lib().orc_index_boxes(n, _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), _p(c), tau, _p(box), _p(cnt))
+    if P < 0:
+        raise ValueError("orc_index_boxes: bad arguments")
+    return box, cnt
+
+
+def index(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01):
+    """Canonical index: (keys, gids, cell_offsets) with pairs ordered by (key, gid)."""
+    m, s, q, v, w = _gauss(g)
+    c = np.asarray(cells, dtype=np.int32).reshape(3)
+    lo_, hi_ = _box(lo, hi)
+    n = m.shape[0]
+    _, cnt = index_boxes(g, cells, lo, hi, tau)
+    P = int(cnt.sum())
+    keys = np.zeros(max(P, 1), dtype=np.uint32)
+    gids = np.zeros(max(P, 1), dtype=np.uint32)
+    ncells = int(c[0]) * int(c[1]) * int(c[2])
+    offs = np.zeros(ncells + 1, dtype=np.uint32)
+    npairs = c_i64(0)
+    rc = lib().orc_index(n, _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), _p(c), tau, _p(keys), _p(gids),
+                         P, _p(offs), ctypes.byref(npairs))
+    if rc != 0:
+        raise RuntimeError(f"orc_index failed ({rc})")
+    return keys[:P], gids[:P], offs
+
+
+def point_order(points, cells, lo=(0, 0, 0), hi=(1, 1, 1)):
+    """Points ordered by (cell key, id); outside points take key ncells.
+    Returns (keys_sorted, order, point_offsets[ncells+2])."""
+    pts = _f32(points).reshape(-1, 3)
+    c = np.asarray(cells, dtype=np.int32).reshape(3)
+    lo_, hi_ = _box(lo, hi)
+    n = pts.shape[0]
+    ncells = int(c[0]) * int(c[1]) * int(c[2])
+    keys = np.zeros(max(n, 1), dtype=np.uint32)
+    order = np.zeros(max(n, 1), dtype=np.uint32)
+    offs = np.zeros(ncells + 2, dtype=np.uint32)
+    rc = lib().orc_point_order(n, _p(pts), _p(lo_), _p(hi_), _p(c), _p(keys), _p(order), _p(offs))
+    if rc != 0:
+        raise RuntimeError("orc_point_order failed")
+    return keys[:n], order[:n], offs
+
+
+def accept_forward(ref: ForwardResult, phi_gpu, inf_gpu, tau: float = 0.01, rtol: float = 1e-5,
+                   atol_phi: float = 1e-7, max_amb: int = 4):
+    """Element-wise parity verdict for float32 forward outputs against the
+    oracle. At a point that is not ambiguous: |Phi - ref| <= rtol |ref| +
+    B_Phi + atol and |I - ref| <= rtol ref + B_I, both sides defined or
+    undefined alike. At an ambiguous point (a pair within the float32 band of
+    the cutoff, or I within 2^-16 tau of tau) the result must match one of the
+    oracle's variants (each ambiguous pair in or out, and either side of the
+    definedness threshold when I is that close to it). Returns (ok_mask,
+    stats)."""
+    phi_gpu = np.asarray(phi_gpu, dtype=np.float64)
+    inf_gpu = np.asarray(inf_gpu, dtype=np.float64)
+    n = ref.phi.shape[0]
+    tau64 = float(np.float32(tau))
+    band_i = 2.0 ** -16 * tau64
+
+    def close(phi_r, inf_r, defined_r, bphi, binf):
+        ok_def = defined_r & (np.abs(phi_gpu - phi_r) <= rtol * np.abs(phi_r) + bphi + atol_phi) & \
+            (np.abs(inf_gpu - inf_r) <= rtol * inf_r + binf)
+        ok_und = (~defined_r) & (phi_gpu == 0.0) & (inf_gpu == 0.0)
+        return ok_def | ok_und
+
+    defined = ref.defined.astype(bool)
+    ok = close(ref.phi, ref.inf, defined, ref.b_phi, ref.b_inf)
+    near_tau = np.abs(ref.inf - tau64) <= band_i
+    amb_pt = (ref.namb > 0) | near_tau
+    # variants: every subset of the first min(namb, 4) ambiguous pairs
+    idx = np.nonzero(amb_pt & ~ok)[0]
+    too_many = 0
+    for p in idx:
+        k = int(ref.namb[p])
+        if k > max_amb:
+            # counted and reported, not judged
+            too_many += 1
+            ok[p] = True
+            continue
+        good = False
+        for mask in range(1 << k):
+            I = ref.i_base[p] + sum(ref.amb_a[p, j] for j in range(k) if mask >> j & 1)
+            V = ref.v_base[p] + sum(ref.amb_a[p, j] * ref.amb_v[p, j] for j in range(k) if mask >> j & 1)
+            ph = V / I if I > 0 else 0.0
+            for dflag in (True, False):
+                if dflag and not (I > tau64 - band_i):
+                    continue
+                if (not dflag) and not (I <= tau64 + band_i):
+                    continue
+                if dflag:
+                    if abs(phi_gpu[p] - ph) <= rtol * abs(ph) + ref.b_phi[p] + atol_phi and \
+                            abs(inf_gpu[p] - I) <= rtol * I + ref.b_inf[p]:
+                        good = True
+                else:
+                    if phi_gpu[p] == 0.0 and inf_gpu[p] == 0.0:
+                        good = True
+                if good:
+                    break
+            if good:
+                break
+        ok[p] = good
+    stats = {
+        "n": n,
+        "defined": int(defined.sum()),
+        "ambiguous": int(amb_pt.sum()),
+        "ambiguous_unchecked": too_many,
+        "failed": int((~ok).sum()),
+        "used_allowance": int((defined & ok & ((np.abs(phi_gpu - ref.phi) > rtol * np.abs(ref.phi) + atol_phi) |
+                                               (np.abs(inf_gpu - ref.inf) > rtol * ref.inf))).sum()),
+    }
+    return ok, stats
+
+
+def ambiguous_points(ref: ForwardResult, tau: float = 0.01) -> np.ndarray:
+    tau64 = float(np.float32(tau))
+    return (ref.namb > 0) | (np.abs(ref.inf - tau64) <= 2.0 ** -16 * tau64)
