@@ -1,0 +1,203 @@
+/*
+ * gs.h - point sampling of a learned 3D-Gaussian scalar field (W-VEG) on
+ * AMD Instinct MI355X (gfx950), forward and backward.
+ *
+ * The field (paper Sec. 3.2, Eq. 2 and Eq. 3):
+ *   Gaussian i has mean mu_i, per-axis standard deviations s_i, a rotation
+ *   given by the quaternion q_i = (w, x, y, z) (normalised inside the library,
+ *   Hamilton convention, rotating the Gaussian's local axes into world axes),
+ *   a value v_i and a weight w_i.
+ *   Q_i(p) = || S_i^-1 R(q_i)^T (p - mu_i) ||^2,  G_i(p) = exp(-Q_i(p) / 2).
+ *   Gaussian i intersects p when G_i(p) >= tau (the cutoff of Sec. 4.1.1),
+ *   i.e. Q_i(p) <= 2 ln(1/tau). Over the intersecting Gaussians
+ *   I(p) = sum w_i G_i(p) and V(p) = sum w_i v_i G_i(p).
+ *   A query point is defined when it lies in the closed box of the grid and
+ *   I(p) > tau (Sec. 4.1.3); its outputs are then (Phi, I) = (V/I, I), and
+ *   (0, 0) otherwise.
+ *
+ * Conventions for every entry point:
+ *   - All array arguments are device pointers to memory the caller allocated
+ *     and owns (hipMalloc or a framework allocator). The library allocates no
+ *     device memory; the workspaces it needs are passed in, sized by the
+ *     *_bytes functions. Workspace pointers must be 256-byte aligned.
+ *   - Work is enqueued on the caller's stream and is asynchronous, except that
+ *     gs_build_index waits once for the number of Gaussian-cell pairs.
+ *   - Errors are reported as gs_status codes; gs_last_error() returns a
+ *     message for the calling thread. Nothing throws across this interface.
+ *   - Host-side arguments are validated (null pointers, negative counts,
+ *     empty or non-finite grids, workspace sizes, query shapes). Device data
+ *     is not: a Gaussian with a non-finite parameter, a non-positive scale or
+ *     a quaternion whose float32 squared norm is zero or not finite
+ *     contributes nothing anywhere; an out-of-range voxel id is a point
+ *     outside the domain.
+ *   - Parameters are taken after the paper's activations (Sec. 4.2: exp for
+ *     scales, sigmoid for values and weights, with any soft cap applied by
+ *     the caller); gradients are returned with respect to those same
+ *     parameters, and for the quaternion with respect to the raw (not
+ *     normalised) input.
+ */
+#ifndef GS_H
+#define GS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gs_status {
+    GS_OK = 0,
+    GS_ERR_INVALID_ARGUMENT = 1, /* a host-side argument is invalid */
+    GS_ERR_CAPACITY = 2,         /* the pair buffers of an index are too small */
+    GS_ERR_WORKSPACE = 3,        /* a workspace is too small or misaligned */
+    GS_ERR_HIP = 4               /* a HIP runtime call failed */
+} gs_status;
+
+/* The Gaussians (Sec. 3.2: mu, S, R, v, w of each W-VEG primitive). */
+typedef struct gs_gaussians {
+    int64_t n;           /* number of Gaussians, 0 <= n < 2^31 */
+    const float *mean;   /* [n][3] */
+    const float *scale;  /* [n][3] standard deviations along the local axes */
+    const float *rot;    /* [n][4] quaternion (w, x, y, z), any non-zero norm */
+    const float *value;  /* [n] */
+    const float *weight; /* [n] */
+} gs_gaussians;
+
+/* The domain box [lo, hi] (closed) and the grid of index cells over it.
+ * Cells play the role of the paper's volume blocks (Sec. 4.1.1, Fig. 4):
+ * each cell gets the list of Gaussians whose cutoff box overlaps it. */
+typedef struct gs_grid {
+    float lo[3];
+    float hi[3];
+    int32_t cells[3]; /* cells per axis, each > 0, product < 2^31 */
+} gs_grid;
+
+/* A built index. The caller fills the buffer fields; gs_build_index fills
+ * the rest. The pair lists are the paper's block intersection lists
+ * (Sec. 4.1.2): pairs (cell key, Gaussian id) with
+ * key = cx + Cx (cy + Cy cz), ordered by key and, within a key, by
+ * increasing Gaussian id; cell_offsets[k] is the number of pairs with
+ * key < k, so the list of cell k is [cell_offsets[k], cell_offsets[k+1]). */
+typedef struct gs_index {
+    /* caller-owned device buffers */
+    uint32_t *keys;         /* [capacity] */
+    uint32_t *gids;         /* [capacity] */
+    uint32_t *cell_offsets; /* [ncells + 1] */
+    int64_t capacity;       /* pairs the two buffers above can hold */
+    void *work;             /* gs_index_work_bytes() bytes; after the build it
+                               holds per-Gaussian records read by gs_sample and
+                               gs_sample_backward: keep it unchanged while the
+                               index is in use */
+    size_t work_bytes;
+    /* filled by gs_build_index */
+    int64_t n_pairs;  /* number of pairs (also set on GS_ERR_CAPACITY) */
+    int64_t n_gauss;  /* Gaussians the index was built from */
+    gs_grid grid;     /* copy of the grid */
+    float tau;        /* copy of the cutoff */
+} gs_index;
+
+/* Query kinds. GRID: every voxel centre of a dims[0] x dims[1] x dims[2]
+ * grid spanning the index box, outputs in x-fastest order; dims must be a
+ * multiple of the index cells on every axis. VOXELS: the centres of the
+ * listed voxel ids (id = x + dims0 (y + dims1 z)) of such a grid (any dims),
+ * outputs in list order. POINTS: arbitrary positions, outputs in input
+ * order. The centre of voxel (i, j, k) is lo + (i + 1/2) * ((hi - lo) / dims)
+ * per axis, in float32 with each operation rounded. */
+enum { GS_QUERY_GRID = 0, GS_QUERY_VOXELS = 1, GS_QUERY_POINTS = 2 };
+
+typedef struct gs_query {
+    int32_t kind;
+    int32_t dims[3];            /* GRID, VOXELS */
+    int64_t n;                  /* VOXELS, POINTS: number of queries, < 2^31 */
+    const uint32_t *voxel_ids;  /* VOXELS: [n] */
+    const float *points;        /* POINTS: [n][3] */
+} gs_query;
+
+/* Number of outputs of a query (dims product for GRID, n otherwise), or -1
+ * when the query is malformed. */
+int64_t gs_query_size(const gs_query *query);
+
+/* Bytes of index workspace for n_gauss Gaussians, a grid and a pair
+ * capacity (per-Gaussian records and boxes, scan and sort buffers). */
+size_t gs_index_work_bytes(int64_t n_gauss, const gs_grid *grid, int64_t capacity);
+
+/*
+ * Build the cell index (Sec. 4.1.1 and Sec. 4.1.2, Fig. 4 A-B): per
+ * Gaussian, the axis-aligned box of its cutoff ellipsoid Q <= 2 ln(1/tau)
+ * in cells, the per-cell intersection lists and their ranges. tau is the
+ * paper's tau_1 (0.01 in its evaluation), 0 < tau < 1.
+ * Boxes are computed in float32 in one fixed order of operations, so the
+ * index is reproducible bit for bit. The half-extent along axis j is
+ * r * sqrt(Sigma_jj) with r = sqrt(2 ln(1/tau)) (1 + 2^-10).
+ * Waits on the stream once, for the pair count. If it exceeds the capacity,
+ * returns GS_ERR_CAPACITY with index->n_pairs set to the count needed and the
+ * index left unusable.
+ */
+gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float tau, gs_index *index,
+                         hipStream_t stream);
+
+/* Bytes of plan workspace a query needs with an index of this grid (0 for
+ * GRID queries; -1 cast to size_t on a malformed query). */
+size_t gs_plan_bytes(const gs_query *query, const gs_grid *grid);
+
+/*
+ * Forward sampling (Eq. 2 with the intersection test of Sec. 4.1.1 and the
+ * definedness rule of Sec. 4.1.3; Fig. 4 C for grids, Sec. 5.1.2 for
+ * unstructured points): writes out_value[t] = Phi and out_influence[t] = I
+ * for every query t, (0, 0) where undefined. gauss must be the Gaussians the
+ * index was built from, unchanged. For VOXELS and POINTS queries, plan
+ * receives the query ordering that gs_sample_backward reuses (the paper
+ * reuses its sample BVH the same way, Sec. 5.1.2); GRID queries need none.
+ * Deterministic: the same inputs give bit-identical outputs.
+ */
+gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                    float *out_value, float *out_influence, void *plan, size_t plan_bytes,
+                    hipStream_t stream);
+
+/* Bytes of backward workspace for an index (built) and a query. */
+size_t gs_backward_work_bytes(const gs_index *index, const gs_query *query);
+
+/*
+ * Backward pass (Sec. 4.1.4, Fig. 4 D-E; Sec. 5.1.2): given the forward
+ * outputs (value, influence) of gs_sample for this index, query and plan,
+ * and cotangents grad_value = dL/dPhi and grad_influence = dL/dI per query,
+ * overwrites the gradients of L with respect to every parameter:
+ * d_mean [n][3], d_scale [n][3], d_rot [n][4] (w.r.t. the raw quaternion),
+ * d_value [n], d_weight [n]. Undefined queries carry no gradient. The
+ * intersecting sets are those of the forward pass (the result is the exact
+ * derivative of the smooth piece). Per-Gaussian sums are accumulated with
+ * floating-point atomics, so the last bits may differ between runs.
+ */
+gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                             const void *plan, size_t plan_bytes, const float *value, const float *influence,
+                             const float *grad_value, const float *grad_influence, float *d_mean,
+                             float *d_scale, float *d_rot, float *d_value, float *d_weight, void *work,
+                             size_t work_bytes, hipStream_t stream);
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char *gs_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int gs_version(void);
+
+/*
+ * Kernel timing, for measurement. While enabled, every kernel the library
+ * launches is bracketed by HIP events on its stream. gs_profile_read waits
+ * for the recorded events and returns, for up to max_entries kernels, their
+ * names (pointers into static storage), launch counts and summed durations
+ * in milliseconds; the return value is the number of distinct kernels seen.
+ * gs_profile_enable(0) stops recording; gs_profile_reset() clears the
+ * records. Not thread-safe; meant for one measuring thread.
+ */
+void gs_profile_enable(int on);
+void gs_profile_reset(void);
+int gs_profile_read(const char **names, int64_t *counts, double *total_ms, int max_entries);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GS_H */

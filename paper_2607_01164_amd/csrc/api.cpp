@@ -1,0 +1,552 @@
+// C-ABI of the library (include/gs.h): argument validation, workspace
+// layout, the three entry points, and kernel timing.
+#include "../../include/gs.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace gs;
+
+namespace {
+
+thread_local std::string g_err;
+
+gs_status fail(gs_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+gs_status fail(gs_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+gs_status hip_fail(hipError_t e, const char *what) {
+    return fail(GS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define GS_TRY(expr, what)                                   \
+    do {                                                     \
+        hipError_t e_ = (expr);                              \
+        if (e_ != hipSuccess) return hip_fail(e_, (what));   \
+    } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+// Bump allocator over a caller workspace (computes the layout when base is null).
+struct Carver {
+    char *base;
+    size_t off = 0;
+    explicit Carver(void *b) : base((char *)b) {}
+    template <typename T>
+    T *take(size_t count) {
+        T *p = base ? (T *)(base + off) : nullptr;
+        off = align_up(off + count * sizeof(T));
+        return p;
+    }
+};
+
+int bits_for(int64_t nkeys) {  // bits needed to hold keys 0..nkeys-1
+    int b = 0;
+    while (b < 40 && ((int64_t)1 << b) < nkeys) ++b;
+    return b;
+}
+
+bool grid_valid(const gs_grid *g, std::string *why) {
+    if (!g) {
+        *why = "grid is null";
+        return false;
+    }
+    int64_t nc = 1;
+    for (int j = 0; j < 3; ++j) {
+        if (!(std::isfinite(g->lo[j]) && std::isfinite(g->hi[j]) && g->hi[j] > g->lo[j])) {
+            *why = "grid box must be finite with hi > lo on every axis";
+            return false;
+        }
+        if (g->cells[j] <= 0) {
+            *why = "grid cells must be positive";
+            return false;
+        }
+        nc *= g->cells[j];
+        if (nc >= ((int64_t)1 << 31)) {
+            *why = "grid has 2^31 cells or more";
+            return false;
+        }
+    }
+    return true;
+}
+
+int64_t ncells_of(const gs_grid *g) { return (int64_t)g->cells[0] * g->cells[1] * g->cells[2]; }
+
+GridParams grid_params(const gs_grid *g) {
+    GridParams p;
+    for (int j = 0; j < 3; ++j) {
+        p.lo[j] = g->lo[j];
+        p.hi[j] = g->hi[j];
+        volatile float ext = g->hi[j] - g->lo[j];
+        p.invc[j] = (float)g->cells[j] / ext;
+        p.cells[j] = g->cells[j];
+    }
+    p.ncells = ncells_of(g);
+    return p;
+}
+
+// Index workspace layout.
+struct IndexWork {
+    Record *rec;
+    CellBox *box;
+    uint64_t *pair_off;  // [n + 1]
+    void *scan_work;
+    uint32_t *keys_alt;
+    uint32_t *gids_alt;
+    void *radix_work;
+    size_t bytes;
+};
+
+IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity) {
+    Carver c(base);
+    IndexWork w;
+    w.rec = c.take<Record>((size_t)(n > 0 ? n : 1));
+    w.box = c.take<CellBox>((size_t)(n > 0 ? n : 1));
+    w.pair_off = c.take<uint64_t>((size_t)n + 1);
+    w.scan_work = c.take<char>(scan_work_bytes(n + 1, 8));
+    const int64_t cap = capacity > 0 ? capacity : 1;
+    w.keys_alt = c.take<uint32_t>((size_t)cap);
+    w.gids_alt = c.take<uint32_t>((size_t)cap);
+    w.radix_work = c.take<char>(radix_work_bytes(cap, bits_for(ncells_of(g))));
+    w.bytes = c.off;
+    return w;
+}
+
+// Plan layout (VOXELS and POINTS queries).
+struct Plan {
+    uint32_t *keys;      // [n] sorted cell keys (ncells = outside)
+    uint32_t *order;     // [n] query ids in cell order
+    uint32_t *keys_alt;  // [n]
+    uint32_t *order_alt; // [n]
+    uint32_t *point_off; // [ncells + 2]
+    void *radix_work;
+    size_t bytes;
+};
+
+Plan plan_layout(void *base, int64_t n, int64_t ncells) {
+    Carver c(base);
+    Plan p;
+    const size_t m = (size_t)(n > 0 ? n : 1);
+    p.keys = c.take<uint32_t>(m);
+    p.order = c.take<uint32_t>(m);
+    p.keys_alt = c.take<uint32_t>(m);
+    p.order_alt = c.take<uint32_t>(m);
+    p.point_off = c.take<uint32_t>((size_t)ncells + 2);
+    p.radix_work = c.take<char>(radix_work_bytes(n > 0 ? n : 1, bits_for(ncells + 1)));
+    p.bytes = c.off;
+    return p;
+}
+
+bool query_valid(const gs_query *q, std::string *why) {
+    if (!q) {
+        *why = "query is null";
+        return false;
+    }
+    if (q->kind == GS_QUERY_GRID || q->kind == GS_QUERY_VOXELS) {
+        int64_t nv = 1;
+        for (int j = 0; j < 3; ++j) {
+            if (q->dims[j] <= 0) {
+                *why = "query dims must be positive";
+                return false;
+            }
+            nv *= q->dims[j];
+        }
+        if (nv >= ((int64_t)1 << 32)) {
+            *why = "query grid has 2^32 voxels or more";
+            return false;
+        }
+    }
+    if (q->kind == GS_QUERY_GRID) return true;
+    if (q->kind != GS_QUERY_VOXELS && q->kind != GS_QUERY_POINTS) {
+        *why = "unknown query kind";
+        return false;
+    }
+    if (q->n < 0 || q->n >= ((int64_t)1 << 31)) {
+        *why = "query count must be in [0, 2^31)";
+        return false;
+    }
+    if (q->n > 0 && q->kind == GS_QUERY_VOXELS && !q->voxel_ids) {
+        *why = "voxel_ids is null";
+        return false;
+    }
+    if (q->n > 0 && q->kind == GS_QUERY_POINTS && !q->points) {
+        *why = "points is null";
+        return false;
+    }
+    return true;
+}
+
+int64_t query_count(const gs_query *q) {
+    if (q->kind == GS_QUERY_GRID) return (int64_t)q->dims[0] * q->dims[1] * q->dims[2];
+    return q->n;
+}
+
+QueryParams query_params(const gs_query *q, const gs_grid *g) {
+    QueryParams p;
+    p.kind = q->kind;
+    for (int j = 0; j < 3; ++j) p.dims[j] = q->kind == GS_QUERY_POINTS ? 1 : q->dims[j];
+    p.n = query_count(q);
+    p.voxel_ids = q->voxel_ids;
+    p.points = q->points;
+    for (int j = 0; j < 3; ++j) {
+        volatile float ext = g->hi[j] - g->lo[j];
+        p.vsz[j] = ext / (float)p.dims[j];
+    }
+    return p;
+}
+
+bool gauss_valid(const gs_gaussians *g, std::string *why) {
+    if (!g) {
+        *why = "gaussians is null";
+        return false;
+    }
+    if (g->n < 0 || g->n >= ((int64_t)1 << 31)) {
+        *why = "number of Gaussians must be in [0, 2^31)";
+        return false;
+    }
+    if (g->n > 0 && (!g->mean || !g->scale || !g->rot || !g->value || !g->weight)) {
+        *why = "a Gaussian parameter array is null";
+        return false;
+    }
+    return true;
+}
+
+bool aligned(const void *p) { return ((uintptr_t)p % kAlign) == 0; }
+
+float cutoff_T(float tau) { return (float)(2.0 * std::log(1.0 / (double)tau)); }
+float index_radius(float tau) {
+    const double rc = std::sqrt(2.0 * std::log(1.0 / (double)tau));
+    return (float)(rc * (1.0 + 1.0 / 1024.0));
+}
+
+// Backward workspace layout.
+struct BwdWork {
+    BackwardBuffers b;
+    size_t bytes;
+};
+
+int64_t max_backward_items(const gs_index *index, const gs_query *q) {
+    int64_t factor = 1;
+    if (q->kind == GS_QUERY_GRID)
+        factor = (int64_t)(q->dims[1] / index->grid.cells[1]) * (q->dims[2] / index->grid.cells[2]);
+    return index->n_pairs * factor / kRowGroup + index->n_gauss + 1;
+}
+
+BwdWork bwd_layout(void *base, const gs_index *index, const gs_query *q) {
+    Carver c(base);
+    BwdWork w;
+    const int64_t n = index->n_gauss;
+    const int64_t nq = query_count(q);
+    const size_t mq = (size_t)(nq > 0 ? nq : 1);
+    w.b.moments = c.take<float>((size_t)(n > 0 ? n : 1) * 12);
+    w.b.item_off = c.take<uint32_t>((size_t)n + 1);
+    w.b.scan_work = c.take<char>(scan_work_bytes(n + 1, 4));
+    w.b.max_items = max_backward_items(index, q);
+    w.b.items = c.take<uint32_t>((size_t)w.b.max_items);
+    if (q->kind == GS_QUERY_GRID) {
+        w.b.pts = nullptr;
+        w.b.alpha = c.take<float>(mq);
+        w.b.beta = c.take<float>(mq);
+    } else {
+        w.b.pts = c.take<float4>(mq);
+        w.b.beta = c.take<float>(mq);
+        w.b.alpha = nullptr;
+    }
+    w.bytes = c.off;
+    return w;
+}
+
+// ---------------------------------------------------------------------------
+// Kernel timing.
+
+struct ProfRec {
+    const char *name;
+    hipEvent_t a, b;
+};
+struct ProfAgg {
+    const char *name;
+    int64_t count;
+    double ms;
+};
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof_open;   // begun, not yet ended
+std::vector<ProfRec> g_prof_done;   // ended, not yet read
+std::vector<hipEvent_t> g_prof_pool;
+std::vector<ProfAgg> g_prof_agg;
+
+hipEvent_t prof_event() {
+    if (!g_prof_pool.empty()) {
+        hipEvent_t e = g_prof_pool.back();
+        g_prof_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+void prof_collect() {
+    for (const ProfRec &r : g_prof_done) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+            bool found = false;
+            for (ProfAgg &a : g_prof_agg)
+                if (std::strcmp(a.name, r.name) == 0) {
+                    a.count++;
+                    a.ms += ms;
+                    found = true;
+                    break;
+                }
+            if (!found) g_prof_agg.push_back({r.name, 1, (double)ms});
+        }
+        g_prof_pool.push_back(r.a);
+        g_prof_pool.push_back(r.b);
+    }
+    g_prof_done.clear();
+}
+
+}  // namespace
+
+namespace gs {
+
+void prof_begin(const char *name, hipStream_t s) {
+    if (!g_prof_on) return;
+    hipEvent_t a = prof_event();
+    if (!a) return;
+    (void)hipEventRecord(a, s);
+    g_prof_open.push_back({name, a, nullptr});
+}
+
+void prof_end(const char *name, hipStream_t s) {
+    if (!g_prof_on) return;
+    for (size_t i = g_prof_open.size(); i-- > 0;) {
+        if (g_prof_open[i].name == name || std::strcmp(g_prof_open[i].name, name) == 0) {
+            ProfRec r = g_prof_open[i];
+            g_prof_open.erase(g_prof_open.begin() + (long)i);
+            r.b = prof_event();
+            if (!r.b) {
+                g_prof_pool.push_back(r.a);
+                return;
+            }
+            (void)hipEventRecord(r.b, s);
+            g_prof_done.push_back(r);
+            if (g_prof_done.size() > 4096) prof_collect();
+            return;
+        }
+    }
+}
+
+}  // namespace gs
+
+extern "C" {
+
+const char *gs_last_error(void) { return g_err.c_str(); }
+
+int gs_version(void) { return 100; }
+
+void gs_profile_enable(int on) { g_prof_on = on != 0; }
+
+void gs_profile_reset(void) {
+    prof_collect();
+    g_prof_agg.clear();
+}
+
+int gs_profile_read(const char **names, int64_t *counts, double *total_ms, int max_entries) {
+    prof_collect();
+    const int n = (int)g_prof_agg.size();
+    for (int i = 0; i < n && i < max_entries; ++i) {
+        if (names) names[i] = g_prof_agg[i].name;
+        if (counts) counts[i] = g_prof_agg[i].count;
+        if (total_ms) total_ms[i] = g_prof_agg[i].ms;
+    }
+    return n;
+}
+
+int64_t gs_query_size(const gs_query *query) {
+    std::string why;
+    if (!query_valid(query, &why)) return -1;
+    return query_count(query);
+}
+
+size_t gs_index_work_bytes(int64_t n_gauss, const gs_grid *grid, int64_t capacity) {
+    std::string why;
+    if (n_gauss < 0 || capacity < 0 || !grid_valid(grid, &why)) return (size_t)-1;
+    return index_layout(nullptr, n_gauss, grid, capacity).bytes;
+}
+
+gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float tau, gs_index *index,
+                         hipStream_t stream) {
+    std::string why;
+    if (!gauss_valid(gauss, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_build_index: %s", why.c_str());
+    if (!grid_valid(grid, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_build_index: %s", why.c_str());
+    if (!(tau > 0.0f && tau < 1.0f)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_build_index: tau must be in (0, 1)");
+    if (!index) return fail(GS_ERR_INVALID_ARGUMENT, "gs_build_index: index is null");
+    if (index->capacity < 0) return fail(GS_ERR_INVALID_ARGUMENT, "gs_build_index: negative capacity");
+    if (!index->cell_offsets) return fail(GS_ERR_INVALID_ARGUMENT, "gs_build_index: cell_offsets is null");
+    if (index->capacity > 0 && (!index->keys || !index->gids))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_build_index: keys/gids are null");
+    const int64_t n = gauss->n;
+    const size_t need = index_layout(nullptr, n, grid, index->capacity).bytes;
+    if (!index->work || index->work_bytes < need || !aligned(index->work))
+        return fail(GS_ERR_WORKSPACE, "gs_build_index: workspace needs %zu bytes, 256-byte aligned (got %zu)", need,
+                    index->work_bytes);
+    index->n_pairs = -1;
+    index->n_gauss = n;
+    index->grid = *grid;
+    index->tau = tau;
+    const GridParams gp = grid_params(grid);
+    const int64_t ncells = gp.ncells;
+    IndexWork w = index_layout(index->work, n, grid, index->capacity);
+
+    GS_TRY(launch_preprocess(gauss->mean, gauss->scale, gauss->rot, gauss->value, gauss->weight, n, gp,
+                             index_radius(tau), w.rec, w.box, w.pair_off, stream),
+           "gs_build_index: preprocess");
+    GS_TRY(exclusive_scan_u64(w.pair_off, w.pair_off, n + 1, w.scan_work, stream), "gs_build_index: scan");
+    uint64_t P = 0;
+    GS_TRY(hipMemcpyAsync(&P, w.pair_off + n, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
+           "gs_build_index: reading the pair count");
+    GS_TRY(hipStreamSynchronize(stream), "gs_build_index: waiting for the pair count");
+    index->n_pairs = (int64_t)P;
+    if ((int64_t)P > index->capacity || P >= ((uint64_t)1 << 32))
+        return fail(GS_ERR_CAPACITY, "gs_build_index: %llu pairs exceed the capacity %lld",
+                    (unsigned long long)P, (long long)index->capacity);
+    if (P == 0) {
+        GS_TRY(fill_u32(index->cell_offsets, 0u, ncells + 1, stream), "gs_build_index: offsets");
+        return GS_OK;
+    }
+    const int bits = bits_for(ncells);
+    const bool odd = (radix_passes(bits) & 1) != 0;
+    // emit where the sort's last pass lands in keys/gids
+    uint32_t *ek = odd ? w.keys_alt : index->keys, *ev = odd ? w.gids_alt : index->gids;
+    uint32_t *ak = odd ? index->keys : w.keys_alt, *av = odd ? index->gids : w.gids_alt;
+    GS_TRY(launch_emit(w.pair_off, w.box, n, (int64_t)P, gp, ek, ev, stream), "gs_build_index: emit");
+    GS_TRY(radix_sort_pairs(ek, ev, ak, av, (int64_t)P, bits, w.radix_work, stream), "gs_build_index: sort");
+    GS_TRY(key_offsets(index->keys, (int64_t)P, index->cell_offsets, ncells, stream), "gs_build_index: ranges");
+    return GS_OK;
+}
+
+size_t gs_plan_bytes(const gs_query *query, const gs_grid *grid) {
+    std::string why;
+    if (!query_valid(query, &why) || !grid_valid(grid, &why)) return (size_t)-1;
+    if (query->kind == GS_QUERY_GRID) return 0;
+    return plan_layout(nullptr, query->n, ncells_of(grid)).bytes;
+}
+
+static gs_status check_index(const char *fn, const gs_gaussians *gauss, const gs_index *index) {
+    std::string why;
+    if (!gauss_valid(gauss, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "%s: %s", fn, why.c_str());
+    if (!index) return fail(GS_ERR_INVALID_ARGUMENT, "%s: index is null", fn);
+    if (index->n_pairs < 0 || index->n_pairs > index->capacity)
+        return fail(GS_ERR_INVALID_ARGUMENT, "%s: the index has not been built", fn);
+    if (index->n_gauss != gauss->n)
+        return fail(GS_ERR_INVALID_ARGUMENT, "%s: the index was built for %lld Gaussians, not %lld", fn,
+                    (long long)index->n_gauss, (long long)gauss->n);
+    if (!grid_valid(&index->grid, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "%s: %s", fn, why.c_str());
+    if (!index->work || !index->cell_offsets || (index->n_pairs > 0 && !index->gids))
+        return fail(GS_ERR_INVALID_ARGUMENT, "%s: index buffers are null", fn);
+    return GS_OK;
+}
+
+static gs_status check_query(const char *fn, const gs_index *index, const gs_query *query) {
+    std::string why;
+    if (!query_valid(query, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "%s: %s", fn, why.c_str());
+    if (query->kind == GS_QUERY_GRID)
+        for (int j = 0; j < 3; ++j)
+            if (query->dims[j] % index->grid.cells[j] != 0)
+                return fail(GS_ERR_INVALID_ARGUMENT,
+                            "%s: grid query dims must be a multiple of the index cells on every axis", fn);
+    return GS_OK;
+}
+
+gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_query *query, float *out_value,
+                    float *out_influence, void *plan, size_t plan_bytes, hipStream_t stream) {
+    gs_status st = check_index("gs_sample", gauss, index);
+    if (st != GS_OK) return st;
+    if ((st = check_query("gs_sample", index, query)) != GS_OK) return st;
+    const int64_t nq = query_count(query);
+    if (nq > 0 && (!out_value || !out_influence))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample: output arrays are null");
+    const GridParams gp = grid_params(&index->grid);
+    const QueryParams qp = query_params(query, &index->grid);
+    IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
+    const float T = cutoff_T(index->tau);
+    if (query->kind == GS_QUERY_GRID) {
+        GS_TRY(launch_sample_grid(qp, gp, w.rec, index->gids, index->cell_offsets, T, index->tau, out_value,
+                                  out_influence, stream),
+               "gs_sample: grid sampler");
+        return GS_OK;
+    }
+    const size_t need = plan_layout(nullptr, nq, gp.ncells).bytes;
+    if (!plan || plan_bytes < need || !aligned(plan))
+        return fail(GS_ERR_WORKSPACE, "gs_sample: plan needs %zu bytes, 256-byte aligned (got %zu)", need, plan_bytes);
+    Plan p = plan_layout(plan, nq, gp.ncells);
+    const int bits = bits_for(gp.ncells + 1);
+    const bool odd = (radix_passes(bits) & 1) != 0;
+    uint32_t *ek = odd ? p.keys_alt : p.keys, *ev = odd ? p.order_alt : p.order;
+    uint32_t *ak = odd ? p.keys : p.keys_alt, *av = odd ? p.order : p.order_alt;
+    GS_TRY(launch_query_keys(qp, gp, ek, ev, stream), "gs_sample: query keys");
+    GS_TRY(radix_sort_pairs(ek, ev, ak, av, nq, bits, p.radix_work, stream), "gs_sample: query sort");
+    GS_TRY(key_offsets(p.keys, nq, p.point_off, gp.ncells + 1, stream), "gs_sample: query ranges");
+    GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.keys, p.order, T, index->tau,
+                                out_value, out_influence, stream),
+           "gs_sample: point sampler");
+    return GS_OK;
+}
+
+size_t gs_backward_work_bytes(const gs_index *index, const gs_query *query) {
+    std::string why;
+    if (!index || index->n_pairs < 0 || !query_valid(query, &why)) return (size_t)-1;
+    return bwd_layout(nullptr, index, query).bytes;
+}
+
+gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                             const void *plan, size_t plan_bytes, const float *value, const float *influence,
+                             const float *grad_value, const float *grad_influence, float *d_mean, float *d_scale,
+                             float *d_rot, float *d_value, float *d_weight, void *work, size_t work_bytes,
+                             hipStream_t stream) {
+    gs_status st = check_index("gs_sample_backward", gauss, index);
+    if (st != GS_OK) return st;
+    if ((st = check_query("gs_sample_backward", index, query)) != GS_OK) return st;
+    const int64_t n = gauss->n;
+    const int64_t nq = query_count(query);
+    if (nq > 0 && (!value || !influence || !grad_value || !grad_influence))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample_backward: forward outputs or cotangents are null");
+    if (n > 0 && (!d_mean || !d_scale || !d_rot || !d_value || !d_weight))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample_backward: gradient arrays are null");
+    const GridParams gp = grid_params(&index->grid);
+    const QueryParams qp = query_params(query, &index->grid);
+    const size_t need = bwd_layout(nullptr, index, query).bytes;
+    if (!work || work_bytes < need || !aligned(work))
+        return fail(GS_ERR_WORKSPACE, "gs_sample_backward: workspace needs %zu bytes, 256-byte aligned (got %zu)",
+                    need, work_bytes);
+    Plan p{};
+    if (query->kind != GS_QUERY_GRID) {
+        const size_t pneed = plan_layout(nullptr, nq, gp.ncells).bytes;
+        if (!plan || plan_bytes < pneed || !aligned(plan))
+            return fail(GS_ERR_WORKSPACE, "gs_sample_backward: plan needs %zu bytes (got %zu)", pneed, plan_bytes);
+        p = plan_layout(const_cast<void *>(plan), nq, gp.ncells);
+    }
+    IndexWork w = index_layout(index->work, n, &index->grid, index->capacity);
+    BwdWork bw = bwd_layout(work, index, query);
+    GS_TRY(launch_backward(qp, gp, w.rec, w.box, n, p.keys, p.order, p.point_off, value, influence, grad_value,
+                           grad_influence, cutoff_T(index->tau), bw.b, gauss->mean, gauss->scale, gauss->rot, d_mean,
+                           d_scale, d_rot, d_value, d_weight, stream),
+           "gs_sample_backward");
+    return GS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,168 @@
+// Cell index of the Gaussians (paper Sec. 4.1.1 and Sec. 4.1.2):
+//  - preprocess: per Gaussian, the axis-aligned box of its cutoff ellipsoid
+//    in cells (canonical float32, each operation rounded separately), its
+//    cell count, and the evaluation record used by the samplers;
+//  - emit: one (cell key, Gaussian id) pair per cell of every box,
+//    parallel over pairs with a per-tile load-balanced search for the owning
+//    Gaussian (the paper parallelises this step over intersections for the
+//    same reason: box sizes vary by orders of magnitude in 3D).
+// The pairs are then sorted by key (primitives.hip) and the per-cell ranges
+// taken from the sorted keys.
+#include "expand.h"
+#include "internal.h"
+
+#pragma clang fp contract(off)
+
+namespace gs {
+
+namespace {
+
+__device__ __forceinline__ bool finite_f(float x) { return __builtin_isfinite(x); }
+
+__global__ __launch_bounds__(kBlock) void k_preprocess(const float *__restrict__ mean, const float *__restrict__ scale,
+                                                       const float *__restrict__ rot, const float *__restrict__ value,
+                                                       const float *__restrict__ weight, int64_t n, GridParams g,
+                                                       float rci, Record *__restrict__ rec, CellBox *__restrict__ box,
+                                                       uint64_t *__restrict__ count) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == n) count[n] = 0;
+    if (i >= n) return;
+    const float mu[3] = {mean[3 * i], mean[3 * i + 1], mean[3 * i + 2]};
+    const float s[3] = {scale[3 * i], scale[3 * i + 1], scale[3 * i + 2]};
+    const float q[4] = {rot[4 * i], rot[4 * i + 1], rot[4 * i + 2], rot[4 * i + 3]};
+    const float v = value[i], w = weight[i];
+
+    bool valid = finite_f(v) && finite_f(w);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) valid = valid && finite_f(mu[j]) && finite_f(s[j]) && (s[j] > 0.0f);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) valid = valid && finite_f(q[j]);
+
+    // canonical float32 rotation (every product and sum rounded in this order)
+    const float n2 = ((q[0] * q[0] + q[1] * q[1]) + q[2] * q[2]) + q[3] * q[3];
+    valid = valid && (n2 > 0.0f) && finite_f(n2);
+    const float inv = 1.0f / sqrtf(n2);
+    const float qw = q[0] * inv, qx = q[1] * inv, qy = q[2] * inv, qz = q[3] * inv;
+    float R[3][3];
+    R[0][0] = 1.0f - 2.0f * (qy * qy + qz * qz);
+    R[0][1] = 2.0f * (qx * qy - qw * qz);
+    R[0][2] = 2.0f * (qx * qz + qw * qy);
+    R[1][0] = 2.0f * (qx * qy + qw * qz);
+    R[1][1] = 1.0f - 2.0f * (qx * qx + qz * qz);
+    R[1][2] = 2.0f * (qy * qz - qw * qx);
+    R[2][0] = 2.0f * (qx * qz - qw * qy);
+    R[2][1] = 2.0f * (qy * qz + qw * qx);
+    R[2][2] = 1.0f - 2.0f * (qx * qx + qy * qy);
+
+    int lo_c[3], hi_c[3];
+    uint64_t cnt = 1;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+        const float a0 = R[j][0] * s[0], a1 = R[j][1] * s[1], a2 = R[j][2] * s[2];
+        const float var = (a0 * a0 + a1 * a1) + a2 * a2;
+        const float h = rci * sqrtf(var);
+        const float lo = mu[j] - h, hi = mu[j] + h;
+        const float tl = (lo - g.lo[j]) * g.invc[j];
+        const float th = (hi - g.lo[j]) * g.invc[j];
+        const float fl = floorf(tl), fh = floorf(th);
+        const float cmax = (float)(g.cells[j] - 1);
+        if (!finite_f(h) || !finite_f(fl) || !finite_f(fh) || !(fh >= 0.0f) || !(fl <= cmax)) valid = false;
+        lo_c[j] = valid ? (int)(fl > 0.0f ? fl : 0.0f) : 0;
+        hi_c[j] = valid ? (int)(fh < cmax ? fh : cmax) : -1;
+        cnt *= valid ? (uint64_t)(hi_c[j] - lo_c[j] + 1) : 0ull;
+    }
+    if (!valid) {
+        lo_c[0] = lo_c[1] = lo_c[2] = 0;
+        hi_c[0] = hi_c[1] = hi_c[2] = -1;
+        cnt = 0;
+    }
+    count[i] = cnt;
+    CellBox b;
+    b.lo = make_int4(lo_c[0], lo_c[1], lo_c[2], 0);
+    b.hi = make_int4(hi_c[0], hi_c[1], hi_c[2], 0);
+    box[i] = b;
+
+    // evaluation record: M = S^-1 R^T formed in float64, rounded once
+    Record r;
+    if (valid) {
+        const double qn = sqrt((double)q[0] * q[0] + (double)q[1] * q[1] + (double)q[2] * q[2] + (double)q[3] * q[3]);
+        const double w_ = q[0] / qn, x = q[1] / qn, y = q[2] / qn, z = q[3] / qn;
+        double Rd[3][3];
+        Rd[0][0] = 1.0 - 2.0 * (y * y + z * z);
+        Rd[0][1] = 2.0 * (x * y - w_ * z);
+        Rd[0][2] = 2.0 * (x * z + w_ * y);
+        Rd[1][0] = 2.0 * (x * y + w_ * z);
+        Rd[1][1] = 1.0 - 2.0 * (x * x + z * z);
+        Rd[1][2] = 2.0 * (y * z - w_ * x);
+        Rd[2][0] = 2.0 * (x * z - w_ * y);
+        Rd[2][1] = 2.0 * (y * z + w_ * x);
+        Rd[2][2] = 1.0 - 2.0 * (x * x + y * y);
+        float M[3][3];
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+#pragma unroll
+            for (int j = 0; j < 3; ++j) M[k][j] = (float)(Rd[j][k] / (double)s[k]);
+        r.r0 = make_float4(mu[0], mu[1], mu[2], w);
+        r.r1 = make_float4(M[0][0], M[0][1], M[0][2], v);
+        r.r2 = make_float4(M[1][0], M[1][1], M[1][2], 0.0f);
+        r.r3 = make_float4(M[2][0], M[2][1], M[2][2], 0.0f);
+    } else {
+        r.r0 = r.r1 = r.r2 = r.r3 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    }
+    rec[i] = r;
+}
+
+__global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pair_off,
+                                                 const CellBox *__restrict__ box, int64_t n, int64_t npairs,
+                                                 GridParams g, uint32_t *__restrict__ keys,
+                                                 uint32_t *__restrict__ gids) {
+    __shared__ ExpandShared sh;
+    const uint32_t tid = threadIdx.x;
+    const uint64_t tile_begin = (uint64_t)blockIdx.x * kExpandTile;
+    const uint64_t rem = (uint64_t)npairs - tile_begin;
+    const uint32_t tile_cnt = rem < (uint64_t)kExpandTile ? (uint32_t)rem : (uint32_t)kExpandTile;
+    const int64_t gfirst = expand_tile(pair_off, n, tile_begin, tile_cnt, sh);
+    const int64_t Cx = g.cells[0], Cy = g.cells[1];
+#pragma unroll 2
+    for (int i = 0; i < kExpandItems; ++i) {
+        const uint32_t slot = (uint32_t)i * kBlock + tid;
+        if (slot < tile_cnt) {
+            const int64_t gg = gfirst + sh.head[slot];
+            const uint32_t local = (uint32_t)(tile_begin + slot - pair_off[gg]);
+            const CellBox b = box[gg];
+            const uint32_t nx = (uint32_t)(b.hi.x - b.lo.x + 1), ny = (uint32_t)(b.hi.y - b.lo.y + 1);
+            const uint32_t t = local / nx;
+            const int64_t cx = b.lo.x + (int64_t)(local - t * nx);
+            const int64_t cy = b.lo.y + (int64_t)(t % ny);
+            const int64_t cz = b.lo.z + (int64_t)(t / ny);
+            keys[tile_begin + slot] = (uint32_t)(cx + Cx * (cy + Cy * cz));
+            gids[tile_begin + slot] = (uint32_t)gg;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
+                             const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
+                             CellBox *box, uint64_t *count, hipStream_t s) {
+    const int64_t threads = n + 1;
+    const uint32_t blocks = (uint32_t)((threads + kBlock - 1) / kBlock);
+    prof_begin("preprocess", s);
+    hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kBlock), 0, s, mean, scale, rot, value, weight, n, g, rci, rec,
+                       box, count);
+    prof_end("preprocess", s);
+    return hipGetLastError();
+}
+
+hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, int64_t n, int64_t npairs, const GridParams &g,
+                       uint32_t *keys, uint32_t *gids, hipStream_t s) {
+    if (npairs <= 0 || n <= 0) return hipSuccess;
+    const uint32_t blocks = (uint32_t)((npairs + kExpandTile - 1) / kExpandTile);
+    prof_begin("emit", s);
+    hipLaunchKernelGGL(k_emit, dim3(blocks), dim3(kBlock), 0, s, pair_off, box, n, npairs, g, keys, gids);
+    prof_end("emit", s);
+    return hipGetLastError();
+}
+
+}  // namespace gs

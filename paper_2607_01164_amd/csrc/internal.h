@@ -1,0 +1,180 @@
+// Internal declarations shared by the HIP translation units of the library:
+// the per-Gaussian record layout, small wave/block primitives, and the host
+// launchers the C-ABI layer calls. Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace gs {
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;             // threads per workgroup for most kernels
+constexpr int kWavesPerBlock = kBlock / kWave;
+
+// Per-Gaussian evaluation record, 64 bytes, written by the preprocess kernel.
+//   r0 = (mu_x, mu_y, mu_z, w)
+//   r1 = (M00, M01, M02, v)      M = S^-1 R^T, so u = M (p - mu), Q = |u|^2
+//   r2 = (M10, M11, M12, 0)
+//   r3 = (M20, M21, M22, 0)
+// M is formed in float64 and rounded once to float32. Invalid Gaussians get
+// an all-zero record and an empty box, and appear in no cell list.
+struct alignas(16) Record {
+    float4 r0, r1, r2, r3;
+};
+
+// Cell box of a Gaussian: (x0, y0, z0, 0) and (x1, y1, z1, 0), inclusive;
+// an empty box has x1 < x0.
+struct alignas(16) CellBox {
+    int4 lo, hi;
+};
+
+// --- float helpers ---------------------------------------------------------
+
+__device__ __forceinline__ float fmaf_(float a, float b, float c) { return __builtin_fmaf(a, b, c); }
+
+// 2^x through the hardware transcendental unit (v_exp_f32). Arguments here
+// are in [-6.65, 0], far from the denormal range.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// --- cross-lane helpers ------------------------------------------------------
+
+__device__ __forceinline__ uint32_t lane_id() {
+    return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over each row of 16 lanes; every lane of the row receives the total.
+// quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_ror:4, row_ror:8.
+__device__ __forceinline__ float row16_sum(float x) {
+    x += dpp_f<0xB1>(x);
+    x += dpp_f<0x4E>(x);
+    x += dpp_f<0x124>(x);
+    x += dpp_f<0x128>(x);
+    return x;
+}
+
+// Inclusive scan of a 32-bit value across the 64 lanes of a wave (sum or max).
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x) {
+    const uint32_t lane = lane_id();
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        uint32_t y = __shfl_up(x, o, 64);
+        if (lane >= (uint32_t)o) x += y;
+    }
+    return x;
+}
+
+__device__ __forceinline__ uint64_t wave_incl_sum64(uint64_t x) {
+    const uint32_t lane = lane_id();
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        uint64_t y = __shfl_up(x, o, 64);
+        if (lane >= (uint32_t)o) x += y;
+    }
+    return x;
+}
+
+__device__ __forceinline__ uint32_t wave_incl_max(uint32_t x) {
+    const uint32_t lane = lane_id();
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        uint32_t y = __shfl_up(x, o, 64);
+        if (lane >= (uint32_t)o) x = x > y ? x : y;
+    }
+    return x;
+}
+
+// Map a linear block id so that consecutive work lands on one XCD: blocks
+// are dispatched round-robin over the 8 XCDs, each with its own L2, so block
+// b runs on XCD b % 8. Blocks past the last full group of 8 keep their id.
+__device__ __forceinline__ uint32_t xcd_block(uint32_t b, uint32_t nblocks) {
+    const uint32_t full = nblocks & ~7u;
+    if (b >= full) return b;
+    return (b & 7u) * (full >> 3) + (b >> 3);
+}
+
+// --- host side ---------------------------------------------------------------
+
+struct Stream {
+    hipStream_t s;
+};
+
+// Kernel timing hooks (api.cpp): every launcher brackets its kernels.
+void prof_begin(const char *name, hipStream_t s);
+void prof_end(const char *name, hipStream_t s);
+
+// Exclusive scans. Workspace: scan_work_bytes(n) bytes. out may equal in.
+size_t scan_work_bytes(int64_t n, int elem_bytes);
+hipError_t exclusive_scan_u32(const uint32_t *in, uint32_t *out, int64_t n, void *work, hipStream_t s);
+hipError_t exclusive_scan_u64(const uint64_t *in, uint64_t *out, int64_t n, void *work, hipStream_t s);
+
+// Stable LSD radix sort of (key, value) pairs by the low `bits` key bits.
+// The result ends in (keys, vals); alt buffers are scratch of n elements.
+size_t radix_work_bytes(int64_t n, int bits);
+int radix_passes(int bits);
+hipError_t radix_sort_pairs(uint32_t *keys, uint32_t *vals, uint32_t *keys_alt, uint32_t *vals_alt, int64_t n,
+                            int bits, void *work, hipStream_t s);
+
+// offsets[k] = number of sorted keys < k, k = 0..nkeys (nkeys+1 entries).
+hipError_t key_offsets(const uint32_t *sorted_keys, int64_t n, uint32_t *offsets, int64_t nkeys, hipStream_t s);
+
+hipError_t fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s);
+hipError_t fill_f32(float *p, float v, int64_t n, hipStream_t s);
+
+// Index build pieces (index.hip).
+struct GridParams {
+    float lo[3], hi[3];
+    float invc[3];   // cells / (hi - lo), float32
+    int32_t cells[3];
+    int64_t ncells;
+};
+hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
+                             const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
+                             CellBox *box, uint64_t *count, hipStream_t s);
+hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, int64_t n, int64_t npairs, const GridParams &g,
+                       uint32_t *keys, uint32_t *gids, hipStream_t s);
+
+// Sampling (sample.hip).
+struct QueryParams {
+    int kind;
+    int32_t dims[3];
+    int64_t n;           // number of outputs
+    const uint32_t *voxel_ids;
+    const float *points;
+    float vsz[3];        // (hi - lo) / dims, float32
+};
+hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids, hipStream_t s);
+hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
+                              const uint32_t *cell_off, float T, float tau, float *out_v, float *out_i,
+                              hipStream_t s);
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
+                                const uint32_t *cell_off, const uint32_t *sorted_keys, const uint32_t *order,
+                                float T, float tau, float *out_v, float *out_i, hipStream_t s);
+
+// Backward (backward.hip).
+constexpr int kRowGroup = 16;  // lanes per backward work item (one DPP row)
+struct BackwardBuffers {
+    float *moments;        // [n_gauss][12]
+    uint32_t *item_off;    // [n_gauss + 1]
+    uint32_t *items;       // [max_items]
+    int64_t max_items;
+    float4 *pts;           // POINTS/VOXELS: [n] (x, y, z, alpha) in plan order
+    float *beta;           // POINTS/VOXELS: [n]; GRID: [n] beta in voxel order
+    float *alpha;          // GRID: [n] alpha in voxel order
+    void *scan_work;
+};
+hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
+                           int64_t n_gauss, const uint32_t *sorted_keys, const uint32_t *order,
+                           const uint32_t *point_off, const float *value, const float *influence,
+                           const float *grad_value, const float *grad_influence, float T,
+                           const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
+                           float *d_mean, float *d_scale, float *d_rot, float *d_value, float *d_weight,
+                           hipStream_t s);
+
+}  // namespace gs

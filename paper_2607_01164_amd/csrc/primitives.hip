@@ -1,0 +1,385 @@
+// Device-wide primitives: exclusive scans, a stable LSD radix sort of
+// (key, value) pairs with wave-level multi-split ranking in LDS, per-key
+// offsets of a sorted key array, and fills.
+#include "internal.h"
+
+namespace gs {
+
+namespace {
+
+constexpr int kScanItems = 16;
+constexpr int kScanTile = kBlock * kScanItems;  // 4096
+
+__device__ __forceinline__ uint32_t wincl(uint32_t x) { return wave_incl_sum(x); }
+__device__ __forceinline__ uint64_t wincl(uint64_t x) { return wave_incl_sum64(x); }
+
+// Exclusive scan of one value per thread over the workgroup; *total gets the
+// workgroup sum. lds needs kWavesPerBlock entries.
+template <typename T>
+__device__ __forceinline__ T block_excl_scan(T x, T *lds, T *total) {
+    const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    T incl = wincl(x);
+    if (lane == kWave - 1) lds[wave] = incl;
+    __syncthreads();
+    T wpre = 0, tot = 0;
+#pragma unroll
+    for (uint32_t w = 0; w < (uint32_t)kWavesPerBlock; ++w) {
+        T v = lds[w];
+        if (w < wave) wpre += v;
+        tot += v;
+    }
+    __syncthreads();
+    *total = tot;
+    return wpre + incl - x;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_scan_reduce(const T *__restrict__ in, int64_t n, T *__restrict__ sums) {
+    __shared__ T lds[kWavesPerBlock];
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    T s = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t idx = base + i;
+        if (idx < n) s += in[idx];
+    }
+    T tot;
+    (void)block_excl_scan(s, lds, &tot);
+    if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_scan_tile(const T *in, T *out, int64_t n, const T *__restrict__ prefix) {
+    __shared__ T lds[kWavesPerBlock];
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    T v[kScanItems];
+    T s = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t idx = base + i;
+        v[i] = idx < n ? in[idx] : T(0);
+        s += v[i];
+    }
+    T tot;
+    T run = block_excl_scan(s, lds, &tot);
+    if (prefix) run += prefix[blockIdx.x];
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t idx = base + i;
+        if (idx < n) out[idx] = run;
+        run += v[i];
+    }
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+template <typename T>
+hipError_t scan_rec(const T *in, T *out, int64_t n, T *work, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    if (n <= kScanTile) {
+        hipLaunchKernelGGL(k_scan_tile<T>, dim3(1), dim3(kBlock), 0, s, in, out, n, (const T *)nullptr);
+        return hipGetLastError();
+    }
+    const int64_t nb = ceil_div(n, kScanTile);
+    T *sums = work;
+    hipLaunchKernelGGL(k_scan_reduce<T>, dim3((uint32_t)nb), dim3(kBlock), 0, s, in, n, sums);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = scan_rec<T>(sums, sums, nb, work + nb, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_scan_tile<T>, dim3((uint32_t)nb), dim3(kBlock), 0, s, in, out, n, (const T *)sums);
+    return hipGetLastError();
+}
+
+int64_t scan_levels_elems(int64_t n) {
+    int64_t tot = 0;
+    while (n > kScanTile) {
+        n = ceil_div(n, kScanTile);
+        tot += n;
+    }
+    return tot;
+}
+
+// ---------------------------------------------------------------------------
+// Radix sort.
+
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kBlock * kSortItems;  // 4096
+constexpr int kMaxDigitBits = 10;
+constexpr int kMaxDigits = 1 << kMaxDigitBits;
+
+int passes_for(int bits) { return bits <= 0 ? 0 : (bits + kMaxDigitBits - 1) / kMaxDigitBits; }
+int digit_bits_for(int bits) {
+    int p = passes_for(bits);
+    return p == 0 ? 0 : (bits + p - 1) / p;
+}
+
+// Digit histogram of one tile, written digit-major: table[d * nb + block].
+__global__ __launch_bounds__(kBlock) void k_radix_upsweep(const uint32_t *__restrict__ keys, int64_t n, int shift,
+                                                          uint32_t mask, uint32_t ndig, uint32_t *__restrict__ table,
+                                                          uint32_t nb) {
+    __shared__ uint32_t h[kMaxDigits];
+    for (uint32_t d = threadIdx.x; d < ndig; d += kBlock) h[d] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+#pragma unroll 4
+    for (int i = 0; i < kSortItems; ++i) {
+        int64_t idx = base + (int64_t)i * kBlock + threadIdx.x;
+        if (idx < n) atomicAdd(&h[(keys[idx] >> shift) & mask], 1u);
+    }
+    __syncthreads();
+    for (uint32_t d = threadIdx.x; d < ndig; d += kBlock) table[(size_t)d * nb + blockIdx.x] = h[d];
+}
+
+// Stable scatter of one tile. Each wave ranks its 16 rows of 64 keys in
+// order: lanes holding the same digit are found with one ballot per digit
+// bit; a per-wave running count per digit in LDS gives each key its rank
+// among earlier keys of the wave. Waves are then combined per digit, the
+// tile is reordered by digit in LDS, and written out in runs.
+__global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__restrict__ kin,
+                                                            const uint32_t *__restrict__ vin,
+                                                            uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
+                                                            int64_t n, int shift, int dbits,
+                                                            const uint32_t *__restrict__ goff, uint32_t nb) {
+    __shared__ uint32_t wcnt[kWavesPerBlock][kMaxDigits];
+    __shared__ uint32_t dstart[kMaxDigits];  // first slot of each digit inside the tile
+    __shared__ uint32_t dglob[kMaxDigits];   // global position of each digit's first key of the tile
+    __shared__ uint32_t sk[kSortTile];
+    __shared__ uint32_t sv[kSortTile];
+    __shared__ uint32_t scan_lds[kWavesPerBlock];
+
+    const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const uint32_t ndig = 1u << dbits, mask = ndig - 1;
+    for (uint32_t d = tid; d < ndig; d += kBlock) {
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][d] = 0;
+        dglob[d] = goff[(size_t)d * nb + blockIdx.x];
+    }
+    __syncthreads();
+
+    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)wave * (kWave * kSortItems);
+    uint32_t k[kSortItems], v[kSortItems], r[kSortItems];
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        int64_t idx = base + (int64_t)i * kWave + lane;
+        bool ok = idx < n;
+        k[i] = ok ? kin[idx] : 0u;
+        v[i] = ok ? vin[idx] : 0u;
+    }
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const int64_t idx = base + (int64_t)i * kWave + lane;
+        const bool ok = idx < n;
+        const uint32_t d = (k[i] >> shift) & mask;
+        uint64_t m = __ballot(ok);
+        for (int b = 0; b < dbits; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t bm = __ballot(bit);
+            m &= bit ? bm : ~bm;
+        }
+        const uint32_t before = (uint32_t)__popcll(m & lt_mask);
+        const uint32_t cnt = (uint32_t)__popcll(m);
+        uint32_t basecnt = 0;
+        if (ok) basecnt = wcnt[wave][d];
+        // all lanes of the wave have read the counter before its leader writes
+        __builtin_amdgcn_wave_barrier();
+        if (ok && before == 0) wcnt[wave][d] = basecnt + cnt;
+        __builtin_amdgcn_wave_barrier();
+        r[i] = basecnt + before;
+    }
+    __syncthreads();
+    // per digit: exclusive scan over the waves, and the tile total
+    uint32_t my_tot[kMaxDigits / kBlock];
+#pragma unroll
+    for (int j = 0; j < kMaxDigits / kBlock; ++j) {
+        uint32_t d = tid + j * kBlock;
+        uint32_t s = 0;
+        if (d < ndig) {
+#pragma unroll
+            for (int w = 0; w < kWavesPerBlock; ++w) {
+                uint32_t t = wcnt[w][d];
+                wcnt[w][d] = s;
+                s += t;
+            }
+        }
+        my_tot[j] = s;
+    }
+    // exclusive scan of digit totals over digits -> dstart (digit d = tid + j*256;
+    // scan thread-major: each thread owns digits tid*J .. tid*J+J-1 instead)
+    __syncthreads();
+    {
+        // gather totals into dstart temporarily
+#pragma unroll
+        for (int j = 0; j < kMaxDigits / kBlock; ++j) {
+            uint32_t d = tid + j * kBlock;
+            if (d < ndig) dstart[d] = my_tot[j];
+        }
+        __syncthreads();
+        constexpr int J = kMaxDigits / kBlock;
+        uint32_t loc[J];
+        uint32_t s = 0;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            uint32_t d = tid * J + j;
+            loc[j] = d < ndig ? dstart[d] : 0u;
+            s += loc[j];
+        }
+        uint32_t tot;
+        uint32_t run = block_excl_scan(s, scan_lds, &tot);
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            uint32_t d = tid * J + j;
+            if (d < ndig) dstart[d] = run;
+            run += loc[j];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const int64_t idx = base + (int64_t)i * kWave + lane;
+        if (idx < n) {
+            const uint32_t d = (k[i] >> shift) & mask;
+            const uint32_t slot = dstart[d] + wcnt[wave][d] + r[i];
+            sk[slot] = k[i];
+            sv[slot] = v[i];
+        }
+    }
+    __syncthreads();
+    const int64_t tile_n = n - (int64_t)blockIdx.x * kSortTile;
+    const uint32_t cnt = tile_n < kSortTile ? (uint32_t)tile_n : (uint32_t)kSortTile;
+#pragma unroll 4
+    for (int i = 0; i < kSortItems; ++i) {
+        const uint32_t slot = (uint32_t)i * kBlock + tid;
+        if (slot < cnt) {
+            const uint32_t key = sk[slot];
+            const uint32_t d = (key >> shift) & mask;
+            const uint32_t pos = dglob[d] + (slot - dstart[d]);
+            if ((int64_t)pos < n) {
+                kout[pos] = key;
+                vout[pos] = sv[slot];
+            }
+        }
+    }
+}
+
+__global__ void k_key_offsets(const uint32_t *__restrict__ keys, int64_t n, uint32_t *__restrict__ off,
+                              int64_t nkeys) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i > n) return;
+    const int64_t a = (i == 0) ? 0 : (int64_t)keys[i - 1] + 1;
+    int64_t b = (i == n) ? nkeys : (int64_t)keys[i];
+    b = b < nkeys ? b : nkeys;
+    for (int64_t k = a; k <= b; ++k) off[k] = (uint32_t)i;
+}
+
+__global__ void k_fill_u32(uint32_t *p, uint32_t v, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+__global__ void k_fill_f32(float *p, float v, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+}  // namespace
+
+size_t scan_work_bytes(int64_t n, int elem_bytes) {
+    return (size_t)(scan_levels_elems(n) + 1) * (size_t)elem_bytes;
+}
+
+hipError_t exclusive_scan_u32(const uint32_t *in, uint32_t *out, int64_t n, void *work, hipStream_t s) {
+    prof_begin("scan_u32", s);
+    hipError_t e = scan_rec<uint32_t>(in, out, n, (uint32_t *)work, s);
+    prof_end("scan_u32", s);
+    return e;
+}
+
+hipError_t exclusive_scan_u64(const uint64_t *in, uint64_t *out, int64_t n, void *work, hipStream_t s) {
+    prof_begin("scan_u64", s);
+    hipError_t e = scan_rec<uint64_t>(in, out, n, (uint64_t *)work, s);
+    prof_end("scan_u64", s);
+    return e;
+}
+
+int radix_passes(int bits) { return passes_for(bits); }
+
+size_t radix_work_bytes(int64_t n, int bits) {
+    const int db = digit_bits_for(bits);
+    if (db == 0) return 256;
+    const int64_t nb = ceil_div(n > 0 ? n : 1, kSortTile);
+    const int64_t table = (int64_t)(1 << db) * nb;
+    size_t bytes = (size_t)table * 4;
+    bytes = (bytes + 255) & ~(size_t)255;
+    return bytes + scan_work_bytes(table, 4) + 256;
+}
+
+// Sorts n pairs that start in (k0, v0); passes alternate between (k0, v0)
+// and (k1, v1). The result is in (k0, v0) after an even number of passes
+// and in (k1, v1) after an odd number (radix_passes(bits)).
+hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n, int bits, void *work,
+                            hipStream_t s) {
+    const int passes = passes_for(bits);
+    if (passes == 0 || n <= 0) return hipSuccess;
+    if (n == 1) {
+        // already sorted; move it where an odd number of passes would leave it
+        if (passes & 1) {
+            hipError_t e = hipMemcpyAsync(k1, k0, 4, hipMemcpyDeviceToDevice, s);
+            if (e == hipSuccess) e = hipMemcpyAsync(v1, v0, 4, hipMemcpyDeviceToDevice, s);
+            return e;
+        }
+        return hipSuccess;
+    }
+    const int db = digit_bits_for(bits);
+    const uint32_t ndig = 1u << db;
+    const uint32_t nb = (uint32_t)ceil_div(n, kSortTile);
+    uint32_t *table = (uint32_t *)work;
+    size_t tbytes = ((size_t)ndig * nb * 4 + 255) & ~(size_t)255;
+    void *scan_work = (char *)work + tbytes;
+    uint32_t *ki = k0, *vi = v0, *ko = k1, *vo = v1;
+    for (int p = 0; p < passes; ++p) {
+        const int shift = p * db;
+        prof_begin("radix_upsweep", s);
+        hipLaunchKernelGGL(k_radix_upsweep, dim3(nb), dim3(kBlock), 0, s, ki, n, shift, ndig - 1, ndig, table, nb);
+        prof_end("radix_upsweep", s);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        e = exclusive_scan_u32(table, table, (int64_t)ndig * nb, scan_work, s);
+        if (e != hipSuccess) return e;
+        prof_begin("radix_downsweep", s);
+        hipLaunchKernelGGL(k_radix_downsweep, dim3(nb), dim3(kBlock), 0, s, ki, vi, ko, vo, n, shift, db, table, nb);
+        prof_end("radix_downsweep", s);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        uint32_t *tk = ki, *tv = vi;
+        ki = ko;
+        vi = vo;
+        ko = tk;
+        vo = tv;
+    }
+    return hipSuccess;
+}
+
+hipError_t key_offsets(const uint32_t *sorted_keys, int64_t n, uint32_t *offsets, int64_t nkeys, hipStream_t s) {
+    const int64_t threads = n + 1;
+    prof_begin("key_offsets", s);
+    hipLaunchKernelGGL(k_key_offsets, dim3((uint32_t)ceil_div(threads, kBlock)), dim3(kBlock), 0, s, sorted_keys, n,
+                       offsets, nkeys);
+    prof_end("key_offsets", s);
+    return hipGetLastError();
+}
+
+hipError_t fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_fill_u32, dim3((uint32_t)ceil_div(n, kBlock)), dim3(kBlock), 0, s, p, v, n);
+    return hipGetLastError();
+}
+
+hipError_t fill_f32(float *p, float v, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_fill_f32, dim3((uint32_t)ceil_div(n, kBlock)), dim3(kBlock), 0, s, p, v, n);
+    return hipGetLastError();
+}
+
+}  // namespace gs

@@ -1,0 +1,356 @@
+"""Python binding of the C-ABI in include/gs.h (ctypes).
+
+Argument marshalling only: every step of sampling runs in the HIP library
+libgsq.so. torch provides device memory and the stream. Importing this module
+does not touch the GPU; the first call loads the library and raises
+GsLibraryMissing if it has not been built (python -m
+paper_2607_01164_amd.build) -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgsq.so")
+
+GS_OK = 0
+GS_ERR_INVALID_ARGUMENT = 1
+GS_ERR_CAPACITY = 2
+GS_ERR_WORKSPACE = 3
+GS_ERR_HIP = 4
+
+GS_QUERY_GRID = 0
+GS_QUERY_VOXELS = 1
+GS_QUERY_POINTS = 2
+
+EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_bytes", "gs_sample",
+            "gs_backward_work_bytes", "gs_sample_backward", "gs_last_error", "gs_version", "gs_profile_enable",
+            "gs_profile_reset", "gs_profile_read")
+
+
+class GsLibraryMissing(RuntimeError):
+    pass
+
+
+class GsError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"[gs status {status}] {message}")
+        self.status = status
+
+
+class GsGaussians(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("mean", ctypes.c_void_p), ("scale", ctypes.c_void_p),
+                ("rot", ctypes.c_void_p), ("value", ctypes.c_void_p), ("weight", ctypes.c_void_p)]
+
+
+class GsGrid(ctypes.Structure):
+    _fields_ = [("lo", ctypes.c_float * 3), ("hi", ctypes.c_float * 3), ("cells", ctypes.c_int32 * 3)]
+
+
+class GsIndex(ctypes.Structure):
+    _fields_ = [("keys", ctypes.c_void_p), ("gids", ctypes.c_void_p), ("cell_offsets", ctypes.c_void_p),
+                ("capacity", ctypes.c_int64), ("work", ctypes.c_void_p), ("work_bytes", ctypes.c_size_t),
+                ("n_pairs", ctypes.c_int64), ("n_gauss", ctypes.c_int64), ("grid", GsGrid), ("tau", ctypes.c_float)]
+
+
+class GsQuery(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("dims", ctypes.c_int32 * 3), ("n", ctypes.c_int64),
+                ("voxel_ids", ctypes.c_void_p), ("points", ctypes.c_void_p)]
+
+
+_LIB = None
+
+
+def load_library():
+    """Load libgsq.so (built in-tree) and declare the exported signatures."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(LIB_PATH):
+        raise GsLibraryMissing(f"{LIB_PATH} is missing: build it with `python -m paper_2607_01164_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+    P = ctypes.POINTER
+    L.gs_query_size.restype = i64
+    L.gs_query_size.argtypes = [P(GsQuery)]
+    L.gs_index_work_bytes.restype = sz
+    L.gs_index_work_bytes.argtypes = [i64, P(GsGrid), i64]
+    L.gs_build_index.restype = ctypes.c_int
+    L.gs_build_index.argtypes = [P(GsGaussians), P(GsGrid), ctypes.c_float, P(GsIndex), vp]
+    L.gs_plan_bytes.restype = sz
+    L.gs_plan_bytes.argtypes = [P(GsQuery), P(GsGrid)]
+    L.gs_sample.restype = ctypes.c_int
+    L.gs_sample.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, vp, vp, sz, vp]
+    L.gs_backward_work_bytes.restype = sz
+    L.gs_backward_work_bytes.argtypes = [P(GsIndex), P(GsQuery)]
+    L.gs_sample_backward.restype = ctypes.c_int
+    L.gs_sample_backward.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, sz, vp, vp, vp, vp, vp, vp, vp, vp,
+                                     vp, vp, sz, vp]
+    L.gs_last_error.restype = ctypes.c_char_p
+    L.gs_last_error.argtypes = []
+    L.gs_version.restype = ctypes.c_int
+    L.gs_version.argtypes = []
+    L.gs_profile_enable.restype = None
+    L.gs_profile_enable.argtypes = [ctypes.c_int]
+    L.gs_profile_reset.restype = None
+    L.gs_profile_reset.argtypes = []
+    L.gs_profile_read.restype = ctypes.c_int
+    L.gs_profile_read.argtypes = [P(ctypes.c_char_p), P(i64), P(ctypes.c_double), ctypes.c_int]
+    _LIB = L
+    return L
+
+
+def _check(status: int):
+    if status != GS_OK:
+        msg = load_library().gs_last_error().decode(errors="replace")
+        raise GsError(status, msg)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev_f32(t: torch.Tensor, name: str, shape_tail=()) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != torch.float32 or not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous float32")
+    if shape_tail and tuple(t.shape[1:]) != tuple(shape_tail):
+        raise ValueError(f"{name} must have shape [n, {', '.join(map(str, shape_tail))}]")
+    return t
+
+
+@dataclass
+class Gaussians:
+    """Post-activation parameters on the device: mean [n,3], scale [n,3],
+    rot [n,4] (w,x,y,z), value [n], weight [n]."""
+    mean: torch.Tensor
+    scale: torch.Tensor
+    rot: torch.Tensor
+    value: torch.Tensor
+    weight: torch.Tensor
+
+    @property
+    def n(self) -> int:
+        return int(self.mean.shape[0])
+
+    def c(self) -> GsGaussians:
+        n = self.n
+        _dev_f32(self.mean, "mean", (3,))
+        _dev_f32(self.scale, "scale", (3,))
+        _dev_f32(self.rot, "rot", (4,))
+        _dev_f32(self.value, "value")
+        _dev_f32(self.weight, "weight")
+        for t in (self.scale, self.rot):
+            if t.shape[0] != n:
+                raise ValueError("parameter arrays disagree on n")
+        for t in (self.value, self.weight):
+            if t.numel() != n:
+                raise ValueError("parameter arrays disagree on n")
+        return GsGaussians(n, self.mean.data_ptr(), self.scale.data_ptr(), self.rot.data_ptr(),
+                           self.value.data_ptr(), self.weight.data_ptr())
+
+
+def make_grid(cells: Sequence[int], lo=(0.0, 0.0, 0.0), hi=(1.0, 1.0, 1.0)) -> GsGrid:
+    return GsGrid((ctypes.c_float * 3)(*lo), (ctypes.c_float * 3)(*hi), (ctypes.c_int32 * 3)(*cells))
+
+
+@dataclass
+class Query:
+    kind: int
+    dims: Sequence[int] = (0, 0, 0)
+    voxel_ids: Optional[torch.Tensor] = None  # uint32 stored as int32 [n]
+    points: Optional[torch.Tensor] = None     # float32 [n,3]
+
+    @staticmethod
+    def grid(dims) -> "Query":
+        return Query(GS_QUERY_GRID, tuple(dims))
+
+    @staticmethod
+    def voxels(dims, ids: torch.Tensor) -> "Query":
+        return Query(GS_QUERY_VOXELS, tuple(dims), voxel_ids=ids)
+
+    @staticmethod
+    def pts(points: torch.Tensor) -> "Query":
+        return Query(GS_QUERY_POINTS, (0, 0, 0), points=points)
+
+    def c(self) -> GsQuery:
+        n = 0
+        if self.kind == GS_QUERY_VOXELS:
+            if self.voxel_ids is None or not self.voxel_ids.is_cuda or self.voxel_ids.element_size() != 4 or \
+                    not self.voxel_ids.is_contiguous():
+                raise ValueError("voxel_ids must be a contiguous 32-bit device tensor")
+            n = self.voxel_ids.numel()
+        elif self.kind == GS_QUERY_POINTS:
+            _dev_f32(self.points, "points", (3,))
+            n = self.points.shape[0]
+        d = tuple(self.dims) if self.kind != GS_QUERY_POINTS else (0, 0, 0)
+        return GsQuery(self.kind, (ctypes.c_int32 * 3)(*d), n, _ptr(self.voxel_ids), _ptr(self.points))
+
+    def size(self) -> int:
+        q = self.c()
+        return int(load_library().gs_query_size(ctypes.byref(q)))
+
+
+def _alloc_bytes(nbytes: int, device) -> torch.Tensor:
+    # 256-byte alignment: torch's caching allocator returns 512-byte aligned blocks
+    t = torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    assert t.data_ptr() % 256 == 0
+    return t
+
+
+class Index:
+    """A built cell index: owns its device buffers (torch tensors) and the
+    C struct that points at them."""
+
+    def __init__(self, grid: GsGrid, n_gauss: int, capacity: int, device):
+        L = load_library()
+        self.grid = grid
+        self.capacity = int(capacity)
+        self.device = device
+        ncells = grid.cells[0] * grid.cells[1] * grid.cells[2]
+        self.keys = torch.empty(max(self.capacity, 1), dtype=torch.int32, device=device)
+        self.gids = torch.empty(max(self.capacity, 1), dtype=torch.int32, device=device)
+        self.cell_offsets = torch.empty(ncells + 1, dtype=torch.int32, device=device)
+        wb = L.gs_index_work_bytes(n_gauss, ctypes.byref(grid), self.capacity)
+        if wb == ctypes.c_size_t(-1).value:
+            raise GsError(GS_ERR_INVALID_ARGUMENT, "bad grid or sizes")
+        self.work = _alloc_bytes(wb, device)
+        self.c = GsIndex(self.keys.data_ptr(), self.gids.data_ptr(), self.cell_offsets.data_ptr(), self.capacity,
+                         self.work.data_ptr(), int(self.work.numel()), -1, 0, grid, 0.0)
+
+    @property
+    def n_pairs(self) -> int:
+        return int(self.c.n_pairs)
+
+
+def gs_build_index(gauss: Gaussians, grid: GsGrid, tau: float, index: Index, stream=None) -> int:
+    """Build the index into `index`; raises GsError (status GS_ERR_CAPACITY
+    with index.n_pairs set when the capacity is too small)."""
+    g = gauss.c()
+    st = load_library().gs_build_index(ctypes.byref(g), ctypes.byref(grid), float(tau), ctypes.byref(index.c),
+                                       _stream(stream))
+    _check(st)
+    return index.n_pairs
+
+
+def build_index(gauss: Gaussians, grid: GsGrid, tau: float = 0.01, capacity: Optional[int] = None,
+                stream=None) -> Index:
+    """Allocate and build an index, growing the pair capacity once if needed."""
+    dev = gauss.mean.device
+    cap = int(capacity) if capacity is not None else max(1 << 16, 64 * gauss.n)
+    idx = Index(grid, gauss.n, cap, dev)
+    try:
+        gs_build_index(gauss, grid, tau, idx, stream)
+    except GsError as e:
+        if e.status != GS_ERR_CAPACITY:
+            raise
+        need = idx.n_pairs
+        idx = Index(grid, gauss.n, int(need * 1.05) + 1024, dev)
+        gs_build_index(gauss, grid, tau, idx, stream)
+    return idx
+
+
+def plan_bytes(query: Query, grid: GsGrid) -> int:
+    q = query.c()
+    b = load_library().gs_plan_bytes(ctypes.byref(q), ctypes.byref(grid))
+    if b == ctypes.c_size_t(-1).value:
+        raise GsError(GS_ERR_INVALID_ARGUMENT, "malformed query or grid")
+    return int(b)
+
+
+def alloc_plan(query: Query, grid: GsGrid, device) -> torch.Tensor:
+    return _alloc_bytes(plan_bytes(query, grid), device)
+
+
+def gs_sample(gauss: Gaussians, index: Index, query: Query, out_value: torch.Tensor, out_influence: torch.Tensor,
+              plan: Optional[torch.Tensor] = None, stream=None) -> None:
+    g = gauss.c()
+    q = query.c()
+    n = query.size()
+    for t, nm in ((out_value, "out_value"), (out_influence, "out_influence")):
+        _dev_f32(t, nm)
+        if t.numel() < n:
+            raise ValueError(f"{nm} needs {n} elements")
+    st = load_library().gs_sample(ctypes.byref(g), ctypes.byref(index.c), ctypes.byref(q), out_value.data_ptr(),
+                                  out_influence.data_ptr(), _ptr(plan), 0 if plan is None else plan.numel(),
+                                  _stream(stream))
+    _check(st)
+
+
+def backward_work_bytes(index: Index, query: Query) -> int:
+    q = query.c()
+    b = load_library().gs_backward_work_bytes(ctypes.byref(index.c), ctypes.byref(q))
+    if b == ctypes.c_size_t(-1).value:
+        raise GsError(GS_ERR_INVALID_ARGUMENT, "index not built or malformed query")
+    return int(b)
+
+
+def alloc_backward_work(index: Index, query: Query, device) -> torch.Tensor:
+    return _alloc_bytes(backward_work_bytes(index, query), device)
+
+
+@dataclass
+class Grads:
+    mean: torch.Tensor
+    scale: torch.Tensor
+    rot: torch.Tensor
+    value: torch.Tensor
+    weight: torch.Tensor
+
+    @staticmethod
+    def empty(n: int, device) -> "Grads":
+        f = dict(dtype=torch.float32, device=device)
+        return Grads(torch.empty(n, 3, **f), torch.empty(n, 3, **f), torch.empty(n, 4, **f), torch.empty(n, **f),
+                     torch.empty(n, **f))
+
+
+def gs_sample_backward(gauss: Gaussians, index: Index, query: Query, plan: Optional[torch.Tensor],
+                       value: torch.Tensor, influence: torch.Tensor, grad_value: torch.Tensor,
+                       grad_influence: torch.Tensor, grads: Grads, work: torch.Tensor, stream=None) -> None:
+    g = gauss.c()
+    q = query.c()
+    n = query.size()
+    for t, nm in ((value, "value"), (influence, "influence"), (grad_value, "grad_value"),
+                  (grad_influence, "grad_influence")):
+        _dev_f32(t, nm)
+        if t.numel() < n:
+            raise ValueError(f"{nm} needs {n} elements")
+    for t, nm in ((grads.mean, "d_mean"), (grads.scale, "d_scale"), (grads.rot, "d_rot"), (grads.value, "d_value"),
+                  (grads.weight, "d_weight")):
+        _dev_f32(t, nm)
+    st = load_library().gs_sample_backward(
+        ctypes.byref(g), ctypes.byref(index.c), ctypes.byref(q), _ptr(plan), 0 if plan is None else plan.numel(),
+        value.data_ptr(), influence.data_ptr(), grad_value.data_ptr(), grad_influence.data_ptr(),
+        grads.mean.data_ptr(), grads.scale.data_ptr(), grads.rot.data_ptr(), grads.value.data_ptr(),
+        grads.weight.data_ptr(), work.data_ptr(), work.numel(), _stream(stream))
+    _check(st)
+
+
+def profile_enable(on: bool = True) -> None:
+    load_library().gs_profile_enable(1 if on else 0)
+
+
+def profile_reset() -> None:
+    load_library().gs_profile_reset()
+
+
+def profile_read(max_entries: int = 64):
+    """{kernel name: (launches, total milliseconds)} recorded while enabled."""
+    L = load_library()
+    names = (ctypes.c_char_p * max_entries)()
+    counts = (ctypes.c_int64 * max_entries)()
+    ms = (ctypes.c_double * max_entries)()
+    n = L.gs_profile_read(names, counts, ms, max_entries)
+    return {names[i].decode(): (int(counts[i]), float(ms[i])) for i in range(min(n, max_entries))}

@@ -67,12 +67,13 @@ class Mixture:
             ok &= np.sum((x - np.asarray(c)[None, :]) ** 2, axis=1) >= r * r
         return ok
 
-    def sample(self, g: np.random.Generator, n: int) -> np.ndarray:
-        """n accepted points (float64), drawn in chunks with rejection."""
-        out = np.empty((n, 3))
+    def sample(self, g: np.random.Generator, n: int, dtype=np.float64) -> np.ndarray:
+        """n accepted points, drawn in rounds of at most 2^22 candidates with
+        rejection; stored as `dtype`."""
+        out = np.empty((n, 3), dtype=dtype)
         filled = 0
         while filled < n:
-            m = max(1024, int((n - filled) * 1.3))
+            m = min(1 << 22, max(1024, int((n - filled) * 1.3)))
             is_uni = g.random(m) < self.uniform_frac
             comp = g.integers(0, self.n_comp, size=m)
             z = g.standard_normal((m, 3)) * self.stds[comp]
@@ -205,7 +206,7 @@ def make_points(w: Workload, n: Optional[int] = None) -> np.ndarray:
     assert w.kind == "points"
     n = w.n_points if n is None else n
     mix = mixture_for(w)
-    return mix.sample(rng(w.cfg, S_POINTS), n).astype(np.float32)
+    return mix.sample(rng(w.cfg, S_POINTS), n, dtype=np.float32)
 
 
 def batch_permutation(w: Workload, total: int) -> np.ndarray:

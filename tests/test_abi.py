@@ -1,0 +1,209 @@
+"""The C-ABI library loads and exports every function include/gs.h declares,
+and its host-side validation rejects malformed arguments before any device
+work (no GPU needed: nothing here launches a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_01164_amd as gs
+from paper_2607_01164_amd import gsq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SIZE_ERR = ctypes.c_size_t(-1).value
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "gs.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gs_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("gs_build_index", "gs_sample", "gs_sample_backward", "gs_last_error"):
+        assert n in names
+    assert set(names) == set(gsq.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    L = gs.load_library()
+    for n in declared_functions():
+        assert hasattr(L, n), n
+    assert L.gs_version() >= 100
+
+
+def test_nm_lists_the_symbols():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", gsq.LIB_PATH], capture_output=True, text=True).stdout
+    for n in declared_functions():
+        assert re.search(rf"\bT {n}\b", out), n
+
+
+def grid(cells=(8, 8, 8), lo=(0, 0, 0), hi=(1, 1, 1)):
+    return gs.make_grid(cells, lo, hi)
+
+
+def test_sizing_functions():
+    L = gs.load_library()
+    g = grid()
+    a = L.gs_index_work_bytes(1000, ctypes.byref(g), 10000)
+    b = L.gs_index_work_bytes(2000, ctypes.byref(g), 10000)
+    c = L.gs_index_work_bytes(1000, ctypes.byref(g), 20000)
+    assert 0 < a < b and a < c and a % 256 == 0
+    assert L.gs_index_work_bytes(-1, ctypes.byref(g), 10) == SIZE_ERR
+    assert L.gs_index_work_bytes(10, ctypes.byref(grid((0, 8, 8))), 10) == SIZE_ERR
+    assert L.gs_index_work_bytes(10, ctypes.byref(grid(hi=(1, 0, 1))), 10) == SIZE_ERR
+    qg = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(32, 32, 32), 0, None, None)
+    assert L.gs_plan_bytes(ctypes.byref(qg), ctypes.byref(g)) == 0
+    assert L.gs_query_size(ctypes.byref(qg)) == 32 ** 3
+    qp = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 1000, None, 4096)
+    assert L.gs_plan_bytes(ctypes.byref(qp), ctypes.byref(g)) > 1000 * 16
+    assert L.gs_query_size(ctypes.byref(qp)) == 1000
+    bad = gsq.GsQuery(7, (ctypes.c_int32 * 3)(0, 0, 0), 10, None, None)
+    assert L.gs_query_size(ctypes.byref(bad)) == -1
+    nullpts = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 10, None, None)
+    assert L.gs_query_size(ctypes.byref(nullpts)) == -1
+    empty = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 0, None, None)
+    assert L.gs_query_size(ctypes.byref(empty)) == 0
+
+
+FAKE = 1 << 20  # a non-null, 256-aligned address that validation never dereferences
+
+
+def fake_gauss(n=10):
+    return gsq.GsGaussians(n, FAKE, FAKE, FAKE, FAKE, FAKE)
+
+
+def fake_index(capacity=100, work_bytes=1 << 30):
+    return gsq.GsIndex(FAKE, FAKE, FAKE, capacity, FAKE, work_bytes, -1, 0, grid(), 0.0)
+
+
+def call_build(gauss, g, tau, idx):
+    L = gs.load_library()
+    return L.gs_build_index(None if gauss is None else ctypes.byref(gauss), None if g is None else ctypes.byref(g),
+                            tau, None if idx is None else ctypes.byref(idx), None)
+
+
+@pytest.mark.parametrize("case", ["null_gauss", "neg_n", "null_param", "null_grid", "bad_cells", "flat_box",
+                                  "nan_box", "tau_zero", "tau_one", "null_index", "neg_capacity", "null_offsets",
+                                  "null_keys"])
+def test_build_index_rejects_bad_arguments(case):
+    L = gs.load_library()
+    gauss, g, tau, idx = fake_gauss(), grid(), 0.01, fake_index()
+    if case == "null_gauss":
+        gauss = None
+    elif case == "neg_n":
+        gauss = fake_gauss(-1)
+    elif case == "null_param":
+        gauss = gsq.GsGaussians(5, FAKE, None, FAKE, FAKE, FAKE)
+    elif case == "null_grid":
+        g = None
+    elif case == "bad_cells":
+        g = grid((8, -1, 8))
+    elif case == "flat_box":
+        g = grid(lo=(0, 0.5, 0), hi=(1, 0.5, 1))
+    elif case == "nan_box":
+        g = grid(lo=(float("nan"), 0, 0))
+    elif case == "tau_zero":
+        tau = 0.0
+    elif case == "tau_one":
+        tau = 1.0
+    elif case == "null_index":
+        idx = None
+    elif case == "neg_capacity":
+        idx = fake_index(capacity=-5)
+    elif case == "null_offsets":
+        idx = fake_index()
+        idx.cell_offsets = None
+    elif case == "null_keys":
+        idx = fake_index()
+        idx.keys = None
+    st = call_build(gauss, g, tau, idx)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+    assert L.gs_last_error().decode().startswith("gs_build_index")
+
+
+def test_build_index_rejects_small_or_misaligned_workspace():
+    L = gs.load_library()
+    st = call_build(fake_gauss(), grid(), 0.01, fake_index(work_bytes=1000))
+    assert st == gs.GS_ERR_WORKSPACE and b"workspace" in L.gs_last_error()
+    idx = fake_index()
+    idx.work = FAKE + 8
+    assert call_build(fake_gauss(), grid(), 0.01, idx) == gs.GS_ERR_WORKSPACE
+
+
+def test_sample_requires_a_built_index():
+    L = gs.load_library()
+    idx = fake_index()  # n_pairs = -1: never built
+    q = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(32, 32, 32), 0, None, None)
+    st = L.gs_sample(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(q), FAKE, FAKE, None, 0, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"not been built" in L.gs_last_error()
+
+
+def built_fake_index(n_gauss=10):
+    idx = fake_index()
+    idx.n_pairs = 50
+    idx.n_gauss = n_gauss
+    idx.tau = 0.01
+    return idx
+
+
+def test_sample_validates_queries():
+    L = gs.load_library()
+    idx = built_fake_index()
+    # GRID dims must be multiples of the index cells
+    q = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(30, 32, 32), 0, None, None)
+    st = L.gs_sample(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(q), FAKE, FAKE, None, 0, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"multiple" in L.gs_last_error()
+    # Gaussian count must match the index
+    q = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(32, 32, 32), 0, None, None)
+    st = L.gs_sample(ctypes.byref(fake_gauss(11)), ctypes.byref(idx), ctypes.byref(q), FAKE, FAKE, None, 0, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"built for 10" in L.gs_last_error()
+    # outputs must be given
+    st = L.gs_sample(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(q), None, FAKE, None, 0, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+    # point queries need a plan of gs_plan_bytes
+    qp = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 100, None, FAKE)
+    st = L.gs_sample(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(qp), FAKE, FAKE, FAKE, 16, None)
+    assert st == gs.GS_ERR_WORKSPACE and b"plan" in L.gs_last_error()
+    # negative counts and unknown kinds
+    qn = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), -3, None, FAKE)
+    st = L.gs_sample(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(qn), FAKE, FAKE, FAKE, 1 << 20, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+    qk = gsq.GsQuery(9, (ctypes.c_int32 * 3)(0, 0, 0), 3, None, FAKE)
+    st = L.gs_sample(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(qk), FAKE, FAKE, FAKE, 1 << 20, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+
+
+def test_backward_validates_arguments():
+    L = gs.load_library()
+    idx = built_fake_index()
+    q = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(32, 32, 32), 0, None, None)
+    args = [ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(q), None, 0] + [FAKE] * 9
+    st = L.gs_sample_backward(*args, FAKE, 16, None)
+    assert st == gs.GS_ERR_WORKSPACE
+    need = L.gs_backward_work_bytes(ctypes.byref(idx), ctypes.byref(q))
+    assert 0 < need < SIZE_ERR
+    args_null = list(args)
+    args_null[5] = None  # value
+    st = L.gs_sample_backward(*args_null, FAKE, need, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+    args_null = list(args)
+    args_null[12] = None  # d_value
+    st = L.gs_sample_backward(*args_null, FAKE, need, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        gs.Gaussians(torch.zeros(3, 3), torch.ones(3, 3), torch.ones(3, 4), torch.ones(3), torch.ones(3)).c()
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch):
+    monkeypatch.setattr(gsq, "_LIB", None)
+    monkeypatch.setattr(gsq, "LIB_PATH", "/nonexistent/libgsq.so")
+    with pytest.raises(gs.GsLibraryMissing):
+        gsq.load_library()

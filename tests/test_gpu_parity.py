@@ -1,0 +1,254 @@
+"""Parity of the HIP path (through the C-ABI) with the CPU oracle.
+
+Index: bit-exact (keys, Gaussian ids, per-cell ranges). Forward: relative
+1e-5 plus the per-point float32 conditioning allowance, with the results
+float32 may legitimately produce at points within rounding of the cutoff or
+of the definedness threshold accepted. Backward: 1e-4 of (|ref| + the sum of
+absolute per-pair terms) plus the conditioning allowance, with cotangents
+zeroed at those ambiguous points on both sides.
+
+Small cases compare every output; the five workloads run at full size, in
+the launch configuration the benchmark times, and compare sampled outputs
+the oracle computes one by one."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from harness import TAU, Run, check_backward, check_forward, check_index, log
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_01164_amd as gs
+    gs.load_library()
+
+
+def masked_cotangents(ref, gv, gi, where=None):
+    amb = oracle.ambiguous_points(ref, TAU)
+    gv = gv.copy()
+    gi = gi.copy()
+    if where is None:
+        gv[amb] = 0
+        gi[amb] = 0
+    else:
+        gv[where[amb]] = 0
+        gi[where[amb]] = 0
+    return gv, gi, amb
+
+
+# ---------------------------------------------------------------- small cases
+
+@pytest.mark.parametrize("cells", [(8, 8, 8), (16, 16, 16)])
+def test_c1_grid_full(cells):
+    w = synth.WORKLOADS["c1_grid32"]
+    g = synth.make_gaussians(w)
+    log(f"case c1 grid 32^3, cells {cells}")
+    r = Run(g, cells, "grid", dims=w.dims)
+    check_index(r)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="c1")
+    gv, gi = synth.cotangents(w, r.nq)
+    gv, gi, amb = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    pts = r.positions()
+    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="c1 all Gaussians")
+
+
+@pytest.mark.parametrize("dims,cells", [((24, 20, 12), (8, 4, 3)), ((40, 40, 40), (4, 4, 4)),
+                                        ((16, 16, 16), (1, 1, 1)), ((30, 18, 7), (5, 3, 7))])
+def test_grid_ragged_cells(dims, cells):
+    """Voxels per cell below, above and not a multiple of the wave size,
+    a single cell, and non-cubic grids."""
+    g = synth.random_gaussians(50, 700, log_mu=np.log(0.04), log_sd=0.5)
+    log(f"case grid dims {dims} cells {cells}")
+    r = Run(g, cells, "grid", dims=dims)
+    check_index(r)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="ragged")
+    gv, gi = synth.random_normal(51, r.nq), synth.random_normal(52, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), r.positions(), ref.phi, ref.inf, gv, gi, label="ragged")
+
+
+def test_grid_non_unit_box():
+    g = synth.random_gaussians(53, 500, log_mu=np.log(0.08), log_sd=0.4, lo=-1.0, hi=2.0)
+    lo, hi = (-1.0, -0.5, 0.25), (2.0, 1.5, 1.0)
+    log("case non-unit box")
+    r = Run(g, (6, 4, 3), "grid", dims=(36, 24, 12), lo=lo, hi=hi)
+    check_index(r)
+    phi, inf = r.forward()
+    check_forward(r, phi, inf, label="box")
+
+
+def test_voxel_list_small():
+    dims = (64, 48, 32)
+    nvox = 64 * 48 * 32
+    g = synth.random_gaussians(54, 3000, log_mu=np.log(0.03), log_sd=0.5)
+    ids = np.random.default_rng(7).choice(nvox, size=20011, replace=False).astype(np.uint32)
+    ids[:5] = [nvox, nvox + 17, 0xFFFFFFF0, 0, nvox - 1]  # out-of-range ids are outside the domain
+    log("case voxel list 20011 ids")
+    r = Run(g, (16, 12, 8), "voxels", dims=dims, ids=ids)
+    check_index(r)
+    phi, inf = r.forward()
+    assert phi[0] == 0 and inf[0] == 0 and phi[1] == 0 and phi[2] == 0
+    ok = np.arange(len(ids)) >= 3
+    check_forward(r, phi, inf, sel=np.nonzero(ok)[0], label="voxels")
+    ref = oracle.forward(g, r.positions(np.nonzero(ok)[0]))
+    gv, gi = synth.random_normal(55, r.nq), synth.random_normal(56, r.nq)
+    gv[~ok] = 0
+    gi[~ok] = 0
+    sub = np.nonzero(ok)[0]
+    gv, gi, _ = masked_cotangents(ref, gv, gi, where=sub)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), r.positions(sub), ref.phi, ref.inf, gv[sub], gi[sub], label="voxels")
+
+
+def test_points_small_with_outside_and_boundary():
+    g = synth.random_gaussians(57, 2500, log_mu=np.log(0.04), log_sd=0.6)
+    pts = synth.random_points(58, 30000, -0.05, 1.05)
+    pts[:6] = [[0, 0, 0], [1, 1, 1], [0, 0.5, 1], [1.0000001, 0.5, 0.5], [-1e-7, 0.5, 0.5], [0.5, 0.5, 0.5]]
+    log("case points 30000 incl. outside")
+    r = Run(g, (10, 10, 10), "points", points=pts)
+    check_index(r)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="points")
+    inside = np.all((pts >= 0) & (pts <= 1), axis=1)
+    assert np.all(phi[~inside] == 0) and np.all(inf[~inside] == 0)
+    gv, gi = synth.random_normal(59, r.nq), synth.random_normal(60, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="points")
+
+
+def test_point_plan_order_matches_oracle():
+    """The query ordering kept in the plan (Sec. 5.1 analogue of the sample
+    BVH): keys and ids bit-exact against the oracle's stable order."""
+    g = synth.random_gaussians(61, 100)
+    pts = synth.random_points(62, 50000, -0.1, 1.1)
+    log("case plan order")
+    r = Run(g, (7, 9, 11), "points", points=pts)
+    r.forward()
+    n = len(pts)
+    plan = r.plan.cpu().numpy()
+    keys = plan[: 4 * n].view(np.uint32)
+    order = plan[_align(4 * n): _align(4 * n) + 4 * n].view(np.uint32)
+    rk, ro, _ = oracle.point_order(pts, (7, 9, 11))
+    np.testing.assert_array_equal(keys, rk)
+    np.testing.assert_array_equal(order, ro)
+
+
+def _align(x):
+    return (x + 255) // 256 * 256
+
+
+def test_invalid_and_degenerate_gaussians():
+    g = synth.random_gaussians(63, 400, log_mu=np.log(0.06))
+    g.rot[0] = 0                       # zero quaternion
+    g.mean[1, 1] = np.nan
+    g.scale[2, 0] = 0
+    g.scale[3, 2] = -0.1
+    g.value[4] = np.inf
+    g.weight[5] = np.nan
+    g.mean[6] = [5, 5, 5]              # entirely outside the domain
+    g.rot[7] = [1e-30, 0, 0, 0]        # float32 squared norm underflows to zero
+    g.rot[8] = [3, -2, 7, 1]           # unnormalised, valid
+    log("case invalid Gaussians")
+    r = Run(g, (8, 8, 8), "grid", dims=(32, 32, 32))
+    check_index(r)
+    phi, inf = r.forward()
+    assert np.all(np.isfinite(phi)) and np.all(np.isfinite(inf))
+    ref, _ = check_forward(r, phi, inf, label="invalid")
+    gv, gi = synth.random_normal(64, r.nq), synth.random_normal(65, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    assert np.all(grads[:8] == 0)
+    assert np.all(np.isfinite(grads))
+    check_backward(r, grads, np.arange(g.n), r.positions(), ref.phi, ref.inf, gv, gi, label="invalid")
+
+
+def test_empty_inputs():
+    import torch
+    import paper_2607_01164_amd as gs
+    log("case empty inputs")
+    # no Gaussians: every point undefined, nothing to differentiate
+    g0 = synth.random_gaussians(66, 1)
+    g0 = g0.subset(np.arange(0))
+    r = Run(g0, (4, 4, 4), "points", points=synth.random_points(67, 1000))
+    assert r.index.n_pairs == 0
+    phi, inf = r.forward()
+    assert np.all(phi == 0) and np.all(inf == 0)
+    # no queries
+    g = synth.random_gaussians(68, 50)
+    r2 = Run(g, (4, 4, 4), "points", points=np.zeros((0, 3), np.float32))
+    assert r2.nq == 0
+    r2.forward()
+    grads = r2.backward(np.zeros(0, np.float32), np.zeros(0, np.float32))
+    assert np.all(grads == 0)
+    # a single Gaussian and a single point
+    g1 = synth.random_gaussians(69, 1, log_mu=np.log(0.1))
+    p1 = g1.mean.copy()
+    r3 = Run(g1, (3, 3, 3), "points", points=p1)
+    phi, inf = r3.forward()
+    assert inf[0] == pytest.approx(float(g1.weight[0]), rel=1e-6)
+    assert phi[0] == pytest.approx(float(g1.value[0]), rel=1e-6)
+    grads = r3.backward(np.ones(1, np.float32), np.ones(1, np.float32))
+    assert grads[0, 10] == pytest.approx(1.0, rel=1e-6)     # dv = gPhi
+    assert grads[0, 11] == pytest.approx(1.0, rel=1e-6)     # dw = gI G, G = 1 at the mean
+    assert np.all(np.abs(grads[0, :3]) < 1e-3)              # at the mean dmu = 0
+    del torch, gs
+
+
+def test_capacity_error_reports_pairs():
+    import paper_2607_01164_amd as gs
+    g = synth.random_gaussians(70, 300, log_mu=np.log(0.05))
+    log("case capacity error")
+    dg = __import__("harness").dev_gauss(g)
+    grid = gs.make_grid((8, 8, 8))
+    box, cnt = oracle.index_boxes(g, (8, 8, 8))
+    idx = gs.Index(grid, g.n, int(cnt.sum()) - 1, "cuda")
+    with pytest.raises(gs.GsError) as e:
+        gs.gs_build_index(dg, grid, TAU, idx)
+    assert e.value.status == gs.GS_ERR_CAPACITY
+    assert idx.n_pairs == int(cnt.sum())
+    idx2 = gs.Index(grid, g.n, int(cnt.sum()), "cuda")
+    assert gs.gs_build_index(dg, grid, TAU, idx2) == int(cnt.sum())
+
+
+def test_forward_is_deterministic():
+    w = synth.WORKLOADS["c1_grid32"]
+    g = synth.make_gaussians(w)
+    pts = synth.random_points(71, 100000)
+    log("case determinism")
+    r = Run(g, (8, 8, 8), "points", points=pts)
+    a = r.forward()
+    b = r.forward()
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    rg = Run(g, (8, 8, 8), "grid", dims=(32, 32, 32))
+    c = rg.forward()
+    d = rg.forward()
+    np.testing.assert_array_equal(c[0], d[0])
+
+
+def test_sum_rules_hold_on_device():
+    """sum_i dv_i = sum over defined points of gPhi, and
+    sum_i w_i dw_i = sum over defined points of gI I (any size)."""
+    w = synth.WORKLOADS["c1_grid32"]
+    g = synth.make_gaussians(w)
+    log("case sum rules")
+    r = Run(g, (8, 8, 8), "grid", dims=(32, 32, 32))
+    phi, inf = r.forward()
+    gv, gi = synth.cotangents(w, r.nq, batch_index=5)
+    grads = r.backward(gv, gi)
+    d = inf > 0
+    s1 = float(gv[d].astype(np.float64).sum())
+    s2 = float((gi[d].astype(np.float64) * inf[d]).sum())
+    assert grads[:, 10].astype(np.float64).sum() == pytest.approx(s1, rel=1e-4, abs=1e-3)
+    assert (g.weight.astype(np.float64) * grads[:, 11]).sum() == pytest.approx(s2, rel=1e-4, abs=1e-3)

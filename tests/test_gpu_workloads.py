@@ -1,0 +1,105 @@
+"""The five workloads at full size on the GPU, in the launch configuration
+the benchmark times: the index compared bit for bit, forward outputs and
+Gaussian gradients compared on seeded samples the oracle computes one by
+one (brute force over every Gaussian)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from harness import TAU, Run, check_backward, check_forward, check_index, log
+
+pytestmark = pytest.mark.gpu
+
+N_FWD_SAMPLE = 2048
+N_BWD_SAMPLE = 96
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def sample_ids(n, k, seed):
+    return np.sort(np.random.default_rng(seed).choice(n, size=min(k, n), replace=False))
+
+
+def sampled_backward(r: Run, w, seed):
+    """Gradients of N_BWD_SAMPLE seeded Gaussians: the oracle recomputes the
+    forward at every query within their reach and the exact gradient."""
+    sel = sample_ids(r.g.n, N_BWD_SAMPLE, seed)
+    pts_all = r.positions()
+    sup = np.nonzero(oracle.support(r.g, pts_all, sel, r.lo, r.hi, TAU))[0]
+    ref = oracle.forward(r.g, pts_all[sup], r.lo, r.hi, TAU)
+    gv, gi = synth.cotangents(w, r.nq)
+    amb = oracle.ambiguous_points(ref, TAU)
+    gv[sup[amb]] = 0
+    gi[sup[amb]] = 0
+    log(f"  support of {len(sel)} Gaussians: {len(sup)} queries, {int(amb.sum())} ambiguous")
+    grads = r.backward(gv, gi)
+    assert np.all(np.isfinite(grads))
+    check_backward(r, grads, sel, pts_all[sup], ref.phi, ref.inf, gv[sup], gi[sup], label=w.name)
+    return grads
+
+
+def test_c2_grid256_batch_step():
+    w = synth.WORKLOADS["c2_grid256_batch"]
+    g = synth.make_gaussians(w)
+    ids = synth.voxel_batch(w)
+    log(f"case {w.name}: {g.n} Gaussians, {len(ids)} voxel queries, cells {w.index_cells}")
+    r = Run(g, w.index_cells, "voxels", dims=w.dims, ids=ids)
+    check_index(r)
+    phi, inf = r.forward()
+    check_forward(r, phi, inf, sel=sample_ids(r.nq, N_FWD_SAMPLE, 1), label=w.name)
+    sampled_backward(r, w, 2)
+
+
+def test_c3_grid512_full_forward():
+    w = synth.WORKLOADS["c3_grid512_full"]
+    g = synth.make_gaussians(w)
+    log(f"case {w.name}: {g.n} Gaussians, 512^3 grid, cells {w.index_cells}")
+    r = Run(g, w.index_cells, "grid", dims=w.dims)
+    check_index(r)
+    phi, inf = r.forward()
+    assert np.all(np.isfinite(phi))
+    check_forward(r, phi, inf, sel=sample_ids(r.nq, N_FWD_SAMPLE, 3), label=w.name)
+    # the sample also covers the densest cells: queries at the cluster cores
+    mix = synth.mixture_for(w)
+    c = np.clip(np.floor(mix.centers[:16] * 512), 0, 511).astype(np.int64)
+    core_ids = c[:, 0] + 512 * (c[:, 1] + 512 * c[:, 2])
+    check_forward(r, phi, inf, sel=core_ids, label="cluster cores")
+
+
+def test_c4_points_batches():
+    w = synth.WORKLOADS["c4_points8m"]
+    g = synth.make_gaussians(w)
+    pts = synth.make_points(w)
+    perm = synth.batch_permutation(w, len(pts))
+    batch = pts[perm[: w.batch]]
+    log(f"case {w.name}: {g.n} Gaussians, batch of {len(batch)} points, cells {w.index_cells}")
+    r = Run(g, w.index_cells, "points", points=batch)
+    check_index(r)
+    phi, inf = r.forward()
+    ref, stats = check_forward(r, phi, inf, sel=sample_ids(r.nq, N_FWD_SAMPLE, 4), label=w.name)
+    # queries inside the cavity lie in empty space
+    cav = np.sum((batch - 0.5) ** 2, axis=1) < 0.2 ** 2
+    assert cav.sum() == 0
+    sampled_backward(r, w, 5)
+
+
+def test_c5_points_full_forward():
+    w = synth.WORKLOADS["c5_points100m"]
+    g = synth.make_gaussians(w)
+    pts = synth.make_points(w)
+    log(f"case {w.name}: {g.n} Gaussians, {len(pts)} points, cells {w.index_cells}")
+    r = Run(g, w.index_cells, "points", points=pts)
+    check_index(r)
+    phi, inf = r.forward()
+    assert np.all(np.isfinite(phi)) and np.all(np.isfinite(inf))
+    check_forward(r, phi, inf, sel=sample_ids(r.nq, 1024, 6), label=w.name)
+    # probes: cavity centres and rims, domain corners
+    probes = np.array([[0.3, 0.3, 0.3], [0.7, 0.7, 0.7], [0.3 + 0.149, 0.3, 0.3], [0, 0, 0], [1, 1, 1]], np.float32)
+    rp = oracle.forward(g, probes)
+    log(f"  probes: oracle I {rp.inf}")
