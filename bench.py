@@ -1,0 +1,220 @@
+"""Benchmark of the Gaussian-field sampling hot path on one MI355X.
+
+Workload: structured 256^3 grid over [0,1]^3, 262,144 Gaussians (means
+U[0,1]^3, log-scales N(ln 0.008, 0.4) per axis, random unit quaternions,
+values U[0,1], weights sigmoid(N(0,1))); one step is a training step on a
+seeded random batch of 2^20 voxel centres: build the cell index, sample
+(query ordering + forward) and backpropagate N(0,1) cotangents to every
+Gaussian parameter. All inputs are resident in HBM before the timed region.
+
+Prints one JSON line: fwd+bwd samples/s over the timed steps, with the
+forward-only query rate, the per-kernel timing of the step (HIP events on
+the library's stream), the roofline of the dominant kernel and the CPU
+oracle's rate on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP32_VEC_PEAK_TFLOPS = 157.3   # MI355X vector FP32 (packed FMA)
+WORKLOAD = "c2_grid256_batch"
+INDEX_CELLS = (64, 64, 64)
+TAU = 0.01
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--cells", type=int, nargs=3, default=list(INDEX_CELLS))
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target length of the CPU oracle sample")
+    p.add_argument("--no-cpu", action="store_true")
+    p.add_argument("--breakdown", action="store_true", help="print the per-kernel table to stderr")
+    return p.parse_args()
+
+
+class Step:
+    def __init__(self, cells):
+        import numpy as np
+        import torch
+
+        import paper_2607_01164_amd as gs
+        import synth
+        self.gs, self.torch, self.np = gs, torch, np
+        w = synth.WORKLOADS[WORKLOAD]
+        self.w = w
+        g = synth.make_gaussians(w)
+        self.g_host = g
+        self.ids_host = synth.voxel_batch(w)
+        gv, gi = synth.cotangents(w, len(self.ids_host))
+        dev = "cuda:0"
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+        self.dg = gs.Gaussians(t(g.mean), t(g.scale), t(g.rot), t(g.value), t(g.weight))
+        self.ids = torch.from_numpy(self.ids_host.view(np.int32)).to(dev)
+        self.gv, self.gi = t(gv), t(gi)
+        self.grid = gs.make_grid(cells)
+        self.query = gs.Query.voxels(w.dims, self.ids)
+        self.n = len(self.ids_host)
+        probe = gs.build_index(self.dg, self.grid, TAU)
+        self.index = gs.Index(self.grid, g.n, int(probe.n_pairs * 1.25) + 4096, dev)
+        del probe
+        self.plan = gs.alloc_plan(self.query, self.grid, dev)
+        self.val = torch.empty(self.n, dtype=torch.float32, device=dev)
+        self.inf = torch.empty(self.n, dtype=torch.float32, device=dev)
+        self.grads = gs.Grads.empty(g.n, dev)
+        gs.gs_build_index(self.dg, self.grid, TAU, self.index)
+        self.work = gs.alloc_backward_work(self.index, self.query, dev)
+        torch.cuda.synchronize()
+
+    def build(self):
+        self.gs.gs_build_index(self.dg, self.grid, TAU, self.index)
+
+    def forward(self):
+        self.gs.gs_sample(self.dg, self.index, self.query, self.val, self.inf, self.plan)
+
+    def backward(self):
+        self.gs.gs_sample_backward(self.dg, self.index, self.query, self.plan, self.val, self.inf, self.gv, self.gi,
+                                   self.grads, self.work)
+
+    def step(self):
+        self.build()
+        self.forward()
+        self.backward()
+
+
+def timed(fn, k, sync):
+    sync()
+    t0 = time.perf_counter()
+    for _ in range(k):
+        fn()
+    sync()
+    return (time.perf_counter() - t0) / k
+
+
+def cpu_baseline(st: Step, target_s: float):
+    """The oracle (float64 brute force over every Gaussian, OpenMP over
+    points, then Gaussian-major backward) on a seeded sample of the batch."""
+    import numpy as np
+
+    import oracle
+    g = st.g_host
+    sel_all = np.random.default_rng(11).permutation(st.n)
+    threads = oracle.default_threads()
+
+    def run(m):
+        sel = sel_all[:m]
+        pts = oracle.voxel_centers(st.w.dims, ids=st.ids_host[sel])
+        gv = st.gv.cpu().numpy()[sel]
+        gi = st.gi.cpu().numpy()[sel]
+        t0 = time.perf_counter()
+        ref = oracle.forward(g, pts, tau=TAU, threads=threads)
+        oracle.backward(g, pts, ref.phi, ref.inf, gv, gi, tau=TAU, threads=threads)
+        return time.perf_counter() - t0, ref
+
+    m = 512
+    dt, ref = run(m)
+    m2 = int(min(65536, max(m, m * target_s / max(dt, 1e-3))))
+    if m2 > m:
+        dt, ref = run(m2)
+        m = m2
+    return {"value": m / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
+            "sample": f"{m} of the {st.n} batch voxels, forward + backward to all {g.n} Gaussians, {dt:.1f} s",
+            "contrib_per_point": float(ref.ncontrib.mean())}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the sharded path is not built",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2607_01164_amd as gs
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    st = Step(tuple(a.cells))
+    sync = torch.cuda.synchronize
+    for _ in range(a.warmup):
+        st.step()
+    sync()
+    # timed region: K whole steps, kernels bracketed by HIP events on the stream
+    gs.profile_reset()
+    gs.profile_enable(True)
+    t_step = timed(st.step, a.steps, sync)
+    gs.profile_enable(False)
+    prof = gs.profile_read()
+    n_pairs = st.index.n_pairs
+    # forward alone and backward alone, for the query rates
+    t_fwd = timed(st.forward, a.steps, sync)
+    t_bwd = timed(st.backward, a.steps, sync)
+    t_build = timed(st.build, a.steps, sync)
+
+    kernels = {k: {"launches_per_step": c / a.steps, "ms_per_step": ms / a.steps, "avg_ms": ms / c}
+               for k, (c, ms) in prof.items()}
+    if a.breakdown:
+        for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
+            log(f"{k:18s} {v['ms_per_step'] * 1e3:9.1f} us/step  {v['launches_per_step']:5.1f} launches  "
+                f"avg {v['avg_ms'] * 1e3:9.1f} us")
+    dom = max(kernels.items(), key=lambda kv: kv[1]["ms_per_step"])
+    roof = roofline(dom[0], dom[1], st, n_pairs)
+
+    cpu = None if a.no_cpu else cpu_baseline(st, a.cpu_seconds)
+    contrib = cpu.pop("contrib_per_point") if cpu else None
+    out = {
+        "metric": "query points/sec fwd and fwd+bwd samples/sec; % of HBM roofline",
+        "value": st.n / t_step,
+        "unit": "fwd+bwd samples/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": t_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{WORKLOAD}: 256^3 grid, 262144 Gaussians, batch of 2^20 random voxel centres, "
+                               f"index {a.cells[0]}x{a.cells[1]}x{a.cells[2]} cells, step = build + forward + backward",
+                   "global_batch": st.n, "n_gauss": st.g_host.n, "index_pairs": n_pairs},
+        "fwd_points_per_s": st.n / t_fwd,
+        "fwd_bwd_samples_per_s_excl_build": st.n / (t_fwd + t_bwd),
+        "ms_build": t_build * 1e3, "ms_fwd": t_fwd * 1e3, "ms_bwd": t_bwd * 1e3,
+        "gauss_point_evals_per_s": (contrib * st.n / t_fwd) if contrib else None,
+        "kernels": {k: round(v["ms_per_step"] * 1e3, 2) for k, v in kernels.items()},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def roofline(name, k, st, n_pairs):
+    """Roofline entry of the dominant kernel: algorithmic bytes (or flops) of
+    one launch over its average launch duration."""
+    avg_s = k["avg_ms"] * 1e-3
+    per_step = k["launches_per_step"]
+    if name == "radix_downsweep":
+        # one pass reads and writes (key, value) of every pair: 16 B per pair
+        byts = 16.0 * n_pairs
+        ach = byts / avg_s / 1e9
+        return {"bound": "hbm", "kernel": name, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": ach / HBM_PEAK_GBS, "traffic": None, "bytes_per_launch": byts, "avg_us": avg_s * 1e6}
+    if name == "emit":
+        byts = 8.0 * n_pairs
+        ach = byts / avg_s / 1e9
+        return {"bound": "hbm", "kernel": name, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": ach / HBM_PEAK_GBS, "traffic": None, "bytes_per_launch": byts, "avg_us": avg_s * 1e6}
+    return {"bound": "unknown", "kernel": name, "avg_us": avg_s * 1e6, "launches_per_step": per_step}
+
+
+if __name__ == "__main__":
+    main()
