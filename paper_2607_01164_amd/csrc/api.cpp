@@ -103,6 +103,11 @@ GridParams grid_params(const gs_grid *g) {
 struct IndexWork {
     Record *rec;
     CellBox *box;
+    uint32_t *gorder;    // [n] Gaussians in spatial order
+    uint32_t *gkeys;     // [n] their sort keys
+    uint32_t *gsort_k;   // [n] sort scratch
+    uint32_t *gsort_v;   // [n] sort scratch
+    void *gsort_work;
     uint64_t *pair_off;  // [n + 1]
     void *scan_work;
     uint32_t *keys_alt;
@@ -116,6 +121,12 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     IndexWork w;
     w.rec = c.take<Record>((size_t)(n > 0 ? n : 1));
     w.box = c.take<CellBox>((size_t)(n > 0 ? n : 1));
+    const size_t n1 = (size_t)(n > 0 ? n : 1);
+    w.gorder = c.take<uint32_t>(n1);
+    w.gkeys = c.take<uint32_t>(n1);
+    w.gsort_k = c.take<uint32_t>(n1);
+    w.gsort_v = c.take<uint32_t>(n1);
+    w.gsort_work = c.take<char>(radix_work_bytes((int64_t)n1, bits_for(ncells_of(g) + 1)));
     w.pair_off = c.take<uint64_t>((size_t)n + 1);
     w.scan_work = c.take<char>(scan_work_bytes(n + 1, 8));
     const int64_t cap = capacity > 0 ? capacity : 1;
@@ -239,13 +250,6 @@ struct BwdWork {
     size_t bytes;
 };
 
-int64_t max_backward_items(const gs_index *index, const gs_query *q) {
-    int64_t factor = 1;
-    if (q->kind == GS_QUERY_GRID)
-        factor = (int64_t)(q->dims[1] / index->grid.cells[1]) * (q->dims[2] / index->grid.cells[2]);
-    return index->n_pairs * factor / kRowGroup + index->n_gauss + 1;
-}
-
 BwdWork bwd_layout(void *base, const gs_index *index, const gs_query *q) {
     Carver c(base);
     BwdWork w;
@@ -253,10 +257,6 @@ BwdWork bwd_layout(void *base, const gs_index *index, const gs_query *q) {
     const int64_t nq = query_count(q);
     const size_t mq = (size_t)(nq > 0 ? nq : 1);
     w.b.moments = c.take<float>((size_t)(n > 0 ? n : 1) * 12);
-    w.b.item_off = c.take<uint32_t>((size_t)n + 1);
-    w.b.scan_work = c.take<char>(scan_work_bytes(n + 1, 4));
-    w.b.max_items = max_backward_items(index, q);
-    w.b.items = c.take<uint32_t>((size_t)w.b.max_items);
     if (q->kind == GS_QUERY_GRID) {
         w.b.pts = nullptr;
         w.b.alpha = c.take<float>(mq);
@@ -415,6 +415,15 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     GS_TRY(launch_preprocess(gauss->mean, gauss->scale, gauss->rot, gauss->value, gauss->weight, n, gp,
                              index_radius(tau), w.rec, w.box, w.pair_off, stream),
            "gs_build_index: preprocess");
+    {
+        // spatial visiting order of the Gaussians (sorted by box corner cell)
+        const int gbits = bits_for(ncells + 1);
+        const bool godd = (radix_passes(gbits) & 1) != 0;
+        uint32_t *k0 = godd ? w.gsort_k : w.gkeys, *v0 = godd ? w.gsort_v : w.gorder;
+        uint32_t *k1 = godd ? w.gkeys : w.gsort_k, *v1 = godd ? w.gorder : w.gsort_v;
+        GS_TRY(launch_gauss_keys(w.box, n, gp, k0, v0, stream), "gs_build_index: Gaussian keys");
+        GS_TRY(radix_sort_pairs(k0, v0, k1, v1, n, gbits, w.gsort_work, stream), "gs_build_index: Gaussian order");
+    }
     GS_TRY(exclusive_scan_u64(w.pair_off, w.pair_off, n + 1, w.scan_work, stream), "gs_build_index: scan");
     uint64_t P = 0;
     GS_TRY(hipMemcpyAsync(&P, w.pair_off + n, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
@@ -542,7 +551,7 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
     }
     IndexWork w = index_layout(index->work, n, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
-    GS_TRY(launch_backward(qp, gp, w.rec, w.box, n, p.keys, p.order, p.point_off, value, influence, grad_value,
+    GS_TRY(launch_backward(qp, gp, w.rec, w.box, w.gorder, n, p.keys, p.order, p.point_off, value, influence, grad_value,
                            grad_influence, cutoff_T(index->tau), bw.b, gauss->mean, gauss->scale, gauss->rot, d_mean,
                            d_scale, d_rot, d_value, d_weight, stream),
            "gs_sample_backward");

@@ -2,13 +2,20 @@
 //
 // The paper assigns a thread to every (Gaussian, block) intersection, sums
 // its Gaussian's partials over the block's cells and issues one atomic add
-// per intersection. Here the work is Gaussian-major at a finer grain: a work
-// item is (Gaussian, up to 16 rows of its box), one DPP row of 16 lanes per
-// item, one lane per row. A row is a run of cells along x, whose query
-// points are contiguous in the cell ordering of the plan (or a run of
-// voxels along x for grids). Each lane accumulates the Gaussian's partial
-// sums over its row in registers, the 16 lanes are reduced with DPP, and one
-// lane issues a single set of atomic adds per item.
+// per intersection; its unstructured backward gives each Gaussian a warp
+// and ends with a warp-wide reduction. Here every Gaussian gets one
+// wavefront and no atomics: the wave walks the query points in the
+// Gaussian's box, accumulates the partial sums in registers and reduces
+// them across the wave with DPP at the end.
+//
+// The points of a box come as rows: a run of cells along x at fixed (y, z)
+// is contiguous in the plan's cell ordering (for grids, a run of voxels is
+// contiguous in the x-fastest layout). The wave splits into groups of W
+// lanes, W chosen from the mean row length of the Gaussian; each group walks
+// one row with W consecutive lanes, so every load instruction reads a few
+// whole cache lines. Gaussians are visited in the spatial order of the
+// index (the cell key of their box corner), so the waves resident at one
+// time work on one region and find its points in L2.
 //
 // Per pair the partials are kept as 11 moments in the Gaussian's whitened
 // frame u = M (p - mu), M = S^-1 R^T, with c = dL/dQ = -1/2 a dL/da:
@@ -20,7 +27,6 @@
 // For a defined query with outputs (Phi, I) and cotangents (gPhi, gI):
 //   dL/da_i = alpha v_i + beta with alpha = gPhi / I, beta = gI - alpha Phi,
 // which a staging kernel computes once per query.
-#include "expand.h"
 #include "internal.h"
 
 #pragma clang fp contract(off)
@@ -40,9 +46,9 @@ __device__ __forceinline__ void voxel_pos(uint32_t id, const QueryParams &q, con
     pz = g.lo[2] + ((float)z + 0.5f) * q.vsz[2];
 }
 
-__device__ __forceinline__ void alpha_beta(float phi, float inf, float gp, float gi, bool defined, float &al,
-                                           float &be) {
-    if (defined && inf > 0.0f) {
+__device__ __forceinline__ void alpha_beta(float phi, float inf, float gp, float gi, float &al, float &be) {
+    // the forward writes I > tau > 0 at defined points and exactly 0 elsewhere
+    if (inf > 0.0f) {
         al = gp / inf;
         be = gi - al * phi;
     } else {
@@ -65,7 +71,7 @@ __global__ __launch_bounds__(kBlock) void k_stage_points(QueryParams q, GridPara
     const uint32_t key = sorted_keys[k];
     const uint32_t pid = order[k];
     float px = 0.0f, py = 0.0f, pz = 0.0f, al = 0.0f, be = 0.0f;
-    if (key < (uint32_t)g.ncells) {
+    if (key < (uint32_t)g.ncells && (int64_t)pid < q.n) {
         if (q.kind == 1) {
             voxel_pos(q.voxel_ids[pid], q, g, px, py, pz);
         } else {
@@ -73,7 +79,7 @@ __global__ __launch_bounds__(kBlock) void k_stage_points(QueryParams q, GridPara
             py = q.points[3 * (uint64_t)pid + 1];
             pz = q.points[3 * (uint64_t)pid + 2];
         }
-        alpha_beta(value[pid], influence[pid], gval[pid], ginf[pid], true, al, be);
+        alpha_beta(value[pid], influence[pid], gval[pid], ginf[pid], al, be);
     }
     pts[k] = make_float4(px, py, pz, al);
     beta[k] = be;
@@ -87,42 +93,9 @@ __global__ __launch_bounds__(kBlock) void k_stage_grid(int64_t n, const float *_
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
     float al, be;
-    alpha_beta(value[i], influence[i], gval[i], ginf[i], true, al, be);
+    alpha_beta(value[i], influence[i], gval[i], ginf[i], al, be);
     alpha[i] = al;
     beta[i] = be;
-}
-
-// Rows of a Gaussian's box: cell rows (cy, cz) for ordered queries, voxel
-// rows (vy, vz) for grids.
-__device__ __forceinline__ uint32_t box_rows(const CellBox &b, bool grid, uint32_t ry, uint32_t rz) {
-    if (b.hi.x < b.lo.x) return 0u;
-    const uint32_t ny = (uint32_t)(b.hi.y - b.lo.y + 1), nz = (uint32_t)(b.hi.z - b.lo.z + 1);
-    return grid ? ny * ry * nz * rz : ny * nz;
-}
-
-__global__ __launch_bounds__(kBlock) void k_item_counts(const CellBox *__restrict__ box, int64_t n, int grid,
-                                                        uint32_t ry, uint32_t rz, uint32_t *__restrict__ item_off) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i == n) item_off[n] = 0;
-    if (i >= n) return;
-    const uint32_t rows = box_rows(box[i], grid != 0, ry, rz);
-    item_off[i] = (rows + kRowGroup - 1) / kRowGroup;
-}
-
-__global__ __launch_bounds__(kBlock) void k_expand_items(const uint32_t *__restrict__ item_off, int64_t n,
-                                                         uint32_t *__restrict__ items, int64_t max_items) {
-    __shared__ ExpandShared sh;
-    const uint64_t total = item_off[n] < (uint64_t)max_items ? item_off[n] : (uint64_t)max_items;
-    const uint64_t tile_begin = (uint64_t)blockIdx.x * kExpandTile;
-    if (tile_begin >= total) return;
-    const uint64_t rem = total - tile_begin;
-    const uint32_t tile_cnt = rem < (uint64_t)kExpandTile ? (uint32_t)rem : (uint32_t)kExpandTile;
-    const int64_t gfirst = expand_tile(item_off, n, tile_begin, tile_cnt, sh);
-#pragma unroll 2
-    for (int i = 0; i < kExpandItems; ++i) {
-        const uint32_t slot = (uint32_t)i * kBlock + threadIdx.x;
-        if (slot < tile_cnt) items[tile_begin + slot] = (uint32_t)(gfirst + sh.head[slot]);
-    }
 }
 
 struct Acc {
@@ -158,79 +131,108 @@ __device__ __forceinline__ void pair_grad(const Record &r, float px, float py, f
     }
 }
 
-// One wave = 4 items of 16 lanes; blocks of 4 waves = 16 items.
-__global__ __launch_bounds__(kBlock) void k_backward_rows(QueryParams q, GridParams g, const Record *__restrict__ rec,
-                                                          const CellBox *__restrict__ box,
-                                                          const uint32_t *__restrict__ item_off, int64_t n_gauss,
-                                                          const uint32_t *__restrict__ items,
-                                                          const uint32_t *__restrict__ point_off,
-                                                          const float4 *__restrict__ pts,
-                                                          const float *__restrict__ alpha,
-                                                          const float *__restrict__ beta, float T,
-                                                          float *__restrict__ moments, int64_t max_items) {
-    const uint32_t total = item_off[n_gauss] < (uint64_t)max_items ? item_off[n_gauss] : (uint32_t)max_items;
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
+    return __builtin_amdgcn_readlane(wave_incl_sum(x), 63);
+}
+
+// lanes per row group for a mean row length
+__device__ __forceinline__ uint32_t group_width(uint32_t mean_len) {
+    return mean_len <= 4 ? 4u : mean_len <= 8 ? 8u : mean_len <= 20 ? 16u : mean_len <= 40 ? 32u : 64u;
+}
+
+template <bool GRID>
+__global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridParams g, const Record *__restrict__ rec,
+                                                           const CellBox *__restrict__ box,
+                                                           const uint32_t *__restrict__ gorder, int64_t n_gauss,
+                                                           const uint32_t *__restrict__ point_off,
+                                                           const float4 *__restrict__ pts,
+                                                           const float *__restrict__ alpha,
+                                                           const float *__restrict__ beta, float T,
+                                                           float *__restrict__ moments) {
     const uint32_t lane = threadIdx.x % kWave;
-    const uint32_t group = lane / kRowGroup, gl = lane % kRowGroup;
-    const uint64_t item = ((uint64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave) * (kWave / kRowGroup) + group;
-    const bool active = item < total;
+    const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave;
+    if (w >= (uint64_t)n_gauss) return;
+    const uint32_t gid = __builtin_amdgcn_readfirstlane(((ConstU32 *)gorder)[w]);
+    const CellBox b = load_box_uniform(box, gid);
+    const Record r = load_record_uniform(rec, gid);
     Acc acc;
 #pragma unroll
     for (int k = 0; k < 3; ++k) acc.m1[k] = 0.0f;
 #pragma unroll
     for (int k = 0; k < 6; ++k) acc.m2[k] = 0.0f;
     acc.dv = acc.dw = 0.0f;
-    uint32_t gid = 0;
-    if (active) {
-        gid = items[item];
-        const uint32_t chunk = (uint32_t)item - item_off[gid];
-        const uint32_t row = chunk * kRowGroup + gl;
-        const CellBox b = box[gid];
-        const Record r = rec[gid];
-        const bool grid = q.kind == 0;
-        if (grid) {
-            const uint32_t rx = (uint32_t)(q.dims[0] / g.cells[0]);
-            const uint32_t ry = (uint32_t)(q.dims[1] / g.cells[1]);
-            const uint32_t rz = (uint32_t)(q.dims[2] / g.cells[2]);
-            const uint32_t nvy = (uint32_t)(b.hi.y - b.lo.y + 1) * ry;
-            const uint32_t nvz = (uint32_t)(b.hi.z - b.lo.z + 1) * rz;
-            if (row < nvy * nvz) {
-                const uint32_t vy = (uint32_t)b.lo.y * ry + row % nvy;
-                const uint32_t vz = (uint32_t)b.lo.z * rz + row / nvy;
-                const uint32_t vx0 = (uint32_t)b.lo.x * rx, vx1 = (uint32_t)(b.hi.x + 1) * rx;
-                const float py = g.lo[1] + ((float)vy + 0.5f) * q.vsz[1];
-                const float pz = g.lo[2] + ((float)vz + 0.5f) * q.vsz[2];
-                const uint64_t rowbase = (uint64_t)q.dims[0] * ((uint64_t)vy + (uint64_t)q.dims[1] * vz);
-                for (uint32_t vx = vx0; vx < vx1; ++vx) {
-                    const float px = g.lo[0] + ((float)vx + 0.5f) * q.vsz[0];
-                    const uint64_t idx = rowbase + vx;
-                    pair_grad(r, px, py, pz, alpha[idx], beta[idx], T, acc);
+    if (b.hi.x >= b.lo.x) {
+        const uint32_t nx = (uint32_t)(b.hi.x - b.lo.x + 1), ny = (uint32_t)(b.hi.y - b.lo.y + 1),
+                       nz = (uint32_t)(b.hi.z - b.lo.z + 1);
+        uint32_t rx = 1, ry = 1, rz = 1;
+        if (GRID) {
+            rx = (uint32_t)(q.dims[0] / g.cells[0]);
+            ry = (uint32_t)(q.dims[1] / g.cells[1]);
+            rz = (uint32_t)(q.dims[2] / g.cells[2]);
+        }
+        const uint32_t nry = ny * ry, R = nry * nz * rz;
+        const uint32_t vx0 = (uint32_t)b.lo.x * rx;
+        for (uint32_t rb = 0; rb < R; rb += kWave) {
+            // lane l describes row rb + l: its first element and its length
+            const uint32_t row = rb + lane;
+            uint32_t start = 0, len = 0, ry_ = 0, rz_ = 0;
+            if (row < R) {
+                const uint32_t yy = row % nry, zz = row / nry;
+                if (GRID) {
+                    const uint32_t vy = (uint32_t)b.lo.y * ry + yy, vz = (uint32_t)b.lo.z * rz + zz;
+                    start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + vx0;
+                    len = nx * rx;
+                    ry_ = vy;
+                    rz_ = vz;
+                } else {
+                    const uint32_t cy = (uint32_t)b.lo.y + yy, cz = (uint32_t)b.lo.z + zz;
+                    const uint32_t kbase = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz);
+                    start = point_off[kbase + (uint32_t)b.lo.x];
+                    len = point_off[kbase + (uint32_t)b.hi.x + 1] - start;
                 }
             }
-        } else {
-            const uint32_t ny = (uint32_t)(b.hi.y - b.lo.y + 1), nz = (uint32_t)(b.hi.z - b.lo.z + 1);
-            if (row < ny * nz) {
-                const uint32_t cy = (uint32_t)b.lo.y + row % ny;
-                const uint32_t cz = (uint32_t)b.lo.z + row / ny;
-                const uint64_t kbase = (uint64_t)g.cells[0] * ((uint64_t)cy + (uint64_t)g.cells[1] * cz);
-                const uint32_t a0 = point_off[kbase + (uint32_t)b.lo.x];
-                const uint32_t a1 = point_off[kbase + (uint32_t)b.hi.x + 1];
-                for (uint32_t k = a0; k < a1; ++k) {
-                    const float4 p = pts[k];
-                    pair_grad(r, p.x, p.y, p.z, p.w, beta[k], T, acc);
+            const uint32_t nrows = (R - rb) < (uint32_t)kWave ? (R - rb) : (uint32_t)kWave;
+            const uint32_t W = group_width((wave_sum_u32(len) + nrows - 1) / nrows);
+            const uint32_t G = kWave / W;
+            const uint32_t grp = lane / W, t = lane % W;
+            for (uint32_t rr = 0; rr < nrows; rr += G) {
+                // every lane takes part in the shuffles (a lane reading from an
+                // inactive lane would get 0); rows past the end have length 0
+                const uint32_t my = rr + grp;
+                const uint32_t s_start = __shfl(start, (int)my, 64);
+                const uint32_t s_len = __shfl(len, (int)my, 64);
+                if (GRID) {
+                    const uint32_t s_y = __shfl(ry_, (int)my, 64), s_z = __shfl(rz_, (int)my, 64);
+                    const float py = g.lo[1] + ((float)s_y + 0.5f) * q.vsz[1];
+                    const float pz = g.lo[2] + ((float)s_z + 0.5f) * q.vsz[2];
+                    for (uint32_t c = t; c < s_len; c += W) {
+                        const float px = g.lo[0] + ((float)(vx0 + c) + 0.5f) * q.vsz[0];
+                        pair_grad(r, px, py, pz, alpha[s_start + c], beta[s_start + c], T, acc);
+                    }
+                } else {
+                    for (uint32_t c = t; c < s_len; c += W) {
+                        const float4 p = pts[s_start + c];
+                        pair_grad(r, p.x, p.y, p.z, p.w, beta[s_start + c], T, acc);
+                    }
                 }
             }
         }
     }
-    // reduce each group's 16 lanes (every lane of the wave takes part)
     float v[11] = {acc.m1[0], acc.m1[1], acc.m1[2], acc.m2[0], acc.m2[1], acc.m2[2],
                    acc.m2[3], acc.m2[4], acc.m2[5], acc.dv,    acc.dw};
 #pragma unroll
-    for (int k = 0; k < 11; ++k) v[k] = row16_sum(v[k]);
-    if (active && gl == 0) {
-        float *m = moments + (size_t)gid * 12;
-#pragma unroll
-        for (int k = 0; k < 11; ++k)
-            if (v[k] != 0.0f) atomicAdd(m + k, v[k]);
+    for (int k = 0; k < 11; ++k) {
+        const float rsum = row16_sum(v[k]);
+        v[k] = (__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rsum), 0)) +
+                __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rsum), 16))) +
+               (__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rsum), 32)) +
+                __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rsum), 48)));
+    }
+    if (lane == 0) {
+        float4 *m = (float4 *)(moments + (size_t)gid * 12);
+        m[0] = make_float4(v[0], v[1], v[2], v[3]);
+        m[1] = make_float4(v[4], v[5], v[6], v[7]);
+        m[2] = make_float4(v[8], v[9], v[10], 0.0f);
     }
 }
 
@@ -307,7 +309,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
 }  // namespace
 
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
-                           int64_t n_gauss, const uint32_t *sorted_keys, const uint32_t *order,
+                           const uint32_t *gorder, int64_t n_gauss, const uint32_t *sorted_keys, const uint32_t *order,
                            const uint32_t *point_off, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
@@ -317,11 +319,7 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
     if (n_gauss <= 0) return hipSuccess;
     hipError_t e;
     const bool grid = q.kind == 0;
-    const uint32_t gblocks = (uint32_t)((n_gauss + 1 + kBlock - 1) / kBlock);
-    prof_begin("bwd_zero", s);
-    e = fill_f32(b.moments, 0.0f, n_gauss * 12, s);
-    prof_end("bwd_zero", s);
-    if (e != hipSuccess) return e;
+    const uint32_t gblocks = (uint32_t)((n_gauss + kBlock - 1) / kBlock);
     if (q.n > 0) {
         const uint32_t qblocks = (uint32_t)((q.n + kBlock - 1) / kBlock);
         prof_begin("bwd_stage", s);
@@ -333,29 +331,21 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
                                influence, grad_value, grad_influence, b.pts, b.beta);
         prof_end("bwd_stage", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        const uint32_t ry = grid ? (uint32_t)(q.dims[1] / g.cells[1]) : 1u;
-        const uint32_t rz = grid ? (uint32_t)(q.dims[2] / g.cells[2]) : 1u;
-        prof_begin("bwd_items", s);
-        hipLaunchKernelGGL(k_item_counts, dim3(gblocks), dim3(kBlock), 0, s, box, n_gauss, grid ? 1 : 0, ry, rz,
-                           b.item_off);
-        prof_end("bwd_items", s);
+        const uint32_t wblocks = (uint32_t)((n_gauss + kWavesPerBlock - 1) / kWavesPerBlock);
+        prof_begin("bwd_gauss", s);
+        if (grid)
+            hipLaunchKernelGGL(k_backward_gauss<true>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, gorder,
+                               n_gauss, point_off, b.pts, b.alpha, b.beta, T, b.moments);
+        else
+            hipLaunchKernelGGL(k_backward_gauss<false>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, gorder,
+                               n_gauss, point_off, b.pts, b.alpha, b.beta, T, b.moments);
+        prof_end("bwd_gauss", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if ((e = exclusive_scan_u32(b.item_off, b.item_off, n_gauss + 1, b.scan_work, s)) != hipSuccess) return e;
-        if (b.max_items > 0) {
-            const uint32_t eblocks = (uint32_t)((b.max_items + kExpandTile - 1) / kExpandTile);
-            prof_begin("bwd_expand", s);
-            hipLaunchKernelGGL(k_expand_items, dim3(eblocks), dim3(kBlock), 0, s, b.item_off, n_gauss, b.items,
-                               b.max_items);
-            prof_end("bwd_expand", s);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-            const int64_t items_per_block = (int64_t)kWavesPerBlock * (kWave / kRowGroup);
-            const uint32_t rblocks = (uint32_t)((b.max_items + items_per_block - 1) / items_per_block);
-            prof_begin("bwd_rows", s);
-            hipLaunchKernelGGL(k_backward_rows, dim3(rblocks), dim3(kBlock), 0, s, q, g, rec, box, b.item_off,
-                               n_gauss, b.items, point_off, b.pts, b.alpha, b.beta, T, b.moments, b.max_items);
-            prof_end("bwd_rows", s);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-        }
+    } else {
+        prof_begin("bwd_zero", s);
+        e = fill_f32(b.moments, 0.0f, n_gauss * 12, s);
+        prof_end("bwd_zero", s);
+        if (e != hipSuccess) return e;
     }
     prof_begin("bwd_finalize", s);
     hipLaunchKernelGGL(k_finalize, dim3(gblocks), dim3(kBlock), 0, s, b.moments, n_gauss, scale, rot, d_mean, d_scale,

@@ -141,7 +141,31 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
     }
 }
 
+// Sort key of each Gaussian for the spatial visiting order: the cell key of
+// its box's low corner, ncells for an empty box.
+__global__ __launch_bounds__(kBlock) void k_gauss_keys(const CellBox *__restrict__ box, int64_t n, GridParams g,
+                                                       uint32_t *__restrict__ keys, uint32_t *__restrict__ ids) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const CellBox b = box[i];
+    uint32_t key = (uint32_t)g.ncells;
+    if (b.hi.x >= b.lo.x)
+        key = (uint32_t)((int64_t)b.lo.x + (int64_t)g.cells[0] * ((int64_t)b.lo.y + (int64_t)g.cells[1] * b.lo.z));
+    keys[i] = key;
+    ids[i] = (uint32_t)i;
+}
+
 }  // namespace
+
+hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g, uint32_t *keys, uint32_t *ids,
+                             hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    prof_begin("gauss_keys", s);
+    hipLaunchKernelGGL(k_gauss_keys, dim3((uint32_t)((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, box, n, g, keys,
+                       ids);
+    prof_end("gauss_keys", s);
+    return hipGetLastError();
+}
 
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,

@@ -30,6 +30,34 @@ struct alignas(16) CellBox {
     int4 lo, hi;
 };
 
+// Read-only views in the constant address space: loads through them with a
+// wave-uniform address become scalar loads into SGPRs.
+typedef float f4v __attribute__((ext_vector_type(4)));
+typedef int i4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(4))) const f4v ConstF4;
+typedef __attribute__((address_space(4))) const i4v ConstI4;
+typedef __attribute__((address_space(4))) const uint32_t ConstU32;
+
+__device__ __forceinline__ Record load_record_uniform(const Record *rec, uint32_t g) {
+    ConstF4 *p = (ConstF4 *)rec + 4 * (size_t)g;
+    const f4v a = p[0], b = p[1], c = p[2], d = p[3];
+    Record r;
+    r.r0 = make_float4(a.x, a.y, a.z, a.w);
+    r.r1 = make_float4(b.x, b.y, b.z, b.w);
+    r.r2 = make_float4(c.x, c.y, c.z, c.w);
+    r.r3 = make_float4(d.x, d.y, d.z, d.w);
+    return r;
+}
+
+__device__ __forceinline__ CellBox load_box_uniform(const CellBox *box, uint32_t g) {
+    ConstI4 *p = (ConstI4 *)box + 2 * (size_t)g;
+    const i4v a = p[0], b = p[1];
+    CellBox c;
+    c.lo = make_int4(a.x, a.y, a.z, a.w);
+    c.hi = make_int4(b.x, b.y, b.z, b.w);
+    return c;
+}
+
 // --- float helpers ---------------------------------------------------------
 
 __device__ __forceinline__ float fmaf_(float a, float b, float c) { return __builtin_fmaf(a, b, c); }
@@ -157,20 +185,20 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
                                 const uint32_t *cell_off, const uint32_t *sorted_keys, const uint32_t *order,
                                 float T, float tau, float *out_v, float *out_i, hipStream_t s);
 
+// Gaussians in spatial order: sorted by the cell key of their box's low
+// corner (empty boxes last), so neighbouring work shares cached queries.
+hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g, uint32_t *keys, uint32_t *ids,
+                             hipStream_t s);
+
 // Backward (backward.hip).
-constexpr int kRowGroup = 16;  // lanes per backward work item (one DPP row)
 struct BackwardBuffers {
     float *moments;        // [n_gauss][12]
-    uint32_t *item_off;    // [n_gauss + 1]
-    uint32_t *items;       // [max_items]
-    int64_t max_items;
     float4 *pts;           // POINTS/VOXELS: [n] (x, y, z, alpha) in plan order
     float *beta;           // POINTS/VOXELS: [n]; GRID: [n] beta in voxel order
     float *alpha;          // GRID: [n] alpha in voxel order
-    void *scan_work;
 };
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
-                           int64_t n_gauss, const uint32_t *sorted_keys, const uint32_t *order,
+                           const uint32_t *gorder, int64_t n_gauss, const uint32_t *sorted_keys, const uint32_t *order,
                            const uint32_t *point_off, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,

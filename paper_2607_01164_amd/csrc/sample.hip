@@ -23,23 +23,6 @@ namespace {
 // -1/2 log2(e): G = exp(-Q/2) = 2^(Q * kNegHalfLog2e)
 constexpr float kNegHalfLog2e = -0.72134752044448170368f;
 
-// Read-only views in the constant address space: a load from them with a
-// wave-uniform address becomes a scalar load.
-typedef float f4v __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(4))) const f4v ConstF4;
-typedef __attribute__((address_space(4))) const uint32_t ConstU32;
-
-__device__ __forceinline__ Record load_record_uniform(const Record *rec, uint32_t g) {
-    ConstF4 *p = (ConstF4 *)rec + 4 * (size_t)g;
-    const f4v a = p[0], b = p[1], c = p[2], d = p[3];
-    Record r;
-    r.r0 = make_float4(a.x, a.y, a.z, a.w);
-    r.r1 = make_float4(b.x, b.y, b.z, b.w);
-    r.r2 = make_float4(c.x, c.y, c.z, c.w);
-    r.r3 = make_float4(d.x, d.y, d.z, d.w);
-    return r;
-}
-
 __device__ __forceinline__ void accumulate(const Record &r, float px, float py, float pz, float T, float &I,
                                            float &V) {
     const float dx = px - r.r0.x, dy = py - r.r0.y, dz = pz - r.r0.z;
