@@ -145,6 +145,7 @@ struct Plan {
     uint32_t *order_alt; // [n]
     uint32_t *point_off; // [ncells + 2]
     void *radix_work;
+    PointItems items;
     size_t bytes;
 };
 
@@ -158,6 +159,10 @@ Plan plan_layout(void *base, int64_t n, int64_t ncells) {
     p.order_alt = c.take<uint32_t>(m);
     p.point_off = c.take<uint32_t>((size_t)ncells + 2);
     p.radix_work = c.take<char>(radix_work_bytes(n > 0 ? n : 1, bits_for(ncells + 1)));
+    p.items.item_off = c.take<uint32_t>((size_t)ncells + 2);
+    p.items.max_items = ncells + 1 + (n > 0 ? n : 0) / 64 + 1;
+    p.items.items = c.take<uint32_t>((size_t)p.items.max_items);
+    p.items.scan_work = c.take<char>(scan_work_bytes(ncells + 2, 4));
     p.bytes = c.off;
     return p;
 }
@@ -510,8 +515,8 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
     GS_TRY(launch_query_keys(qp, gp, ek, ev, stream), "gs_sample: query keys");
     GS_TRY(radix_sort_pairs(ek, ev, ak, av, nq, bits, p.radix_work, stream), "gs_sample: query sort");
     GS_TRY(key_offsets(p.keys, nq, p.point_off, gp.ncells + 1, stream), "gs_sample: query ranges");
-    GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.keys, p.order, T, index->tau,
-                                out_value, out_influence, stream),
+    GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
+                                index->tau, out_value, out_influence, stream),
            "gs_sample: point sampler");
     return GS_OK;
 }

@@ -181,9 +181,17 @@ hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t
 hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                               const uint32_t *cell_off, float T, float tau, float *out_v, float *out_i,
                               hipStream_t s);
+// Work items of the ordered-query sampler (kept in the plan).
+struct PointItems {
+    uint32_t *item_off;  // [ncells + 2]
+    uint32_t *items;     // [max_items]
+    int64_t max_items;   // ncells + 1 + n / 64 + 1
+    void *scan_work;
+};
 hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
-                                const uint32_t *cell_off, const uint32_t *sorted_keys, const uint32_t *order,
-                                float T, float tau, float *out_v, float *out_i, hipStream_t s);
+                                const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
+                                const PointItems &it, float T, float tau, float *out_v, float *out_i,
+                                hipStream_t s);
 
 // Gaussians in spatial order: sorted by the cell key of their box's low
 // corner (empty boxes last), so neighbouring work shares cached queries.

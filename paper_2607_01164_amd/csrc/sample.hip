@@ -8,10 +8,10 @@
 // shared-memory batches.
 //
 // Voxel-list and point queries (Sec. 5.1.2): the queries are first ordered
-// by cell (query_keys + radix sort, kept in the plan); a wavefront takes 64
-// consecutive ordered queries. When they share one cell the wave takes the
-// same scalar path; otherwise every lane walks its own cell's list with
-// vector loads, which neighbouring lanes of one cell share.
+// by cell (query_keys + radix sort, kept in the plan) and the work is split
+// by cell: dense cells run like grid cells, sparse cells put the cell's
+// candidate Gaussians in the lanes instead (see k_sample_cells).
+#include "expand.h"
 #include "internal.h"
 
 #pragma clang fp contract(off)
@@ -55,16 +55,6 @@ __device__ __forceinline__ void walk_uniform(const Record *rec, const uint32_t *
         const uint32_t g0 = __builtin_amdgcn_readfirstlane(cg[j]);
         const Record a = load_record_uniform(rec, g0);
         accumulate(a, px, py, pz, T, I, V);
-    }
-}
-
-// Walk a per-lane list with vector loads.
-__device__ __forceinline__ void walk_lane(const Record *__restrict__ rec, const uint32_t *__restrict__ gids, uint32_t j0,
-                                          uint32_t j1, float px, float py, float pz, float T, float &I, float &V) {
-    for (uint32_t j = j0; j < j1; ++j) {
-        const uint32_t gg = gids[j];
-        const Record r = rec[gg];
-        accumulate(r, px, py, pz, T, I, V);
     }
 }
 
@@ -155,38 +145,151 @@ __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams
     ids[i] = (uint32_t)i;
 }
 
-__global__ __launch_bounds__(kBlock) void k_sample_points(QueryParams q, GridParams g, const Record *__restrict__ rec,
-                                                          const uint32_t *__restrict__ gids,
-                                                          const uint32_t *__restrict__ cell_off,
-                                                          const uint32_t *__restrict__ sorted_keys,
-                                                          const uint32_t *__restrict__ order, float T, float tau,
-                                                          float *__restrict__ out_v, float *__restrict__ out_i) {
-    const int64_t k = (int64_t)xcd_block(blockIdx.x, gridDim.x) * kBlock + threadIdx.x;
-    const bool active = k < q.n;
-    const uint32_t ncells = (uint32_t)g.ncells;
-    const uint32_t pid = active ? order[k] : 0u;
-    const uint32_t key = (active && (int64_t)pid < q.n) ? sorted_keys[k] : ncells;
-    float px = 0.0f, py = 0.0f, pz = 0.0f;
-    bool valid = false;
-    if (active && key < ncells) query_position(q, g, pid, px, py, pz, valid);
-    const bool work = active && key < ncells && valid;
-    float I = 0.0f, V = 0.0f;
-    // all working lanes in one cell: walk the shared list through the scalar path
-    const uint64_t wmask = __ballot(work);
-    const uint32_t kfirst = wmask ? __shfl(key, (int)__builtin_ctzll(wmask), 64) : 0u;
-    const bool uniform = wmask != 0 && __ballot(work && key != kfirst) == 0;
-    if (uniform) {
-        const uint32_t kk = __builtin_amdgcn_readfirstlane(kfirst);
-        const uint32_t j0 = __builtin_amdgcn_readfirstlane(cell_off[kk]);
-        const uint32_t j1 = __builtin_amdgcn_readfirstlane(cell_off[kk + 1]);
-        walk_uniform(rec, gids, j0, j1, px, py, pz, T, I, V);
-    } else if (work) {
-        walk_lane(rec, gids, cell_off[key], cell_off[key + 1], px, py, pz, T, I, V);
+// Work items of the ordered-query sampler: one per cell holding fewer than
+// kDenseMin queries, one per 64 queries of a denser cell. The bucket of
+// queries outside the domain (key ncells) is an item with an empty list.
+constexpr uint32_t kDenseMin = 32;
+constexpr uint32_t kChunkB = 8;  // queries evaluated together by a sparse-cell item
+
+__global__ __launch_bounds__(kBlock) void k_cell_items(const uint32_t *__restrict__ point_off, int64_t nbuckets,
+                                                       uint32_t *__restrict__ item_off) {
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c == nbuckets) item_off[nbuckets] = 0;
+    if (c >= nbuckets) return;
+    const uint32_t n = point_off[c + 1] - point_off[c];
+    item_off[c] = n == 0 ? 0u : (n < kDenseMin ? 1u : (n + kWave - 1) / kWave);
+}
+
+__global__ __launch_bounds__(kBlock) void k_expand_cell_items(const uint32_t *__restrict__ item_off, int64_t nbuckets,
+                                                              uint32_t *__restrict__ items, int64_t max_items) {
+    __shared__ ExpandShared sh;
+    const uint64_t tot = item_off[nbuckets];
+    const uint64_t total = tot < (uint64_t)max_items ? tot : (uint64_t)max_items;
+    const uint64_t tile_begin = (uint64_t)blockIdx.x * kExpandTile;
+    if (tile_begin >= total) return;
+    const uint64_t rem = total - tile_begin;
+    const uint32_t tile_cnt = rem < (uint64_t)kExpandTile ? (uint32_t)rem : (uint32_t)kExpandTile;
+    const int64_t first = expand_tile(item_off, nbuckets, tile_begin, tile_cnt, sh);
+#pragma unroll 2
+    for (int i = 0; i < kExpandItems; ++i) {
+        const uint32_t slot = (uint32_t)i * kBlock + threadIdx.x;
+        if (slot < tile_cnt) items[tile_begin + slot] = (uint32_t)(first + sh.head[slot]);
     }
-    if (active && (int64_t)pid < q.n) {
-        const bool def = work && I > tau;
-        out_v[pid] = def ? V / I : 0.0f;
-        out_i[pid] = def ? I : 0.0f;
+}
+
+__device__ __forceinline__ float eval_a(const Record &r, float px, float py, float pz, float T) {
+    const float dx = px - r.r0.x, dy = py - r.r0.y, dz = pz - r.r0.z;
+    const float u0 = fmaf_(r.r1.x, dx, fmaf_(r.r1.y, dy, r.r1.z * dz));
+    const float u1 = fmaf_(r.r2.x, dx, fmaf_(r.r2.y, dy, r.r2.z * dz));
+    const float u2 = fmaf_(r.r3.x, dx, fmaf_(r.r3.y, dy, r.r3.z * dz));
+    const float Q = fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
+    return Q <= T ? r.r0.w * exp2_hw(Q * kNegHalfLog2e) : 0.0f;
+}
+
+__device__ __forceinline__ float readlane_f(float x, uint32_t l) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), (int)l));
+}
+
+// sum over the 64 lanes, returned to every lane
+__device__ __forceinline__ float wave_total(float x) {
+    const float r = row16_sum(x);
+    return (readlane_f(r, 0) + readlane_f(r, 16)) + (readlane_f(r, 32) + readlane_f(r, 48));
+}
+
+__device__ __forceinline__ void write_out(float I, float V, float tau, bool work, uint32_t pid, float *out_v,
+                                          float *out_i) {
+    const bool def = work && I > tau;
+    out_v[pid] = def ? V / I : 0.0f;
+    out_i[pid] = def ? I : 0.0f;
+}
+
+// One wavefront per item. Dense cells: lanes are queries of the cell and
+// walk its list together (records through the scalar path). Sparse cells:
+// lanes are the cell's candidate Gaussians (64 at a time, records loaded
+// once per cell) and the cell's queries are visited in turn, their
+// positions broadcast from SGPRs; per-lane partial sums are reduced across
+// the wave at the end, in a fixed order.
+__global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
+                                                         const uint32_t *__restrict__ gids,
+                                                         const uint32_t *__restrict__ cell_off,
+                                                         const uint32_t *__restrict__ point_off,
+                                                         const uint32_t *__restrict__ order,
+                                                         const uint32_t *__restrict__ item_off,
+                                                         const uint32_t *__restrict__ items, int64_t max_items,
+                                                         float T, float tau, float *__restrict__ out_v,
+                                                         float *__restrict__ out_i) {
+    const uint32_t lane = threadIdx.x % kWave;
+    const uint32_t ncells = (uint32_t)g.ncells;
+    const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave;
+    const uint32_t tot = ((ConstU32 *)item_off)[ncells + 1];
+    const uint64_t total = tot < (uint64_t)max_items ? tot : (uint64_t)max_items;
+    if (w >= total) return;
+    const uint32_t c = __builtin_amdgcn_readfirstlane(((ConstU32 *)items)[w]);
+    const uint32_t chunk = (uint32_t)w - ((ConstU32 *)item_off)[c];
+    const uint32_t pa = ((ConstU32 *)point_off)[c], pb = ((ConstU32 *)point_off)[c + 1];
+    const uint32_t n = pb - pa;
+    uint32_t ja = 0, jb = 0;
+    if (c < ncells) {
+        ja = ((ConstU32 *)cell_off)[c];
+        jb = ((ConstU32 *)cell_off)[c + 1];
+    }
+    if (n >= kDenseMin) {
+        const uint32_t k = pa + chunk * kWave + lane;
+        const bool active = k < pb;
+        uint32_t pid = 0;
+        float px = 0.0f, py = 0.0f, pz = 0.0f;
+        bool valid = false;
+        if (active) {
+            pid = order[k];
+            if ((int64_t)pid < q.n) query_position(q, g, pid, px, py, pz, valid);
+        }
+        float I = 0.0f, V = 0.0f;
+        walk_uniform(rec, gids, ja, jb, px, py, pz, T, I, V);
+        if (active && (int64_t)pid < q.n) write_out(I, V, tau, valid && c < ncells, pid, out_v, out_i);
+        return;
+    }
+    for (uint32_t p0 = pa; p0 < pb; p0 += kChunkB) {
+        const uint32_t m = (pb - p0) < kChunkB ? (pb - p0) : kChunkB;
+        uint32_t pid = 0;
+        float mx = 0.0f, my = 0.0f, mz = 0.0f;
+        bool valid = false;
+        if (lane < m) {
+            pid = order[p0 + lane];
+            if ((int64_t)pid < q.n) query_position(q, g, pid, mx, my, mz, valid);
+        }
+        float Ip[kChunkB], Vp[kChunkB];
+#pragma unroll
+        for (uint32_t t = 0; t < kChunkB; ++t) Ip[t] = Vp[t] = 0.0f;
+        for (uint32_t j0 = ja; j0 < jb; j0 += kWave) {
+            const uint32_t j = j0 + lane;
+            Record r;
+            if (j < jb) {
+                r = rec[gids[j]];
+            } else {
+                r.r0 = r.r1 = r.r2 = r.r3 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                r.r0.w = 0.0f;
+            }
+#pragma unroll
+            for (uint32_t t = 0; t < kChunkB; ++t) {
+                if (t < m) {
+                    const float a = eval_a(r, readlane_f(mx, t), readlane_f(my, t), readlane_f(mz, t), T);
+                    Ip[t] += a;
+                    Vp[t] = fmaf_(a, r.r1.w, Vp[t]);
+                }
+            }
+        }
+        float Io = 0.0f, Vo = 0.0f;
+#pragma unroll
+        for (uint32_t t = 0; t < kChunkB; ++t) {
+            if (t < m) {
+                const float It = wave_total(Ip[t]), Vt = wave_total(Vp[t]);
+                if (lane == t) {
+                    Io = It;
+                    Vo = Vt;
+                }
+            }
+        }
+        if (lane < m && (int64_t)pid < q.n) write_out(Io, Vo, tau, valid && c < ncells, pid, out_v, out_i);
     }
 }
 
@@ -218,12 +321,27 @@ hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const R
 }
 
 hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
-                                const uint32_t *cell_off, const uint32_t *sorted_keys, const uint32_t *order,
-                                float T, float tau, float *out_v, float *out_i, hipStream_t s) {
+                                const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
+                                const PointItems &it, float T, float tau, float *out_v, float *out_i,
+                                hipStream_t s) {
     if (q.n <= 0) return hipSuccess;
+    const int64_t nbuckets = g.ncells + 1;  // cells and the outside bucket
+    prof_begin("cell_items", s);
+    hipLaunchKernelGGL(k_cell_items, dim3((uint32_t)((nbuckets + 1 + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
+                       point_off, nbuckets, it.item_off);
+    prof_end("cell_items", s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if ((e = exclusive_scan_u32(it.item_off, it.item_off, nbuckets + 1, it.scan_work, s)) != hipSuccess) return e;
+    prof_begin("cell_expand", s);
+    hipLaunchKernelGGL(k_expand_cell_items, dim3((uint32_t)((it.max_items + kExpandTile - 1) / kExpandTile)),
+                       dim3(kBlock), 0, s, it.item_off, nbuckets, it.items, it.max_items);
+    prof_end("cell_expand", s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     prof_begin("sample_points", s);
-    hipLaunchKernelGGL(k_sample_points, dim3((uint32_t)((q.n + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, q, g, rec,
-                       gids, cell_off, sorted_keys, order, T, tau, out_v, out_i);
+    hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kWavesPerBlock - 1) / kWavesPerBlock)),
+                       dim3(kBlock), 0, s, q, g, rec, gids, cell_off, point_off, order, it.item_off, it.items,
+                       it.max_items, T, tau, out_v, out_i);
     prof_end("sample_points", s);
     return hipGetLastError();
 }
