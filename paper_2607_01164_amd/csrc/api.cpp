@@ -99,6 +99,15 @@ GridParams grid_params(const gs_grid *g) {
     return p;
 }
 
+// Gaussians are ordered by the cell key of their box corner, coarsened to
+// at most 10 bits so that one radix pass sorts them.
+int gauss_order_full_bits(const gs_grid *g) { return bits_for(ncells_of(g) + 1); }
+int gauss_order_shift(const gs_grid *g) {
+    const int b = gauss_order_full_bits(g);
+    return b > 10 ? b - 10 : 0;
+}
+int gauss_order_bits(const gs_grid *g) { return gauss_order_full_bits(g) - gauss_order_shift(g); }
+
 // Index workspace layout.
 struct IndexWork {
     Record *rec;
@@ -110,6 +119,7 @@ struct IndexWork {
     void *gsort_work;
     uint64_t *pair_off;  // [n + 1]
     void *scan_work;
+    uint32_t *tile_first;  // [pair tiles] first Gaussian of every emit tile
     uint32_t *keys_alt;
     uint32_t *gids_alt;
     void *radix_work;
@@ -126,9 +136,10 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     w.gkeys = c.take<uint32_t>(n1);
     w.gsort_k = c.take<uint32_t>(n1);
     w.gsort_v = c.take<uint32_t>(n1);
-    w.gsort_work = c.take<char>(radix_work_bytes((int64_t)n1, bits_for(ncells_of(g) + 1)));
+    w.gsort_work = c.take<char>(radix_work_bytes((int64_t)n1, gauss_order_bits(g)));
     w.pair_off = c.take<uint64_t>((size_t)n + 1);
     w.scan_work = c.take<char>(scan_work_bytes(n + 1, 8));
+    w.tile_first = c.take<uint32_t>((size_t)((capacity > 0 ? capacity : 1) + 2047) / 2048 + 1);
     const int64_t cap = capacity > 0 ? capacity : 1;
     w.keys_alt = c.take<uint32_t>((size_t)cap);
     w.gids_alt = c.take<uint32_t>((size_t)cap);
@@ -422,12 +433,15 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
            "gs_build_index: preprocess");
     {
         // spatial visiting order of the Gaussians (sorted by box corner cell)
-        const int gbits = bits_for(ncells + 1);
+        const int gbits = gauss_order_bits(grid);
         const bool godd = (radix_passes(gbits) & 1) != 0;
         uint32_t *k0 = godd ? w.gsort_k : w.gkeys, *v0 = godd ? w.gsort_v : w.gorder;
         uint32_t *k1 = godd ? w.gkeys : w.gsort_k, *v1 = godd ? w.gorder : w.gsort_v;
-        GS_TRY(launch_gauss_keys(w.box, n, gp, k0, v0, stream), "gs_build_index: Gaussian keys");
-        GS_TRY(radix_sort_pairs(k0, v0, k1, v1, n, gbits, w.gsort_work, stream), "gs_build_index: Gaussian order");
+        GS_TRY(launch_gauss_keys(w.box, n, gp, gauss_order_shift(grid), k0, v0, radix_pass0(w.gsort_work, n, gbits),
+                                 stream),
+               "gs_build_index: Gaussian keys");
+        GS_TRY(radix_sort_pairs(k0, v0, k1, v1, n, gbits, w.gsort_work, stream, true),
+               "gs_build_index: Gaussian order");
     }
     GS_TRY(exclusive_scan_u64(w.pair_off, w.pair_off, n + 1, w.scan_work, stream), "gs_build_index: scan");
     uint64_t P = 0;
@@ -447,8 +461,10 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     // emit where the sort's last pass lands in keys/gids
     uint32_t *ek = odd ? w.keys_alt : index->keys, *ev = odd ? w.gids_alt : index->gids;
     uint32_t *ak = odd ? index->keys : w.keys_alt, *av = odd ? index->gids : w.gids_alt;
-    GS_TRY(launch_emit(w.pair_off, w.box, n, (int64_t)P, gp, ek, ev, stream), "gs_build_index: emit");
-    GS_TRY(radix_sort_pairs(ek, ev, ak, av, (int64_t)P, bits, w.radix_work, stream), "gs_build_index: sort");
+    GS_TRY(launch_emit(w.pair_off, w.box, n, (int64_t)P, gp, w.tile_first, ek, ev,
+                       radix_pass0(w.radix_work, (int64_t)P, bits), stream),
+           "gs_build_index: emit");
+    GS_TRY(radix_sort_pairs(ek, ev, ak, av, (int64_t)P, bits, w.radix_work, stream, true), "gs_build_index: sort");
     GS_TRY(key_offsets(index->keys, (int64_t)P, index->cell_offsets, ncells, stream), "gs_build_index: ranges");
     return GS_OK;
 }
@@ -512,8 +528,8 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
     const bool odd = (radix_passes(bits) & 1) != 0;
     uint32_t *ek = odd ? p.keys_alt : p.keys, *ev = odd ? p.order_alt : p.order;
     uint32_t *ak = odd ? p.keys : p.keys_alt, *av = odd ? p.order : p.order_alt;
-    GS_TRY(launch_query_keys(qp, gp, ek, ev, stream), "gs_sample: query keys");
-    GS_TRY(radix_sort_pairs(ek, ev, ak, av, nq, bits, p.radix_work, stream), "gs_sample: query sort");
+    GS_TRY(launch_query_keys(qp, gp, ek, ev, radix_pass0(p.radix_work, nq, bits), stream), "gs_sample: query keys");
+    GS_TRY(radix_sort_pairs(ek, ev, ak, av, nq, bits, p.radix_work, stream, true), "gs_sample: query sort");
     GS_TRY(key_offsets(p.keys, nq, p.point_off, gp.ncells + 1, stream), "gs_sample: query ranges");
     GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
                                 index->tau, out_value, out_influence, stream),

@@ -10,6 +10,7 @@
 // taken from the sorted keys.
 #include "expand.h"
 #include "internal.h"
+#include "radix.h"
 
 #pragma clang fp contract(off)
 
@@ -114,20 +115,57 @@ __global__ __launch_bounds__(kBlock) void k_preprocess(const float *__restrict__
 
 __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pair_off,
                                                  const CellBox *__restrict__ box, int64_t n, int64_t npairs,
-                                                 GridParams g, uint32_t *__restrict__ keys,
-                                                 uint32_t *__restrict__ gids) {
-    __shared__ ExpandShared sh;
-    const uint32_t tid = threadIdx.x;
-    const uint64_t tile_begin = (uint64_t)blockIdx.x * kExpandTile;
+                                                 const uint32_t *__restrict__ tile_first, GridParams g,
+                                                 uint32_t *__restrict__ keys, uint32_t *__restrict__ gids,
+                                                 RadixPass0 pass0) {
+    __shared__ uint32_t head[kExpandTile];
+    __shared__ uint32_t wmax[kWavesPerBlock];
+    __shared__ uint32_t hist_lds[kMaxDigits];
+    Pass0Hist hist(hist_lds, pass0);
+    const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
+    const uint64_t tile_begin = (uint64_t)tile * kExpandTile;
     const uint64_t rem = (uint64_t)npairs - tile_begin;
     const uint32_t tile_cnt = rem < (uint64_t)kExpandTile ? (uint32_t)rem : (uint32_t)kExpandTile;
-    const int64_t gfirst = expand_tile(pair_off, n, tile_begin, tile_cnt, sh);
+    const int64_t gfirst = tile_first[tile];
+    const int64_t glast = (tile + 1 < gridDim.x) ? (int64_t)tile_first[tile + 1] : n - 1;
+    for (uint32_t s = tid; s < (uint32_t)kExpandTile; s += kBlock) head[s] = 0;
+    __syncthreads();
+    // mark the first pair of every Gaussian that starts inside the tile
+    for (int64_t gg = gfirst + 1 + tid; gg <= glast; gg += kBlock) {
+        const uint64_t pos = pair_off[gg] - tile_begin;
+        if (pos < tile_cnt) atomicMax(&head[pos], (uint32_t)(gg - gfirst));
+    }
+    __syncthreads();
+    // inclusive max-scan carries each mark over the Gaussian's pairs
+    uint32_t run = 0;
+    const uint32_t b0 = tid * kExpandItems;
+#pragma unroll
+    for (int i = 0; i < kExpandItems; ++i) {
+        const uint32_t h = head[b0 + i];
+        run = h > run ? h : run;
+        head[b0 + i] = run;
+    }
+    const uint32_t incl = wave_incl_max(run);
+    uint32_t excl = __shfl_up(incl, 1, 64);
+    if (lane == 0) excl = 0;
+    if (lane == kWave - 1) wmax[wave] = incl;
+    __syncthreads();
+    uint32_t wpre = 0;
+    for (uint32_t w = 0; w < wave; ++w) wpre = wmax[w] > wpre ? wmax[w] : wpre;
+    const uint32_t carry = excl > wpre ? excl : wpre;
+#pragma unroll
+    for (int i = 0; i < kExpandItems; ++i) {
+        const uint32_t h = head[b0 + i];
+        head[b0 + i] = h > carry ? h : carry;
+    }
+    __syncthreads();
     const int64_t Cx = g.cells[0], Cy = g.cells[1];
 #pragma unroll 2
     for (int i = 0; i < kExpandItems; ++i) {
         const uint32_t slot = (uint32_t)i * kBlock + tid;
         if (slot < tile_cnt) {
-            const int64_t gg = gfirst + sh.head[slot];
+            const int64_t gg = gfirst + head[slot];
             const uint32_t local = (uint32_t)(tile_begin + slot - pair_off[gg]);
             const CellBox b = box[gg];
             const uint32_t nx = (uint32_t)(b.hi.x - b.lo.x + 1), ny = (uint32_t)(b.hi.y - b.lo.y + 1);
@@ -135,34 +173,59 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
             const int64_t cx = b.lo.x + (int64_t)(local - t * nx);
             const int64_t cy = b.lo.y + (int64_t)(t % ny);
             const int64_t cz = b.lo.z + (int64_t)(t / ny);
-            keys[tile_begin + slot] = (uint32_t)(cx + Cx * (cy + Cy * cz));
+            const uint32_t key = (uint32_t)(cx + Cx * (cy + Cy * cz));
+            keys[tile_begin + slot] = key;
             gids[tile_begin + slot] = (uint32_t)gg;
+            hist.add(key);
         }
     }
+    hist.finish_tile(tile);
 }
 
 // Sort key of each Gaussian for the spatial visiting order: the cell key of
-// its box's low corner, ncells for an empty box.
+// its box's low corner (ncells for an empty box), shifted right by `shift`
+// so that one radix pass orders it. Tiles of kSortTile Gaussians per
+// workgroup, with the pass's digit counts.
 __global__ __launch_bounds__(kBlock) void k_gauss_keys(const CellBox *__restrict__ box, int64_t n, GridParams g,
-                                                       uint32_t *__restrict__ keys, uint32_t *__restrict__ ids) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    const CellBox b = box[i];
-    uint32_t key = (uint32_t)g.ncells;
-    if (b.hi.x >= b.lo.x)
-        key = (uint32_t)((int64_t)b.lo.x + (int64_t)g.cells[0] * ((int64_t)b.lo.y + (int64_t)g.cells[1] * b.lo.z));
-    keys[i] = key;
-    ids[i] = (uint32_t)i;
+                                                       int shift, uint32_t *__restrict__ keys,
+                                                       uint32_t *__restrict__ ids, RadixPass0 pass0) {
+    __shared__ uint32_t hist_lds[kMaxDigits];
+    Pass0Hist hist(hist_lds, pass0);
+#pragma unroll
+    for (int it = 0; it < kSortItems; ++it) {
+        const int64_t i = (int64_t)blockIdx.x * kSortTile + (int64_t)it * kBlock + threadIdx.x;
+        if (i < n) {
+            const CellBox b = box[i];
+            uint32_t key = (uint32_t)g.ncells;
+            if (b.hi.x >= b.lo.x)
+                key = (uint32_t)((int64_t)b.lo.x + (int64_t)g.cells[0] * ((int64_t)b.lo.y + (int64_t)g.cells[1] * b.lo.z));
+            key >>= shift;
+            keys[i] = key;
+            ids[i] = (uint32_t)i;
+            hist.add(key);
+        }
+    }
+    hist.finish_tile(blockIdx.x);
+}
+
+// First segment of every emit tile: tile_first[t] = the Gaussian owning pair
+// t * kSortTile (all searches run in parallel, one thread per tile).
+__global__ __launch_bounds__(kBlock) void k_tile_first(const uint64_t *__restrict__ pair_off, int64_t n,
+                                                       int64_t npairs, uint32_t ntiles,
+                                                       uint32_t *__restrict__ tile_first) {
+    const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= ntiles) return;
+    tile_first[t] = (uint32_t)segment_search(pair_off, n, (uint64_t)t * kSortTile);
 }
 
 }  // namespace
 
-hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g, uint32_t *keys, uint32_t *ids,
-                             hipStream_t s) {
+hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g, int shift, uint32_t *keys,
+                             uint32_t *ids, const RadixPass0 &pass0, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     prof_begin("gauss_keys", s);
-    hipLaunchKernelGGL(k_gauss_keys, dim3((uint32_t)((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, box, n, g, keys,
-                       ids);
+    hipLaunchKernelGGL(k_gauss_keys, dim3((uint32_t)((n + kSortTile - 1) / kSortTile)), dim3(kBlock), 0, s, box, n, g,
+                       shift, keys, ids, pass0);
     prof_end("gauss_keys", s);
     return hipGetLastError();
 }
@@ -180,11 +243,18 @@ hipError_t launch_preprocess(const float *mean, const float *scale, const float 
 }
 
 hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, int64_t n, int64_t npairs, const GridParams &g,
-                       uint32_t *keys, uint32_t *gids, hipStream_t s) {
+                       uint32_t *tile_first, uint32_t *keys, uint32_t *gids, const RadixPass0 &pass0, hipStream_t s) {
     if (npairs <= 0 || n <= 0) return hipSuccess;
     const uint32_t blocks = (uint32_t)((npairs + kExpandTile - 1) / kExpandTile);
+    prof_begin("emit_partition", s);
+    hipLaunchKernelGGL(k_tile_first, dim3((blocks + kBlock - 1) / kBlock), dim3(kBlock), 0, s, pair_off, n, npairs,
+                       blocks, tile_first);
+    prof_end("emit_partition", s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
     prof_begin("emit", s);
-    hipLaunchKernelGGL(k_emit, dim3(blocks), dim3(kBlock), 0, s, pair_off, box, n, npairs, g, keys, gids);
+    hipLaunchKernelGGL(k_emit, dim3(blocks), dim3(kBlock), 0, s, pair_off, box, n, npairs, tile_first, g, keys, gids,
+                       pass0);
     prof_end("emit", s);
     return hipGetLastError();
 }

@@ -142,12 +142,27 @@ size_t scan_work_bytes(int64_t n, int elem_bytes);
 hipError_t exclusive_scan_u32(const uint32_t *in, uint32_t *out, int64_t n, void *work, hipStream_t s);
 hipError_t exclusive_scan_u64(const uint64_t *in, uint64_t *out, int64_t n, void *work, hipStream_t s);
 
-// Stable LSD radix sort of (key, value) pairs by the low `bits` key bits.
-// The result ends in (keys, vals); alt buffers are scratch of n elements.
+// Stable LSD radix sort of (key, value) pairs by the low `bits` key bits
+// (radix.h has the tile geometry). Passes alternate between the two buffer
+// pairs; radix_passes(bits) tells which one holds the result.
+struct RadixLayout {
+    uint32_t *table;       // [ndig][nb] tile counts, scanned in place
+    uint32_t *digit_base;  // [ndig]
+    uint32_t nb;           // tiles
+    int passes, dbits;
+    size_t bytes;
+};
+struct RadixPass0 {       // lets the producer of the keys count the first digit
+    uint32_t *table;       // null: the sort counts it itself
+    uint32_t nb;
+    uint32_t mask;
+};
+RadixLayout radix_layout(void *work, int64_t n, int bits);
 size_t radix_work_bytes(int64_t n, int bits);
+RadixPass0 radix_pass0(void *work, int64_t n, int bits);
 int radix_passes(int bits);
-hipError_t radix_sort_pairs(uint32_t *keys, uint32_t *vals, uint32_t *keys_alt, uint32_t *vals_alt, int64_t n,
-                            int bits, void *work, hipStream_t s);
+hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n, int bits, void *work,
+                            hipStream_t s, bool pass0_ready);
 
 // offsets[k] = number of sorted keys < k, k = 0..nkeys (nkeys+1 entries).
 hipError_t key_offsets(const uint32_t *sorted_keys, int64_t n, uint32_t *offsets, int64_t nkeys, hipStream_t s);
@@ -165,8 +180,9 @@ struct GridParams {
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
                              CellBox *box, uint64_t *count, hipStream_t s);
+// tile_first: ceil(npairs / kSortTile) words of scratch
 hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, int64_t n, int64_t npairs, const GridParams &g,
-                       uint32_t *keys, uint32_t *gids, hipStream_t s);
+                       uint32_t *tile_first, uint32_t *keys, uint32_t *gids, const RadixPass0 &pass0, hipStream_t s);
 
 // Sampling (sample.hip).
 struct QueryParams {
@@ -177,7 +193,10 @@ struct QueryParams {
     const float *points;
     float vsz[3];        // (hi - lo) / dims, float32
 };
-hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids, hipStream_t s);
+// Cell key of every query (ncells outside the domain), identity ids and
+// the first sort digit's tile counts.
+hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids,
+                             const RadixPass0 &pass0, hipStream_t s);
 hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                               const uint32_t *cell_off, float T, float tau, float *out_v, float *out_i,
                               hipStream_t s);
@@ -195,8 +214,8 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
 
 // Gaussians in spatial order: sorted by the cell key of their box's low
 // corner (empty boxes last), so neighbouring work shares cached queries.
-hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g, uint32_t *keys, uint32_t *ids,
-                             hipStream_t s);
+hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g, int shift, uint32_t *keys,
+                             uint32_t *ids, const RadixPass0 &pass0, hipStream_t s);
 
 // Backward (backward.hip).
 struct BackwardBuffers {

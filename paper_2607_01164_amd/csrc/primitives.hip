@@ -2,6 +2,7 @@
 // (key, value) pairs with wave-level multi-split ranking in LDS, per-key
 // offsets of a sorted key array, and fills.
 #include "internal.h"
+#include "radix.h"
 
 namespace gs {
 
@@ -101,12 +102,11 @@ int64_t scan_levels_elems(int64_t n) {
 }
 
 // ---------------------------------------------------------------------------
-// Radix sort.
-
-constexpr int kSortItems = 16;
-constexpr int kSortTile = kBlock * kSortItems;  // 4096
-constexpr int kMaxDigitBits = 10;
-constexpr int kMaxDigits = 1 << kMaxDigitBits;
+// Radix sort (stable LSD, reduce-then-scan). Per pass: tile histograms of
+// the digit (the first pass's can come from the kernel that produced the
+// keys), an exclusive scan of every digit's row of tile counts plus one of
+// the digit totals, and a scatter that ranks each tile in LDS and writes it
+// out digit by digit.
 
 int passes_for(int bits) { return bits <= 0 ? 0 : (bits + kMaxDigitBits - 1) / kMaxDigitBits; }
 int digit_bits_for(int bits) {
@@ -114,59 +114,116 @@ int digit_bits_for(int bits) {
     return p == 0 ? 0 : (bits + p - 1) / p;
 }
 
-// Digit histogram of one tile, written digit-major: table[d * nb + block].
 __global__ __launch_bounds__(kBlock) void k_radix_upsweep(const uint32_t *__restrict__ keys, int64_t n, int shift,
                                                           uint32_t mask, uint32_t ndig, uint32_t *__restrict__ table,
                                                           uint32_t nb) {
     __shared__ uint32_t h[kMaxDigits];
     for (uint32_t d = threadIdx.x; d < ndig; d += kBlock) h[d] = 0;
     __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * kSortTile;
-#pragma unroll 4
+    const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
+    const int64_t base = (int64_t)tile * kSortTile;
+#pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
-        int64_t idx = base + (int64_t)i * kBlock + threadIdx.x;
+        const int64_t idx = base + (int64_t)i * kBlock + threadIdx.x;
         if (idx < n) atomicAdd(&h[(keys[idx] >> shift) & mask], 1u);
     }
     __syncthreads();
-    for (uint32_t d = threadIdx.x; d < ndig; d += kBlock) table[(size_t)d * nb + blockIdx.x] = h[d];
+    for (uint32_t d = threadIdx.x; d < ndig; d += kBlock) table[(size_t)d * nb + tile] = h[d];
 }
 
-// Stable scatter of one tile. Each wave ranks its 16 rows of 64 keys in
-// order: lanes holding the same digit are found with one ballot per digit
-// bit; a per-wave running count per digit in LDS gives each key its rank
-// among earlier keys of the wave. Waves are then combined per digit, the
-// tile is reordered by digit in LDS, and written out in runs.
+// One workgroup per digit: exclusive scan of the digit's tile counts in
+// place, and the digit's total.
+__global__ __launch_bounds__(kBlock) void k_digit_scan(uint32_t *__restrict__ table, uint32_t nb,
+                                                       uint32_t *__restrict__ digit_tot) {
+    __shared__ uint32_t lds[kWavesPerBlock];
+    uint32_t *row = table + (size_t)blockIdx.x * nb;
+    uint32_t carry = 0;
+    for (uint32_t c0 = 0; c0 < nb; c0 += kBlock * 4) {
+        uint32_t v[4];
+        uint32_t s = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t idx = c0 + threadIdx.x * 4 + i;
+            v[i] = idx < nb ? row[idx] : 0u;
+            s += v[i];
+        }
+        uint32_t tot;
+        uint32_t run = block_excl_scan(s, lds, &tot) + carry;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t idx = c0 + threadIdx.x * 4 + i;
+            if (idx < nb) row[idx] = run;
+            run += v[i];
+        }
+        carry += tot;
+    }
+    if (threadIdx.x == 0) digit_tot[blockIdx.x] = carry;
+}
+
+// exclusive scan of the digit totals (ndig <= 1024) in place
+__global__ __launch_bounds__(kBlock) void k_digit_base(uint32_t *__restrict__ digit, uint32_t ndig) {
+    __shared__ uint32_t lds[kWavesPerBlock];
+    constexpr int J = kMaxDigits / kBlock;
+    uint32_t v[J];
+    uint32_t s = 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const uint32_t d = threadIdx.x * J + j;
+        v[j] = d < ndig ? digit[d] : 0u;
+        s += v[j];
+    }
+    uint32_t tot;
+    uint32_t run = block_excl_scan(s, lds, &tot);
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const uint32_t d = threadIdx.x * J + j;
+        if (d < ndig) digit[d] = run;
+        run += v[j];
+    }
+}
+
+// Stable scatter of one tile of kSortTile keys. Each wave ranks its
+// kSortItems rows of 64 keys in order: lanes holding the same digit are
+// found with one ballot per digit bit, and a per-wave running count per
+// digit in LDS gives each key its rank among earlier keys of the wave.
+// Waves are then combined per digit, the tile is reordered by digit in LDS
+// and written out in runs. LDS: (6 ndig + 2 kSortTile) words, dynamic.
 __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__restrict__ kin,
                                                             const uint32_t *__restrict__ vin,
                                                             uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
                                                             int64_t n, int shift, int dbits,
-                                                            const uint32_t *__restrict__ goff, uint32_t nb) {
-    __shared__ uint32_t wcnt[kWavesPerBlock][kMaxDigits];
-    __shared__ uint32_t dstart[kMaxDigits];  // first slot of each digit inside the tile
-    __shared__ uint32_t dglob[kMaxDigits];   // global position of each digit's first key of the tile
-    __shared__ uint32_t sk[kSortTile];
-    __shared__ uint32_t sv[kSortTile];
+                                                            const uint32_t *__restrict__ table,
+                                                            const uint32_t *__restrict__ digit_base, uint32_t nb) {
+    extern __shared__ uint32_t lds[];
     __shared__ uint32_t scan_lds[kWavesPerBlock];
-
     const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const uint32_t ndig = 1u << dbits, mask = ndig - 1;
+    // consecutive tiles on one XCD: their runs of each digit are adjacent in
+    // the output and merge in that XCD's L2
+    const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
+    uint32_t *wcnt = lds;                        // [kWavesPerBlock][ndig]
+    uint32_t *dstart = wcnt + kWavesPerBlock * ndig;
+    uint32_t *dglob = dstart + ndig;
+    uint32_t *sk = dglob + ndig;                 // [kSortTile]
+    uint32_t *sv = sk + kSortTile;               // [kSortTile]
     for (uint32_t d = tid; d < ndig; d += kBlock) {
 #pragma unroll
-        for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][d] = 0;
-        dglob[d] = goff[(size_t)d * nb + blockIdx.x];
+        for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w * ndig + d] = 0;
+        dglob[d] = digit_base[d] + table[(size_t)d * nb + tile];
     }
     __syncthreads();
 
-    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)wave * (kWave * kSortItems);
+    const int64_t base = (int64_t)tile * kSortTile + (int64_t)wave * (kWave * kSortItems);
     uint32_t k[kSortItems], v[kSortItems], r[kSortItems];
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
-        int64_t idx = base + (int64_t)i * kWave + lane;
-        bool ok = idx < n;
+        const int64_t idx = base + (int64_t)i * kWave + lane;
+        const bool ok = idx < n;
         k[i] = ok ? kin[idx] : 0u;
         v[i] = ok ? vin[idx] : 0u;
     }
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    uint32_t *mycnt = wcnt + wave * ndig;
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         const int64_t idx = base + (int64_t)i * kWave + lane;
@@ -181,47 +238,33 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
         const uint32_t before = (uint32_t)__popcll(m & lt_mask);
         const uint32_t cnt = (uint32_t)__popcll(m);
         uint32_t basecnt = 0;
-        if (ok) basecnt = wcnt[wave][d];
-        // all lanes of the wave have read the counter before its leader writes
+        if (ok) basecnt = mycnt[d];
+        // every lane of the wave has read the counter before its leader writes
         __builtin_amdgcn_wave_barrier();
-        if (ok && before == 0) wcnt[wave][d] = basecnt + cnt;
+        if (ok && before == 0) mycnt[d] = basecnt + cnt;
         __builtin_amdgcn_wave_barrier();
         r[i] = basecnt + before;
     }
     __syncthreads();
-    // per digit: exclusive scan over the waves, and the tile total
-    uint32_t my_tot[kMaxDigits / kBlock];
-#pragma unroll
-    for (int j = 0; j < kMaxDigits / kBlock; ++j) {
-        uint32_t d = tid + j * kBlock;
+    // per digit: exclusive scan over the waves (in place) and the tile total
+    constexpr int J = kMaxDigits / kBlock;
+    for (uint32_t d = tid; d < ndig; d += kBlock) {
         uint32_t s = 0;
-        if (d < ndig) {
 #pragma unroll
-            for (int w = 0; w < kWavesPerBlock; ++w) {
-                uint32_t t = wcnt[w][d];
-                wcnt[w][d] = s;
-                s += t;
-            }
+        for (int w = 0; w < kWavesPerBlock; ++w) {
+            const uint32_t t = wcnt[w * ndig + d];
+            wcnt[w * ndig + d] = s;
+            s += t;
         }
-        my_tot[j] = s;
+        dstart[d] = s;
     }
-    // exclusive scan of digit totals over digits -> dstart (digit d = tid + j*256;
-    // scan thread-major: each thread owns digits tid*J .. tid*J+J-1 instead)
     __syncthreads();
     {
-        // gather totals into dstart temporarily
-#pragma unroll
-        for (int j = 0; j < kMaxDigits / kBlock; ++j) {
-            uint32_t d = tid + j * kBlock;
-            if (d < ndig) dstart[d] = my_tot[j];
-        }
-        __syncthreads();
-        constexpr int J = kMaxDigits / kBlock;
         uint32_t loc[J];
         uint32_t s = 0;
 #pragma unroll
         for (int j = 0; j < J; ++j) {
-            uint32_t d = tid * J + j;
+            const uint32_t d = tid * J + j;
             loc[j] = d < ndig ? dstart[d] : 0u;
             s += loc[j];
         }
@@ -229,7 +272,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
         uint32_t run = block_excl_scan(s, scan_lds, &tot);
 #pragma unroll
         for (int j = 0; j < J; ++j) {
-            uint32_t d = tid * J + j;
+            const uint32_t d = tid * J + j;
             if (d < ndig) dstart[d] = run;
             run += loc[j];
         }
@@ -240,15 +283,15 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
         const int64_t idx = base + (int64_t)i * kWave + lane;
         if (idx < n) {
             const uint32_t d = (k[i] >> shift) & mask;
-            const uint32_t slot = dstart[d] + wcnt[wave][d] + r[i];
+            const uint32_t slot = dstart[d] + mycnt[d] + r[i];
             sk[slot] = k[i];
             sv[slot] = v[i];
         }
     }
     __syncthreads();
-    const int64_t tile_n = n - (int64_t)blockIdx.x * kSortTile;
+    const int64_t tile_n = n - (int64_t)tile * kSortTile;
     const uint32_t cnt = tile_n < kSortTile ? (uint32_t)tile_n : (uint32_t)kSortTile;
-#pragma unroll 4
+#pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         const uint32_t slot = (uint32_t)i * kBlock + tid;
         if (slot < cnt) {
@@ -263,14 +306,19 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     }
 }
 
-__global__ void k_key_offsets(const uint32_t *__restrict__ keys, int64_t n, uint32_t *__restrict__ off,
-                              int64_t nkeys) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i > n) return;
-    const int64_t a = (i == 0) ? 0 : (int64_t)keys[i - 1] + 1;
-    int64_t b = (i == n) ? nkeys : (int64_t)keys[i];
-    b = b < nkeys ? b : nkeys;
-    for (int64_t k = a; k <= b; ++k) off[k] = (uint32_t)i;
+// offsets[k] = number of keys < k: thread t looks at the boundaries after
+// keys t*8-1 .. t*8+7 of the sorted array
+__global__ __launch_bounds__(kBlock) void k_key_offsets(const uint32_t *__restrict__ keys, int64_t n,
+                                                        uint32_t *__restrict__ off, int64_t nkeys) {
+    const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+    if (i0 > n) return;
+    int64_t prev = (i0 == 0) ? -1 : (int64_t)keys[i0 - 1];
+    for (int64_t i = i0; i < i0 + 8 && i <= n; ++i) {
+        int64_t cur = (i == n) ? nkeys : (int64_t)keys[i];
+        cur = cur < nkeys ? cur : nkeys;
+        for (int64_t k = prev + 1; k <= cur; ++k) off[k] = (uint32_t)i;
+        prev = cur > prev ? cur : prev;
+    }
 }
 
 __global__ void k_fill_u32(uint32_t *p, uint32_t v, int64_t n) {
@@ -305,53 +353,72 @@ hipError_t exclusive_scan_u64(const uint64_t *in, uint64_t *out, int64_t n, void
 
 int radix_passes(int bits) { return passes_for(bits); }
 
-size_t radix_work_bytes(int64_t n, int bits) {
-    const int db = digit_bits_for(bits);
-    if (db == 0) return 256;
-    const int64_t nb = ceil_div(n > 0 ? n : 1, kSortTile);
-    const int64_t table = (int64_t)(1 << db) * nb;
-    size_t bytes = (size_t)table * 4;
-    bytes = (bytes + 255) & ~(size_t)255;
-    return bytes + scan_work_bytes(table, 4) + 256;
+RadixLayout radix_layout(void *work, int64_t n, int bits) {
+    RadixLayout L;
+    L.passes = passes_for(bits);
+    L.dbits = digit_bits_for(bits);
+    L.nb = (uint32_t)ceil_div(n > 0 ? n : 1, kSortTile);
+    const uint32_t ndig = L.dbits > 0 ? (1u << L.dbits) : 1u;
+    char *b = (char *)work;
+    L.table = (uint32_t *)b;
+    const size_t tbytes = ((size_t)ndig * L.nb * 4 + 255) & ~(size_t)255;
+    L.digit_base = b ? (uint32_t *)(b + tbytes) : nullptr;
+    L.bytes = tbytes + (((size_t)ndig * 4 + 255) & ~(size_t)255);
+    return L;
+}
+
+size_t radix_work_bytes(int64_t n, int bits) { return radix_layout(nullptr, n, bits).bytes; }
+
+RadixPass0 radix_pass0(void *work, int64_t n, int bits) {
+    const RadixLayout L = radix_layout(work, n, bits);
+    RadixPass0 p;
+    p.table = L.passes > 0 ? L.table : nullptr;
+    p.nb = L.nb;
+    p.mask = L.dbits > 0 ? (1u << L.dbits) - 1u : 0u;
+    return p;
 }
 
 // Sorts n pairs that start in (k0, v0); passes alternate between (k0, v0)
 // and (k1, v1). The result is in (k0, v0) after an even number of passes
-// and in (k1, v1) after an odd number (radix_passes(bits)).
+// and in (k1, v1) after an odd number (radix_passes(bits)). When pass0_ready
+// the producer of the keys has already written the first pass's tile
+// histograms (radix_pass0).
 hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n, int bits, void *work,
-                            hipStream_t s) {
-    const int passes = passes_for(bits);
-    if (passes == 0 || n <= 0) return hipSuccess;
+                            hipStream_t s, bool pass0_ready) {
+    const RadixLayout L = radix_layout(work, n, bits);
+    if (L.passes == 0 || n <= 0) return hipSuccess;
     if (n == 1) {
         // already sorted; move it where an odd number of passes would leave it
-        if (passes & 1) {
+        if (L.passes & 1) {
             hipError_t e = hipMemcpyAsync(k1, k0, 4, hipMemcpyDeviceToDevice, s);
             if (e == hipSuccess) e = hipMemcpyAsync(v1, v0, 4, hipMemcpyDeviceToDevice, s);
             return e;
         }
         return hipSuccess;
     }
-    const int db = digit_bits_for(bits);
-    const uint32_t ndig = 1u << db;
-    const uint32_t nb = (uint32_t)ceil_div(n, kSortTile);
-    uint32_t *table = (uint32_t *)work;
-    size_t tbytes = ((size_t)ndig * nb * 4 + 255) & ~(size_t)255;
-    void *scan_work = (char *)work + tbytes;
+    const uint32_t ndig = 1u << L.dbits;
+    const size_t lds = ((size_t)6 * ndig + 2 * kSortTile) * 4;
     uint32_t *ki = k0, *vi = v0, *ko = k1, *vo = v1;
-    for (int p = 0; p < passes; ++p) {
-        const int shift = p * db;
-        prof_begin("radix_upsweep", s);
-        hipLaunchKernelGGL(k_radix_upsweep, dim3(nb), dim3(kBlock), 0, s, ki, n, shift, ndig - 1, ndig, table, nb);
-        prof_end("radix_upsweep", s);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        e = exclusive_scan_u32(table, table, (int64_t)ndig * nb, scan_work, s);
-        if (e != hipSuccess) return e;
+    for (int p = 0; p < L.passes; ++p) {
+        const int shift = p * L.dbits;
+        hipError_t e;
+        if (p > 0 || !pass0_ready) {
+            prof_begin("radix_upsweep", s);
+            hipLaunchKernelGGL(k_radix_upsweep, dim3(L.nb), dim3(kBlock), 0, s, ki, n, shift, ndig - 1, ndig, L.table,
+                               L.nb);
+            prof_end("radix_upsweep", s);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        prof_begin("radix_scan", s);
+        hipLaunchKernelGGL(k_digit_scan, dim3(ndig), dim3(kBlock), 0, s, L.table, L.nb, L.digit_base);
+        hipLaunchKernelGGL(k_digit_base, dim3(1), dim3(kBlock), 0, s, L.digit_base, ndig);
+        prof_end("radix_scan", s);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
         prof_begin("radix_downsweep", s);
-        hipLaunchKernelGGL(k_radix_downsweep, dim3(nb), dim3(kBlock), 0, s, ki, vi, ko, vo, n, shift, db, table, nb);
+        hipLaunchKernelGGL(k_radix_downsweep, dim3(L.nb), dim3(kBlock), lds, s, ki, vi, ko, vo, n, shift, L.dbits,
+                           L.table, L.digit_base, L.nb);
         prof_end("radix_downsweep", s);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        if ((e = hipGetLastError()) != hipSuccess) return e;
         uint32_t *tk = ki, *tv = vi;
         ki = ko;
         vi = vo;
@@ -362,7 +429,7 @@ hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *
 }
 
 hipError_t key_offsets(const uint32_t *sorted_keys, int64_t n, uint32_t *offsets, int64_t nkeys, hipStream_t s) {
-    const int64_t threads = n + 1;
+    const int64_t threads = n / 8 + 1;
     prof_begin("key_offsets", s);
     hipLaunchKernelGGL(k_key_offsets, dim3((uint32_t)ceil_div(threads, kBlock)), dim3(kBlock), 0, s, sorted_keys, n,
                        offsets, nkeys);

@@ -13,6 +13,7 @@
 // candidate Gaussians in the lanes instead (see k_sample_cells).
 #include "expand.h"
 #include "internal.h"
+#include "radix.h"
 
 #pragma clang fp contract(off)
 
@@ -120,29 +121,37 @@ __device__ __forceinline__ void query_position(const QueryParams &q, const GridP
 }
 
 __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams g, uint32_t *__restrict__ keys,
-                                                       uint32_t *__restrict__ ids) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= q.n) return;
-    float p[3];
-    bool valid;
-    query_position(q, g, (uint32_t)i, p[0], p[1], p[2], valid);
-    uint32_t key = (uint32_t)g.ncells;
-    if (valid) {
-        bool inside = true;
-        int64_t c[3];
+                                                       uint32_t *__restrict__ ids, RadixPass0 pass0) {
+    __shared__ uint32_t hist_lds[kMaxDigits];
+    Pass0Hist hist(hist_lds, pass0);
 #pragma unroll
-        for (int j = 0; j < 3; ++j) {
-            inside = inside && (p[j] >= g.lo[j]) && (p[j] <= g.hi[j]);
-            const float t = (p[j] - g.lo[j]) * g.invc[j];
-            int64_t ci = (int64_t)floorf(t);
-            ci = ci < 0 ? 0 : ci;
-            ci = ci > g.cells[j] - 1 ? g.cells[j] - 1 : ci;
-            c[j] = ci;
+    for (int it = 0; it < kSortItems; ++it) {
+        const int64_t i = (int64_t)blockIdx.x * kSortTile + (int64_t)it * kBlock + threadIdx.x;
+        if (i < q.n) {
+            float p[3];
+            bool valid;
+            query_position(q, g, (uint32_t)i, p[0], p[1], p[2], valid);
+            uint32_t key = (uint32_t)g.ncells;
+            if (valid) {
+                bool inside = true;
+                int64_t c[3];
+#pragma unroll
+                for (int j = 0; j < 3; ++j) {
+                    inside = inside && (p[j] >= g.lo[j]) && (p[j] <= g.hi[j]);
+                    const float t = (p[j] - g.lo[j]) * g.invc[j];
+                    int64_t ci = (int64_t)floorf(t);
+                    ci = ci < 0 ? 0 : ci;
+                    ci = ci > g.cells[j] - 1 ? g.cells[j] - 1 : ci;
+                    c[j] = ci;
+                }
+                if (inside) key = (uint32_t)(c[0] + (int64_t)g.cells[0] * (c[1] + (int64_t)g.cells[1] * c[2]));
+            }
+            keys[i] = key;
+            ids[i] = (uint32_t)i;
+            hist.add(key);
         }
-        if (inside) key = (uint32_t)(c[0] + (int64_t)g.cells[0] * (c[1] + (int64_t)g.cells[1] * c[2]));
     }
-    keys[i] = key;
-    ids[i] = (uint32_t)i;
+    hist.finish_tile(blockIdx.x);
 }
 
 // Work items of the ordered-query sampler: one per cell holding fewer than
@@ -296,11 +305,11 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
 }  // namespace
 
 hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids,
-                             hipStream_t s) {
+                             const RadixPass0 &pass0, hipStream_t s) {
     if (q.n <= 0) return hipSuccess;
     prof_begin("query_keys", s);
-    hipLaunchKernelGGL(k_query_keys, dim3((uint32_t)((q.n + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, q, g, keys,
-                       ids);
+    hipLaunchKernelGGL(k_query_keys, dim3((uint32_t)((q.n + kSortTile - 1) / kSortTile)), dim3(kBlock), 0, s, q, g,
+                       keys, ids, pass0);
     prof_end("query_keys", s);
     return hipGetLastError();
 }
