@@ -24,7 +24,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_VEC_PEAK_TFLOPS = 157.3   # MI355X vector FP32 (packed FMA)
 WORKLOAD = "c2_grid256_batch"
-INDEX_CELLS = (64, 64, 64)
+INDEX_CELLS = (40, 40, 40)
 TAU = 0.01
 
 
