@@ -13,8 +13,10 @@ the library's stream), the roofline of the dominant kernel and the CPU
 oracle's rate on a bounded sample of the same workload.
 """
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -22,7 +24,17 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
-FP32_VEC_PEAK_TFLOPS = 157.3   # MI355X vector FP32 (packed FMA)
+FP32_VEC_PEAK_TFLOPS = 157.3   # MI355X vector FP32: 256 CUs x 2.4 GHz x 128 lanes x 2 (packed FMA)
+# Algorithmic work per contributing (Gaussian, point) pair: forward evaluates
+# d = p - mu, u = M d, Q = |u|^2, a = w exp(-Q/2), I += a, V += a v; the
+# backward repeats u, Q, a and forms dL/da, the per-pair moment terms and dv,
+# dw. Counted as adds and multiplies (an FMA is 2), the exponential as 1.
+FLOPS_PER_PAIR = {"sample_points": 31.0, "sample_grid": 31.0, "bwd_gauss": 61.0}
+# Bytes one pass of the LSD sort moves per pair: read and write key and value.
+SORT_BYTES_PER_PAIR = 16.0
+EMIT_BYTES_PER_PAIR = 8.0
+COPY_PROBE_BYTES = 256 << 20   # plain copy used to calibrate the HBM byte counters
+SRC_DIR = os.path.join(ROOT, "paper_2607_01164_amd", "csrc")
 WORKLOAD = "c2_grid256_batch"
 INDEX_CELLS = (40, 40, 40)
 TAU = 0.01
@@ -38,9 +50,11 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--cells", type=int, nargs=3, default=list(INDEX_CELLS))
-    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target length of the CPU oracle sample")
+    p.add_argument("--cpu-seconds", type=float, default=16.0, help="target length of the CPU oracle sample")
     p.add_argument("--no-cpu", action="store_true")
     p.add_argument("--breakdown", action="store_true", help="print the per-kernel table to stderr")
+    p.add_argument("--copy-probe", action="store_true",
+                   help="after the timed region, run a plain 256 MiB copy (counter calibration under rocprofv3)")
     return p.parse_args()
 
 
@@ -147,29 +161,45 @@ def main():
     for _ in range(a.warmup):
         st.step()
     sync()
-    # timed region: K whole steps, kernels bracketed by HIP events on the stream
+    # untimed pass with every kernel bracketed by events: the per-kernel table
+    # and the dominant kernel
+    gs.profile_select(None)
+    gs.profile_reset()
+    gs.profile_enable(True)
+    for _ in range(a.steps):
+        st.step()
+    sync()
+    gs.profile_enable(False)
+    prof = gs.profile_read()
+    kernels = {k: {"launches_per_step": c / a.steps, "ms_per_step": ms / a.steps, "avg_ms": ms / c}
+               for k, (c, ms) in prof.items()}
+    dom_name = max(kernels.items(), key=lambda kv: kv[1]["ms_per_step"])[0]
+    # timed region: K whole steps; only the dominant kernel is bracketed by
+    # HIP events (on the library's stream), for its roofline entry
+    gs.profile_select(dom_name)
     gs.profile_reset()
     gs.profile_enable(True)
     t_step = timed(st.step, a.steps, sync)
     gs.profile_enable(False)
-    prof = gs.profile_read()
+    gs.profile_select(None)
+    c, ms = gs.profile_read()[dom_name]
+    dom = (dom_name, {"launches_per_step": c / a.steps, "ms_per_step": ms / a.steps, "avg_ms": ms / c})
     n_pairs = st.index.n_pairs
     # forward alone and backward alone, for the query rates
     t_fwd = timed(st.forward, a.steps, sync)
     t_bwd = timed(st.backward, a.steps, sync)
     t_build = timed(st.build, a.steps, sync)
 
-    kernels = {k: {"launches_per_step": c / a.steps, "ms_per_step": ms / a.steps, "avg_ms": ms / c}
-               for k, (c, ms) in prof.items()}
     if a.breakdown:
         for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
             log(f"{k:18s} {v['ms_per_step'] * 1e3:9.1f} us/step  {v['launches_per_step']:5.1f} launches  "
                 f"avg {v['avg_ms'] * 1e3:9.1f} us")
-    dom = max(kernels.items(), key=lambda kv: kv[1]["ms_per_step"])
-    roof = roofline(dom[0], dom[1], st, n_pairs)
+    if a.copy_probe:
+        copy_probe()
 
     cpu = None if a.no_cpu else cpu_baseline(st, a.cpu_seconds)
     contrib = cpu.pop("contrib_per_point") if cpu else None
+    roof = roofline(dom[0], dom[1], st, n_pairs, contrib)
     out = {
         "metric": "query points/sec fwd and fwd+bwd samples/sec; % of HBM roofline",
         "value": st.n / t_step,
@@ -197,23 +227,75 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def roofline(name, k, st, n_pairs):
-    """Roofline entry of the dominant kernel: algorithmic bytes (or flops) of
-    one launch over its average launch duration."""
+def copy_probe():
+    """A plain device copy of COPY_PROBE_BYTES (read once, written once), so
+    that a counter run sees the HBM bytes of a kernel of known traffic."""
+    import torch
+    src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+
+
+def source_digest():
+    """sha256 over the kernel sources; a stored counter reading is used only
+    while the sources it was taken on are unchanged."""
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(SRC_DIR)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            with open(os.path.join(SRC_DIR, f), "rb") as fh:
+                h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(name):
+    """HBM bytes per launch of kernel `name` from the committed counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by the copy-probe calibration),
+    or None when there is none or the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", f"{name}_c2_step_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    dig = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not dig or not val or dig.group(1) != source_digest():
+        return None
+    return float(val.group(1))
+
+
+def roofline(name, k, st, n_pairs, contrib_per_point):
+    """Roofline entry of the dominant kernel: algorithmic flops (or bytes) of
+    one launch over its average launch duration (HIP events on the stream the
+    kernel runs on)."""
     avg_s = k["avg_ms"] * 1e-3
-    per_step = k["launches_per_step"]
-    if name == "radix_downsweep":
-        # one pass reads and writes (key, value) of every pair: 16 B per pair
-        byts = 16.0 * n_pairs
-        ach = byts / avg_s / 1e9
-        return {"bound": "hbm", "kernel": name, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBS, "traffic": None, "bytes_per_launch": byts, "avg_us": avg_s * 1e6}
-    if name == "emit":
-        byts = 8.0 * n_pairs
-        ach = byts / avg_s / 1e9
-        return {"bound": "hbm", "kernel": name, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBS, "traffic": None, "bytes_per_launch": byts, "avg_us": avg_s * 1e6}
-    return {"bound": "unknown", "kernel": name, "avg_us": avg_s * 1e6, "launches_per_step": per_step}
+    out = {"kernel": name, "avg_us": avg_s * 1e6, "launches_per_step": k["launches_per_step"]}
+    traffic = measured_traffic(name)
+    if name in FLOPS_PER_PAIR:
+        # units: contributing pairs of the batch, from the oracle's count on the
+        # CPU-baseline sample (None without it)
+        if contrib_per_point is None:
+            out.update({"bound": "alu", "achieved": None, "peak": FP32_VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": None, "traffic": traffic})
+            return out
+        units = contrib_per_point * st.n
+        flops = FLOPS_PER_PAIR[name] * units
+        ach = flops / avg_s / 1e12
+        out.update({"bound": "alu", "achieved": ach, "peak": FP32_VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": ach / FP32_VEC_PEAK_TFLOPS, "traffic": traffic,
+                    "flops_per_launch": flops, "contributing_pairs": units})
+        return out
+    per_pair = {"radix_downsweep": SORT_BYTES_PER_PAIR, "emit": EMIT_BYTES_PER_PAIR}.get(name)
+    if per_pair is None:
+        out.update({"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": None,
+                    "traffic": traffic})
+        return out
+    byts = per_pair * n_pairs
+    ach = byts / avg_s / 1e9
+    out.update({"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+                "traffic": traffic, "bytes_per_launch": byts})
+    return out
 
 
 if __name__ == "__main__":

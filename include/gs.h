@@ -149,8 +149,9 @@ size_t gs_plan_bytes(const gs_query *query, const gs_grid *grid);
  * unstructured points): writes out_value[t] = Phi and out_influence[t] = I
  * for every query t, (0, 0) where undefined. gauss must be the Gaussians the
  * index was built from, unchanged. For VOXELS and POINTS queries, plan
- * receives the query ordering that gs_sample_backward reuses (the paper
- * reuses its sample BVH the same way, Sec. 5.1.2); GRID queries need none.
+ * receives the query ordering and, in that order, each query's position and
+ * (Phi, I), which gs_sample_backward reuses (the paper reuses its sample BVH
+ * the same way, Sec. 5.1.2); GRID queries need none.
  * Deterministic: the same inputs give bit-identical outputs.
  */
 gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
@@ -168,8 +169,11 @@ size_t gs_backward_work_bytes(const gs_index *index, const gs_query *query);
  * d_mean [n][3], d_scale [n][3], d_rot [n][4] (w.r.t. the raw quaternion),
  * d_value [n], d_weight [n]. Undefined queries carry no gradient. The
  * intersecting sets are those of the forward pass (the result is the exact
- * derivative of the smooth piece). Per-Gaussian sums are accumulated with
- * floating-point atomics, so the last bits may differ between runs.
+ * derivative of the smooth piece). For VOXELS and POINTS queries the
+ * forward outputs are read from the copy gs_sample left in the plan, so
+ * value and influence must be that call's outputs (they are read as given
+ * for GRID queries). Every per-Gaussian sum is formed by one wavefront in a
+ * fixed order, without atomics: the same inputs give bit-identical results.
  */
 gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
                              const void *plan, size_t plan_bytes, const float *value, const float *influence,
@@ -190,9 +194,12 @@ int gs_version(void);
  * names (pointers into static storage), launch counts and summed durations
  * in milliseconds; the return value is the number of distinct kernels seen.
  * gs_profile_enable(0) stops recording; gs_profile_reset() clears the
- * records. Not thread-safe; meant for one measuring thread.
+ * records. gs_profile_select(name) limits the recording to the kernel of
+ * that name (the names gs_profile_read reports); NULL records every kernel.
+ * The name is copied. Not thread-safe; meant for one measuring thread.
  */
 void gs_profile_enable(int on);
+void gs_profile_select(const char *name);
 void gs_profile_reset(void);
 int gs_profile_read(const char **names, int64_t *counts, double *total_ms, int max_entries);
 

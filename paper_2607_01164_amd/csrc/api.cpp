@@ -157,6 +157,7 @@ struct Plan {
     uint32_t *point_off; // [ncells + 2]
     void *radix_work;
     PointItems items;
+    PlanResults res;
     size_t bytes;
 };
 
@@ -174,6 +175,8 @@ Plan plan_layout(void *base, int64_t n, int64_t ncells) {
     p.items.max_items = ncells + 1 + (n > 0 ? n : 0) / 64 + 1;
     p.items.items = c.take<uint32_t>((size_t)p.items.max_items);
     p.items.scan_work = c.take<char>(scan_work_bytes(ncells + 2, 4));
+    p.res.pos = c.take<float4>(m);
+    p.res.out = c.take<float2>(m);
     p.bytes = c.off;
     return p;
 }
@@ -273,15 +276,8 @@ BwdWork bwd_layout(void *base, const gs_index *index, const gs_query *q) {
     const int64_t nq = query_count(q);
     const size_t mq = (size_t)(nq > 0 ? nq : 1);
     w.b.moments = c.take<float>((size_t)(n > 0 ? n : 1) * 12);
-    if (q->kind == GS_QUERY_GRID) {
-        w.b.pts = nullptr;
-        w.b.alpha = c.take<float>(mq);
-        w.b.beta = c.take<float>(mq);
-    } else {
-        w.b.pts = c.take<float4>(mq);
-        w.b.beta = c.take<float>(mq);
-        w.b.alpha = nullptr;
-    }
+    (void)q;
+    w.b.ab = c.take<float2>(mq);
     w.bytes = c.off;
     return w;
 }
@@ -299,6 +295,7 @@ struct ProfAgg {
     double ms;
 };
 bool g_prof_on = false;
+std::string g_prof_only;             // record only this kernel when non-empty
 std::vector<ProfRec> g_prof_open;   // begun, not yet ended
 std::vector<ProfRec> g_prof_done;   // ended, not yet read
 std::vector<hipEvent_t> g_prof_pool;
@@ -341,6 +338,7 @@ namespace gs {
 
 void prof_begin(const char *name, hipStream_t s) {
     if (!g_prof_on) return;
+    if (!g_prof_only.empty() && g_prof_only != name) return;
     hipEvent_t a = prof_event();
     if (!a) return;
     (void)hipEventRecord(a, s);
@@ -375,6 +373,8 @@ const char *gs_last_error(void) { return g_err.c_str(); }
 int gs_version(void) { return 100; }
 
 void gs_profile_enable(int on) { g_prof_on = on != 0; }
+
+void gs_profile_select(const char *name) { g_prof_only = name ? name : ""; }
 
 void gs_profile_reset(void) {
     prof_collect();
@@ -532,7 +532,7 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
     GS_TRY(radix_sort_pairs(ek, ev, ak, av, nq, bits, p.radix_work, stream, true), "gs_sample: query sort");
     GS_TRY(key_offsets(p.keys, nq, p.point_off, gp.ncells + 1, stream), "gs_sample: query ranges");
     GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
-                                index->tau, out_value, out_influence, stream),
+                                index->tau, out_value, out_influence, p.res, stream),
            "gs_sample: point sampler");
     return GS_OK;
 }
@@ -572,7 +572,8 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
     }
     IndexWork w = index_layout(index->work, n, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
-    GS_TRY(launch_backward(qp, gp, w.rec, w.box, w.gorder, n, p.keys, p.order, p.point_off, value, influence, grad_value,
+    GS_TRY(launch_backward(qp, gp, w.rec, w.box, w.gorder, n, p.order, p.point_off, p.res.pos, p.res.out, value,
+                           influence, grad_value,
                            grad_influence, cutoff_T(index->tau), bw.b, gauss->mean, gauss->scale, gauss->rot, d_mean,
                            d_scale, d_rot, d_value, d_weight, stream),
            "gs_sample_backward");

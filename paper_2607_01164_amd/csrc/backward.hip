@@ -10,12 +10,14 @@
 //
 // The points of a box come as rows: a run of cells along x at fixed (y, z)
 // is contiguous in the plan's cell ordering (for grids, a run of voxels is
-// contiguous in the x-fastest layout). The wave splits into groups of W
-// lanes, W chosen from the mean row length of the Gaussian; each group walks
-// one row with W consecutive lanes, so every load instruction reads a few
-// whole cache lines. Gaussians are visited in the spatial order of the
-// index (the cell key of their box corner), so the waves resident at one
-// time work on one region and find its points in L2.
+// contiguous in the x-fastest layout). The wave concatenates up to 64 rows
+// and walks them 64 elements per step, so the lanes stay busy across row
+// ends and every load reads whole cache lines. Most tested pairs fail the
+// cutoff; the ones that pass are queued in LDS and processed 64 at a time,
+// so the longer per-pair work runs with every lane busy. Gaussians are
+// visited in the spatial order of the index (the cell key of their box
+// corner), so the waves resident at one time work on one region and find
+// its points in L2.
 //
 // Per pair the partials are kept as 11 moments in the Gaussian's whitened
 // frame u = M (p - mu), M = S^-1 R^T, with c = dL/dQ = -1/2 a dL/da:
@@ -37,15 +39,6 @@ namespace {
 
 constexpr float kNegHalfLog2e = -0.72134752044448170368f;
 
-__device__ __forceinline__ void voxel_pos(uint32_t id, const QueryParams &q, const GridParams &g, float &px, float &py,
-                                          float &pz) {
-    const uint32_t nx = (uint32_t)q.dims[0], ny = (uint32_t)q.dims[1];
-    const uint32_t x = id % nx, t = id / nx, y = t % ny, z = t / ny;
-    px = g.lo[0] + ((float)x + 0.5f) * q.vsz[0];
-    py = g.lo[1] + ((float)y + 0.5f) * q.vsz[1];
-    pz = g.lo[2] + ((float)z + 0.5f) * q.vsz[2];
-}
-
 __device__ __forceinline__ void alpha_beta(float phi, float inf, float gp, float gi, float &al, float &be) {
     // the forward writes I > tau > 0 at defined points and exactly 0 elsewhere
     if (inf > 0.0f) {
@@ -57,45 +50,33 @@ __device__ __forceinline__ void alpha_beta(float phi, float inf, float gp, float
     }
 }
 
-// Cotangent staging for ordered queries: pts[k] = (x, y, z, alpha) and
-// beta[k] of the k-th query in the plan's cell order.
-__global__ __launch_bounds__(kBlock) void k_stage_points(QueryParams q, GridParams g,
-                                                         const uint32_t *__restrict__ sorted_keys,
-                                                         const uint32_t *__restrict__ order,
-                                                         const float *__restrict__ value,
-                                                         const float *__restrict__ influence,
+// Cotangent staging for ordered queries: (alpha, beta) of the k-th
+// query in plan order, from the forward's (Phi, I) that the plan keeps in
+// that order; only the cotangents are gathered by query id.
+__global__ __launch_bounds__(kBlock) void k_stage_points(int64_t n, const uint32_t *__restrict__ order,
+                                                         const float2 *__restrict__ plan_out,
                                                          const float *__restrict__ gval, const float *__restrict__ ginf,
-                                                         float4 *__restrict__ pts, float *__restrict__ beta) {
+                                                         float2 *__restrict__ ab) {
     const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= q.n) return;
-    const uint32_t key = sorted_keys[k];
-    const uint32_t pid = order[k];
-    float px = 0.0f, py = 0.0f, pz = 0.0f, al = 0.0f, be = 0.0f;
-    if (key < (uint32_t)g.ncells && (int64_t)pid < q.n) {
-        if (q.kind == 1) {
-            voxel_pos(q.voxel_ids[pid], q, g, px, py, pz);
-        } else {
-            px = q.points[3 * (uint64_t)pid];
-            py = q.points[3 * (uint64_t)pid + 1];
-            pz = q.points[3 * (uint64_t)pid + 2];
-        }
-        alpha_beta(value[pid], influence[pid], gval[pid], ginf[pid], al, be);
+    if (k >= n) return;
+    const float2 o = plan_out[k];
+    float al = 0.0f, be = 0.0f;
+    if (o.y > 0.0f) {
+        const uint32_t pid = order[k];
+        alpha_beta(o.x, o.y, gval[pid], ginf[pid], al, be);
     }
-    pts[k] = make_float4(px, py, pz, al);
-    beta[k] = be;
+    ab[k] = make_float2(al, be);
 }
 
 __global__ __launch_bounds__(kBlock) void k_stage_grid(int64_t n, const float *__restrict__ value,
                                                        const float *__restrict__ influence,
                                                        const float *__restrict__ gval,
-                                                       const float *__restrict__ ginf, float *__restrict__ alpha,
-                                                       float *__restrict__ beta) {
+                                                       const float *__restrict__ ginf, float2 *__restrict__ ab) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
     float al, be;
     alpha_beta(value[i], influence[i], gval[i], ginf[i], al, be);
-    alpha[i] = al;
-    beta[i] = be;
+    ab[i] = make_float2(al, be);
 }
 
 struct Acc {
@@ -104,54 +85,108 @@ struct Acc {
     float dv, dw;
 };
 
-__device__ __forceinline__ void pair_grad(const Record &r, float px, float py, float pz, float al, float be, float T,
-                                          Acc &acc) {
+// Whitened offset u = M (p - mu) and Q = |u|^2 (paper Eq. 1 and 3).
+__device__ __forceinline__ float whiten(const Record &r, float px, float py, float pz, float &u0, float &u1,
+                                        float &u2) {
     const float dx = px - r.r0.x, dy = py - r.r0.y, dz = pz - r.r0.z;
-    const float u0 = fmaf_(r.r1.x, dx, fmaf_(r.r1.y, dy, r.r1.z * dz));
-    const float u1 = fmaf_(r.r2.x, dx, fmaf_(r.r2.y, dy, r.r2.z * dz));
-    const float u2 = fmaf_(r.r3.x, dx, fmaf_(r.r3.y, dy, r.r3.z * dz));
-    const float Q = fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
-    if (Q <= T) {
-        const float G = exp2_hw(Q * kNegHalfLog2e);
-        const float a = r.r0.w * G;
-        const float dLda = fmaf_(al, r.r1.w, be);
-        acc.dv = fmaf_(al, a, acc.dv);
-        acc.dw = fmaf_(dLda, G, acc.dw);
-        const float c = -0.5f * a * dLda;
-        const float c0 = c * u0, c1 = c * u1, c2 = c * u2;
-        acc.m1[0] += c0;
-        acc.m1[1] += c1;
-        acc.m1[2] += c2;
-        acc.m2[0] = fmaf_(c0, u0, acc.m2[0]);
-        acc.m2[1] = fmaf_(c0, u1, acc.m2[1]);
-        acc.m2[2] = fmaf_(c0, u2, acc.m2[2]);
-        acc.m2[3] = fmaf_(c1, u1, acc.m2[3]);
-        acc.m2[4] = fmaf_(c1, u2, acc.m2[4]);
-        acc.m2[5] = fmaf_(c2, u2, acc.m2[5]);
+    u0 = fmaf_(r.r1.x, dx, fmaf_(r.r1.y, dy, r.r1.z * dz));
+    u1 = fmaf_(r.r2.x, dx, fmaf_(r.r2.y, dy, r.r2.z * dz));
+    u2 = fmaf_(r.r3.x, dx, fmaf_(r.r3.y, dy, r.r3.z * dz));
+    return fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
+}
+
+// Partials of one contributing pair (Q <= T), given u, Q and the query's
+// alpha, beta.
+__device__ __forceinline__ void pair_grad(const Record &r, float u0, float u1, float u2, float Q, float al, float be,
+                                          Acc &acc) {
+    const float G = exp2_hw(Q * kNegHalfLog2e);
+    const float a = r.r0.w * G;
+    const float dLda = fmaf_(al, r.r1.w, be);
+    acc.dv = fmaf_(al, a, acc.dv);
+    acc.dw = fmaf_(dLda, G, acc.dw);
+    const float c = -0.5f * a * dLda;
+    const float c0 = c * u0, c1 = c * u1, c2 = c * u2;
+    acc.m1[0] += c0;
+    acc.m1[1] += c1;
+    acc.m1[2] += c2;
+    acc.m2[0] = fmaf_(c0, u0, acc.m2[0]);
+    acc.m2[1] = fmaf_(c0, u1, acc.m2[1]);
+    acc.m2[2] = fmaf_(c0, u2, acc.m2[2]);
+    acc.m2[3] = fmaf_(c1, u1, acc.m2[3]);
+    acc.m2[4] = fmaf_(c1, u2, acc.m2[4]);
+    acc.m2[5] = fmaf_(c2, u2, acc.m2[5]);
+}
+
+// One step of a transposed reduction: the lane keeps one of (lo, hi) by its
+// lane bit and adds the partner's copy of the same element; the partner
+// (reached with DPP control CTRL) differs from the lane in that bit.
+template <int CTRL>
+__device__ __forceinline__ float tr_step(float lo, float hi, bool bit) {
+    const float keep = bit ? hi : lo, send = bit ? lo : hi;
+    return keep + dpp_f<CTRL>(send);
+}
+
+// Sum of 11 per-lane values over the wave; lane k < 11 returns total k
+// (lanes 11..15 return 0). Four transposed steps inside each row of 16
+// (lane bits 0, 1, 2, 3 through quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_ror:4, row_ror:8) leave lane l holding element l & 15 summed over its
+// row; two xor shuffles then add the four rows.
+__device__ __forceinline__ float reduce11(const float v[11], uint32_t lane) {
+    const bool b0 = lane & 1u, b1 = lane & 2u, b2 = lane & 4u, b3 = lane & 8u;
+    float w[6];
+#pragma unroll
+    for (int i = 0; i < 5; ++i) w[i] = tr_step<0xB1>(v[2 * i], v[2 * i + 1], b0);
+    w[5] = tr_step<0xB1>(v[10], 0.0f, b0);
+    float x[3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) x[j] = tr_step<0x4E>(w[2 * j], w[2 * j + 1], b1);
+    const float y0 = tr_step<0x124>(x[0], x[1], b2);
+    const float y1 = tr_step<0x124>(x[2], 0.0f, b2);
+    float z = tr_step<0x128>(y0, y1, b3);
+    z += __shfl_xor(z, 16, 64);
+    z += __shfl_xor(z, 32, 64);
+    return z;
+}
+
+// Queue of contributing pairs of one wave: (u0, u1, u2, Q) and the point.
+constexpr uint32_t kQueue = 2 * kWave;
+
+__device__ __forceinline__ void drain(const Record &r, const float4 *qu, const uint32_t *qk, uint32_t head,
+                                      uint32_t cnt, uint32_t lane, const float2 *__restrict__ ab, Acc &acc) {
+    if (lane < cnt) {
+        const uint32_t slot = (head + lane) & (kQueue - 1);
+        const float4 e = qu[slot];
+        const float2 c = ab[qk[slot]];
+        pair_grad(r, e.x, e.y, e.z, e.w, c.x, c.y, acc);
     }
 }
 
-__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
-    return __builtin_amdgcn_readlane(wave_incl_sum(x), 63);
-}
-
-// lanes per row group for a mean row length
-__device__ __forceinline__ uint32_t group_width(uint32_t mean_len) {
-    return mean_len <= 4 ? 4u : mean_len <= 8 ? 8u : mean_len <= 20 ? 16u : mean_len <= 40 ? 32u : 64u;
-}
-
+// One wavefront per Gaussian, visited in gorder. The points of the box are
+// taken as rows (a row is a run of consecutive elements: the queries of the
+// cells lo.x..hi.x at one (y, z) in plan order, or one x-run of voxels of a
+// grid), up to 64 rows at a time with lane r describing row r. The rows are
+// concatenated and walked 64 elements per step, lane l taking element
+// e0 + l, so the lanes stay busy across row ends; a lane finds its row by
+// comparing e with the row ends inside the step's window (uniform values,
+// read with readlane). The cutoff test is all a non-contributing pair
+// costs; contributing pairs go to a per-wave LDS queue, and every 64 queued
+// pairs are processed with all lanes busy.
 template <bool GRID>
 __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                            const CellBox *__restrict__ box,
                                                            const uint32_t *__restrict__ gorder, int64_t n_gauss,
                                                            const uint32_t *__restrict__ point_off,
-                                                           const float4 *__restrict__ pts,
-                                                           const float *__restrict__ alpha,
-                                                           const float *__restrict__ beta, float T,
+                                                           const float4 *__restrict__ plan_pos,
+                                                           const float2 *__restrict__ ab, float T,
                                                            float *__restrict__ moments) {
+    __shared__ float4 s_qu[kWavesPerBlock][kQueue];
+    __shared__ uint32_t s_qk[kWavesPerBlock][kQueue];
     const uint32_t lane = threadIdx.x % kWave;
-    const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave;
+    const uint32_t wib = threadIdx.x / kWave;
+    const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + wib;
     if (w >= (uint64_t)n_gauss) return;
+    float4 *qu = s_qu[wib];
+    uint32_t *qk = s_qk[wib];
     const uint32_t gid = __builtin_amdgcn_readfirstlane(((ConstU32 *)gorder)[w]);
     const CellBox b = load_box_uniform(box, gid);
     const Record r = load_record_uniform(rec, gid);
@@ -161,6 +196,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
 #pragma unroll
     for (int k = 0; k < 6; ++k) acc.m2[k] = 0.0f;
     acc.dv = acc.dw = 0.0f;
+    uint32_t head = 0, cnt = 0;
     if (b.hi.x >= b.lo.x) {
         const uint32_t nx = (uint32_t)(b.hi.x - b.lo.x + 1), ny = (uint32_t)(b.hi.y - b.lo.y + 1),
                        nz = (uint32_t)(b.hi.z - b.lo.z + 1);
@@ -175,15 +211,16 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
         for (uint32_t rb = 0; rb < R; rb += kWave) {
             // lane l describes row rb + l: its first element and its length
             const uint32_t row = rb + lane;
-            uint32_t start = 0, len = 0, ry_ = 0, rz_ = 0;
+            uint32_t start = 0, len = 0;
+            float rpy = 0.0f, rpz = 0.0f;
             if (row < R) {
                 const uint32_t yy = row % nry, zz = row / nry;
                 if (GRID) {
                     const uint32_t vy = (uint32_t)b.lo.y * ry + yy, vz = (uint32_t)b.lo.z * rz + zz;
                     start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + vx0;
                     len = nx * rx;
-                    ry_ = vy;
-                    rz_ = vz;
+                    rpy = g.lo[1] + ((float)vy + 0.5f) * q.vsz[1];
+                    rpz = g.lo[2] + ((float)vz + 0.5f) * q.vsz[2];
                 } else {
                     const uint32_t cy = (uint32_t)b.lo.y + yy, cz = (uint32_t)b.lo.z + zz;
                     const uint32_t kbase = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz);
@@ -192,48 +229,78 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                 }
             }
             const uint32_t nrows = (R - rb) < (uint32_t)kWave ? (R - rb) : (uint32_t)kWave;
-            const uint32_t W = group_width((wave_sum_u32(len) + nrows - 1) / nrows);
-            const uint32_t G = kWave / W;
-            const uint32_t grp = lane / W, t = lane % W;
-            for (uint32_t rr = 0; rr < nrows; rr += G) {
-                // every lane takes part in the shuffles (a lane reading from an
-                // inactive lane would get 0); rows past the end have length 0
-                const uint32_t my = rr + grp;
-                const uint32_t s_start = __shfl(start, (int)my, 64);
-                const uint32_t s_len = __shfl(len, (int)my, 64);
+            const uint32_t incl = wave_incl_sum(len);  // end of row l in the concatenation
+            const uint32_t E = __builtin_amdgcn_readlane(incl, 63);
+            const uint32_t kofs = start - (incl - len);  // element e of row l is point e + kofs
+            const uint32_t xofs = vx0 - (incl - len);    // grids: element e of row l has x = e + xofs
+            if (E == 0) continue;  // no query in these rows
+            uint32_t j0 = 0;       // first row not finished before the window
+            for (uint32_t e0 = 0; e0 < E; e0 += kWave) {
+                // e0 < E, so the row holding element e0 is below nrows
+                while (j0 + 1 < nrows && __builtin_amdgcn_readlane(incl, j0) <= e0) ++j0;
+                const uint32_t e = e0 + lane;
+                uint32_t j = j0;
+                uint32_t ko = __builtin_amdgcn_readlane(kofs, j), xo = 0;
+                float py = 0.0f, pz = 0.0f;
                 if (GRID) {
-                    const uint32_t s_y = __shfl(ry_, (int)my, 64), s_z = __shfl(rz_, (int)my, 64);
-                    const float py = g.lo[1] + ((float)s_y + 0.5f) * q.vsz[1];
-                    const float pz = g.lo[2] + ((float)s_z + 0.5f) * q.vsz[2];
-                    for (uint32_t c = t; c < s_len; c += W) {
-                        const float px = g.lo[0] + ((float)(vx0 + c) + 0.5f) * q.vsz[0];
-                        pair_grad(r, px, py, pz, alpha[s_start + c], beta[s_start + c], T, acc);
+                    xo = __builtin_amdgcn_readlane(xofs, j);
+                    py = readlane_f(rpy, j);
+                    pz = readlane_f(rpz, j);
+                }
+                // row ends inside the window move the later lanes on
+                while (j + 1 < nrows) {
+                    const uint32_t bnd = __builtin_amdgcn_readlane(incl, j);
+                    if (bnd >= e0 + kWave) break;
+                    const bool nxt = e >= bnd;
+                    ++j;
+                    ko = nxt ? __builtin_amdgcn_readlane(kofs, j) : ko;
+                    if (GRID) {
+                        xo = nxt ? __builtin_amdgcn_readlane(xofs, j) : xo;
+                        py = nxt ? readlane_f(rpy, j) : py;
+                        pz = nxt ? readlane_f(rpz, j) : pz;
                     }
-                } else {
-                    for (uint32_t c = t; c < s_len; c += W) {
-                        const float4 p = pts[s_start + c];
-                        pair_grad(r, p.x, p.y, p.z, p.w, beta[s_start + c], T, acc);
+                }
+                const bool valid = e < E;
+                const uint32_t k = e + ko;
+                float u0 = 0.0f, u1 = 0.0f, u2 = 0.0f, Q = 0.0f;
+                if (valid) {
+                    if (GRID) {
+                        const float px = g.lo[0] + ((float)(e + xo) + 0.5f) * q.vsz[0];
+                        Q = whiten(r, px, py, pz, u0, u1, u2);
+                    } else {
+                        const float4 p = plan_pos[k];
+                        Q = whiten(r, p.x, p.y, p.z, u0, u1, u2);
                     }
+                }
+                const bool hit = valid && Q <= T;
+                const uint64_t mask = __ballot(hit);
+                if (mask == 0) continue;
+                if (hit) {
+                    const uint32_t pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                    const uint32_t slot = (head + cnt + pos) & (kQueue - 1);
+                    qu[slot] = make_float4(u0, u1, u2, Q);
+                    qk[slot] = k;
+                }
+                cnt += (uint32_t)__popcll(mask);
+                if (cnt >= (uint32_t)kWave) {
+                    __builtin_amdgcn_wave_barrier();
+                    drain(r, qu, qk, head, kWave, lane, ab, acc);
+                    __builtin_amdgcn_wave_barrier();
+                    head = (head + kWave) & (kQueue - 1);
+                    cnt -= kWave;
                 }
             }
         }
     }
-    float v[11] = {acc.m1[0], acc.m1[1], acc.m1[2], acc.m2[0], acc.m2[1], acc.m2[2],
-                   acc.m2[3], acc.m2[4], acc.m2[5], acc.dv,    acc.dw};
-#pragma unroll
-    for (int k = 0; k < 11; ++k) {
-        const float rsum = row16_sum(v[k]);
-        v[k] = (__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rsum), 0)) +
-                __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rsum), 16))) +
-               (__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rsum), 32)) +
-                __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rsum), 48)));
+    if (cnt > 0) {
+        __builtin_amdgcn_wave_barrier();
+        drain(r, qu, qk, head, cnt, lane, ab, acc);
     }
-    if (lane == 0) {
-        float4 *m = (float4 *)(moments + (size_t)gid * 12);
-        m[0] = make_float4(v[0], v[1], v[2], v[3]);
-        m[1] = make_float4(v[4], v[5], v[6], v[7]);
-        m[2] = make_float4(v[8], v[9], v[10], 0.0f);
-    }
+    const float v[11] = {acc.m1[0], acc.m1[1], acc.m1[2], acc.m2[0], acc.m2[1], acc.m2[2],
+                         acc.m2[3], acc.m2[4], acc.m2[5], acc.dv,    acc.dw};
+    const float tot = reduce11(v, lane);
+    if (lane < 12) moments[(size_t)gid * 12 + lane] = tot;
 }
 
 __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ moments, int64_t n,
@@ -309,8 +376,8 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
 }  // namespace
 
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
-                           const uint32_t *gorder, int64_t n_gauss, const uint32_t *sorted_keys, const uint32_t *order,
-                           const uint32_t *point_off, const float *value, const float *influence,
+                           const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
+                           const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
                            float *d_mean, float *d_scale, float *d_rot, float *d_value, float *d_weight,
@@ -325,20 +392,20 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
         prof_begin("bwd_stage", s);
         if (grid)
             hipLaunchKernelGGL(k_stage_grid, dim3(qblocks), dim3(kBlock), 0, s, q.n, value, influence, grad_value,
-                               grad_influence, b.alpha, b.beta);
+                               grad_influence, b.ab);
         else
-            hipLaunchKernelGGL(k_stage_points, dim3(qblocks), dim3(kBlock), 0, s, q, g, sorted_keys, order, value,
-                               influence, grad_value, grad_influence, b.pts, b.beta);
+            hipLaunchKernelGGL(k_stage_points, dim3(qblocks), dim3(kBlock), 0, s, q.n, order, plan_out, grad_value,
+                               grad_influence, b.ab);
         prof_end("bwd_stage", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         const uint32_t wblocks = (uint32_t)((n_gauss + kWavesPerBlock - 1) / kWavesPerBlock);
         prof_begin("bwd_gauss", s);
         if (grid)
             hipLaunchKernelGGL(k_backward_gauss<true>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, gorder,
-                               n_gauss, point_off, b.pts, b.alpha, b.beta, T, b.moments);
+                               n_gauss, point_off, plan_pos, b.ab, T, b.moments);
         else
             hipLaunchKernelGGL(k_backward_gauss<false>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, gorder,
-                               n_gauss, point_off, b.pts, b.alpha, b.beta, T, b.moments);
+                               n_gauss, point_off, plan_pos, b.ab, T, b.moments);
         prof_end("bwd_gauss", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {

@@ -87,6 +87,37 @@ __device__ __forceinline__ float row16_sum(float x) {
     return x;
 }
 
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ float readlane_f(float x, uint32_t l) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), (int)l));
+}
+
+// Wave-uniform sum and maximum of a 32-bit value (every lane must be active):
+// DPP within each row of 16 lanes, then the four row results by readlane.
+__device__ __forceinline__ uint32_t wave_sum_uniform(uint32_t x) {
+    x += dpp_u<0xB1>(x);
+    x += dpp_u<0x4E>(x);
+    x += dpp_u<0x124>(x);
+    x += dpp_u<0x128>(x);
+    return (__builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16)) +
+           (__builtin_amdgcn_readlane(x, 32) + __builtin_amdgcn_readlane(x, 48));
+}
+
+__device__ __forceinline__ uint32_t umax_(uint32_t a, uint32_t b) { return a > b ? a : b; }
+
+__device__ __forceinline__ uint32_t wave_max_uniform(uint32_t x) {
+    x = umax_(x, dpp_u<0xB1>(x));
+    x = umax_(x, dpp_u<0x4E>(x));
+    x = umax_(x, dpp_u<0x124>(x));
+    x = umax_(x, dpp_u<0x128>(x));
+    return umax_(umax_(__builtin_amdgcn_readlane(x, 0), __builtin_amdgcn_readlane(x, 16)),
+                 umax_(__builtin_amdgcn_readlane(x, 32), __builtin_amdgcn_readlane(x, 48)));
+}
+
 // Inclusive scan of a 32-bit value across the 64 lanes of a wave (sum or max).
 __device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x) {
     const uint32_t lane = lane_id();
@@ -207,10 +238,17 @@ struct PointItems {
     int64_t max_items;   // ncells + 1 + n / 64 + 1
     void *scan_work;
 };
+// The forward's results in plan order, kept in the plan for the backward:
+// position (x, y, z, 0) and (Phi, I) of the k-th query in cell order.
+struct PlanResults {
+    float4 *pos;
+    float2 *out;
+};
+
 hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                                 const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
-                                hipStream_t s);
+                                const PlanResults &pr, hipStream_t s);
 
 // Gaussians in spatial order: sorted by the cell key of their box's low
 // corner (empty boxes last), so neighbouring work shares cached queries.
@@ -220,13 +258,11 @@ hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g,
 // Backward (backward.hip).
 struct BackwardBuffers {
     float *moments;        // [n_gauss][12]
-    float4 *pts;           // POINTS/VOXELS: [n] (x, y, z, alpha) in plan order
-    float *beta;           // POINTS/VOXELS: [n]; GRID: [n] beta in voxel order
-    float *alpha;          // GRID: [n] alpha in voxel order
+    float2 *ab;            // [n] (alpha, beta) per query: plan order (points, voxels) or voxel order (grid)
 };
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
-                           const uint32_t *gorder, int64_t n_gauss, const uint32_t *sorted_keys, const uint32_t *order,
-                           const uint32_t *point_off, const float *value, const float *influence,
+                           const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
+                           const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
                            float *d_mean, float *d_scale, float *d_rot, float *d_value, float *d_weight,

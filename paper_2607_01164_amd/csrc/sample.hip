@@ -159,6 +159,8 @@ __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams
 // queries outside the domain (key ncells) is an item with an empty list.
 constexpr uint32_t kDenseMin = 32;
 constexpr uint32_t kChunkB = 8;  // queries evaluated together by a sparse-cell item
+constexpr uint32_t kRowsMin = 4;                 // from this many queries a cell uses 4 query rows
+constexpr uint32_t kRowsMax = (kDenseMin + 3) / 4;  // queries per row at most
 
 __global__ __launch_bounds__(kBlock) void k_cell_items(const uint32_t *__restrict__ point_off, int64_t nbuckets,
                                                        uint32_t *__restrict__ item_off) {
@@ -195,21 +197,22 @@ __device__ __forceinline__ float eval_a(const Record &r, float px, float py, flo
     return Q <= T ? r.r0.w * exp2_hw(Q * kNegHalfLog2e) : 0.0f;
 }
 
-__device__ __forceinline__ float readlane_f(float x, uint32_t l) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), (int)l));
-}
-
 // sum over the 64 lanes, returned to every lane
 __device__ __forceinline__ float wave_total(float x) {
     const float r = row16_sum(x);
     return (readlane_f(r, 0) + readlane_f(r, 16)) + (readlane_f(r, 32) + readlane_f(r, 48));
 }
 
-__device__ __forceinline__ void write_out(float I, float V, float tau, bool work, uint32_t pid, float *out_v,
-                                          float *out_i) {
+// Outputs of one query: (Phi, I) at its id in query order, and its position
+// and (Phi, I) at its index k in plan order for the backward.
+__device__ __forceinline__ void write_out(float I, float V, float tau, bool work, uint32_t pid, uint32_t k, float px,
+                                          float py, float pz, float *out_v, float *out_i, const PlanResults &pr) {
     const bool def = work && I > tau;
-    out_v[pid] = def ? V / I : 0.0f;
-    out_i[pid] = def ? I : 0.0f;
+    const float phi = def ? V / I : 0.0f, inf = def ? I : 0.0f;
+    out_v[pid] = phi;
+    out_i[pid] = inf;
+    pr.pos[k] = make_float4(px, py, pz, 0.0f);
+    pr.out[k] = make_float2(phi, inf);
 }
 
 // One wavefront per item. Dense cells: lanes are queries of the cell and
@@ -226,7 +229,7 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
                                                          const uint32_t *__restrict__ item_off,
                                                          const uint32_t *__restrict__ items, int64_t max_items,
                                                          float T, float tau, float *__restrict__ out_v,
-                                                         float *__restrict__ out_i) {
+                                                         float *__restrict__ out_i, PlanResults pr) {
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t ncells = (uint32_t)g.ncells;
     const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave;
@@ -254,7 +257,71 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
         }
         float I = 0.0f, V = 0.0f;
         walk_uniform(rec, gids, ja, jb, px, py, pz, T, I, V);
-        if (active && (int64_t)pid < q.n) write_out(I, V, tau, valid && c < ncells, pid, out_v, out_i);
+        if (active && (int64_t)pid < q.n)
+            write_out(I, V, tau, valid && c < ncells, pid, k, px, py, pz, out_v, out_i, pr);
+        return;
+    }
+    if (n >= kRowsMin) {
+        // 4 query rows x 16 candidate slots: lane (r, s) evaluates queries
+        // r, r + 4, r + 8, ... against candidates s, s + 16, ... of the list;
+        // a query's partial sums are then summed over its row with DPP.
+        const uint32_t row = lane >> 4, sl = lane & 15u;
+        const uint32_t nt = (n + 3) >> 2;  // queries per row, <= kRowsMax
+        uint32_t pid = 0;
+        float mx = 0.0f, my = 0.0f, mz = 0.0f;
+        bool valid = false;
+        if (lane < n) {
+            pid = order[pa + lane];
+            if ((int64_t)pid < q.n) query_position(q, g, pid, mx, my, mz, valid);
+        }
+        float px[kRowsMax], py[kRowsMax], pz[kRowsMax], Ip[kRowsMax], Vp[kRowsMax];
+#pragma unroll
+        for (uint32_t t = 0; t < kRowsMax; ++t) {
+            px[t] = py[t] = pz[t] = 0.0f;
+            Ip[t] = Vp[t] = 0.0f;
+            if (t < nt) {
+                const int src = (int)(row + 4u * t);
+                px[t] = __shfl(mx, src, 64);
+                py[t] = __shfl(my, src, 64);
+                pz[t] = __shfl(mz, src, 64);
+            }
+        }
+        for (uint32_t j0 = ja; j0 < jb; j0 += 16) {
+            const uint32_t j = j0 + sl;
+            Record r;
+            if (j < jb) {
+                r = rec[gids[j]];
+            } else {
+                r.r0 = r.r1 = r.r2 = r.r3 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+#pragma unroll
+            for (uint32_t t = 0; t < kRowsMax; ++t) {
+                if (t < nt) {
+                    const float a = eval_a(r, px[t], py[t], pz[t], T);
+                    Ip[t] += a;
+                    Vp[t] = fmaf_(a, r.r1.w, Vp[t]);
+                }
+            }
+        }
+        float Io = 0.0f, Vo = 0.0f;
+#pragma unroll
+        for (uint32_t t = 0; t < kRowsMax; ++t) {
+            if (t < nt) {
+                const float It = row16_sum(Ip[t]), Vt = row16_sum(Vp[t]);
+                if (sl == t) {
+                    Io = It;
+                    Vo = Vt;
+                }
+            }
+        }
+        // lane (r, t) writes query r + 4 t, whose id and position lane r + 4 t holds
+        const uint32_t qi = row + 4u * sl;
+        const int src = (int)(qi & 63u);
+        const uint32_t wpid = __shfl(pid, src, 64);
+        const float wx = __shfl(mx, src, 64), wy = __shfl(my, src, 64), wz = __shfl(mz, src, 64);
+        const bool wvalid = __shfl((int)valid, src, 64) != 0;
+        if (sl < nt && qi < n && (int64_t)wpid < q.n)
+            write_out(Io, Vo, tau, wvalid && c < ncells, wpid, pa + qi, wx, wy, wz, out_v, out_i, pr);
         return;
     }
     for (uint32_t p0 = pa; p0 < pb; p0 += kChunkB) {
@@ -298,7 +365,8 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
                 }
             }
         }
-        if (lane < m && (int64_t)pid < q.n) write_out(Io, Vo, tau, valid && c < ncells, pid, out_v, out_i);
+        if (lane < m && (int64_t)pid < q.n)
+            write_out(Io, Vo, tau, valid && c < ncells, pid, p0 + lane, mx, my, mz, out_v, out_i, pr);
     }
 }
 
@@ -332,7 +400,7 @@ hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const R
 hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                                 const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
-                                hipStream_t s) {
+                                const PlanResults &pr, hipStream_t s) {
     if (q.n <= 0) return hipSuccess;
     const int64_t nbuckets = g.ncells + 1;  // cells and the outside bucket
     prof_begin("cell_items", s);
@@ -350,7 +418,7 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
     prof_begin("sample_points", s);
     hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kWavesPerBlock - 1) / kWavesPerBlock)),
                        dim3(kBlock), 0, s, q, g, rec, gids, cell_off, point_off, order, it.item_off, it.items,
-                       it.max_items, T, tau, out_v, out_i);
+                       it.max_items, T, tau, out_v, out_i, pr);
     prof_end("sample_points", s);
     return hipGetLastError();
 }

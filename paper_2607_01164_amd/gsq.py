@@ -30,7 +30,7 @@ GS_QUERY_POINTS = 2
 
 EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_bytes", "gs_sample",
             "gs_backward_work_bytes", "gs_sample_backward", "gs_last_error", "gs_version", "gs_profile_enable",
-            "gs_profile_reset", "gs_profile_read")
+            "gs_profile_select", "gs_profile_reset", "gs_profile_read")
 
 
 class GsLibraryMissing(RuntimeError):
@@ -97,6 +97,8 @@ def load_library():
     L.gs_version.argtypes = []
     L.gs_profile_enable.restype = None
     L.gs_profile_enable.argtypes = [ctypes.c_int]
+    L.gs_profile_select.restype = None
+    L.gs_profile_select.argtypes = [ctypes.c_char_p]
     L.gs_profile_reset.restype = None
     L.gs_profile_reset.argtypes = []
     L.gs_profile_read.restype = ctypes.c_int
@@ -340,6 +342,11 @@ def gs_sample_backward(gauss: Gaussians, index: Index, query: Query, plan: Optio
 
 def profile_enable(on: bool = True) -> None:
     load_library().gs_profile_enable(1 if on else 0)
+
+
+def profile_select(name=None) -> None:
+    """Record only the kernel `name` (None: every kernel)."""
+    load_library().gs_profile_select(None if name is None else name.encode())
 
 
 def profile_reset() -> None:

@@ -127,6 +127,23 @@ def test_points_small_with_outside_and_boundary():
     check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="points")
 
 
+def test_backward_with_empty_rows_and_boxes():
+    """Points fill only one corner of the domain: many Gaussian boxes hold
+    no query, and large Gaussians span several batches of 64 rows, some of
+    them empty."""
+    g = synth.random_gaussians(71, 1500, log_mu=np.log(0.05), log_sd=0.7)
+    pts = synth.random_points(72, 20000, 0.0, 0.45)
+    pts[:50] += 0.5
+    log("case points in one corner, empty boxes and row batches")
+    r = Run(g, (24, 24, 24), "points", points=pts)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="corner")
+    gv, gi = synth.random_normal(73, r.nq), synth.random_normal(74, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="corner")
+
+
 def test_point_plan_order_matches_oracle():
     """The query ordering kept in the plan (Sec. 5.1 analogue of the sample
     BVH): keys and ids bit-exact against the oracle's stable order."""
