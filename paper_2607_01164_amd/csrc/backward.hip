@@ -85,7 +85,7 @@ struct Acc {
     float dv, dw;
 };
 
-// Whitened offset u = M (p - mu) and Q = |u|^2 (paper Eq. 1 and 3).
+// Whitened offset u = M (p - mu) and Q = |u|^2, the exponent of paper Eq. 3.
 __device__ __forceinline__ float whiten(const Record &r, float px, float py, float pz, float &u0, float &u1,
                                         float &u2) {
     const float dx = px - r.r0.x, dy = py - r.r0.y, dz = pz - r.r0.z;
