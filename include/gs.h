@@ -131,7 +131,15 @@ size_t gs_index_work_bytes(int64_t n_gauss, const gs_grid *grid, int64_t capacit
  * paper's tau_1 (0.01 in its evaluation), 0 < tau < 1.
  * Boxes are computed in float32 in one fixed order of operations, so the
  * index is reproducible bit for bit. The half-extent along axis j is
- * r * sqrt(Sigma_jj) with r = sqrt(2 ln(1/tau)) (1 + 2^-10).
+ * r * sqrt(Sigma_jj) with r = sqrt(2 ln(1/tau)) (1 + 2^-10). A box of at
+ * most 64 (y, z) rows of at most 16 cells lists, in each row, only the run
+ * of cells that the enlarged ellipsoid Q <= r^2 can reach over the row's
+ * (y, z) slab, bounded in float64: x conditioned on (y, z) is centred on a
+ * line through the mean with half-width sqrt((r^2 - Q2) vc), Q2 the (y, z)
+ * marginal's quadratic form and vc the conditional variance; the run covers
+ * [min centre - wm, max centre + wm] over the slab's corners, with
+ * wm = sqrt((r^2 - min Q2) vc), and is empty when min Q2 > r^2. Every cell
+ * holding a point with Q <= 2 ln(1/tau) is still listed.
  * Waits on the stream once, for the pair count. If it exceeds the capacity,
  * returns GS_ERR_CAPACITY with index->n_pairs set to the count needed and the
  * index left unusable.

@@ -47,7 +47,7 @@ def lib():
         L.orc_voxel_centers.restype = c_int
         L.orc_voxel_centers.argtypes = [vp, vp, vp, c_i64, vp, vp]
         L.orc_index_boxes.restype = c_i64
-        L.orc_index_boxes.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp]
+        L.orc_index_boxes.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp, vp, vp]
         L.orc_index.restype = c_int
         L.orc_index.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp, c_i64, vp, vp]
         L.orc_point_order.restype = c_int
@@ -182,17 +182,28 @@ def voxel_centers(dims, lo=(0, 0, 0), hi=(1, 1, 1), ids=None) -> np.ndarray:
     return out
 
 
-def index_boxes(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01):
-    """Canonical float32 cell box per Gaussian ([n,6], -1 when empty) and pair counts."""
+SPAN_ROWS = 64
+
+
+def index_boxes(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01, spans: bool = False):
+    """Canonical float32 cell box per Gaussian ([n,6], -1 when empty) and the
+    number of cells it lists; with spans=True also the trimmed flags [n] and
+    the row spans [n, 64] (byte: first | last << 4, offsets from the box's
+    low x; 0x0F for an empty row)."""
     m, s, q, v, w = _gauss(g)
     c = np.asarray(cells, dtype=np.int32).reshape(3)
     lo_, hi_ = _box(lo, hi)
     n = m.shape[0]
     box = np.zeros((n, 6), dtype=np.int32)
     cnt = np.zeros(n, dtype=np.int64)
-    P = lib().orc_index_boxes(n, _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), _p(c), tau, _p(box), _p(cnt))
+    tr = np.zeros(n, dtype=np.uint8)
+    sp = np.zeros((n, SPAN_ROWS), dtype=np.uint8)
+    P = lib().orc_index_boxes(n, _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), _p(c), tau, _p(box), _p(cnt),
+                              _p(tr), _p(sp))
     if P < 0:
         raise ValueError("orc_index_boxes: bad arguments")
+    if spans:
+        return box, cnt, tr.astype(bool), sp
     return box, cnt
 
 

@@ -574,6 +574,127 @@ static int64_t cell_box(const float *mu, const float *s, const float *q, float v
     return count;
 }
 
+/*
+ * Row spans (refinement of the box of Sec. 4.1.1, canonical float64).
+ *
+ * The cells of a box come in x-rows at fixed (cy, cz). The cutoff
+ * ellipsoid E = {p : (p - mu)^T Sigma^-1 (p - mu) <= T'} (T' = RCI^2, the
+ * same enlarged cutoff as the box) meets the slab of a row, y in [y0, y1],
+ * z in [z0, z1], in a convex set, so the cells of the row it reaches form one
+ * run. The span kept for the row is a superset of that run:
+ *   - conditioning on (y, z): x | (y, z) is centred on
+ *     c(y, z) = mu_x + b_y dy + b_z dz with half-width sqrt((T' - Q2) vc),
+ *     where Q2 is the quadratic form of the (y, z) marginal (precision
+ *     Sigma_yz^-1), b = Sigma_x,yz Sigma_yz^-1 and vc the conditional variance;
+ *   - Q2min = the minimum of Q2 over the slab's rectangle (0 when the centre
+ *     lies inside, else the least of the four edge minima); the row is empty
+ *     when Q2min > T';
+ *   - otherwise x lies in [min c - wm, max c + wm] with wm = sqrt((T' - Q2min) vc)
+ *     and the extremes of the linear c taken at the rectangle's corners.
+ * The span is clipped to the box. A box is trimmed only when it has at most
+ * SPAN_ROWS rows and at most SPAN_NX cells per row; a span is stored as one
+ * byte (first and last cell offset from the box's low x, 4 bits each;
+ * SPAN_EMPTY for none). Every float64 operation is performed in the order
+ * written here.
+ */
+#define SPAN_ROWS 64
+#define SPAN_NX 16
+#define SPAN_EMPTY 0x0F
+
+static double rect_qmin(double P00, double P01, double P11, double kz, double ky, double Y0, double Y1,
+                        double Z0, double Z1)
+{
+    if (Y0 <= 0.0 && 0.0 <= Y1 && Z0 <= 0.0 && 0.0 <= Z1) return 0.0;
+    double best = INFINITY;
+    const double Ys[2] = {Y0, Y1}, Zs[2] = {Z0, Z1};
+    for (int e = 0; e < 2; e++) {
+        const double Y = Ys[e];
+        double zs = kz * Y;
+        zs = zs < Z0 ? Z0 : (zs > Z1 ? Z1 : zs);
+        const double v = ((P00 * Y) * Y + 2.0 * ((P01 * Y) * zs)) + (P11 * zs) * zs;
+        best = v < best ? v : best;
+    }
+    for (int e = 0; e < 2; e++) {
+        const double Z = Zs[e];
+        double ys = ky * Z;
+        ys = ys < Y0 ? Y0 : (ys > Y1 ? Y1 : ys);
+        const double v = ((P00 * ys) * ys + 2.0 * ((P01 * ys) * Z)) + (P11 * Z) * Z;
+        best = v < best ? v : best;
+    }
+    return best;
+}
+
+/* Returns 1 and fills span[0 .. ny*nz) and *count when the box is trimmed,
+ * 0 when it keeps every cell of its box. */
+static int row_spans(const float *mu, const float *s, const float *q, const int32_t b[6], const float glo[3],
+                     const float ghi[3], const int32_t cells[3], float RCI, uint8_t *span, int64_t *count)
+{
+    const int64_t nx = b[3] - b[0] + 1, ny = b[4] - b[1] + 1, nz = b[5] - b[2] + 1;
+    if (ny * nz > SPAN_ROWS || nx > SPAN_NX) return 0;
+    const double qw = q[0], qx = q[1], qy = q[2], qz = q[3];
+    const double qn = sqrt(((qw * qw + qx * qx) + qy * qy) + qz * qz);
+    const double w = qw / qn, x = qx / qn, y = qy / qn, z = qz / qn;
+    double R[3][3];
+    R[0][0] = 1.0 - 2.0 * (y * y + z * z);
+    R[0][1] = 2.0 * (x * y - w * z);
+    R[0][2] = 2.0 * (x * z + w * y);
+    R[1][0] = 2.0 * (x * y + w * z);
+    R[1][1] = 1.0 - 2.0 * (x * x + z * z);
+    R[1][2] = 2.0 * (y * z - w * x);
+    R[2][0] = 2.0 * (x * z - w * y);
+    R[2][1] = 2.0 * (y * z + w * x);
+    R[2][2] = 1.0 - 2.0 * (x * x + y * y);
+    double a[3][3], S[3][3];
+    for (int j = 0; j < 3; j++)
+        for (int m = 0; m < 3; m++) a[j][m] = R[j][m] * (double)s[m];
+    for (int j = 0; j < 3; j++)
+        for (int k = 0; k < 3; k++) S[j][k] = ((a[j][0] * a[k][0]) + (a[j][1] * a[k][1])) + (a[j][2] * a[k][2]);
+    const double det = S[1][1] * S[2][2] - S[1][2] * S[1][2];
+    if (!(det > 0.0) || !isfinite(det)) return 0;
+    const double by = (S[0][1] * S[2][2] - S[0][2] * S[1][2]) / det;
+    const double bz = (S[0][2] * S[1][1] - S[0][1] * S[1][2]) / det;
+    const double vc = S[0][0] - (by * S[0][1] + bz * S[0][2]);
+    if (!(vc > 0.0) || !isfinite(vc)) return 0;
+    const double P00 = S[2][2] / det, P01 = -S[1][2] / det, P11 = S[1][1] / det;
+    const double kz = -(P01 / P11), ky = -(P01 / P00);  /* edge vertices: z = kz y, y = ky z */
+    const double Tq = (double)RCI * (double)RCI;
+    const double icx = (double)cells[0] / ((double)ghi[0] - (double)glo[0]);
+    const double wdy = ((double)ghi[1] - (double)glo[1]) / (double)cells[1];
+    const double wdz = ((double)ghi[2] - (double)glo[2]) / (double)cells[2];
+    int64_t cnt = 0;
+    for (int64_t r = 0; r < ny * nz; r++) {
+        const int64_t cy = b[1] + r % ny, cz = b[2] + r / ny;
+        const double Y0 = ((double)glo[1] + (double)cy * wdy) - (double)mu[1];
+        const double Y1 = ((double)glo[1] + (double)(cy + 1) * wdy) - (double)mu[1];
+        const double Z0 = ((double)glo[2] + (double)cz * wdz) - (double)mu[2];
+        const double Z1 = ((double)glo[2] + (double)(cz + 1) * wdz) - (double)mu[2];
+        const double qmin = rect_qmin(P00, P01, P11, kz, ky, Y0, Y1, Z0, Z1);
+        uint8_t code = SPAN_EMPTY;
+        if (!(qmin > Tq)) {
+            int64_t cl = b[0], ch = b[3];
+            const double wm = sqrt((Tq - qmin) * vc);
+            const double c00 = (double)mu[0] + (by * Y0 + bz * Z0), c01 = (double)mu[0] + (by * Y0 + bz * Z1);
+            const double c10 = (double)mu[0] + (by * Y1 + bz * Z0), c11 = (double)mu[0] + (by * Y1 + bz * Z1);
+            const double m0 = c00 < c01 ? c00 : c01, m1 = c10 < c11 ? c10 : c11;
+            const double M0 = c00 > c01 ? c00 : c01, M1 = c10 > c11 ? c10 : c11;
+            const double cmin = m0 < m1 ? m0 : m1, cmax = M0 > M1 ? M0 : M1;
+            const double fl = floor(((cmin - wm) - (double)glo[0]) * icx);
+            const double fh = floor(((cmax + wm) - (double)glo[0]) * icx);
+            if (isfinite(fl) && isfinite(fh)) {
+                cl = fl < (double)b[0] ? b[0] : (fl > (double)b[3] ? b[3] + 1 : (int64_t)fl);
+                ch = fh > (double)b[3] ? b[3] : (fh < (double)b[0] ? b[0] - 1 : (int64_t)fh);
+            }
+            if (cl <= ch) {
+                code = (uint8_t)((cl - b[0]) | ((ch - b[0]) << 4));
+                cnt += ch - cl + 1;
+            }
+        }
+        span[r] = code;
+    }
+    *count = cnt;
+    return 1;
+}
+
 static void grid_invc(const float lo[3], const float hi[3], const int32_t cells[3], float invc[3])
 {
     for (int j = 0; j < 3; j++) {
@@ -592,11 +713,16 @@ static int grid_ok(const float lo[3], const float hi[3], const int32_t cells[3])
     return nc < ((int64_t)1 << 31);
 }
 
-/* box[n][6] = (cx_lo, cy_lo, cz_lo, cx_hi, cy_hi, cz_hi) or -1, count[n];
- * returns the total number of pairs (or -1 on bad arguments). */
+/* box[n][6] = (cx_lo, cy_lo, cz_lo, cx_hi, cy_hi, cz_hi) or -1, count[n]
+ * (cells listed: the trimmed count for a trimmed box), trimmed[n] (1 when
+ * the box's rows carry spans), spans[n][SPAN_ROWS] (row spans of trimmed
+ * boxes; SPAN_EMPTY for rows past the box and for untrimmed boxes); any
+ * output may be NULL. Returns the total number of
+ * pairs (or -1 on bad arguments). */
 int64_t orc_index_boxes(int64_t n, const float *mean, const float *scale, const float *rot,
                         const float *value, const float *weight, const float lo[3], const float hi[3],
-                        const int32_t cells[3], float tau, int32_t *box, int64_t *count)
+                        const int32_t cells[3], float tau, int32_t *box, int64_t *count, uint8_t *trimmed,
+                        uint8_t *spans)
 {
     if (n < 0 || !grid_ok(lo, hi, cells) || !(tau > 0.0f) || !(tau < 1.0f)) return -1;
     float invc[3];
@@ -605,9 +731,19 @@ int64_t orc_index_boxes(int64_t n, const float *mean, const float *scale, const 
     int64_t total = 0;
     for (int64_t i = 0; i < n; i++) {
         int32_t b[6];
+        uint8_t sp[SPAN_ROWS];
+        memset(sp, SPAN_EMPTY, sizeof(sp));
         int64_t c = cell_box(mean + 3 * i, scale + 3 * i, rot + 4 * i, value[i], weight[i], lo, invc, cells, RCI, b);
+        int tr = 0;
+        if (c > 0) {
+            int64_t ct = 0;
+            tr = row_spans(mean + 3 * i, scale + 3 * i, rot + 4 * i, b, lo, hi, cells, RCI, sp, &ct);
+            if (tr) c = ct;
+        }
         if (box) memcpy(box + 6 * i, b, sizeof(b));
         if (count) count[i] = c;
+        if (trimmed) trimmed[i] = (uint8_t)tr;
+        if (spans) memcpy(spans + SPAN_ROWS * i, sp, sizeof(sp));
         total += c;
     }
     return total;
@@ -627,43 +763,62 @@ int orc_index(int64_t n, const float *mean, const float *scale, const float *rot
 {
     if (n < 0 || !grid_ok(lo, hi, cells) || !(tau > 0.0f) || !(tau < 1.0f)) return ORC_ERR_ARG;
     int64_t ncells = (int64_t)cells[0] * cells[1] * cells[2];
-    int32_t *box = (int32_t *)malloc(sizeof(int32_t) * 6 * (size_t)(n > 0 ? n : 1));
+    const size_t nn = (size_t)(n > 0 ? n : 1);
+    int32_t *box = (int32_t *)malloc(sizeof(int32_t) * 6 * nn);
+    uint8_t *tr = (uint8_t *)malloc(nn);
+    uint8_t *sp = (uint8_t *)malloc((size_t)SPAN_ROWS * nn);
     int64_t *cursor = (int64_t *)calloc((size_t)ncells + 1, sizeof(int64_t));
-    if (!box || !cursor) {
+    if (!box || !cursor || !tr || !sp) {
         free(box);
+        free(tr);
+        free(sp);
         free(cursor);
         return ORC_ERR_NOMEM;
     }
-    int64_t P = orc_index_boxes(n, mean, scale, rot, value, weight, lo, hi, cells, tau, box, NULL);
+    int64_t P = orc_index_boxes(n, mean, scale, rot, value, weight, lo, hi, cells, tau, box, NULL, tr, sp);
     *n_pairs = P;
     if (P > capacity || P >= ((int64_t)1 << 32)) {
         free(box);
+        free(tr);
+        free(sp);
         free(cursor);
         return ORC_ERR_CAPACITY;
     }
     int64_t Cx = cells[0], Cy = cells[1];
-    for (int64_t i = 0; i < n; i++) {
-        const int32_t *b = box + 6 * i;
-        if (b[0] < 0) continue;
-        for (int64_t z = b[2]; z <= b[5]; z++)
-            for (int64_t y = b[1]; y <= b[4]; y++)
-                for (int64_t x = b[0]; x <= b[3]; x++) cursor[x + Cx * (y + Cy * z) + 1]++;
-    }
-    for (int64_t k = 0; k < ncells; k++) cursor[k + 1] += cursor[k];
-    for (int64_t k = 0; k <= ncells; k++) cell_offsets[k] = (uint32_t)cursor[k];
-    for (int64_t i = 0; i < n; i++) {
-        const int32_t *b = box + 6 * i;
-        if (b[0] < 0) continue;
-        for (int64_t z = b[2]; z <= b[5]; z++)
-            for (int64_t y = b[1]; y <= b[4]; y++)
-                for (int64_t x = b[0]; x <= b[3]; x++) {
-                    int64_t key = x + Cx * (y + Cy * z);
-                    int64_t at = cursor[key]++;
-                    keys[at] = (uint32_t)key;
-                    gids[at] = (uint32_t)i;
+    /* two sweeps over the listed cells: count per cell, then place (key, gid) */
+    for (int sweep = 0; sweep < 2; sweep++) {
+        if (sweep == 1) {
+            for (int64_t k = 0; k < ncells; k++) cursor[k + 1] += cursor[k];
+            for (int64_t k = 0; k <= ncells; k++) cell_offsets[k] = (uint32_t)cursor[k];
+        }
+        for (int64_t i = 0; i < n; i++) {
+            const int32_t *b = box + 6 * i;
+            if (b[0] < 0) continue;
+            const int64_t ny = b[4] - b[1] + 1;
+            for (int64_t z = b[2]; z <= b[5]; z++)
+                for (int64_t y = b[1]; y <= b[4]; y++) {
+                    int64_t x0 = b[0], x1 = b[3];
+                    if (tr[i]) {
+                        const uint8_t code = sp[SPAN_ROWS * i + (y - b[1]) + ny * (z - b[2])];
+                        x0 = b[0] + (code & 15);
+                        x1 = b[0] + (code >> 4);
+                    }
+                    for (int64_t x = x0; x <= x1; x++) {
+                        int64_t key = x + Cx * (y + Cy * z);
+                        if (sweep == 0) {
+                            cursor[key + 1]++;
+                        } else {
+                            int64_t at = cursor[key]++;
+                            keys[at] = (uint32_t)key;
+                            gids[at] = (uint32_t)i;
+                        }
+                    }
                 }
+        }
     }
     free(box);
+    free(tr);
+    free(sp);
     free(cursor);
     return ORC_OK;
 }

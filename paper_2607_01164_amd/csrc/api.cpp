@@ -112,6 +112,7 @@ int gauss_order_bits(const gs_grid *g) { return gauss_order_full_bits(g) - gauss
 struct IndexWork {
     Record *rec;
     CellBox *box;
+    uint8_t *spans;      // [n][kSpanRows] row spans of trimmed boxes
     uint32_t *gorder;    // [n] Gaussians in spatial order
     uint32_t *gkeys;     // [n] their sort keys
     uint32_t *gsort_k;   // [n] sort scratch
@@ -132,6 +133,7 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     w.rec = c.take<Record>((size_t)(n > 0 ? n : 1));
     w.box = c.take<CellBox>((size_t)(n > 0 ? n : 1));
     const size_t n1 = (size_t)(n > 0 ? n : 1);
+    w.spans = c.take<uint8_t>(n1 * kSpanRows);
     w.gorder = c.take<uint32_t>(n1);
     w.gkeys = c.take<uint32_t>(n1);
     w.gsort_k = c.take<uint32_t>(n1);
@@ -429,7 +431,7 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     IndexWork w = index_layout(index->work, n, grid, index->capacity);
 
     GS_TRY(launch_preprocess(gauss->mean, gauss->scale, gauss->rot, gauss->value, gauss->weight, n, gp,
-                             index_radius(tau), w.rec, w.box, w.pair_off, stream),
+                             index_radius(tau), w.rec, w.box, w.spans, w.pair_off, stream),
            "gs_build_index: preprocess");
     {
         // spatial visiting order of the Gaussians (sorted by box corner cell)
@@ -461,7 +463,7 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     // emit where the sort's last pass lands in keys/gids
     uint32_t *ek = odd ? w.keys_alt : index->keys, *ev = odd ? w.gids_alt : index->gids;
     uint32_t *ak = odd ? index->keys : w.keys_alt, *av = odd ? index->gids : w.gids_alt;
-    GS_TRY(launch_emit(w.pair_off, w.box, n, (int64_t)P, gp, w.tile_first, ek, ev,
+    GS_TRY(launch_emit(w.pair_off, w.box, w.spans, n, (int64_t)P, gp, w.tile_first, ek, ev,
                        radix_pass0(w.radix_work, (int64_t)P, bits), stream),
            "gs_build_index: emit");
     GS_TRY(radix_sort_pairs(ek, ev, ak, av, (int64_t)P, bits, w.radix_work, stream, true), "gs_build_index: sort");
@@ -572,7 +574,7 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
     }
     IndexWork w = index_layout(index->work, n, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
-    GS_TRY(launch_backward(qp, gp, w.rec, w.box, w.gorder, n, p.order, p.point_off, p.res.pos, p.res.out, value,
+    GS_TRY(launch_backward(qp, gp, w.rec, w.box, w.spans, w.gorder, n, p.order, p.point_off, p.res.pos, p.res.out, value,
                            influence, grad_value,
                            grad_influence, cutoff_T(index->tau), bw.b, gauss->mean, gauss->scale, gauss->rot, d_mean,
                            d_scale, d_rot, d_value, d_weight, stream),

@@ -174,6 +174,7 @@ __device__ __forceinline__ void drain(const Record &r, const float4 *qu, const u
 template <bool GRID>
 __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                            const CellBox *__restrict__ box,
+                                                           const uint8_t *__restrict__ spans,
                                                            const uint32_t *__restrict__ gorder, int64_t n_gauss,
                                                            const uint32_t *__restrict__ point_off,
                                                            const float4 *__restrict__ plan_pos,
@@ -211,28 +212,36 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
         for (uint32_t rb = 0; rb < R; rb += kWave) {
             // lane l describes row rb + l: its first element and its length
             const uint32_t row = rb + lane;
-            uint32_t start = 0, len = 0;
+            uint32_t start = 0, len = 0, rx0 = vx0;
             float rpy = 0.0f, rpz = 0.0f;
             if (row < R) {
                 const uint32_t yy = row % nry, zz = row / nry;
+                // the row's run of cells: the whole box row, or its span
+                uint32_t xa = 0, xn = nx;
+                if (b.lo.w) {
+                    const uint32_t code = spans[(size_t)gid * kSpanRows + (yy / ry) + ny * (zz / rz)];
+                    xa = span_first(code);
+                    xn = span_len(code);
+                }
                 if (GRID) {
                     const uint32_t vy = (uint32_t)b.lo.y * ry + yy, vz = (uint32_t)b.lo.z * rz + zz;
-                    start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + vx0;
-                    len = nx * rx;
+                    rx0 = vx0 + xa * rx;
+                    start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + rx0;
+                    len = xn * rx;
                     rpy = g.lo[1] + ((float)vy + 0.5f) * q.vsz[1];
                     rpz = g.lo[2] + ((float)vz + 0.5f) * q.vsz[2];
-                } else {
+                } else if (xn > 0) {
                     const uint32_t cy = (uint32_t)b.lo.y + yy, cz = (uint32_t)b.lo.z + zz;
-                    const uint32_t kbase = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz);
-                    start = point_off[kbase + (uint32_t)b.lo.x];
-                    len = point_off[kbase + (uint32_t)b.hi.x + 1] - start;
+                    const uint32_t kbase = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz) + (uint32_t)b.lo.x;
+                    start = point_off[kbase + xa];
+                    len = point_off[kbase + xa + xn] - start;
                 }
             }
             const uint32_t nrows = (R - rb) < (uint32_t)kWave ? (R - rb) : (uint32_t)kWave;
             const uint32_t incl = wave_incl_sum(len);  // end of row l in the concatenation
             const uint32_t E = __builtin_amdgcn_readlane(incl, 63);
             const uint32_t kofs = start - (incl - len);  // element e of row l is point e + kofs
-            const uint32_t xofs = vx0 - (incl - len);    // grids: element e of row l has x = e + xofs
+            const uint32_t xofs = rx0 - (incl - len);    // grids: element e of row l has x = e + xofs
             if (E == 0) continue;  // no query in these rows
             uint32_t j0 = 0;       // first row not finished before the window
             for (uint32_t e0 = 0; e0 < E; e0 += kWave) {
@@ -376,7 +385,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
 }  // namespace
 
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
-                           const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
+                           const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
                            const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
@@ -401,10 +410,10 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
         const uint32_t wblocks = (uint32_t)((n_gauss + kWavesPerBlock - 1) / kWavesPerBlock);
         prof_begin("bwd_gauss", s);
         if (grid)
-            hipLaunchKernelGGL(k_backward_gauss<true>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, gorder,
+            hipLaunchKernelGGL(k_backward_gauss<true>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans, gorder,
                                n_gauss, point_off, plan_pos, b.ab, T, b.moments);
         else
-            hipLaunchKernelGGL(k_backward_gauss<false>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, gorder,
+            hipLaunchKernelGGL(k_backward_gauss<false>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans, gorder,
                                n_gauss, point_off, plan_pos, b.ab, T, b.moments);
         prof_end("bwd_gauss", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;

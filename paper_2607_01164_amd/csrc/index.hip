@@ -2,7 +2,10 @@
 //  - preprocess: per Gaussian, the axis-aligned box of its cutoff ellipsoid
 //    in cells (canonical float32, each operation rounded separately), its
 //    cell count, and the evaluation record used by the samplers;
-//  - emit: one (cell key, Gaussian id) pair per cell of every box,
+//  - row spans: boxes of at most kSpanRows (y, z) rows of at most kSpanNx
+//    cells keep, per row, only the run of cells a float64 bound of the
+//    cutoff ellipsoid's section over the row's slab can reach;
+//  - emit: one (cell key, Gaussian id) pair per listed cell of every box,
 //    parallel over pairs with a per-tile load-balanced search for the owning
 //    Gaussian (the paper parallelises this step over intersections for the
 //    same reason: box sizes vary by orders of magnitude in 3D).
@@ -20,11 +23,128 @@ namespace {
 
 __device__ __forceinline__ bool finite_f(float x) { return __builtin_isfinite(x); }
 
+// Minimum over the rectangle [Y0, Y1] x [Z0, Z1] of the quadratic form
+// P00 y^2 + 2 P01 y z + P11 z^2 (positive definite): 0 when the origin is
+// inside, else the least of the four edge minima (each a clamped 1D vertex).
+__device__ double rect_qmin(double P00, double P01, double P11, double kz, double ky, double Y0, double Y1,
+                            double Z0, double Z1) {
+    if (Y0 <= 0.0 && 0.0 <= Y1 && Z0 <= 0.0 && 0.0 <= Z1) return 0.0;
+    double best = __builtin_inf();
+    const double Ys[2] = {Y0, Y1}, Zs[2] = {Z0, Z1};
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const double Y = Ys[e];
+        double zs = kz * Y;
+        zs = zs < Z0 ? Z0 : (zs > Z1 ? Z1 : zs);
+        const double v = ((P00 * Y) * Y + 2.0 * ((P01 * Y) * zs)) + (P11 * zs) * zs;
+        best = v < best ? v : best;
+    }
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const double Z = Zs[e];
+        double ys = ky * Z;
+        ys = ys < Y0 ? Y0 : (ys > Y1 ? Y1 : ys);
+        const double v = ((P00 * ys) * ys + 2.0 * ((P01 * ys) * Z)) + (P11 * Z) * Z;
+        best = v < best ? v : best;
+    }
+    return best;
+}
+
+// Row spans of a box (the box refined per x-row, Sec. 4.1.1). The cutoff
+// ellipsoid, enlarged like the box to Q <= rci^2, meets a row's slab
+// y in [y0, y1], z in [z0, z1] in a convex set. Conditioned on (y, z), x is
+// centred on mu_x + b . (dy, dz) with half-width sqrt((T' - Q2) vc), Q2 the
+// quadratic form of the (y, z) marginal, b = Sigma_x,yz Sigma_yz^-1 and vc
+// the conditional variance; the row keeps the cells of
+// [min c - wm, max c + wm], wm = sqrt((T' - min Q2) vc), with min Q2 over the
+// slab's rectangle and the extremes of c at its corners, or none when
+// min Q2 > T'. float64 throughout, each operation in this order. Returns
+// false (box not trimmed) for boxes with more than kSpanRows rows or kSpanNx
+// cells per row, or a degenerate marginal.
+__device__ bool row_spans(const float mu[3], const float s[3], const float q[4], const int lo_c[3],
+                          const int hi_c[3], const GridParams &g, float rci, uint8_t *__restrict__ out,
+                          uint64_t &count) {
+    const int nx = hi_c[0] - lo_c[0] + 1, ny = hi_c[1] - lo_c[1] + 1, nz = hi_c[2] - lo_c[2] + 1;
+    if (ny * nz > kSpanRows || nx > kSpanNx) return false;
+    const double qw = q[0], qx = q[1], qy = q[2], qz = q[3];
+    const double qn = sqrt(((qw * qw + qx * qx) + qy * qy) + qz * qz);
+    const double w = qw / qn, x = qx / qn, y = qy / qn, z = qz / qn;
+    double R[3][3];
+    R[0][0] = 1.0 - 2.0 * (y * y + z * z);
+    R[0][1] = 2.0 * (x * y - w * z);
+    R[0][2] = 2.0 * (x * z + w * y);
+    R[1][0] = 2.0 * (x * y + w * z);
+    R[1][1] = 1.0 - 2.0 * (x * x + z * z);
+    R[1][2] = 2.0 * (y * z - w * x);
+    R[2][0] = 2.0 * (x * z - w * y);
+    R[2][1] = 2.0 * (y * z + w * x);
+    R[2][2] = 1.0 - 2.0 * (x * x + y * y);
+    double a[3][3], S[3][3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int m = 0; m < 3; ++m) a[j][m] = R[j][m] * (double)s[m];
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int k = 0; k < 3; ++k) S[j][k] = ((a[j][0] * a[k][0]) + (a[j][1] * a[k][1])) + (a[j][2] * a[k][2]);
+    const double det = S[1][1] * S[2][2] - S[1][2] * S[1][2];
+    if (!(det > 0.0) || !__builtin_isfinite(det)) return false;
+    const double by = (S[0][1] * S[2][2] - S[0][2] * S[1][2]) / det;
+    const double bz = (S[0][2] * S[1][1] - S[0][1] * S[1][2]) / det;
+    const double vc = S[0][0] - (by * S[0][1] + bz * S[0][2]);
+    if (!(vc > 0.0) || !__builtin_isfinite(vc)) return false;
+    const double P00 = S[2][2] / det, P01 = -S[1][2] / det, P11 = S[1][1] / det;
+    const double kz = -(P01 / P11), ky = -(P01 / P00);  // edge vertices: z = kz y, y = ky z
+    const double Tq = (double)rci * (double)rci;
+    const double icx = (double)g.cells[0] / ((double)g.hi[0] - (double)g.lo[0]);
+    const double wdy = ((double)g.hi[1] - (double)g.lo[1]) / (double)g.cells[1];
+    const double wdz = ((double)g.hi[2] - (double)g.lo[2]) / (double)g.cells[2];
+    uint64_t cnt = 0;
+    // every row byte starts empty; rows of the box are then written in turn
+    const uint32_t e4 = kSpanEmpty * 0x01010101u;
+#pragma unroll
+    for (int k = 0; k < kSpanRows / 16; ++k) ((uint4 *)out)[k] = make_uint4(e4, e4, e4, e4);
+    // rows r = (cy - y0) + ny (cz - z0), in increasing r
+    int r = 0;
+    for (int cz = lo_c[2]; cz <= hi_c[2]; ++cz)
+    for (int cy = lo_c[1]; cy <= hi_c[1]; ++cy, ++r) {
+        const double Y0 = ((double)g.lo[1] + (double)cy * wdy) - (double)mu[1];
+        const double Y1 = ((double)g.lo[1] + (double)(cy + 1) * wdy) - (double)mu[1];
+        const double Z0 = ((double)g.lo[2] + (double)cz * wdz) - (double)mu[2];
+        const double Z1 = ((double)g.lo[2] + (double)(cz + 1) * wdz) - (double)mu[2];
+        const double qmin = rect_qmin(P00, P01, P11, kz, ky, Y0, Y1, Z0, Z1);
+        uint32_t code = kSpanEmpty;
+        if (!(qmin > Tq)) {
+            int cl = lo_c[0], ch = hi_c[0];
+            const double wm = sqrt((Tq - qmin) * vc);
+            const double c00 = (double)mu[0] + (by * Y0 + bz * Z0), c01 = (double)mu[0] + (by * Y0 + bz * Z1);
+            const double c10 = (double)mu[0] + (by * Y1 + bz * Z0), c11 = (double)mu[0] + (by * Y1 + bz * Z1);
+            const double m0 = c00 < c01 ? c00 : c01, m1 = c10 < c11 ? c10 : c11;
+            const double M0 = c00 > c01 ? c00 : c01, M1 = c10 > c11 ? c10 : c11;
+            const double cmin = m0 < m1 ? m0 : m1, cmax = M0 > M1 ? M0 : M1;
+            const double fl = floor(((cmin - wm) - (double)g.lo[0]) * icx);
+            const double fh = floor(((cmax + wm) - (double)g.lo[0]) * icx);
+            if (__builtin_isfinite(fl) && __builtin_isfinite(fh)) {
+                cl = fl < (double)lo_c[0] ? lo_c[0] : (fl > (double)hi_c[0] ? hi_c[0] + 1 : (int)fl);
+                ch = fh > (double)hi_c[0] ? hi_c[0] : (fh < (double)lo_c[0] ? lo_c[0] - 1 : (int)fh);
+            }
+            if (cl <= ch) {
+                code = (uint32_t)(cl - lo_c[0]) | ((uint32_t)(ch - lo_c[0]) << 4);
+                cnt += (uint64_t)(ch - cl + 1);
+            }
+        }
+        out[r] = (uint8_t)code;
+    }
+    count = cnt;
+    return true;
+}
+
 __global__ __launch_bounds__(kBlock) void k_preprocess(const float *__restrict__ mean, const float *__restrict__ scale,
                                                        const float *__restrict__ rot, const float *__restrict__ value,
                                                        const float *__restrict__ weight, int64_t n, GridParams g,
                                                        float rci, Record *__restrict__ rec, CellBox *__restrict__ box,
-                                                       uint64_t *__restrict__ count) {
+                                                       uint8_t *__restrict__ spans, uint64_t *__restrict__ count) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i == n) count[n] = 0;
     if (i >= n) return;
@@ -77,9 +197,15 @@ __global__ __launch_bounds__(kBlock) void k_preprocess(const float *__restrict__
         hi_c[0] = hi_c[1] = hi_c[2] = -1;
         cnt = 0;
     }
+    bool trimmed = false;
+    if (valid) {
+        uint64_t tc = 0;
+        trimmed = row_spans(mu, s, q, lo_c, hi_c, g, rci, spans + (size_t)i * kSpanRows, tc);
+        if (trimmed) cnt = tc;
+    }
     count[i] = cnt;
     CellBox b;
-    b.lo = make_int4(lo_c[0], lo_c[1], lo_c[2], 0);
+    b.lo = make_int4(lo_c[0], lo_c[1], lo_c[2], trimmed ? 1 : 0);
     b.hi = make_int4(hi_c[0], hi_c[1], hi_c[2], 0);
     box[i] = b;
 
@@ -113,38 +239,17 @@ __global__ __launch_bounds__(kBlock) void k_preprocess(const float *__restrict__
     rec[i] = r;
 }
 
-__global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pair_off,
-                                                 const CellBox *__restrict__ box, int64_t n, int64_t npairs,
-                                                 const uint32_t *__restrict__ tile_first, GridParams g,
-                                                 uint32_t *__restrict__ keys, uint32_t *__restrict__ gids,
-                                                 RadixPass0 pass0) {
-    __shared__ uint32_t head[kExpandTile];
-    __shared__ uint32_t wmax[kWavesPerBlock];
-    __shared__ uint32_t hist_lds[kMaxDigits];
-    Pass0Hist hist(hist_lds, pass0);
+// In-place inclusive max-scan of a tile's kExpandTile marks (kExpandItems
+// consecutive marks per thread, then across the block).
+__device__ void tile_max_scan(uint32_t *mark, uint32_t *wmax) {
     const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-    const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
-    const uint64_t tile_begin = (uint64_t)tile * kExpandTile;
-    const uint64_t rem = (uint64_t)npairs - tile_begin;
-    const uint32_t tile_cnt = rem < (uint64_t)kExpandTile ? (uint32_t)rem : (uint32_t)kExpandTile;
-    const int64_t gfirst = tile_first[tile];
-    const int64_t glast = (tile + 1 < gridDim.x) ? (int64_t)tile_first[tile + 1] : n - 1;
-    for (uint32_t s = tid; s < (uint32_t)kExpandTile; s += kBlock) head[s] = 0;
-    __syncthreads();
-    // mark the first pair of every Gaussian that starts inside the tile
-    for (int64_t gg = gfirst + 1 + tid; gg <= glast; gg += kBlock) {
-        const uint64_t pos = pair_off[gg] - tile_begin;
-        if (pos < tile_cnt) atomicMax(&head[pos], (uint32_t)(gg - gfirst));
-    }
-    __syncthreads();
-    // inclusive max-scan carries each mark over the Gaussian's pairs
     uint32_t run = 0;
     const uint32_t b0 = tid * kExpandItems;
 #pragma unroll
     for (int i = 0; i < kExpandItems; ++i) {
-        const uint32_t h = head[b0 + i];
+        const uint32_t h = mark[b0 + i];
         run = h > run ? h : run;
-        head[b0 + i] = run;
+        mark[b0 + i] = run;
     }
     const uint32_t incl = wave_incl_max(run);
     uint32_t excl = __shfl_up(incl, 1, 64);
@@ -156,21 +261,90 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
     const uint32_t carry = excl > wpre ? excl : wpre;
 #pragma unroll
     for (int i = 0; i < kExpandItems; ++i) {
-        const uint32_t h = head[b0 + i];
-        head[b0 + i] = h > carry ? h : carry;
+        const uint32_t h = mark[b0 + i];
+        mark[b0 + i] = h > carry ? h : carry;
     }
     __syncthreads();
+}
+
+// Row marks of trimmed boxes: at the first slot p of the tile covered by a
+// non-empty row (its first pair, or slot 0 for a row begun in an earlier
+// tile) the mark ((p + 1) << 16) | (row << 8) | (first << 4) | (p - start)
+// holds the row, the offset of its first cell and how far into the row
+// slot p is. Marks grow with p, so a max-scan hands every slot the mark of
+// its row.
+__device__ void mark_rows(const uint8_t *sp, uint32_t nrows, int64_t base, uint32_t tile_cnt, uint32_t *rowmark) {
+    int64_t start = base;
+#pragma unroll 8
+    for (uint32_t r = 0; r < nrows; ++r) {
+        const uint32_t code = sp[r];
+        const uint32_t len = span_len(code);
+        if (len > 0 && start + len > 0 && start < (int64_t)tile_cnt) {
+            const uint32_t p = start > 0 ? (uint32_t)start : 0u;
+            rowmark[p] = ((p + 1u) << 16) | (r << 8) | (span_first(code) << 4) | (uint32_t)((int64_t)p - start);
+        }
+        start += len;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pair_off,
+                                                 const CellBox *__restrict__ box,
+                                                 const uint8_t *__restrict__ spans, int64_t n, int64_t npairs,
+                                                 const uint32_t *__restrict__ tile_first, GridParams g,
+                                                 uint32_t *__restrict__ keys, uint32_t *__restrict__ gids,
+                                                 RadixPass0 pass0) {
+    __shared__ uint32_t head[kExpandTile];
+    __shared__ uint32_t rowmark[kExpandTile];
+    __shared__ uint32_t wmax[kWavesPerBlock];
+    __shared__ uint32_t hist_lds[kMaxDigits];
+    Pass0Hist hist(hist_lds, pass0);
+    const uint32_t tid = threadIdx.x;
+    const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
+    const uint64_t tile_begin = (uint64_t)tile * kExpandTile;
+    const uint64_t rem = (uint64_t)npairs - tile_begin;
+    const uint32_t tile_cnt = rem < (uint64_t)kExpandTile ? (uint32_t)rem : (uint32_t)kExpandTile;
+    const int64_t gfirst = tile_first[tile];
+    const int64_t glast = (tile + 1 < gridDim.x) ? (int64_t)tile_first[tile + 1] : n - 1;
+    for (uint32_t s = tid; s < (uint32_t)kExpandTile; s += kBlock) {
+        head[s] = 0;
+        rowmark[s] = 0;
+    }
+    __syncthreads();
+    // mark the first pair of every Gaussian that starts inside the tile, and
+    // the rows of the trimmed boxes that reach into it
+    for (int64_t gg = gfirst + tid; gg <= glast; gg += kBlock) {
+        const int64_t base = (int64_t)(pair_off[gg] - tile_begin);
+        if (gg > gfirst && base < (int64_t)tile_cnt) atomicMax(&head[base], (uint32_t)(gg - gfirst));
+        const CellBox b = box[gg];
+        if (b.lo.w && b.hi.x >= b.lo.x) {
+            const uint32_t nrows = (uint32_t)((b.hi.y - b.lo.y + 1) * (b.hi.z - b.lo.z + 1));
+            mark_rows(spans + (size_t)gg * kSpanRows, nrows, base, tile_cnt, rowmark);
+        }
+    }
+    __syncthreads();
+    // inclusive max-scans carry each mark over its Gaussian's (row's) pairs
+    tile_max_scan(head, wmax);
+    tile_max_scan(rowmark, wmax);
     const int64_t Cx = g.cells[0], Cy = g.cells[1];
 #pragma unroll 2
     for (int i = 0; i < kExpandItems; ++i) {
         const uint32_t slot = (uint32_t)i * kBlock + tid;
         if (slot < tile_cnt) {
             const int64_t gg = gfirst + head[slot];
-            const uint32_t local = (uint32_t)(tile_begin + slot - pair_off[gg]);
             const CellBox b = box[gg];
             const uint32_t nx = (uint32_t)(b.hi.x - b.lo.x + 1), ny = (uint32_t)(b.hi.y - b.lo.y + 1);
-            const uint32_t t = local / nx;
-            const int64_t cx = b.lo.x + (int64_t)(local - t * nx);
+            uint32_t t, xo;
+            if (b.lo.w) {
+                const uint32_t m = rowmark[slot];
+                const uint32_t p = (m >> 16) - 1u;
+                t = (m >> 8) & 63u;
+                xo = ((m >> 4) & 15u) + (m & 15u) + (slot - p);
+            } else {
+                const uint32_t local = (uint32_t)(tile_begin + slot - pair_off[gg]);
+                t = local / nx;
+                xo = local - t * nx;
+            }
+            const int64_t cx = b.lo.x + (int64_t)xo;
             const int64_t cy = b.lo.y + (int64_t)(t % ny);
             const int64_t cz = b.lo.z + (int64_t)(t / ny);
             const uint32_t key = (uint32_t)(cx + Cx * (cy + Cy * cz));
@@ -232,18 +406,19 @@ hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g,
 
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
-                             CellBox *box, uint64_t *count, hipStream_t s) {
+                             CellBox *box, uint8_t *spans, uint64_t *count, hipStream_t s) {
     const int64_t threads = n + 1;
     const uint32_t blocks = (uint32_t)((threads + kBlock - 1) / kBlock);
     prof_begin("preprocess", s);
     hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kBlock), 0, s, mean, scale, rot, value, weight, n, g, rci, rec,
-                       box, count);
+                       box, spans, count);
     prof_end("preprocess", s);
     return hipGetLastError();
 }
 
-hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, int64_t n, int64_t npairs, const GridParams &g,
-                       uint32_t *tile_first, uint32_t *keys, uint32_t *gids, const RadixPass0 &pass0, hipStream_t s) {
+hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8_t *spans, int64_t n, int64_t npairs,
+                       const GridParams &g, uint32_t *tile_first, uint32_t *keys, uint32_t *gids,
+                       const RadixPass0 &pass0, hipStream_t s) {
     if (npairs <= 0 || n <= 0) return hipSuccess;
     const uint32_t blocks = (uint32_t)((npairs + kExpandTile - 1) / kExpandTile);
     prof_begin("emit_partition", s);
@@ -253,8 +428,8 @@ hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, int64_t n, 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     prof_begin("emit", s);
-    hipLaunchKernelGGL(k_emit, dim3(blocks), dim3(kBlock), 0, s, pair_off, box, n, npairs, tile_first, g, keys, gids,
-                       pass0);
+    hipLaunchKernelGGL(k_emit, dim3(blocks), dim3(kBlock), 0, s, pair_off, box, spans, n, npairs, tile_first, g, keys,
+                       gids, pass0);
     prof_end("emit", s);
     return hipGetLastError();
 }

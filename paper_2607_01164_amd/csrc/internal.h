@@ -24,11 +24,24 @@ struct alignas(16) Record {
     float4 r0, r1, r2, r3;
 };
 
-// Cell box of a Gaussian: (x0, y0, z0, 0) and (x1, y1, z1, 0), inclusive;
-// an empty box has x1 < x0.
+// Cell box of a Gaussian: (x0, y0, z0, trimmed) and (x1, y1, z1, 0),
+// inclusive; an empty box has x1 < x0. When trimmed is 1 the box lists, in
+// each of its (y, z) rows (row r = (y - y0) + ny (z - z0)), only the cells
+// of the row's span: byte r of the Gaussian's span record holds the first
+// and last cell as offsets from x0 (low and high 4 bits), kSpanEmpty for a
+// row with none.
 struct alignas(16) CellBox {
     int4 lo, hi;
 };
+constexpr int kSpanRows = 64;          // rows of a trimmed box at most
+constexpr int kSpanNx = 16;            // cells per row of a trimmed box at most
+constexpr uint32_t kSpanEmpty = 0x0Fu;
+
+__device__ __forceinline__ uint32_t span_first(uint32_t code) { return code & 15u; }
+__device__ __forceinline__ uint32_t span_len(uint32_t code) {
+    const uint32_t a = code & 15u, b = code >> 4;
+    return b >= a ? b - a + 1 : 0u;
+}
 
 // Read-only views in the constant address space: loads through them with a
 // wave-uniform address become scalar loads into SGPRs.
@@ -210,9 +223,10 @@ struct GridParams {
 };
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
-                             CellBox *box, uint64_t *count, hipStream_t s);
+                             CellBox *box, uint8_t *spans, uint64_t *count, hipStream_t s);
 // tile_first: ceil(npairs / kSortTile) words of scratch
-hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, int64_t n, int64_t npairs, const GridParams &g,
+hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8_t *spans, int64_t n, int64_t npairs,
+                       const GridParams &g,
                        uint32_t *tile_first, uint32_t *keys, uint32_t *gids, const RadixPass0 &pass0, hipStream_t s);
 
 // Sampling (sample.hip).
@@ -261,7 +275,7 @@ struct BackwardBuffers {
     float2 *ab;            // [n] (alpha, beta) per query: plan order (points, voxels) or voxel order (grid)
 };
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
-                           const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
+                           const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
                            const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,

@@ -20,21 +20,46 @@ def sigma_diag(g):
 
 
 def test_axis_aligned_boxes_closed_form(orc):
-    """q = identity: the box half-extent is r_c' s_j on each axis."""
-    m = np.array([[0.5, 0.5, 0.5], [0.1, 0.9, 0.33], [0.0, 1.0, 0.5], [0.97, 0.02, 0.5]], np.float32)
-    s = np.array([[0.05, 0.02, 0.1], [0.01, 0.01, 0.01], [0.2, 0.05, 0.003], [0.04, 0.04, 0.04]], np.float32)
+    """q = identity: the box half-extent is r_c' s_j on each axis, and the
+    row spans are exact: the slab bound's centre line is flat and its
+    half-width is r_c' s_x sqrt(1 - d2) with d2 the squared scaled distance
+    from the mean to the row's (y, z) rectangle."""
+    m = np.array([[0.5, 0.5, 0.5], [0.1, 0.9, 0.33], [0.0, 1.0, 0.5], [0.97, 0.02, 0.5], [0.31, 0.62, 0.47]],
+                 np.float32)
+    s = np.array([[0.05, 0.02, 0.1], [0.01, 0.01, 0.01], [0.2, 0.05, 0.003], [0.04, 0.04, 0.04],
+                  [0.03, 0.045, 0.02]], np.float32)
     n = len(m)
     g = synth.Gaussians(m, s, np.tile(np.float32([1, 0, 0, 0]), (n, 1)), np.full(n, 0.5, np.float32),
                         np.full(n, 0.5, np.float32))
     cells = 16
-    box, cnt = orc.index_boxes(g, (cells,) * 3)
+    box, cnt, trimmed, spans = orc.index_boxes(g, (cells,) * 3, spans=True)
     for i in range(n):
         for j in range(3):
             lo = float(m[i, j]) - RCI64 * float(s[i, j])
             hi = float(m[i, j]) + RCI64 * float(s[i, j])
             assert box[i, j] == max(0, math.floor(lo * cells))
             assert box[i, 3 + j] == min(cells - 1, math.floor(hi * cells))
-        assert cnt[i] == np.prod(box[i, 3:] - box[i, :3] + 1)
+        nx, ny, nz = box[i, 3:] - box[i, :3] + 1
+        assert trimmed[i] == (ny * nz <= 64 and nx <= 16)
+        if not trimmed[i]:
+            assert cnt[i] == nx * ny * nz
+            continue
+        total = 0
+        for r in range(ny * nz):
+            cy, cz = box[i, 1] + r % ny, box[i, 2] + r // ny
+            dy = max(cy / cells - m[i, 1], 0.0, m[i, 1] - (cy + 1) / cells) / s[i, 1]
+            dz = max(cz / cells - m[i, 2], 0.0, m[i, 2] - (cz + 1) / cells) / s[i, 2]
+            d2 = (dy * dy + dz * dz) / RCI64 ** 2
+            code = spans[i, r]
+            if d2 > 1.0 + 1e-12:
+                assert code == 0x0F
+                continue
+            half = RCI64 * float(s[i, 0]) * math.sqrt(max(0.0, 1.0 - d2))
+            xl = min(max(math.floor((float(m[i, 0]) - half) * cells), box[i, 0]), box[i, 3])
+            xh = max(min(math.floor((float(m[i, 0]) + half) * cells), box[i, 3]), box[i, 0])
+            assert (box[i, 0] + (code & 15), box[i, 0] + (code >> 4)) == (xl, xh), (i, r)
+            total += xh - xl + 1
+        assert cnt[i] == total
 
 
 def test_rotated_boxes_against_float64_extent(orc):
@@ -62,15 +87,22 @@ def test_rotated_boxes_against_float64_extent(orc):
         np.testing.assert_array_equal(cnt[emp], 0)
 
 
-def brute_pairs(box, cells):
+def listed_pairs(box, trimmed, spans, cells):
+    """(key, gid) of every cell a box lists: all cells of an untrimmed box,
+    the row spans of a trimmed one."""
     pairs = []
     C = cells
     for i, b in enumerate(box):
         if b[0] < 0:
             continue
+        ny = b[4] - b[1] + 1
         for z in range(b[2], b[5] + 1):
             for y in range(b[1], b[4] + 1):
-                for x in range(b[0], b[3] + 1):
+                x0, x1 = b[0], b[3]
+                if trimmed[i]:
+                    code = spans[i, (y - b[1]) + ny * (z - b[2])]
+                    x0, x1 = b[0] + (code & 15), b[0] + (code >> 4)
+                for x in range(x0, x1 + 1):
                     pairs.append((x + C * (y + C * z), i))
     return sorted(pairs)
 
@@ -79,10 +111,11 @@ def test_index_structure_and_order(orc):
     g = synth.random_gaussians(42, 400, log_mu=np.log(0.04), log_sd=0.5)
     cells = 12
     keys, gids, offs = orc.index(g, (cells,) * 3)
-    box, cnt = orc.index_boxes(g, (cells,) * 3)
+    box, cnt, trimmed, spans = orc.index_boxes(g, (cells,) * 3, spans=True)
     P = len(keys)
     assert P == cnt.sum() and offs[-1] == P and offs[0] == 0
-    exp = brute_pairs(box, cells)
+    assert trimmed.sum() > 300
+    exp = listed_pairs(box, trimmed, spans, cells)
     np.testing.assert_array_equal(keys, [k for k, _ in exp])
     np.testing.assert_array_equal(gids, [i for _, i in exp])
     assert np.all(np.diff(offs.astype(np.int64)) >= 0)
@@ -116,6 +149,45 @@ def test_index_is_complete_near_the_cutoff(orc):
             c = np.clip(np.floor(p.astype(np.float32) * np.float32(cells)), 0, cells - 1).astype(int)
             k = c[0] + cells * (c[1] + cells * c[2])
             assert i in lists.get(k, ()), (i, p)
+
+
+def test_row_spans_are_tight(orc):
+    """The spans keep every cell the (enlarged) cutoff ellipsoid reaches and
+    few others: against the exact cell set, found by minimising Q over each
+    cell of the box, on C2-like Gaussians."""
+    from scipy.optimize import minimize
+    from scipy.spatial.transform import Rotation
+    g = synth.random_gaussians(45, 150, log_mu=np.log(0.008), log_sd=0.4, lo=0.1, hi=0.9)
+    cells = 40
+    box, cnt, trimmed, spans = orc.index_boxes(g, (cells,) * 3, spans=True)
+    q = g.rot.astype(np.float64)
+    R = Rotation.from_quat(np.stack([q[:, 1], q[:, 2], q[:, 3], q[:, 0]], axis=1)).as_matrix()
+    Tq = RCI64 ** 2
+    kept = exact = aabb = 0
+    for i in range(g.n):
+        if not trimmed[i]:
+            continue
+        A = np.linalg.inv(R[i] @ np.diag(g.scale[i].astype(np.float64) ** 2) @ R[i].T)
+        mu = g.mean[i].astype(np.float64)
+        b = box[i]
+        ny = b[4] - b[1] + 1
+        for cz in range(b[2], b[5] + 1):
+            for cy in range(b[1], b[4] + 1):
+                code = spans[i, (cy - b[1]) + ny * (cz - b[2])]
+                x0, x1 = b[0] + (code & 15), b[0] + (code >> 4)
+                for cx in range(b[0], b[3] + 1):
+                    aabb += 1
+                    lo = np.array([cx, cy, cz]) / cells
+                    hi = lo + 1.0 / cells
+                    res = minimize(lambda p: (p - mu) @ A @ (p - mu), np.clip(mu, lo, hi),
+                                   jac=lambda p: 2 * A @ (p - mu), bounds=list(zip(lo, hi)), method="L-BFGS-B")
+                    reach = res.fun <= Tq * (1 - 1e-6)
+                    listed = x0 <= cx <= x1
+                    exact += reach
+                    kept += listed
+                    assert listed or not reach, (i, cx, cy, cz, res.fun / Tq)
+    print(f"row spans: kept {kept}, exact {exact}, box {aabb}")
+    assert kept <= 1.15 * exact and kept < 0.85 * aabb, (kept, exact, aabb)
 
 
 def test_index_capacity_and_empty(orc):
