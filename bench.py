@@ -36,7 +36,7 @@ EMIT_BYTES_PER_PAIR = 8.0
 COPY_PROBE_BYTES = 256 << 20   # plain copy used to calibrate the HBM byte counters
 SRC_DIR = os.path.join(ROOT, "paper_2607_01164_amd", "csrc")
 WORKLOAD = "c2_grid256_batch"
-INDEX_CELLS = (40, 40, 40)
+INDEX_CELLS = (36, 36, 36)
 TAU = 0.01
 
 

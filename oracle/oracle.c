@@ -633,7 +633,8 @@ static int row_spans(const float *mu, const float *s, const float *q, const int3
     if (ny * nz > SPAN_ROWS || nx > SPAN_NX) return 0;
     const double qw = q[0], qx = q[1], qy = q[2], qz = q[3];
     const double qn = sqrt(((qw * qw + qx * qx) + qy * qy) + qz * qz);
-    const double w = qw / qn, x = qx / qn, y = qy / qn, z = qz / qn;
+    const double iq = 1.0 / qn;
+    const double w = qw * iq, x = qx * iq, y = qy * iq, z = qz * iq;
     double R[3][3];
     R[0][0] = 1.0 - 2.0 * (y * y + z * z);
     R[0][1] = 2.0 * (x * y - w * z);
@@ -651,11 +652,12 @@ static int row_spans(const float *mu, const float *s, const float *q, const int3
         for (int k = 0; k < 3; k++) S[j][k] = ((a[j][0] * a[k][0]) + (a[j][1] * a[k][1])) + (a[j][2] * a[k][2]);
     const double det = S[1][1] * S[2][2] - S[1][2] * S[1][2];
     if (!(det > 0.0) || !isfinite(det)) return 0;
-    const double by = (S[0][1] * S[2][2] - S[0][2] * S[1][2]) / det;
-    const double bz = (S[0][2] * S[1][1] - S[0][1] * S[1][2]) / det;
+    const double idet = 1.0 / det;
+    const double by = (S[0][1] * S[2][2] - S[0][2] * S[1][2]) * idet;
+    const double bz = (S[0][2] * S[1][1] - S[0][1] * S[1][2]) * idet;
     const double vc = S[0][0] - (by * S[0][1] + bz * S[0][2]);
     if (!(vc > 0.0) || !isfinite(vc)) return 0;
-    const double P00 = S[2][2] / det, P01 = -S[1][2] / det, P11 = S[1][1] / det;
+    const double P00 = S[2][2] * idet, P01 = -S[1][2] * idet, P11 = S[1][1] * idet;
     const double kz = -(P01 / P11), ky = -(P01 / P00);  /* edge vertices: z = kz y, y = ky z */
     const double Tq = (double)RCI * (double)RCI;
     const double icx = (double)cells[0] / ((double)ghi[0] - (double)glo[0]);

@@ -58,17 +58,23 @@ __device__ double rect_qmin(double P00, double P01, double P11, double kz, doubl
 // the conditional variance; the row keeps the cells of
 // [min c - wm, max c + wm], wm = sqrt((T' - min Q2) vc), with min Q2 over the
 // slab's rectangle and the extremes of c at its corners, or none when
-// min Q2 > T'. float64 throughout, each operation in this order. Returns
-// false (box not trimmed) for boxes with more than kSpanRows rows or kSpanNx
-// cells per row, or a degenerate marginal.
-__device__ bool row_spans(const float mu[3], const float s[3], const float q[4], const int lo_c[3],
-                          const int hi_c[3], const GridParams &g, float rci, uint8_t *__restrict__ out,
-                          uint64_t &count) {
+// min Q2 > T'. float64 throughout, each operation in this order. Boxes with
+// more than kSpanRows rows or kSpanNx cells per row, or a degenerate
+// marginal, keep every cell.
+struct SpanParams {
+    double P00, P01, P11, kz, ky, by, bz, vc;
+    float mu[3];
+    int x0, x1, y0, z0, ny;
+};
+
+__device__ bool span_setup(const float mu[3], const float s[3], const float q[4], const int lo_c[3],
+                           const int hi_c[3], SpanParams &p) {
     const int nx = hi_c[0] - lo_c[0] + 1, ny = hi_c[1] - lo_c[1] + 1, nz = hi_c[2] - lo_c[2] + 1;
     if (ny * nz > kSpanRows || nx > kSpanNx) return false;
     const double qw = q[0], qx = q[1], qy = q[2], qz = q[3];
     const double qn = sqrt(((qw * qw + qx * qx) + qy * qy) + qz * qz);
-    const double w = qw / qn, x = qx / qn, y = qy / qn, z = qz / qn;
+    const double iq = 1.0 / qn;
+    const double w = qw * iq, x = qx * iq, y = qy * iq, z = qz * iq;
     double R[3][3];
     R[0][0] = 1.0 - 2.0 * (y * y + z * z);
     R[0][1] = 2.0 * (x * y - w * z);
@@ -90,70 +96,95 @@ __device__ bool row_spans(const float mu[3], const float s[3], const float q[4],
         for (int k = 0; k < 3; ++k) S[j][k] = ((a[j][0] * a[k][0]) + (a[j][1] * a[k][1])) + (a[j][2] * a[k][2]);
     const double det = S[1][1] * S[2][2] - S[1][2] * S[1][2];
     if (!(det > 0.0) || !__builtin_isfinite(det)) return false;
-    const double by = (S[0][1] * S[2][2] - S[0][2] * S[1][2]) / det;
-    const double bz = (S[0][2] * S[1][1] - S[0][1] * S[1][2]) / det;
-    const double vc = S[0][0] - (by * S[0][1] + bz * S[0][2]);
-    if (!(vc > 0.0) || !__builtin_isfinite(vc)) return false;
-    const double P00 = S[2][2] / det, P01 = -S[1][2] / det, P11 = S[1][1] / det;
-    const double kz = -(P01 / P11), ky = -(P01 / P00);  // edge vertices: z = kz y, y = ky z
-    const double Tq = (double)rci * (double)rci;
-    const double icx = (double)g.cells[0] / ((double)g.hi[0] - (double)g.lo[0]);
-    const double wdy = ((double)g.hi[1] - (double)g.lo[1]) / (double)g.cells[1];
-    const double wdz = ((double)g.hi[2] - (double)g.lo[2]) / (double)g.cells[2];
-    uint64_t cnt = 0;
-    // every row byte starts empty; rows of the box are then written in turn
-    const uint32_t e4 = kSpanEmpty * 0x01010101u;
-#pragma unroll
-    for (int k = 0; k < kSpanRows / 16; ++k) ((uint4 *)out)[k] = make_uint4(e4, e4, e4, e4);
-    // rows r = (cy - y0) + ny (cz - z0), in increasing r
-    int r = 0;
-    for (int cz = lo_c[2]; cz <= hi_c[2]; ++cz)
-    for (int cy = lo_c[1]; cy <= hi_c[1]; ++cy, ++r) {
-        const double Y0 = ((double)g.lo[1] + (double)cy * wdy) - (double)mu[1];
-        const double Y1 = ((double)g.lo[1] + (double)(cy + 1) * wdy) - (double)mu[1];
-        const double Z0 = ((double)g.lo[2] + (double)cz * wdz) - (double)mu[2];
-        const double Z1 = ((double)g.lo[2] + (double)(cz + 1) * wdz) - (double)mu[2];
-        const double qmin = rect_qmin(P00, P01, P11, kz, ky, Y0, Y1, Z0, Z1);
-        uint32_t code = kSpanEmpty;
-        if (!(qmin > Tq)) {
-            int cl = lo_c[0], ch = hi_c[0];
-            const double wm = sqrt((Tq - qmin) * vc);
-            const double c00 = (double)mu[0] + (by * Y0 + bz * Z0), c01 = (double)mu[0] + (by * Y0 + bz * Z1);
-            const double c10 = (double)mu[0] + (by * Y1 + bz * Z0), c11 = (double)mu[0] + (by * Y1 + bz * Z1);
-            const double m0 = c00 < c01 ? c00 : c01, m1 = c10 < c11 ? c10 : c11;
-            const double M0 = c00 > c01 ? c00 : c01, M1 = c10 > c11 ? c10 : c11;
-            const double cmin = m0 < m1 ? m0 : m1, cmax = M0 > M1 ? M0 : M1;
-            const double fl = floor(((cmin - wm) - (double)g.lo[0]) * icx);
-            const double fh = floor(((cmax + wm) - (double)g.lo[0]) * icx);
-            if (__builtin_isfinite(fl) && __builtin_isfinite(fh)) {
-                cl = fl < (double)lo_c[0] ? lo_c[0] : (fl > (double)hi_c[0] ? hi_c[0] + 1 : (int)fl);
-                ch = fh > (double)hi_c[0] ? hi_c[0] : (fh < (double)lo_c[0] ? lo_c[0] - 1 : (int)fh);
-            }
-            if (cl <= ch) {
-                code = (uint32_t)(cl - lo_c[0]) | ((uint32_t)(ch - lo_c[0]) << 4);
-                cnt += (uint64_t)(ch - cl + 1);
-            }
-        }
-        out[r] = (uint8_t)code;
-    }
-    count = cnt;
+    const double idet = 1.0 / det;
+    p.by = (S[0][1] * S[2][2] - S[0][2] * S[1][2]) * idet;
+    p.bz = (S[0][2] * S[1][1] - S[0][1] * S[1][2]) * idet;
+    p.vc = S[0][0] - (p.by * S[0][1] + p.bz * S[0][2]);
+    if (!(p.vc > 0.0) || !__builtin_isfinite(p.vc)) return false;
+    p.P00 = S[2][2] * idet;
+    p.P01 = -S[1][2] * idet;
+    p.P11 = S[1][1] * idet;
+    p.kz = -(p.P01 / p.P11);  // edge vertices: z = kz y, y = ky z
+    p.ky = -(p.P01 / p.P00);
+    p.mu[0] = mu[0];
+    p.mu[1] = mu[1];
+    p.mu[2] = mu[2];
+    p.x0 = lo_c[0];
+    p.x1 = hi_c[0];
+    p.y0 = lo_c[1];
+    p.z0 = lo_c[2];
+    p.ny = ny;
     return true;
 }
 
-__global__ __launch_bounds__(kBlock) void k_preprocess(const float *__restrict__ mean, const float *__restrict__ scale,
+// Span code of row r of a box (kSpanEmpty or first | last << 4) and its
+// number of cells.
+struct SpanGrid {
+    double glo[3], icx, wdy, wdz, Tq;
+};
+
+__device__ uint32_t span_row(const SpanParams &p, int r, const SpanGrid &sg, uint32_t &len) {
+    const int cy = p.y0 + r % p.ny, cz = p.z0 + r / p.ny;
+    const double Y0 = (sg.glo[1] + (double)cy * sg.wdy) - (double)p.mu[1];
+    const double Y1 = (sg.glo[1] + (double)(cy + 1) * sg.wdy) - (double)p.mu[1];
+    const double Z0 = (sg.glo[2] + (double)cz * sg.wdz) - (double)p.mu[2];
+    const double Z1 = (sg.glo[2] + (double)(cz + 1) * sg.wdz) - (double)p.mu[2];
+    const double qmin = rect_qmin(p.P00, p.P01, p.P11, p.kz, p.ky, Y0, Y1, Z0, Z1);
+    len = 0;
+    if (qmin > sg.Tq) return kSpanEmpty;
+    int cl = p.x0, ch = p.x1;
+    const double wm = sqrt((sg.Tq - qmin) * p.vc);
+    const double mx = (double)p.mu[0];
+    const double c00 = mx + (p.by * Y0 + p.bz * Z0), c01 = mx + (p.by * Y0 + p.bz * Z1);
+    const double c10 = mx + (p.by * Y1 + p.bz * Z0), c11 = mx + (p.by * Y1 + p.bz * Z1);
+    const double m0 = c00 < c01 ? c00 : c01, m1 = c10 < c11 ? c10 : c11;
+    const double M0 = c00 > c01 ? c00 : c01, M1 = c10 > c11 ? c10 : c11;
+    const double cmin = m0 < m1 ? m0 : m1, cmax = M0 > M1 ? M0 : M1;
+    const double fl = floor(((cmin - wm) - sg.glo[0]) * sg.icx);
+    const double fh = floor(((cmax + wm) - sg.glo[0]) * sg.icx);
+    if (__builtin_isfinite(fl) && __builtin_isfinite(fh)) {
+        cl = fl < (double)p.x0 ? p.x0 : (fl > (double)p.x1 ? p.x1 + 1 : (int)fl);
+        ch = fh > (double)p.x1 ? p.x1 : (fh < (double)p.x0 ? p.x0 - 1 : (int)fh);
+    }
+    if (cl > ch) return kSpanEmpty;
+    len = (uint32_t)(ch - cl + 1);
+    return (uint32_t)(cl - p.x0) | ((uint32_t)(ch - p.x0) << 4);
+}
+
+constexpr int kPreBlock = kWave;  // one wave per workgroup: the span walk is per wave
+
+__global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restrict__ mean, const float *__restrict__ scale,
                                                        const float *__restrict__ rot, const float *__restrict__ value,
                                                        const float *__restrict__ weight, int64_t n, GridParams g,
                                                        float rci, Record *__restrict__ rec, CellBox *__restrict__ box,
                                                        uint8_t *__restrict__ spans, uint64_t *__restrict__ count) {
+    // span parameters of the wave's boxes, one array per field (lane stride
+    // 4 or 8 bytes: no bank conflicts)
+    __shared__ double sp_d[8][kPreBlock];
+    __shared__ float sp_f[3][kPreBlock];
+    __shared__ int sp_i[5][kPreBlock];
+    // span bytes, word w of box t holding rows 4w..4w+3 at sp_code[w][t]
+    __shared__ uint32_t sp_code[kSpanRows / 4][kPreBlock];
+    __shared__ uint32_t sp_cnt[kPreBlock];
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t tid = threadIdx.x, lane = tid % kWave, wbase = tid - lane;
     if (i == n) count[n] = 0;
-    if (i >= n) return;
-    const float mu[3] = {mean[3 * i], mean[3 * i + 1], mean[3 * i + 2]};
-    const float s[3] = {scale[3 * i], scale[3 * i + 1], scale[3 * i + 2]};
-    const float q[4] = {rot[4 * i], rot[4 * i + 1], rot[4 * i + 2], rot[4 * i + 3]};
-    const float v = value[i], w = weight[i];
+    const bool active = i < n;
+    float mu[3] = {0.0f, 0.0f, 0.0f}, s[3] = {1.0f, 1.0f, 1.0f}, q[4] = {1.0f, 0.0f, 0.0f, 0.0f};
+    float v = 0.0f, w = 0.0f;
+    if (active) {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            mu[j] = mean[3 * i + j];
+            s[j] = scale[3 * i + j];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) q[j] = rot[4 * i + j];
+        v = value[i];
+        w = weight[i];
+    }
 
-    bool valid = finite_f(v) && finite_f(w);
+    bool valid = active && finite_f(v) && finite_f(w);
 #pragma unroll
     for (int j = 0; j < 3; ++j) valid = valid && finite_f(mu[j]) && finite_f(s[j]) && (s[j] > 0.0f);
 #pragma unroll
@@ -197,23 +228,110 @@ __global__ __launch_bounds__(kBlock) void k_preprocess(const float *__restrict__
         hi_c[0] = hi_c[1] = hi_c[2] = -1;
         cnt = 0;
     }
+    // row spans: every lane sets up its box, then the wave walks the rows of
+    // all its trimmed boxes 64 at a time (a lane finds its box by comparing
+    // with the boxes' row ends, read with readlane)
     bool trimmed = false;
-    if (valid) {
-        uint64_t tc = 0;
-        trimmed = row_spans(mu, s, q, lo_c, hi_c, g, rci, spans + (size_t)i * kSpanRows, tc);
-        if (trimmed) cnt = tc;
+    {
+        SpanParams sp;
+        if (valid) trimmed = span_setup(mu, s, q, lo_c, hi_c, sp);
+        if (trimmed) {
+            sp_d[0][tid] = sp.P00;
+            sp_d[1][tid] = sp.P01;
+            sp_d[2][tid] = sp.P11;
+            sp_d[3][tid] = sp.kz;
+            sp_d[4][tid] = sp.ky;
+            sp_d[5][tid] = sp.by;
+            sp_d[6][tid] = sp.bz;
+            sp_d[7][tid] = sp.vc;
+            sp_f[0][tid] = sp.mu[0];
+            sp_f[1][tid] = sp.mu[1];
+            sp_f[2][tid] = sp.mu[2];
+            sp_i[0][tid] = sp.x0;
+            sp_i[1][tid] = sp.x1;
+            sp_i[2][tid] = sp.y0;
+            sp_i[3][tid] = sp.z0;
+            sp_i[4][tid] = sp.ny;
+        }
     }
+    const uint32_t nrows = trimmed ? (uint32_t)((hi_c[1] - lo_c[1] + 1) * (hi_c[2] - lo_c[2] + 1)) : 0u;
+#pragma unroll
+    for (int k = 0; k < kSpanRows / 4; ++k) sp_code[k][tid] = kSpanEmpty * 0x01010101u;
+    sp_cnt[tid] = 0;
+    SpanGrid sg;
+    sg.glo[0] = (double)g.lo[0];
+    sg.glo[1] = (double)g.lo[1];
+    sg.glo[2] = (double)g.lo[2];
+    sg.icx = (double)g.cells[0] / ((double)g.hi[0] - (double)g.lo[0]);
+    sg.wdy = ((double)g.hi[1] - (double)g.lo[1]) / (double)g.cells[1];
+    sg.wdz = ((double)g.hi[2] - (double)g.lo[2]) / (double)g.cells[2];
+    sg.Tq = (double)rci * (double)rci;
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t incl = wave_incl_sum(nrows);
+    const uint32_t E = __builtin_amdgcn_readlane(incl, 63);
+    const uint32_t excl = incl - nrows;
+    uint32_t j0 = 0;  // first box whose rows are not finished before the window
+    for (uint32_t e0 = 0; e0 < E; e0 += kWave) {
+        while (j0 + 1 < (uint32_t)kWave && __builtin_amdgcn_readlane(incl, j0) <= e0) ++j0;
+        const uint32_t e = e0 + lane;
+        // owner box o of element e and the element where o's rows begin
+        uint32_t o = j0, base = __builtin_amdgcn_readlane(excl, j0);
+        for (uint32_t jb = j0; jb + 1 < (uint32_t)kWave; ++jb) {
+            const uint32_t bnd = __builtin_amdgcn_readlane(incl, jb);
+            if (bnd >= e0 + kWave) break;
+            if (e >= bnd) {
+                o = jb + 1;
+                base = bnd;
+            }
+        }
+        if (e < E) {
+            uint32_t len;
+            const int r = (int)(e - base);
+            const uint32_t t = wbase + o;
+            SpanParams sp;
+            sp.P00 = sp_d[0][t];
+            sp.P01 = sp_d[1][t];
+            sp.P11 = sp_d[2][t];
+            sp.kz = sp_d[3][t];
+            sp.ky = sp_d[4][t];
+            sp.by = sp_d[5][t];
+            sp.bz = sp_d[6][t];
+            sp.vc = sp_d[7][t];
+            sp.mu[0] = sp_f[0][t];
+            sp.mu[1] = sp_f[1][t];
+            sp.mu[2] = sp_f[2][t];
+            sp.x0 = sp_i[0][t];
+            sp.x1 = sp_i[1][t];
+            sp.y0 = sp_i[2][t];
+            sp.z0 = sp_i[3][t];
+            sp.ny = sp_i[4][t];
+            const uint32_t code = span_row(sp, r, sg, len);
+            ((uint8_t *)&sp_code[r >> 2][t])[r & 3] = (uint8_t)code;
+            atomicAdd(&sp_cnt[wbase + o], len);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (trimmed) {
+        cnt = sp_cnt[tid];
+        uint4 *dst = (uint4 *)(spans + (size_t)i * kSpanRows);
+#pragma unroll
+        for (int k = 0; k < kSpanRows / 16; ++k)
+            dst[k] = make_uint4(sp_code[4 * k][tid], sp_code[4 * k + 1][tid], sp_code[4 * k + 2][tid],
+                                sp_code[4 * k + 3][tid]);
+    }
+    if (!active) return;
     count[i] = cnt;
     CellBox b;
     b.lo = make_int4(lo_c[0], lo_c[1], lo_c[2], trimmed ? 1 : 0);
     b.hi = make_int4(hi_c[0], hi_c[1], hi_c[2], 0);
     box[i] = b;
 
-    // evaluation record: M = S^-1 R^T formed in float64, rounded once
+    // evaluation record: M = S^-1 R^T formed in float64, rounded once to float32
     Record r;
     if (valid) {
         const double qn = sqrt((double)q[0] * q[0] + (double)q[1] * q[1] + (double)q[2] * q[2] + (double)q[3] * q[3]);
-        const double w_ = q[0] / qn, x = q[1] / qn, y = q[2] / qn, z = q[3] / qn;
+        const double iq = 1.0 / qn;
+        const double w_ = q[0] * iq, x = q[1] * iq, y = q[2] * iq, z = q[3] * iq;
         double Rd[3][3];
         Rd[0][0] = 1.0 - 2.0 * (y * y + z * z);
         Rd[0][1] = 2.0 * (x * y - w_ * z);
@@ -226,9 +344,11 @@ __global__ __launch_bounds__(kBlock) void k_preprocess(const float *__restrict__
         Rd[2][2] = 1.0 - 2.0 * (x * x + y * y);
         float M[3][3];
 #pragma unroll
-        for (int k = 0; k < 3; ++k)
+        for (int k = 0; k < 3; ++k) {
+            const double is = 1.0 / (double)s[k];
 #pragma unroll
-            for (int j = 0; j < 3; ++j) M[k][j] = (float)(Rd[j][k] / (double)s[k]);
+            for (int j = 0; j < 3; ++j) M[k][j] = (float)(Rd[j][k] * is);
+        }
         r.r0 = make_float4(mu[0], mu[1], mu[2], w);
         r.r1 = make_float4(M[0][0], M[0][1], M[0][2], v);
         r.r2 = make_float4(M[1][0], M[1][1], M[1][2], 0.0f);
@@ -408,9 +528,9 @@ hipError_t launch_preprocess(const float *mean, const float *scale, const float 
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
                              CellBox *box, uint8_t *spans, uint64_t *count, hipStream_t s) {
     const int64_t threads = n + 1;
-    const uint32_t blocks = (uint32_t)((threads + kBlock - 1) / kBlock);
+    const uint32_t blocks = (uint32_t)((threads + kPreBlock - 1) / kPreBlock);
     prof_begin("preprocess", s);
-    hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kBlock), 0, s, mean, scale, rot, value, weight, n, g, rci, rec,
+    hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kPreBlock), 0, s, mean, scale, rot, value, weight, n, g, rci, rec,
                        box, spans, count);
     prof_end("preprocess", s);
     return hipGetLastError();
