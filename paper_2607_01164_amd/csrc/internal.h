@@ -191,7 +191,7 @@ hipError_t exclusive_scan_u64(const uint64_t *in, uint64_t *out, int64_t n, void
 // pairs; radix_passes(bits) tells which one holds the result.
 struct RadixLayout {
     uint32_t *table;       // [ndig][nb] tile counts, scanned in place
-    uint32_t *digit_base;  // [ndig]
+    uint32_t *digit_tot;   // [ndig] digit totals of the pass
     uint32_t nb;           // tiles
     int passes, dbits;
     size_t bytes;

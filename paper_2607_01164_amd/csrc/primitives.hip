@@ -104,9 +104,9 @@ int64_t scan_levels_elems(int64_t n) {
 // ---------------------------------------------------------------------------
 // Radix sort (stable LSD, reduce-then-scan). Per pass: tile histograms of
 // the digit (the first pass's can come from the kernel that produced the
-// keys), an exclusive scan of every digit's row of tile counts plus one of
-// the digit totals, and a scatter that ranks each tile in LDS and writes it
-// out digit by digit.
+// keys), an exclusive scan of every digit's row of tile counts that also
+// yields the digit totals, and a scatter that scans the totals, ranks its
+// tile in LDS and writes it out digit by digit.
 
 int passes_for(int bits) { return bits <= 0 ? 0 : (bits + kMaxDigitBits - 1) / kMaxDigitBits; }
 int digit_bits_for(int bits) {
@@ -160,28 +160,6 @@ __global__ __launch_bounds__(kBlock) void k_digit_scan(uint32_t *__restrict__ ta
     if (threadIdx.x == 0) digit_tot[blockIdx.x] = carry;
 }
 
-// exclusive scan of the digit totals (ndig <= 1024) in place
-__global__ __launch_bounds__(kBlock) void k_digit_base(uint32_t *__restrict__ digit, uint32_t ndig) {
-    __shared__ uint32_t lds[kWavesPerBlock];
-    constexpr int J = kMaxDigits / kBlock;
-    uint32_t v[J];
-    uint32_t s = 0;
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-        const uint32_t d = threadIdx.x * J + j;
-        v[j] = d < ndig ? digit[d] : 0u;
-        s += v[j];
-    }
-    uint32_t tot;
-    uint32_t run = block_excl_scan(s, lds, &tot);
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-        const uint32_t d = threadIdx.x * J + j;
-        if (d < ndig) digit[d] = run;
-        run += v[j];
-    }
-}
-
 // Stable scatter of one tile of kSortTile keys. Each wave ranks its
 // kSortItems rows of 64 keys in order: lanes holding the same digit are
 // found with one ballot per digit bit, and a per-wave running count per
@@ -193,7 +171,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
                                                             uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
                                                             int64_t n, int shift, int dbits,
                                                             const uint32_t *__restrict__ table,
-                                                            const uint32_t *__restrict__ digit_base, uint32_t nb) {
+                                                            const uint32_t *__restrict__ digit_tot, uint32_t nb) {
     extern __shared__ uint32_t lds[];
     __shared__ uint32_t scan_lds[kWavesPerBlock];
     const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -206,13 +184,6 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     uint32_t *dglob = dstart + ndig;
     uint32_t *sk = dglob + ndig;                 // [kSortTile]
     uint32_t *sv = sk + kSortTile;               // [kSortTile]
-    for (uint32_t d = tid; d < ndig; d += kBlock) {
-#pragma unroll
-        for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w * ndig + d] = 0;
-        dglob[d] = digit_base[d] + table[(size_t)d * nb + tile];
-    }
-    __syncthreads();
-
     const int64_t base = (int64_t)tile * kSortTile + (int64_t)wave * (kWave * kSortItems);
     uint32_t k[kSortItems], v[kSortItems], r[kSortItems];
 #pragma unroll
@@ -222,6 +193,36 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
         k[i] = ok ? kin[idx] : 0u;
         v[i] = ok ? vin[idx] : 0u;
     }
+    // output start of every digit in this tile: the exclusive scan of the
+    // digit totals plus the tile's place in its digit's row (all loads are
+    // issued before the first wait)
+    constexpr int J = kMaxDigits / kBlock;
+    uint32_t loc[J], tpre[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const uint32_t d = tid * J + j;
+        loc[j] = d < ndig ? digit_tot[d] : 0u;
+        tpre[j] = d < ndig ? table[(size_t)d * nb + tile] : 0u;
+    }
+    for (uint32_t d = tid; d < ndig; d += kBlock) {
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w * ndig + d] = 0;
+    }
+    {
+        uint32_t s = 0;
+#pragma unroll
+        for (int j = 0; j < J; ++j) s += loc[j];
+        uint32_t tot;
+        uint32_t run = block_excl_scan(s, scan_lds, &tot);
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const uint32_t d = tid * J + j;
+            if (d < ndig) dglob[d] = run + tpre[j];
+            run += loc[j];
+        }
+    }
+    __syncthreads();
+
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     uint32_t *mycnt = wcnt + wave * ndig;
 #pragma unroll
@@ -247,7 +248,6 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     }
     __syncthreads();
     // per digit: exclusive scan over the waves (in place) and the tile total
-    constexpr int J = kMaxDigits / kBlock;
     for (uint32_t d = tid; d < ndig; d += kBlock) {
         uint32_t s = 0;
 #pragma unroll
@@ -306,17 +306,32 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     }
 }
 
-// offsets[k] = number of keys < k: thread t looks at the boundaries after
-// keys t*8-1 .. t*8+7 of the sorted array
+// offsets[k] = number of keys < k. Thread t covers the boundaries before
+// keys 4t .. 4t+3 (and the end, after key n-1), reading its four keys with
+// one 16-byte load where the array is 16-byte aligned.
 __global__ __launch_bounds__(kBlock) void k_key_offsets(const uint32_t *__restrict__ keys, int64_t n,
                                                         uint32_t *__restrict__ off, int64_t nkeys) {
-    const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+    const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
     if (i0 > n) return;
+    uint32_t k4[4];
+    if (i0 + 4 <= n && (reinterpret_cast<uintptr_t>(keys) & 15u) == 0) {
+        const uint4 q = *(const uint4 *)(keys + i0);
+        k4[0] = q.x;
+        k4[1] = q.y;
+        k4[2] = q.z;
+        k4[3] = q.w;
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) k4[i] = i0 + i < n ? keys[i0 + i] : 0u;
+    }
     int64_t prev = (i0 == 0) ? -1 : (int64_t)keys[i0 - 1];
-    for (int64_t i = i0; i < i0 + 8 && i <= n; ++i) {
-        int64_t cur = (i == n) ? nkeys : (int64_t)keys[i];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t idx = i0 + i;
+        if (idx > n) break;
+        int64_t cur = idx == n ? nkeys : (int64_t)k4[i];
         cur = cur < nkeys ? cur : nkeys;
-        for (int64_t k = prev + 1; k <= cur; ++k) off[k] = (uint32_t)i;
+        for (int64_t k = prev + 1; k <= cur; ++k) off[k] = (uint32_t)idx;
         prev = cur > prev ? cur : prev;
     }
 }
@@ -362,7 +377,7 @@ RadixLayout radix_layout(void *work, int64_t n, int bits) {
     char *b = (char *)work;
     L.table = (uint32_t *)b;
     const size_t tbytes = ((size_t)ndig * L.nb * 4 + 255) & ~(size_t)255;
-    L.digit_base = b ? (uint32_t *)(b + tbytes) : nullptr;
+    L.digit_tot = b ? (uint32_t *)(b + tbytes) : nullptr;
     L.bytes = tbytes + (((size_t)ndig * 4 + 255) & ~(size_t)255);
     return L;
 }
@@ -410,13 +425,12 @@ hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
         prof_begin("radix_scan", s);
-        hipLaunchKernelGGL(k_digit_scan, dim3(ndig), dim3(kBlock), 0, s, L.table, L.nb, L.digit_base);
-        hipLaunchKernelGGL(k_digit_base, dim3(1), dim3(kBlock), 0, s, L.digit_base, ndig);
+        hipLaunchKernelGGL(k_digit_scan, dim3(ndig), dim3(kBlock), 0, s, L.table, L.nb, L.digit_tot);
         prof_end("radix_scan", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         prof_begin("radix_downsweep", s);
         hipLaunchKernelGGL(k_radix_downsweep, dim3(L.nb), dim3(kBlock), lds, s, ki, vi, ko, vo, n, shift, L.dbits,
-                           L.table, L.digit_base, L.nb);
+                           L.table, L.digit_tot, L.nb);
         prof_end("radix_downsweep", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         uint32_t *tk = ki, *tv = vi;
@@ -429,7 +443,7 @@ hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *
 }
 
 hipError_t key_offsets(const uint32_t *sorted_keys, int64_t n, uint32_t *offsets, int64_t nkeys, hipStream_t s) {
-    const int64_t threads = n / 8 + 1;
+    const int64_t threads = n / 4 + 1;
     prof_begin("key_offsets", s);
     hipLaunchKernelGGL(k_key_offsets, dim3((uint32_t)ceil_div(threads, kBlock)), dim3(kBlock), 0, s, sorted_keys, n,
                        offsets, nkeys);

@@ -144,6 +144,33 @@ def test_backward_with_empty_rows_and_boxes():
     check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="corner")
 
 
+@pytest.mark.parametrize("case", ["one cell", "one pair"])
+def test_index_and_backward_without_sort_passes(case):
+    """Indexes whose pair sort runs no radix pass: a grid of one cell (every
+    key is 0) and an index holding a single pair. The pair ids and the
+    emit-to-sorted map the backward reads still come out right."""
+    if case == "one cell":
+        g = synth.random_gaussians(75, 40, log_mu=np.log(0.08))
+        cells = (1, 1, 1)
+        pts = synth.random_points(76, 3000)
+    else:
+        g = synth.random_gaussians(77, 1, log_mu=np.log(0.008), log_sd=0.1)
+        g.mean[0] = [0.55, 0.55, 0.55]
+        cells = (10, 10, 10)
+        pts = g.mean + synth.random_normal(78, 30).reshape(10, 3).astype(np.float32) * 0.005
+    log("case sort without passes:", case)
+    r = Run(g, cells, "points", points=pts)
+    if case == "one pair":
+        assert r.index.n_pairs == 1
+    check_index(r)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label=case)
+    gv, gi = synth.random_normal(79, r.nq), synth.random_normal(80, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label=case)
+
+
 def test_point_plan_order_matches_oracle():
     """The query ordering kept in the plan (Sec. 5.1 analogue of the sample
     BVH): keys and ids bit-exact against the oracle's stable order."""
