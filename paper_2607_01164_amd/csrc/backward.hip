@@ -53,19 +53,60 @@ __device__ __forceinline__ void alpha_beta(float phi, float inf, float gp, float
 // Cotangent staging for ordered queries: (alpha, beta) of the k-th
 // query in plan order, from the forward's (Phi, I) that the plan keeps in
 // that order; only the cotangents are gathered by query id.
+constexpr int kStageItems = 4;  // queries per thread of the point staging
+
+// Thread t stages queries 4t .. 4t+3 with 16-byte loads of their ids and
+// outputs, so the eight cotangent gathers of a thread are in flight together.
 __global__ __launch_bounds__(kBlock) void k_stage_points(int64_t n, const uint32_t *__restrict__ order,
                                                          const float2 *__restrict__ plan_out,
                                                          const float *__restrict__ gval, const float *__restrict__ ginf,
                                                          float2 *__restrict__ ab) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    const float2 o = plan_out[k];
-    float al = 0.0f, be = 0.0f;
-    if (o.y > 0.0f) {
-        const uint32_t pid = order[k];
-        alpha_beta(o.x, o.y, gval[pid], ginf[pid], al, be);
+    const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kStageItems;
+    if (k0 >= n) return;
+    uint32_t pid[kStageItems];
+    float2 o[kStageItems];
+    if (k0 + kStageItems <= n) {
+        const uint4 p4 = *(const uint4 *)(order + k0);
+        const float4 o01 = *(const float4 *)(plan_out + k0), o23 = *(const float4 *)(plan_out + k0 + 2);
+        pid[0] = p4.x;
+        pid[1] = p4.y;
+        pid[2] = p4.z;
+        pid[3] = p4.w;
+        o[0] = make_float2(o01.x, o01.y);
+        o[1] = make_float2(o01.z, o01.w);
+        o[2] = make_float2(o23.x, o23.y);
+        o[3] = make_float2(o23.z, o23.w);
+    } else {
+#pragma unroll
+        for (int i = 0; i < kStageItems; ++i) {
+            const bool ok = k0 + i < n;
+            pid[i] = ok ? order[k0 + i] : 0u;
+            o[i] = ok ? plan_out[k0 + i] : make_float2(0.0f, 0.0f);
+        }
     }
-    ab[k] = make_float2(al, be);
+    float gv[kStageItems], gi[kStageItems];
+#pragma unroll
+    for (int i = 0; i < kStageItems; ++i) {
+        // undefined queries (I = 0) have no gradient: their cotangents are not read
+        const bool need = o[i].y > 0.0f;
+        gv[i] = need ? gval[pid[i]] : 0.0f;
+        gi[i] = need ? ginf[pid[i]] : 0.0f;
+    }
+    float2 r[kStageItems];
+#pragma unroll
+    for (int i = 0; i < kStageItems; ++i) {
+        float al, be;
+        alpha_beta(o[i].x, o[i].y, gv[i], gi[i], al, be);
+        r[i] = make_float2(al, be);
+    }
+    if (k0 + kStageItems <= n) {
+        *(float4 *)(ab + k0) = make_float4(r[0].x, r[0].y, r[1].x, r[1].y);
+        *(float4 *)(ab + k0 + 2) = make_float4(r[2].x, r[2].y, r[3].x, r[3].y);
+    } else {
+#pragma unroll
+        for (int i = 0; i < kStageItems; ++i)
+            if (k0 + i < n) ab[k0 + i] = r[i];
+    }
 }
 
 __global__ __launch_bounds__(kBlock) void k_stage_grid(int64_t n, const float *__restrict__ value,
@@ -325,12 +366,15 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
     const double m2s[6] = {ma.w, mb.x, mb.y, mb.z, mb.w, mc.x};
     const bool any = ma.x != 0.0f || ma.y != 0.0f || ma.z != 0.0f || ma.w != 0.0f || mb.x != 0.0f ||
                      mb.y != 0.0f || mb.z != 0.0f || mb.w != 0.0f || mc.x != 0.0f || mc.y != 0.0f || mc.z != 0.0f;
+    // the parameters are loaded with the moments, whatever these hold
+    const double s[3] = {scale[3 * i], scale[3 * i + 1], scale[3 * i + 2]};
+    const double q[4] = {rot[4 * i], rot[4 * i + 1], rot[4 * i + 2], rot[4 * i + 3]};
     double dmu[3] = {0, 0, 0}, ds[3] = {0, 0, 0}, dq[4] = {0, 0, 0, 0};
     if (any) {
-        const double s[3] = {scale[3 * i], scale[3 * i + 1], scale[3 * i + 2]};
-        const double q[4] = {rot[4 * i], rot[4 * i + 1], rot[4 * i + 2], rot[4 * i + 3]};
+        const double is[3] = {1.0 / s[0], 1.0 / s[1], 1.0 / s[2]};
         const double qn = sqrt(q[0] * q[0] + q[1] * q[1] + q[2] * q[2] + q[3] * q[3]);
-        const double w = q[0] / qn, x = q[1] / qn, y = q[2] / qn, z = q[3] / qn;
+        const double iqn = 1.0 / qn;
+        const double w = q[0] * iqn, x = q[1] * iqn, y = q[2] * iqn, z = q[3] * iqn;
         double R[3][3];
         R[0][0] = 1.0 - 2.0 * (y * y + z * z);
         R[0][1] = 2.0 * (x * y - w * z);
@@ -350,16 +394,16 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
         M2[2][2] = m2s[5];
         for (int j = 0; j < 3; ++j) {
             double acc = 0.0;
-            for (int k = 0; k < 3; ++k) acc += R[j][k] * m1[k] / s[k];
+            for (int k = 0; k < 3; ++k) acc += R[j][k] * m1[k] * is[k];
             dmu[j] = -2.0 * acc;
         }
-        for (int k = 0; k < 3; ++k) ds[k] = -2.0 * M2[k][k] / s[k];
+        for (int k = 0; k < 3; ++k) ds[k] = -2.0 * M2[k][k] * is[k];
         double G[3][3];
         for (int j = 0; j < 3; ++j)
             for (int k = 0; k < 3; ++k) {
                 double acc = 0.0;
                 for (int mm = 0; mm < 3; ++mm) acc += R[j][mm] * s[mm] * M2[mm][k];
-                G[j][k] = 2.0 * acc / s[k];
+                G[j][k] = 2.0 * acc * is[k];
             }
         double dqh[4];
         dqh[0] = 2.0 * (-z * G[0][1] + y * G[0][2] + z * G[1][0] - x * G[1][2] - y * G[2][0] + x * G[2][1]);
@@ -371,7 +415,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
                         y * G[1][2] + x * G[2][0] + y * G[2][1]);
         const double dot = w * dqh[0] + x * dqh[1] + y * dqh[2] + z * dqh[3];
         const double qh[4] = {w, x, y, z};
-        for (int k = 0; k < 4; ++k) dq[k] = (dqh[k] - qh[k] * dot) / qn;
+        for (int k = 0; k < 4; ++k) dq[k] = (dqh[k] - qh[k] * dot) * iqn;
     }
     for (int j = 0; j < 3; ++j) {
         d_mean[3 * i + j] = (float)dmu[j];
@@ -403,8 +447,8 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
             hipLaunchKernelGGL(k_stage_grid, dim3(qblocks), dim3(kBlock), 0, s, q.n, value, influence, grad_value,
                                grad_influence, b.ab);
         else
-            hipLaunchKernelGGL(k_stage_points, dim3(qblocks), dim3(kBlock), 0, s, q.n, order, plan_out, grad_value,
-                               grad_influence, b.ab);
+            hipLaunchKernelGGL(k_stage_points, dim3((uint32_t)((q.n + kBlock * kStageItems - 1) / (kBlock * kStageItems))),
+                               dim3(kBlock), 0, s, q.n, order, plan_out, grad_value, grad_influence, b.ab);
         prof_end("bwd_stage", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         const uint32_t wblocks = (uint32_t)((n_gauss + kWavesPerBlock - 1) / kWavesPerBlock);
