@@ -250,13 +250,23 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
         }
         const uint32_t nry = ny * ry, R = nry * nz * rz;
         const uint32_t vx0 = (uint32_t)b.lo.x * rx;
+        // row -> (yy, zz) by a float reciprocal: (row + 1/2) / nry lies at
+        // least 1/(2 nry) from an integer, which the rounding error
+        // (< row 2^-22 / nry) cannot cross while row < 2^21
+        const bool fdiv = R < (1u << 21);
+        const float inry = 1.0f / (float)nry;
         for (uint32_t rb = 0; rb < R; rb += kWave) {
             // lane l describes row rb + l: its first element and its length
             const uint32_t row = rb + lane;
             uint32_t start = 0, len = 0, rx0 = vx0;
             float rpy = 0.0f, rpz = 0.0f;
             if (row < R) {
-                const uint32_t yy = row % nry, zz = row / nry;
+                uint32_t zz;
+                if (fdiv)
+                    zz = (uint32_t)(((float)row + 0.5f) * inry);
+                else
+                    zz = row / nry;
+                const uint32_t yy = row - zz * nry;
                 // the row's run of cells: the whole box row, or its span
                 uint32_t xa = 0, xn = nx;
                 if (b.lo.w) {
@@ -281,28 +291,30 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
             const uint32_t nrows = (R - rb) < (uint32_t)kWave ? (R - rb) : (uint32_t)kWave;
             const uint32_t incl = wave_incl_sum(len);  // end of row l in the concatenation
             const uint32_t E = __builtin_amdgcn_readlane(incl, 63);
-            const uint32_t kofs = start - (incl - len);  // element e of row l is point e + kofs
-            const uint32_t xofs = rx0 - (incl - len);    // grids: element e of row l has x = e + xofs
             if (E == 0) continue;  // no query in these rows
-            uint32_t j0 = 0;       // first row not finished before the window
+            const uint32_t rbeg = incl - len;          // first element of row l
+            const uint32_t kofs = start - rbeg;        // element e of row l is point e + kofs
+            const uint32_t xofs = rx0 - rbeg;          // grids: element e of row l has x = e + xofs
             for (uint32_t e0 = 0; e0 < E; e0 += kWave) {
-                // e0 < E, so the row holding element e0 is below nrows
-                while (j0 + 1 < nrows && __builtin_amdgcn_readlane(incl, j0) <= e0) ++j0;
+                // rbeg rises with the lane (lanes past nrows hold E), so the
+                // rows starting at or before e0 are a prefix of the lanes and
+                // the last of them holds element e0
+                const uint32_t j0 = (uint32_t)__popcll(__ballot(rbeg <= e0)) - 1u;
                 const uint32_t e = e0 + lane;
-                uint32_t j = j0;
-                uint32_t ko = __builtin_amdgcn_readlane(kofs, j), xo = 0;
+                uint32_t ko = __builtin_amdgcn_readlane(kofs, j0), xo = 0;
                 float py = 0.0f, pz = 0.0f;
                 if (GRID) {
-                    xo = __builtin_amdgcn_readlane(xofs, j);
-                    py = readlane_f(rpy, j);
-                    pz = readlane_f(rpz, j);
+                    xo = __builtin_amdgcn_readlane(xofs, j0);
+                    py = readlane_f(rpy, j0);
+                    pz = readlane_f(rpz, j0);
                 }
-                // row ends inside the window move the later lanes on
-                while (j + 1 < nrows) {
-                    const uint32_t bnd = __builtin_amdgcn_readlane(incl, j);
-                    if (bnd >= e0 + kWave) break;
-                    const bool nxt = e >= bnd;
-                    ++j;
+                // rows starting inside the window move the later lanes on, in
+                // row order (an empty row is overridden by the next)
+                uint64_t inw = __ballot(lane < nrows && rbeg - e0 - 1u < (uint32_t)kWave - 1u);
+                while (inw != 0) {
+                    const uint32_t j = (uint32_t)__builtin_ctzll(inw);
+                    inw &= inw - 1;
+                    const bool nxt = e >= __builtin_amdgcn_readlane(rbeg, j);
                     ko = nxt ? __builtin_amdgcn_readlane(kofs, j) : ko;
                     if (GRID) {
                         xo = nxt ? __builtin_amdgcn_readlane(xofs, j) : xo;

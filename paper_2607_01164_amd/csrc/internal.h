@@ -132,13 +132,17 @@ __device__ __forceinline__ uint32_t wave_max_uniform(uint32_t x) {
 }
 
 // Inclusive scan of a 32-bit value across the 64 lanes of a wave (sum or max).
+// The sum runs on DPP alone and needs all 64 lanes active: row_shr 1, 2, 4,
+// 8 scan each row of 16 (lanes without a source add 0), then row_bcast:15
+// adds row 0's total to row 1 and row 2's to row 3, and row_bcast:31 adds the
+// total of rows 0-1 to rows 2 and 3.
 __device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x) {
-    const uint32_t lane = lane_id();
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        uint32_t y = __shfl_up(x, o, 64);
-        if (lane >= (uint32_t)o) x += y;
-    }
+    x += dpp_u<0x111>(x);
+    x += dpp_u<0x112>(x);
+    x += dpp_u<0x114>(x);
+    x += dpp_u<0x118>(x);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);
     return x;
 }
 
