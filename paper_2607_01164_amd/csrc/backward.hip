@@ -171,7 +171,7 @@ __device__ __forceinline__ float tr_step(float lo, float hi, bool bit) {
 // (lanes 11..15 return 0). Four transposed steps inside each row of 16
 // (lane bits 0, 1, 2, 3 through quad_perm [1,0,3,2], quad_perm [2,3,0,1],
 // row_ror:4, row_ror:8) leave lane l holding element l & 15 summed over its
-// row; two xor shuffles then add the four rows.
+// row; an xor-16 swizzle and an xor-32 permute then add the four rows.
 __device__ __forceinline__ float reduce11(const float v[11], uint32_t lane) {
     const bool b0 = lane & 1u, b1 = lane & 2u, b2 = lane & 4u, b3 = lane & 8u;
     float w[6];
@@ -184,8 +184,8 @@ __device__ __forceinline__ float reduce11(const float v[11], uint32_t lane) {
     const float y0 = tr_step<0x124>(x[0], x[1], b2);
     const float y1 = tr_step<0x124>(x[2], 0.0f, b2);
     float z = tr_step<0x128>(y0, y1, b3);
-    z += __shfl_xor(z, 16, 64);
-    z += __shfl_xor(z, 32, 64);
+    z += swz_xor16(z);
+    z += perm_xor32(z, lane);
     return z;
 }
 
@@ -251,10 +251,11 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
         const uint32_t nry = ny * ry, R = nry * nz * rz;
         const uint32_t vx0 = (uint32_t)b.lo.x * rx;
         // row -> (yy, zz) by a float reciprocal: (row + 1/2) / nry lies at
-        // least 1/(2 nry) from an integer, which the rounding error
-        // (< row 2^-22 / nry) cannot cross while row < 2^21
+        // least 1/(2 nry) from an integer; v_rcp (1 ulp) and the product
+        // err by less than 1.5 2^-23 (row + 1/2) / nry, which cannot cross
+        // it while row < 2^21
         const bool fdiv = R < (1u << 21);
-        const float inry = 1.0f / (float)nry;
+        const float inry = __builtin_amdgcn_rcpf((float)nry);
         for (uint32_t rb = 0; rb < R; rb += kWave) {
             // lane l describes row rb + l: its first element and its length
             const uint32_t row = rb + lane;
@@ -299,9 +300,10 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                 // rbeg rises with the lane (lanes past nrows hold E), so the
                 // rows starting at or before e0 are a prefix of the lanes and
                 // the last of them holds element e0
-                const uint32_t j0 = (uint32_t)__popcll(__ballot(rbeg <= e0)) - 1u;
+                const uint32_t j0 = (uint32_t)__popcll(ballot(rbeg <= e0)) - 1u;
                 const uint32_t e = e0 + lane;
-                uint32_t ko = __builtin_amdgcn_readlane(kofs, j0), xo = 0;
+                const uint32_t ko0 = __builtin_amdgcn_readlane(kofs, j0);  // row of element e0
+                uint32_t ko = ko0, xo = 0;
                 float py = 0.0f, pz = 0.0f;
                 if (GRID) {
                     xo = __builtin_amdgcn_readlane(xofs, j0);
@@ -310,7 +312,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                 }
                 // rows starting inside the window move the later lanes on, in
                 // row order (an empty row is overridden by the next)
-                uint64_t inw = __ballot(lane < nrows && rbeg - e0 - 1u < (uint32_t)kWave - 1u);
+                uint64_t inw = ballot(lane < nrows && rbeg - e0 - 1u < (uint32_t)kWave - 1u);
                 while (inw != 0) {
                     const uint32_t j = (uint32_t)__builtin_ctzll(inw);
                     inw &= inw - 1;
@@ -322,20 +324,20 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                         pz = nxt ? readlane_f(rpz, j) : pz;
                     }
                 }
+                // lanes past the last element load the window's first point
+                // again; their test has no effect
                 const bool valid = e < E;
-                const uint32_t k = e + ko;
-                float u0 = 0.0f, u1 = 0.0f, u2 = 0.0f, Q = 0.0f;
-                if (valid) {
-                    if (GRID) {
-                        const float px = g.lo[0] + ((float)(e + xo) + 0.5f) * q.vsz[0];
-                        Q = whiten(r, px, py, pz, u0, u1, u2);
-                    } else {
-                        const float4 p = plan_pos[k];
-                        Q = whiten(r, p.x, p.y, p.z, u0, u1, u2);
-                    }
+                const uint32_t k = valid ? e + ko : e0 + ko0;
+                float u0, u1, u2, Q;
+                if (GRID) {
+                    const float px = g.lo[0] + ((float)(e + xo) + 0.5f) * q.vsz[0];
+                    Q = whiten(r, px, py, pz, u0, u1, u2);
+                } else {
+                    const float4 p = plan_pos[k];
+                    Q = whiten(r, p.x, p.y, p.z, u0, u1, u2);
                 }
                 const bool hit = valid && Q <= T;
-                const uint64_t mask = __ballot(hit);
+                const uint64_t mask = ballot(hit);
                 if (mask == 0) continue;
                 if (hit) {
                     const uint32_t pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),

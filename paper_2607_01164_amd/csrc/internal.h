@@ -105,6 +105,20 @@ __device__ __forceinline__ uint32_t dpp_u(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
 }
 
+// Ballot of a predicate that is already a lane mask (a comparison): no
+// round trip through a 0/1 integer.
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
+// x of lane l ^ 16, within each half of the wave (ds_swizzle, xor mask 16)
+__device__ __forceinline__ float swz_xor16(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+}
+
+// x of lane l ^ 32 (ds_bpermute; every lane must be active)
+__device__ __forceinline__ float perm_xor32(float x, uint32_t lane) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((int)((lane ^ 32u) << 2), __builtin_bit_cast(int, x)));
+}
+
 __device__ __forceinline__ float readlane_f(float x, uint32_t l) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), (int)l));
 }
