@@ -300,7 +300,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                 // rbeg rises with the lane (lanes past nrows hold E), so the
                 // rows starting at or before e0 are a prefix of the lanes and
                 // the last of them holds element e0
-                const uint32_t j0 = (uint32_t)__popcll(ballot(rbeg <= e0)) - 1u;
+                const uint32_t j0 = (uint32_t)__popcll(mask_le_u(rbeg, e0)) - 1u;
                 const uint32_t e = e0 + lane;
                 const uint32_t ko0 = __builtin_amdgcn_readlane(kofs, j0);  // row of element e0
                 uint32_t ko = ko0, xo = 0;
@@ -312,7 +312,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                 }
                 // rows starting inside the window move the later lanes on, in
                 // row order (an empty row is overridden by the next)
-                uint64_t inw = ballot(lane < nrows && rbeg - e0 - 1u < (uint32_t)kWave - 1u);
+                uint64_t inw = mask_lt_u(lane, nrows) & mask_lt_u(rbeg - e0 - 1u, (uint32_t)kWave - 1u);
                 while (inw != 0) {
                     const uint32_t j = (uint32_t)__builtin_ctzll(inw);
                     inw &= inw - 1;
@@ -337,7 +337,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                     Q = whiten(r, p.x, p.y, p.z, u0, u1, u2);
                 }
                 const bool hit = valid && Q <= T;
-                const uint64_t mask = ballot(hit);
+                const uint64_t mask = mask_le_f(Q, T) & mask_lt_u(e, E);
                 if (mask == 0) continue;
                 if (hit) {
                     const uint32_t pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),

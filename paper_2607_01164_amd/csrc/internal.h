@@ -105,9 +105,11 @@ __device__ __forceinline__ uint32_t dpp_u(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
 }
 
-// Ballot of a predicate that is already a lane mask (a comparison): no
-// round trip through a 0/1 integer.
-__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+// Lane masks of comparisons (bit l: lane l active and the comparison true),
+// straight from the compare instruction.
+__device__ __forceinline__ uint64_t mask_le_f(float a, float b) { return __builtin_amdgcn_fcmpf(a, b, 5); }
+__device__ __forceinline__ uint64_t mask_lt_u(uint32_t a, uint32_t b) { return __builtin_amdgcn_uicmp(a, b, 36); }
+__device__ __forceinline__ uint64_t mask_le_u(uint32_t a, uint32_t b) { return __builtin_amdgcn_uicmp(a, b, 37); }
 
 // x of lane l ^ 16, within each half of the wave (ds_swizzle, xor mask 16)
 __device__ __forceinline__ float swz_xor16(float x) {
