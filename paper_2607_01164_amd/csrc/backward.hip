@@ -202,16 +202,47 @@ __device__ __forceinline__ void drain(const Record &r, const float4 *qu, const u
     }
 }
 
-// One wavefront per Gaussian, visited in gorder. The points of the box are
-// taken as rows (a row is a run of consecutive elements: the queries of the
-// cells lo.x..hi.x at one (y, z) in plan order, or one x-run of voxels of a
-// grid), up to 64 rows at a time with lane r describing row r. The rows are
-// concatenated and walked 64 elements per step, lane l taking element
-// e0 + l, so the lanes stay busy across row ends; a lane finds its row by
-// comparing e with the row ends inside the step's window (uniform values,
-// read with readlane). The cutoff test is all a non-contributing pair
-// costs; contributing pairs go to a per-wave LDS queue, and every 64 queued
-// pairs are processed with all lanes busy.
+// Gaussians per wavefront: consecutive Gaussians of gorder share a wave.
+constexpr uint32_t kPack = 4;
+
+// Partials of the wave's current Gaussian are reduced over the wave and
+// stored: lane k < 12 writes moment k (the 12th is 0).
+__device__ __forceinline__ void finish_gauss(const Record &r, const float4 *qu, const uint32_t *qk, uint32_t head,
+                                             uint32_t cnt, uint32_t lane, const float2 *__restrict__ ab, Acc &acc,
+                                             uint32_t gid, float *__restrict__ moments) {
+    if (cnt > 0) {
+        __builtin_amdgcn_wave_barrier();
+        drain(r, qu, qk, head, cnt, lane, ab, acc);
+    }
+    const float v[11] = {acc.m1[0], acc.m1[1], acc.m1[2], acc.m2[0], acc.m2[1], acc.m2[2],
+                         acc.m2[3], acc.m2[4], acc.m2[5], acc.dv,    acc.dw};
+    const float tot = reduce11(v, lane);
+    if (lane < 12) moments[(size_t)gid * 12 + lane] = tot;
+}
+
+__device__ __forceinline__ void acc_zero(Acc &acc) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) acc.m1[k] = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 6; ++k) acc.m2[k] = 0.0f;
+    acc.dv = acc.dw = 0.0f;
+}
+
+// kPack consecutive Gaussians of gorder per wavefront. The points of a box
+// come as rows: a run of cells along x at fixed (y, z) is contiguous in the
+// plan's cell ordering (for grids, a run of voxels is contiguous in the
+// x-fastest layout). The rows of the wave's Gaussians are listed one
+// Gaussian after the other and taken 64 at a time, lane l describing row
+// l of the batch, so the loads that find the rows (spans, cell offsets)
+// are issued once for several Gaussians. Within a batch the rows are
+// concatenated; each Gaussian walks its own part 64 elements per step,
+// lane l taking element e0 + l, so the lanes stay busy across row ends and
+// every load reads whole cache lines; a lane finds its row from the row
+// starts with two ballots. The cutoff test is all a non-contributing pair
+// costs; contributing pairs go to a per-wave LDS queue, and every 64
+// queued pairs are processed with all lanes busy. Gaussians are visited in
+// the spatial order of the index (the cell key of their box corner), so the
+// waves resident at one time work on one region and find its points in L2.
 template <bool GRID>
 __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                            const CellBox *__restrict__ box,
@@ -226,77 +257,127 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t wib = threadIdx.x / kWave;
     const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + wib;
-    if (w >= (uint64_t)n_gauss) return;
+    const uint64_t first = w * kPack;
+    if (first >= (uint64_t)n_gauss) return;
+    const uint32_t nk = (uint64_t)n_gauss - first < kPack ? (uint32_t)((uint64_t)n_gauss - first) : kPack;
     float4 *qu = s_qu[wib];
     uint32_t *qk = s_qk[wib];
-    const uint32_t gid = __builtin_amdgcn_readfirstlane(((ConstU32 *)gorder)[w]);
-    const CellBox b = load_box_uniform(box, gid);
-    const Record r = load_record_uniform(rec, gid);
-    Acc acc;
-#pragma unroll
-    for (int k = 0; k < 3; ++k) acc.m1[k] = 0.0f;
-#pragma unroll
-    for (int k = 0; k < 6; ++k) acc.m2[k] = 0.0f;
-    acc.dv = acc.dw = 0.0f;
-    uint32_t head = 0, cnt = 0;
-    if (b.hi.x >= b.lo.x) {
-        const uint32_t nx = (uint32_t)(b.hi.x - b.lo.x + 1), ny = (uint32_t)(b.hi.y - b.lo.y + 1),
-                       nz = (uint32_t)(b.hi.z - b.lo.z + 1);
-        uint32_t rx = 1, ry = 1, rz = 1;
-        if (GRID) {
-            rx = (uint32_t)(q.dims[0] / g.cells[0]);
-            ry = (uint32_t)(q.dims[1] / g.cells[1]);
-            rz = (uint32_t)(q.dims[2] / g.cells[2]);
+    uint32_t rx = 1, ry = 1, rz = 1;
+    if (GRID) {
+        rx = (uint32_t)(q.dims[0] / g.cells[0]);
+        ry = (uint32_t)(q.dims[1] / g.cells[1]);
+        rz = (uint32_t)(q.dims[2] / g.cells[2]);
+    }
+    // lane i < nk describes Gaussian i of the wave: id, box, rows
+    uint32_t mgid = 0, mR = 0, mnx = 0, mny = 1, mtrim = 0;
+    int32_t mlx = 0, mly = 0, mlz = 0;
+    if (lane < nk) {
+        mgid = gorder[first + lane];
+        const CellBox bx = box[mgid];
+        if (bx.hi.x >= bx.lo.x) {
+            mnx = (uint32_t)(bx.hi.x - bx.lo.x + 1);
+            mny = (uint32_t)(bx.hi.y - bx.lo.y + 1);
+            mR = mny * ry * (uint32_t)(bx.hi.z - bx.lo.z + 1) * rz;
+            mtrim = (uint32_t)bx.lo.w;
+            mlx = bx.lo.x;
+            mly = bx.lo.y;
+            mlz = bx.lo.z;
         }
-        const uint32_t nry = ny * ry, R = nry * nz * rz;
-        const uint32_t vx0 = (uint32_t)b.lo.x * rx;
-        // row -> (yy, zz) by a float reciprocal: (row + 1/2) / nry lies at
-        // least 1/(2 nry) from an integer; v_rcp (1 ulp) and the product
-        // err by less than 1.5 2^-23 (row + 1/2) / nry, which cannot cross
-        // it while row < 2^21
-        const bool fdiv = R < (1u << 21);
-        const float inry = __builtin_amdgcn_rcpf((float)nry);
-        for (uint32_t rb = 0; rb < R; rb += kWave) {
-            // lane l describes row rb + l: its first element and its length
-            const uint32_t row = rb + lane;
-            uint32_t start = 0, len = 0, rx0 = vx0;
-            float rpy = 0.0f, rpz = 0.0f;
-            if (row < R) {
-                uint32_t zz;
-                if (fdiv)
-                    zz = (uint32_t)(((float)row + 0.5f) * inry);
-                else
-                    zz = row / nry;
-                const uint32_t yy = row - zz * nry;
-                // the row's run of cells: the whole box row, or its span
-                uint32_t xa = 0, xn = nx;
-                if (b.lo.w) {
-                    const uint32_t code = spans[(size_t)gid * kSpanRows + (yy / ry) + ny * (zz / rz)];
-                    xa = span_first(code);
-                    xn = span_len(code);
-                }
-                if (GRID) {
-                    const uint32_t vy = (uint32_t)b.lo.y * ry + yy, vz = (uint32_t)b.lo.z * rz + zz;
-                    rx0 = vx0 + xa * rx;
-                    start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + rx0;
-                    len = xn * rx;
-                    rpy = g.lo[1] + ((float)vy + 0.5f) * q.vsz[1];
-                    rpz = g.lo[2] + ((float)vz + 0.5f) * q.vsz[2];
-                } else if (xn > 0) {
-                    const uint32_t cy = (uint32_t)b.lo.y + yy, cz = (uint32_t)b.lo.z + zz;
-                    const uint32_t kbase = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz) + (uint32_t)b.lo.x;
-                    start = point_off[kbase + xa];
-                    len = point_off[kbase + xa + xn] - start;
-                }
+        // a Gaussian without rows gets zero moments here
+        if (mR == 0) {
+            float4 *m4 = (float4 *)(moments + (size_t)mgid * 12);
+            const float4 z = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            m4[0] = z;
+            m4[1] = z;
+            m4[2] = z;
+        }
+    }
+    const uint32_t mRend = wave_incl_sum(mR);  // end of Gaussian i's rows in the wave's list
+    const uint32_t Rw = __builtin_amdgcn_readlane(mRend, kWave - 1);
+    // row -> (yy, zz) by a float reciprocal: (row + 1/2) / nry lies at least
+    // 1/(2 nry) from an integer; v_rcp (1 ulp) and the product err by less
+    // than 1.5 2^-23 (row + 1/2) / nry, which cannot cross it while
+    // row < 2^21
+    const bool fdiv = wave_max_uniform(mR) < (1u << 21);
+    Record r;
+    r.r0 = r.r1 = r.r2 = r.r3 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    Acc acc;
+    acc_zero(acc);
+    uint32_t head = 0, cnt = 0;
+    uint32_t cur = kPack, cur_gid = 0;  // the Gaussian being walked (none yet)
+    for (uint32_t rb = 0; rb < Rw; rb += kWave) {
+        // lane l describes row rb + l of the wave's list: its Gaussian i is
+        // the number of Gaussians whose rows end at or before it
+        const uint32_t gr = rb + lane;
+        uint32_t i = 0;
+        for (uint32_t t = 0; t < nk; ++t) i += __builtin_amdgcn_readlane(mRend, t) <= gr ? 1u : 0u;
+        const uint32_t src = (i < kWave ? i : 0u) << 2;
+        const uint32_t f_gid = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mgid);
+        const uint32_t f_end = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mRend);
+        const uint32_t f_R = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mR);
+        const uint32_t f_nx = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mnx);
+        const uint32_t f_ny = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mny);
+        const uint32_t f_trim = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mtrim);
+        const uint32_t f_lx = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, mlx);
+        const uint32_t f_ly = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, mly);
+        const uint32_t f_lz = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, mlz);
+        uint32_t start = 0, len = 0, rx0 = 0;
+        float rpy = 0.0f, rpz = 0.0f;
+        if (gr < Rw) {
+            const uint32_t row = gr - (f_end - f_R);  // row within its Gaussian
+            const uint32_t nry = f_ny * ry;
+            uint32_t zz;
+            if (fdiv)
+                zz = (uint32_t)(((float)row + 0.5f) * __builtin_amdgcn_rcpf((float)nry));
+            else
+                zz = row / nry;
+            const uint32_t yy = row - zz * nry;
+            // the row's run of cells: the whole box row, or its span
+            uint32_t xa = 0, xn = f_nx;
+            if (f_trim) {
+                const uint32_t code = spans[(size_t)f_gid * kSpanRows + (yy / ry) + f_ny * (zz / rz)];
+                xa = span_first(code);
+                xn = span_len(code);
             }
-            const uint32_t nrows = (R - rb) < (uint32_t)kWave ? (R - rb) : (uint32_t)kWave;
-            const uint32_t incl = wave_incl_sum(len);  // end of row l in the concatenation
-            const uint32_t E = __builtin_amdgcn_readlane(incl, 63);
-            if (E == 0) continue;  // no query in these rows
-            const uint32_t rbeg = incl - len;          // first element of row l
-            const uint32_t kofs = start - rbeg;        // element e of row l is point e + kofs
-            const uint32_t xofs = rx0 - rbeg;          // grids: element e of row l has x = e + xofs
-            for (uint32_t e0 = 0; e0 < E; e0 += kWave) {
+            if (GRID) {
+                const uint32_t vy = f_ly * ry + yy, vz = f_lz * rz + zz;
+                rx0 = (f_lx + xa) * rx;
+                start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + rx0;
+                len = xn * rx;
+                rpy = g.lo[1] + ((float)vy + 0.5f) * q.vsz[1];
+                rpz = g.lo[2] + ((float)vz + 0.5f) * q.vsz[2];
+            } else if (xn > 0) {
+                const uint32_t cy = f_ly + yy, cz = f_lz + zz;
+                const uint32_t kbase = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz) + f_lx;
+                start = point_off[kbase + xa];
+                len = point_off[kbase + xa + xn] - start;
+            }
+        }
+        const uint32_t nrows = (Rw - rb) < (uint32_t)kWave ? (Rw - rb) : (uint32_t)kWave;
+        const uint32_t incl = wave_incl_sum(len);   // end of row l in the batch's concatenation
+        const uint32_t E = __builtin_amdgcn_readlane(incl, kWave - 1);
+        const uint32_t rbeg = incl - len;           // first element of row l
+        const uint32_t kofs = start - rbeg;         // element e of row l is point e + kofs
+        const uint32_t xofs = rx0 - rbeg;           // grids: element e of row l has x = e + xofs
+        // the Gaussians with rows in this batch, in order
+        const uint32_t ia = __builtin_amdgcn_readlane(i, 0), ib = __builtin_amdgcn_readlane(i, nrows - 1);
+        for (uint32_t gi = ia; gi <= ib; ++gi) {
+            const uint32_t gend = __builtin_amdgcn_readlane(mRend, gi), gR = __builtin_amdgcn_readlane(mR, gi);
+            if (gR == 0) continue;  // no rows: its moments are written above
+            if (gi != cur) {
+                if (cur < kPack) finish_gauss(r, qu, qk, head, cnt, lane, ab, acc, cur_gid, moments);
+                head = cnt = 0;
+                acc_zero(acc);
+                cur = gi;
+                cur_gid = __builtin_amdgcn_readlane(mgid, gi);
+                r = load_record_uniform(rec, cur_gid);
+            }
+            // its rows in this batch and their elements [Ea, Eb)
+            const uint32_t la = gend - gR > rb ? gend - gR - rb : 0u;
+            const uint32_t lb = gend - rb < nrows ? gend - rb : nrows;
+            const uint32_t Ea = __builtin_amdgcn_readlane(rbeg, la);
+            const uint32_t Eb = lb < (uint32_t)kWave ? __builtin_amdgcn_readlane(rbeg, lb) : E;
+            for (uint32_t e0 = Ea; e0 < Eb; e0 += kWave) {
                 // rbeg rises with the lane (lanes past nrows hold E), so the
                 // rows starting at or before e0 are a prefix of the lanes and
                 // the last of them holds element e0
@@ -324,9 +405,9 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                         pz = nxt ? readlane_f(rpz, j) : pz;
                     }
                 }
-                // lanes past the last element load the window's first point
-                // again; their test has no effect
-                const bool valid = e < E;
+                // lanes past the Gaussian's last element load the window's
+                // first point again; their test has no effect
+                const bool valid = e < Eb;
                 const uint32_t k = valid ? e + ko : e0 + ko0;
                 float u0, u1, u2, Q;
                 if (GRID) {
@@ -337,7 +418,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                     Q = whiten(r, p.x, p.y, p.z, u0, u1, u2);
                 }
                 const bool hit = valid && Q <= T;
-                const uint64_t mask = mask_le_f(Q, T) & mask_lt_u(e, E);
+                const uint64_t mask = mask_le_f(Q, T) & mask_lt_u(e, Eb);
                 if (mask == 0) continue;
                 if (hit) {
                     const uint32_t pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -357,14 +438,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
             }
         }
     }
-    if (cnt > 0) {
-        __builtin_amdgcn_wave_barrier();
-        drain(r, qu, qk, head, cnt, lane, ab, acc);
-    }
-    const float v[11] = {acc.m1[0], acc.m1[1], acc.m1[2], acc.m2[0], acc.m2[1], acc.m2[2],
-                         acc.m2[3], acc.m2[4], acc.m2[5], acc.dv,    acc.dw};
-    const float tot = reduce11(v, lane);
-    if (lane < 12) moments[(size_t)gid * 12 + lane] = tot;
+    if (cur < kPack) finish_gauss(r, qu, qk, head, cnt, lane, ab, acc, cur_gid, moments);
 }
 
 __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ moments, int64_t n,
@@ -465,7 +539,8 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
                                dim3(kBlock), 0, s, q.n, order, plan_out, grad_value, grad_influence, b.ab);
         prof_end("bwd_stage", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        const uint32_t wblocks = (uint32_t)((n_gauss + kWavesPerBlock - 1) / kWavesPerBlock);
+        const uint32_t wblocks =
+            (uint32_t)((n_gauss + (int64_t)kPack * kWavesPerBlock - 1) / ((int64_t)kPack * kWavesPerBlock));
         prof_begin("bwd_gauss", s);
         if (grid)
             hipLaunchKernelGGL(k_backward_gauss<true>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans, gorder,
