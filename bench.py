@@ -25,11 +25,14 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_VEC_PEAK_TFLOPS = 157.3   # MI355X vector FP32: 256 CUs x 2.4 GHz x 128 lanes x 2 (packed FMA)
-# Algorithmic work per contributing (Gaussian, point) pair: forward evaluates
-# d = p - mu, u = M d, Q = |u|^2, a = w exp(-Q/2), I += a, V += a v; the
-# backward repeats u, Q, a and forms dL/da, the per-pair moment terms and dv,
-# dw. Counted as adds and multiplies (an FMA is 2), the exponential as 1.
-FLOPS_PER_PAIR = {"sample_points": 31.0, "sample_grid": 31.0, "bwd_gauss": 61.0}
+# Algorithmic work, counted as adds and multiplies (an FMA is 2) and the
+# exponential as 1. Every candidate (Gaussian, point) pair of a cell list is
+# tested: d = p - mu (3), u = M d (15), Q = |u|^2 (5), the cutoff compare (1).
+# A contributing pair (Q <= T) adds, in the forward, a = w exp(-Q/2),
+# I += a, V += a v; in the backward, a, dL/da, the per-pair moment terms and
+# dv, dw.
+FLOPS_PER_TEST = 24.0
+FLOPS_PER_CONTRIB = {"sample_points": 7.0, "sample_grid": 7.0, "bwd_gauss": 37.0}
 # Bytes one pass of the LSD sort moves per pair: read and write key and value.
 SORT_BYTES_PER_PAIR = 16.0
 EMIT_BYTES_PER_PAIR = 8.0
@@ -105,6 +108,21 @@ class Step:
         self.build()
         self.forward()
         self.backward()
+
+    def candidate_tests(self) -> int:
+        """(Gaussian, point) pairs the forward and the backward test: the sum
+        over cells of (pairs listed in the cell) x (queries in the cell), from
+        the index's cell offsets and the plan's per-cell query offsets (after
+        the four 256-byte aligned query-length arrays of the plan)."""
+        torch = self.torch
+        ncells = self.grid.cells[0] * self.grid.cells[1] * self.grid.cells[2]
+        al = lambda b: (b + 255) // 256 * 256
+        off = 4 * al(4 * max(self.n, 1))
+        point_off = self.plan[off: off + 4 * (ncells + 2)].view(torch.int32).to(torch.int64)
+        pts = point_off[1:ncells + 1] - point_off[:ncells]
+        co = self.index.cell_offsets.to(torch.int64)
+        pairs = co[1:] - co[:-1]
+        return int((pts * pairs).sum().item())
 
 
 def timed(fn, k, sync):
@@ -185,6 +203,7 @@ def main():
     c, ms = gs.profile_read()[dom_name]
     dom = (dom_name, {"launches_per_step": c / a.steps, "ms_per_step": ms / a.steps, "avg_ms": ms / c})
     n_pairs = st.index.n_pairs
+    n_tests = st.candidate_tests()
     # forward alone and backward alone, for the query rates
     t_fwd = timed(st.forward, a.steps, sync)
     t_bwd = timed(st.backward, a.steps, sync)
@@ -199,7 +218,7 @@ def main():
 
     cpu = None if a.no_cpu else cpu_baseline(st, a.cpu_seconds)
     contrib = cpu.pop("contrib_per_point") if cpu else None
-    roof = roofline(dom[0], dom[1], st, n_pairs, contrib)
+    roof = roofline(dom[0], dom[1], st, n_pairs, n_tests, contrib)
     out = {
         "metric": "query points/sec fwd and fwd+bwd samples/sec; % of HBM roofline",
         "value": st.n / t_step,
@@ -215,7 +234,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{WORKLOAD}: 256^3 grid, 262144 Gaussians, batch of 2^20 random voxel centres, "
                                f"index {a.cells[0]}x{a.cells[1]}x{a.cells[2]} cells, step = build + forward + backward",
-                   "global_batch": st.n, "n_gauss": st.g_host.n, "index_pairs": n_pairs},
+                   "global_batch": st.n, "n_gauss": st.g_host.n, "index_pairs": n_pairs,
+                   "candidate_tests": n_tests},
         "fwd_points_per_s": st.n / t_fwd,
         "fwd_bwd_samples_per_s_excl_build": st.n / (t_fwd + t_bwd),
         "ms_build": t_build * 1e3, "ms_fwd": t_fwd * 1e3, "ms_bwd": t_bwd * 1e3,
@@ -265,26 +285,27 @@ def measured_traffic(name):
     return float(val.group(1))
 
 
-def roofline(name, k, st, n_pairs, contrib_per_point):
+def roofline(name, k, st, n_pairs, n_tests, contrib_per_point):
     """Roofline entry of the dominant kernel: algorithmic flops (or bytes) of
     one launch over its average launch duration (HIP events on the stream the
     kernel runs on)."""
     avg_s = k["avg_ms"] * 1e-3
     out = {"kernel": name, "avg_us": avg_s * 1e6, "launches_per_step": k["launches_per_step"]}
     traffic = measured_traffic(name)
-    if name in FLOPS_PER_PAIR:
-        # units: contributing pairs of the batch, from the oracle's count on the
-        # CPU-baseline sample (None without it)
+    if name in FLOPS_PER_CONTRIB:
+        # units: the candidate tests of the launch (exact, from the index and
+        # the plan) and its contributing pairs (the oracle's count per point
+        # on the CPU-baseline sample, times the batch; None without it)
         if contrib_per_point is None:
             out.update({"bound": "alu", "achieved": None, "peak": FP32_VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
-                        "frac": None, "traffic": traffic})
+                        "frac": None, "traffic": traffic, "candidate_tests": n_tests})
             return out
         units = contrib_per_point * st.n
-        flops = FLOPS_PER_PAIR[name] * units
+        flops = FLOPS_PER_TEST * n_tests + FLOPS_PER_CONTRIB[name] * units
         ach = flops / avg_s / 1e12
         out.update({"bound": "alu", "achieved": ach, "peak": FP32_VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": ach / FP32_VEC_PEAK_TFLOPS, "traffic": traffic,
-                    "flops_per_launch": flops, "contributing_pairs": units})
+                    "flops_per_launch": flops, "candidate_tests": n_tests, "contributing_pairs": units})
         return out
     per_pair = {"radix_downsweep": SORT_BYTES_PER_PAIR, "emit": EMIT_BYTES_PER_PAIR}.get(name)
     if per_pair is None:
