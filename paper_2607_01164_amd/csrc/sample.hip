@@ -230,6 +230,9 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
                                                          const uint32_t *__restrict__ items, int64_t max_items,
                                                          float T, float tau, float *__restrict__ out_v,
                                                          float *__restrict__ out_i, PlanResults pr) {
+    // per wave: the records of 64 candidates, as four 1 KiB planes of 16-byte
+    // quarters (quarter q of candidate s at [q][s])
+    __shared__ float4 s_rec[kWavesPerBlock][4 * kWave];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t ncells = (uint32_t)g.ncells;
     const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave;
@@ -286,22 +289,44 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
                 pz[t] = __shfl(mz, src, 64);
             }
         }
-        for (uint32_t j0 = ja; j0 < jb; j0 += 16) {
-            const uint32_t j = j0 + sl;
-            Record r;
-            if (j < jb) {
-                r = rec[gids[j]];
-            } else {
-                r.r0 = r.r1 = r.r2 = r.r3 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            }
+        // The list is taken 64 candidates at a time: lane l copies candidate
+        // c0 + l's record from memory straight into the wave's LDS planes
+        // (lanes past the list copy its last record), the ids of the next 64
+        // are fetched meanwhile, and the steps of 16 read the records from
+        // LDS, so a chunk waits for memory once instead of once per step.
+        float4 *buf = s_rec[threadIdx.x / kWave];
+        uint32_t gnext = 0;
+        if (ja < jb) gnext = gids[ja + lane < jb ? ja + lane : jb - 1];
+        for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
+            const float4 *src = (const float4 *)(rec + gnext);
 #pragma unroll
-            for (uint32_t t = 0; t < kRowsMax; ++t) {
-                if (t < nt) {
-                    const float a = eval_a(r, px[t], py[t], pz[t], T);
-                    Ip[t] += a;
-                    Vp[t] = fmaf_(a, r.r1.w, Vp[t]);
+            for (int qq = 0; qq < 4; ++qq)
+                __builtin_amdgcn_global_load_lds((const void *)(src + qq),
+                                                 (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
+            if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
+            __builtin_amdgcn_s_waitcnt(0);
+            __builtin_amdgcn_wave_barrier();
+            const uint32_t left = jb - c0;
+            const uint32_t nstep = left >= (uint32_t)kWave ? 4u : (left + 15) / 16;
+            for (uint32_t st = 0; st < nstep; ++st) {
+                const uint32_t sidx = 16 * st + sl;
+                Record r;
+                r.r0 = buf[sidx];
+                r.r1 = buf[kWave + sidx];
+                r.r2 = buf[2 * kWave + sidx];
+                r.r3 = buf[3 * kWave + sidx];
+                if (c0 + sidx >= jb) r.r0.w = 0.0f;  // past the list: weight 0
+#pragma unroll
+                for (uint32_t t = 0; t < kRowsMax; ++t) {
+                    if (t < nt) {
+                        const float a = eval_a(r, px[t], py[t], pz[t], T);
+                        Ip[t] += a;
+                        Vp[t] = fmaf_(a, r.r1.w, Vp[t]);
+                    }
                 }
             }
+            // every lane has read the planes before the next chunk overwrites them
+            __builtin_amdgcn_wave_barrier();
         }
         float Io = 0.0f, Vo = 0.0f;
 #pragma unroll
