@@ -177,7 +177,9 @@ Plan plan_layout(void *base, int64_t n, int64_t ncells) {
     p.items.max_items = ncells + 1 + (n > 0 ? n : 0) / 64 + 1;
     p.items.items = c.take<uint32_t>((size_t)p.items.max_items);
     p.items.scan_work = c.take<char>(scan_work_bytes(ncells + 2, 4));
-    p.res.pos = c.take<float4>(m);
+    // 64 spare entries: the backward's lanes past a Gaussian's last point
+    // read up to 63 entries beyond the last row of the plan
+    p.res.pos = c.take<float4>(m + kWave);
     p.res.out = c.take<float2>(m);
     p.bytes = c.off;
     return p;

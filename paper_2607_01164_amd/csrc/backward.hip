@@ -405,10 +405,12 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                         pz = nxt ? readlane_f(rpz, j) : pz;
                     }
                 }
-                // lanes past the Gaussian's last element load the window's
-                // first point again; their test has no effect
+                // lanes past the Gaussian's last element read the elements
+                // after it: points of later rows, or past the batch's last
+                // row, whose last point is at most n - 1, up to 63 entries of
+                // the plan's spare tail; their test has no effect
                 const bool valid = e < Eb;
-                const uint32_t k = valid ? e + ko : e0 + ko0;
+                const uint32_t k = e + ko;
                 float u0, u1, u2, Q;
                 if (GRID) {
                     const float px = g.lo[0] + ((float)(e + xo) + 0.5f) * q.vsz[0];
