@@ -361,61 +361,55 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
 
 // In-place inclusive max-scan of a tile's kExpandTile marks (kExpandItems
 // consecutive marks per thread, then across the block).
-__device__ void tile_max_scan(uint32_t *mark, uint32_t *wmax) {
+// Inclusive max-scan of a tile of 64-bit marks in LDS (kExpandItems per
+// thread, then across lanes and waves).
+__device__ void tile_max_scan64(uint64_t *mark, uint64_t *wmax) {
     const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-    uint32_t run = 0;
+    uint64_t run = 0;
     const uint32_t b0 = tid * kExpandItems;
 #pragma unroll
     for (int i = 0; i < kExpandItems; ++i) {
-        const uint32_t h = mark[b0 + i];
+        const uint64_t h = mark[b0 + i];
         run = h > run ? h : run;
         mark[b0 + i] = run;
     }
-    const uint32_t incl = wave_incl_max(run);
-    uint32_t excl = __shfl_up(incl, 1, 64);
+    uint64_t incl = run;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint64_t y = __shfl_up(incl, o, 64);
+        if (lane >= (uint32_t)o) incl = y > incl ? y : incl;
+    }
+    uint64_t excl = __shfl_up(incl, 1, 64);
     if (lane == 0) excl = 0;
     if (lane == kWave - 1) wmax[wave] = incl;
     __syncthreads();
-    uint32_t wpre = 0;
-    for (uint32_t w = 0; w < wave; ++w) wpre = wmax[w] > wpre ? wmax[w] : wpre;
-    const uint32_t carry = excl > wpre ? excl : wpre;
+    uint64_t carry = excl;
+    for (uint32_t w = 0; w < wave; ++w) carry = wmax[w] > carry ? wmax[w] : carry;
 #pragma unroll
     for (int i = 0; i < kExpandItems; ++i) {
-        const uint32_t h = mark[b0 + i];
+        const uint64_t h = mark[b0 + i];
         mark[b0 + i] = h > carry ? h : carry;
     }
     __syncthreads();
 }
 
-// Row marks of trimmed boxes: at the first slot p of the tile covered by a
-// non-empty row (its first pair, or slot 0 for a row begun in an earlier
-// tile) the mark ((p + 1) << 16) | (row << 8) | (first << 4) | (p - start)
-// holds the row, the offset of its first cell and how far into the row
-// slot p is. Marks grow with p, so a max-scan hands every slot the mark of
-// its row.
-__device__ void mark_rows(const uint8_t *sp, uint32_t nrows, int64_t base, uint32_t tile_cnt, uint32_t *rowmark) {
-    int64_t start = base;
-#pragma unroll 8
-    for (uint32_t r = 0; r < nrows; ++r) {
-        const uint32_t code = sp[r];
-        const uint32_t len = span_len(code);
-        if (len > 0 && start + len > 0 && start < (int64_t)tile_cnt) {
-            const uint32_t p = start > 0 ? (uint32_t)start : 0u;
-            rowmark[p] = ((p + 1u) << 16) | (r << 8) | (span_first(code) << 4) | (uint32_t)((int64_t)p - start);
-        }
-        start += len;
-    }
-}
-
+// Pair-parallel emit (Sec. 4.1.2): workgroup t writes pairs
+// [t kExpandTile, (t + 1) kExpandTile) of the Gaussian-major list. Every row
+// of cells (fixed y, z; the whole box row or its span) that reaches into the
+// tile marks its first slot p in the tile with
+//   (p + 1) << 52 | (Gaussian - first Gaussian of the tile) << 32 | key(p),
+// so a max-scan hands every slot the mark of its row, and slot s of that row
+// holds cell key(p) + s - p (keys grow by one along x). The Gaussian offset
+// takes 20 bits; a tile whose Gaussian range is wider (many Gaussians without
+// cells) finds the Gaussian of each slot by binary search instead.
 __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pair_off,
                                                  const CellBox *__restrict__ box,
                                                  const uint8_t *__restrict__ spans, int64_t n, int64_t npairs,
                                                  const uint32_t *__restrict__ tile_first, GridParams g,
                                                  uint32_t *__restrict__ keys, uint32_t *__restrict__ gids,
                                                  RadixPass0 pass0) {
-    __shared__ uint32_t head[kExpandTile];
-    __shared__ uint32_t rowmark[kExpandTile];
-    __shared__ uint32_t wmax[kWavesPerBlock];
+    __shared__ uint64_t mark[kExpandTile];
+    __shared__ uint64_t wmax[kWavesPerBlock];
     __shared__ uint32_t hist_lds[kMaxDigits];
     Pass0Hist hist(hist_lds, pass0);
     const uint32_t tid = threadIdx.x;
@@ -425,49 +419,64 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
     const uint32_t tile_cnt = rem < (uint64_t)kExpandTile ? (uint32_t)rem : (uint32_t)kExpandTile;
     const int64_t gfirst = tile_first[tile];
     const int64_t glast = (tile + 1 < gridDim.x) ? (int64_t)tile_first[tile + 1] : n - 1;
-    for (uint32_t s = tid; s < (uint32_t)kExpandTile; s += kBlock) {
-        head[s] = 0;
-        rowmark[s] = 0;
-    }
+    const bool fold = glast - gfirst < ((int64_t)1 << 20);
+    for (uint32_t s = tid; s < (uint32_t)kExpandTile; s += kBlock) mark[s] = 0;
     __syncthreads();
-    // mark the first pair of every Gaussian that starts inside the tile, and
-    // the rows of the trimmed boxes that reach into it
+    const int64_t Cx = g.cells[0], Cy = g.cells[1];
     for (int64_t gg = gfirst + tid; gg <= glast; gg += kBlock) {
-        const int64_t base = (int64_t)(pair_off[gg] - tile_begin);
-        if (gg > gfirst && base < (int64_t)tile_cnt) atomicMax(&head[base], (uint32_t)(gg - gfirst));
+        const int64_t base = (int64_t)(pair_off[gg] - tile_begin);  // the Gaussian's first pair, tile-relative
         const CellBox b = box[gg];
-        if (b.lo.w && b.hi.x >= b.lo.x) {
-            const uint32_t nrows = (uint32_t)((b.hi.y - b.lo.y + 1) * (b.hi.z - b.lo.z + 1));
-            mark_rows(spans + (size_t)gg * kSpanRows, nrows, base, tile_cnt, rowmark);
+        // the span line is read whole, together with the box
+        const uint4 *sp4 = (const uint4 *)(spans + (size_t)gg * kSpanRows);
+        const uint4 c0 = sp4[0], c1 = sp4[1], c2 = sp4[2], c3 = sp4[3];
+        if (b.hi.x < b.lo.x || base >= (int64_t)tile_cnt) continue;
+        const uint64_t gbits = fold ? (uint64_t)(gg - gfirst) << 32 : 0ull;
+        const int64_t nx = b.hi.x - b.lo.x + 1, ny = b.hi.y - b.lo.y + 1, nz = b.hi.z - b.lo.z + 1;
+        if (b.lo.w) {
+            const uint32_t words[16] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w,
+                                        c2.x, c2.y, c2.z, c2.w, c3.x, c3.y, c3.z, c3.w};
+            const uint32_t nrows = (uint32_t)(ny * nz);
+            int64_t start = base;
+            for (uint32_t r = 0; r < nrows && start < (int64_t)tile_cnt; ++r) {
+                const uint32_t code = (words[r >> 2] >> (8 * (r & 3))) & 0xFFu;
+                const uint32_t len = span_len(code);
+                if (len > 0 && start + len > 0) {
+                    const int64_t p = start > 0 ? start : 0;
+                    const int64_t cy = b.lo.y + (int64_t)(r % (uint32_t)ny), cz = b.lo.z + (int64_t)(r / (uint32_t)ny);
+                    const int64_t kp = b.lo.x + (int64_t)span_first(code) + (p - start) + Cx * (cy + Cy * cz);
+                    mark[p] = ((uint64_t)(p + 1) << 52) | gbits | (uint64_t)(uint32_t)kp;
+                }
+                start += len;
+            }
+        } else {
+            // whole rows of nx cells: only those reaching into the tile
+            const int64_t R = ny * nz;
+            const int64_t r0 = base < 0 ? (-base) / nx : 0;
+            int64_t r1 = ((int64_t)tile_cnt - base + nx - 1) / nx;
+            r1 = r1 < R ? r1 : R;
+            for (int64_t r = r0; r < r1; ++r) {
+                const int64_t start = base + r * nx;
+                const int64_t p = start > 0 ? start : 0;
+                const int64_t cy = b.lo.y + r % ny, cz = b.lo.z + r / ny;
+                const int64_t kp = b.lo.x + (p - start) + Cx * (cy + Cy * cz);
+                mark[p] = ((uint64_t)(p + 1) << 52) | gbits | (uint64_t)(uint32_t)kp;
+            }
         }
     }
     __syncthreads();
-    // inclusive max-scans carry each mark over its Gaussian's (row's) pairs
-    tile_max_scan(head, wmax);
-    tile_max_scan(rowmark, wmax);
-    const int64_t Cx = g.cells[0], Cy = g.cells[1];
+    tile_max_scan64(mark, wmax);
 #pragma unroll 2
     for (int i = 0; i < kExpandItems; ++i) {
         const uint32_t slot = (uint32_t)i * kBlock + tid;
         if (slot < tile_cnt) {
-            const int64_t gg = gfirst + head[slot];
-            const CellBox b = box[gg];
-            const uint32_t nx = (uint32_t)(b.hi.x - b.lo.x + 1), ny = (uint32_t)(b.hi.y - b.lo.y + 1);
-            uint32_t t, xo;
-            if (b.lo.w) {
-                const uint32_t m = rowmark[slot];
-                const uint32_t p = (m >> 16) - 1u;
-                t = (m >> 8) & 63u;
-                xo = ((m >> 4) & 15u) + (m & 15u) + (slot - p);
-            } else {
-                const uint32_t local = (uint32_t)(tile_begin + slot - pair_off[gg]);
-                t = local / nx;
-                xo = local - t * nx;
-            }
-            const int64_t cx = b.lo.x + (int64_t)xo;
-            const int64_t cy = b.lo.y + (int64_t)(t % ny);
-            const int64_t cz = b.lo.z + (int64_t)(t / ny);
-            const uint32_t key = (uint32_t)(cx + Cx * (cy + Cy * cz));
+            const uint64_t m = mark[slot];
+            const uint32_t p = (uint32_t)(m >> 52) - 1u;
+            const uint32_t key = (uint32_t)m + (slot - p);
+            int64_t gg;
+            if (fold)
+                gg = gfirst + (int64_t)((m >> 32) & 0xFFFFFu);
+            else
+                gg = gfirst + segment_search(pair_off + gfirst, glast - gfirst + 1, tile_begin + slot);
             keys[tile_begin + slot] = key;
             gids[tile_begin + slot] = (uint32_t)gg;
             hist.add(key);

@@ -172,13 +172,15 @@ __device__ __forceinline__ uint64_t wave_incl_sum64(uint64_t x) {
     return x;
 }
 
+// The max scan takes the sum's DPP steps (lanes without a source see 0);
+// all 64 lanes must be active.
 __device__ __forceinline__ uint32_t wave_incl_max(uint32_t x) {
-    const uint32_t lane = lane_id();
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        uint32_t y = __shfl_up(x, o, 64);
-        if (lane >= (uint32_t)o) x = x > y ? x : y;
-    }
+    x = umax_(x, dpp_u<0x111>(x));
+    x = umax_(x, dpp_u<0x112>(x));
+    x = umax_(x, dpp_u<0x114>(x));
+    x = umax_(x, dpp_u<0x118>(x));
+    x = umax_(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false));
+    x = umax_(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false));
     return x;
 }
 

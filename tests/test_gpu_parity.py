@@ -171,6 +171,22 @@ def test_index_and_backward_without_sort_passes(case):
     check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label=case)
 
 
+def test_index_tile_spanning_many_empty_gaussians():
+    """An emit tile whose Gaussians span more than 2^20 ids (1.1 M Gaussians
+    outside the domain, hence without cells, between two groups inside it):
+    the emit finds each pair's Gaussian by binary search there."""
+    inner = synth.random_gaussians(81, 40, log_mu=np.log(0.1))
+    n_out = 1_100_000
+    g = synth.random_gaussians(82, 40 + n_out + 40, log_mu=np.log(0.1))
+    g.mean[:40] = inner.mean
+    g.mean[40:40 + n_out] = 5.0
+    log("case emit tile over 1.1 M empty Gaussians")
+    r = Run(g, (6, 6, 6), "points", points=synth.random_points(83, 2000))
+    check_index(r)
+    phi, inf = r.forward()
+    check_forward(r, phi, inf, label="wide range")
+
+
 def test_point_plan_order_matches_oracle():
     """The query ordering kept in the plan (Sec. 5.1 analogue of the sample
     BVH): keys and ids bit-exact against the oracle's stable order."""
