@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "internal.h"
+#include "radix.h"
 
 using namespace gs;
 
@@ -119,6 +120,7 @@ struct IndexWork {
     uint32_t *gsort_v;   // [n] sort scratch
     void *gsort_work;
     uint64_t *pair_off;  // [n + 1]
+    uint64_t *pair_sum;  // [ceil((n + 1) / 64)] pair counts per 64 Gaussians, then their scan
     void *scan_work;
     uint32_t *tile_first;  // [pair tiles] first Gaussian of every emit tile
     uint32_t *keys_alt;
@@ -126,6 +128,13 @@ struct IndexWork {
     void *radix_work;
     size_t bytes;
 };
+
+// pair counts are summed per 64 Gaussians (the preprocess workgroups, the
+// last one holding count[n] = 0); the scan of the sums of the first
+// ceil(n / 64) groups is followed by their total
+int64_t pair_groups(int64_t n) { return (n + 1 + 63) / 64; }
+int64_t pair_groups_scanned(int64_t n) { return (n + 63) / 64; }
+int64_t tile_first_len(int64_t capacity) { return ((capacity > 0 ? capacity : 1) + kSortTile - 1) / kSortTile + 1; }
 
 IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity) {
     Carver c(base);
@@ -140,8 +149,9 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     w.gsort_v = c.take<uint32_t>(n1);
     w.gsort_work = c.take<char>(radix_work_bytes((int64_t)n1, gauss_order_bits(g)));
     w.pair_off = c.take<uint64_t>((size_t)n + 1);
-    w.scan_work = c.take<char>(scan_work_bytes(n + 1, 8));
-    w.tile_first = c.take<uint32_t>((size_t)((capacity > 0 ? capacity : 1) + 2047) / 2048 + 1);
+    w.pair_sum = c.take<uint64_t>((size_t)pair_groups_scanned(n) + 1);
+    w.scan_work = c.take<char>(scan_work_bytes(pair_groups_scanned(n), 8));
+    w.tile_first = c.take<uint32_t>((size_t)tile_first_len(capacity));
     const int64_t cap = capacity > 0 ? capacity : 1;
     w.keys_alt = c.take<uint32_t>((size_t)cap);
     w.gids_alt = c.take<uint32_t>((size_t)cap);
@@ -433,7 +443,7 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     IndexWork w = index_layout(index->work, n, grid, index->capacity);
 
     GS_TRY(launch_preprocess(gauss->mean, gauss->scale, gauss->rot, gauss->value, gauss->weight, n, gp,
-                             index_radius(tau), w.rec, w.box, w.spans, w.pair_off, stream),
+                             index_radius(tau), w.rec, w.box, w.spans, w.pair_off, w.pair_sum, stream),
            "gs_build_index: preprocess");
     {
         // spatial visiting order of the Gaussians (sorted by box corner cell)
@@ -447,7 +457,17 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
         GS_TRY(radix_sort_pairs(k0, v0, k1, v1, n, gbits, w.gsort_work, stream, true),
                "gs_build_index: Gaussian order");
     }
-    GS_TRY(exclusive_scan_u64(w.pair_off, w.pair_off, n + 1, w.scan_work, stream), "gs_build_index: scan");
+    {
+        // groups past ceil(n / 64) hold only count[n] = 0: their prefix is the total
+        const int64_t G = pair_groups_scanned(n);
+        if (G > 0)
+            GS_TRY(exclusive_scan_u64_total(w.pair_sum, w.pair_sum, G, w.pair_sum + G, w.scan_work, stream),
+                   "gs_build_index: scan of the group sums");
+        else
+            GS_TRY(fill_u32((uint32_t *)w.pair_sum, 0u, 2, stream), "gs_build_index: scan of the group sums");
+    }
+    GS_TRY(pair_offsets(w.pair_off, n + 1, w.pair_sum, w.tile_first, tile_first_len(index->capacity), kSortTile, stream),
+           "gs_build_index: pair offsets");
     uint64_t P = 0;
     GS_TRY(hipMemcpyAsync(&P, w.pair_off + n, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
            "gs_build_index: reading the pair count");

@@ -157,7 +157,8 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
                                                        const float *__restrict__ rot, const float *__restrict__ value,
                                                        const float *__restrict__ weight, int64_t n, GridParams g,
                                                        float rci, Record *__restrict__ rec, CellBox *__restrict__ box,
-                                                       uint8_t *__restrict__ spans, uint64_t *__restrict__ count) {
+                                                       uint8_t *__restrict__ spans, uint64_t *__restrict__ count,
+                                                       uint64_t *__restrict__ block_sum) {
     // span parameters of the wave's boxes, one array per field (lane stride
     // 4 or 8 bytes: no bank conflicts)
     __shared__ double sp_d[8][kPreBlock];
@@ -318,6 +319,11 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
         for (int k = 0; k < kSpanRows / 16; ++k)
             dst[k] = make_uint4(sp_code[4 * k][tid], sp_code[4 * k + 1][tid], sp_code[4 * k + 2][tid],
                                 sp_code[4 * k + 3][tid]);
+    }
+    // the workgroup's pair count (one wave), for the offsets' scan
+    {
+        const uint64_t tot = wave_incl_sum64(active ? cnt : 0ull);
+        if (lane == kWave - 1) block_sum[blockIdx.x] = tot;
     }
     if (!active) return;
     count[i] = cnt;
@@ -511,16 +517,6 @@ __global__ __launch_bounds__(kBlock) void k_gauss_keys(const CellBox *__restrict
     hist.finish_tile(blockIdx.x);
 }
 
-// First segment of every emit tile: tile_first[t] = the Gaussian owning pair
-// t * kSortTile (all searches run in parallel, one thread per tile).
-__global__ __launch_bounds__(kBlock) void k_tile_first(const uint64_t *__restrict__ pair_off, int64_t n,
-                                                       int64_t npairs, uint32_t ntiles,
-                                                       uint32_t *__restrict__ tile_first) {
-    const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= ntiles) return;
-    tile_first[t] = (uint32_t)segment_search(pair_off, n, (uint64_t)t * kSortTile);
-}
-
 }  // namespace
 
 hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g, int shift, uint32_t *keys,
@@ -535,12 +531,12 @@ hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g,
 
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
-                             CellBox *box, uint8_t *spans, uint64_t *count, hipStream_t s) {
+                             CellBox *box, uint8_t *spans, uint64_t *count, uint64_t *block_sum, hipStream_t s) {
     const int64_t threads = n + 1;
     const uint32_t blocks = (uint32_t)((threads + kPreBlock - 1) / kPreBlock);
     prof_begin("preprocess", s);
     hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kPreBlock), 0, s, mean, scale, rot, value, weight, n, g, rci, rec,
-                       box, spans, count);
+                       box, spans, count, block_sum);
     prof_end("preprocess", s);
     return hipGetLastError();
 }
@@ -550,12 +546,6 @@ hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8
                        const RadixPass0 &pass0, hipStream_t s) {
     if (npairs <= 0 || n <= 0) return hipSuccess;
     const uint32_t blocks = (uint32_t)((npairs + kExpandTile - 1) / kExpandTile);
-    prof_begin("emit_partition", s);
-    hipLaunchKernelGGL(k_tile_first, dim3((blocks + kBlock - 1) / kBlock), dim3(kBlock), 0, s, pair_off, n, npairs,
-                       blocks, tile_first);
-    prof_end("emit_partition", s);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
     prof_begin("emit", s);
     hipLaunchKernelGGL(k_emit, dim3(blocks), dim3(kBlock), 0, s, pair_off, box, spans, n, npairs, tile_first, g, keys,
                        gids, pass0);

@@ -207,6 +207,15 @@ void prof_end(const char *name, hipStream_t s);
 size_t scan_work_bytes(int64_t n, int elem_bytes);
 hipError_t exclusive_scan_u32(const uint32_t *in, uint32_t *out, int64_t n, void *work, hipStream_t s);
 hipError_t exclusive_scan_u64(const uint64_t *in, uint64_t *out, int64_t n, void *work, hipStream_t s);
+// exclusive scan of n elements; *total receives their sum
+hipError_t exclusive_scan_u64_total(const uint64_t *in, uint64_t *out, int64_t n, uint64_t *total, void *work,
+                                    hipStream_t s);
+// count[0..n) -> exclusive offsets in place, given group_prefix = the
+// exclusive scan of the counts' sums over groups of 64 followed by their
+// total; tile_first[t] (t < ntiles) = the segment holding element
+// t * tile_size
+hipError_t pair_offsets(uint64_t *count, int64_t n, const uint64_t *group_prefix, uint32_t *tile_first,
+                        int64_t ntiles, uint32_t tile_size, hipStream_t s);
 
 // Stable LSD radix sort of (key, value) pairs by the low `bits` key bits
 // (radix.h has the tile geometry). Passes alternate between the two buffer
@@ -243,9 +252,11 @@ struct GridParams {
     int32_t cells[3];
     int64_t ncells;
 };
+// count[0..n] receives the pair count of every Gaussian (count[n] = 0) and
+// block_sum[b] the sum over elements [64 b, 64 b + 64) of count
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
-                             CellBox *box, uint8_t *spans, uint64_t *count, hipStream_t s);
+                             CellBox *box, uint8_t *spans, uint64_t *count, uint64_t *block_sum, hipStream_t s);
 // tile_first: ceil(npairs / kSortTile) words of scratch
 hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8_t *spans, int64_t n, int64_t npairs,
                        const GridParams &g,

@@ -50,7 +50,8 @@ __global__ __launch_bounds__(kBlock) void k_scan_reduce(const T *__restrict__ in
 }
 
 template <typename T>
-__global__ __launch_bounds__(kBlock) void k_scan_tile(const T *in, T *out, int64_t n, const T *__restrict__ prefix) {
+__global__ __launch_bounds__(kBlock) void k_scan_tile(const T *in, T *out, int64_t n, const T *__restrict__ prefix,
+                                                      T *__restrict__ total) {
     __shared__ T lds[kWavesPerBlock];
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
     T v[kScanItems];
@@ -64,6 +65,8 @@ __global__ __launch_bounds__(kBlock) void k_scan_tile(const T *in, T *out, int64
     T tot;
     T run = block_excl_scan(s, lds, &tot);
     if (prefix) run += prefix[blockIdx.x];
+    // the last workgroup's last thread ends with the grand total
+    if (total && blockIdx.x == gridDim.x - 1 && threadIdx.x == kBlock - 1) *total = run + s;
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i) {
         int64_t idx = base + i;
@@ -74,11 +77,12 @@ __global__ __launch_bounds__(kBlock) void k_scan_tile(const T *in, T *out, int64
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// total (optional) receives the sum of all n elements
 template <typename T>
-hipError_t scan_rec(const T *in, T *out, int64_t n, T *work, hipStream_t s) {
+hipError_t scan_rec(const T *in, T *out, int64_t n, T *work, hipStream_t s, T *total = nullptr) {
     if (n <= 0) return hipSuccess;
     if (n <= kScanTile) {
-        hipLaunchKernelGGL(k_scan_tile<T>, dim3(1), dim3(kBlock), 0, s, in, out, n, (const T *)nullptr);
+        hipLaunchKernelGGL(k_scan_tile<T>, dim3(1), dim3(kBlock), 0, s, in, out, n, (const T *)nullptr, total);
         return hipGetLastError();
     }
     const int64_t nb = ceil_div(n, kScanTile);
@@ -88,7 +92,7 @@ hipError_t scan_rec(const T *in, T *out, int64_t n, T *work, hipStream_t s) {
     if (e != hipSuccess) return e;
     e = scan_rec<T>(sums, sums, nb, work + nb, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_scan_tile<T>, dim3((uint32_t)nb), dim3(kBlock), 0, s, in, out, n, (const T *)sums);
+    hipLaunchKernelGGL(k_scan_tile<T>, dim3((uint32_t)nb), dim3(kBlock), 0, s, in, out, n, (const T *)sums, total);
     return hipGetLastError();
 }
 
@@ -306,6 +310,46 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     }
 }
 
+// Exclusive scan of per-segment counts into offsets, in place, for counts
+// whose sums over groups of kPairSumGroup elements were scanned already
+// (group_prefix, with the grand total after the last group): workgroup b
+// takes kPairTile elements and starts at group_prefix[b kPairTile / 64].
+// Every non-empty segment i also records itself as the first segment of the
+// tiles of tile_size elements that start inside it.
+constexpr int kPairSumGroup = 64;
+constexpr int kPairItems = 4;
+constexpr int kPairTile = kBlock * kPairItems;  // 1024
+static_assert(kPairTile % kPairSumGroup == 0, "offset tiles are whole groups");
+__global__ __launch_bounds__(kBlock) void k_pair_offsets(uint64_t *__restrict__ off, int64_t n,
+                                                         const uint64_t *__restrict__ group_prefix,
+                                                         uint32_t *__restrict__ tile_first, int64_t ntiles,
+                                                         uint32_t tile_size) {
+    __shared__ uint64_t lds[kWavesPerBlock];
+    const int64_t base = (int64_t)blockIdx.x * kPairTile + (int64_t)threadIdx.x * kPairItems;
+    uint64_t v[kPairItems];
+    uint64_t s = 0;
+#pragma unroll
+    for (int i = 0; i < kPairItems; ++i) {
+        const int64_t idx = base + i;
+        v[i] = idx < n ? off[idx] : 0ull;
+        s += v[i];
+    }
+    uint64_t tot;
+    uint64_t run = block_excl_scan(s, lds, &tot) + group_prefix[(size_t)blockIdx.x * (kPairTile / kPairSumGroup)];
+#pragma unroll
+    for (int i = 0; i < kPairItems; ++i) {
+        const int64_t idx = base + i;
+        if (idx < n) {
+            off[idx] = run;
+            if (v[i] > 0) {
+                const uint64_t t0 = (run + tile_size - 1) / tile_size, t1 = (run + v[i] - 1) / tile_size;
+                for (uint64_t t = t0; t <= t1 && t < (uint64_t)ntiles; ++t) tile_first[t] = (uint32_t)idx;
+            }
+        }
+        run += v[i];
+    }
+}
+
 // offsets[k] = number of keys < k. Thread t covers the boundaries before
 // keys 4t .. 4t+3 (and the end, after key n-1), reading its four keys with
 // one 16-byte load where the array is 16-byte aligned.
@@ -356,6 +400,24 @@ hipError_t exclusive_scan_u32(const uint32_t *in, uint32_t *out, int64_t n, void
     prof_begin("scan_u32", s);
     hipError_t e = scan_rec<uint32_t>(in, out, n, (uint32_t *)work, s);
     prof_end("scan_u32", s);
+    return e;
+}
+
+hipError_t pair_offsets(uint64_t *count, int64_t n, const uint64_t *group_prefix, uint32_t *tile_first,
+                        int64_t ntiles, uint32_t tile_size, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    prof_begin("pair_offsets", s);
+    hipLaunchKernelGGL(k_pair_offsets, dim3((uint32_t)ceil_div(n, kPairTile)), dim3(kBlock), 0, s, count, n,
+                       group_prefix, tile_first, ntiles, tile_size);
+    prof_end("pair_offsets", s);
+    return hipGetLastError();
+}
+
+hipError_t exclusive_scan_u64_total(const uint64_t *in, uint64_t *out, int64_t n, uint64_t *total, void *work,
+                                    hipStream_t s) {
+    prof_begin("scan_u64", s);
+    hipError_t e = scan_rec<uint64_t>(in, out, n, (uint64_t *)work, s, total);
+    prof_end("scan_u64", s);
     return e;
 }
 
