@@ -172,6 +172,30 @@ __device__ __forceinline__ uint64_t wave_incl_sum64(uint64_t x) {
     return x;
 }
 
+__device__ __forceinline__ uint32_t wincl(uint32_t x) { return wave_incl_sum(x); }
+__device__ __forceinline__ uint64_t wincl(uint64_t x) { return wave_incl_sum64(x); }
+
+// Exclusive scan of one value per thread over the workgroup (kBlock
+// threads); *total gets the
+// workgroup sum. lds needs kWavesPerBlock entries.
+template <typename T>
+__device__ __forceinline__ T block_excl_scan(T x, T *lds, T *total) {
+    const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    T incl = wincl(x);
+    if (lane == kWave - 1) lds[wave] = incl;
+    __syncthreads();
+    T wpre = 0, tot = 0;
+#pragma unroll
+    for (uint32_t w = 0; w < (uint32_t)kWavesPerBlock; ++w) {
+        T v = lds[w];
+        if (w < wave) wpre += v;
+        tot += v;
+    }
+    __syncthreads();
+    *total = tot;
+    return wpre + incl - x;
+}
+
 // The max scan takes the sum's DPP steps (lanes without a source see 0);
 // all 64 lanes must be active.
 __device__ __forceinline__ uint32_t wave_incl_max(uint32_t x) {
@@ -280,11 +304,14 @@ hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const R
                               hipStream_t s);
 // Work items of the ordered-query sampler (kept in the plan).
 struct PointItems {
-    uint32_t *item_off;  // [ncells + 2]
-    uint32_t *items;     // [max_items]
-    int64_t max_items;   // ncells + 1 + n / 64 + 1
-    void *scan_work;
+    uint32_t *item_off;   // [ncells + 2]
+    uint32_t *items;      // [max_items]
+    int64_t max_items;    // ncells + 1 + n / 64 + 1
+    uint32_t *group_sum;  // [item_groups(ncells + 1)] work items per 1024 buckets
+    void *scan_work;      // scan of group_sum
 };
+// groups of 1024 buckets (plus the element after the last bucket)
+inline int64_t item_groups(int64_t nbuckets) { return (nbuckets + 1 + 1023) / 1024; }
 // The forward's results in plan order, kept in the plan for the backward:
 // position (x, y, z, 0) and (Phi, I) of the k-th query in cell order.
 struct PlanResults {

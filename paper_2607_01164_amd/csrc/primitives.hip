@@ -11,29 +11,6 @@ namespace {
 constexpr int kScanItems = 16;
 constexpr int kScanTile = kBlock * kScanItems;  // 4096
 
-__device__ __forceinline__ uint32_t wincl(uint32_t x) { return wave_incl_sum(x); }
-__device__ __forceinline__ uint64_t wincl(uint64_t x) { return wave_incl_sum64(x); }
-
-// Exclusive scan of one value per thread over the workgroup; *total gets the
-// workgroup sum. lds needs kWavesPerBlock entries.
-template <typename T>
-__device__ __forceinline__ T block_excl_scan(T x, T *lds, T *total) {
-    const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-    T incl = wincl(x);
-    if (lane == kWave - 1) lds[wave] = incl;
-    __syncthreads();
-    T wpre = 0, tot = 0;
-#pragma unroll
-    for (uint32_t w = 0; w < (uint32_t)kWavesPerBlock; ++w) {
-        T v = lds[w];
-        if (w < wave) wpre += v;
-        tot += v;
-    }
-    __syncthreads();
-    *total = tot;
-    return wpre + incl - x;
-}
-
 template <typename T>
 __global__ __launch_bounds__(kBlock) void k_scan_reduce(const T *__restrict__ in, int64_t n, T *__restrict__ sums) {
     __shared__ T lds[kWavesPerBlock];

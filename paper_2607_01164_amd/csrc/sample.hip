@@ -162,29 +162,68 @@ constexpr uint32_t kChunkB = 8;  // queries evaluated together by a sparse-cell 
 constexpr uint32_t kRowsMin = 4;                 // from this many queries a cell uses 4 query rows
 constexpr uint32_t kRowsMax = (kDenseMin + 3) / 4;  // queries per row at most
 
-__global__ __launch_bounds__(kBlock) void k_cell_items(const uint32_t *__restrict__ point_off, int64_t nbuckets,
-                                                       uint32_t *__restrict__ item_off) {
-    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (c == nbuckets) item_off[nbuckets] = 0;
-    if (c >= nbuckets) return;
+// Work items per bucket (cell, and the outside bucket last): none for an
+// empty bucket, one for a sparse one, one per 64 queries of a dense one.
+__device__ __forceinline__ uint32_t bucket_items(const uint32_t *point_off, int64_t c, int64_t nbuckets) {
+    if (c >= nbuckets) return 0u;
     const uint32_t n = point_off[c + 1] - point_off[c];
-    item_off[c] = n == 0 ? 0u : (n < kDenseMin ? 1u : (n + kWave - 1) / kWave);
+    return n == 0 ? 0u : (n < kDenseMin ? 1u : (n + kWave - 1) / kWave);
 }
 
-__global__ __launch_bounds__(kBlock) void k_expand_cell_items(const uint32_t *__restrict__ item_off, int64_t nbuckets,
-                                                              uint32_t *__restrict__ items, int64_t max_items) {
-    __shared__ ExpandShared sh;
-    const uint64_t tot = item_off[nbuckets];
-    const uint64_t total = tot < (uint64_t)max_items ? tot : (uint64_t)max_items;
-    const uint64_t tile_begin = (uint64_t)blockIdx.x * kExpandTile;
-    if (tile_begin >= total) return;
-    const uint64_t rem = total - tile_begin;
-    const uint32_t tile_cnt = rem < (uint64_t)kExpandTile ? (uint32_t)rem : (uint32_t)kExpandTile;
-    const int64_t first = expand_tile(item_off, nbuckets, tile_begin, tile_cnt, sh);
-#pragma unroll 2
-    for (int i = 0; i < kExpandItems; ++i) {
-        const uint32_t slot = (uint32_t)i * kBlock + threadIdx.x;
-        if (slot < tile_cnt) items[tile_begin + slot] = (uint32_t)(first + sh.head[slot]);
+// Buckets are taken kItemGroup at a time (kItemsPerThread per thread).
+constexpr int kItemsPerThread = 4;
+constexpr int kItemGroup = kBlock * kItemsPerThread;  // 1024
+// Up to this many groups, the offsets kernel sums the earlier groups itself;
+// beyond, their sums are scanned by a separate pass.
+constexpr int64_t kInlineGroups = 1024;
+
+__global__ __launch_bounds__(kBlock) void k_item_sums(const uint32_t *__restrict__ point_off, int64_t nbuckets,
+                                                      uint32_t *__restrict__ group_sum) {
+    __shared__ uint32_t lds[kWavesPerBlock];
+    const int64_t base = (int64_t)blockIdx.x * kItemGroup + (int64_t)threadIdx.x * kItemsPerThread;
+    uint32_t s = 0;
+#pragma unroll
+    for (int i = 0; i < kItemsPerThread; ++i) s += bucket_items(point_off, base + i, nbuckets);
+    uint32_t tot;
+    (void)block_excl_scan(s, lds, &tot);
+    if (threadIdx.x == 0) group_sum[blockIdx.x] = tot;
+}
+
+// item_off[c] for c <= nbuckets (item_off[nbuckets] = the total) and the
+// item list: item_off[c] .. item_off[c] + items(c) - 1 name bucket c.
+// group_sum: the groups' sums, or (scanned) their exclusive prefixes.
+__global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restrict__ point_off, int64_t nbuckets,
+                                                         const uint32_t *__restrict__ group_sum, bool scanned,
+                                                         uint32_t *__restrict__ item_off, uint32_t *__restrict__ items,
+                                                         int64_t max_items) {
+    __shared__ uint32_t lds[kWavesPerBlock];
+    uint32_t prefix;
+    if (scanned) {
+        prefix = group_sum[blockIdx.x];
+    } else {
+        uint32_t p = 0;
+        for (uint32_t j = threadIdx.x; j < blockIdx.x; j += kBlock) p += group_sum[j];
+        uint32_t tot;
+        (void)block_excl_scan(p, lds, &tot);
+        prefix = tot;
+    }
+    const int64_t base = (int64_t)blockIdx.x * kItemGroup + (int64_t)threadIdx.x * kItemsPerThread;
+    uint32_t v[kItemsPerThread];
+    uint32_t s = 0;
+#pragma unroll
+    for (int i = 0; i < kItemsPerThread; ++i) {
+        v[i] = bucket_items(point_off, base + i, nbuckets);
+        s += v[i];
+    }
+    uint32_t tot;
+    uint32_t run = block_excl_scan(s, lds, &tot) + prefix;
+#pragma unroll
+    for (int i = 0; i < kItemsPerThread; ++i) {
+        const int64_t c = base + i;
+        if (c <= nbuckets) item_off[c] = run;
+        for (uint32_t k = 0; k < v[i]; ++k)
+            if ((int64_t)(run + k) < max_items) items[run + k] = (uint32_t)c;
+        run += v[i];
     }
 }
 
@@ -428,18 +467,20 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
                                 const PlanResults &pr, hipStream_t s) {
     if (q.n <= 0) return hipSuccess;
     const int64_t nbuckets = g.ncells + 1;  // cells and the outside bucket
+    // buckets 0..nbuckets-1 and one empty element after them (its offset is the total)
+    const int64_t ngroups = (nbuckets + 1 + kItemGroup - 1) / kItemGroup;
+    const bool scanned = ngroups > kInlineGroups;
     prof_begin("cell_items", s);
-    hipLaunchKernelGGL(k_cell_items, dim3((uint32_t)((nbuckets + 1 + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
-                       point_off, nbuckets, it.item_off);
-    prof_end("cell_items", s);
+    hipLaunchKernelGGL(k_item_sums, dim3((uint32_t)ngroups), dim3(kBlock), 0, s, point_off, nbuckets, it.group_sum);
     hipError_t e = hipGetLastError();
+    if (e == hipSuccess && scanned) e = exclusive_scan_u32(it.group_sum, it.group_sum, ngroups, it.scan_work, s);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(k_item_offsets, dim3((uint32_t)ngroups), dim3(kBlock), 0, s, point_off, nbuckets,
+                           it.group_sum, scanned, it.item_off, it.items, it.max_items);
+        e = hipGetLastError();
+    }
+    prof_end("cell_items", s);
     if (e != hipSuccess) return e;
-    if ((e = exclusive_scan_u32(it.item_off, it.item_off, nbuckets + 1, it.scan_work, s)) != hipSuccess) return e;
-    prof_begin("cell_expand", s);
-    hipLaunchKernelGGL(k_expand_cell_items, dim3((uint32_t)((it.max_items + kExpandTile - 1) / kExpandTile)),
-                       dim3(kBlock), 0, s, it.item_off, nbuckets, it.items, it.max_items);
-    prof_end("cell_expand", s);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     prof_begin("sample_points", s);
     hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kWavesPerBlock - 1) / kWavesPerBlock)),
                        dim3(kBlock), 0, s, q, g, rec, gids, cell_off, point_off, order, it.item_off, it.items,

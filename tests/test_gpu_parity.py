@@ -171,6 +171,21 @@ def test_index_and_backward_without_sort_passes(case):
     check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label=case)
 
 
+def test_points_on_a_fine_index():
+    """Point queries on an index of 104^3 cells: more than 2^20 buckets, so
+    the work-item offsets scan their group sums in a separate pass."""
+    g = synth.random_gaussians(84, 400, log_mu=np.log(0.02), log_sd=0.4)
+    pts = synth.random_points(85, 6000)
+    log("case points on 104^3 cells")
+    r = Run(g, (104, 104, 104), "points", points=pts)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="fine index")
+    gv, gi = synth.random_normal(86, r.nq), synth.random_normal(87, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="fine index")
+
+
 def test_index_tile_spanning_many_empty_gaussians():
     """An emit tile whose Gaussians span more than 2^20 ids (1.1 M Gaussians
     outside the domain, hence without cells, between two groups inside it):
