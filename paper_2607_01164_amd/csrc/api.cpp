@@ -347,6 +347,28 @@ void prof_collect() {
     g_prof_done.clear();
 }
 
+// A pinned host word per host thread for the pair count read back by the
+// index build, with the event that marks its copy (created on first use,
+// kept until the process ends).
+struct PinnedCount {
+    uint64_t *value = nullptr;
+    hipEvent_t copied = nullptr;
+};
+
+PinnedCount *pinned_count() {
+    static thread_local PinnedCount pc;
+    if (!pc.value) {
+        void *p = nullptr;
+        if (hipHostMalloc(&p, sizeof(uint64_t), hipHostMallocDefault) != hipSuccess) return nullptr;
+        if (hipEventCreateWithFlags(&pc.copied, hipEventDisableTiming) != hipSuccess) {
+            (void)hipHostFree(p);
+            return nullptr;
+        }
+        pc.value = (uint64_t *)p;
+    }
+    return &pc;
+}
+
 }  // namespace
 
 namespace gs {
@@ -447,6 +469,26 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
                              index_radius(tau), w.rec, w.box, w.spans, w.pair_off, w.pair_sum, stream),
            "gs_build_index: preprocess");
     {
+        // groups past ceil(n / 64) hold only count[n] = 0: their prefix is the total
+        const int64_t G = pair_groups_scanned(n);
+        if (G > 0)
+            GS_TRY(exclusive_scan_u64_total(w.pair_sum, w.pair_sum, G, w.pair_sum + G, w.scan_work, stream),
+                   "gs_build_index: scan of the group sums");
+        else
+            GS_TRY(fill_u32((uint32_t *)w.pair_sum, 0u, 2, stream), "gs_build_index: scan of the group sums");
+    }
+    GS_TRY(pair_offsets(w.pair_off, n + 1, w.pair_sum, w.tile_first, tile_first_len(index->capacity), kSortTile, stream),
+           "gs_build_index: pair offsets");
+    // the pair count goes to a pinned host word; the host waits for that copy
+    // only, while the device goes on with the Gaussian sort
+    PinnedCount *pc = pinned_count();
+    if (!pc) return fail(GS_ERR_HIP, "gs_build_index: cannot set up the pinned pair-count slot");
+    GS_TRY(hipMemcpyAsync(pc->value, w.pair_off + n, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
+           "gs_build_index: reading the pair count");
+    GS_TRY(hipEventRecord(pc->copied, stream), "gs_build_index: reading the pair count");
+    // the Gaussians' visiting order needs only the boxes: the device sorts
+    // them while the host waits for the pair count
+    {
         // spatial visiting order of the Gaussians (sorted by box corner cell)
         const int gbits = gauss_order_bits(grid);
         const bool godd = (radix_passes(gbits) & 1) != 0;
@@ -458,21 +500,8 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
         GS_TRY(radix_sort_pairs(k0, v0, k1, v1, n, gbits, w.gsort_work, stream, true),
                "gs_build_index: Gaussian order");
     }
-    {
-        // groups past ceil(n / 64) hold only count[n] = 0: their prefix is the total
-        const int64_t G = pair_groups_scanned(n);
-        if (G > 0)
-            GS_TRY(exclusive_scan_u64_total(w.pair_sum, w.pair_sum, G, w.pair_sum + G, w.scan_work, stream),
-                   "gs_build_index: scan of the group sums");
-        else
-            GS_TRY(fill_u32((uint32_t *)w.pair_sum, 0u, 2, stream), "gs_build_index: scan of the group sums");
-    }
-    GS_TRY(pair_offsets(w.pair_off, n + 1, w.pair_sum, w.tile_first, tile_first_len(index->capacity), kSortTile, stream),
-           "gs_build_index: pair offsets");
-    uint64_t P = 0;
-    GS_TRY(hipMemcpyAsync(&P, w.pair_off + n, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
-           "gs_build_index: reading the pair count");
-    GS_TRY(hipStreamSynchronize(stream), "gs_build_index: waiting for the pair count");
+    GS_TRY(hipEventSynchronize(pc->copied), "gs_build_index: waiting for the pair count");
+    const uint64_t P = *pc->value;
     index->n_pairs = (int64_t)P;
     if ((int64_t)P > index->capacity || P >= ((uint64_t)1 << 32))
         return fail(GS_ERR_CAPACITY, "gs_build_index: %llu pairs exceed the capacity %lld",
