@@ -254,12 +254,117 @@ __device__ __forceinline__ void write_out(float I, float V, float tau, bool work
     pr.out[k] = make_float2(phi, inf);
 }
 
-// One wavefront per item. Dense cells: lanes are queries of the cell and
-// walk its list together (records through the scalar path). Sparse cells:
-// lanes are the cell's candidate Gaussians (64 at a time, records loaded
-// once per cell) and the cell's queries are visited in turn, their
-// positions broadcast from SGPRs; per-lane partial sums are reduced across
-// the wave at the end, in a fixed order.
+// Sum over the SL lanes of a candidate-slot row (16: DPP row sum; 8: quad
+// sums, then row_half_mirror pairs the two quads of each half row).
+template <uint32_t SL>
+__device__ __forceinline__ float slot_sum(float x) {
+    if (SL == 16) return row16_sum(x);
+    x += dpp_f<0xB1>(x);
+    x += dpp_f<0x4E>(x);
+    x += dpp_f<0x141>(x);
+    return x;
+}
+
+// ROWS query rows x (64 / ROWS) candidate slots for a cell of
+// n < 8 ROWS queries: lane (r, s) evaluates queries r, r + ROWS, ... against
+// candidates s, s + 64 / ROWS, ... of the list; a query's partial sums are
+// then summed over its row with DPP.
+template <uint32_t ROWS>
+__device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t pa, uint32_t ja, uint32_t jb,
+                                           uint32_t c, uint32_t ncells, const QueryParams &q, const GridParams &g,
+                                           const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
+                                           const uint32_t *__restrict__ order, float T, float tau,
+                                           float *__restrict__ out_v, float *__restrict__ out_i,
+                                           const PlanResults &pr, float4 *buf) {
+        constexpr uint32_t SL = kWave / ROWS;  // candidate slots per row
+        const uint32_t row = lane / SL, sl = lane % SL;
+        const uint32_t nt = (n + ROWS - 1) / ROWS;  // queries per row, <= kRowsMax
+        uint32_t pid = 0;
+        float mx = 0.0f, my = 0.0f, mz = 0.0f;
+        bool valid = false;
+        if (lane < n) {
+            pid = order[pa + lane];
+            if ((int64_t)pid < q.n) query_position(q, g, pid, mx, my, mz, valid);
+        }
+        float px[kRowsMax], py[kRowsMax], pz[kRowsMax], Ip[kRowsMax], Vp[kRowsMax];
+#pragma unroll
+        for (uint32_t t = 0; t < kRowsMax; ++t) {
+            px[t] = py[t] = pz[t] = 0.0f;
+            Ip[t] = Vp[t] = 0.0f;
+            if (t < nt) {
+                const int src = (int)(row + ROWS * t);
+                px[t] = __shfl(mx, src, 64);
+                py[t] = __shfl(my, src, 64);
+                pz[t] = __shfl(mz, src, 64);
+            }
+        }
+        // The list is taken 64 candidates at a time: lane l copies candidate
+        // c0 + l's record from memory straight into the wave's LDS planes
+        // (lanes past the list copy its last record), the ids of the next 64
+        // are fetched meanwhile, and the steps of SL read the records from
+        // LDS, so a chunk waits for memory once instead of once per step.
+        uint32_t gnext = 0;
+        if (ja < jb) gnext = gids[ja + lane < jb ? ja + lane : jb - 1];
+        for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
+            const float4 *src = (const float4 *)(rec + gnext);
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq)
+                __builtin_amdgcn_global_load_lds((const void *)(src + qq),
+                                                 (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
+            if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
+            __builtin_amdgcn_s_waitcnt(0);
+            __builtin_amdgcn_wave_barrier();
+            const uint32_t left = jb - c0;
+            const uint32_t nstep = left >= (uint32_t)kWave ? kWave / SL : (left + SL - 1) / SL;
+            for (uint32_t st = 0; st < nstep; ++st) {
+                const uint32_t sidx = SL * st + sl;
+                Record r;
+                r.r0 = buf[sidx];
+                r.r1 = buf[kWave + sidx];
+                r.r2 = buf[2 * kWave + sidx];
+                r.r3 = buf[3 * kWave + sidx];
+                if (c0 + sidx >= jb) r.r0.w = 0.0f;  // past the list: weight 0
+#pragma unroll
+                for (uint32_t t = 0; t < kRowsMax; ++t) {
+                    if (t < nt) {
+                        const float a = eval_a(r, px[t], py[t], pz[t], T);
+                        Ip[t] += a;
+                        Vp[t] = fmaf_(a, r.r1.w, Vp[t]);
+                    }
+                }
+            }
+            // every lane has read the planes before the next chunk overwrites them
+            __builtin_amdgcn_wave_barrier();
+        }
+        float Io = 0.0f, Vo = 0.0f;
+#pragma unroll
+        for (uint32_t t = 0; t < kRowsMax; ++t) {
+            if (t < nt) {
+                const float It = slot_sum<SL>(Ip[t]), Vt = slot_sum<SL>(Vp[t]);
+                if (sl == t) {
+                    Io = It;
+                    Vo = Vt;
+                }
+            }
+        }
+        // lane (r, t) writes query r + ROWS t, whose id and position that lane holds
+        const uint32_t qi = row + ROWS * sl;
+        const int src = (int)(qi & 63u);
+        const uint32_t wpid = __shfl(pid, src, 64);
+        const float wx = __shfl(mx, src, 64), wy = __shfl(my, src, 64), wz = __shfl(mz, src, 64);
+        const bool wvalid = __shfl((int)valid, src, 64) != 0;
+        if (sl < nt && qi < n && (int64_t)wpid < q.n)
+            write_out(Io, Vo, tau, wvalid && c < ncells, wpid, pa + qi, wx, wy, wz, out_v, out_i, pr);
+}
+
+// One wavefront per item, by the queries n of the cell:
+//  * n >= 64: lanes are queries (64 per item) and walk the list together,
+//    records through the scalar path;
+//  * 4 <= n < 64: query rows x candidate slots (4 x 16 below 32 queries,
+//    8 x 8 from 32), records staged in LDS 64 at a time;
+//  * n < 4: lanes are the cell's candidates (64 at a time) and the queries
+//    are visited in turn, their positions broadcast from SGPRs.
+// Every query's sums are reduced in a fixed order.
 __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                          const uint32_t *__restrict__ gids,
                                                          const uint32_t *__restrict__ cell_off,
@@ -287,7 +392,7 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
         ja = ((ConstU32 *)cell_off)[c];
         jb = ((ConstU32 *)cell_off)[c + 1];
     }
-    if (n >= kDenseMin) {
+    if (n >= 2 * kDenseMin) {
         const uint32_t k = pa + chunk * kWave + lane;
         const bool active = k < pb;
         uint32_t pid = 0;
@@ -304,88 +409,11 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
         return;
     }
     if (n >= kRowsMin) {
-        // 4 query rows x 16 candidate slots: lane (r, s) evaluates queries
-        // r, r + 4, r + 8, ... against candidates s, s + 16, ... of the list;
-        // a query's partial sums are then summed over its row with DPP.
-        const uint32_t row = lane >> 4, sl = lane & 15u;
-        const uint32_t nt = (n + 3) >> 2;  // queries per row, <= kRowsMax
-        uint32_t pid = 0;
-        float mx = 0.0f, my = 0.0f, mz = 0.0f;
-        bool valid = false;
-        if (lane < n) {
-            pid = order[pa + lane];
-            if ((int64_t)pid < q.n) query_position(q, g, pid, mx, my, mz, valid);
-        }
-        float px[kRowsMax], py[kRowsMax], pz[kRowsMax], Ip[kRowsMax], Vp[kRowsMax];
-#pragma unroll
-        for (uint32_t t = 0; t < kRowsMax; ++t) {
-            px[t] = py[t] = pz[t] = 0.0f;
-            Ip[t] = Vp[t] = 0.0f;
-            if (t < nt) {
-                const int src = (int)(row + 4u * t);
-                px[t] = __shfl(mx, src, 64);
-                py[t] = __shfl(my, src, 64);
-                pz[t] = __shfl(mz, src, 64);
-            }
-        }
-        // The list is taken 64 candidates at a time: lane l copies candidate
-        // c0 + l's record from memory straight into the wave's LDS planes
-        // (lanes past the list copy its last record), the ids of the next 64
-        // are fetched meanwhile, and the steps of 16 read the records from
-        // LDS, so a chunk waits for memory once instead of once per step.
         float4 *buf = s_rec[threadIdx.x / kWave];
-        uint32_t gnext = 0;
-        if (ja < jb) gnext = gids[ja + lane < jb ? ja + lane : jb - 1];
-        for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
-            const float4 *src = (const float4 *)(rec + gnext);
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq)
-                __builtin_amdgcn_global_load_lds((const void *)(src + qq),
-                                                 (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
-            if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
-            __builtin_amdgcn_s_waitcnt(0);
-            __builtin_amdgcn_wave_barrier();
-            const uint32_t left = jb - c0;
-            const uint32_t nstep = left >= (uint32_t)kWave ? 4u : (left + 15) / 16;
-            for (uint32_t st = 0; st < nstep; ++st) {
-                const uint32_t sidx = 16 * st + sl;
-                Record r;
-                r.r0 = buf[sidx];
-                r.r1 = buf[kWave + sidx];
-                r.r2 = buf[2 * kWave + sidx];
-                r.r3 = buf[3 * kWave + sidx];
-                if (c0 + sidx >= jb) r.r0.w = 0.0f;  // past the list: weight 0
-#pragma unroll
-                for (uint32_t t = 0; t < kRowsMax; ++t) {
-                    if (t < nt) {
-                        const float a = eval_a(r, px[t], py[t], pz[t], T);
-                        Ip[t] += a;
-                        Vp[t] = fmaf_(a, r.r1.w, Vp[t]);
-                    }
-                }
-            }
-            // every lane has read the planes before the next chunk overwrites them
-            __builtin_amdgcn_wave_barrier();
-        }
-        float Io = 0.0f, Vo = 0.0f;
-#pragma unroll
-        for (uint32_t t = 0; t < kRowsMax; ++t) {
-            if (t < nt) {
-                const float It = row16_sum(Ip[t]), Vt = row16_sum(Vp[t]);
-                if (sl == t) {
-                    Io = It;
-                    Vo = Vt;
-                }
-            }
-        }
-        // lane (r, t) writes query r + 4 t, whose id and position lane r + 4 t holds
-        const uint32_t qi = row + 4u * sl;
-        const int src = (int)(qi & 63u);
-        const uint32_t wpid = __shfl(pid, src, 64);
-        const float wx = __shfl(mx, src, 64), wy = __shfl(my, src, 64), wz = __shfl(mz, src, 64);
-        const bool wvalid = __shfl((int)valid, src, 64) != 0;
-        if (sl < nt && qi < n && (int64_t)wpid < q.n)
-            write_out(Io, Vo, tau, wvalid && c < ncells, wpid, pa + qi, wx, wy, wz, out_v, out_i, pr);
+        if (n >= kDenseMin)
+            query_rows<8>(lane, n, pa, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr, buf);
+        else
+            query_rows<4>(lane, n, pa, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr, buf);
         return;
     }
     for (uint32_t p0 = pa; p0 < pb; p0 += kChunkB) {
