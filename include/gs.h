@@ -105,15 +105,22 @@ typedef struct gs_index {
  * listed voxel ids (id = x + dims0 (y + dims1 z)) of such a grid (any dims),
  * outputs in list order. POINTS: arbitrary positions, outputs in input
  * order. The centre of voxel (i, j, k) is lo + (i + 1/2) * ((hi - lo) / dims)
- * per axis, in float32 with each operation rounded. */
-enum { GS_QUERY_GRID = 0, GS_QUERY_VOXELS = 1, GS_QUERY_POINTS = 2 };
+ * per axis, in float32 with each operation rounded.
+ * JITTER: the training samples of Sec. 4.2.2, one random position inside
+ * each listed voxel (every voxel, x fastest, when voxel_ids is NULL; then n
+ * must equal the voxel count): query t lies at
+ * lo + (i + u) * ((hi - lo) / dims) per axis, with the caller's offsets
+ * u = points[t][axis] (drawn in [0, 1) for a position inside the voxel),
+ * in float32 with each operation rounded; outputs in list order. A voxel id
+ * past the grid gives an undefined output, as for VOXELS. */
+enum { GS_QUERY_GRID = 0, GS_QUERY_VOXELS = 1, GS_QUERY_POINTS = 2, GS_QUERY_JITTER = 3 };
 
 typedef struct gs_query {
     int32_t kind;
-    int32_t dims[3];            /* GRID, VOXELS */
-    int64_t n;                  /* VOXELS, POINTS: number of queries, < 2^31 */
-    const uint32_t *voxel_ids;  /* VOXELS: [n] */
-    const float *points;        /* POINTS: [n][3] */
+    int32_t dims[3];            /* GRID, VOXELS, JITTER */
+    int64_t n;                  /* VOXELS, POINTS, JITTER: number of queries, < 2^31 */
+    const uint32_t *voxel_ids;  /* VOXELS: [n]; JITTER: [n] or NULL (all voxels) */
+    const float *points;        /* POINTS: [n][3] positions; JITTER: [n][3] offsets u */
 } gs_query;
 
 /* Number of outputs of a query (dims product for GRID, n otherwise), or -1

@@ -46,6 +46,8 @@ def lib():
         L.orc_support.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, c_i64, vp, c_int, vp]
         L.orc_voxel_centers.restype = c_int
         L.orc_voxel_centers.argtypes = [vp, vp, vp, c_i64, vp, vp]
+        L.orc_jitter_positions.restype = c_int
+        L.orc_jitter_positions.argtypes = [vp, vp, vp, c_i64, vp, vp, vp]
         L.orc_index_boxes.restype = c_i64
         L.orc_index_boxes.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp, vp, vp]
         L.orc_index.restype = c_int
@@ -179,6 +181,29 @@ def voxel_centers(dims, lo=(0, 0, 0), hi=(1, 1, 1), ids=None) -> np.ndarray:
     rc = lib().orc_voxel_centers(_p(d), _p(lo_), _p(hi_), n, _p(idp), _p(out))
     if rc != 0:
         raise RuntimeError("orc_voxel_centers failed")
+    return out
+
+
+def jitter_positions(dims, u, lo=(0, 0, 0), hi=(1, 1, 1), ids=None) -> np.ndarray:
+    """Canonical float32 training positions lo + (i + u) * voxel size (Sec.
+    4.2.2): offsets u [n, 3] for the voxels ids (x fastest), or for every
+    voxel in order when ids is None."""
+    d = np.asarray(dims, dtype=np.int32).reshape(3)
+    lo_, hi_ = _box(lo, hi)
+    u = np.ascontiguousarray(u, dtype=np.float32).reshape(-1, 3)
+    n = u.shape[0]
+    idp = None
+    if ids is not None:
+        ids = np.ascontiguousarray(ids, dtype=np.uint32)
+        if ids.shape[0] != n:
+            raise ValueError("one offset row per voxel id")
+        idp = ids
+    elif n != int(d[0]) * int(d[1]) * int(d[2]):
+        raise ValueError("without ids there is one offset row per voxel")
+    out = np.zeros((n, 3), dtype=np.float32)
+    rc = lib().orc_jitter_positions(_p(d), _p(lo_), _p(hi_), n, _p(idp), _p(u), _p(out))
+    if rc != 0:
+        raise RuntimeError("orc_jitter_positions failed")
     return out
 
 

@@ -357,7 +357,8 @@ int orc_forward(int64_t n, const double *mean, const double *scale, const double
  * then through R(qhat) to qhat, and through qhat = q/|q| to q:
  *   dL/dq = (dL/dqhat - qhat (qhat . dL/dqhat)) / |q|.
  * Output per selected Gaussian, 12 values: dmu[3], ds[3], dq[4], dv, dw;
- * abs_out holds the sum over pairs of the absolute per-pair terms.
+ * abs_out holds the sum over pairs of the absolute per-pair terms, with
+ * dL/da counted as the sum of the magnitudes of its parts (see below).
  * Points with zero_mask[p] != 0 contribute nothing (their cotangents are
  * taken as zero). sel == NULL selects every Gaussian.
  */
@@ -397,8 +398,14 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
                 double G = exp(-0.5 * Q);
                 double a = g.w * G;
                 double dLda = gP * (g.v - Ph) / I + gI;
+                /* the size of dL/da as its two parts gPhi v / I and
+                 * gI - gPhi Phi / I: what an evaluation in float32 rounds,
+                 * for the tolerance sums (dL/da itself can cancel to ~0) */
+                double dLdaMag = fabs(gP * g.v / I) + fabs(gP * Ph / I) + fabs(gI);
                 double term[12];
-                double dLdQ = -0.5 * a * dLda;
+                /* every term but dv is linear in dL/dQ: form them for a unit
+                 * dL/dQ, then scale by the pair's value and by its size */
+                double dLdQ = 1.0;
                 for (int j = 0; j < 3; j++) {
                     double s_ = 0.0;
                     for (int k = 0; k < 3; k++) s_ += dLdQ * 2.0 * u[k] * g.R[j][k] / g.s[k];
@@ -420,12 +427,16 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
                                 y * dR[1][2] + x * dR[2][0] + y * dR[2][1]);
                 double dot = w * dqh[0] + x * dqh[1] + y * dqh[2] + z * dqh[3];
                 for (int k = 0; k < 4; k++) term[6 + k] = (dqh[k] - g.qhat[k] * dot) / g.qnorm;
-                term[10] = gP * a / I;
-                term[11] = dLda * G;
-                for (int k = 0; k < 12; k++) {
-                    acc[k] += term[k];
-                    aab[k] += fabs(term[k]);
+                const double dLdQv = -0.5 * a * dLda, dLdQm = 0.5 * a * dLdaMag;
+                for (int k = 0; k < 10; k++) {
+                    acc[k] += term[k] * dLdQv;
+                    aab[k] += fabs(term[k]) * dLdQm;
                 }
+                term[10] = gP * a / I;
+                acc[10] += term[10];
+                aab[10] += fabs(term[10]);
+                acc[11] += dLda * G;
+                aab[11] += dLdaMag * G;
             }
         }
         for (int k = 0; k < 12; k++) {
@@ -498,6 +509,34 @@ int orc_voxel_centers(const int32_t dims[3], const float lo[3], const float hi[3
         int64_t c[3] = {id % nx, (id / nx) % ny, id / (nx * ny)};
         for (int j = 0; j < 3; j++) {
             volatile float f = (float)c[j] + 0.5f;
+            volatile float m = f * vs[j];
+            out[3 * t + j] = lo[j] + m;
+        }
+    }
+    return ORC_OK;
+}
+
+/* Training sample positions (the structured training of Sec. 4.2.2: a random
+ * position in each voxel every iteration): voxel (i, j, k) of ids[t] (or t
+ * when ids is NULL) with the caller's offsets u = u[3t .. 3t + 2] lies at
+ * lo + (i + u) * ((hi - lo) / dims) per axis, in float32 with each operation
+ * rounded (u = 1/2 gives the voxel centre above). */
+int orc_jitter_positions(const int32_t dims[3], const float lo[3], const float hi[3], int64_t nids,
+                         const uint32_t *ids, const float *u, float *out)
+{
+    for (int j = 0; j < 3; j++)
+        if (dims[j] <= 0) return ORC_ERR_ARG;
+    float vs[3];
+    for (int j = 0; j < 3; j++) {
+        volatile float ext = hi[j] - lo[j];
+        vs[j] = ext / (float)dims[j];
+    }
+    int64_t nx = dims[0], ny = dims[1];
+    for (int64_t t = 0; t < nids; t++) {
+        int64_t id = ids ? (int64_t)ids[t] : t;
+        int64_t c[3] = {id % nx, (id / nx) % ny, id / (nx * ny)};
+        for (int j = 0; j < 3; j++) {
+            volatile float f = (float)c[j] + u[3 * t + j];
             volatile float m = f * vs[j];
             out[3 * t + j] = lo[j] + m;
         }

@@ -201,8 +201,8 @@ bool query_valid(const gs_query *q, std::string *why) {
         *why = "query is null";
         return false;
     }
-    if (q->kind == GS_QUERY_GRID || q->kind == GS_QUERY_VOXELS) {
-        int64_t nv = 1;
+    int64_t nv = 1;
+    if (q->kind == GS_QUERY_GRID || q->kind == GS_QUERY_VOXELS || q->kind == GS_QUERY_JITTER) {
         for (int j = 0; j < 3; ++j) {
             if (q->dims[j] <= 0) {
                 *why = "query dims must be positive";
@@ -216,7 +216,7 @@ bool query_valid(const gs_query *q, std::string *why) {
         }
     }
     if (q->kind == GS_QUERY_GRID) return true;
-    if (q->kind != GS_QUERY_VOXELS && q->kind != GS_QUERY_POINTS) {
+    if (q->kind != GS_QUERY_VOXELS && q->kind != GS_QUERY_POINTS && q->kind != GS_QUERY_JITTER) {
         *why = "unknown query kind";
         return false;
     }
@@ -230,6 +230,14 @@ bool query_valid(const gs_query *q, std::string *why) {
     }
     if (q->n > 0 && q->kind == GS_QUERY_POINTS && !q->points) {
         *why = "points is null";
+        return false;
+    }
+    if (q->n > 0 && q->kind == GS_QUERY_JITTER && !q->points) {
+        *why = "jitter offsets (points) are null";
+        return false;
+    }
+    if (q->kind == GS_QUERY_JITTER && !q->voxel_ids && q->n != nv) {
+        *why = "a jitter query without voxel_ids covers every voxel: n must equal the voxel count";
         return false;
     }
     return true;

@@ -27,6 +27,7 @@ GS_ERR_HIP = 4
 GS_QUERY_GRID = 0
 GS_QUERY_VOXELS = 1
 GS_QUERY_POINTS = 2
+GS_QUERY_JITTER = 3
 
 EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_bytes", "gs_sample",
             "gs_backward_work_bytes", "gs_sample_backward", "gs_last_error", "gs_version", "gs_profile_enable",
@@ -187,16 +188,29 @@ class Query:
     def pts(points: torch.Tensor) -> "Query":
         return Query(GS_QUERY_POINTS, (0, 0, 0), points=points)
 
+    @staticmethod
+    def jitter(dims, offsets: torch.Tensor, ids: Optional[torch.Tensor] = None) -> "Query":
+        """One position per voxel at lo + (i + u) * voxel size: offsets u
+        [n, 3] (in [0, 1) for a position inside the voxel), for the listed
+        voxel ids, or for every voxel (x fastest) when ids is None."""
+        return Query(GS_QUERY_JITTER, tuple(dims), voxel_ids=ids, points=offsets)
+
     def c(self) -> GsQuery:
         n = 0
-        if self.kind == GS_QUERY_VOXELS:
+        if self.kind == GS_QUERY_VOXELS or (self.kind == GS_QUERY_JITTER and self.voxel_ids is not None):
             if self.voxel_ids is None or not self.voxel_ids.is_cuda or self.voxel_ids.element_size() != 4 or \
                     not self.voxel_ids.is_contiguous():
                 raise ValueError("voxel_ids must be a contiguous 32-bit device tensor")
             n = self.voxel_ids.numel()
-        elif self.kind == GS_QUERY_POINTS:
+        if self.kind == GS_QUERY_POINTS:
             _dev_f32(self.points, "points", (3,))
             n = self.points.shape[0]
+        elif self.kind == GS_QUERY_JITTER:
+            _dev_f32(self.points, "jitter offsets", (3,))
+            if self.voxel_ids is None:
+                n = self.points.shape[0]
+            elif self.points.shape[0] != n:
+                raise ValueError("jitter offsets must have one row per voxel id")
         d = tuple(self.dims) if self.kind != GS_QUERY_POINTS else (0, 0, 0)
         return GsQuery(self.kind, (ctypes.c_int32 * 3)(*d), n, _ptr(self.voxel_ids), _ptr(self.points))
 

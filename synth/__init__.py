@@ -26,7 +26,7 @@ import numpy as np
 SEED = 260701164
 
 # stream ids
-S_MEAN, S_LOGSCALE, S_QUAT, S_VALUE, S_WEIGHT, S_MEANMIX, S_POINTS, S_BATCH, S_COTAN, S_COMP = range(10)
+S_MEAN, S_LOGSCALE, S_QUAT, S_VALUE, S_WEIGHT, S_MEANMIX, S_POINTS, S_BATCH, S_COTAN, S_COMP, S_JITTER = range(11)
 
 
 def rng(cfg: int, stream: int) -> np.random.Generator:
@@ -227,6 +227,13 @@ def cotangents(w: Workload, n: int, batch_index: int = 0) -> Tuple[np.ndarray, n
     gv = g.standard_normal(n).astype(np.float32)
     gi = g.standard_normal(n).astype(np.float32)
     return gv, gi
+
+
+def jitter_offsets(cfg: int, n: int, iteration: int = 0) -> np.ndarray:
+    """Training-sample offsets u in [0, 1)^3 per voxel (a random position in
+    each voxel every iteration), drawn directly in float32 so that u < 1."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(SEED, spawn_key=(cfg, S_JITTER, iteration))))
+    return g.random((n, 3), dtype=np.float32)
 
 
 def random_gaussians(seed: int, n: int, log_mu: float = np.log(0.05), log_sd: float = 0.3,

@@ -32,7 +32,7 @@ class Run:
     """One index + forward (+ backward) on the GPU."""
 
     def __init__(self, g: synth.Gaussians, cells, kind, dims=(0, 0, 0), ids=None, points=None, tau=TAU,
-                 lo=(0, 0, 0), hi=(1, 1, 1), capacity=None):
+                 lo=(0, 0, 0), hi=(1, 1, 1), capacity=None, offsets=None):
         import torch
         import paper_2607_01164_amd as gs
         self.gs, self.torch = gs, torch
@@ -51,6 +51,12 @@ class Run:
             self.ids_np = np.ascontiguousarray(ids, dtype=np.uint32)
             self.ids_dev = torch.from_numpy(self.ids_np.view(np.int32)).cuda()
             self.query = gs.Query.voxels(dims, self.ids_dev)
+        elif kind == "jitter":
+            self.ids_np = None if ids is None else np.ascontiguousarray(ids, dtype=np.uint32)
+            self.ids_dev = None if ids is None else torch.from_numpy(self.ids_np.view(np.int32)).cuda()
+            self.u_np = np.ascontiguousarray(offsets, dtype=np.float32)
+            self.u_dev = torch.from_numpy(self.u_np).cuda()
+            self.query = gs.Query.jitter(dims, self.u_dev, self.ids_dev)
         else:
             self.points_np = np.ascontiguousarray(points, dtype=np.float32)
             self.points_dev = torch.from_numpy(self.points_np).cuda()
@@ -64,7 +70,9 @@ class Run:
         self.influence = torch.empty(max(self.nq, 1), dtype=torch.float32, device="cuda")
         self.gs.gs_sample(self.dg, self.index, self.query, self.value, self.influence, self.plan)
         torch.cuda.synchronize()
-        return self.value[:self.nq].cpu().numpy(), self.influence[:self.nq].cpu().numpy()
+        self.phi_np = self.value[:self.nq].cpu().numpy()
+        self.inf_np = self.influence[:self.nq].cpu().numpy()
+        return self.phi_np, self.inf_np
 
     def backward(self, gv: np.ndarray, gi: np.ndarray):
         torch = self.torch
@@ -93,6 +101,14 @@ class Run:
         if self.kind == "voxels":
             ids = self.ids_np if sel is None else self.ids_np[sel]
             return oracle.voxel_centers(self.dims, self.lo, self.hi, ids=ids)
+        if self.kind == "jitter":
+            u = self.u_np if sel is None else self.u_np[sel]
+            ids = self.ids_np
+            if ids is None and sel is not None:
+                ids = np.asarray(sel, dtype=np.uint32)
+            elif ids is not None and sel is not None:
+                ids = ids[sel]
+            return oracle.jitter_positions(self.dims, u, self.lo, self.hi, ids=ids)
         return self.points_np if sel is None else self.points_np[sel]
 
 
@@ -138,10 +154,19 @@ def grad_tolerance(ref, ab, kap, rtol=1e-4):
     return rtol * (np.abs(ref) + ab) + 2.0 * e[:, None] * ab
 
 
-def check_backward(run: Run, grads_gpu: np.ndarray, sel, pts_sup, phi_sup, inf_sup, gv_sup, gi_sup, label=""):
+def check_backward(run: Run, grads_gpu: np.ndarray, sel, sup, gv_sup, gi_sup, label=""):
     """grads_gpu: [n, 12] for all Gaussians; the oracle recomputes the
-    selected Gaussians from the support points."""
+    selected Gaussians from the support queries sup (indices into the
+    query). The backward takes the forward's outputs as inputs (Sec. 4.1.4:
+    it consumes V, I and their cotangents), so the oracle is evaluated at
+    the outputs the GPU forward produced (run.forward() first): near the
+    definedness threshold dL/da = gPhi (v - Phi) / I + gI cancels, and the
+    forward's own tolerance on Phi would otherwise show up amplified."""
     t0 = time.time()
+    sup = np.asarray(sup)
+    pts_sup = run.positions(sup)
+    phi_sup = run.phi_np[sup].astype(np.float64)
+    inf_sup = run.inf_np[sup].astype(np.float64)
     ref, ab = oracle.backward(run.g, pts_sup, phi_sup, inf_sup, gv_sup, gi_sup, run.lo, run.hi, run.tau, select=sel)
     got = grads_gpu[sel]
     tol = grad_tolerance(ref, ab, kappa(run.g)[sel])

@@ -69,6 +69,25 @@ def test_sizing_functions():
     assert L.gs_query_size(ctypes.byref(empty)) == 0
 
 
+def test_jitter_query_validation():
+    """Training-sample queries: offsets required; without voxel ids the query
+    covers every voxel, so n must be the voxel count."""
+    L = gs.load_library()
+    g = grid()
+    dims = (ctypes.c_int32 * 3)(16, 8, 4)
+    full = gsq.GsQuery(gs.GS_QUERY_JITTER, dims, 16 * 8 * 4, None, FAKE)
+    assert L.gs_query_size(ctypes.byref(full)) == 16 * 8 * 4
+    assert L.gs_plan_bytes(ctypes.byref(full), ctypes.byref(g)) > 512 * 16
+    listed = gsq.GsQuery(gs.GS_QUERY_JITTER, dims, 100, FAKE, FAKE)
+    assert L.gs_query_size(ctypes.byref(listed)) == 100
+    short = gsq.GsQuery(gs.GS_QUERY_JITTER, dims, 100, None, FAKE)
+    assert L.gs_query_size(ctypes.byref(short)) == -1
+    no_offsets = gsq.GsQuery(gs.GS_QUERY_JITTER, dims, 100, FAKE, None)
+    assert L.gs_query_size(ctypes.byref(no_offsets)) == -1
+    bad_dims = gsq.GsQuery(gs.GS_QUERY_JITTER, (ctypes.c_int32 * 3)(16, 0, 4), 100, FAKE, FAKE)
+    assert L.gs_query_size(ctypes.byref(bad_dims)) == -1
+
+
 FAKE = 1 << 20  # a non-null, 256-aligned address that validation never dereferences
 
 

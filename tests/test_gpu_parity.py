@@ -57,7 +57,7 @@ def test_c1_grid_full(cells):
     gv, gi, amb = masked_cotangents(ref, gv, gi)
     grads = r.backward(gv, gi)
     pts = r.positions()
-    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="c1 all Gaussians")
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="c1 all Gaussians")
 
 
 @pytest.mark.parametrize("dims,cells", [((24, 20, 12), (8, 4, 3)), ((40, 40, 40), (4, 4, 4)),
@@ -74,7 +74,7 @@ def test_grid_ragged_cells(dims, cells):
     gv, gi = synth.random_normal(51, r.nq), synth.random_normal(52, r.nq)
     gv, gi, _ = masked_cotangents(ref, gv, gi)
     grads = r.backward(gv, gi)
-    check_backward(r, grads, np.arange(g.n), r.positions(), ref.phi, ref.inf, gv, gi, label="ragged")
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="ragged")
 
 
 def test_grid_non_unit_box():
@@ -107,7 +107,7 @@ def test_voxel_list_small():
     sub = np.nonzero(ok)[0]
     gv, gi, _ = masked_cotangents(ref, gv, gi, where=sub)
     grads = r.backward(gv, gi)
-    check_backward(r, grads, np.arange(g.n), r.positions(sub), ref.phi, ref.inf, gv[sub], gi[sub], label="voxels")
+    check_backward(r, grads, np.arange(g.n), sub, gv[sub], gi[sub], label="voxels")
 
 
 def test_points_small_with_outside_and_boundary():
@@ -124,7 +124,7 @@ def test_points_small_with_outside_and_boundary():
     gv, gi = synth.random_normal(59, r.nq), synth.random_normal(60, r.nq)
     gv, gi, _ = masked_cotangents(ref, gv, gi)
     grads = r.backward(gv, gi)
-    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="points")
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="points")
 
 
 def test_backward_with_empty_rows_and_boxes():
@@ -141,7 +141,7 @@ def test_backward_with_empty_rows_and_boxes():
     gv, gi = synth.random_normal(73, r.nq), synth.random_normal(74, r.nq)
     gv, gi, _ = masked_cotangents(ref, gv, gi)
     grads = r.backward(gv, gi)
-    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="corner")
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="corner")
 
 
 @pytest.mark.parametrize("case", ["one cell", "one pair"])
@@ -168,7 +168,51 @@ def test_index_and_backward_without_sort_passes(case):
     gv, gi = synth.random_normal(79, r.nq), synth.random_normal(80, r.nq)
     gv, gi, _ = masked_cotangents(ref, gv, gi)
     grads = r.backward(gv, gi)
-    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label=case)
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label=case)
+
+
+def test_jitter_queries_full_grid():
+    """Training samples (Sec. 4.2.2): one random position per voxel of a
+    whole grid, at the caller's offsets."""
+    g = synth.random_gaussians(88, 1200, log_mu=np.log(0.05), log_sd=0.5)
+    dims = (24, 20, 16)
+    n = 24 * 20 * 16
+    u = synth.jitter_offsets(88, n)
+    log("case jitter, every voxel of 24x20x16")
+    r = Run(g, (6, 5, 4), "jitter", dims=dims, offsets=u)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="jitter")
+    gv, gi = synth.random_normal(89, n), synth.random_normal(90, n)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="jitter")
+
+
+def test_jitter_queries_listed_voxels():
+    """Jittered positions of listed voxels, with offsets at 0 and just below
+    1 and ids past the grid (undefined outputs)."""
+    g = synth.random_gaussians(91, 2000, log_mu=np.log(0.04), log_sd=0.5, lo=-0.5, hi=1.5)
+    dims = (40, 30, 20)
+    nvox = 40 * 30 * 20
+    ids = np.random.default_rng(92).choice(nvox, size=9000, replace=False).astype(np.uint32)
+    ids[:3] = [nvox, nvox + 5, 0xFFFFFFF0]
+    u = synth.jitter_offsets(93, len(ids))
+    u[3:20] = 0.0
+    u[20:40] = np.nextafter(np.float32(1), np.float32(0))
+    lo, hi = (-0.5, -0.25, 0.0), (1.5, 1.25, 1.0)
+    log("case jitter, 9000 listed voxels")
+    r = Run(g, (8, 6, 5), "jitter", dims=dims, ids=ids, offsets=u, lo=lo, hi=hi)
+    phi, inf = r.forward()
+    assert np.all(phi[:3] == 0) and np.all(inf[:3] == 0)
+    sub = np.arange(3, len(ids))
+    check_forward(r, phi, inf, sel=sub, label="jitter listed")
+    ref = oracle.forward(g, r.positions(sub), lo, hi)
+    gv, gi = synth.random_normal(94, r.nq), synth.random_normal(95, r.nq)
+    gv[:3] = 0
+    gi[:3] = 0
+    gv, gi, _ = masked_cotangents(ref, gv, gi, where=sub)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), sub, gv[sub], gi[sub], label="jitter listed")
 
 
 def test_points_on_a_fine_index():
@@ -183,7 +227,7 @@ def test_points_on_a_fine_index():
     gv, gi = synth.random_normal(86, r.nq), synth.random_normal(87, r.nq)
     gv, gi, _ = masked_cotangents(ref, gv, gi)
     grads = r.backward(gv, gi)
-    check_backward(r, grads, np.arange(g.n), pts, ref.phi, ref.inf, gv, gi, label="fine index")
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="fine index")
 
 
 def test_index_tile_spanning_many_empty_gaussians():
@@ -245,7 +289,7 @@ def test_invalid_and_degenerate_gaussians():
     grads = r.backward(gv, gi)
     assert np.all(grads[:8] == 0)
     assert np.all(np.isfinite(grads))
-    check_backward(r, grads, np.arange(g.n), r.positions(), ref.phi, ref.inf, gv, gi, label="invalid")
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="invalid")
 
 
 def test_empty_inputs():

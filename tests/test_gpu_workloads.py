@@ -40,7 +40,7 @@ def sampled_backward(r: Run, w, seed):
     log(f"  support of {len(sel)} Gaussians: {len(sup)} queries, {int(amb.sum())} ambiguous")
     grads = r.backward(gv, gi)
     assert np.all(np.isfinite(grads))
-    check_backward(r, grads, sel, pts_all[sup], ref.phi, ref.inf, gv[sup], gi[sup], label=w.name)
+    check_backward(r, grads, sel, sup, gv[sup], gi[sup], label=w.name)
     return grads
 
 
