@@ -9,8 +9,10 @@ Gaussian parameter. All inputs are resident in HBM before the timed region.
 
 Prints one JSON line: fwd+bwd samples/s over the timed steps, with the
 forward-only query rate, the per-kernel timing of the step (HIP events on
-the library's stream), the roofline of the dominant kernel and the CPU
-oracle's rate on a bounded sample of the same workload.
+the library's stream), the roofline of the dominant kernel, the CPU
+oracle's rate on a bounded sample of the same workload, and the rate of a
+structured training step: 128^3 jittered samples (one random position per
+voxel) over the same Gaussians.
 """
 import argparse
 import hashlib
@@ -55,6 +57,7 @@ def parse():
     p.add_argument("--cells", type=int, nargs=3, default=list(INDEX_CELLS))
     p.add_argument("--cpu-seconds", type=float, default=16.0, help="target length of the CPU oracle sample")
     p.add_argument("--no-cpu", action="store_true")
+    p.add_argument("--no-jitter", action="store_true", help="skip the 128^3 jittered training-step line")
     p.add_argument("--breakdown", action="store_true", help="print the per-kernel table to stderr")
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, run a plain 256 MiB copy (counter calibration under rocprofv3)")
@@ -123,6 +126,50 @@ class Step:
         co = self.index.cell_offsets.to(torch.int64)
         pairs = co[1:] - co[:-1]
         return int((pts * pairs).sum().item())
+
+
+class JitterStep:
+    """Structured training step: one random position in every voxel of a
+    128^3 grid (2,097,152 samples), over the same Gaussians and index. The
+    offsets of several iterations are drawn beforehand and stay in HBM; each
+    step takes the next set, as training draws new positions every
+    iteration."""
+    DIMS = (128, 128, 128)
+    SETS = 4
+
+    def __init__(self, st: Step):
+        import numpy as np
+        import synth
+        gs, torch = st.gs, st.torch
+        self.st, self.gs = st, gs
+        self.n = self.DIMS[0] * self.DIMS[1] * self.DIMS[2]
+        dev = "cuda:0"
+        self.offsets = [torch.from_numpy(synth.jitter_offsets(st.w.cfg, self.n, it)).to(dev)
+                        for it in range(self.SETS)]
+        self.queries = [gs.Query.jitter(self.DIMS, u) for u in self.offsets]
+        gv, gi = synth.cotangents(st.w, self.n, batch_index=1)
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+        self.gv, self.gi = t(gv), t(gi)
+        self.plan = gs.alloc_plan(self.queries[0], st.grid, dev)
+        self.val = torch.empty(self.n, dtype=torch.float32, device=dev)
+        self.inf = torch.empty(self.n, dtype=torch.float32, device=dev)
+        self.grads = gs.Grads.empty(st.g_host.n, dev)
+        self.work = gs.alloc_backward_work(st.index, self.queries[0], dev)
+        self.it = 0
+        torch.cuda.synchronize()
+
+    def forward(self):
+        self.gs.gs_sample(self.st.dg, self.st.index, self.queries[self.it % self.SETS], self.val, self.inf, self.plan)
+
+    def backward(self):
+        self.gs.gs_sample_backward(self.st.dg, self.st.index, self.queries[self.it % self.SETS], self.plan, self.val,
+                                   self.inf, self.gv, self.gi, self.grads, self.work)
+
+    def step(self):
+        self.st.build()
+        self.forward()
+        self.backward()
+        self.it += 1
 
 
 def timed(fn, k, sync):
@@ -208,6 +255,16 @@ def main():
     t_fwd = timed(st.forward, a.steps, sync)
     t_bwd = timed(st.backward, a.steps, sync)
     t_build = timed(st.build, a.steps, sync)
+    jit = None
+    if not a.no_jitter:
+        js = JitterStep(st)
+        for _ in range(a.warmup):
+            js.step()
+        t_js = timed(js.step, a.steps, sync)
+        jit = {"workload": "128^3 grid, one random position per voxel (offsets redrawn each step, "
+                           f"{JitterStep.SETS} sets resident in HBM), same Gaussians; step = build + forward + backward",
+               "samples_per_step": js.n, "ms_per_step": t_js * 1e3, "fwd_bwd_samples_per_s": js.n / t_js}
+        del js
 
     if a.breakdown:
         for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
@@ -241,6 +298,7 @@ def main():
         "ms_build": t_build * 1e3, "ms_fwd": t_fwd * 1e3, "ms_bwd": t_bwd * 1e3,
         "gauss_point_evals_per_s": (contrib * st.n / t_fwd) if contrib else None,
         "kernels": {k: round(v["ms_per_step"] * 1e3, 2) for k, v in kernels.items()},
+        "jittered_training_step": jit,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
