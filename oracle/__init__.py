@@ -5,7 +5,9 @@ the benchmark's CPU-baseline leg, never by the product library. It is an
 independent float64 brute-force implementation (oracle.c) of the paper's
 Eq. 2 and Eq. 3 with the cutoff of Sec. 4.1.1 and the definedness rule of
 Sec. 4.1.3, their exact derivatives (Sec. 4.1.4), and the canonical float32
-cell index (Sec. 4.1.1, Sec. 4.1.2).
+cell index (Sec. 4.1.1, Sec. 4.1.2); and (train.c) the training steps on
+either side of the path: the activations of Sec. 4.2 and the losses of
+Sec. 4.2, Eq. 4 and Eq. 5 with their cotangents.
 
 Every function here is pinned by the tests in tests/test_oracle_*.py against
 closed forms, invariants, finite differences and brute-force recounts.
@@ -52,6 +54,12 @@ def lib():
         L.orc_index_boxes.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp, vp, vp]
         L.orc_index.restype = c_int
         L.orc_index.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp, c_i64, vp, vp]
+        L.orc_activate.restype = c_int
+        L.orc_activate.argtypes = [c_i64, vp, vp, vp, ctypes.c_double, vp, vp, vp]
+        L.orc_activate_backward.restype = c_int
+        L.orc_activate_backward.argtypes = [c_i64, vp, vp, vp, ctypes.c_double, vp, vp, vp, vp, vp, vp]
+        L.orc_loss.restype = c_int
+        L.orc_loss.argtypes = [c_i64, vp, vp, vp, vp, c_float, c_float, c_float, c_float, vp, vp, vp, vp]
         L.orc_point_order.restype = c_int
         L.orc_point_order.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp]
         _LIB = L
@@ -342,3 +350,69 @@ def accept_forward(ref: ForwardResult, phi_gpu, inf_gpu, tau: float = 0.01, rtol
 def ambiguous_points(ref: ForwardResult, tau: float = 0.01) -> np.ndarray:
     tau64 = float(np.float32(tau))
     return (ref.namb > 0) | (np.abs(ref.inf - tau64) <= 2.0 ** -16 * tau64)
+
+
+class RawGaussians:
+    """Free parameters before the activations of Sec. 4.2: log-scales
+    [n][3], value and weight logits [n] (means and quaternions pass through
+    the activations unchanged and are not needed here)."""
+
+    def __init__(self, log_scale, value_logit, weight_logit):
+        self.log_scale = _f64(log_scale).reshape(-1, 3)
+        self.value_logit = _f64(value_logit).reshape(-1)
+        self.weight_logit = _f64(weight_logit).reshape(-1)
+        self.n = self.log_scale.shape[0]
+
+
+def activate(raw: RawGaussians, cap: float):
+    """(scale [n][3], value [n], weight [n]) in float64: sigmoid values and
+    weights, exp scales with the soft norm cap c (none when c <= 0)."""
+    n = raw.n
+    s = np.zeros((n, 3))
+    v = np.zeros(n)
+    w = np.zeros(n)
+    rc = lib().orc_activate(n, _p(raw.log_scale), _p(raw.value_logit), _p(raw.weight_logit), float(cap),
+                            _p(s), _p(v), _p(w))
+    assert rc == 0, rc
+    return s, v, w
+
+
+def activate_backward(raw: RawGaussians, cap: float, d_scale, d_value, d_weight):
+    """Gradients of the free parameters (d log-scale [n][3], d value logit,
+    d weight logit) from those of the activated ones, in float64."""
+    n = raw.n
+    ds, dv, dw = _f64(d_scale).reshape(-1, 3), _f64(d_value).reshape(-1), _f64(d_weight).reshape(-1)
+    a = np.zeros((n, 3))
+    b = np.zeros(n)
+    c = np.zeros(n)
+    rc = lib().orc_activate_backward(n, _p(raw.log_scale), _p(raw.value_logit), _p(raw.weight_logit), float(cap),
+                                     _p(ds), _p(dv), _p(dw), _p(a), _p(b), _p(c))
+    assert rc == 0, rc
+    return a, b, c
+
+
+class LossResult:
+    def __init__(self, terms, counts, grad_value, grad_influence):
+        self.l1, self.fn, self.fp, self.total = (float(x) for x in terms)
+        self.n_defined, self.n_fn, self.n_fp = (int(x) for x in counts)
+        self.grad_value = grad_value
+        self.grad_influence = grad_influence
+
+
+def loss(value, influence, target, defined=None, tau=0.01, eps=0.1, lambda_fn=1.0, lambda_fp=1.0) -> LossResult:
+    """L1 + false-negative (Eq. 4) + false-positive (Eq. 5) losses of a batch
+    of sampler outputs against targets, and the cotangents for the sampler's
+    backward (float32). defined: per-sample flag of the original volume, or
+    None when every sample is defined there."""
+    v, i, y = _f32(value).reshape(-1), _f32(influence).reshape(-1), _f32(target).reshape(-1)
+    n = v.shape[0]
+    assert i.shape[0] == n and y.shape[0] == n
+    d = None if defined is None else np.ascontiguousarray(defined, dtype=np.uint8).reshape(-1)
+    terms = np.zeros(4)
+    counts = np.zeros(3, dtype=np.int64)
+    gv = np.zeros(n, dtype=np.float32)
+    gi = np.zeros(n, dtype=np.float32)
+    rc = lib().orc_loss(n, _p(v), _p(i), _p(y), _p(d), float(tau), float(eps), float(lambda_fn),
+                        float(lambda_fp), _p(terms), _p(counts), _p(gv), _p(gi))
+    assert rc == 0, rc
+    return LossResult(terms, counts, gv, gi)
