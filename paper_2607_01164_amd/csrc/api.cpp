@@ -1,6 +1,7 @@
 // C-ABI of the library (include/gs.h): argument validation, workspace
 // layout, the three entry points, and kernel timing.
 #include "../../include/gs.h"
+#include "../../include/gs_train.h"
 
 #include <cmath>
 #include <cstdarg>
@@ -11,6 +12,12 @@
 
 #include "internal.h"
 #include "radix.h"
+
+namespace gs {
+hipError_t launch_loss(int64_t n, const float *value, const float *influence, const float *target,
+                       const uint8_t *defined, float tau, float eps, float lambda_fn, float lambda_fp,
+                       float *grad_value, float *grad_influence, gs_loss_terms *terms, void *work, hipStream_t s);
+}
 
 using namespace gs;
 
@@ -132,7 +139,6 @@ struct IndexWork {
 // pair counts are summed per 64 Gaussians (the preprocess workgroups, the
 // last one holding count[n] = 0); the scan of the sums of the first
 // ceil(n / 64) groups is followed by their total
-int64_t pair_groups(int64_t n) { return (n + 1 + 63) / 64; }
 int64_t pair_groups_scanned(int64_t n) { return (n + 63) / 64; }
 int64_t tile_first_len(int64_t capacity) { return ((capacity > 0 ? capacity : 1) + kSortTile - 1) / kSortTile + 1; }
 
@@ -639,6 +645,68 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
                            grad_influence, cutoff_T(index->tau), bw.b, gauss->mean, gauss->scale, gauss->rot, d_mean,
                            d_scale, d_rot, d_value, d_weight, stream),
            "gs_sample_backward");
+    return GS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Training epilogue (include/gs_train.h).
+
+gs_status gs_activate(int64_t n, const float *log_scale, const float *value_logit, const float *weight_logit,
+                      float scale_cap, float *scale, float *value, float *weight, hipStream_t stream) {
+    if (n < 0 || n >= ((int64_t)1 << 31)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_activate: n = %lld out of range",
+                                                      (long long)n);
+    if (n == 0) return GS_OK;
+    if (!log_scale || !value_logit || !weight_logit || !scale || !value || !weight)
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_activate: null array");
+    const double cap = std::isfinite(scale_cap) && scale_cap > 0.0f ? (double)scale_cap : 0.0;
+    GS_TRY(launch_activate(n, log_scale, value_logit, weight_logit, cap, scale, value, weight, stream),
+           "gs_activate");
+    return GS_OK;
+}
+
+gs_status gs_activate_backward(int64_t n, const float *log_scale, const float *value_logit,
+                               const float *weight_logit, float scale_cap, const float *d_scale,
+                               const float *d_value, const float *d_weight, float *d_log_scale,
+                               float *d_value_logit, float *d_weight_logit, hipStream_t stream) {
+    if (n < 0 || n >= ((int64_t)1 << 31))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_activate_backward: n = %lld out of range", (long long)n);
+    if (n == 0) return GS_OK;
+    if (!log_scale || !value_logit || !weight_logit || !d_scale || !d_value || !d_weight || !d_log_scale ||
+        !d_value_logit || !d_weight_logit)
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_activate_backward: null array");
+    const double cap = std::isfinite(scale_cap) && scale_cap > 0.0f ? (double)scale_cap : 0.0;
+    GS_TRY(launch_activate_backward(n, log_scale, value_logit, weight_logit, cap, d_scale, d_value, d_weight,
+                                    d_log_scale, d_value_logit, d_weight_logit, stream),
+           "gs_activate_backward");
+    return GS_OK;
+}
+
+size_t gs_loss_work_bytes(int64_t n) {
+    if (n < 0 || n >= ((int64_t)1 << 31)) return (size_t)-1;
+    return loss_work_bytes(n);
+}
+
+gs_status gs_loss(int64_t n, const float *value, const float *influence, const float *target,
+                  const uint8_t *defined, const gs_loss_params *params, float *grad_value, float *grad_influence,
+                  gs_loss_terms *terms, void *work, size_t work_bytes, hipStream_t stream) {
+    if (n < 0 || n >= ((int64_t)1 << 31)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_loss: n = %lld out of range",
+                                                      (long long)n);
+    if (!params || !terms) return fail(GS_ERR_INVALID_ARGUMENT, "gs_loss: params or terms is null");
+    if (n > 0 && (!value || !influence || !target || !grad_value || !grad_influence))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_loss: null array");
+    const gs_loss_params p = *params;
+    if (!(p.tau > 0.0f && p.tau < 1.0f)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_loss: tau must lie in (0, 1)");
+    if (!(std::isfinite(p.fn_eps) && p.fn_eps >= 0.0f))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_loss: fn_eps must be finite and >= 0");
+    if (!std::isfinite(p.fn_lambda) || !std::isfinite(p.fp_lambda))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_loss: loss weights must be finite");
+    const size_t need = loss_work_bytes(n);
+    if (!work || work_bytes < need || !aligned(work))
+        return fail(GS_ERR_WORKSPACE, "gs_loss: workspace needs %zu bytes, 256-byte aligned (got %zu)", need,
+                    work_bytes);
+    GS_TRY(launch_loss(n, value, influence, target, defined, p.tau, p.fn_eps, p.fn_lambda, p.fp_lambda, grad_value,
+                       grad_influence, terms, work, stream),
+           "gs_loss");
     return GS_OK;
 }
 

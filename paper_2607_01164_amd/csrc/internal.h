@@ -342,4 +342,13 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
                            float *d_mean, float *d_scale, float *d_rot, float *d_value, float *d_weight,
                            hipStream_t s);
 
+// Training epilogue (train.hip). cap <= 0 disables the soft cap.
+size_t loss_work_bytes(int64_t n);
+hipError_t launch_activate(int64_t n, const float *log_scale, const float *value_logit, const float *weight_logit,
+                           double cap, float *scale, float *value, float *weight, hipStream_t s);
+hipError_t launch_activate_backward(int64_t n, const float *log_scale, const float *value_logit,
+                                    const float *weight_logit, double cap, const float *d_scale,
+                                    const float *d_value, const float *d_weight, float *d_log_scale,
+                                    float *d_value_logit, float *d_weight_logit, hipStream_t s);
+
 }  // namespace gs

@@ -1,4 +1,4 @@
-"""Python binding of the C-ABI in include/gs.h (ctypes).
+"""Python binding of the C-ABI in include/gs.h and include/gs_train.h (ctypes).
 
 Argument marshalling only: every step of sampling runs in the HIP library
 libgsq.so. torch provides device memory and the stream. Importing this module
@@ -31,7 +31,8 @@ GS_QUERY_JITTER = 3
 
 EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_bytes", "gs_sample",
             "gs_backward_work_bytes", "gs_sample_backward", "gs_last_error", "gs_version", "gs_profile_enable",
-            "gs_profile_select", "gs_profile_reset", "gs_profile_read")
+            "gs_profile_select", "gs_profile_reset", "gs_profile_read", "gs_activate", "gs_activate_backward",
+            "gs_loss_work_bytes", "gs_loss")
 
 
 class GsLibraryMissing(RuntimeError):
@@ -63,6 +64,13 @@ class GsQuery(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("dims", ctypes.c_int32 * 3), ("n", ctypes.c_int64),
                 ("voxel_ids", ctypes.c_void_p), ("points", ctypes.c_void_p)]
 
+
+class GsLossParams(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("fn_eps", ctypes.c_float), ("fn_lambda", ctypes.c_float),
+                ("fp_lambda", ctypes.c_float)]
+
+
+LOSS_TERMS_BYTES = 64  # gs_loss_terms: four float64 values, then four int64 counts
 
 _LIB = None
 
@@ -104,6 +112,15 @@ def load_library():
     L.gs_profile_reset.argtypes = []
     L.gs_profile_read.restype = ctypes.c_int
     L.gs_profile_read.argtypes = [P(ctypes.c_char_p), P(i64), P(ctypes.c_double), ctypes.c_int]
+    f32 = ctypes.c_float
+    L.gs_activate.restype = ctypes.c_int
+    L.gs_activate.argtypes = [i64, vp, vp, vp, f32, vp, vp, vp, vp]
+    L.gs_activate_backward.restype = ctypes.c_int
+    L.gs_activate_backward.argtypes = [i64, vp, vp, vp, f32, vp, vp, vp, vp, vp, vp, vp]
+    L.gs_loss_work_bytes.restype = sz
+    L.gs_loss_work_bytes.argtypes = [i64]
+    L.gs_loss.restype = ctypes.c_int
+    L.gs_loss.argtypes = [i64, vp, vp, vp, vp, P(GsLossParams), vp, vp, vp, vp, sz, vp]
     _LIB = L
     return L
 
@@ -351,6 +368,109 @@ def gs_sample_backward(gauss: Gaussians, index: Index, query: Query, plan: Optio
         value.data_ptr(), influence.data_ptr(), grad_value.data_ptr(), grad_influence.data_ptr(),
         grads.mean.data_ptr(), grads.scale.data_ptr(), grads.rot.data_ptr(), grads.value.data_ptr(),
         grads.weight.data_ptr(), work.data_ptr(), work.numel(), _stream(stream))
+    _check(st)
+
+
+@dataclass
+class RawParams:
+    """Free parameters before the activations of Sec. 4.2: log_scale [n,3],
+    value_logit [n], weight_logit [n] (means and quaternions are used as
+    they are)."""
+    log_scale: torch.Tensor
+    value_logit: torch.Tensor
+    weight_logit: torch.Tensor
+
+    @property
+    def n(self) -> int:
+        return int(self.log_scale.shape[0])
+
+    def check(self):
+        _dev_f32(self.log_scale, "log_scale", (3,))
+        for t, nm in ((self.value_logit, "value_logit"), (self.weight_logit, "weight_logit")):
+            _dev_f32(t, nm)
+            if t.numel() != self.n:
+                raise ValueError("parameter arrays disagree on n")
+
+
+def gs_activate(raw: RawParams, scale_cap: float, scale: torch.Tensor, value: torch.Tensor, weight: torch.Tensor,
+                stream=None) -> None:
+    raw.check()
+    n = raw.n
+    _dev_f32(scale, "scale", (3,))
+    for t, nm in ((value, "value"), (weight, "weight")):
+        _dev_f32(t, nm)
+    if scale.shape[0] != n or value.numel() != n or weight.numel() != n:
+        raise ValueError("output arrays must hold n Gaussians")
+    st = load_library().gs_activate(n, raw.log_scale.data_ptr(), raw.value_logit.data_ptr(),
+                                    raw.weight_logit.data_ptr(), float(scale_cap), scale.data_ptr(),
+                                    value.data_ptr(), weight.data_ptr(), _stream(stream))
+    _check(st)
+
+
+def gs_activate_backward(raw: RawParams, scale_cap: float, grads: "Grads", out: RawParams, stream=None) -> None:
+    """Gradients of the free parameters (into out) from grads, the
+    gradients of the activated scale, value and weight."""
+    raw.check()
+    out.check()
+    n = raw.n
+    for t, nm in ((grads.scale, "d_scale"), (grads.value, "d_value"), (grads.weight, "d_weight")):
+        _dev_f32(t, nm)
+        if t.shape[0] != n:
+            raise ValueError(f"{nm} must hold n Gaussians")
+    if out.n != n:
+        raise ValueError("output arrays must hold n Gaussians")
+    st = load_library().gs_activate_backward(
+        n, raw.log_scale.data_ptr(), raw.value_logit.data_ptr(), raw.weight_logit.data_ptr(), float(scale_cap),
+        grads.scale.data_ptr(), grads.value.data_ptr(), grads.weight.data_ptr(), out.log_scale.data_ptr(),
+        out.value_logit.data_ptr(), out.weight_logit.data_ptr(), _stream(stream))
+    _check(st)
+
+
+def loss_work_bytes(n: int) -> int:
+    b = load_library().gs_loss_work_bytes(int(n))
+    if b == ctypes.c_size_t(-1).value:
+        raise GsError(GS_ERR_INVALID_ARGUMENT, f"batch size {n} out of range")
+    return int(b)
+
+
+def alloc_loss_work(n: int, device) -> torch.Tensor:
+    return _alloc_bytes(loss_work_bytes(n), device)
+
+
+def alloc_loss_terms(device) -> torch.Tensor:
+    return torch.zeros(LOSS_TERMS_BYTES, dtype=torch.uint8, device=device)
+
+
+def read_loss_terms(terms: torch.Tensor) -> dict:
+    """The gs_loss_terms a gs_loss call wrote (copies to the host)."""
+    b = terms.cpu()
+    d = b[:32].view(torch.float64).tolist()
+    c = b[32:64].view(torch.int64).tolist()
+    return {"l1": d[0], "fn": d[1], "fp": d[2], "total": d[3], "n_defined": c[0], "n_fn": c[1], "n_fp": c[2],
+            "n": c[3]}
+
+
+def gs_loss(value: torch.Tensor, influence: torch.Tensor, target: torch.Tensor, defined: Optional[torch.Tensor],
+            tau: float, fn_eps: float, fn_lambda: float, fp_lambda: float, grad_value: torch.Tensor,
+            grad_influence: torch.Tensor, terms: torch.Tensor, work: torch.Tensor, stream=None) -> None:
+    """L1 + false-negative (Eq. 4) + false-positive (Eq. 5) losses of a
+    batch and their cotangents; defined is a uint8 flag per sample (None:
+    every sample lies in the volume). terms: LOSS_TERMS_BYTES device bytes."""
+    n = int(value.numel())
+    for t, nm in ((value, "value"), (influence, "influence"), (target, "target"), (grad_value, "grad_value"),
+                  (grad_influence, "grad_influence")):
+        _dev_f32(t, nm)
+        if t.numel() != n:
+            raise ValueError(f"{nm} must have {n} elements")
+    if defined is not None:
+        if not defined.is_cuda or defined.dtype != torch.uint8 or not defined.is_contiguous() or defined.numel() != n:
+            raise ValueError("defined must be a contiguous uint8 device tensor of n elements")
+    if not terms.is_cuda or terms.numel() * terms.element_size() < LOSS_TERMS_BYTES or terms.data_ptr() % 8:
+        raise ValueError("terms must be a device buffer of at least 64 bytes, 8-byte aligned")
+    p = GsLossParams(float(tau), float(fn_eps), float(fn_lambda), float(fp_lambda))
+    st = load_library().gs_loss(n, value.data_ptr(), influence.data_ptr(), target.data_ptr(), _ptr(defined),
+                                ctypes.byref(p), grad_value.data_ptr(), grad_influence.data_ptr(), terms.data_ptr(),
+                                work.data_ptr(), work.numel() * work.element_size(), _stream(stream))
     _check(st)
 
 

@@ -26,7 +26,8 @@ import numpy as np
 SEED = 260701164
 
 # stream ids
-S_MEAN, S_LOGSCALE, S_QUAT, S_VALUE, S_WEIGHT, S_MEANMIX, S_POINTS, S_BATCH, S_COTAN, S_COMP, S_JITTER = range(11)
+S_MEAN, S_LOGSCALE, S_QUAT, S_VALUE, S_WEIGHT, S_MEANMIX, S_POINTS, S_BATCH, S_COTAN, S_COMP, S_JITTER, S_TARGET = \
+    range(12)
 
 
 def rng(cfg: int, stream: int) -> np.random.Generator:
@@ -234,6 +235,26 @@ def jitter_offsets(cfg: int, n: int, iteration: int = 0) -> np.ndarray:
     each voxel every iteration), drawn directly in float32 so that u < 1."""
     g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(SEED, spawn_key=(cfg, S_JITTER, iteration))))
     return g.random((n, 3), dtype=np.float32)
+
+
+def raw_params(w: Workload, n: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Free parameters behind make_gaussians, before the activations:
+    log-scales [n,3] (the same draws), value logits log(v / (1 - v)) of the
+    same U[0,1] values (clipped to [1e-6, 1 - 1e-6]) and weight logits (the
+    same standard normals); float32."""
+    n = w.n_gauss if n is None else n
+    log_s = rng(w.cfg, S_LOGSCALE).normal(w.log_scale_mu, w.log_scale_sd, size=(n, 3))
+    v = np.clip(rng(w.cfg, S_VALUE).random(n), 1e-6, 1.0 - 1e-6)
+    z = rng(w.cfg, S_WEIGHT).standard_normal(n)
+    f = np.float32
+    return log_s.astype(f), np.log(v / (1.0 - v)).astype(f), z.astype(f)
+
+
+def targets(cfg: int, n: int, iteration: int = 0) -> np.ndarray:
+    """Target values of a training batch, U[0,1] float32 (the ground truth a
+    structured volume would give at the samples)."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(SEED, spawn_key=(cfg, S_TARGET, iteration))))
+    return g.random(n, dtype=np.float32)
 
 
 def random_gaussians(seed: int, n: int, log_mu: float = np.log(0.05), log_sd: float = 0.3,

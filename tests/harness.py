@@ -140,6 +140,22 @@ def check_forward(run: Run, phi, inf, sel=None, label=""):
     return ref, stats
 
 
+def masked_cotangents(ref, gv, gi, where=None):
+    """Cotangents with the points that lie within float32 rounding of a
+    cutoff or of the definedness threshold zeroed (on both sides of a
+    backward comparison): there the intersecting set itself may differ."""
+    amb = oracle.ambiguous_points(ref, TAU)
+    gv = gv.copy()
+    gi = gi.copy()
+    if where is None:
+        gv[amb] = 0
+        gi[amb] = 0
+    else:
+        gv[where[amb]] = 0
+        gi[where[amb]] = 0
+    return gv, gi, amb
+
+
 def kappa(g: synth.Gaussians) -> np.ndarray:
     """Axis ratio per Gaussian (1 for invalid ones, which contribute nothing)."""
     s = g.scale.astype(np.float64)

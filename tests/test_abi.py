@@ -1,4 +1,4 @@
-"""The C-ABI library loads and exports every function include/gs.h declares,
+"""The C-ABI library loads and exports every function include/*.h declares,
 and its host-side validation rejects malformed arguments before any device
 work (no GPU needed: nothing here launches a kernel)."""
 import ctypes
@@ -15,7 +15,8 @@ SIZE_ERR = ctypes.c_size_t(-1).value
 
 
 def declared_functions():
-    text = open(os.path.join(ROOT, "include", "gs.h")).read()
+    inc = os.path.join(ROOT, "include")
+    text = "".join(open(os.path.join(inc, f)).read() for f in sorted(os.listdir(inc)) if f.endswith(".h"))
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(gs_[a-z_]+)\s*\(", text)))
 
@@ -226,3 +227,40 @@ def test_binding_fails_loudly_without_the_library(monkeypatch):
     monkeypatch.setattr(gsq, "LIB_PATH", "/nonexistent/libgsq.so")
     with pytest.raises(gs.GsLibraryMissing):
         gsq.load_library()
+
+
+def test_training_epilogue_validation():
+    """gs_train.h entry points reject malformed arguments before any launch."""
+    L = gs.load_library()
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: every call below fails validation first
+    assert L.gs_activate(-1, fake, fake, fake, 0.02, fake, fake, fake, None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert L.gs_activate(1 << 31, fake, fake, fake, 0.02, fake, fake, fake, None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert L.gs_activate(0, None, None, None, 0.02, None, None, None, None) == gs.GS_OK  # nothing to do
+    assert L.gs_activate(5, fake, None, fake, 0.02, fake, fake, fake, None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert b"null" in L.gs_last_error()
+    assert L.gs_activate_backward(5, fake, fake, fake, 0.0, fake, fake, None, fake, fake, fake, None) == \
+        gs.GS_ERR_INVALID_ARGUMENT
+    assert L.gs_activate_backward(0, None, None, None, 0.0, None, None, None, None, None, None, None) == gs.GS_OK
+    # loss workspace sizing
+    a, b = L.gs_loss_work_bytes(1), L.gs_loss_work_bytes(1 << 24)
+    assert 0 < a <= b and a % 256 == 0 and b % 256 == 0
+    assert L.gs_loss_work_bytes(0) > 0
+    assert L.gs_loss_work_bytes(-1) == SIZE_ERR and L.gs_loss_work_bytes(1 << 31) == SIZE_ERR
+    ok = gsq.GsLossParams(0.01, 0.1, 1.0, 1.0)
+    P = ctypes.byref
+    n, need = 1000, L.gs_loss_work_bytes(1000)
+    args = lambda p, work=ctypes.c_void_p(1 << 20), wb=need, terms=fake, v=fake: \
+        L.gs_loss(n, v, fake, fake, None, p, fake, fake, terms, work, wb, None)
+    assert args(None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert args(P(ok), terms=None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert args(P(ok), v=None) == gs.GS_ERR_INVALID_ARGUMENT
+    for bad in (gsq.GsLossParams(0.0, 0.1, 1, 1), gsq.GsLossParams(1.0, 0.1, 1, 1),
+                gsq.GsLossParams(float("nan"), 0.1, 1, 1), gsq.GsLossParams(0.01, -0.1, 1, 1),
+                gsq.GsLossParams(0.01, float("inf"), 1, 1), gsq.GsLossParams(0.01, 0.1, float("nan"), 1),
+                gsq.GsLossParams(0.01, 0.1, 1, float("inf"))):
+        assert args(P(bad)) == gs.GS_ERR_INVALID_ARGUMENT, (bad.tau, bad.fn_eps, bad.fn_lambda, bad.fp_lambda)
+    assert args(P(ok), wb=need - 1) == gs.GS_ERR_WORKSPACE
+    assert args(P(ok), work=ctypes.c_void_p((1 << 20) + 8)) == gs.GS_ERR_WORKSPACE
+    assert args(P(ok), work=None) == gs.GS_ERR_WORKSPACE
+    assert L.gs_loss(-1, fake, fake, fake, None, P(ok), fake, fake, fake, fake, need, None) == \
+        gs.GS_ERR_INVALID_ARGUMENT

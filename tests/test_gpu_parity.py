@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 import synth
-from harness import TAU, Run, check_backward, check_forward, check_index, log
+from harness import TAU, Run, check_backward, check_forward, check_index, log, masked_cotangents
 
 pytestmark = pytest.mark.gpu
 
@@ -27,19 +27,6 @@ def _gpu():
         pytest.skip("no GPU")
     import paper_2607_01164_amd as gs
     gs.load_library()
-
-
-def masked_cotangents(ref, gv, gi, where=None):
-    amb = oracle.ambiguous_points(ref, TAU)
-    gv = gv.copy()
-    gi = gi.copy()
-    if where is None:
-        gv[amb] = 0
-        gi[amb] = 0
-    else:
-        gv[where[amb]] = 0
-        gi[where[amb]] = 0
-    return gv, gi, amb
 
 
 # ---------------------------------------------------------------- small cases

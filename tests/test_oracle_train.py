@@ -153,6 +153,11 @@ def test_sigmoid_closed_forms():
     _, dv, dw = oracle.activate_backward(r, 0.0, np.zeros((3, 3)), np.ones(3), np.ones(3))
     np.testing.assert_allclose(dv, [0.25, 0.1875, 0.1875], rtol=1e-15)
     assert dw[0] == 0.25
+    # far in the tail the derivative is e^-x (1 + O(e^-x)), not a rounded 0
+    r = oracle.RawGaussians(np.zeros((2, 3)), [40.0, -60.0], [80.0, 700.0])
+    _, dv, dw = oracle.activate_backward(r, 0.0, np.zeros((2, 3)), np.ones(2), np.ones(2))
+    np.testing.assert_allclose(dv, [math.exp(-40.0), math.exp(-60.0)], rtol=1e-15)
+    np.testing.assert_allclose(dw, [math.exp(-80.0), math.exp(-700.0)], rtol=1e-15)
 
 
 def test_scale_without_cap_is_exp():
