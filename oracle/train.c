@@ -85,7 +85,7 @@ int orc_activate(int64_t n, const double *log_scale, const double *value_logit, 
 /* Chain rule through the activations: from the gradients with respect to
  * the activated scale, value and weight to those of the free parameters.
  * With s_k = e_k g(|e|): dL/de_j = g dL/ds_j + (sum_k dL/ds_k e_k) g'(|e|)
- * e_j / |e|, and dL/ds'_j = dL/de_j e_j; sigmoid' = sigmoid (1 - sigmoid). */
+ * e_j / |e|, and dL/ds'_j = dL/de_j e_j; sigmoid'(x) = sigmoid(x) sigmoid(-x). */
 int orc_activate_backward(int64_t n, const double *log_scale, const double *value_logit,
                           const double *weight_logit, double cap, const double *d_scale, const double *d_value,
                           const double *d_weight, double *d_log_scale, double *d_value_logit,
@@ -105,9 +105,10 @@ int orc_activate_backward(int64_t n, const double *log_scale, const double *valu
             const double dLde = g * d_scale[3 * i + k] + dot * dgn * e[k];
             d_log_scale[3 * i + k] = dLde * e[k];
         }
-        const double sv = sigmoid(value_logit[i]), sw = sigmoid(weight_logit[i]);
-        d_value_logit[i] = d_value[i] * sv * (1.0 - sv);
-        d_weight_logit[i] = d_weight[i] * sw * (1.0 - sw);
+        /* sigmoid'(x) = sigmoid(x) sigmoid(-x), which unlike
+         * sigmoid(x) (1 - sigmoid(x)) does not round to 0 for large x */
+        d_value_logit[i] = d_value[i] * (sigmoid(value_logit[i]) * sigmoid(-value_logit[i]));
+        d_weight_logit[i] = d_weight[i] * (sigmoid(weight_logit[i]) * sigmoid(-weight_logit[i]));
     }
     return ORC_OK;
 }
