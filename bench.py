@@ -11,8 +11,9 @@ Prints one JSON line: fwd+bwd samples/s over the timed steps, with the
 forward-only query rate, the per-kernel timing of the step (HIP events on
 the library's stream), the roofline of the dominant kernel, the CPU
 oracle's rate on a bounded sample of the same workload, and the rate of a
-structured training step: 128^3 jittered samples (one random position per
-voxel) over the same Gaussians.
+structured training step: activations, index, 128^3 jittered samples (one
+random position per voxel), losses, backward and the activations' backward
+over the free parameters behind the same Gaussians.
 """
 import argparse
 import hashlib
@@ -57,7 +58,7 @@ def parse():
     p.add_argument("--cells", type=int, nargs=3, default=list(INDEX_CELLS))
     p.add_argument("--cpu-seconds", type=float, default=16.0, help="target length of the CPU oracle sample")
     p.add_argument("--no-cpu", action="store_true")
-    p.add_argument("--no-jitter", action="store_true", help="skip the 128^3 jittered training-step line")
+    p.add_argument("--no-train", action="store_true", help="skip the 128^3 structured training-step line")
     p.add_argument("--breakdown", action="store_true", help="print the per-kernel table to stderr")
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, run a plain 256 MiB copy (counter calibration under rocprofv3)")
@@ -128,47 +129,66 @@ class Step:
         return int((pts * pairs).sum().item())
 
 
-class JitterStep:
-    """Structured training step: one random position in every voxel of a
-    128^3 grid (2,097,152 samples), over the same Gaussians and index. The
-    offsets of several iterations are drawn beforehand and stay in HBM; each
-    step takes the next set, as training draws new positions every
-    iteration."""
+class TrainStep:
+    """Structured training step (Sec. 4.2, Sec. 4.2.2, Sec. 6.1) over the
+    free parameters behind the C2 Gaussians: activations (sigmoid values
+    and weights, exp scales with the 0.02 soft norm cap), index build, one
+    random position in every voxel of a 128^3 grid (2,097,152 samples),
+    forward, L1 + false-negative losses against targets, backward, and the
+    activations' backward. The offsets and targets of several iterations
+    are drawn beforehand and stay in HBM; each step takes the next set, as
+    training draws new positions every iteration."""
     DIMS = (128, 128, 128)
     SETS = 4
+    CAP = 0.02
+    FN_EPS, FN_LAMBDA, FP_LAMBDA = 0.1, 1.0, 0.0
 
     def __init__(self, st: Step):
         import numpy as np
         import synth
         gs, torch = st.gs, st.torch
-        self.st, self.gs = st, gs
+        self.st, self.gs, self.torch = st, gs, torch
         self.n = self.DIMS[0] * self.DIMS[1] * self.DIMS[2]
         dev = "cuda:0"
-        self.offsets = [torch.from_numpy(synth.jitter_offsets(st.w.cfg, self.n, it)).to(dev)
-                        for it in range(self.SETS)]
-        self.queries = [gs.Query.jitter(self.DIMS, u) for u in self.offsets]
-        gv, gi = synth.cotangents(st.w, self.n, batch_index=1)
         t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
-        self.gv, self.gi = t(gv), t(gi)
+        ls, vl, wl = synth.raw_params(st.w)
+        self.raw = gs.RawParams(t(ls), t(vl), t(wl))
+        ng = st.g_host.n
+        self.gauss = gs.Gaussians(st.dg.mean, torch.empty(ng, 3, device=dev), st.dg.rot,
+                                  torch.empty(ng, device=dev), torch.empty(ng, device=dev))
+        self.offsets = [t(synth.jitter_offsets(st.w.cfg, self.n, it)) for it in range(self.SETS)]
+        self.targets = [t(synth.targets(st.w.cfg, self.n, it)) for it in range(self.SETS)]
+        self.queries = [gs.Query.jitter(self.DIMS, u) for u in self.offsets]
         self.plan = gs.alloc_plan(self.queries[0], st.grid, dev)
-        self.val = torch.empty(self.n, dtype=torch.float32, device=dev)
-        self.inf = torch.empty(self.n, dtype=torch.float32, device=dev)
-        self.grads = gs.Grads.empty(st.g_host.n, dev)
+        self.val = torch.empty(self.n, device=dev)
+        self.inf = torch.empty(self.n, device=dev)
+        self.gv = torch.empty(self.n, device=dev)
+        self.gi = torch.empty(self.n, device=dev)
+        self.terms = gs.alloc_loss_terms(dev)
+        self.loss_work = gs.alloc_loss_work(self.n, dev)
+        self.grads = gs.Grads.empty(ng, dev)
+        self.raw_grads = gs.RawParams(torch.empty(ng, 3, device=dev), torch.empty(ng, device=dev),
+                                      torch.empty(ng, device=dev))
+        self.activate()
+        gs.gs_build_index(self.gauss, st.grid, TAU, st.index)
         self.work = gs.alloc_backward_work(st.index, self.queries[0], dev)
         self.it = 0
         torch.cuda.synchronize()
 
-    def forward(self):
-        self.gs.gs_sample(self.st.dg, self.st.index, self.queries[self.it % self.SETS], self.val, self.inf, self.plan)
-
-    def backward(self):
-        self.gs.gs_sample_backward(self.st.dg, self.st.index, self.queries[self.it % self.SETS], self.plan, self.val,
-                                   self.inf, self.gv, self.gi, self.grads, self.work)
+    def activate(self):
+        self.gs.gs_activate(self.raw, self.CAP, self.gauss.scale, self.gauss.value, self.gauss.weight)
 
     def step(self):
-        self.st.build()
-        self.forward()
-        self.backward()
+        gs, st = self.gs, self.st
+        q = self.queries[self.it % self.SETS]
+        self.activate()
+        gs.gs_build_index(self.gauss, st.grid, TAU, st.index)
+        gs.gs_sample(self.gauss, st.index, q, self.val, self.inf, self.plan)
+        gs.gs_loss(self.val, self.inf, self.targets[self.it % self.SETS], None, TAU, self.FN_EPS, self.FN_LAMBDA,
+                   self.FP_LAMBDA, self.gv, self.gi, self.terms, self.loss_work)
+        gs.gs_sample_backward(self.gauss, st.index, q, self.plan, self.val, self.inf, self.gv, self.gi, self.grads,
+                              self.work)
+        gs.gs_activate_backward(self.raw, self.CAP, self.grads, self.raw_grads)
         self.it += 1
 
 
@@ -255,16 +275,29 @@ def main():
     t_fwd = timed(st.forward, a.steps, sync)
     t_bwd = timed(st.backward, a.steps, sync)
     t_build = timed(st.build, a.steps, sync)
-    jit = None
-    if not a.no_jitter:
-        js = JitterStep(st)
+    train = None
+    if not a.no_train:
+        ts = TrainStep(st)
         for _ in range(a.warmup):
-            js.step()
-        t_js = timed(js.step, a.steps, sync)
-        jit = {"workload": "128^3 grid, one random position per voxel (offsets redrawn each step, "
-                           f"{JitterStep.SETS} sets resident in HBM), same Gaussians; step = build + forward + backward",
-               "samples_per_step": js.n, "ms_per_step": t_js * 1e3, "fwd_bwd_samples_per_s": js.n / t_js}
-        del js
+            ts.step()
+        sync()
+        gs.profile_select(None)
+        gs.profile_reset()
+        gs.profile_enable(True)
+        for _ in range(a.steps):
+            ts.step()
+        sync()
+        gs.profile_enable(False)
+        tk = {k: round(ms / a.steps * 1e3, 2) for k, (c, ms) in gs.profile_read().items()}
+        t_ts = timed(ts.step, a.steps, sync)
+        terms = gs.read_loss_terms(ts.terms)
+        train = {"workload": "structured training step: free parameters of the 262144 Gaussians -> activations "
+                             "(soft norm cap 0.02) -> index -> 128^3 jittered samples (one random position per "
+                             f"voxel, offsets and targets redrawn each step from {TrainStep.SETS} sets resident in "
+                             "HBM) -> forward -> L1 + false-negative losses -> backward -> activation backward",
+                 "samples_per_step": ts.n, "ms_per_step": t_ts * 1e3, "fwd_bwd_samples_per_s": ts.n / t_ts,
+                 "loss": {k: terms[k] for k in ("l1", "fn", "total", "n_fn")}, "kernels_us": tk}
+        del ts
 
     if a.breakdown:
         for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
@@ -298,7 +331,7 @@ def main():
         "ms_build": t_build * 1e3, "ms_fwd": t_fwd * 1e3, "ms_bwd": t_bwd * 1e3,
         "gauss_point_evals_per_s": (contrib * st.n / t_fwd) if contrib else None,
         "kernels": {k: round(v["ms_per_step"] * 1e3, 2) for k, v in kernels.items()},
-        "jittered_training_step": jit,
+        "training_step": train,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
