@@ -60,6 +60,9 @@ def lib():
         L.orc_activate_backward.argtypes = [c_i64, vp, vp, vp, ctypes.c_double, vp, vp, vp, vp, vp, vp]
         L.orc_loss.restype = c_int
         L.orc_loss.argtypes = [c_i64, vp, vp, vp, vp, c_float, c_float, c_float, c_float, vp, vp, vp, vp]
+        L.orc_densify.restype = c_i64
+        L.orc_densify.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, vp, vp, vp, vp, vp, c_float,
+                                  c_float, c_float, c_i64, c_i64, vp, vp, vp, vp, vp, vp]
         L.orc_point_order.restype = c_int
         L.orc_point_order.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp]
         _LIB = L
@@ -416,3 +419,42 @@ def loss(value, influence, target, defined=None, tau=0.01, eps=0.1, lambda_fn=1.
                         float(lambda_fp), _p(terms), _p(counts), _p(gv), _p(gi))
     assert rc == 0, rc
     return LossResult(terms, counts, gv, gi)
+
+
+class DensifyResult:
+    def __init__(self, n_out, kept, mean, log_scale, rot, value_logit, weight_logit, source):
+        self.n = n_out
+        self.kept = kept
+        self.mean, self.log_scale, self.rot = mean, log_scale, rot
+        self.value_logit, self.weight_logit, self.source = value_logit, weight_logit, source
+
+
+def densify(mean, log_scale, rot, value_logit, weight_logit, weight, positions, valid, value, influence, target,
+            defined=None, tau2=0.005, tau=0.01, new_log_scale=-5.0, new_weight_logit=-4.59511985,
+            max_new=0, capacity=None):
+    """Weight pruning and sample-error densification (Sec. 4.2.1, false
+    negatives first, Sec. 4.2.2) of a set of free Gaussian parameters
+    (float32). positions [nq][3] and valid [nq] give each sample's position
+    (as the sampler computes it) and whether it has one. Returns a
+    DensifyResult, or raises ValueError when the kept Gaussians alone exceed
+    the capacity."""
+    mean, log_scale, rot = _f32(mean).reshape(-1, 3), _f32(log_scale).reshape(-1, 3), _f32(rot).reshape(-1, 4)
+    vl, wl, w = _f32(value_logit).reshape(-1), _f32(weight_logit).reshape(-1), _f32(weight).reshape(-1)
+    n_in = mean.shape[0]
+    pos = _f32(positions).reshape(-1, 3)
+    nq = pos.shape[0]
+    ok = np.ascontiguousarray(valid, dtype=np.uint8).reshape(-1)
+    v, i, y = _f32(value).reshape(-1), _f32(influence).reshape(-1), _f32(target).reshape(-1)
+    d = None if defined is None else np.ascontiguousarray(defined, dtype=np.uint8).reshape(-1)
+    cap = n_in + nq if capacity is None else int(capacity)
+    om, ols, orot = np.zeros((cap, 3), np.float32), np.zeros((cap, 3), np.float32), np.zeros((cap, 4), np.float32)
+    ovl, owl = np.zeros(cap, np.float32), np.zeros(cap, np.float32)
+    src = np.zeros(cap, np.int32)
+    r = lib().orc_densify(n_in, _p(mean), _p(log_scale), _p(rot), _p(vl), _p(wl), _p(w), float(tau2), nq, _p(pos),
+                          _p(ok), _p(v), _p(i), _p(y), _p(d), float(tau), float(new_log_scale),
+                          float(new_weight_logit), int(max_new), cap, _p(om), _p(ols), _p(orot), _p(ovl), _p(owl),
+                          _p(src))
+    if r < 0:
+        raise ValueError(f"{-1 - r} kept Gaussians exceed the capacity {cap}")
+    kept = int(np.count_nonzero(w >= np.float32(tau2)))
+    return DensifyResult(int(r), kept, om[:r], ols[:r], orot[:r], ovl[:r], owl[:r], src[:r])

@@ -1,8 +1,9 @@
 /*
  * CPU oracle for the steps on either side of the sampling path in training:
- * the parameter activations and their derivatives (Sec. 4.2), and the
+ * the parameter activations and their derivatives (Sec. 4.2), the
  * reconstruction, false-negative and false-positive losses (Sec. 4.2, Eq. 4,
- * Eq. 5) with the cotangents they hand to the sampler's backward.
+ * Eq. 5) with the cotangents they hand to the sampler's backward, and
+ * sample-error densification with weight pruning (Sec. 4.2.1).
  *
  * TEST INFRASTRUCTURE ONLY. Nothing in the product library links, loads or
  * calls this file; only the tests, the smoke check and the benchmark's CPU
@@ -37,6 +38,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #define ORC_OK 0
 #define ORC_ERR_ARG 1
@@ -168,4 +170,97 @@ int orc_loss(int64_t n, const float *value, const float *influence, const float 
         grad_influence[i] = gi;
     }
     return ORC_OK;
+}
+
+/*
+ * Sample-error densification and weight pruning (Sec. 4.2.1, with the false
+ * negatives of Sec. 4.2.2 taking priority).
+ *   Pruning: a Gaussian is kept when its (activated, float32) weight is at
+ *   least tau2; the kept ones stay in their order.
+ *   Ranking: a sample is eligible when it lies in the volume (defined flag,
+ *   or every sample when the flags are absent) and has a position (valid).
+ *   It is a false negative when the model is undefined there (I <= tau).
+ *   Eligible samples are ranked false negatives first, then by the float32
+ *   error |Phi - y| from largest to smallest, ties by increasing index.
+ *   Spawning: k = min(max_new, capacity - kept, eligible) new Gaussians, one
+ *   at the position of each of the first k ranked samples, set up as at
+ *   initialisation: isotropic log-scale new_log_scale, identity rotation,
+ *   the sample's target as value (logit of y clamped to [2^-20, 1 - 2^-20]),
+ *   weight logit new_weight_logit.
+ * Output: the kept Gaussians' parameters in order, then the new ones in rank
+ * order; source[j] = the input index of output j, or -1 - s for a new
+ * Gaussian made at sample s. Returns the output count, or -1 - kept when
+ * the kept Gaussians alone exceed the capacity (nothing written then).
+ */
+typedef struct {
+    int fn;
+    float err;
+    int64_t idx;
+} ranked;
+
+static int rank_cmp(const void *pa, const void *pb)
+{
+    const ranked *a = (const ranked *)pa, *b = (const ranked *)pb;
+    if (a->fn != b->fn) return a->fn > b->fn ? -1 : 1;
+    if (a->err != b->err) return a->err > b->err ? -1 : 1;
+    return a->idx < b->idx ? -1 : (a->idx > b->idx ? 1 : 0);
+}
+
+int64_t orc_densify(int64_t n_in, const float *mean, const float *log_scale, const float *rot,
+                    const float *value_logit, const float *weight_logit, const float *weight, float tau2,
+                    int64_t nq, const float *pos, const uint8_t *valid, const float *value, const float *influence,
+                    const float *target, const uint8_t *defined, float tau, float new_log_scale,
+                    float new_weight_logit, int64_t max_new, int64_t capacity, float *o_mean, float *o_log_scale,
+                    float *o_rot, float *o_value_logit, float *o_weight_logit, int32_t *source)
+{
+    int64_t kept = 0;
+    for (int64_t i = 0; i < n_in; ++i)
+        if (weight[i] >= tau2) ++kept;
+    if (kept > capacity) return -1 - kept;
+    ranked *r = (ranked *)malloc(sizeof(ranked) * (size_t)(nq > 0 ? nq : 1));
+    if (!r) return -1 - kept;
+    int64_t ne = 0;
+    for (int64_t s = 0; s < nq; ++s) {
+        const int in_d = defined ? defined[s] != 0 : 1;
+        if (!in_d || !valid[s]) continue;
+        r[ne].fn = !(influence[s] > tau);
+        r[ne].err = fabsf(value[s] - target[s]);
+        r[ne].idx = s;
+        ++ne;
+    }
+    qsort(r, (size_t)ne, sizeof(ranked), rank_cmp);
+    int64_t k = max_new;
+    if (capacity - kept < k) k = capacity - kept;
+    if (ne < k) k = ne;
+    if (k < 0) k = 0;
+    int64_t j = 0;
+    for (int64_t i = 0; i < n_in; ++i) {
+        if (!(weight[i] >= tau2)) continue;
+        for (int a = 0; a < 3; ++a) {
+            o_mean[3 * j + a] = mean[3 * i + a];
+            o_log_scale[3 * j + a] = log_scale[3 * i + a];
+        }
+        for (int a = 0; a < 4; ++a) o_rot[4 * j + a] = rot[4 * i + a];
+        o_value_logit[j] = value_logit[i];
+        o_weight_logit[j] = weight_logit[i];
+        source[j] = (int32_t)i;
+        ++j;
+    }
+    const double ylo = 1.0 / 1048576.0, yhi = 1.0 - 1.0 / 1048576.0;
+    for (int64_t t = 0; t < k; ++t, ++j) {
+        const int64_t s = r[t].idx;
+        for (int a = 0; a < 3; ++a) {
+            o_mean[3 * j + a] = pos[3 * s + a];
+            o_log_scale[3 * j + a] = new_log_scale;
+        }
+        o_rot[4 * j] = 1.0f;
+        o_rot[4 * j + 1] = o_rot[4 * j + 2] = o_rot[4 * j + 3] = 0.0f;
+        double y = (double)target[s];
+        y = y < ylo ? ylo : (y > yhi ? yhi : y);
+        o_value_logit[j] = (float)log(y / (1.0 - y));
+        o_weight_logit[j] = new_weight_logit;
+        source[j] = (int32_t)(-1 - s);
+    }
+    free(r);
+    return j;
 }
