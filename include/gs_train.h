@@ -1,8 +1,9 @@
 /*
  * gs_train.h - the steps on either side of the sampling path in training
- * (paper Sec. 4.2, Sec. 4.2.2, Sec. 5.2): parameter activations and their
- * derivatives, and the reconstruction, false-negative and false-positive
- * losses with the cotangents they hand to gs_sample_backward. Same library
+ * (paper Sec. 4.2, Sec. 4.2.1, Sec. 4.2.2, Sec. 5.2): parameter activations
+ * and their derivatives, the reconstruction, false-negative and
+ * false-positive losses with the cotangents they hand to
+ * gs_sample_backward, and weight pruning with sample-error densification. Same library
  * and conventions as gs.h: device pointers the caller owns, work enqueued
  * on the caller's stream, gs_status codes with gs_last_error(), no device
  * memory allocated by the library.
@@ -101,6 +102,64 @@ gs_status gs_loss(int64_t n, const float *value, const float *influence, const f
                   const uint8_t *defined, const gs_loss_params *params, float *grad_value,
                   float *grad_influence, gs_loss_terms *terms, void *work, size_t work_bytes,
                   hipStream_t stream);
+
+/* Free parameters of a set of Gaussians, before the activations: means
+ * [n][3], log-scales [n][3], quaternions [n][4] (w, x, y, z), value logits
+ * [n] and weight logits [n]. */
+typedef struct gs_params {
+    float *mean;
+    float *log_scale;
+    float *rot;
+    float *value_logit;
+    float *weight_logit;
+} gs_params;
+
+/* Densification and pruning settings (Sec. 4.2.1). */
+typedef struct gs_densify_params {
+    float prune_weight;     /* tau_2: a Gaussian whose activated weight is below it is removed (0.005) */
+    float tau;              /* the sampler's cutoff: the model is undefined where I <= tau */
+    float new_log_scale;    /* log of the isotropic standard deviation of a new Gaussian */
+    float new_weight_logit; /* weight logit of a new Gaussian (logit(0.01) for the initial weight 0.01) */
+    int64_t max_new;        /* k: new Gaussians at most (the paper uses 1/5 of the final count) */
+} gs_densify_params;
+
+/* Bytes of densification workspace for n_in Gaussians and a query (-1 cast
+ * to size_t for a malformed query or count). */
+size_t gs_densify_work_bytes(int64_t n_in, const gs_query *query);
+
+/*
+ * Weight pruning and sample-error densification (Sec. 4.2.1, with false
+ * negatives first, Sec. 4.2.2), run after a forward pass and gs_loss.
+ *   Pruning: Gaussian i of the input set is kept when weight[i] (its
+ *   activated weight, float32, as gs_activate wrote it) >= prune_weight;
+ *   the kept Gaussians keep their order.
+ *   Ranking: sample t of the query (the outputs value, influence of
+ *   gs_sample, the targets, and the volume flags as for gs_loss, NULL: all
+ *   in the volume) is eligible when it lies in the volume and has a
+ *   position (a voxel id past the grid has none). Eligible samples are
+ *   ranked false negatives (I <= tau) first, then by the float32 error
+ *   |value - target| from largest to smallest, ties by increasing t.
+ *   Spawning: k = min(max_new, capacity - kept, eligible) new Gaussians at
+ *   the positions (as gs_sample computes them, over the box of domain) of
+ *   the first k ranked samples, set up as at initialisation: log-scale
+ *   new_log_scale on every axis, rotation (1, 0, 0, 0), value logit
+ *   log(y / (1 - y)) of the sample's target clamped to [2^-20, 1 - 2^-20]
+ *   (float64, rounded once), weight logit new_weight_logit.
+ * Output (out, arrays of capacity Gaussians, not overlapping in): the kept
+ * Gaussians, then the new ones in rank order; source[j] = the input index
+ * of output j, or -1 - t for a new Gaussian made at sample t, so that other
+ * per-Gaussian state (optimiser moments) can be carried over with the same
+ * map. Waits on the stream once and sets *n_out (host) to the output count.
+ * When the kept Gaussians alone exceed the capacity, returns
+ * GS_ERR_CAPACITY with *n_out = the kept count and out unspecified (nothing
+ * is written past the capacity). Rebuild the index (gs_build_index) on the
+ * new set before sampling it. 0 <= n_in, capacity < 2^31.
+ */
+gs_status gs_densify(const gs_params *in, int64_t n_in, const float *weight, const gs_grid *domain,
+                     const gs_query *query, const float *value, const float *influence, const float *target,
+                     const uint8_t *defined, const gs_densify_params *params, const gs_params *out,
+                     int64_t capacity, int32_t *source, int64_t *n_out, void *work, size_t work_bytes,
+                     hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -17,6 +17,11 @@ namespace gs {
 hipError_t launch_loss(int64_t n, const float *value, const float *influence, const float *target,
                        const uint8_t *defined, float tau, float eps, float lambda_fn, float lambda_fp,
                        float *grad_value, float *grad_influence, gs_loss_terms *terms, void *work, hipStream_t s);
+hipError_t launch_densify(const gs_params &in, int64_t n_in, const float *weight, float tau2, const QueryParams &q,
+                          const GridParams &g, const float *value, const float *influence, const float *target,
+                          const uint8_t *defined, float tau, float new_log_scale, float new_weight_logit,
+                          int64_t max_new, int64_t capacity, const gs_params &out, int32_t *source, void *work,
+                          long long **n_out_dev, hipStream_t s);
 }
 
 using namespace gs;
@@ -707,6 +712,63 @@ gs_status gs_loss(int64_t n, const float *value, const float *influence, const f
     GS_TRY(launch_loss(n, value, influence, target, defined, p.tau, p.fn_eps, p.fn_lambda, p.fp_lambda, grad_value,
                        grad_influence, terms, work, stream),
            "gs_loss");
+    return GS_OK;
+}
+
+size_t gs_densify_work_bytes(int64_t n_in, const gs_query *query) {
+    if (n_in < 0 || n_in >= ((int64_t)1 << 31)) return (size_t)-1;
+    std::string why;
+    if (!query_valid(query, &why)) return (size_t)-1;
+    return densify_work_bytes(n_in, query_count(query));
+}
+
+gs_status gs_densify(const gs_params *in, int64_t n_in, const float *weight, const gs_grid *domain,
+                     const gs_query *query, const float *value, const float *influence, const float *target,
+                     const uint8_t *defined, const gs_densify_params *params, const gs_params *out,
+                     int64_t capacity, int32_t *source, int64_t *n_out, void *work, size_t work_bytes,
+                     hipStream_t stream) {
+    if (!in || !out || !params || !n_out || !domain)
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: null argument");
+    *n_out = 0;
+    if (n_in < 0 || n_in >= ((int64_t)1 << 31) || capacity < 0 || capacity >= ((int64_t)1 << 31))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: counts out of range");
+    std::string why;
+    if (!grid_valid(domain, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: %s", why.c_str());
+    if (!query_valid(query, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: %s", why.c_str());
+    const int64_t nq = query_count(query);
+    if (n_in > 0 && (!weight || !in->mean || !in->log_scale || !in->rot || !in->value_logit || !in->weight_logit))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: input arrays are null");
+    if (capacity > 0 &&
+        (!source || !out->mean || !out->log_scale || !out->rot || !out->value_logit || !out->weight_logit))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: output arrays are null");
+    if (nq > 0 && (!value || !influence || !target))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: forward outputs or targets are null");
+    const gs_densify_params p = *params;
+    if (!(p.tau > 0.0f && p.tau < 1.0f)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: tau must lie in (0, 1)");
+    if (std::isnan(p.prune_weight) || !std::isfinite(p.new_log_scale) || !std::isfinite(p.new_weight_logit) ||
+        p.max_new < 0)
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_densify: invalid settings");
+    const size_t need = densify_work_bytes(n_in, nq);
+    if (!work || work_bytes < need || !aligned(work))
+        return fail(GS_ERR_WORKSPACE, "gs_densify: workspace needs %zu bytes, 256-byte aligned (got %zu)", need,
+                    work_bytes);
+    PinnedCount *pc = pinned_count();
+    if (!pc) return fail(GS_ERR_HIP, "gs_densify: could not allocate the pinned read-back word");
+    const GridParams gp = grid_params(domain);
+    const QueryParams qp = query_params(query, domain);
+    long long *n_out_dev = nullptr;
+    GS_TRY(launch_densify(*in, n_in, weight, p.prune_weight, qp, gp, value, influence, target, defined, p.tau,
+                          p.new_log_scale, p.new_weight_logit, p.max_new, capacity, *out, source, work, &n_out_dev,
+                          stream),
+           "gs_densify");
+    GS_TRY(hipMemcpyAsync(pc->value, n_out_dev, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
+           "gs_densify: count read-back");
+    GS_TRY(hipEventRecord(pc->copied, stream), "gs_densify: event");
+    GS_TRY(hipEventSynchronize(pc->copied), "gs_densify: wait");
+    *n_out = (int64_t)*pc->value;
+    if (*n_out > capacity)
+        return fail(GS_ERR_CAPACITY, "gs_densify: %lld kept Gaussians exceed the capacity %lld", (long long)*n_out,
+                    (long long)capacity);
     return GS_OK;
 }
 

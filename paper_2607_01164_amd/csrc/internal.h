@@ -295,6 +295,44 @@ struct QueryParams {
     const float *points;
     float vsz[3];        // (hi - lo) / dims, float32
 };
+
+__device__ __forceinline__ float voxel_center(int32_t i, float lo, float vs) { return lo + ((float)i + 0.5f) * vs; }
+
+// Position of query pid, each operation rounded in float32: the centre of
+// voxel pid (GRID) or of the listed voxel (VOXELS), the position at the
+// caller's offsets in the listed voxel, or in voxel pid without a list
+// (JITTER), or the given point (POINTS). valid is false for a voxel id past
+// the grid.
+__device__ __forceinline__ void query_position(const QueryParams &q, const GridParams &g, uint32_t pid, float &px,
+                                               float &py, float &pz, bool &valid) {
+    valid = true;
+    if (q.kind != 2) {
+        // voxel queries: centred (0, 1) or at the caller's offsets (3)
+        const uint32_t id = (q.kind == 0 || (q.kind == 3 && !q.voxel_ids)) ? pid : q.voxel_ids[pid];
+        const uint32_t nx = (uint32_t)q.dims[0], ny = (uint32_t)q.dims[1], nz = (uint32_t)q.dims[2];
+        const uint64_t nvox = (uint64_t)nx * ny * nz;
+        if ((uint64_t)id >= nvox) {
+            valid = false;
+            px = py = pz = 0.0f;
+            return;
+        }
+        const uint32_t x = id % nx, t = id / nx, y = t % ny, z = t / ny;
+        if (q.kind != 3) {
+            px = voxel_center((int32_t)x, g.lo[0], q.vsz[0]);
+            py = voxel_center((int32_t)y, g.lo[1], q.vsz[1]);
+            pz = voxel_center((int32_t)z, g.lo[2], q.vsz[2]);
+        } else {
+            const float *u = q.points + 3 * (uint64_t)pid;
+            px = g.lo[0] + ((float)x + u[0]) * q.vsz[0];
+            py = g.lo[1] + ((float)y + u[1]) * q.vsz[1];
+            pz = g.lo[2] + ((float)z + u[2]) * q.vsz[2];
+        }
+    } else {
+        px = q.points[3 * (uint64_t)pid];
+        py = q.points[3 * (uint64_t)pid + 1];
+        pz = q.points[3 * (uint64_t)pid + 2];
+    }
+}
 // Cell key of every query (ncells outside the domain), identity ids and
 // the first sort digit's tile counts.
 hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids,
@@ -341,6 +379,9 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
                            float *d_mean, float *d_scale, float *d_rot, float *d_value, float *d_weight,
                            hipStream_t s);
+
+// Densification (densify.hip).
+size_t densify_work_bytes(int64_t n_in, int64_t nq);
 
 // Training epilogue (train.hip). cap <= 0 disables the soft cap.
 size_t loss_work_bytes(int64_t n);

@@ -59,7 +59,6 @@ __device__ __forceinline__ void walk_uniform(const Record *rec, const uint32_t *
     }
 }
 
-__device__ __forceinline__ float voxel_center(int32_t i, float lo, float vs) { return lo + ((float)i + 0.5f) * vs; }
 
 __global__ __launch_bounds__(kBlock) void k_sample_grid(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                         const uint32_t *__restrict__ gids,
@@ -94,37 +93,6 @@ __global__ __launch_bounds__(kBlock) void k_sample_grid(QueryParams q, GridParam
         const bool def = I > tau;
         out_v[idx] = def ? V / I : 0.0f;
         out_i[idx] = def ? I : 0.0f;
-    }
-}
-
-__device__ __forceinline__ void query_position(const QueryParams &q, const GridParams &g, uint32_t pid, float &px,
-                                               float &py, float &pz, bool &valid) {
-    valid = true;
-    if (q.kind == 1 || q.kind == 3) {
-        // voxel queries, centred (1) or at the caller's offsets (3)
-        const uint32_t id = (q.kind == 3 && !q.voxel_ids) ? pid : q.voxel_ids[pid];
-        const uint32_t nx = (uint32_t)q.dims[0], ny = (uint32_t)q.dims[1], nz = (uint32_t)q.dims[2];
-        const uint64_t nvox = (uint64_t)nx * ny * nz;
-        if ((uint64_t)id >= nvox) {
-            valid = false;
-            px = py = pz = 0.0f;
-            return;
-        }
-        const uint32_t x = id % nx, t = id / nx, y = t % ny, z = t / ny;
-        if (q.kind == 1) {
-            px = voxel_center((int32_t)x, g.lo[0], q.vsz[0]);
-            py = voxel_center((int32_t)y, g.lo[1], q.vsz[1]);
-            pz = voxel_center((int32_t)z, g.lo[2], q.vsz[2]);
-        } else {
-            const float *u = q.points + 3 * (uint64_t)pid;
-            px = g.lo[0] + ((float)x + u[0]) * q.vsz[0];
-            py = g.lo[1] + ((float)y + u[1]) * q.vsz[1];
-            pz = g.lo[2] + ((float)z + u[2]) * q.vsz[2];
-        }
-    } else {
-        px = q.points[3 * (uint64_t)pid];
-        py = q.points[3 * (uint64_t)pid + 1];
-        pz = q.points[3 * (uint64_t)pid + 2];
     }
 }
 

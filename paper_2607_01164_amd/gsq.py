@@ -32,7 +32,7 @@ GS_QUERY_JITTER = 3
 EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_bytes", "gs_sample",
             "gs_backward_work_bytes", "gs_sample_backward", "gs_last_error", "gs_version", "gs_profile_enable",
             "gs_profile_select", "gs_profile_reset", "gs_profile_read", "gs_activate", "gs_activate_backward",
-            "gs_loss_work_bytes", "gs_loss")
+            "gs_loss_work_bytes", "gs_loss", "gs_densify_work_bytes", "gs_densify")
 
 
 class GsLibraryMissing(RuntimeError):
@@ -68,6 +68,16 @@ class GsQuery(ctypes.Structure):
 class GsLossParams(ctypes.Structure):
     _fields_ = [("tau", ctypes.c_float), ("fn_eps", ctypes.c_float), ("fn_lambda", ctypes.c_float),
                 ("fp_lambda", ctypes.c_float)]
+
+
+class GsParams(ctypes.Structure):
+    _fields_ = [("mean", ctypes.c_void_p), ("log_scale", ctypes.c_void_p), ("rot", ctypes.c_void_p),
+                ("value_logit", ctypes.c_void_p), ("weight_logit", ctypes.c_void_p)]
+
+
+class GsDensifyParams(ctypes.Structure):
+    _fields_ = [("prune_weight", ctypes.c_float), ("tau", ctypes.c_float), ("new_log_scale", ctypes.c_float),
+                ("new_weight_logit", ctypes.c_float), ("max_new", ctypes.c_int64)]
 
 
 LOSS_TERMS_BYTES = 64  # gs_loss_terms: four float64 values, then four int64 counts
@@ -121,6 +131,11 @@ def load_library():
     L.gs_loss_work_bytes.argtypes = [i64]
     L.gs_loss.restype = ctypes.c_int
     L.gs_loss.argtypes = [i64, vp, vp, vp, vp, P(GsLossParams), vp, vp, vp, vp, sz, vp]
+    L.gs_densify_work_bytes.restype = sz
+    L.gs_densify_work_bytes.argtypes = [i64, P(GsQuery)]
+    L.gs_densify.restype = ctypes.c_int
+    L.gs_densify.argtypes = [P(GsParams), i64, vp, P(GsGrid), P(GsQuery), vp, vp, vp, vp, P(GsDensifyParams),
+                             P(GsParams), i64, vp, P(i64), vp, sz, vp]
     _LIB = L
     return L
 
@@ -472,6 +487,90 @@ def gs_loss(value: torch.Tensor, influence: torch.Tensor, target: torch.Tensor, 
                                 ctypes.byref(p), grad_value.data_ptr(), grad_influence.data_ptr(), terms.data_ptr(),
                                 work.data_ptr(), work.numel() * work.element_size(), _stream(stream))
     _check(st)
+
+
+@dataclass
+class ParamSet:
+    """Free parameters of up to `rows` Gaussians on the device: mean [rows,3],
+    log_scale [rows,3], rot [rows,4], value_logit [rows], weight_logit
+    [rows]."""
+    mean: torch.Tensor
+    log_scale: torch.Tensor
+    rot: torch.Tensor
+    value_logit: torch.Tensor
+    weight_logit: torch.Tensor
+
+    @staticmethod
+    def empty(rows: int, device) -> "ParamSet":
+        f = dict(dtype=torch.float32, device=device)
+        return ParamSet(torch.empty(rows, 3, **f), torch.empty(rows, 3, **f), torch.empty(rows, 4, **f),
+                        torch.empty(rows, **f), torch.empty(rows, **f))
+
+    @property
+    def rows(self) -> int:
+        return int(self.mean.shape[0])
+
+    def c(self) -> GsParams:
+        r = self.rows
+        for t, nm, tail in ((self.mean, "mean", (3,)), (self.log_scale, "log_scale", (3,)), (self.rot, "rot", (4,)),
+                            (self.value_logit, "value_logit", ()), (self.weight_logit, "weight_logit", ())):
+            _dev_f32(t, nm, tail)
+            if t.shape[0] != r:
+                raise ValueError("parameter arrays disagree on their rows")
+        return GsParams(self.mean.data_ptr(), self.log_scale.data_ptr(), self.rot.data_ptr(),
+                        self.value_logit.data_ptr(), self.weight_logit.data_ptr())
+
+    def raw(self, n: Optional[int] = None) -> RawParams:
+        n = self.rows if n is None else n
+        return RawParams(self.log_scale[:n], self.value_logit[:n], self.weight_logit[:n])
+
+
+def densify_work_bytes(n_in: int, query: Query) -> int:
+    q = query.c()
+    b = load_library().gs_densify_work_bytes(int(n_in), ctypes.byref(q))
+    if b == ctypes.c_size_t(-1).value:
+        raise GsError(GS_ERR_INVALID_ARGUMENT, "malformed query or count")
+    return int(b)
+
+
+def alloc_densify_work(n_in: int, query: Query, device) -> torch.Tensor:
+    return _alloc_bytes(densify_work_bytes(n_in, query), device)
+
+
+def gs_densify(params_in: ParamSet, n_in: int, weight: torch.Tensor, domain: GsGrid, query: Query,
+               value: torch.Tensor, influence: torch.Tensor, target: torch.Tensor, defined: Optional[torch.Tensor],
+               prune_weight: float, tau: float, new_log_scale: float, new_weight_logit: float, max_new: int,
+               params_out: ParamSet, source: torch.Tensor, work: torch.Tensor, stream=None) -> int:
+    """Weight pruning and sample-error densification (Sec. 4.2.1): writes the
+    kept and new Gaussians into params_out (capacity = its rows) and the
+    source map, and returns the new count (waits for it)."""
+    nq = query.size()
+    q = query.c()
+    if n_in > params_in.rows:
+        raise ValueError("n_in exceeds the input rows")
+    _dev_f32(weight, "weight")
+    if weight.numel() < n_in:
+        raise ValueError("weight needs n_in elements")
+    for t, nm in ((value, "value"), (influence, "influence"), (target, "target")):
+        _dev_f32(t, nm)
+        if t.numel() < nq:
+            raise ValueError(f"{nm} needs {nq} elements")
+    if defined is not None and (not defined.is_cuda or defined.dtype != torch.uint8 or defined.numel() < nq):
+        raise ValueError("defined must be a uint8 device tensor of the query's size")
+    cap = params_out.rows
+    if not source.is_cuda or source.dtype != torch.int32 or source.numel() < cap:
+        raise ValueError("source must be an int32 device tensor with a slot per output row")
+    p = GsDensifyParams(float(prune_weight), float(tau), float(new_log_scale), float(new_weight_logit), int(max_new))
+    n_out = ctypes.c_int64(0)
+    st = load_library().gs_densify(ctypes.byref(params_in.c()), int(n_in), weight.data_ptr(), ctypes.byref(domain),
+                                   ctypes.byref(q), value.data_ptr(), influence.data_ptr(), target.data_ptr(),
+                                   _ptr(defined), ctypes.byref(p), ctypes.byref(params_out.c()), cap,
+                                   source.data_ptr(), ctypes.byref(n_out), work.data_ptr(),
+                                   work.numel() * work.element_size(), _stream(stream))
+    if st == GS_ERR_CAPACITY:
+        raise GsError(st, load_library().gs_last_error().decode(errors="replace") + f" (kept {n_out.value})")
+    _check(st)
+    return int(n_out.value)
 
 
 def profile_enable(on: bool = True) -> None:

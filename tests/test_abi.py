@@ -264,3 +264,42 @@ def test_training_epilogue_validation():
     assert args(P(ok), work=None) == gs.GS_ERR_WORKSPACE
     assert L.gs_loss(-1, fake, fake, fake, None, P(ok), fake, fake, fake, fake, need, None) == \
         gs.GS_ERR_INVALID_ARGUMENT
+
+
+def test_densify_validation():
+    """gs_densify rejects malformed arguments before any device work."""
+    L = gs.load_library()
+    P = ctypes.byref
+    fake = 1 << 20
+    prm = gsq.GsParams(fake, fake, fake, fake, fake)
+    g = grid()
+    q = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(16, 16, 16), 0, None, None)
+    ok = gsq.GsDensifyParams(0.005, 0.01, -5.0, -4.6, 100)
+    need = L.gs_densify_work_bytes(1000, P(q))
+    assert need != SIZE_ERR and need % 256 == 0 and need > 16 ** 3 * 16
+    assert L.gs_densify_work_bytes(-1, P(q)) == SIZE_ERR
+    bad_q = gsq.GsQuery(gs.GS_QUERY_VOXELS, (ctypes.c_int32 * 3)(16, 16, 16), 10, None, None)
+    assert L.gs_densify_work_bytes(10, P(bad_q)) == SIZE_ERR
+    n_out = ctypes.c_int64(-7)
+
+    def call(n_in=1000, prm_in=prm, dp=ok, cap=2000, out=prm, work=fake, wb=need, qq=q, src=fake, dom=g):
+        return L.gs_densify(None if prm_in is None else P(prm_in), n_in, fake, None if dom is None else P(dom),
+                            P(qq), fake, fake, fake, None, None if dp is None else P(dp),
+                            None if out is None else P(out), cap, src, P(n_out), work, wb, None)
+
+    assert call(prm_in=None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(out=None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(dp=None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(dom=None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(n_in=-1) == gs.GS_ERR_INVALID_ARGUMENT and n_out.value == 0
+    assert call(cap=1 << 31) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(qq=bad_q) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(dom=grid((0, 4, 4))) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(src=None) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(out=gsq.GsParams(fake, None, fake, fake, fake)) == gs.GS_ERR_INVALID_ARGUMENT
+    for bad in (gsq.GsDensifyParams(0.005, 0.0, -5, -4.6, 1), gsq.GsDensifyParams(float("nan"), 0.01, -5, -4.6, 1),
+                gsq.GsDensifyParams(0.005, 0.01, float("inf"), -4.6, 1),
+                gsq.GsDensifyParams(0.005, 0.01, -5, float("nan"), 1), gsq.GsDensifyParams(0.005, 0.01, -5, -4.6, -1)):
+        assert call(dp=bad) == gs.GS_ERR_INVALID_ARGUMENT
+    assert call(wb=need - 1) == gs.GS_ERR_WORKSPACE
+    assert call(work=fake + 64) == gs.GS_ERR_WORKSPACE
