@@ -18,6 +18,7 @@ over the free parameters behind the same Gaussians.
 import argparse
 import hashlib
 import json
+import math
 import os
 import re
 import sys
@@ -178,6 +179,40 @@ class TrainStep:
     def activate(self):
         self.gs.gs_activate(self.raw, self.CAP, self.gauss.scale, self.gauss.value, self.gauss.weight)
 
+    def densify_bench(self, k):
+        """Pruning and densification after a step (Sec. 4.2.1), as training
+        runs it every 100 iterations: weights below 0.005 removed, the
+        2^21 samples ranked, and a fifth of the count (52,428) added at the
+        worst samples within a target count 20 % above the current one.
+        Each call includes its read-back of the new count."""
+        gs, st, torch = self.gs, self.st, self.torch
+        ng = st.g_host.n
+        kmax = ng // 5
+        cur = gs.ParamSet(st.dg.mean, self.raw.log_scale, st.dg.rot, self.raw.value_logit, self.raw.weight_logit)
+        out = gs.ParamSet.empty(ng + kmax, "cuda:0")
+        src = torch.empty(ng + kmax, dtype=torch.int32, device="cuda:0")
+        q = self.queries[(self.it - 1) % self.SETS]
+        work = gs.alloc_densify_work(ng, q, "cuda:0")
+        tgt = self.targets[(self.it - 1) % self.SETS]
+
+        def call():
+            return gs.gs_densify(cur, ng, self.gauss.weight, st.grid, q, self.val, self.inf, tgt, None, 0.005, TAU,
+                                 math.log(0.005), math.log(0.01 / 0.99), kmax, out, src, work)
+
+        n_out = call()
+        gs.profile_select(None)
+        gs.profile_reset()
+        gs.profile_enable(True)
+        for _ in range(k):
+            call()
+        torch.cuda.synchronize()
+        gs.profile_enable(False)
+        kern = {name: round(ms / k * 1e3, 2) for name, (c, ms) in gs.profile_read().items()}
+        t = timed(call, k, torch.cuda.synchronize)
+        return {"ms_per_call": t * 1e3, "n_in": ng, "n_out": n_out, "added": n_out - int(src[:n_out].ge(0).sum()),
+                "samples_ranked": self.n, "kernels_us": kern,
+                "amortised_ms_per_step": t * 1e3 / 100.0}
+
     def step(self):
         gs, st = self.gs, self.st
         q = self.queries[self.it % self.SETS]
@@ -291,12 +326,14 @@ def main():
         tk = {k: round(ms / a.steps * 1e3, 2) for k, (c, ms) in gs.profile_read().items()}
         t_ts = timed(ts.step, a.steps, sync)
         terms = gs.read_loss_terms(ts.terms)
+        dens = ts.densify_bench(a.steps)
         train = {"workload": "structured training step: free parameters of the 262144 Gaussians -> activations "
                              "(soft norm cap 0.02) -> index -> 128^3 jittered samples (one random position per "
                              f"voxel, offsets and targets redrawn each step from {TrainStep.SETS} sets resident in "
                              "HBM) -> forward -> L1 + false-negative losses -> backward -> activation backward",
                  "samples_per_step": ts.n, "ms_per_step": t_ts * 1e3, "fwd_bwd_samples_per_s": ts.n / t_ts,
-                 "loss": {k: terms[k] for k in ("l1", "fn", "total", "n_fn")}, "kernels_us": tk}
+                 "loss": {k: terms[k] for k in ("l1", "fn", "total", "n_fn")}, "kernels_us": tk,
+                 "densify": dens}
         del ts
 
     if a.breakdown:
