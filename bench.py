@@ -60,6 +60,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=16.0, help="target length of the CPU oracle sample")
     p.add_argument("--no-cpu", action="store_true")
     p.add_argument("--no-train", action="store_true", help="skip the 128^3 structured training-step line")
+    p.add_argument("--no-ab", action="store_true", help="skip the point-major / Gaussian-major comparison")
+    p.add_argument("--ab-c5", action="store_true",
+                   help="also compare the two forwards on the 10^8-point cloud (slow to generate)")
     p.add_argument("--breakdown", action="store_true", help="print the per-kernel table to stderr")
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, run a plain 256 MiB copy (counter calibration under rocprofv3)")
@@ -227,6 +230,68 @@ class TrainStep:
         self.it += 1
 
 
+class ABStep:
+    """Point-major (gs_sample) against Gaussian-major
+    (gs_sample_gaussian_major, the paper's unstructured design) forward on a
+    point-cloud workload: both whole calls, query ordering included, on the
+    same index and points resident in HBM."""
+
+    def __init__(self, name, batch_only):
+        import numpy as np
+        import torch
+
+        import paper_2607_01164_amd as gs
+        import synth
+        self.gs, self.torch = gs, torch
+        w = synth.WORKLOADS[name]
+        self.w = w
+        g = synth.make_gaussians(w)
+        pts = synth.make_points(w)
+        if batch_only:
+            pts = pts[synth.batch_permutation(w, len(pts))[: w.batch]]
+        self.n, self.n_gauss = len(pts), g.n
+        dev = "cuda:0"
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+        self.dg = gs.Gaussians(t(g.mean), t(g.scale), t(g.rot), t(g.value), t(g.weight))
+        self.pts = t(pts)
+        del pts
+        self.grid = gs.make_grid(w.index_cells)
+        self.index = gs.build_index(self.dg, self.grid, TAU)
+        self.query = gs.Query.pts(self.pts)
+        self.plan = gs.alloc_plan(self.query, self.grid, dev)
+        self.work = gs.alloc_gaussian_major_work(self.query, dev)
+        self.val = torch.empty(self.n, device=dev)
+        self.inf = torch.empty(self.n, device=dev)
+        torch.cuda.synchronize()
+
+    def pm(self):
+        self.gs.gs_sample(self.dg, self.index, self.query, self.val, self.inf, self.plan)
+
+    def gm(self):
+        self.gs.gs_sample_gaussian_major(self.dg, self.index, self.query, self.val, self.inf, self.plan, self.work)
+
+    def run(self, k):
+        gs, sync = self.gs, self.torch.cuda.synchronize
+        out = {"workload": f"{self.w.name}: {self.n} points, {self.n_gauss} Gaussians, index "
+                           f"{'x'.join(map(str, self.w.index_cells))} cells, forward only",
+               "points": self.n}
+        for name, fn in (("point_major", self.pm), ("gaussian_major", self.gm)):
+            fn()
+            sync()
+            gs.profile_select(None)
+            gs.profile_reset()
+            gs.profile_enable(True)
+            for _ in range(k):
+                fn()
+            sync()
+            gs.profile_enable(False)
+            kern = {kn: round(ms / k * 1e3, 1) for kn, (c, ms) in gs.profile_read().items()}
+            t = timed(fn, k, sync)
+            out[name] = {"ms": t * 1e3, "points_per_s": self.n / t, "kernels_us": kern}
+        out["gaussian_major_over_point_major"] = out["gaussian_major"]["ms"] / out["point_major"]["ms"]
+        return out
+
+
 def timed(fn, k, sync):
     sync()
     t0 = time.perf_counter()
@@ -336,6 +401,12 @@ def main():
                  "densify": dens}
         del ts
 
+    ab = None
+    if not a.no_ab:
+        ab = {"c4": ABStep("c4_points8m", True).run(max(3, a.steps // 5))}
+        if a.ab_c5:
+            ab["c5"] = ABStep("c5_points100m", False).run(3)
+        sync()
     if a.breakdown:
         for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
             log(f"{k:18s} {v['ms_per_step'] * 1e3:9.1f} us/step  {v['launches_per_step']:5.1f} launches  "
@@ -369,6 +440,7 @@ def main():
         "gauss_point_evals_per_s": (contrib * st.n / t_fwd) if contrib else None,
         "kernels": {k: round(v["ms_per_step"] * 1e3, 2) for k, v in kernels.items()},
         "training_step": train,
+        "forward_ab": ab,
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -173,6 +173,28 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
                     float *out_value, float *out_influence, void *plan, size_t plan_bytes,
                     hipStream_t stream);
 
+/* Bytes of workspace gs_sample_gaussian_major needs for a query (16 per
+ * query; -1 cast to size_t for a GRID or malformed query). */
+size_t gs_sample_gaussian_major_work_bytes(const gs_query *query);
+
+/*
+ * Forward sampling in the paper's Gaussian-major form (Sec. 5.1.2, Fig. 6
+ * B), a variant of gs_sample for VOXELS, POINTS and JITTER queries kept for
+ * comparing the two ways of pairing Gaussians with points. The queries are
+ * ordered by cell as gs_sample orders them; then one wavefront per Gaussian
+ * walks the points of its box (its row spans where trimmed), tests each
+ * against the cutoff and adds w G and w v G to that point's float64 sums
+ * with atomic adds; a last pass writes (Phi, I) = (V/I, I) where I > tau
+ * and the point lies in the box, (0, 0) elsewhere. The outputs equal
+ * gs_sample's up to float32 rounding: the atomic sums have no fixed order,
+ * so they are not bit-reproducible between runs. The plan is left as
+ * gs_sample leaves it, so gs_sample_backward can follow. work: 256-byte
+ * aligned, gs_sample_gaussian_major_work_bytes() bytes.
+ */
+gs_status gs_sample_gaussian_major(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                                   float *out_value, float *out_influence, void *plan, size_t plan_bytes,
+                                   void *work, size_t work_bytes, hipStream_t stream);
+
 /* Bytes of backward workspace for an index (built) and a query. */
 size_t gs_backward_work_bytes(const gs_index *index, const gs_query *query);
 

@@ -13,7 +13,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libgsq.so")
-SOURCES = ["api.cpp", "primitives.hip", "index.hip", "sample.hip", "backward.hip", "train.hip", "densify.hip"]
+SOURCES = ["api.cpp", "primitives.hip", "index.hip", "sample.hip", "backward.hip", "train.hip", "densify.hip", "gauss_major.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = os.environ.get("GS_OFFLOAD_ARCH", "gfx950")
 

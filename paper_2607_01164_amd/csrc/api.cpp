@@ -17,6 +17,12 @@ namespace gs {
 hipError_t launch_loss(int64_t n, const float *value, const float *influence, const float *target,
                        const uint8_t *defined, float tau, float eps, float lambda_fn, float lambda_fp,
                        float *grad_value, float *grad_influence, gs_loss_terms *terms, void *work, hipStream_t s);
+hipError_t launch_sample_gauss_major(const QueryParams &q, const GridParams &g, const Record *rec,
+                                     const CellBox *box, const uint8_t *spans, const uint32_t *gorder,
+                                     int64_t n_gauss, const uint32_t *order, const uint32_t *point_off, float T,
+                                     float tau, float *out_v, float *out_i, const PlanResults &pr, void *work,
+                                     hipStream_t s);
+size_t gauss_major_work_bytes(int64_t nq);
 hipError_t launch_densify(const gs_params &in, int64_t n_in, const float *weight, float tau2, const QueryParams &q,
                           const GridParams &g, const float *value, const float *influence, const float *target,
                           const uint8_t *defined, float tau, float new_log_scale, float new_weight_logit,
@@ -388,6 +394,26 @@ PinnedCount *pinned_count() {
     return &pc;
 }
 
+// The query ordering both forwards share (Sec. 5.1.1's point index in the
+// form of a cell ordering): cell key per query, stable radix sort, per-cell
+// ranges. Leaves the order and ranges in the plan.
+gs_status order_queries(const char *who, const QueryParams &qp, const GridParams &gp, int64_t nq, void *plan,
+                        size_t plan_bytes, Plan *out, hipStream_t stream) {
+    const size_t need = plan_layout(nullptr, nq, gp.ncells).bytes;
+    if (!plan || plan_bytes < need || !aligned(plan))
+        return fail(GS_ERR_WORKSPACE, "%s: plan needs %zu bytes, 256-byte aligned (got %zu)", who, need, plan_bytes);
+    Plan p = plan_layout(plan, nq, gp.ncells);
+    const int bits = bits_for(gp.ncells + 1);
+    const bool odd = (radix_passes(bits) & 1) != 0;
+    uint32_t *ek = odd ? p.keys_alt : p.keys, *ev = odd ? p.order_alt : p.order;
+    uint32_t *ak = odd ? p.keys : p.keys_alt, *av = odd ? p.order : p.order_alt;
+    GS_TRY(launch_query_keys(qp, gp, ek, ev, radix_pass0(p.radix_work, nq, bits), stream), "query keys");
+    GS_TRY(radix_sort_pairs(ek, ev, ak, av, nq, bits, p.radix_work, stream, true), "query sort");
+    GS_TRY(key_offsets(p.keys, nq, p.point_off, gp.ncells + 1, stream), "query ranges");
+    *out = p;
+    return GS_OK;
+}
+
 }  // namespace
 
 namespace gs {
@@ -593,20 +619,44 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
                "gs_sample: grid sampler");
         return GS_OK;
     }
-    const size_t need = plan_layout(nullptr, nq, gp.ncells).bytes;
-    if (!plan || plan_bytes < need || !aligned(plan))
-        return fail(GS_ERR_WORKSPACE, "gs_sample: plan needs %zu bytes, 256-byte aligned (got %zu)", need, plan_bytes);
-    Plan p = plan_layout(plan, nq, gp.ncells);
-    const int bits = bits_for(gp.ncells + 1);
-    const bool odd = (radix_passes(bits) & 1) != 0;
-    uint32_t *ek = odd ? p.keys_alt : p.keys, *ev = odd ? p.order_alt : p.order;
-    uint32_t *ak = odd ? p.keys : p.keys_alt, *av = odd ? p.order : p.order_alt;
-    GS_TRY(launch_query_keys(qp, gp, ek, ev, radix_pass0(p.radix_work, nq, bits), stream), "gs_sample: query keys");
-    GS_TRY(radix_sort_pairs(ek, ev, ak, av, nq, bits, p.radix_work, stream, true), "gs_sample: query sort");
-    GS_TRY(key_offsets(p.keys, nq, p.point_off, gp.ncells + 1, stream), "gs_sample: query ranges");
+    Plan p;
+    if ((st = order_queries("gs_sample", qp, gp, nq, plan, plan_bytes, &p, stream)) != GS_OK) return st;
     GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
                                 index->tau, out_value, out_influence, p.res, stream),
            "gs_sample: point sampler");
+    return GS_OK;
+}
+
+size_t gs_sample_gaussian_major_work_bytes(const gs_query *query) {
+    std::string why;
+    if (!query_valid(query, &why) || query->kind == GS_QUERY_GRID) return (size_t)-1;
+    return gauss_major_work_bytes(query_count(query));
+}
+
+gs_status gs_sample_gaussian_major(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                                   float *out_value, float *out_influence, void *plan, size_t plan_bytes, void *work,
+                                   size_t work_bytes, hipStream_t stream) {
+    gs_status st = check_index("gs_sample_gaussian_major", gauss, index);
+    if (st != GS_OK) return st;
+    if ((st = check_query("gs_sample_gaussian_major", index, query)) != GS_OK) return st;
+    if (query->kind == GS_QUERY_GRID)
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample_gaussian_major: grid queries are not supported (use gs_sample)");
+    const int64_t nq = query_count(query);
+    if (nq > 0 && (!out_value || !out_influence))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample_gaussian_major: output arrays are null");
+    const size_t wneed = gauss_major_work_bytes(nq);
+    if (!work || work_bytes < wneed || !aligned(work))
+        return fail(GS_ERR_WORKSPACE, "gs_sample_gaussian_major: workspace needs %zu bytes, 256-byte aligned (got %zu)",
+                    wneed, work_bytes);
+    const GridParams gp = grid_params(&index->grid);
+    const QueryParams qp = query_params(query, &index->grid);
+    IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
+    Plan p;
+    if ((st = order_queries("gs_sample_gaussian_major", qp, gp, nq, plan, plan_bytes, &p, stream)) != GS_OK)
+        return st;
+    GS_TRY(launch_sample_gauss_major(qp, gp, w.rec, w.box, w.spans, w.gorder, index->n_gauss, p.order, p.point_off,
+                                     cutoff_T(index->tau), index->tau, out_value, out_influence, p.res, work, stream),
+           "gs_sample_gaussian_major");
     return GS_OK;
 }
 

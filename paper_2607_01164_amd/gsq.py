@@ -32,7 +32,8 @@ GS_QUERY_JITTER = 3
 EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_bytes", "gs_sample",
             "gs_backward_work_bytes", "gs_sample_backward", "gs_last_error", "gs_version", "gs_profile_enable",
             "gs_profile_select", "gs_profile_reset", "gs_profile_read", "gs_activate", "gs_activate_backward",
-            "gs_loss_work_bytes", "gs_loss", "gs_densify_work_bytes", "gs_densify")
+            "gs_loss_work_bytes", "gs_loss", "gs_densify_work_bytes", "gs_densify",
+            "gs_sample_gaussian_major_work_bytes", "gs_sample_gaussian_major")
 
 
 class GsLibraryMissing(RuntimeError):
@@ -105,6 +106,10 @@ def load_library():
     L.gs_plan_bytes.argtypes = [P(GsQuery), P(GsGrid)]
     L.gs_sample.restype = ctypes.c_int
     L.gs_sample.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, vp, vp, sz, vp]
+    L.gs_sample_gaussian_major_work_bytes.restype = sz
+    L.gs_sample_gaussian_major_work_bytes.argtypes = [P(GsQuery)]
+    L.gs_sample_gaussian_major.restype = ctypes.c_int
+    L.gs_sample_gaussian_major.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, vp, vp, sz, vp, sz, vp]
     L.gs_backward_work_bytes.restype = sz
     L.gs_backward_work_bytes.argtypes = [P(GsIndex), P(GsQuery)]
     L.gs_sample_backward.restype = ctypes.c_int
@@ -334,6 +339,36 @@ def gs_sample(gauss: Gaussians, index: Index, query: Query, out_value: torch.Ten
     st = load_library().gs_sample(ctypes.byref(g), ctypes.byref(index.c), ctypes.byref(q), out_value.data_ptr(),
                                   out_influence.data_ptr(), _ptr(plan), 0 if plan is None else plan.numel(),
                                   _stream(stream))
+    _check(st)
+
+
+def gaussian_major_work_bytes(query: Query) -> int:
+    q = query.c()
+    b = load_library().gs_sample_gaussian_major_work_bytes(ctypes.byref(q))
+    if b == ctypes.c_size_t(-1).value:
+        raise GsError(GS_ERR_INVALID_ARGUMENT, "grid or malformed query")
+    return int(b)
+
+
+def alloc_gaussian_major_work(query: Query, device) -> torch.Tensor:
+    return _alloc_bytes(gaussian_major_work_bytes(query), device)
+
+
+def gs_sample_gaussian_major(gauss: Gaussians, index: Index, query: Query, out_value: torch.Tensor,
+                             out_influence: torch.Tensor, plan: torch.Tensor, work: torch.Tensor, stream=None) -> None:
+    """The paper's Gaussian-major forward (Sec. 5.1.2) as a variant of
+    gs_sample for voxel-list, point and jittered queries."""
+    g = gauss.c()
+    q = query.c()
+    n = query.size()
+    for t, nm in ((out_value, "out_value"), (out_influence, "out_influence")):
+        _dev_f32(t, nm)
+        if t.numel() < n:
+            raise ValueError(f"{nm} needs {n} elements")
+    st = load_library().gs_sample_gaussian_major(ctypes.byref(g), ctypes.byref(index.c), ctypes.byref(q),
+                                                 out_value.data_ptr(), out_influence.data_ptr(), _ptr(plan),
+                                                 0 if plan is None else plan.numel(), _ptr(work),
+                                                 0 if work is None else work.numel(), _stream(stream))
     _check(st)
 
 

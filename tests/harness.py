@@ -74,6 +74,18 @@ class Run:
         self.inf_np = self.influence[:self.nq].cpu().numpy()
         return self.phi_np, self.inf_np
 
+    def forward_gm(self):
+        """The Gaussian-major forward variant; leaves the plan as forward()."""
+        torch = self.torch
+        self.value = torch.empty(max(self.nq, 1), dtype=torch.float32, device="cuda")
+        self.influence = torch.empty(max(self.nq, 1), dtype=torch.float32, device="cuda")
+        work = self.gs.alloc_gaussian_major_work(self.query, "cuda")
+        self.gs.gs_sample_gaussian_major(self.dg, self.index, self.query, self.value, self.influence, self.plan, work)
+        torch.cuda.synchronize()
+        self.phi_np = self.value[:self.nq].cpu().numpy()
+        self.inf_np = self.influence[:self.nq].cpu().numpy()
+        return self.phi_np, self.inf_np
+
     def backward(self, gv: np.ndarray, gi: np.ndarray):
         torch = self.torch
         self.gv = torch.from_numpy(np.ascontiguousarray(gv, dtype=np.float32)).cuda()

@@ -303,3 +303,17 @@ def test_densify_validation():
         assert call(dp=bad) == gs.GS_ERR_INVALID_ARGUMENT
     assert call(wb=need - 1) == gs.GS_ERR_WORKSPACE
     assert call(work=fake + 64) == gs.GS_ERR_WORKSPACE
+
+
+def test_gaussian_major_validation():
+    L = gs.load_library()
+    qg = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(8, 8, 8), 0, None, None)
+    assert L.gs_sample_gaussian_major_work_bytes(ctypes.byref(qg)) == SIZE_ERR
+    qp = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 1000, 1 << 20, 1 << 20)
+    assert L.gs_sample_gaussian_major_work_bytes(ctypes.byref(qp)) == 16000
+    # an unbuilt index is rejected before any device work
+    idx = gsq.GsIndex()
+    idx.n_pairs = -1
+    gauss = gsq.GsGaussians(0, None, None, None, None, None)
+    assert L.gs_sample_gaussian_major(ctypes.byref(gauss), ctypes.byref(idx), ctypes.byref(qp), None, None, None, 0,
+                                      None, 0, None) == gs.GS_ERR_INVALID_ARGUMENT

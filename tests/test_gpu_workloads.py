@@ -98,7 +98,11 @@ def test_c5_points_full_forward():
     check_index(r)
     phi, inf = r.forward()
     assert np.all(np.isfinite(phi)) and np.all(np.isfinite(inf))
-    check_forward(r, phi, inf, sel=sample_ids(r.nq, 1024, 6), label=w.name)
+    sel = sample_ids(r.nq, 1024, 6)
+    check_forward(r, phi, inf, sel=sel, label=w.name)
+    # the Gaussian-major variant on the same heavy-tailed cloud
+    phi_g, inf_g = r.forward_gm()
+    check_forward(r, phi_g, inf_g, sel=sel, label=f"{w.name} gaussian-major")
     # probes: cavity centres and rims, domain corners
     probes = np.array([[0.3, 0.3, 0.3], [0.7, 0.7, 0.7], [0.3 + 0.149, 0.3, 0.3], [0, 0, 0], [1, 1, 1]], np.float32)
     rp = oracle.forward(g, probes)
