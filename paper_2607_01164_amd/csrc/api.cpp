@@ -318,6 +318,7 @@ BwdWork bwd_layout(void *base, const gs_index *index, const gs_query *q) {
     w.b.moments = c.take<float>((size_t)(n > 0 ? n : 1) * 12);
     (void)q;
     w.b.ab = c.take<float2>(mq);
+    w.b.cot = c.take<float2>(mq);
     w.bytes = c.off;
     return w;
 }

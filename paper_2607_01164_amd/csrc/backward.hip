@@ -52,15 +52,31 @@ __device__ __forceinline__ void alpha_beta(float phi, float inf, float gp, float
 
 // Cotangent staging for ordered queries: (alpha, beta) of the k-th
 // query in plan order, from the forward's (Phi, I) that the plan keeps in
-// that order; only the cotangents are gathered by query id.
+// that order. The cotangents are first packed in query order as pairs
+// (coalesced), so staging gathers one 8-byte pair per query by id instead
+// of two 4-byte values from two arrays.
 constexpr int kStageItems = 4;  // queries per thread of the point staging
 
+__global__ __launch_bounds__(kBlock) void k_pack_cotangents(int64_t n, const float *__restrict__ gval,
+                                                            const float *__restrict__ ginf, bool vec,
+                                                            float2 *__restrict__ cot) {
+    const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kStageItems;
+    if (i0 >= n) return;
+    if (vec && i0 + kStageItems <= n) {
+        const float4 v = *(const float4 *)(gval + i0), g = *(const float4 *)(ginf + i0);
+        *(float4 *)(cot + i0) = make_float4(v.x, g.x, v.y, g.y);
+        *(float4 *)(cot + i0 + 2) = make_float4(v.z, g.z, v.w, g.w);
+    } else {
+        for (int i = 0; i < kStageItems; ++i)
+            if (i0 + i < n) cot[i0 + i] = make_float2(gval[i0 + i], ginf[i0 + i]);
+    }
+}
+
 // Thread t stages queries 4t .. 4t+3 with 16-byte loads of their ids and
-// outputs, so the eight cotangent gathers of a thread are in flight together.
+// outputs, so the four cotangent gathers of a thread are in flight together.
 __global__ __launch_bounds__(kBlock) void k_stage_points(int64_t n, const uint32_t *__restrict__ order,
                                                          const float2 *__restrict__ plan_out,
-                                                         const float *__restrict__ gval, const float *__restrict__ ginf,
-                                                         float2 *__restrict__ ab) {
+                                                         const float2 *__restrict__ cot, float2 *__restrict__ ab) {
     const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kStageItems;
     if (k0 >= n) return;
     uint32_t pid[kStageItems];
@@ -84,19 +100,18 @@ __global__ __launch_bounds__(kBlock) void k_stage_points(int64_t n, const uint32
             o[i] = ok ? plan_out[k0 + i] : make_float2(0.0f, 0.0f);
         }
     }
-    float gv[kStageItems], gi[kStageItems];
+    float2 c[kStageItems];
 #pragma unroll
     for (int i = 0; i < kStageItems; ++i) {
         // undefined queries (I = 0) have no gradient: their cotangents are not read
         const bool need = o[i].y > 0.0f;
-        gv[i] = need ? gval[pid[i]] : 0.0f;
-        gi[i] = need ? ginf[pid[i]] : 0.0f;
+        c[i] = need ? cot[pid[i]] : make_float2(0.0f, 0.0f);
     }
     float2 r[kStageItems];
 #pragma unroll
     for (int i = 0; i < kStageItems; ++i) {
         float al, be;
-        alpha_beta(o[i].x, o[i].y, gv[i], gi[i], al, be);
+        alpha_beta(o[i].x, o[i].y, c[i].x, c[i].y, al, be);
         r[i] = make_float2(al, be);
     }
     if (k0 + kStageItems <= n) {
@@ -536,9 +551,12 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
         if (grid)
             hipLaunchKernelGGL(k_stage_grid, dim3(qblocks), dim3(kBlock), 0, s, q.n, value, influence, grad_value,
                                grad_influence, b.ab);
-        else
-            hipLaunchKernelGGL(k_stage_points, dim3((uint32_t)((q.n + kBlock * kStageItems - 1) / (kBlock * kStageItems))),
-                               dim3(kBlock), 0, s, q.n, order, plan_out, grad_value, grad_influence, b.ab);
+        else {
+            const dim3 sb((uint32_t)((q.n + kBlock * kStageItems - 1) / (kBlock * kStageItems)));
+            const bool vec = ((uintptr_t)grad_value % 16 == 0) && ((uintptr_t)grad_influence % 16 == 0);
+            hipLaunchKernelGGL(k_pack_cotangents, sb, dim3(kBlock), 0, s, q.n, grad_value, grad_influence, vec, b.cot);
+            hipLaunchKernelGGL(k_stage_points, sb, dim3(kBlock), 0, s, q.n, order, plan_out, b.cot, b.ab);
+        }
         prof_end("bwd_stage", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         const uint32_t wblocks =

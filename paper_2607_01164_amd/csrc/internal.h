@@ -371,6 +371,7 @@ hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g,
 struct BackwardBuffers {
     float *moments;        // [n_gauss][12]
     float2 *ab;            // [n] (alpha, beta) per query: plan order (points, voxels) or voxel order (grid)
+    float2 *cot;           // [n] (dL/dPhi, dL/dI) packed in query order (points, voxels)
 };
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
                            const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
