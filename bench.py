@@ -121,13 +121,15 @@ class Step:
         """(Gaussian, point) pairs the forward and the backward test: the sum
         over cells of (pairs listed in the cell) x (queries in the cell), from
         the index's cell offsets and the plan's per-cell query offsets (after
-        the four 256-byte aligned query-length arrays of the plan)."""
+        the four 256-byte aligned query-length arrays of the plan, one offset
+        per quarter of a cell along x)."""
         torch = self.torch
         ncells = self.grid.cells[0] * self.grid.cells[1] * self.grid.cells[2]
         al = lambda b: (b + 255) // 256 * 256
         off = 4 * al(4 * max(self.n, 1))
-        point_off = self.plan[off: off + 4 * (ncells + 2)].view(torch.int32).to(torch.int64)
-        pts = point_off[1:ncells + 1] - point_off[:ncells]
+        # the plan's offsets are per quarter of a cell along x (4 keys a cell)
+        point_off = self.plan[off: off + 4 * (4 * ncells + 2)].view(torch.int32).to(torch.int64)
+        pts = point_off[4:4 * ncells + 1:4] - point_off[0:4 * ncells:4]
         co = self.index.cell_offsets.to(torch.int64)
         pairs = co[1:] - co[:-1]
         return int((pts * pairs).sum().item())
@@ -371,6 +373,7 @@ def main():
     dom = (dom_name, {"launches_per_step": c / a.steps, "ms_per_step": ms / a.steps, "avg_ms": ms / c})
     n_pairs = st.index.n_pairs
     n_tests = st.candidate_tests()
+    bwd_tests = gs.backward_pair_count(st.index, st.query, st.plan, st.work)
     # forward alone and backward alone, for the query rates
     t_fwd = timed(st.forward, a.steps, sync)
     t_bwd = timed(st.backward, a.steps, sync)
@@ -416,7 +419,7 @@ def main():
 
     cpu = None if a.no_cpu else cpu_baseline(st, a.cpu_seconds)
     contrib = cpu.pop("contrib_per_point") if cpu else None
-    roof = roofline(dom[0], dom[1], st, n_pairs, n_tests, contrib)
+    roof = roofline(dom[0], dom[1], st, n_pairs, bwd_tests if dom[0] == "bwd_gauss" else n_tests, contrib)
     out = {
         "metric": "query points/sec fwd and fwd+bwd samples/sec; % of HBM roofline",
         "value": st.n / t_step,
@@ -433,7 +436,7 @@ def main():
         "config": {"workload": f"{WORKLOAD}: 256^3 grid, 262144 Gaussians, batch of 2^20 random voxel centres, "
                                f"index {a.cells[0]}x{a.cells[1]}x{a.cells[2]} cells, step = build + forward + backward",
                    "global_batch": st.n, "n_gauss": st.g_host.n, "index_pairs": n_pairs,
-                   "candidate_tests": n_tests},
+                   "candidate_tests": n_tests, "backward_tests": bwd_tests},
         "fwd_points_per_s": st.n / t_fwd,
         "fwd_bwd_samples_per_s_excl_build": st.n / (t_fwd + t_bwd),
         "ms_build": t_build * 1e3, "ms_fwd": t_fwd * 1e3, "ms_bwd": t_bwd * 1e3,
@@ -493,19 +496,21 @@ def roofline(name, k, st, n_pairs, n_tests, contrib_per_point):
     out = {"kernel": name, "avg_us": avg_s * 1e6, "launches_per_step": k["launches_per_step"]}
     traffic = measured_traffic(name)
     if name in FLOPS_PER_CONTRIB:
-        # units: the candidate tests of the launch (exact, from the index and
-        # the plan) and its contributing pairs (the oracle's count per point
-        # on the CPU-baseline sample, times the batch; None without it)
+        # units: the pairs the launch tests (exact: for the forward, the cell
+        # lists times the cells' queries, from the index and the plan; for the
+        # backward, the queries of each Gaussian's trimmed rows, counted by
+        # the library) and its contributing pairs (the oracle's count per
+        # point on the CPU-baseline sample, times the batch; None without it)
         if contrib_per_point is None:
             out.update({"bound": "alu", "achieved": None, "peak": FP32_VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
-                        "frac": None, "traffic": traffic, "candidate_tests": n_tests})
+                        "frac": None, "traffic": traffic, "pair_tests": n_tests})
             return out
         units = contrib_per_point * st.n
         flops = FLOPS_PER_TEST * n_tests + FLOPS_PER_CONTRIB[name] * units
         ach = flops / avg_s / 1e12
         out.update({"bound": "alu", "achieved": ach, "peak": FP32_VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": ach / FP32_VEC_PEAK_TFLOPS, "traffic": traffic,
-                    "flops_per_launch": flops, "candidate_tests": n_tests, "contributing_pairs": units})
+                    "flops_per_launch": flops, "pair_tests": n_tests, "contributing_pairs": units})
         return out
     per_pair = {"radix_downsweep": SORT_BYTES_PER_PAIR, "emit": EMIT_BYTES_PER_PAIR}.get(name)
     if per_pair is None:

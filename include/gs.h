@@ -218,6 +218,19 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
                              float *d_scale, float *d_rot, float *d_value, float *d_weight, void *work,
                              size_t work_bytes, hipStream_t stream);
 
+/*
+ * For measurement: the number of (Gaussian, query) pairs gs_sample_backward
+ * tests against the cutoff for this built index, query and plan (the plan
+ * a gs_sample call filled; none for GRID queries): per Gaussian, the
+ * queries of its box rows, cut to the row spans of a trimmed box and, for
+ * ordered queries, to the quarters of the end cells along x that the row's
+ * bound reaches. Uses work (gs_backward_work_bytes() bytes, its contents
+ * are overwritten) and waits on the stream for the count.
+ */
+gs_status gs_backward_pair_count(const gs_index *index, const gs_query *query, const void *plan,
+                                 size_t plan_bytes, void *work, size_t work_bytes, int64_t *count,
+                                 hipStream_t stream);
+
 /* Message describing the last failure on the calling thread ("" if none). */
 const char *gs_last_error(void);
 

@@ -264,8 +264,9 @@ def index(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01):
 
 
 def point_order(points, cells, lo=(0, 0, 0), hi=(1, 1, 1)):
-    """Points ordered by (cell key, id); outside points take key ncells.
-    Returns (keys_sorted, order, point_offsets[ncells+2])."""
+    """Points ordered by (4 cell key + quarter of the cell along x, id);
+    outside points take key 4 ncells. Returns (keys_sorted, order,
+    point_offsets[4 ncells + 2])."""
     pts = _f32(points).reshape(-1, 3)
     c = np.asarray(cells, dtype=np.int32).reshape(3)
     lo_, hi_ = _box(lo, hi)
@@ -273,7 +274,7 @@ def point_order(points, cells, lo=(0, 0, 0), hi=(1, 1, 1)):
     ncells = int(c[0]) * int(c[1]) * int(c[2])
     keys = np.zeros(max(n, 1), dtype=np.uint32)
     order = np.zeros(max(n, 1), dtype=np.uint32)
-    offs = np.zeros(ncells + 2, dtype=np.uint32)
+    offs = np.zeros(4 * ncells + 2, dtype=np.uint32)
     rc = lib().orc_point_order(n, _p(pts), _p(lo_), _p(hi_), _p(c), _p(keys), _p(order), _p(offs))
     if rc != 0:
         raise RuntimeError("orc_point_order failed")

@@ -865,20 +865,24 @@ int orc_index(int64_t n, const float *mean, const float *scale, const float *rot
 }
 
 /*
- * Query ordering for unstructured queries: each point's key is its cell
- * key (cell_j = clamp(floor((p_j - lo_j) * invc_j), 0, C_j - 1), float32) or
- * ncells for a point outside the closed box; order[] lists point ids by
- * (key, id); point_offsets[k] = number of points with key < k, k = 0..ncells+1.
+ * Query ordering for unstructured queries (the library's plan, standing in
+ * for the paper's sample BVH): each point's key is 4 cell + j, with the cell
+ * key cell = cx + Cx (cy + Cy cz), c_j = clamp(floor(t_j), 0, C_j - 1),
+ * t_j = (p_j - lo_j) * invc_j in float32, and j = floor(4 (t_x - c_x)) in
+ * [0, 3] the quarter of the cell along x; 4 ncells for a point outside the
+ * closed box. order[] lists point ids by (key, id); point_offsets[k] =
+ * number of points with key < k, k = 0 .. 4 ncells + 1.
  */
 int orc_point_order(int64_t npts, const float *pts, const float lo[3], const float hi[3],
                     const int32_t cells[3], uint32_t *keys_out, uint32_t *order, uint32_t *point_offsets)
 {
     if (npts < 0 || !grid_ok(lo, hi, cells)) return ORC_ERR_ARG;
     int64_t ncells = (int64_t)cells[0] * cells[1] * cells[2];
+    const int64_t nkeys = 4 * ncells + 1; /* 4 keys per cell, then the outside key */
     float invc[3];
     grid_invc(lo, hi, cells, invc);
     uint32_t *key = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(npts > 0 ? npts : 1));
-    int64_t *cursor = (int64_t *)calloc((size_t)ncells + 2, sizeof(int64_t));
+    int64_t *cursor = (int64_t *)calloc((size_t)nkeys + 1, sizeof(int64_t));
     if (!key || !cursor) {
         free(key);
         free(cursor);
@@ -886,9 +890,10 @@ int orc_point_order(int64_t npts, const float *pts, const float lo[3], const flo
     }
     for (int64_t p = 0; p < npts; p++) {
         const float *pp = pts + 3 * p;
-        int64_t k = ncells;
+        int64_t k = 4 * ncells;
         if (in_box(pp, lo, hi)) {
             int64_t c[3];
+            float tx = 0.0f;
             for (int j = 0; j < 3; j++) {
                 volatile float dl = pp[j] - lo[j];
                 volatile float t = dl * invc[j];
@@ -897,14 +902,19 @@ int orc_point_order(int64_t npts, const float *pts, const float lo[3], const flo
                 if (ci < 0) ci = 0;
                 if (ci > cells[j] - 1) ci = cells[j] - 1;
                 c[j] = ci;
+                if (j == 0) tx = t;
             }
-            k = c[0] + (int64_t)cells[0] * (c[1] + (int64_t)cells[1] * c[2]);
+            /* the quarter of the cell along x, floor(4 (t - c)) in float32 */
+            volatile float fr = tx - (float)c[0];
+            float fq = floorf(fr * 4.0f);
+            int64_t qx = fq < 0.0f ? 0 : (fq > 3.0f ? 3 : (int64_t)fq);
+            k = 4 * (c[0] + (int64_t)cells[0] * (c[1] + (int64_t)cells[1] * c[2])) + qx;
         }
         key[p] = (uint32_t)k;
         cursor[k + 1]++;
     }
-    for (int64_t k = 0; k <= ncells; k++) cursor[k + 1] += cursor[k];
-    for (int64_t k = 0; k <= ncells + 1; k++) point_offsets[k] = (uint32_t)cursor[k];
+    for (int64_t k = 0; k < nkeys; k++) cursor[k + 1] += cursor[k];
+    for (int64_t k = 0; k <= nkeys; k++) point_offsets[k] = (uint32_t)cursor[k];
     for (int64_t p = 0; p < npts; p++) {
         int64_t at = cursor[key[p]]++;
         order[at] = (uint32_t)p;

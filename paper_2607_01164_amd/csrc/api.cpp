@@ -131,7 +131,7 @@ int gauss_order_bits(const gs_grid *g) { return gauss_order_full_bits(g) - gauss
 struct IndexWork {
     Record *rec;
     CellBox *box;
-    uint8_t *spans;      // [n][kSpanRows] row spans of trimmed boxes
+    uint8_t *spans;      // [n][kSpanStride] row spans and quarter codes of trimmed boxes
     uint32_t *gorder;    // [n] Gaussians in spatial order
     uint32_t *gkeys;     // [n] their sort keys
     uint32_t *gsort_k;   // [n] sort scratch
@@ -159,7 +159,7 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     w.rec = c.take<Record>((size_t)(n > 0 ? n : 1));
     w.box = c.take<CellBox>((size_t)(n > 0 ? n : 1));
     const size_t n1 = (size_t)(n > 0 ? n : 1);
-    w.spans = c.take<uint8_t>(n1 * kSpanRows);
+    w.spans = c.take<uint8_t>(n1 * kSpanStride);
     w.gorder = c.take<uint32_t>(n1);
     w.gkeys = c.take<uint32_t>(n1);
     w.gsort_k = c.take<uint32_t>(n1);
@@ -183,7 +183,7 @@ struct Plan {
     uint32_t *order;     // [n] query ids in cell order
     uint32_t *keys_alt;  // [n]
     uint32_t *order_alt; // [n]
-    uint32_t *point_off; // [ncells + 2]
+    uint32_t *point_off; // [kSub ncells + 2]
     void *radix_work;
     PointItems items;
     PlanResults res;
@@ -198,8 +198,8 @@ Plan plan_layout(void *base, int64_t n, int64_t ncells) {
     p.order = c.take<uint32_t>(m);
     p.keys_alt = c.take<uint32_t>(m);
     p.order_alt = c.take<uint32_t>(m);
-    p.point_off = c.take<uint32_t>((size_t)ncells + 2);
-    p.radix_work = c.take<char>(radix_work_bytes(n > 0 ? n : 1, bits_for(ncells + 1)));
+    p.point_off = c.take<uint32_t>((size_t)kSub * ncells + 2);
+    p.radix_work = c.take<char>(radix_work_bytes(n > 0 ? n : 1, bits_for((int64_t)kSub * ncells + 1)));
     p.items.item_off = c.take<uint32_t>((size_t)ncells + 2);
     p.items.max_items = ncells + 1 + (n > 0 ? n : 0) / 64 + 1;
     p.items.items = c.take<uint32_t>((size_t)p.items.max_items);
@@ -404,13 +404,13 @@ gs_status order_queries(const char *who, const QueryParams &qp, const GridParams
     if (!plan || plan_bytes < need || !aligned(plan))
         return fail(GS_ERR_WORKSPACE, "%s: plan needs %zu bytes, 256-byte aligned (got %zu)", who, need, plan_bytes);
     Plan p = plan_layout(plan, nq, gp.ncells);
-    const int bits = bits_for(gp.ncells + 1);
+    const int bits = bits_for((int64_t)kSub * gp.ncells + 1);
     const bool odd = (radix_passes(bits) & 1) != 0;
     uint32_t *ek = odd ? p.keys_alt : p.keys, *ev = odd ? p.order_alt : p.order;
     uint32_t *ak = odd ? p.keys : p.keys_alt, *av = odd ? p.order : p.order_alt;
     GS_TRY(launch_query_keys(qp, gp, ek, ev, radix_pass0(p.radix_work, nq, bits), stream), "query keys");
     GS_TRY(radix_sort_pairs(ek, ev, ak, av, nq, bits, p.radix_work, stream, true), "query sort");
-    GS_TRY(key_offsets(p.keys, nq, p.point_off, gp.ncells + 1, stream), "query ranges");
+    GS_TRY(key_offsets(p.keys, nq, p.point_off, (int64_t)kSub * gp.ncells + 1, stream), "query ranges");
     *out = p;
     return GS_OK;
 }
@@ -820,6 +820,45 @@ gs_status gs_densify(const gs_params *in, int64_t n_in, const float *weight, con
     if (*n_out > capacity)
         return fail(GS_ERR_CAPACITY, "gs_densify: %lld kept Gaussians exceed the capacity %lld", (long long)*n_out,
                     (long long)capacity);
+    return GS_OK;
+}
+
+gs_status gs_backward_pair_count(const gs_index *index, const gs_query *query, const void *plan,
+                                 size_t plan_bytes, void *work, size_t work_bytes, int64_t *count,
+                                 hipStream_t stream) {
+    if (!count) return fail(GS_ERR_INVALID_ARGUMENT, "gs_backward_pair_count: count is null");
+    *count = 0;
+    if (!index || index->n_pairs < 0 || index->n_gauss < 0)
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_backward_pair_count: index not built");
+    gs_status st = check_query("gs_backward_pair_count", index, query);
+    if (st != GS_OK) return st;
+    const int64_t nq = query_count(query);
+    const GridParams gp = grid_params(&index->grid);
+    const QueryParams qp = query_params(query, &index->grid);
+    const size_t need = bwd_layout(nullptr, index, query).bytes;
+    if (!work || work_bytes < need || !aligned(work))
+        return fail(GS_ERR_WORKSPACE, "gs_backward_pair_count: workspace needs %zu bytes (got %zu)", need,
+                    work_bytes);
+    Plan p{};
+    if (query->kind != GS_QUERY_GRID) {
+        const size_t pneed = plan_layout(nullptr, nq, gp.ncells).bytes;
+        if (!plan || plan_bytes < pneed || !aligned(plan))
+            return fail(GS_ERR_WORKSPACE, "gs_backward_pair_count: plan needs %zu bytes (got %zu)", pneed,
+                        plan_bytes);
+        p = plan_layout(const_cast<void *>(plan), nq, gp.ncells);
+    }
+    PinnedCount *pc = pinned_count();
+    if (!pc) return fail(GS_ERR_HIP, "gs_backward_pair_count: could not allocate the pinned read-back word");
+    IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
+    BwdWork bw = bwd_layout(work, index, query);
+    unsigned long long *total = (unsigned long long *)bw.b.moments;
+    GS_TRY(launch_count_backward_pairs(qp, gp, w.box, w.spans, index->n_gauss, p.point_off, total, stream),
+           "gs_backward_pair_count");
+    GS_TRY(hipMemcpyAsync(pc->value, total, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
+           "gs_backward_pair_count: read-back");
+    GS_TRY(hipEventRecord(pc->copied, stream), "gs_backward_pair_count: event");
+    GS_TRY(hipEventSynchronize(pc->copied), "gs_backward_pair_count: wait");
+    *count = (int64_t)*pc->value;
     return GS_OK;
 }
 

@@ -348,11 +348,18 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                 zz = row / nry;
             const uint32_t yy = row - zz * nry;
             // the row's run of cells: the whole box row, or its span
-            uint32_t xa = 0, xn = f_nx;
+            uint32_t xa = 0, xn = f_nx, qa = 0, qb = 0;
             if (f_trim) {
-                const uint32_t code = spans[(size_t)f_gid * kSpanRows + (yy / ry) + f_ny * (zz / rz)];
+                const size_t at = (size_t)f_gid * kSpanStride + (yy / ry) + f_ny * (zz / rz);
+                const uint32_t code = spans[at];
                 xa = span_first(code);
                 xn = span_len(code);
+                if (!GRID) {
+                    // the quarters of the run's end cells the bound reaches
+                    const uint32_t qc = spans[at + kSpanRows];
+                    qa = qc & 3u;
+                    qb = qc >> 2;
+                }
             }
             if (GRID) {
                 const uint32_t vy = f_ly * ry + yy, vz = f_lz * rz + zz;
@@ -364,8 +371,8 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
             } else if (xn > 0) {
                 const uint32_t cy = f_ly + yy, cz = f_lz + zz;
                 const uint32_t kbase = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz) + f_lx;
-                start = point_off[kbase + xa];
-                len = point_off[kbase + xa + xn] - start;
+                start = point_off[kSub * (kbase + xa) + qa];
+                len = point_off[kSub * (kbase + xa + xn) - qb] - start;
             }
         }
         const uint32_t nrows = (Rw - rb) < (uint32_t)kWave ? (Rw - rb) : (uint32_t)kWave;
@@ -531,7 +538,73 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
     d_weight[i] = mc.z;
 }
 
+// Pairs the backward tests, for measurement: per Gaussian the queries in
+// its box rows, cut to the row spans and end-cell quarters of a trimmed box
+// (grids: the voxels of its box rows). Summed per block, then into *total
+// with one integer atomic per block (the sum does not depend on its order).
+__global__ __launch_bounds__(kBlock) void k_count_backward_pairs(QueryParams q, GridParams g,
+                                                                 const CellBox *__restrict__ box,
+                                                                 const uint8_t *__restrict__ spans, int64_t n_gauss,
+                                                                 const uint32_t *__restrict__ point_off,
+                                                                 unsigned long long *total) {
+    __shared__ unsigned long long lds[kWavesPerBlock];
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    unsigned long long c = 0;
+    if (i < n_gauss) {
+        const CellBox bx = box[i];
+        if (bx.hi.x >= bx.lo.x) {
+            const bool grid = q.kind == 0;
+            const uint32_t rx = grid ? (uint32_t)(q.dims[0] / g.cells[0]) : 1u;
+            const uint32_t ry = grid ? (uint32_t)(q.dims[1] / g.cells[1]) : 1u;
+            const uint32_t rz = grid ? (uint32_t)(q.dims[2] / g.cells[2]) : 1u;
+            const uint32_t nx = (uint32_t)(bx.hi.x - bx.lo.x + 1), ny = (uint32_t)(bx.hi.y - bx.lo.y + 1);
+            const uint32_t nz = (uint32_t)(bx.hi.z - bx.lo.z + 1);
+            for (uint32_t zz = 0; zz < nz; ++zz)
+                for (uint32_t yy = 0; yy < ny; ++yy) {
+                    uint32_t xa = 0, xn = nx, qa = 0, qb = 0;
+                    if (bx.lo.w) {
+                        const size_t at = (size_t)i * kSpanStride + yy + ny * zz;
+                        xa = span_first(spans[at]);
+                        xn = span_len(spans[at]);
+                        qa = spans[at + kSpanRows] & 3u;
+                        qb = spans[at + kSpanRows] >> 2;
+                    }
+                    if (xn == 0) continue;
+                    if (grid) {
+                        c += (unsigned long long)xn * rx * ry * rz;
+                    } else {
+                        const uint32_t kb = (uint32_t)g.cells[0] * ((uint32_t)bx.lo.y + yy +
+                                                                    (uint32_t)g.cells[1] * ((uint32_t)bx.lo.z + zz)) +
+                                            (uint32_t)bx.lo.x + xa;
+                        c += point_off[kSub * (kb + xn) - qb] - point_off[kSub * kb + qa];
+                    }
+                }
+        }
+    }
+    // block sum in a fixed order, then one atomic per block
+    const uint32_t lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) c += __shfl_xor(c, o, kWave);
+    if (lane == 0) lds[wid] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long t = 0;
+        for (int w = 0; w < kWavesPerBlock; ++w) t += lds[w];
+        if (t) atomicAdd(total, t);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g, const CellBox *box,
+                                      const uint8_t *spans, int64_t n_gauss, const uint32_t *point_off,
+                                      unsigned long long *total, hipStream_t s) {
+    hipError_t e = fill_u32((uint32_t *)total, 0u, 2, s);
+    if (e != hipSuccess || n_gauss <= 0) return e;
+    hipLaunchKernelGGL(k_count_backward_pairs, dim3((uint32_t)((n_gauss + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
+                       q, g, box, spans, n_gauss, point_off, total);
+    return hipGetLastError();
+}
 
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
                            const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,

@@ -76,17 +76,21 @@ __global__ __launch_bounds__(kBlock) void k_forward_gauss(GridParams g, const Re
         uint32_t start = 0, len = 0;
         if (row < R) {
             const uint32_t zz = row / ny, yy = row - zz * ny;
-            uint32_t xa = 0, xn = nx;
+            uint32_t xa = 0, xn = nx, qa = 0, qb = 0;
             if (trimmed) {
-                const uint32_t code = spans[(size_t)gid * kSpanRows + yy + ny * zz];
+                const size_t at = (size_t)gid * kSpanStride + yy + ny * zz;
+                const uint32_t code = spans[at];
                 xa = span_first(code);
                 xn = span_len(code);
+                const uint32_t qc = spans[at + kSpanRows];  // quarters of the end cells reached
+                qa = qc & 3u;
+                qb = qc >> 2;
             }
             if (xn > 0) {
                 const uint32_t cy = (uint32_t)bx.lo.y + yy, cz = (uint32_t)bx.lo.z + zz;
                 const uint32_t kb = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz) + (uint32_t)bx.lo.x + xa;
-                start = point_off[kb];
-                len = point_off[kb + xn] - start;
+                start = point_off[kSub * kb + qa];
+                len = point_off[kSub * (kb + xn) - qb] - start;
             }
         }
         const uint32_t nrows = R - rb < (uint32_t)kWave ? R - rb : (uint32_t)kWave;

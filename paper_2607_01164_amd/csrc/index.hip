@@ -123,7 +123,7 @@ struct SpanGrid {
     double glo[3], icx, wdy, wdz, Tq;
 };
 
-__device__ uint32_t span_row(const SpanParams &p, int r, const SpanGrid &sg, uint32_t &len) {
+__device__ uint32_t span_row(const SpanParams &p, int r, const SpanGrid &sg, uint32_t &len, uint32_t &qcode) {
     const int cy = p.y0 + r % p.ny, cz = p.z0 + r / p.ny;
     const double Y0 = (sg.glo[1] + (double)cy * sg.wdy) - (double)p.mu[1];
     const double Y1 = (sg.glo[1] + (double)(cy + 1) * sg.wdy) - (double)p.mu[1];
@@ -131,6 +131,7 @@ __device__ uint32_t span_row(const SpanParams &p, int r, const SpanGrid &sg, uin
     const double Z1 = (sg.glo[2] + (double)(cz + 1) * sg.wdz) - (double)p.mu[2];
     const double qmin = rect_qmin(p.P00, p.P01, p.P11, p.kz, p.ky, Y0, Y1, Z0, Z1);
     len = 0;
+    qcode = 0;
     if (qmin > sg.Tq) return kSpanEmpty;
     int cl = p.x0, ch = p.x1;
     const double wm = sqrt((sg.Tq - qmin) * p.vc);
@@ -140,14 +141,32 @@ __device__ uint32_t span_row(const SpanParams &p, int r, const SpanGrid &sg, uin
     const double m0 = c00 < c01 ? c00 : c01, m1 = c10 < c11 ? c10 : c11;
     const double M0 = c00 > c01 ? c00 : c01, M1 = c10 > c11 ? c10 : c11;
     const double cmin = m0 < m1 ? m0 : m1, cmax = M0 > M1 ? M0 : M1;
-    const double fl = floor(((cmin - wm) - sg.glo[0]) * sg.icx);
-    const double fh = floor(((cmax + wm) - sg.glo[0]) * sg.icx);
+    const double xl = ((cmin - wm) - sg.glo[0]) * sg.icx, xh = ((cmax + wm) - sg.glo[0]) * sg.icx;
+    const double fl = floor(xl);
+    const double fh = floor(xh);
     if (__builtin_isfinite(fl) && __builtin_isfinite(fh)) {
         cl = fl < (double)p.x0 ? p.x0 : (fl > (double)p.x1 ? p.x1 + 1 : (int)fl);
         ch = fh > (double)p.x1 ? p.x1 : (fh < (double)p.x0 ? p.x0 - 1 : (int)fh);
     }
     if (cl > ch) return kSpanEmpty;
     len = (uint32_t)(ch - cl + 1);
+    // The quarters of the run's end cells the bound does not reach, for the
+    // query order by quarter of a cell along x: quarter j of cell c holds
+    // the queries whose float32 cell coordinate t has floor(4 (t - c)) = j.
+    // The bound is widened by 2^-12 cells first, far more than float32
+    // places t away from its exact value (under 36 2^-22 cells for a grid of
+    // up to 2^12 cells per axis, far below the margin the enlarged radius
+    // already gives).
+    if (__builtin_isfinite(fl) && __builtin_isfinite(fh)) {
+        const double gl = xl - 1.0 / 4096.0, gh = xh + 1.0 / 4096.0;
+        int q0 = 0, q1 = 0;
+        if ((double)cl <= gl) q0 = (int)floor((gl - (double)cl) * (double)kSub);
+        if ((double)ch + 1.0 > gh) q1 = (int)kSub - 1 - (int)floor((gh - (double)ch) * (double)kSub);
+        q0 = q0 < 0 ? 0 : (q0 > (int)kSub - 1 ? (int)kSub - 1 : q0);
+        q1 = q1 < 0 ? 0 : (q1 > (int)kSub - 1 ? (int)kSub - 1 : q1);
+        if (cl == ch && q0 + q1 > (int)kSub - 1) q0 = q1 = 0;  // cannot happen for a non-empty run; kept safe
+        qcode = (uint32_t)q0 | ((uint32_t)q1 << 2);
+    }
     return (uint32_t)(cl - p.x0) | ((uint32_t)(ch - p.x0) << 4);
 }
 
@@ -306,15 +325,17 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
             sp.y0 = sp_i[2][t];
             sp.z0 = sp_i[3][t];
             sp.ny = sp_i[4][t];
-            const uint32_t code = span_row(sp, r, sg, len);
+            uint32_t qcode;
+            const uint32_t code = span_row(sp, r, sg, len, qcode);
             ((uint8_t *)&sp_code[r >> 2][t])[r & 3] = (uint8_t)code;
+            spans[((size_t)blockIdx.x * kPreBlock + t) * kSpanStride + kSpanRows + (uint32_t)r] = (uint8_t)qcode;
             atomicAdd(&sp_cnt[wbase + o], len);
         }
     }
     __builtin_amdgcn_wave_barrier();
     if (trimmed) {
         cnt = sp_cnt[tid];
-        uint4 *dst = (uint4 *)(spans + (size_t)i * kSpanRows);
+        uint4 *dst = (uint4 *)(spans + (size_t)i * kSpanStride);
 #pragma unroll
         for (int k = 0; k < kSpanRows / 16; ++k)
             dst[k] = make_uint4(sp_code[4 * k][tid], sp_code[4 * k + 1][tid], sp_code[4 * k + 2][tid],
@@ -433,7 +454,7 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
         const int64_t base = (int64_t)(pair_off[gg] - tile_begin);  // the Gaussian's first pair, tile-relative
         const CellBox b = box[gg];
         // the span line is read whole, together with the box
-        const uint4 *sp4 = (const uint4 *)(spans + (size_t)gg * kSpanRows);
+        const uint4 *sp4 = (const uint4 *)(spans + (size_t)gg * kSpanStride);
         const uint4 c0 = sp4[0], c1 = sp4[1], c2 = sp4[2], c3 = sp4[3];
         if (b.hi.x < b.lo.x || base >= (int64_t)tile_cnt) continue;
         const uint64_t gbits = fold ? (uint64_t)(gg - gfirst) << 32 : 0ull;

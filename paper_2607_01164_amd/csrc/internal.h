@@ -34,6 +34,11 @@ struct alignas(16) CellBox {
     int4 lo, hi;
 };
 constexpr int kSpanRows = 64;          // rows of a trimmed box at most
+// A trimmed box's line of span data: its kSpanRows span codes, then one
+// quarter code per row: (first quarter of the row's first cell that the
+// bound reaches) | (quarters of its last cell past the bound) << 2, for the
+// query order by quarter of a cell (kSub below).
+constexpr int kSpanStride = 2 * kSpanRows;
 constexpr int kSpanNx = 16;            // cells per row of a trimmed box at most
 constexpr uint32_t kSpanEmpty = 0x0Fu;
 
@@ -287,6 +292,14 @@ hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8
                        uint32_t *tile_first, uint32_t *keys, uint32_t *gids, const RadixPass0 &pass0, hipStream_t s);
 
 // Sampling (sample.hip).
+// The plan orders the queries by cell and, inside a cell, by the quarter of
+// the cell along x that their position falls in: key kSub c + j for quarter
+// j of cell c, kSub ncells outside the domain. Its offsets point_off (kSub
+// ncells + 2 entries) give every cell's queries, [point_off[kSub c],
+// point_off[kSub (c + 1)]), and every quarter's, so that a box row can
+// start and end at a quarter of a cell.
+constexpr uint32_t kSub = 4;
+
 struct QueryParams {
     int kind;
     int32_t dims[3];
@@ -333,7 +346,8 @@ __device__ __forceinline__ void query_position(const QueryParams &q, const GridP
         pz = q.points[3 * (uint64_t)pid + 2];
     }
 }
-// Cell key of every query (ncells outside the domain), identity ids and
+// Sort key of every query (kSub cell + quarter of the cell along x, kSub
+// ncells outside the domain), identity ids and
 // the first sort digit's tile counts.
 hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids,
                              const RadixPass0 &pass0, hipStream_t s);
@@ -373,6 +387,10 @@ struct BackwardBuffers {
     float2 *ab;            // [n] (alpha, beta) per query: plan order (points, voxels) or voxel order (grid)
     float2 *cot;           // [n] (dL/dPhi, dL/dI) packed in query order (points, voxels)
 };
+// Pairs the backward tests (measurement), into *total (device, 8 bytes).
+hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g, const CellBox *box,
+                                      const uint8_t *spans, int64_t n_gauss, const uint32_t *point_off,
+                                      unsigned long long *total, hipStream_t s);
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
                            const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
                            const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,

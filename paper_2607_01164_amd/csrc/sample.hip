@@ -107,10 +107,11 @@ __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams
             float p[3];
             bool valid;
             query_position(q, g, (uint32_t)i, p[0], p[1], p[2], valid);
-            uint32_t key = (uint32_t)g.ncells;
+            uint32_t key = kSub * (uint32_t)g.ncells;
             if (valid) {
                 bool inside = true;
                 int64_t c[3];
+                float tx = 0.0f;
 #pragma unroll
                 for (int j = 0; j < 3; ++j) {
                     inside = inside && (p[j] >= g.lo[j]) && (p[j] <= g.hi[j]);
@@ -119,8 +120,15 @@ __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams
                     ci = ci < 0 ? 0 : ci;
                     ci = ci > g.cells[j] - 1 ? g.cells[j] - 1 : ci;
                     c[j] = ci;
+                    if (j == 0) tx = t;
                 }
-                if (inside) key = (uint32_t)(c[0] + (int64_t)g.cells[0] * (c[1] + (int64_t)g.cells[1] * c[2]));
+                if (inside) {
+                    // the quarter of the cell along x: floor(4 (t - c)), exact
+                    // in float32 (t - c is exact, the product by 4 too)
+                    const float fq = floorf((tx - (float)c[0]) * (float)kSub);
+                    const uint32_t qx = fq < 0.0f ? 0u : (fq > (float)(kSub - 1) ? kSub - 1 : (uint32_t)fq);
+                    key = kSub * (uint32_t)(c[0] + (int64_t)g.cells[0] * (c[1] + (int64_t)g.cells[1] * c[2])) + qx;
+                }
             }
             keys[i] = key;
             ids[i] = (uint32_t)i;
@@ -142,7 +150,8 @@ constexpr uint32_t kRowsMax = (kDenseMin + 3) / 4;  // queries per row at most
 // empty bucket, one for a sparse one, one per 64 queries of a dense one.
 __device__ __forceinline__ uint32_t bucket_items(const uint32_t *point_off, int64_t c, int64_t nbuckets) {
     if (c >= nbuckets) return 0u;
-    const uint32_t n = point_off[c + 1] - point_off[c];
+    // the outside bucket (c = nbuckets - 1) has a single key
+    const uint32_t n = point_off[c + 1 < nbuckets ? kSub * (c + 1) : kSub * c + 1] - point_off[kSub * c];
     return n == 0 ? 0u : (n < kDenseMin ? 1u : (n + kWave - 1) / kWave);
 }
 
@@ -361,7 +370,8 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
     if (w >= total) return;
     const uint32_t c = __builtin_amdgcn_readfirstlane(((ConstU32 *)items)[w]);
     const uint32_t chunk = (uint32_t)w - ((ConstU32 *)item_off)[c];
-    const uint32_t pa = ((ConstU32 *)point_off)[c], pb = ((ConstU32 *)point_off)[c + 1];
+    const uint32_t pa = ((ConstU32 *)point_off)[kSub * c];
+    const uint32_t pb = ((ConstU32 *)point_off)[c < ncells ? kSub * (c + 1) : kSub * c + 1];
     const uint32_t n = pb - pa;
     uint32_t ja = 0, jb = 0;
     if (c < ncells) {

@@ -33,7 +33,7 @@ EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_b
             "gs_backward_work_bytes", "gs_sample_backward", "gs_last_error", "gs_version", "gs_profile_enable",
             "gs_profile_select", "gs_profile_reset", "gs_profile_read", "gs_activate", "gs_activate_backward",
             "gs_loss_work_bytes", "gs_loss", "gs_densify_work_bytes", "gs_densify",
-            "gs_sample_gaussian_major_work_bytes", "gs_sample_gaussian_major")
+            "gs_sample_gaussian_major_work_bytes", "gs_sample_gaussian_major", "gs_backward_pair_count")
 
 
 class GsLibraryMissing(RuntimeError):
@@ -110,6 +110,8 @@ def load_library():
     L.gs_sample_gaussian_major_work_bytes.argtypes = [P(GsQuery)]
     L.gs_sample_gaussian_major.restype = ctypes.c_int
     L.gs_sample_gaussian_major.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, vp, vp, sz, vp, sz, vp]
+    L.gs_backward_pair_count.restype = ctypes.c_int
+    L.gs_backward_pair_count.argtypes = [P(GsIndex), P(GsQuery), vp, sz, vp, sz, P(i64), vp]
     L.gs_backward_work_bytes.restype = sz
     L.gs_backward_work_bytes.argtypes = [P(GsIndex), P(GsQuery)]
     L.gs_sample_backward.restype = ctypes.c_int
@@ -606,6 +608,19 @@ def gs_densify(params_in: ParamSet, n_in: int, weight: torch.Tensor, domain: GsG
         raise GsError(st, load_library().gs_last_error().decode(errors="replace") + f" (kept {n_out.value})")
     _check(st)
     return int(n_out.value)
+
+
+def backward_pair_count(index: Index, query: Query, plan: Optional[torch.Tensor], work: torch.Tensor,
+                        stream=None) -> int:
+    """(Gaussian, query) pairs gs_sample_backward tests, for measurement
+    (waits for the count; overwrites work)."""
+    q = query.c()
+    out = ctypes.c_int64(0)
+    st = load_library().gs_backward_pair_count(ctypes.byref(index.c), ctypes.byref(q), _ptr(plan),
+                                               0 if plan is None else plan.numel(), work.data_ptr(), work.numel(),
+                                               ctypes.byref(out), _stream(stream))
+    _check(st)
+    return int(out.value)
 
 
 def profile_enable(on: bool = True) -> None:

@@ -358,3 +358,33 @@ def test_sum_rules_hold_on_device():
     s2 = float((gi[d].astype(np.float64) * inf[d]).sum())
     assert grads[:, 10].astype(np.float64).sum() == pytest.approx(s1, rel=1e-4, abs=1e-3)
     assert (g.weight.astype(np.float64) * grads[:, 11]).sum() == pytest.approx(s2, rel=1e-4, abs=1e-3)
+
+
+def test_backward_pair_count():
+    """The pairs the backward tests: on a grid exactly the index pairs times
+    the voxels of a cell (trimming works at cell granularity there); for
+    points at most the cell lists times the cells' queries, and at least
+    every contributing pair (the oracle's count), which the quarter cuts of
+    the row ends must never drop."""
+    import paper_2607_01164_amd as gs
+    g = synth.random_gaussians(71, 3000, log_mu=np.log(0.03), log_sd=0.5)
+    log("case backward pair count, grid")
+    r = Run(g, (8, 8, 8), "grid", dims=(32, 32, 32))
+    r.forward()
+    work = gs.alloc_backward_work(r.index, r.query, "cuda")
+    assert gs.backward_pair_count(r.index, r.query, None, work) == r.index.n_pairs * 64
+    log("case backward pair count, points")
+    pts = synth.random_points(72, 40000)
+    r = Run(g, (9, 8, 7), "points", points=pts)
+    r.forward()
+    work = gs.alloc_backward_work(r.index, r.query, "cuda")
+    cnt = gs.backward_pair_count(r.index, r.query, r.plan, work)
+    keys, gids, offs = r.index_arrays()
+    _, _, poff = oracle.point_order(pts, (9, 8, 7))
+    ncells = 9 * 8 * 7
+    per_cell = (poff[4:4 * ncells + 1:4].astype(np.int64) - poff[0:4 * ncells:4])
+    cell_tests = int((np.diff(offs.astype(np.int64)) * per_cell).sum())
+    ref = oracle.forward(g, pts)
+    contrib = int(ref.ncontrib.sum())
+    log(f"  backward tests {cnt}, cell-list tests {cell_tests}, contributing pairs {contrib}")
+    assert contrib <= cnt < cell_tests

@@ -208,13 +208,17 @@ def test_point_order(orc):
     for k in np.unique(keys):
         seg = order[keys == k]
         assert np.all(np.diff(seg.astype(np.int64)) > 0)
-    np.testing.assert_array_equal(offs, np.searchsorted(keys, np.arange(ncells + 2), side="left"))
+    np.testing.assert_array_equal(offs, np.searchsorted(keys, np.arange(4 * ncells + 2), side="left"))
     inside = np.all((pts >= 0) & (pts <= 1), axis=1)
     kp = np.empty(5000, np.int64)
     kp[order] = keys
-    assert np.all(kp[~inside] == ncells)
-    c = np.clip(np.floor(pts[inside].astype(np.float64) * np.array(cells)), 0, np.array(cells) - 1).astype(np.int64)
-    np.testing.assert_array_equal(kp[inside], c[:, 0] + 8 * (c[:, 1] + 4 * c[:, 2]))
+    assert np.all(kp[~inside] == 4 * ncells)
+    # cells per axis are powers of two, so t = p * cells is exact and float64
+    # reproduces both the cell and the quarter of the cell along x
+    t = pts[inside].astype(np.float64) * np.array(cells)
+    c = np.clip(np.floor(t), 0, np.array(cells) - 1).astype(np.int64)
+    qx = np.clip(np.floor(4 * (t[:, 0] - c[:, 0])), 0, 3).astype(np.int64)
+    np.testing.assert_array_equal(kp[inside], 4 * (c[:, 0] + 8 * (c[:, 1] + 4 * c[:, 2])) + qx)
 
 
 def test_voxel_cells_by_integer_division(orc):
@@ -226,4 +230,5 @@ def test_voxel_cells_by_integer_division(orc):
     kp = np.empty(3000, np.int64)
     kp[order] = keys
     x, y, z = ids % 32, (ids // 32) % 16, ids // (32 * 16)
-    np.testing.assert_array_equal(kp, x // 4 + 8 * (y // 4 + 4 * (z // 4)))
+    # four voxels per cell along x: the quarter is the voxel's place in its cell
+    np.testing.assert_array_equal(kp, 4 * (x // 4 + 8 * (y // 4 + 4 * (z // 4))) + x % 4)
