@@ -21,7 +21,9 @@
  *     device memory; the workspaces it needs are passed in, sized by the
  *     *_bytes functions. Workspace pointers must be 256-byte aligned.
  *   - Work is enqueued on the caller's stream and is asynchronous, except that
- *     gs_build_index waits once for the number of Gaussian-cell pairs.
+ *     gs_build_index waits once for the number of Gaussian-cell pairs,
+ *     gs_densify (gs_train.h) once for the new Gaussian count and
+ *     gs_backward_pair_count for its count.
  *   - Errors are reported as gs_status codes; gs_last_error() returns a
  *     message for the calling thread. Nothing throws across this interface.
  *   - Host-side arguments are validated (null pointers, negative counts,
