@@ -43,7 +43,8 @@ EMIT_BYTES_PER_PAIR = 8.0
 COPY_PROBE_BYTES = 256 << 20   # plain copy used to calibrate the HBM byte counters
 SRC_DIR = os.path.join(ROOT, "paper_2607_01164_amd", "csrc")
 WORKLOAD = "c2_grid256_batch"
-INDEX_CELLS = (36, 36, 36)
+INDEX_CELLS = (32, 32, 32)
+TRAIN_CELLS = (40, 40, 40)     # the training step's index: twice C2's query density
 TAU = 0.01
 
 
@@ -57,6 +58,7 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--cells", type=int, nargs=3, default=list(INDEX_CELLS))
+    p.add_argument("--train-cells", type=int, nargs=3, default=list(TRAIN_CELLS))
     p.add_argument("--cpu-seconds", type=float, default=16.0, help="target length of the CPU oracle sample")
     p.add_argument("--no-cpu", action="store_true")
     p.add_argument("--no-train", action="store_true", help="skip the 128^3 structured training-step line")
@@ -149,7 +151,7 @@ class TrainStep:
     CAP = 0.02
     FN_EPS, FN_LAMBDA, FP_LAMBDA = 0.1, 1.0, 0.0
 
-    def __init__(self, st: Step):
+    def __init__(self, st: Step, cells):
         import numpy as np
         import synth
         gs, torch = st.gs, st.torch
@@ -165,7 +167,6 @@ class TrainStep:
         self.offsets = [t(synth.jitter_offsets(st.w.cfg, self.n, it)) for it in range(self.SETS)]
         self.targets = [t(synth.targets(st.w.cfg, self.n, it)) for it in range(self.SETS)]
         self.queries = [gs.Query.jitter(self.DIMS, u) for u in self.offsets]
-        self.plan = gs.alloc_plan(self.queries[0], st.grid, dev)
         self.val = torch.empty(self.n, device=dev)
         self.inf = torch.empty(self.n, device=dev)
         self.gv = torch.empty(self.n, device=dev)
@@ -175,9 +176,14 @@ class TrainStep:
         self.grads = gs.Grads.empty(ng, dev)
         self.raw_grads = gs.RawParams(torch.empty(ng, 3, device=dev), torch.empty(ng, device=dev),
                                       torch.empty(ng, device=dev))
+        self.grid = gs.make_grid(cells)
         self.activate()
-        gs.gs_build_index(self.gauss, st.grid, TAU, st.index)
-        self.work = gs.alloc_backward_work(st.index, self.queries[0], dev)
+        probe = gs.build_index(self.gauss, self.grid, TAU)
+        self.index = gs.Index(self.grid, ng, int(probe.n_pairs * 1.25) + 4096, dev)
+        del probe
+        self.plan = gs.alloc_plan(self.queries[0], self.grid, dev)
+        gs.gs_build_index(self.gauss, self.grid, TAU, self.index)
+        self.work = gs.alloc_backward_work(self.index, self.queries[0], dev)
         self.it = 0
         torch.cuda.synchronize()
 
@@ -201,7 +207,7 @@ class TrainStep:
         tgt = self.targets[(self.it - 1) % self.SETS]
 
         def call():
-            return gs.gs_densify(cur, ng, self.gauss.weight, st.grid, q, self.val, self.inf, tgt, None, 0.005, TAU,
+            return gs.gs_densify(cur, ng, self.gauss.weight, self.grid, q, self.val, self.inf, tgt, None, 0.005, TAU,
                                  math.log(0.005), math.log(0.01 / 0.99), kmax, out, src, work)
 
         n_out = call()
@@ -222,11 +228,11 @@ class TrainStep:
         gs, st = self.gs, self.st
         q = self.queries[self.it % self.SETS]
         self.activate()
-        gs.gs_build_index(self.gauss, st.grid, TAU, st.index)
-        gs.gs_sample(self.gauss, st.index, q, self.val, self.inf, self.plan)
+        gs.gs_build_index(self.gauss, self.grid, TAU, self.index)
+        gs.gs_sample(self.gauss, self.index, q, self.val, self.inf, self.plan)
         gs.gs_loss(self.val, self.inf, self.targets[self.it % self.SETS], None, TAU, self.FN_EPS, self.FN_LAMBDA,
                    self.FP_LAMBDA, self.gv, self.gi, self.terms, self.loss_work)
-        gs.gs_sample_backward(self.gauss, st.index, q, self.plan, self.val, self.inf, self.gv, self.gi, self.grads,
+        gs.gs_sample_backward(self.gauss, self.index, q, self.plan, self.val, self.inf, self.gv, self.gi, self.grads,
                               self.work)
         gs.gs_activate_backward(self.raw, self.CAP, self.grads, self.raw_grads)
         self.it += 1
@@ -380,7 +386,7 @@ def main():
     t_build = timed(st.build, a.steps, sync)
     train = None
     if not a.no_train:
-        ts = TrainStep(st)
+        ts = TrainStep(st, tuple(a.train_cells))
         for _ in range(a.warmup):
             ts.step()
         sync()
@@ -396,7 +402,8 @@ def main():
         terms = gs.read_loss_terms(ts.terms)
         dens = ts.densify_bench(a.steps)
         train = {"workload": "structured training step: free parameters of the 262144 Gaussians -> activations "
-                             "(soft norm cap 0.02) -> index -> 128^3 jittered samples (one random position per "
+                             f"(soft norm cap 0.02) -> index ({'x'.join(map(str, a.train_cells))} cells) -> 128^3 "
+                             "jittered samples (one random position per "
                              f"voxel, offsets and targets redrawn each step from {TrainStep.SETS} sets resident in "
                              "HBM) -> forward -> L1 + false-negative losses -> backward -> activation backward",
                  "samples_per_step": ts.n, "ms_per_step": t_ts * 1e3, "fwd_bwd_samples_per_s": ts.n / t_ts,
