@@ -389,7 +389,48 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
             if ((int64_t)pid < q.n) query_position(q, g, pid, px, py, pz, valid);
         }
         float I = 0.0f, V = 0.0f;
-        walk_uniform(rec, gids, ja, jb, px, py, pz, T, I, V);
+        // the list is staged in the wave's LDS planes 64 records at a time,
+        // as for the row layouts, and every lane reads each record there with
+        // the same address (a broadcast): one wait for memory per 64
+        // candidates instead of a dependent id and record load per candidate
+        float4 *buf = s_rec[threadIdx.x / kWave];
+        uint32_t gnext = 0;
+        if (ja < jb) gnext = gids[ja + lane < jb ? ja + lane : jb - 1];
+        for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
+            const float4 *src = (const float4 *)(rec + gnext);
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq)
+                __builtin_amdgcn_global_load_lds((const void *)(src + qq),
+                                                 (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
+            if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
+            __builtin_amdgcn_s_waitcnt(0);
+            __builtin_amdgcn_wave_barrier();
+            const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
+            uint32_t s = 0;
+            for (; s + 2 <= cnt; s += 2) {
+                Record a, b;
+                a.r0 = buf[s];
+                a.r1 = buf[kWave + s];
+                a.r2 = buf[2 * kWave + s];
+                a.r3 = buf[3 * kWave + s];
+                b.r0 = buf[s + 1];
+                b.r1 = buf[kWave + s + 1];
+                b.r2 = buf[2 * kWave + s + 1];
+                b.r3 = buf[3 * kWave + s + 1];
+                accumulate(a, px, py, pz, T, I, V);
+                accumulate(b, px, py, pz, T, I, V);
+            }
+            if (s < cnt) {
+                Record a;
+                a.r0 = buf[s];
+                a.r1 = buf[kWave + s];
+                a.r2 = buf[2 * kWave + s];
+                a.r3 = buf[3 * kWave + s];
+                accumulate(a, px, py, pz, T, I, V);
+            }
+            // every lane has read the planes before the next chunk overwrites them
+            __builtin_amdgcn_wave_barrier();
+        }
         if (active && (int64_t)pid < q.n)
             write_out(I, V, tau, valid && c < ncells, pid, k, px, py, pz, out_v, out_i, pr);
         return;
