@@ -38,24 +38,52 @@ __device__ __forceinline__ void accumulate(const Record &r, float px, float py, 
     }
 }
 
-// Walk a wave-uniform list [j0, j1): list entries and records through the
-// scalar path.
-__device__ __forceinline__ void walk_uniform(const Record *rec, const uint32_t *gids, uint32_t j0, uint32_t j1,
-                                             float px, float py, float pz, float T, float &I, float &V) {
-    ConstU32 *cg = (ConstU32 *)gids;
-    uint32_t j = j0;
-    for (; j + 2 <= j1; j += 2) {
-        const uint32_t g0 = __builtin_amdgcn_readfirstlane(cg[j]);
-        const uint32_t g1 = __builtin_amdgcn_readfirstlane(cg[j + 1]);
-        const Record a = load_record_uniform(rec, g0);
-        const Record b = load_record_uniform(rec, g1);
-        accumulate(a, px, py, pz, T, I, V);
-        accumulate(b, px, py, pz, T, I, V);
-    }
-    if (j < j1) {
-        const uint32_t g0 = __builtin_amdgcn_readfirstlane(cg[j]);
-        const Record a = load_record_uniform(rec, g0);
-        accumulate(a, px, py, pz, T, I, V);
+// Walk a wave-uniform candidate list [ja, jb) for one query per lane. The
+// list is staged in the wave's LDS planes (buf: 4 planes of kWave float4) 64
+// records at a time: lane l copies candidate c0 + l's record from memory
+// straight into LDS (lanes past the list copy its last record), the ids of
+// the next 64 are fetched meanwhile, and every lane then reads each record
+// with the same address (a broadcast). One wait for memory per 64
+// candidates, instead of a dependent id and record load per candidate.
+__device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
+                                            uint32_t ja, uint32_t jb, uint32_t lane, float4 *buf, float px,
+                                            float py, float pz, float T, float &I, float &V) {
+    uint32_t gnext = 0;
+    if (ja < jb) gnext = gids[ja + lane < jb ? ja + lane : jb - 1];
+    for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
+        const float4 *src = (const float4 *)(rec + gnext);
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq)
+            __builtin_amdgcn_global_load_lds((const void *)(src + qq),
+                                             (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
+        if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_wave_barrier();
+        const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
+        uint32_t s = 0;
+        for (; s + 2 <= cnt; s += 2) {
+            Record a, b;
+            a.r0 = buf[s];
+            a.r1 = buf[kWave + s];
+            a.r2 = buf[2 * kWave + s];
+            a.r3 = buf[3 * kWave + s];
+            b.r0 = buf[s + 1];
+            b.r1 = buf[kWave + s + 1];
+            b.r2 = buf[2 * kWave + s + 1];
+            b.r3 = buf[3 * kWave + s + 1];
+            accumulate(a, px, py, pz, T, I, V);
+            accumulate(b, px, py, pz, T, I, V);
+        }
+        if (s < cnt) {
+            Record a;
+            a.r0 = buf[s];
+            a.r1 = buf[kWave + s];
+            a.r2 = buf[2 * kWave + s];
+            a.r3 = buf[3 * kWave + s];
+            accumulate(a, px, py, pz, T, I, V);
+        }
+        // every lane has read the planes before the next chunk overwrites them
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -64,6 +92,7 @@ __global__ __launch_bounds__(kBlock) void k_sample_grid(QueryParams q, GridParam
                                                         const uint32_t *__restrict__ gids,
                                                         const uint32_t *__restrict__ cell_off, float T, float tau,
                                                         float *__restrict__ out_v, float *__restrict__ out_i) {
+    __shared__ float4 s_grec[kWavesPerBlock][4 * kWave];
     const uint32_t rx = (uint32_t)(q.dims[0] / g.cells[0]);
     const uint32_t ry = (uint32_t)(q.dims[1] / g.cells[1]);
     const uint32_t rz = (uint32_t)(q.dims[2] / g.cells[2]);
@@ -87,7 +116,7 @@ __global__ __launch_bounds__(kBlock) void k_sample_grid(QueryParams q, GridParam
     const uint32_t j0 = __builtin_amdgcn_readfirstlane(cell_off[cell]);
     const uint32_t j1 = __builtin_amdgcn_readfirstlane(cell_off[cell + 1]);
     float I = 0.0f, V = 0.0f;
-    walk_uniform(rec, gids, j0, j1, px, py, pz, T, I, V);
+    walk_staged(rec, gids, j0, j1, lane, s_grec[threadIdx.x / kWave], px, py, pz, T, I, V);
     if (local < vpc) {
         const uint64_t idx = (uint64_t)vx + (uint64_t)q.dims[0] * ((uint64_t)vy + (uint64_t)q.dims[1] * (uint64_t)vz);
         const bool def = I > tau;
@@ -389,48 +418,7 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
             if ((int64_t)pid < q.n) query_position(q, g, pid, px, py, pz, valid);
         }
         float I = 0.0f, V = 0.0f;
-        // the list is staged in the wave's LDS planes 64 records at a time,
-        // as for the row layouts, and every lane reads each record there with
-        // the same address (a broadcast): one wait for memory per 64
-        // candidates instead of a dependent id and record load per candidate
-        float4 *buf = s_rec[threadIdx.x / kWave];
-        uint32_t gnext = 0;
-        if (ja < jb) gnext = gids[ja + lane < jb ? ja + lane : jb - 1];
-        for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
-            const float4 *src = (const float4 *)(rec + gnext);
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq)
-                __builtin_amdgcn_global_load_lds((const void *)(src + qq),
-                                                 (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
-            if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
-            __builtin_amdgcn_s_waitcnt(0);
-            __builtin_amdgcn_wave_barrier();
-            const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
-            uint32_t s = 0;
-            for (; s + 2 <= cnt; s += 2) {
-                Record a, b;
-                a.r0 = buf[s];
-                a.r1 = buf[kWave + s];
-                a.r2 = buf[2 * kWave + s];
-                a.r3 = buf[3 * kWave + s];
-                b.r0 = buf[s + 1];
-                b.r1 = buf[kWave + s + 1];
-                b.r2 = buf[2 * kWave + s + 1];
-                b.r3 = buf[3 * kWave + s + 1];
-                accumulate(a, px, py, pz, T, I, V);
-                accumulate(b, px, py, pz, T, I, V);
-            }
-            if (s < cnt) {
-                Record a;
-                a.r0 = buf[s];
-                a.r1 = buf[kWave + s];
-                a.r2 = buf[2 * kWave + s];
-                a.r3 = buf[3 * kWave + s];
-                accumulate(a, px, py, pz, T, I, V);
-            }
-            // every lane has read the planes before the next chunk overwrites them
-            __builtin_amdgcn_wave_barrier();
-        }
+        walk_staged(rec, gids, ja, jb, lane, s_rec[threadIdx.x / kWave], px, py, pz, T, I, V);
         if (active && (int64_t)pid < q.n)
             write_out(I, V, tau, valid && c < ncells, pid, k, px, py, pz, out_v, out_i, pr);
         return;
