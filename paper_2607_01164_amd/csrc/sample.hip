@@ -38,6 +38,29 @@ __device__ __forceinline__ void accumulate(const Record &r, float px, float py, 
     }
 }
 
+// Walk a wave-uniform candidate list [j0, j1) for one query per lane, ids
+// and records through the scalar cache, two candidates at a time. The work
+// items of a cell with many queries walk the same list at about the same
+// time on one compute unit and share its records in that cache.
+__device__ __forceinline__ void walk_scalar(const Record *rec, const uint32_t *gids, uint32_t j0, uint32_t j1,
+                                            float px, float py, float pz, float T, float &I, float &V) {
+    ConstU32 *cg = (ConstU32 *)gids;
+    uint32_t j = j0;
+    for (; j + 2 <= j1; j += 2) {
+        const uint32_t g0 = __builtin_amdgcn_readfirstlane(cg[j]);
+        const uint32_t g1 = __builtin_amdgcn_readfirstlane(cg[j + 1]);
+        const Record a = load_record_uniform(rec, g0);
+        const Record b = load_record_uniform(rec, g1);
+        accumulate(a, px, py, pz, T, I, V);
+        accumulate(b, px, py, pz, T, I, V);
+    }
+    if (j < j1) {
+        const uint32_t g0 = __builtin_amdgcn_readfirstlane(cg[j]);
+        const Record a = load_record_uniform(rec, g0);
+        accumulate(a, px, py, pz, T, I, V);
+    }
+}
+
 // Walk a wave-uniform candidate list [ja, jb) for one query per lane. The
 // list is staged in the wave's LDS planes (buf: 4 planes of kWave float4) 64
 // records at a time: lane l copies candidate c0 + l's record from memory
@@ -171,6 +194,10 @@ __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams
 // kDenseMin queries, one per 64 queries of a denser cell. The bucket of
 // queries outside the domain (key ncells) is an item with an empty list.
 constexpr uint32_t kDenseMin = 32;
+// From this many queries (five work items of 64) a cell's items walk its
+// candidates through the scalar cache, where the items share the records;
+// fewer items stage the records in LDS instead.
+constexpr uint32_t kScalarWalkMin = 320;
 constexpr uint32_t kChunkB = 8;  // queries evaluated together by a sparse-cell item
 constexpr uint32_t kRowsMin = 4;                 // from this many queries a cell uses 4 query rows
 constexpr uint32_t kRowsMax = (kDenseMin + 3) / 4;  // queries per row at most
@@ -418,7 +445,10 @@ __global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridPara
             if ((int64_t)pid < q.n) query_position(q, g, pid, px, py, pz, valid);
         }
         float I = 0.0f, V = 0.0f;
-        walk_staged(rec, gids, ja, jb, lane, s_rec[threadIdx.x / kWave], px, py, pz, T, I, V);
+        if (n >= kScalarWalkMin)
+            walk_scalar(rec, gids, ja, jb, px, py, pz, T, I, V);
+        else
+            walk_staged(rec, gids, ja, jb, lane, s_rec[threadIdx.x / kWave], px, py, pz, T, I, V);
         if (active && (int64_t)pid < q.n)
             write_out(I, V, tau, valid && c < ncells, pid, k, px, py, pz, out_v, out_i, pr);
         return;
