@@ -3,14 +3,14 @@
 //
 // Grid queries (Sec. 4.1.3, Fig. 4 C): one wavefront per (cell, 64 voxels of
 // the cell); every lane is a voxel and all lanes walk the cell's Gaussian
-// list together, so the list entries and the 64-byte Gaussian records are
-// wave-uniform and come through scalar loads into SGPRs rather than through
-// shared-memory batches.
+// list together. The 64-byte Gaussian records are staged in the wave's LDS
+// planes 64 at a time (the paper's shared-memory batches) and read there
+// with one address for all lanes.
 //
 // Voxel-list and point queries (Sec. 5.1.2): the queries are first ordered
 // by cell (query_keys + radix sort, kept in the plan) and the work is split
-// by cell: dense cells run like grid cells, sparse cells put the cell's
-// candidate Gaussians in the lanes instead (see k_sample_cells).
+// by cell: dense cells run like grid cells, cells of fewer queries spread
+// queries and candidates over the lanes (see k_sample_cells).
 #include "expand.h"
 #include "internal.h"
 #include "radix.h"
@@ -400,7 +400,8 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
 
 // One wavefront per item, by the queries n of the cell:
 //  * n >= 64: lanes are queries (64 per item) and walk the list together,
-//    records through the scalar path;
+//    records staged in LDS below kScalarWalkMin queries, through the scalar
+//    cache from there (the cell's items then share them);
 //  * 4 <= n < 64: query rows x candidate slots (4 x 16 below 32 queries,
 //    8 x 8 from 32), records staged in LDS 64 at a time;
 //  * n < 4: lanes are the cell's candidates (64 at a time) and the queries
