@@ -427,10 +427,31 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
                                 y * dR[1][2] + x * dR[2][0] + y * dR[2][1]);
                 double dot = w * dqh[0] + x * dqh[1] + y * dqh[2] + z * dqh[3];
                 for (int k = 0; k < 4; k++) term[6 + k] = (dqh[k] - g.qhat[k] * dot) / g.qnorm;
+                /* the size of the quaternion terms before they cancel: each
+                 * component is a signed sum of dL/dR entries (exactly zero
+                 * for a spherical Gaussian), so float arithmetic rounds it at
+                 * the size of those entries, not at its own */
+                const double aw = fabs(w), ax = fabs(x), ay = fabs(y), az = fabs(z);
+                double A_[3][3];
+                for (int j = 0; j < 3; j++)
+                    for (int k = 0; k < 3; k++) A_[j][k] = fabs(dR[j][k]);
+                double mq[4];
+                mq[0] = 2.0 * (az * A_[0][1] + ay * A_[0][2] + az * A_[1][0] + ax * A_[1][2] + ay * A_[2][0] +
+                               ax * A_[2][1]);
+                mq[1] = 2.0 * (ay * A_[0][1] + az * A_[0][2] + ay * A_[1][0] + 2.0 * ax * A_[1][1] + aw * A_[1][2] +
+                               az * A_[2][0] + aw * A_[2][1] + 2.0 * ax * A_[2][2]);
+                mq[2] = 2.0 * (2.0 * ay * A_[0][0] + ax * A_[0][1] + aw * A_[0][2] + ax * A_[1][0] + az * A_[1][2] +
+                               aw * A_[2][0] + az * A_[2][1] + 2.0 * ay * A_[2][2]);
+                mq[3] = 2.0 * (2.0 * az * A_[0][0] + aw * A_[0][1] + ax * A_[0][2] + aw * A_[1][0] +
+                               2.0 * az * A_[1][1] + ay * A_[1][2] + ax * A_[2][0] + ay * A_[2][1]);
+                const double mdot = aw * mq[0] + ax * mq[1] + ay * mq[2] + az * mq[3];
+                double mag[10];
+                for (int k = 0; k < 6; k++) mag[k] = fabs(term[k]);
+                for (int k = 0; k < 4; k++) mag[6 + k] = (mq[k] + fabs(g.qhat[k]) * mdot) / g.qnorm;
                 const double dLdQv = -0.5 * a * dLda, dLdQm = 0.5 * a * dLdaMag;
                 for (int k = 0; k < 10; k++) {
                     acc[k] += term[k] * dLdQv;
-                    aab[k] += fabs(term[k]) * dLdQm;
+                    aab[k] += mag[k] * dLdQm;
                 }
                 term[10] = gP * a / I;
                 acc[10] += term[10];

@@ -258,3 +258,17 @@ def test_rebuilt_index_matches_oracle():
     np.testing.assert_array_equal(idx.keys[:P].cpu().numpy().view(np.uint32), rk)
     np.testing.assert_array_equal(idx.gids[:P].cpu().numpy().view(np.uint32), rg)
     np.testing.assert_array_equal(idx.cell_offsets.cpu().numpy().view(np.uint32), ro)
+    # the next iteration samples the densified set: forward and backward on
+    # new jittered positions, against the oracle
+    from harness import Run, check_backward, check_forward, masked_cotangents
+    u2 = synth.jitter_offsets(0, nq, iteration=12)
+    log("  next iteration on the densified set")
+    r = Run(host_g, w_.index_cells, "jitter", dims=dims, offsets=u2)
+    phi2, inf2 = r.forward()
+    ref2, _ = check_forward(r, phi2, inf2, label="forward after densification")
+    gv, gi = synth.random_normal(13, nq), synth.random_normal(14, nq)
+    gv, gi, _ = masked_cotangents(ref2, gv, gi)
+    grads = r.backward(gv, gi)
+    sel = np.random.default_rng(15).choice(n, size=min(n, 400), replace=False)
+    sel = np.unique(np.concatenate([sel, np.arange(kept, n)[:200]]))  # new Gaussians among them
+    check_backward(r, grads, sel, np.arange(nq), gv, gi, label="backward after densification")
