@@ -432,9 +432,17 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
                  * for a spherical Gaussian), so float arithmetic rounds it at
                  * the size of those entries, not at its own */
                 const double aw = fabs(w), ax = fabs(x), ay = fabs(y), az = fabs(z);
+                /* u_k itself is a sum of three products R_jk d_j / s_k, which
+                 * cancel for points near a principal plane: U_k is the size
+                 * at which any evaluation rounds it */
+                double U[3];
+                for (int k = 0; k < 3; k++) {
+                    U[k] = 0.0;
+                    for (int j = 0; j < 3; j++) U[k] += fabs(g.R[j][k] * d[j]) / g.s[k];
+                }
                 double A_[3][3];
                 for (int j = 0; j < 3; j++)
-                    for (int k = 0; k < 3; k++) A_[j][k] = fabs(dR[j][k]);
+                    for (int k = 0; k < 3; k++) A_[j][k] = 2.0 * U[k] * fabs(d[j]) / g.s[k];
                 double mq[4];
                 mq[0] = 2.0 * (az * A_[0][1] + ay * A_[0][2] + az * A_[1][0] + ax * A_[1][2] + ay * A_[2][0] +
                                ax * A_[2][1]);
@@ -446,7 +454,16 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
                                2.0 * az * A_[1][1] + ay * A_[1][2] + ax * A_[2][0] + ay * A_[2][1]);
                 const double mdot = aw * mq[0] + ax * mq[1] + ay * mq[2] + az * mq[3];
                 double mag[10];
-                for (int k = 0; k < 6; k++) mag[k] = fabs(term[k]);
+                /* the mean terms -2 (M^T u)_j likewise: three products that
+                 * cancel where d lies along a principal direction of the
+                 * covariance (at the ellipsoid's axis-extreme points); the
+                 * scale terms -2 u_k^2 / s_k at the size of u_k's parts */
+                for (int j = 0; j < 3; j++) {
+                    double m = 0.0;
+                    for (int k = 0; k < 3; k++) m += 2.0 * U[k] * fabs(g.R[j][k]) / g.s[k];
+                    mag[j] = m;
+                }
+                for (int k = 0; k < 3; k++) mag[3 + k] = 2.0 * U[k] * U[k] / g.s[k];
                 for (int k = 0; k < 4; k++) mag[6 + k] = (mq[k] + fabs(g.qhat[k]) * mdot) / g.qnorm;
                 const double dLdQv = -0.5 * a * dLda, dLdQm = 0.5 * a * dLdaMag;
                 for (int k = 0; k < 10; k++) {

@@ -388,3 +388,34 @@ def test_backward_pair_count():
     contrib = int(ref.ncontrib.sum())
     log(f"  backward tests {cnt}, cell-list tests {cell_tests}, contributing pairs {contrib}")
     assert contrib <= cnt < cell_tests
+
+
+def test_backward_quarter_cuts_keep_extreme_points():
+    """Points just inside every ellipsoid's x-extremes, d = Sigma e_x
+    sqrt(T / Sigma_xx) (1 - 1e-5): the backward cuts a box row to the
+    quarters of its end cells that the row's bound reaches, and such points
+    sit in those end quarters. Each pair must still be found (the gradients
+    against the oracle) and counted."""
+    import paper_2607_01164_amd as gs
+    g = synth.random_gaussians(81, 1500, log_mu=np.log(0.02), log_sd=0.6, lo=0.1, hi=0.9)
+    q = g.rot.astype(np.float64)
+    q /= np.linalg.norm(q, axis=1, keepdims=True)
+    w_, x, y, z = q.T
+    R = np.stack([np.stack([1 - 2 * (y * y + z * z), 2 * (x * y - w_ * z), 2 * (x * z + w_ * y)], -1),
+                  np.stack([2 * (x * y + w_ * z), 1 - 2 * (x * x + z * z), 2 * (y * z - w_ * x)], -1),
+                  np.stack([2 * (x * z - w_ * y), 2 * (y * z + w_ * x), 1 - 2 * (x * x + y * y)], -1)], 1)
+    S2 = g.scale.astype(np.float64) ** 2
+    Sig = np.einsum("nij,nj,nkj->nik", R, S2, R)
+    T = 2.0 * np.log(1.0 / float(np.float32(TAU)))
+    d = Sig[:, :, 0] * np.sqrt(T / Sig[:, 0, 0])[:, None] * (1.0 - 1e-5)
+    pts = np.concatenate([g.mean + d, g.mean - d]).astype(np.float32)
+    log(f"case backward at the ellipsoids' x-extremes, {len(pts)} points")
+    r = Run(g, (12, 10, 9), "points", points=pts)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="x-extremes")
+    gv, gi = synth.random_normal(82, r.nq), synth.random_normal(83, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="x-extremes")
+    work = gs.alloc_backward_work(r.index, r.query, "cuda")
+    assert gs.backward_pair_count(r.index, r.query, r.plan, work) >= int(ref.ncontrib.sum())
