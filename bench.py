@@ -65,6 +65,7 @@ def parse():
     p.add_argument("--no-ab", action="store_true", help="skip the point-major / Gaussian-major comparison")
     p.add_argument("--ab-c5", action="store_true",
                    help="also compare the two forwards on the 10^8-point cloud (slow to generate)")
+    p.add_argument("--no-configs", action="store_true", help="skip the C1, C3 and C4 lines")
     p.add_argument("--breakdown", action="store_true", help="print the per-kernel table to stderr")
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, run a plain 256 MiB copy (counter calibration under rocprofv3)")
@@ -300,6 +301,81 @@ class ABStep:
         return out
 
 
+class ConfigStep:
+    """One of the other workloads at its own configuration (index cells,
+    queries), with the same calls as the headline step: index build,
+    forward, and the backward where the workload has one. Inputs resident
+    in HBM; each part timed over k calls."""
+
+    def __init__(self, name):
+        import numpy as np
+        import torch
+
+        import paper_2607_01164_amd as gs
+        import synth
+        self.gs, self.torch = gs, torch
+        w = synth.WORKLOADS[name]
+        self.w = w
+        g = synth.make_gaussians(w)
+        dev = "cuda:0"
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+        self.dg = gs.Gaussians(t(g.mean), t(g.scale), t(g.rot), t(g.value), t(g.weight))
+        self.grid = gs.make_grid(w.index_cells)
+        if w.kind == "grid":
+            self.query = gs.Query.grid(w.dims)
+            self.plan = None
+        else:
+            pts = synth.make_points(w)
+            if 0 < w.batch < len(pts):
+                pts = pts[synth.batch_permutation(w, len(pts))[: w.batch]]
+            self.pts = t(pts)
+            del pts
+            self.query = gs.Query.pts(self.pts)
+            self.plan = gs.alloc_plan(self.query, self.grid, dev)
+        self.n = self.query.size()
+        probe = gs.build_index(self.dg, self.grid, TAU)
+        self.index = gs.Index(self.grid, g.n, int(probe.n_pairs * 1.25) + 4096, dev)
+        del probe
+        gs.gs_build_index(self.dg, self.grid, TAU, self.index)
+        self.val = torch.empty(self.n, device=dev)
+        self.inf = torch.empty(self.n, device=dev)
+        self.has_bwd = w.backward
+        if self.has_bwd:
+            gv, gi = synth.cotangents(w, self.n)
+            self.gv, self.gi = t(gv), t(gi)
+            self.grads = gs.Grads.empty(g.n, dev)
+            self.work = gs.alloc_backward_work(self.index, self.query, dev)
+        torch.cuda.synchronize()
+
+    def build(self):
+        self.gs.gs_build_index(self.dg, self.grid, TAU, self.index)
+
+    def forward(self):
+        self.gs.gs_sample(self.dg, self.index, self.query, self.val, self.inf, self.plan)
+
+    def backward(self):
+        self.gs.gs_sample_backward(self.dg, self.index, self.query, self.plan, self.val, self.inf, self.gv, self.gi,
+                                   self.grads, self.work)
+
+    def run(self, k):
+        sync = self.torch.cuda.synchronize
+        self.build()
+        self.forward()
+        if self.has_bwd:
+            self.backward()
+        sync()
+        tb, tf = timed(self.build, k, sync), timed(self.forward, k, sync)
+        out = {"workload": self.w.description, "queries": self.n, "index_cells": list(self.w.index_cells),
+               "index_pairs": self.index.n_pairs, "ms_build": tb * 1e3, "ms_fwd": tf * 1e3,
+               "fwd_points_per_s": self.n / tf}
+        if self.has_bwd:
+            self.forward()
+            tw = timed(self.backward, k, sync)
+            out.update({"ms_bwd": tw * 1e3, "fwd_bwd_samples_per_s": self.n / (tb + tf + tw),
+                        "fwd_bwd_samples_per_s_excl_build": self.n / (tf + tw)})
+        return out
+
+
 def timed(fn, k, sync):
     sync()
     t0 = time.perf_counter()
@@ -411,6 +487,14 @@ def main():
                  "densify": dens}
         del ts
 
+    configs = None
+    if not a.no_configs:
+        configs = {}
+        for name in ("c1_grid32", "c3_grid512_full", "c4_points8m") + (("c5_points100m",) if a.ab_c5 else ()):
+            cs = ConfigStep(name)
+            configs[name] = cs.run(3 if cs.n > 5e7 else max(5, a.steps // 5))
+            del cs
+            torch.cuda.empty_cache()
     ab = None
     if not a.no_ab:
         ab = {"c4": ABStep("c4_points8m", True).run(max(3, a.steps // 5))}
@@ -451,6 +535,7 @@ def main():
         "kernels": {k: round(v["ms_per_step"] * 1e3, 2) for k, v in kernels.items()},
         "training_step": train,
         "forward_ab": ab,
+        "configs": configs,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
