@@ -217,8 +217,10 @@ __device__ __forceinline__ void drain(const Record &r, const float4 *qu, const u
     }
 }
 
-// Gaussians per wavefront: consecutive Gaussians of gorder share a wave.
+// Gaussians per wavefront: consecutive Gaussians of gorder share a wave;
+// below kPackMinGauss Gaussians one per wave (4 would leave SIMDs idle).
 constexpr uint32_t kPack = 4;
+constexpr int64_t kPackMinGauss = 65536;
 
 // Partials of the wave's current Gaussian are reduced over the wave and
 // stored: lane k < 12 writes moment k (the 12th is 0).
@@ -243,7 +245,7 @@ __device__ __forceinline__ void acc_zero(Acc &acc) {
     acc.dv = acc.dw = 0.0f;
 }
 
-// kPack consecutive Gaussians of gorder per wavefront. The points of a box
+// PACK consecutive Gaussians of gorder per wavefront. The points of a box
 // come as rows: a run of cells along x at fixed (y, z) is contiguous in the
 // plan's cell ordering (for grids, a run of voxels is contiguous in the
 // x-fastest layout). The rows of the wave's Gaussians are listed one
@@ -258,7 +260,7 @@ __device__ __forceinline__ void acc_zero(Acc &acc) {
 // queued pairs are processed with all lanes busy. Gaussians are visited in
 // the spatial order of the index (the cell key of their box corner), so the
 // waves resident at one time work on one region and find its points in L2.
-template <bool GRID>
+template <bool GRID, uint32_t PACK>
 __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                            const CellBox *__restrict__ box,
                                                            const uint8_t *__restrict__ spans,
@@ -272,9 +274,9 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t wib = threadIdx.x / kWave;
     const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + wib;
-    const uint64_t first = w * kPack;
+    const uint64_t first = w * PACK;
     if (first >= (uint64_t)n_gauss) return;
-    const uint32_t nk = (uint64_t)n_gauss - first < kPack ? (uint32_t)((uint64_t)n_gauss - first) : kPack;
+    const uint32_t nk = (uint64_t)n_gauss - first < PACK ? (uint32_t)((uint64_t)n_gauss - first) : PACK;
     float4 *qu = s_qu[wib];
     uint32_t *qk = s_qk[wib];
     uint32_t rx = 1, ry = 1, rz = 1;
@@ -319,7 +321,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
     Acc acc;
     acc_zero(acc);
     uint32_t head = 0, cnt = 0;
-    uint32_t cur = kPack, cur_gid = 0;  // the Gaussian being walked (none yet)
+    uint32_t cur = PACK, cur_gid = 0;  // the Gaussian being walked (none yet)
     for (uint32_t rb = 0; rb < Rw; rb += kWave) {
         // lane l describes row rb + l of the wave's list: its Gaussian i is
         // the number of Gaussians whose rows end at or before it
@@ -387,7 +389,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
             const uint32_t gend = __builtin_amdgcn_readlane(mRend, gi), gR = __builtin_amdgcn_readlane(mR, gi);
             if (gR == 0) continue;  // no rows: its moments are written above
             if (gi != cur) {
-                if (cur < kPack) finish_gauss(r, qu, qk, head, cnt, lane, ab, acc, cur_gid, moments);
+                if (cur < PACK) finish_gauss(r, qu, qk, head, cnt, lane, ab, acc, cur_gid, moments);
                 head = cnt = 0;
                 acc_zero(acc);
                 cur = gi;
@@ -462,7 +464,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
             }
         }
     }
-    if (cur < kPack) finish_gauss(r, qu, qk, head, cnt, lane, ab, acc, cur_gid, moments);
+    if (cur < PACK) finish_gauss(r, qu, qk, head, cnt, lane, ab, acc, cur_gid, moments);
 }
 
 __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ moments, int64_t n,
@@ -632,15 +634,22 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
         }
         prof_end("bwd_stage", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        const uint32_t wblocks =
-            (uint32_t)((n_gauss + (int64_t)kPack * kWavesPerBlock - 1) / ((int64_t)kPack * kWavesPerBlock));
+        // few Gaussians: one per wave, so that they still fill the chip
+        const int64_t pack = n_gauss < kPackMinGauss ? 1 : kPack;
+        const uint32_t wblocks = (uint32_t)((n_gauss + pack * kWavesPerBlock - 1) / (pack * kWavesPerBlock));
         prof_begin("bwd_gauss", s);
-        if (grid)
-            hipLaunchKernelGGL(k_backward_gauss<true>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans, gorder,
-                               n_gauss, point_off, plan_pos, b.ab, T, b.moments);
+        if (grid && pack == 1)
+            hipLaunchKernelGGL((k_backward_gauss<true, 1>), dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans,
+                               gorder, n_gauss, point_off, plan_pos, b.ab, T, b.moments);
+        else if (grid)
+            hipLaunchKernelGGL((k_backward_gauss<true, kPack>), dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box,
+                               spans, gorder, n_gauss, point_off, plan_pos, b.ab, T, b.moments);
+        else if (pack == 1)
+            hipLaunchKernelGGL((k_backward_gauss<false, 1>), dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans,
+                               gorder, n_gauss, point_off, plan_pos, b.ab, T, b.moments);
         else
-            hipLaunchKernelGGL(k_backward_gauss<false>, dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans, gorder,
-                               n_gauss, point_off, plan_pos, b.ab, T, b.moments);
+            hipLaunchKernelGGL((k_backward_gauss<false, kPack>), dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box,
+                               spans, gorder, n_gauss, point_off, plan_pos, b.ab, T, b.moments);
         prof_end("bwd_gauss", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
