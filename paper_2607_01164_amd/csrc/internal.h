@@ -130,19 +130,10 @@ __device__ __forceinline__ float readlane_f(float x, uint32_t l) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), (int)l));
 }
 
-// Wave-uniform sum and maximum of a 32-bit value (every lane must be active):
-// DPP within each row of 16 lanes, then the four row results by readlane.
-__device__ __forceinline__ uint32_t wave_sum_uniform(uint32_t x) {
-    x += dpp_u<0xB1>(x);
-    x += dpp_u<0x4E>(x);
-    x += dpp_u<0x124>(x);
-    x += dpp_u<0x128>(x);
-    return (__builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16)) +
-           (__builtin_amdgcn_readlane(x, 32) + __builtin_amdgcn_readlane(x, 48));
-}
-
 __device__ __forceinline__ uint32_t umax_(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
+// Wave-uniform maximum of a 32-bit value (every lane must be active): DPP
+// within each row of 16 lanes, then the four row results by readlane.
 __device__ __forceinline__ uint32_t wave_max_uniform(uint32_t x) {
     x = umax_(x, dpp_u<0xB1>(x));
     x = umax_(x, dpp_u<0x4E>(x));
