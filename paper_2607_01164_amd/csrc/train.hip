@@ -114,22 +114,38 @@ __device__ __forceinline__ T wave_sum_xor(T x) {
     return x;
 }
 
-// Sum over a block of NT threads in a fixed order (wave trees, then the
-// waves' sums in wave order by the first wave); the result is valid in
-// thread 0. lds holds NT / kWave entries.
-template <int NT, typename T>
-__device__ __forceinline__ T block_sum_fixed(T x, T *lds) {
+
+// The six loss sums of a block, reduced together in a fixed order: each
+// wave's tree sums, one LDS row per wave, then the first wave sums the rows
+// in wave order (one barrier for all six instead of two per sum). The
+// result is valid in thread 0.
+struct LossSums {
+    double l1, fn, fp;
+    unsigned long long nd, nfn, nfp;
+};
+
+template <int NT>
+__device__ __forceinline__ LossSums block_sum_loss(LossSums x, LossSums *lds) {
     constexpr int kW = NT / kWave;
     const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
-    x = wave_sum_xor(x);
+    x.l1 = wave_sum_xor(x.l1);
+    x.fn = wave_sum_xor(x.fn);
+    x.fp = wave_sum_xor(x.fp);
+    x.nd = wave_sum_xor(x.nd);
+    x.nfn = wave_sum_xor(x.nfn);
+    x.nfp = wave_sum_xor(x.nfp);
     if (lane == 0) lds[wid] = x;
     __syncthreads();
-    T r = 0;
+    LossSums r{0.0, 0.0, 0.0, 0ull, 0ull, 0ull};
     if (wid == 0) {
-        r = lane < kW ? lds[lane] : (T)0;
-        r = wave_sum_xor(r);
+        if (lane < kW) r = lds[lane];
+        r.l1 = wave_sum_xor(r.l1);
+        r.fn = wave_sum_xor(r.fn);
+        r.fp = wave_sum_xor(r.fp);
+        r.nd = wave_sum_xor(r.nd);
+        r.nfn = wave_sum_xor(r.nfn);
+        r.nfp = wave_sum_xor(r.nfp);
     }
-    __syncthreads();
     return r;
 }
 
@@ -137,8 +153,7 @@ __global__ __launch_bounds__(kBlock) void k_loss_partials(int64_t n, int64_t chu
                                                           const float *influence, const float *target,
                                                           const uint8_t *defined, float tau, double thr,
                                                           LossPart *part) {
-    __shared__ double lds_d[kBlock / kWave];
-    __shared__ unsigned lds_u[kBlock / kWave];
+    __shared__ LossSums lds[kBlock / kWave];
     double l1 = 0.0, fn = 0.0, fp = 0.0;
     unsigned nd = 0, nfn = 0, nfp = 0;
     for (int64_t c = blockIdx.x; c < chunks; c += gridDim.x) {
@@ -170,20 +185,15 @@ __global__ __launch_bounds__(kBlock) void k_loss_partials(int64_t n, int64_t chu
             }
         }
     }
-    l1 = block_sum_fixed<kBlock>(l1, lds_d);
-    fn = block_sum_fixed<kBlock>(fn, lds_d);
-    fp = block_sum_fixed<kBlock>(fp, lds_d);
-    nd = block_sum_fixed<kBlock>(nd, lds_u);
-    nfn = block_sum_fixed<kBlock>(nfn, lds_u);
-    nfp = block_sum_fixed<kBlock>(nfp, lds_u);
+    const LossSums r = block_sum_loss<kBlock>(LossSums{l1, fn, fp, nd, nfn, nfp}, lds);
     if (threadIdx.x == 0) {
         LossPart p;
-        p.l1 = l1;
-        p.fn = fn;
-        p.fp = fp;
-        p.nd = nd;
-        p.nfn = nfn;
-        p.nfp = nfp;
+        p.l1 = r.l1;
+        p.fn = r.fn;
+        p.fp = r.fp;
+        p.nd = r.nd;
+        p.nfn = r.nfn;
+        p.nfp = r.nfp;
         part[blockIdx.x] = p;
     }
 }
@@ -191,8 +201,7 @@ __global__ __launch_bounds__(kBlock) void k_loss_partials(int64_t n, int64_t chu
 __global__ __launch_bounds__(kFinishThreads) void k_loss_finish(int nparts, const LossPart *part, int64_t n,
                                                                  float lambda_fn, float lambda_fp,
                                                                  gs_loss_terms *terms, LossScales *scales) {
-    __shared__ double lds_d[kFinishThreads / kWave];
-    __shared__ unsigned long long lds_u[kFinishThreads / kWave];
+    __shared__ LossSums lds[kFinishThreads / kWave];
     const int t = threadIdx.x;
     double l1 = 0.0, fn = 0.0, fp = 0.0;
     unsigned long long nd = 0, nfn = 0, nfp = 0;
@@ -205,12 +214,13 @@ __global__ __launch_bounds__(kFinishThreads) void k_loss_finish(int nparts, cons
         nfn = p.nfn;
         nfp = p.nfp;
     }
-    l1 = block_sum_fixed<kFinishThreads>(l1, lds_d);
-    fn = block_sum_fixed<kFinishThreads>(fn, lds_d);
-    fp = block_sum_fixed<kFinishThreads>(fp, lds_d);
-    nd = block_sum_fixed<kFinishThreads>(nd, lds_u);
-    nfn = block_sum_fixed<kFinishThreads>(nfn, lds_u);
-    nfp = block_sum_fixed<kFinishThreads>(nfp, lds_u);
+    const LossSums r = block_sum_loss<kFinishThreads>(LossSums{l1, fn, fp, nd, nfn, nfp}, lds);
+    l1 = r.l1;
+    fn = r.fn;
+    fp = r.fp;
+    nd = r.nd;
+    nfn = r.nfn;
+    nfp = r.nfp;
     if (t == 0) {
         const double dnd = (double)nd, dnfn = (double)nfn, dnfp = (double)nfp;
         gs_loss_terms r;
