@@ -343,6 +343,26 @@ def test_forward_is_deterministic():
     np.testing.assert_array_equal(c[0], d[0])
 
 
+def test_backward_is_deterministic():
+    """Every per-Gaussian sum is formed by one wavefront in a fixed order,
+    without atomics: repeated backward passes (and a whole repeated step,
+    index included) give the same bits, for both packings of Gaussians per
+    wave."""
+    for n_gauss, seed in ((3000, 73), (70000, 74)):
+        g = synth.random_gaussians(seed, n_gauss, log_mu=np.log(0.02), log_sd=0.4)
+        pts = synth.random_points(seed + 1, 60000)
+        log(f"case backward determinism, {n_gauss} Gaussians")
+        r = Run(g, (16, 16, 16), "points", points=pts)
+        r.forward()
+        gv, gi = synth.random_normal(seed + 2, r.nq), synth.random_normal(seed + 3, r.nq)
+        a = r.backward(gv, gi)
+        b = r.backward(gv, gi)
+        np.testing.assert_array_equal(a, b)
+        r2 = Run(g, (16, 16, 16), "points", points=pts)
+        r2.forward()
+        np.testing.assert_array_equal(r2.backward(gv, gi), a)
+
+
 def test_sum_rules_hold_on_device():
     """sum_i dv_i = sum over defined points of gPhi, and
     sum_i w_i dw_i = sum over defined points of gI I (any size)."""
@@ -419,3 +439,27 @@ def test_backward_quarter_cuts_keep_extreme_points():
     check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="x-extremes")
     work = gs.alloc_backward_work(r.index, r.query, "cuda")
     assert gs.backward_pair_count(r.index, r.query, r.plan, work) >= int(ref.ncontrib.sum())
+
+
+@pytest.mark.parametrize("kind", ["points corner", "grid", "jitter"])
+def test_backward_four_gaussians_a_wave(kind):
+    """From 65,536 Gaussians the backward packs four consecutive Gaussians of
+    the spatial order into a wave (fewer take one each): small Gaussians,
+    every one of them checked, with empty boxes (points in one corner),
+    grid rows and jittered queries."""
+    g = synth.random_gaussians(91, 70000, log_mu=np.log(0.012), log_sd=0.4)
+    log(f"case backward, four Gaussians a wave: {kind}")
+    if kind == "points corner":
+        pts = synth.random_points(92, 30000, 0.0, 0.6)
+        r = Run(g, (20, 20, 20), "points", points=pts)
+    elif kind == "grid":
+        r = Run(g, (16, 16, 16), "grid", dims=(48, 48, 48))
+    else:
+        dims = (40, 36, 32)
+        r = Run(g, (20, 18, 16), "jitter", dims=dims, offsets=synth.jitter_offsets(93, 40 * 36 * 32))
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label=kind)
+    gv, gi = synth.random_normal(94, r.nq), synth.random_normal(95, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label=kind)
