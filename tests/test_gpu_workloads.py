@@ -107,3 +107,71 @@ def test_c5_points_full_forward():
     probes = np.array([[0.3, 0.3, 0.3], [0.7, 0.7, 0.7], [0.3 + 0.149, 0.3, 0.3], [0, 0, 0], [1, 1, 1]], np.float32)
     rp = oracle.forward(g, probes)
     log(f"  probes: oracle I {rp.inf}")
+
+
+def test_training_step_128cubed():
+    """The structured training step in the configuration bench.py times
+    (Sec. 4.2, Sec. 4.2.2, Sec. 6.1): the free parameters behind C2's
+    Gaussians, activations with the 0.02 cap, a 40^3 index, one random
+    position in every voxel of 128^3, the L1 + false-negative losses, the
+    backward and the activations' backward. Forward outputs on seeded
+    samples, the losses over all 2^21 samples, the gradients of seeded
+    Gaussians."""
+    import math
+
+    import torch
+
+    import paper_2607_01164_amd as gs
+    w = synth.WORKLOADS["c2_grid256_batch"]
+    ls, vl, wl = synth.raw_params(w)
+    base = synth.make_gaussians(w)
+    cap = float(np.float32(0.02))
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    raw = gs.RawParams(t(ls), t(vl), t(wl))
+    n = w.n_gauss
+    s, v, wt = torch.empty(n, 3, device="cuda"), torch.empty(n, device="cuda"), torch.empty(n, device="cuda")
+    gs.gs_activate(raw, cap, s, v, wt)
+    torch.cuda.synchronize()
+    g_act = synth.Gaussians(base.mean, s.cpu().numpy(), base.rot, v.cpu().numpy(), wt.cpu().numpy())
+    dims = (128, 128, 128)
+    nq = 128 ** 3
+    u = synth.jitter_offsets(w.cfg, nq, iteration=0)
+    log(f"case training step: {n} Gaussians, {nq} jittered samples, cells 40^3")
+    r = Run(g_act, (40, 40, 40), "jitter", dims=dims, offsets=u)
+    check_index(r)
+    phi, inf = r.forward()
+    check_forward(r, phi, inf, sel=sample_ids(nq, N_FWD_SAMPLE, 21), label="training forward")
+    y = synth.targets(w.cfg, nq, iteration=0)
+    gv_d, gi_d = torch.empty(nq, device="cuda"), torch.empty(nq, device="cuda")
+    terms = gs.alloc_loss_terms("cuda")
+    gs.gs_loss(torch.from_numpy(phi).cuda(), torch.from_numpy(inf).cuda(), t(y), None, TAU, 0.1, 1.0, 0.0, gv_d, gi_d,
+               terms, gs.alloc_loss_work(nq, "cuda"))
+    got = gs.read_loss_terms(terms)
+    ref = oracle.loss(phi, inf, y, None, tau=TAU, eps=0.1, lambda_fn=1.0, lambda_fp=0.0)
+    gv, gi = gv_d.cpu().numpy(), gi_d.cpu().numpy()
+    np.testing.assert_array_equal(gv, ref.grad_value)
+    np.testing.assert_array_equal(gi, ref.grad_influence)
+    assert (got["n_defined"], got["n_fn"]) == (ref.n_defined, ref.n_fn)
+    assert abs(got["total"] - ref.total) <= (2 * nq + 8) * 2.0 ** -53 * ref.total
+    log(f"  losses: L1 {ref.l1:.6g}, false negatives {ref.n_fn} ({ref.fn:.3g})")
+    # the backward of seeded Gaussians with the loss's cotangents
+    sel = sample_ids(n, N_BWD_SAMPLE, 22)
+    pts_all = r.positions()
+    sup = np.nonzero(oracle.support(g_act, pts_all, sel, r.lo, r.hi, TAU))[0]
+    fref = oracle.forward(g_act, pts_all[sup], r.lo, r.hi, TAU)
+    amb = oracle.ambiguous_points(fref, TAU)
+    gv[sup[amb]] = 0
+    gi[sup[amb]] = 0
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, sel, sup, gv[sup], gi[sup], label="training backward")
+    # and the activations' backward of the same Gaussians, on the device's gradients
+    post = gs.Grads(None, t(grads[:, 3:6]), None, t(grads[:, 10]), t(grads[:, 11]))
+    out = gs.RawParams(torch.empty(n, 3, device="cuda"), torch.empty(n, device="cuda"), torch.empty(n, device="cuda"))
+    gs.gs_activate_backward(raw, cap, post, out)
+    torch.cuda.synchronize()
+    a, b, c = oracle.activate_backward(oracle.RawGaussians(ls[sel], vl[sel], wl[sel]), cap, grads[sel, 3:6],
+                                       grads[sel, 10], grads[sel, 11])
+    for got_, want in ((out.log_scale.cpu().numpy()[sel], a), (out.value_logit.cpu().numpy()[sel], b),
+                       (out.weight_logit.cpu().numpy()[sel], c)):
+        tol = 2.0 ** -24 * np.abs(want) * (1 + 1e-6) + 2.0 ** -149 + 1e-14 * np.abs(want).max()
+        assert np.all(np.abs(got_.astype(np.float64) - want) <= tol)
