@@ -532,6 +532,8 @@ def main():
         "fwd_bwd_samples_per_s_excl_build": st.n / (t_fwd + t_bwd),
         "ms_build": t_build * 1e3, "ms_fwd": t_fwd * 1e3, "ms_bwd": t_bwd * 1e3,
         "gauss_point_evals_per_s": (contrib * st.n / t_fwd) if contrib else None,
+        "candidate_tests_per_s_fwd": n_tests / t_fwd,
+        "candidate_tests_per_s_bwd": bwd_tests / t_bwd,
         "kernels": {k: round(v["ms_per_step"] * 1e3, 2) for k, v in kernels.items()},
         "training_step": train,
         "forward_ab": ab,
