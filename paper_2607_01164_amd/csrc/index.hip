@@ -185,10 +185,9 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
     __shared__ int sp_i[5][kPreBlock];
     // span bytes, word w of box t holding rows 4w..4w+3 at sp_code[w][t]
     __shared__ uint32_t sp_code[kSpanRows / 4][kPreBlock];
-    __shared__ uint32_t sp_cnt[kPreBlock];
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint32_t tid = threadIdx.x, lane = tid % kWave, wbase = tid - lane;
-    if (i == n) count[n] = 0;
+    if (i == 0) count[n] = 0;  // the element after the last count, for the offsets' scan
     const bool active = i < n;
     float mu[3] = {0.0f, 0.0f, 0.0f}, s[3] = {1.0f, 1.0f, 1.0f}, q[4] = {1.0f, 0.0f, 0.0f, 0.0f};
     float v = 0.0f, w = 0.0f;
@@ -277,7 +276,6 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
     const uint32_t nrows = trimmed ? (uint32_t)((hi_c[1] - lo_c[1] + 1) * (hi_c[2] - lo_c[2] + 1)) : 0u;
 #pragma unroll
     for (int k = 0; k < kSpanRows / 4; ++k) sp_code[k][tid] = kSpanEmpty * 0x01010101u;
-    sp_cnt[tid] = 0;
     SpanGrid sg;
     sg.glo[0] = (double)g.lo[0];
     sg.glo[1] = (double)g.lo[1];
@@ -329,12 +327,14 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
             const uint32_t code = span_row(sp, r, sg, len, qcode);
             ((uint8_t *)&sp_code[r >> 2][t])[r & 3] = (uint8_t)code;
             spans[((size_t)blockIdx.x * kPreBlock + t) * kSpanStride + kSpanRows + (uint32_t)r] = (uint8_t)qcode;
-            atomicAdd(&sp_cnt[wbase + o], len);
         }
     }
     __builtin_amdgcn_wave_barrier();
     if (trimmed) {
-        cnt = sp_cnt[tid];
+        // the box's pairs: the lengths of its rows' runs
+        uint32_t c = 0;
+        for (uint32_t r = 0; r < nrows; ++r) c += span_len((sp_code[r >> 2][tid] >> (8u * (r & 3u))) & 0xFFu);
+        cnt = c;
         uint4 *dst = (uint4 *)(spans + (size_t)i * kSpanStride);
 #pragma unroll
         for (int k = 0; k < kSpanRows / 16; ++k)
@@ -553,7 +553,9 @@ hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g,
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
                              CellBox *box, uint8_t *spans, uint64_t *count, uint64_t *block_sum, hipStream_t s) {
-    const int64_t threads = n + 1;
+    // one thread per Gaussian (thread 0 also writes count[n]): for n a
+    // multiple of 64 the launch fits one round of the chip
+    const int64_t threads = n > 0 ? n : 1;
     const uint32_t blocks = (uint32_t)((threads + kPreBlock - 1) / kPreBlock);
     prof_begin("preprocess", s);
     hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kPreBlock), 0, s, mean, scale, rot, value, weight, n, g, rci, rec,
