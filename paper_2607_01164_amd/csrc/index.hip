@@ -437,7 +437,7 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
                                                  RadixPass0 pass0) {
     __shared__ uint64_t mark[kExpandTile];
     __shared__ uint64_t wmax[kWavesPerBlock];
-    __shared__ uint32_t hist_lds[kMaxDigits];
+    extern __shared__ uint32_t hist_lds[];  // the first pass's digits, sized at launch
     Pass0Hist hist(hist_lds, pass0);
     const uint32_t tid = threadIdx.x;
     const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
@@ -570,8 +570,11 @@ hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8
     if (npairs <= 0 || n <= 0) return hipSuccess;
     const uint32_t blocks = (uint32_t)((npairs + kExpandTile - 1) / kExpandTile);
     prof_begin("emit", s);
-    hipLaunchKernelGGL(k_emit, dim3(blocks), dim3(kBlock), 0, s, pair_off, box, spans, n, npairs, tile_first, g, keys,
-                       gids, pass0);
+    // the histogram takes only the first pass's digits: with 8-bit digits the
+    // block's LDS lets 9 blocks share a compute unit instead of 7
+    const size_t hist_bytes = sizeof(uint32_t) * ((size_t)pass0.mask + 1);
+    hipLaunchKernelGGL(k_emit, dim3(blocks), dim3(kBlock), hist_bytes, s, pair_off, box, spans, n, npairs, tile_first,
+                       g, keys, gids, pass0);
     prof_end("emit", s);
     return hipGetLastError();
 }

@@ -160,11 +160,13 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     // consecutive tiles on one XCD: their runs of each digit are adjacent in
     // the output and merge in that XCD's L2
     const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
-    uint32_t *wcnt = lds;                        // [kWavesPerBlock][ndig]
-    uint32_t *dstart = wcnt + kWavesPerBlock * ndig;
-    uint32_t *dglob = dstart + ndig;
+    uint32_t *dstart = lds;                      // [ndig]
+    uint32_t *dglob = dstart + ndig;             // [ndig]
     uint32_t *sk = dglob + ndig;                 // [kSortTile]
     uint32_t *sv = sk + kSortTile;               // [kSortTile]
+    // the per-wave digit counts share the tile buffers' space: they are all
+    // read before the tile is written there (kWavesPerBlock ndig <= 2 kSortTile)
+    uint32_t *wcnt = sk;                         // [kWavesPerBlock][ndig]
     const int64_t base = (int64_t)tile * kSortTile + (int64_t)wave * (kWave * kSortItems);
     uint32_t k[kSortItems], v[kSortItems], r[kSortItems];
 #pragma unroll
@@ -259,14 +261,21 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
         }
     }
     __syncthreads();
+    uint32_t slot[kSortItems];
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const int64_t idx = base + (int64_t)i * kWave + lane;
+        const uint32_t d = (k[i] >> shift) & mask;
+        slot[i] = idx < n ? dstart[d] + mycnt[d] + r[i] : 0u;
+    }
+    // every counter is read before the tile overwrites their space
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         const int64_t idx = base + (int64_t)i * kWave + lane;
         if (idx < n) {
-            const uint32_t d = (k[i] >> shift) & mask;
-            const uint32_t slot = dstart[d] + mycnt[d] + r[i];
-            sk[slot] = k[i];
-            sv[slot] = v[i];
+            sk[slot[i]] = k[i];
+            sv[slot[i]] = v[i];
         }
     }
     __syncthreads();
@@ -451,7 +460,8 @@ hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *
         return hipSuccess;
     }
     const uint32_t ndig = 1u << L.dbits;
-    const size_t lds = ((size_t)6 * ndig + 2 * kSortTile) * 4;
+    static_assert(kWavesPerBlock * kMaxDigits <= 2 * kSortTile, "the wave counts fit the tile buffers");
+    const size_t lds = ((size_t)2 * ndig + 2 * kSortTile) * 4;
     uint32_t *ki = k0, *vi = v0, *ko = k1, *vo = v1;
     for (int p = 0; p < L.passes; ++p) {
         const int shift = p * L.dbits;
