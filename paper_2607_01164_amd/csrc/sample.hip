@@ -407,7 +407,12 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
 //  * n < 4: lanes are the cell's candidates (64 at a time) and the queries
 //    are visited in turn, their positions broadcast from SGPRs.
 // Every query's sums are reduced in a fixed order.
-__global__ __launch_bounds__(kBlock) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
+// Seven waves per SIMD (at most 72 VGPRs; the compiler keeps a few values in
+// scratch): the row layouts' per-row arrays would otherwise take 83 VGPRs and
+// leave five, and the dense-cell walks need the extra waves to hide their
+// loads (C4 5.76 -> 5.13 ms, C5 166 -> 145 ms; eight waves spill enough to
+// slow the row layouts by a sixth).
+__global__ __launch_bounds__(kBlock, 7) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                          const uint32_t *__restrict__ gids,
                                                          const uint32_t *__restrict__ cell_off,
                                                          const uint32_t *__restrict__ point_off,
