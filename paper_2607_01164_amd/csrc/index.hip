@@ -4,7 +4,9 @@
 //    cell count, and the evaluation record used by the samplers;
 //  - row spans: boxes of at most kSpanRows (y, z) rows of at most kSpanNx
 //    cells keep, per row, only the run of cells a float64 bound of the
-//    cutoff ellipsoid's section over the row's slab can reach;
+//    cutoff ellipsoid's section over the row's slab can reach, and the
+//    quarters (along x) of the run's two end cells that the bound reaches,
+//    which the backward uses with the plan's order by quarter of a cell;
 //  - emit: one (cell key, Gaussian id) pair per listed cell of every box,
 //    parallel over pairs with a per-tile load-balanced search for the owning
 //    Gaussian (the paper parallelises this step over intersections for the

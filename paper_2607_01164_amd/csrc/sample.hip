@@ -8,8 +8,8 @@
 // with one address for all lanes.
 //
 // Voxel-list and point queries (Sec. 5.1.2): the queries are first ordered
-// by cell (query_keys + radix sort, kept in the plan) and the work is split
-// by cell: dense cells run like grid cells, cells of fewer queries spread
+// by cell and, inside a cell, by quarter of the cell along x (query_keys +
+// radix sort, kept in the plan) and the work is split by cell: dense cells run like grid cells, cells of fewer queries spread
 // queries and candidates over the lanes (see k_sample_cells).
 #include "expand.h"
 #include "internal.h"
