@@ -1,19 +1,23 @@
 """Benchmark of the Gaussian-field sampling hot path on one MI355X.
 
-Workload: structured 256^3 grid over [0,1]^3, 262,144 Gaussians (means
-U[0,1]^3, log-scales N(ln 0.008, 0.4) per axis, random unit quaternions,
-values U[0,1], weights sigmoid(N(0,1))); one step is a training step on a
-seeded random batch of 2^20 voxel centres: build the cell index, sample
-(query ordering + forward) and backpropagate N(0,1) cotangents to every
-Gaussian parameter. All inputs are resident in HBM before the timed region.
+Headline workload: the unstructured training step of the largest
+configuration with a backward. 8,388,608 points drawn from a seeded
+64-component anisotropic mixture on [0,1]^3 with a spherical cavity of
+radius 0.2 left empty, 524,288 Gaussians with means from the same density
+and log-scales N(ln 0.005, 0.8) per axis, index 64^3 cells. One step runs
+the cloud as four batches of 2^21 points, each a training iteration: build
+the cell index, sample (query ordering + forward) and backpropagate N(0,1)
+cotangents to every Gaussian parameter. All inputs are resident in HBM
+before the timed region.
 
-Prints one JSON line: fwd+bwd samples/s over the timed steps, with the
-forward-only query rate, the per-kernel timing of the step (HIP events on
-the library's stream), the roofline of the dominant kernel, the CPU
-oracle's rate on a bounded sample of the same workload, and the rate of a
-structured training step: activations, index, 128^3 jittered samples (one
-random position per voxel), losses, backward and the activations' backward
-over the free parameters behind the same Gaussians.
+Prints one JSON line: fwd+bwd samples/s over the timed steps, the per-kernel
+timing of the step (HIP events on the library's stream), the roofline of
+the dominant kernel, the CPU oracle's rate on a bounded sample of the same
+workload, and secondary entries: the 10^8-point full-field forward, the
+structured 256^3 batch step, a structured training step (activations,
+index, 128^3 jittered samples, losses, backward, activations' backward),
+the 32^3 and 512^3 grids, and the point-major against Gaussian-major
+forward.
 """
 import argparse
 import hashlib
@@ -29,22 +33,22 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_VEC_PEAK_TFLOPS = 157.3   # MI355X vector FP32: 256 CUs x 2.4 GHz x 128 lanes x 2 (packed FMA)
-# Algorithmic work, counted as adds and multiplies (an FMA is 2) and the
-# exponential as 1. Every candidate (Gaussian, point) pair of a cell list is
-# tested: d = p - mu (3), u = M d (15), Q = |u|^2 (5), the cutoff compare (1).
-# A contributing pair (Q <= T) adds, in the forward, a = w exp(-Q/2),
-# I += a, V += a v; in the backward, a, dL/da, the per-pair moment terms and
-# dv, dw.
-FLOPS_PER_TEST = 24.0
-FLOPS_PER_CONTRIB = {"sample_points": 7.0, "sample_grid": 7.0, "bwd_gauss": 37.0}
+# Algorithmic work of the samplers: a (Gaussian, point) pair that fails the
+# cutoff costs the test itself, d = p - mu, u = M d, Q = |u|^2 and the
+# compare, counted as 16 operations; a contributing pair costs 30 flops and
+# one exponential in the forward (the test, a = w exp(-Q/2), I += a,
+# V += a v) and 60 flops and one exponential in the backward (the test, a,
+# dL/da, the per-pair moment terms, dv, dw).
+FLOPS_FAILING_PAIR = 16.0
+FLOPS_CONTRIB = {"sample_points": 31.0, "sample_grid": 31.0, "bwd_gauss": 61.0}
 # Bytes one pass of the LSD sort moves per pair: read and write key and value.
 SORT_BYTES_PER_PAIR = 16.0
 EMIT_BYTES_PER_PAIR = 8.0
 COPY_PROBE_BYTES = 256 << 20   # plain copy used to calibrate the HBM byte counters
 SRC_DIR = os.path.join(ROOT, "paper_2607_01164_amd", "csrc")
-WORKLOAD = "c2_grid256_batch"
-INDEX_CELLS = (32, 32, 32)
-TRAIN_CELLS = (40, 40, 40)     # the training step's index: twice C2's query density
+HEADLINE = "c4_points8m"
+C2_CELLS = (32, 32, 32)        # the 256^3 batch step's index, the best of a sweep
+TRAIN_CELLS = (40, 40, 40)     # the training step's index: twice the batch's query density
 TAU = 0.01
 
 
@@ -55,42 +59,165 @@ def log(*a):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--cells", type=int, nargs=3, default=list(INDEX_CELLS))
-    p.add_argument("--train-cells", type=int, nargs=3, default=list(TRAIN_CELLS))
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--only", choices=["c4", "c5", "c2", "c3", "c1", "train"], default=None,
+                   help="run only this workload's step loop (warmup + steps) and print a short line: for profiling")
     p.add_argument("--cpu-seconds", type=float, default=16.0, help="target length of the CPU oracle sample")
     p.add_argument("--no-cpu", action="store_true")
-    p.add_argument("--no-train", action="store_true", help="skip the 128^3 structured training-step line")
-    p.add_argument("--no-ab", action="store_true", help="skip the point-major / Gaussian-major comparison")
-    p.add_argument("--ab-c5", action="store_true",
-                   help="also compare the two forwards on the 10^8-point cloud (slow to generate)")
-    p.add_argument("--no-configs", action="store_true", help="skip the C1, C3 and C4 lines")
+    p.add_argument("--no-c5", action="store_true", help="skip the 10^8-point full-field forward")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the secondary entries (256^3 batch step, training step, C1, C3, forward A/B)")
     p.add_argument("--breakdown", action="store_true", help="print the per-kernel table to stderr")
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, run a plain 256 MiB copy (counter calibration under rocprofv3)")
     return p.parse_args()
 
 
-class Step:
-    def __init__(self, cells):
+def timed(fn, k, sync):
+    sync()
+    t0 = time.perf_counter()
+    for _ in range(k):
+        fn()
+    sync()
+    return (time.perf_counter() - t0) / k
+
+
+def kernel_table(gs, fn, k, sync):
+    """{kernel: (launches per call, microseconds per call)} over k calls of
+    fn with every library kernel bracketed by HIP events (an untimed pass)."""
+    gs.profile_select(None)
+    gs.profile_reset()
+    gs.profile_enable(True)
+    for _ in range(k):
+        fn()
+    sync()
+    gs.profile_enable(False)
+    return {name: (c / k, ms / k * 1e3) for name, (c, ms) in gs.profile_read().items()}
+
+
+def kernel_avg_us(gs, name, fn, k, sync):
+    """(wall seconds per call, average microseconds per launch of kernel
+    `name`) over k timed calls of fn, only that kernel bracketed by HIP
+    events on the library's stream."""
+    gs.profile_select(name)
+    gs.profile_reset()
+    gs.profile_enable(True)
+    t = timed(fn, k, sync)
+    gs.profile_enable(False)
+    gs.profile_select(None)
+    c, ms = gs.profile_read().get(name, (0, 0.0))
+    return t, (ms / c * 1e3 if c else None), c / k
+
+
+def _dev(torch, np, a, dev="cuda:0"):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+
+class PointsStep:
+    """The unstructured workload's training step: the point cloud in
+    `batches` resident batches; each is one iteration of index build,
+    forward (query ordering included) and backward with its own N(0,1)
+    cotangents. The index is rebuilt every iteration, as training changes
+    the Gaussians after each one."""
+
+    def __init__(self, name="c4_points8m"):
         import numpy as np
         import torch
 
         import paper_2607_01164_amd as gs
         import synth
         self.gs, self.torch, self.np = gs, torch, np
-        w = synth.WORKLOADS[WORKLOAD]
+        w = synth.WORKLOADS[name]
+        self.w = w
+        g = synth.make_gaussians(w)
+        self.g_host = g
+        pts = synth.make_points(w)
+        perm = synth.batch_permutation(w, len(pts))
+        self.batches = len(pts) // w.batch
+        dev = "cuda:0"
+        self.dg = gs.Gaussians(*(_dev(torch, np, a) for a in (g.mean, g.scale, g.rot, g.value, g.weight)))
+        self.pts, self.gv, self.gi, self.queries = [], [], [], []
+        for b in range(self.batches):
+            bp = pts[perm[b * w.batch:(b + 1) * w.batch]]
+            if b == 0:
+                self.batch0_host = bp
+            self.pts.append(_dev(torch, np, bp))
+            gv, gi = synth.cotangents(w, w.batch, batch_index=b)
+            self.gv.append(_dev(torch, np, gv))
+            self.gi.append(_dev(torch, np, gi))
+            self.queries.append(gs.Query.pts(self.pts[-1]))
+        del pts
+        self.n = w.batch
+        self.grid = gs.make_grid(w.index_cells)
+        probe = gs.build_index(self.dg, self.grid, TAU)
+        self.index = gs.Index(self.grid, g.n, int(probe.n_pairs * 1.25) + 4096, dev)
+        del probe
+        self.plan = gs.alloc_plan(self.queries[0], self.grid, dev)
+        self.val = torch.empty(self.n, device=dev)
+        self.inf = torch.empty(self.n, device=dev)
+        self.grads = gs.Grads.empty(g.n, dev)
+        gs.gs_build_index(self.dg, self.grid, TAU, self.index)
+        self.work = gs.alloc_backward_work(self.index, self.queries[0], dev)
+        self.b = 0
+        torch.cuda.synchronize()
+
+    def build(self):
+        self.gs.gs_build_index(self.dg, self.grid, TAU, self.index)
+
+    def forward(self, b=None):
+        b = self.b if b is None else b
+        self.gs.gs_sample(self.dg, self.index, self.queries[b], self.val, self.inf, self.plan)
+
+    def backward(self, b=None):
+        b = self.b if b is None else b
+        self.gs.gs_sample_backward(self.dg, self.index, self.queries[b], self.plan, self.val, self.inf, self.gv[b],
+                                   self.gi[b], self.grads, self.work)
+
+    def iteration(self):
+        self.build()
+        self.forward()
+        self.backward()
+        self.b = (self.b + 1) % self.batches
+
+    def step(self):
+        for _ in range(self.batches):
+            self.iteration()
+
+    def pair_counts(self):
+        """Per batch (forward tests, backward tests, contributing pairs),
+        counted on the device after each batch's forward."""
+        out = []
+        for b in range(self.batches):
+            self.forward(b)
+            t, c = self.gs.sample_pair_counts(self.index, self.queries[b], self.plan, self.work)
+            bt = self.gs.backward_pair_count(self.index, self.queries[b], self.plan, self.work)
+            out.append((t, bt, c))
+        return out
+
+
+class GridBatchStep:
+    """The structured 256^3 batch step: 262,144 Gaussians, a seeded batch of
+    2^20 distinct voxel centres; index build + forward + backward."""
+
+    def __init__(self, cells=C2_CELLS):
+        import numpy as np
+        import torch
+
+        import paper_2607_01164_amd as gs
+        import synth
+        self.gs, self.torch, self.np = gs, torch, np
+        w = synth.WORKLOADS["c2_grid256_batch"]
         self.w = w
         g = synth.make_gaussians(w)
         self.g_host = g
         self.ids_host = synth.voxel_batch(w)
         gv, gi = synth.cotangents(w, len(self.ids_host))
         dev = "cuda:0"
-        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
-        self.dg = gs.Gaussians(t(g.mean), t(g.scale), t(g.rot), t(g.value), t(g.weight))
+        self.dg = gs.Gaussians(*(_dev(torch, np, a) for a in (g.mean, g.scale, g.rot, g.value, g.weight)))
         self.ids = torch.from_numpy(self.ids_host.view(np.int32)).to(dev)
-        self.gv, self.gi = t(gv), t(gi)
+        self.gv, self.gi = _dev(torch, np, gv), _dev(torch, np, gi)
+        self.cells = tuple(cells)
         self.grid = gs.make_grid(cells)
         self.query = gs.Query.voxels(w.dims, self.ids)
         self.n = len(self.ids_host)
@@ -120,22 +247,11 @@ class Step:
         self.forward()
         self.backward()
 
-    def candidate_tests(self) -> int:
-        """(Gaussian, point) pairs the forward and the backward test: the sum
-        over cells of (pairs listed in the cell) x (queries in the cell), from
-        the index's cell offsets and the plan's per-cell query offsets (after
-        the four 256-byte aligned query-length arrays of the plan, one offset
-        per quarter of a cell along x)."""
-        torch = self.torch
-        ncells = self.grid.cells[0] * self.grid.cells[1] * self.grid.cells[2]
-        al = lambda b: (b + 255) // 256 * 256
-        off = 4 * al(4 * max(self.n, 1))
-        # the plan's offsets are per quarter of a cell along x (4 keys a cell)
-        point_off = self.plan[off: off + 4 * (4 * ncells + 2)].view(torch.int32).to(torch.int64)
-        pts = point_off[4:4 * ncells + 1:4] - point_off[0:4 * ncells:4]
-        co = self.index.cell_offsets.to(torch.int64)
-        pairs = co[1:] - co[:-1]
-        return int((pts * pairs).sum().item())
+    def pair_counts(self):
+        self.forward()
+        t, c = self.gs.sample_pair_counts(self.index, self.query, self.plan, self.work)
+        bt = self.gs.backward_pair_count(self.index, self.query, self.plan, self.work)
+        return t, bt, c
 
 
 class TrainStep:
@@ -152,7 +268,7 @@ class TrainStep:
     CAP = 0.02
     FN_EPS, FN_LAMBDA, FP_LAMBDA = 0.1, 1.0, 0.0
 
-    def __init__(self, st: Step, cells):
+    def __init__(self, st: "GridBatchStep", cells):
         import numpy as np
         import synth
         gs, torch = st.gs, st.torch
@@ -357,63 +473,119 @@ class ConfigStep:
         self.gs.gs_sample_backward(self.dg, self.index, self.query, self.plan, self.val, self.inf, self.gv, self.gi,
                                    self.grads, self.work)
 
-    def run(self, k):
-        sync = self.torch.cuda.synchronize
+    def run(self, k, tag):
+        gs, sync = self.gs, self.torch.cuda.synchronize
         self.build()
         self.forward()
         if self.has_bwd:
             self.backward()
         sync()
-        tb, tf = timed(self.build, k, sync), timed(self.forward, k, sync)
+        tb = timed(self.build, k, sync)
+        fk = "sample_grid" if self.w.kind == "grid" else "sample_points"
+        tf, fwd_us, _ = kernel_avg_us(gs, fk, self.forward, k, sync)
+        work = self.work if self.has_bwd else gs.alloc_backward_work(self.index, self.query, "cuda:0")
+        self.forward()
+        tests, contrib = gs.sample_pair_counts(self.index, self.query, self.plan, work)
         out = {"workload": self.w.description, "queries": self.n, "index_cells": list(self.w.index_cells),
                "index_pairs": self.index.n_pairs, "ms_build": tb * 1e3, "ms_fwd": tf * 1e3,
-               "fwd_points_per_s": self.n / tf}
+               "fwd_points_per_s": self.n / tf, "forward_tests": tests, "contributing_pairs": contrib,
+               "gauss_point_evals_per_s": contrib / tf,
+               "samplers": {fk: sampler_entry(fk, tag, fwd_us, tests, contrib)}}
         if self.has_bwd:
             self.forward()
-            tw = timed(self.backward, k, sync)
+            tw, bwd_us, _ = kernel_avg_us(gs, "bwd_gauss", self.backward, k, sync)
+            bt = gs.backward_pair_count(self.index, self.query, self.plan, self.work)
             out.update({"ms_bwd": tw * 1e3, "fwd_bwd_samples_per_s": self.n / (tb + tf + tw),
-                        "fwd_bwd_samples_per_s_excl_build": self.n / (tf + tw)})
+                        "fwd_bwd_samples_per_s_excl_build": self.n / (tf + tw), "backward_tests": bt})
+            out["samplers"]["bwd_gauss"] = sampler_entry("bwd_gauss", tag, bwd_us, bt, contrib)
         return out
 
 
-def timed(fn, k, sync):
-    sync()
-    t0 = time.perf_counter()
-    for _ in range(k):
-        fn()
-    sync()
-    return (time.perf_counter() - t0) / k
+def sampler_flops(kernel, tests, contrib):
+    """Algorithmic flops of one sampler launch from its tested and
+    contributing pairs."""
+    return FLOPS_FAILING_PAIR * (tests - contrib) + FLOPS_CONTRIB[kernel] * contrib
 
 
-def cpu_baseline(st: Step, target_s: float):
+def sampler_entry(kernel, tag, avg_us, tests, contrib):
+    """A sampler kernel's algorithmic rate against the fp32 vector peak, and
+    its HBM traffic (committed counter reading, when the sources match)
+    against the HBM peak."""
+    out = {"avg_us": avg_us, "pair_tests": tests, "contributing_pairs": contrib}
+    if avg_us:
+        fl = sampler_flops(kernel, tests, contrib)
+        out.update({"flops_per_launch": fl, "tflops": fl / (avg_us * 1e-6) / 1e12,
+                    "frac": fl / (avg_us * 1e-6) / 1e12 / FP32_VEC_PEAK_TFLOPS})
+    tr = measured_traffic(kernel, tag)
+    out["hbm_bytes"] = tr
+    out["hbm_frac"] = (tr / (avg_us * 1e-6) / (HBM_PEAK_GBS * 1e9)) if (tr and avg_us) else None
+    return out
+
+
+def cpu_baseline(st: PointsStep, target_s: float):
     """The oracle (float64 brute force over every Gaussian, OpenMP over
-    points, then Gaussian-major backward) on a seeded sample of the batch."""
+    points, then Gaussian-major backward) on a seeded sample of the first
+    batch."""
     import numpy as np
 
     import oracle
     g = st.g_host
     sel_all = np.random.default_rng(11).permutation(st.n)
     threads = oracle.default_threads()
+    gv_all, gi_all = st.gv[0].cpu().numpy(), st.gi[0].cpu().numpy()
 
     def run(m):
         sel = sel_all[:m]
-        pts = oracle.voxel_centers(st.w.dims, ids=st.ids_host[sel])
-        gv = st.gv.cpu().numpy()[sel]
-        gi = st.gi.cpu().numpy()[sel]
+        pts = st.batch0_host[sel]
         t0 = time.perf_counter()
         ref = oracle.forward(g, pts, tau=TAU, threads=threads)
-        oracle.backward(g, pts, ref.phi, ref.inf, gv, gi, tau=TAU, threads=threads)
+        oracle.backward(g, pts, ref.phi, ref.inf, gv_all[sel], gi_all[sel], tau=TAU, threads=threads)
         return time.perf_counter() - t0, ref
 
-    m = 512
+    m = 256
     dt, ref = run(m)
     m2 = int(min(65536, max(m, m * target_s / max(dt, 1e-3))))
     if m2 > m:
         dt, ref = run(m2)
         m = m2
     return {"value": m / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
-            "sample": f"{m} of the {st.n} batch voxels, forward + backward to all {g.n} Gaussians, {dt:.1f} s",
-            "contrib_per_point": float(ref.ncontrib.mean())}
+            "sample": f"{m} of the {st.n} points of the first batch, forward + backward to all {g.n} Gaussians, "
+                      f"{dt:.1f} s"}
+
+
+def run_only(a):
+    """One workload's step loop alone (warmup + steps), for profiling."""
+    import torch
+    sync = torch.cuda.synchronize
+    if a.only == "c4":
+        st = PointsStep(HEADLINE)
+        fn, n = st.step, st.n * st.batches
+    elif a.only == "c2":
+        st = GridBatchStep()
+        fn, n = st.step, st.n
+    elif a.only == "train":
+        ts = TrainStep(GridBatchStep(), TRAIN_CELLS)
+        fn, n = ts.step, ts.n
+    else:
+        name = {"c5": "c5_points100m", "c3": "c3_grid512_full", "c1": "c1_grid32"}[a.only]
+        cs = ConfigStep(name)
+
+        def fn():
+            cs.build()
+            cs.forward()
+            if cs.has_bwd:
+                cs.backward()
+        n = cs.n
+    import paper_2607_01164_amd as gs
+    for _ in range(a.warmup):
+        fn()
+    sync()
+    t = timed(fn, a.steps, sync)
+    kern = {k: round(v[1], 2) for k, v in kernel_table(gs, fn, a.steps, sync).items()}
+    print(json.dumps({"only": a.only, "steps": a.steps, "ms_per_step": t * 1e3, "per_s": n / t, "kernels_us": kern}),
+          flush=True)
+    if a.copy_probe:
+        copy_probe()
 
 
 def main():
@@ -425,95 +597,96 @@ def main():
     import torch
     import paper_2607_01164_amd as gs
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    st = Step(tuple(a.cells))
+    if a.only:
+        run_only(a)
+        return
     sync = torch.cuda.synchronize
+    st = PointsStep(HEADLINE)
     for _ in range(a.warmup):
         st.step()
     sync()
     # untimed pass with every kernel bracketed by events: the per-kernel table
     # and the dominant kernel
-    gs.profile_select(None)
-    gs.profile_reset()
-    gs.profile_enable(True)
-    for _ in range(a.steps):
-        st.step()
-    sync()
-    gs.profile_enable(False)
-    prof = gs.profile_read()
-    kernels = {k: {"launches_per_step": c / a.steps, "ms_per_step": ms / a.steps, "avg_ms": ms / c}
-               for k, (c, ms) in prof.items()}
-    dom_name = max(kernels.items(), key=lambda kv: kv[1]["ms_per_step"])[0]
+    kernels = kernel_table(gs, st.step, a.steps, sync)
+    dom = max(kernels.items(), key=lambda kv: kv[1][1])[0]
     # timed region: K whole steps; only the dominant kernel is bracketed by
     # HIP events (on the library's stream), for its roofline entry
-    gs.profile_select(dom_name)
-    gs.profile_reset()
-    gs.profile_enable(True)
-    t_step = timed(st.step, a.steps, sync)
-    gs.profile_enable(False)
-    gs.profile_select(None)
-    c, ms = gs.profile_read()[dom_name]
-    dom = (dom_name, {"launches_per_step": c / a.steps, "ms_per_step": ms / a.steps, "avg_ms": ms / c})
-    n_pairs = st.index.n_pairs
-    n_tests = st.candidate_tests()
-    bwd_tests = gs.backward_pair_count(st.index, st.query, st.plan, st.work)
-    # forward alone and backward alone, for the query rates
-    t_fwd = timed(st.forward, a.steps, sync)
-    t_bwd = timed(st.backward, a.steps, sync)
+    t_step, dom_us, dom_launches = kernel_avg_us(gs, dom, st.step, a.steps, sync)
+    counts = st.pair_counts()
+    tests = sum(c[0] for c in counts) / len(counts)
+    btests = sum(c[1] for c in counts) / len(counts)
+    contrib = sum(c[2] for c in counts) / len(counts)
+    # the parts alone, per batch, for the query rates
     t_build = timed(st.build, a.steps, sync)
-    train = None
-    if not a.no_train:
-        ts = TrainStep(st, tuple(a.train_cells))
+    st.b = 0
+    t_fwd, fwd_us, _ = kernel_avg_us(gs, "sample_points", lambda: st.forward(0), a.steps, sync)
+    t_bwd, bwd_us, _ = kernel_avg_us(gs, "bwd_gauss", lambda: st.backward(0), a.steps, sync)
+    samplers = {"sample_points": sampler_entry("sample_points", HEADLINE, fwd_us, tests, contrib),
+                "bwd_gauss": sampler_entry("bwd_gauss", HEADLINE, bwd_us, btests, contrib)}
+    roof = roofline(dom, dom_us, dom_launches, tests, btests, contrib, st.index.n_pairs)
+    n_step = st.n * st.batches
+
+    c5 = None
+    if not a.no_c5:
+        cs = ConfigStep("c5_points100m")
+        c5 = cs.run(3, "c5_points100m")
+        del cs
+        torch.cuda.empty_cache()
+    extras = {}
+    if not a.no_extras:
+        c2 = GridBatchStep()
+        for _ in range(a.warmup):
+            c2.step()
+        t2 = timed(c2.step, a.steps, sync)
+        t2f, f2_us, _ = kernel_avg_us(gs, "sample_points", c2.forward, a.steps, sync)
+        t2b, b2_us, _ = kernel_avg_us(gs, "bwd_gauss", c2.backward, a.steps, sync)
+        t2i = timed(c2.build, a.steps, sync)
+        ct, cbt, cc = c2.pair_counts()
+        extras["c2_grid256_batch"] = {
+            "workload": f"structured 256^3 grid, 262144 Gaussians, batch of 2^20 random voxel centres, index "
+                        f"{'x'.join(map(str, c2.cells))} cells, step = build + forward + backward",
+            "samples_per_step": c2.n, "ms_per_step": t2 * 1e3, "fwd_bwd_samples_per_s": c2.n / t2,
+            "ms_build": t2i * 1e3, "ms_fwd": t2f * 1e3, "ms_bwd": t2b * 1e3, "index_pairs": c2.index.n_pairs,
+            "forward_tests": ct, "backward_tests": cbt, "contributing_pairs": cc,
+            "gauss_point_evals_per_s": cc / t2f,
+            "samplers": {"sample_points": sampler_entry("sample_points", "c2_grid256_batch", f2_us, ct, cc),
+                         "bwd_gauss": sampler_entry("bwd_gauss", "c2_grid256_batch", b2_us, cbt, cc)},
+            "kernels_us": {k: round(v[1], 2) for k, v in kernel_table(gs, c2.step, a.steps, sync).items()}}
+        ts = TrainStep(c2, TRAIN_CELLS)
         for _ in range(a.warmup):
             ts.step()
         sync()
-        gs.profile_select(None)
-        gs.profile_reset()
-        gs.profile_enable(True)
-        for _ in range(a.steps):
-            ts.step()
-        sync()
-        gs.profile_enable(False)
-        tk = {k: round(ms / a.steps * 1e3, 2) for k, (c, ms) in gs.profile_read().items()}
+        tk = {k: round(v[1], 2) for k, v in kernel_table(gs, ts.step, a.steps, sync).items()}
         t_ts = timed(ts.step, a.steps, sync)
         terms = gs.read_loss_terms(ts.terms)
         dens = ts.densify_bench(a.steps)
-        train = {"workload": "structured training step: free parameters of the 262144 Gaussians -> activations "
-                             f"(soft norm cap 0.02) -> index ({'x'.join(map(str, a.train_cells))} cells) -> 128^3 "
-                             "jittered samples (one random position per "
-                             f"voxel, offsets and targets redrawn each step from {TrainStep.SETS} sets resident in "
-                             "HBM) -> forward -> L1 + false-negative losses -> backward -> activation backward",
-                 "samples_per_step": ts.n, "ms_per_step": t_ts * 1e3, "fwd_bwd_samples_per_s": ts.n / t_ts,
-                 "loss": {k: terms[k] for k in ("l1", "fn", "total", "n_fn")}, "kernels_us": tk,
-                 "densify": dens}
-        del ts
-
-    configs = None
-    if not a.no_configs:
-        configs = {}
-        for name in ("c1_grid32", "c3_grid512_full", "c4_points8m") + (("c5_points100m",) if a.ab_c5 else ()):
+        extras["training_step"] = {
+            "workload": "structured training step: free parameters of the 262144 Gaussians -> activations "
+                        f"(soft norm cap 0.02) -> index ({'x'.join(map(str, TRAIN_CELLS))} cells) -> 128^3 "
+                        "jittered samples (one random position per "
+                        f"voxel, offsets and targets redrawn each step from {TrainStep.SETS} sets resident in "
+                        "HBM) -> forward -> L1 + false-negative losses -> backward -> activation backward",
+            "samples_per_step": ts.n, "ms_per_step": t_ts * 1e3, "fwd_bwd_samples_per_s": ts.n / t_ts,
+            "loss": {k: terms[k] for k in ("l1", "fn", "total", "n_fn")}, "kernels_us": tk, "densify": dens}
+        del ts, c2
+        torch.cuda.empty_cache()
+        for name in ("c1_grid32", "c3_grid512_full"):
             cs = ConfigStep(name)
-            configs[name] = cs.run(3 if cs.n > 5e7 else max(5, a.steps // 5))
+            extras[name] = cs.run(3 if cs.n > 5e7 else a.steps, name)
             del cs
             torch.cuda.empty_cache()
-    ab = None
-    if not a.no_ab:
-        ab = {"c4": ABStep("c4_points8m", True).run(max(3, a.steps // 5))}
-        if a.ab_c5:
-            ab["c5"] = ABStep("c5_points100m", False).run(3)
+        extras["forward_ab_c4"] = ABStep("c4_points8m", True).run(max(3, a.steps // 3))
         sync()
     if a.breakdown:
-        for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
-            log(f"{k:18s} {v['ms_per_step'] * 1e3:9.1f} us/step  {v['launches_per_step']:5.1f} launches  "
-                f"avg {v['avg_ms'] * 1e3:9.1f} us")
+        for k, (c, us) in sorted(kernels.items(), key=lambda kv: -kv[1][1]):
+            log(f"{k:18s} {us:9.1f} us/step  {c:5.1f} launches")
     if a.copy_probe:
         copy_probe()
 
     cpu = None if a.no_cpu else cpu_baseline(st, a.cpu_seconds)
-    contrib = cpu.pop("contrib_per_point") if cpu else None
-    roof = roofline(dom[0], dom[1], st, n_pairs, bwd_tests if dom[0] == "bwd_gauss" else n_tests, contrib)
     out = {
         "metric": "query points/sec fwd and fwd+bwd samples/sec; % of HBM roofline",
-        "value": st.n / t_step,
+        "value": n_step / t_step,
         "unit": "fwd+bwd samples/s",
         "n_gpus": 1,
         "steps": a.steps,
@@ -524,21 +697,22 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{WORKLOAD}: 256^3 grid, 262144 Gaussians, batch of 2^20 random voxel centres, "
-                               f"index {a.cells[0]}x{a.cells[1]}x{a.cells[2]} cells, step = build + forward + backward",
-                   "global_batch": st.n, "n_gauss": st.g_host.n, "index_pairs": n_pairs,
-                   "candidate_tests": n_tests, "backward_tests": bwd_tests},
+        "config": {"workload": f"{HEADLINE}: 8388608 clustered points (64-component anisotropic mixture, cavity of "
+                               f"radius 0.2), {st.g_host.n} Gaussians, index "
+                               f"{'x'.join(map(str, st.w.index_cells))} cells; step = {st.batches} batches of "
+                               f"{st.n} points, each build + forward + backward",
+                   "global_batch": n_step, "batch": st.n, "batches": st.batches, "n_gauss": st.g_host.n,
+                   "index_pairs": st.index.n_pairs, "forward_tests": tests, "backward_tests": btests,
+                   "contributing_pairs": contrib},
         "fwd_points_per_s": st.n / t_fwd,
         "fwd_bwd_samples_per_s_excl_build": st.n / (t_fwd + t_bwd),
         "ms_build": t_build * 1e3, "ms_fwd": t_fwd * 1e3, "ms_bwd": t_bwd * 1e3,
-        "gauss_point_evals_per_s": (contrib * st.n / t_fwd) if contrib else None,
-        "candidate_tests_per_s_fwd": n_tests / t_fwd,
-        "candidate_tests_per_s_bwd": bwd_tests / t_bwd,
-        "kernels": {k: round(v["ms_per_step"] * 1e3, 2) for k, v in kernels.items()},
-        "training_step": train,
-        "forward_ab": ab,
-        "configs": configs,
+        "gauss_point_evals_per_s": contrib / t_fwd,
+        "samplers": samplers,
+        "kernels": {k: round(v[1], 2) for k, v in kernels.items()},
         "roofline": roof,
+        "c5_points100m_forward": c5,
+        "secondary": extras or None,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -567,11 +741,12 @@ def source_digest():
     return h.hexdigest()
 
 
-def measured_traffic(name):
-    """HBM bytes per launch of kernel `name` from the committed counter
-    summary (FETCH_SIZE + WRITE_SIZE, scaled by the copy-probe calibration),
-    or None when there is none or the kernel sources changed since."""
-    path = os.path.join(ROOT, "profiles", f"{name}_c2_step_hbm_traffic.md")
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    counter summary (FETCH_SIZE + WRITE_SIZE, scaled by the copy-probe
+    calibration), or None when there is none or the kernel sources changed
+    since."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_hbm_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -582,29 +757,21 @@ def measured_traffic(name):
     return float(val.group(1))
 
 
-def roofline(name, k, st, n_pairs, n_tests, contrib_per_point):
+def roofline(name, avg_us, launches, tests, btests, contrib, n_pairs):
     """Roofline entry of the dominant kernel: algorithmic flops (or bytes) of
     one launch over its average launch duration (HIP events on the stream the
-    kernel runs on)."""
-    avg_s = k["avg_ms"] * 1e-3
-    out = {"kernel": name, "avg_us": avg_s * 1e6, "launches_per_step": k["launches_per_step"]}
-    traffic = measured_traffic(name)
-    if name in FLOPS_PER_CONTRIB:
-        # units: the pairs the launch tests (exact: for the forward, the cell
-        # lists times the cells' queries, from the index and the plan; for the
-        # backward, the queries of each Gaussian's trimmed rows, counted by
-        # the library) and its contributing pairs (the oracle's count per
-        # point on the CPU-baseline sample, times the batch; None without it)
-        if contrib_per_point is None:
-            out.update({"bound": "alu", "achieved": None, "peak": FP32_VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
-                        "frac": None, "traffic": traffic, "pair_tests": n_tests})
-            return out
-        units = contrib_per_point * st.n
-        flops = FLOPS_PER_TEST * n_tests + FLOPS_PER_CONTRIB[name] * units
+    kernel runs on, over the timed region)."""
+    avg_s = avg_us * 1e-6
+    out = {"kernel": name, "avg_us": avg_us, "launches_per_step": launches}
+    traffic = measured_traffic(name, HEADLINE)
+    if name in FLOPS_CONTRIB:
+        t = btests if name == "bwd_gauss" else tests
+        flops = sampler_flops(name, t, contrib)
         ach = flops / avg_s / 1e12
         out.update({"bound": "alu", "achieved": ach, "peak": FP32_VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": ach / FP32_VEC_PEAK_TFLOPS, "traffic": traffic,
-                    "flops_per_launch": flops, "pair_tests": n_tests, "contributing_pairs": units})
+                    "frac": ach / FP32_VEC_PEAK_TFLOPS, "traffic": traffic, "flops_per_launch": flops,
+                    "pair_tests": t, "contributing_pairs": contrib,
+                    "hbm_frac": (traffic / avg_s / (HBM_PEAK_GBS * 1e9)) if traffic else None})
         return out
     per_pair = {"radix_downsweep": SORT_BYTES_PER_PAIR, "emit": EMIT_BYTES_PER_PAIR}.get(name)
     if per_pair is None:

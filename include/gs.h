@@ -22,8 +22,8 @@
  *     *_bytes functions. Workspace pointers must be 256-byte aligned.
  *   - Work is enqueued on the caller's stream and is asynchronous, except that
  *     gs_build_index waits once for the number of Gaussian-cell pairs,
- *     gs_densify (gs_train.h) once for the new Gaussian count and
- *     gs_backward_pair_count for its count.
+ *     gs_densify (gs_train.h) once for the new Gaussian count, and
+ *     gs_backward_pair_count and gs_sample_pair_counts for their counts.
  *   - Errors are reported as gs_status codes; gs_last_error() returns a
  *     message for the calling thread. Nothing throws across this interface.
  *   - Host-side arguments are validated (null pointers, negative counts,
@@ -74,7 +74,9 @@ typedef struct gs_gaussians {
 typedef struct gs_grid {
     float lo[3];
     float hi[3];
-    int32_t cells[3]; /* cells per axis, each > 0, product < 2^31 */
+    int32_t cells[3]; /* cells per axis, each > 0, product < 2^31 (< 2^30 for
+                         VOXELS, POINTS and JITTER queries, whose sort keys
+                         are 4 cell + quarter in 32 bits) */
 } gs_grid;
 
 /* A built index. The caller fills the buffer fields; gs_build_index fills
@@ -157,7 +159,9 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
                          hipStream_t stream);
 
 /* Bytes of plan workspace a query needs with an index of this grid (0 for
- * GRID queries; -1 cast to size_t on a malformed query). */
+ * GRID queries; -1 cast to size_t on a malformed query, or for an ordered
+ * query on a grid of 2^30 cells or more, which gs_sample rejects with
+ * GS_ERR_INVALID_ARGUMENT). */
 size_t gs_plan_bytes(const gs_query *query, const gs_grid *grid);
 
 /*
@@ -232,6 +236,21 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
 gs_status gs_backward_pair_count(const gs_index *index, const gs_query *query, const void *plan,
                                  size_t plan_bytes, void *work, size_t work_bytes, int64_t *count,
                                  hipStream_t stream);
+
+/*
+ * For measurement: the (Gaussian, query) pairs gs_sample tests against the
+ * cutoff for this built index and query (*tests: per query, the length of
+ * its cell's list; queries outside the domain test none) and how many of
+ * them pass it (*contributing: Q <= 2 ln(1/tau) in the samplers' own float32
+ * arithmetic, the pairs that enter Eq. 2; the backward's contributing pairs
+ * are the same). For VOXELS, POINTS and JITTER queries plan must be the one
+ * a gs_sample call on this index and query filled (it reads the query order
+ * and positions kept there). Uses work (gs_backward_work_bytes() bytes, its
+ * contents are overwritten) and waits on the stream for the counts.
+ */
+gs_status gs_sample_pair_counts(const gs_index *index, const gs_query *query, const void *plan, size_t plan_bytes,
+                                void *work, size_t work_bytes, int64_t *tests, int64_t *contributing,
+                                hipStream_t stream);
 
 /* Message describing the last failure on the calling thread ("" if none). */
 const char *gs_last_error(void);

@@ -569,10 +569,16 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     return GS_OK;
 }
 
+// Ordered queries (VOXELS, POINTS, JITTER) sort 32-bit keys kSub cell +
+// quarter, with kSub ncells for the outside bucket: the grid must keep
+// kSub ncells + 1 below 2^32.
+bool ordered_grid_ok(const gs_grid *g) { return (int64_t)kSub * ncells_of(g) + 1 < ((int64_t)1 << 32); }
+
 size_t gs_plan_bytes(const gs_query *query, const gs_grid *grid) {
     std::string why;
     if (!query_valid(query, &why) || !grid_valid(grid, &why)) return (size_t)-1;
     if (query->kind == GS_QUERY_GRID) return 0;
+    if (!ordered_grid_ok(grid)) return (size_t)-1;
     return plan_layout(nullptr, query->n, ncells_of(grid)).bytes;
 }
 
@@ -599,6 +605,9 @@ static gs_status check_query(const char *fn, const gs_index *index, const gs_que
             if (query->dims[j] % index->grid.cells[j] != 0)
                 return fail(GS_ERR_INVALID_ARGUMENT,
                             "%s: grid query dims must be a multiple of the index cells on every axis", fn);
+    if (query->kind != GS_QUERY_GRID && !ordered_grid_ok(&index->grid))
+        return fail(GS_ERR_INVALID_ARGUMENT,
+                    "%s: voxel, point and jitter queries need an index grid of fewer than 2^30 cells", fn);
     return GS_OK;
 }
 
@@ -696,7 +705,7 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
     }
     IndexWork w = index_layout(index->work, n, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
-    GS_TRY(launch_backward(qp, gp, w.rec, w.box, w.spans, w.gorder, n, p.order, p.point_off, p.res.pos, p.res.out, value,
+    GS_TRY(launch_backward(qp, gp, w.rec, w.box, w.spans, w.gorder, n, index->n_pairs, p.order, p.point_off, p.res.pos, p.res.out, value,
                            influence, grad_value,
                            grad_influence, cutoff_T(index->tau), bw.b, gauss->mean, gauss->scale, gauss->rot, d_mean,
                            d_scale, d_rot, d_value, d_weight, stream),
@@ -859,6 +868,49 @@ gs_status gs_backward_pair_count(const gs_index *index, const gs_query *query, c
     GS_TRY(hipEventRecord(pc->copied, stream), "gs_backward_pair_count: event");
     GS_TRY(hipEventSynchronize(pc->copied), "gs_backward_pair_count: wait");
     *count = (int64_t)*pc->value;
+    return GS_OK;
+}
+
+gs_status gs_sample_pair_counts(const gs_index *index, const gs_query *query, const void *plan, size_t plan_bytes,
+                                void *work, size_t work_bytes, int64_t *tests, int64_t *contributing,
+                                hipStream_t stream) {
+    if (!tests || !contributing)
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample_pair_counts: output counts are null");
+    *tests = *contributing = 0;
+    if (!index || index->n_pairs < 0 || index->n_pairs > index->capacity || index->n_gauss < 0 || !index->work ||
+        !index->cell_offsets)
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample_pair_counts: index not built");
+    gs_status st = check_query("gs_sample_pair_counts", index, query);
+    if (st != GS_OK) return st;
+    const int64_t nq = query_count(query);
+    const GridParams gp = grid_params(&index->grid);
+    const QueryParams qp = query_params(query, &index->grid);
+    const size_t need = bwd_layout(nullptr, index, query).bytes;
+    if (!work || work_bytes < need || !aligned(work))
+        return fail(GS_ERR_WORKSPACE, "gs_sample_pair_counts: workspace needs %zu bytes (got %zu)", need, work_bytes);
+    Plan p{};
+    if (query->kind != GS_QUERY_GRID) {
+        const size_t pneed = plan_layout(nullptr, nq, gp.ncells).bytes;
+        if (!plan || plan_bytes < pneed || !aligned(plan))
+            return fail(GS_ERR_WORKSPACE, "gs_sample_pair_counts: plan needs %zu bytes (got %zu)", pneed,
+                        plan_bytes);
+        p = plan_layout(const_cast<void *>(plan), nq, gp.ncells);
+    }
+    PinnedCount *pc = pinned_count();
+    if (!pc) return fail(GS_ERR_HIP, "gs_sample_pair_counts: could not allocate the pinned read-back word");
+    IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
+    BwdWork bw = bwd_layout(work, index, query);
+    unsigned long long *totals = (unsigned long long *)bw.b.moments;
+    GS_TRY(launch_count_sample_pairs(qp, gp, w.rec, index->gids, index->cell_offsets, p.keys, p.res.pos,
+                                     cutoff_T(index->tau), totals, stream),
+           "gs_sample_pair_counts");
+    for (int k = 0; k < 2; ++k) {
+        GS_TRY(hipMemcpyAsync(pc->value, totals + k, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
+               "gs_sample_pair_counts: read-back");
+        GS_TRY(hipEventRecord(pc->copied, stream), "gs_sample_pair_counts: event");
+        GS_TRY(hipEventSynchronize(pc->copied), "gs_sample_pair_counts: wait");
+        (k == 0 ? *tests : *contributing) = (int64_t)*pc->value;
+    }
     return GS_OK;
 }
 

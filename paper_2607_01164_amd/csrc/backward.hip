@@ -217,10 +217,24 @@ __device__ __forceinline__ void drain(const Record &r, const float4 *qu, const u
     }
 }
 
-// Gaussians per wavefront: consecutive Gaussians of gorder share a wave;
-// below kPackMinGauss Gaussians one per wave (4 would leave SIMDs idle).
+// The per-Gaussian kernel runs one wave per workgroup: its waves are
+// independent (each has its own LDS queue) and their costs vary with the
+// Gaussians' boxes; a workgroup keeps its LDS until its slowest wave ends.
+// Waves are taken in launch order (dealt round-robin over the XCDs by the
+// dispatcher), so every XCD works on the same stretch of the spatial order
+// at a time rather than on a fixed eighth of it.
+constexpr int kBwdWaves = 1;
+constexpr int kBwdBlock = kBwdWaves * kWave;
+
+// Gaussians per wavefront: consecutive Gaussians of gorder share a wave, so
+// that their rows are found together. Below kPackMinGauss Gaussians one per
+// wave (more would leave SIMDs idle); otherwise kPack, or kPackLarge when
+// the boxes list at least kLargeBoxCells cells on average (a wave's cost
+// grows with its Gaussians' boxes, and fewer per wave balance better).
 constexpr uint32_t kPack = 4;
+constexpr uint32_t kPackLarge = 2;
 constexpr int64_t kPackMinGauss = 65536;
+constexpr int64_t kLargeBoxCells = 32;
 
 // Partials of the wave's current Gaussian are reduced over the wave and
 // stored: lane k < 12 writes moment k (the 12th is 0).
@@ -261,7 +275,7 @@ __device__ __forceinline__ void acc_zero(Acc &acc) {
 // the spatial order of the index (the cell key of their box corner), so the
 // waves resident at one time work on one region and find its points in L2.
 template <bool GRID, uint32_t PACK>
-__global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridParams g, const Record *__restrict__ rec,
+__global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                            const CellBox *__restrict__ box,
                                                            const uint8_t *__restrict__ spans,
                                                            const uint32_t *__restrict__ gorder, int64_t n_gauss,
@@ -269,11 +283,11 @@ __global__ __launch_bounds__(kBlock) void k_backward_gauss(QueryParams q, GridPa
                                                            const float4 *__restrict__ plan_pos,
                                                            const float2 *__restrict__ ab, float T,
                                                            float *__restrict__ moments) {
-    __shared__ float4 s_qu[kWavesPerBlock][kQueue];
-    __shared__ uint32_t s_qk[kWavesPerBlock][kQueue];
+    __shared__ float4 s_qu[kBwdWaves][kQueue];
+    __shared__ uint32_t s_qk[kBwdWaves][kQueue];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t wib = threadIdx.x / kWave;
-    const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + wib;
+    const uint64_t w = (uint64_t)blockIdx.x * kBwdWaves + wib;
     const uint64_t first = w * PACK;
     if (first >= (uint64_t)n_gauss) return;
     const uint32_t nk = (uint64_t)n_gauss - first < PACK ? (uint32_t)((uint64_t)n_gauss - first) : PACK;
@@ -596,6 +610,21 @@ __global__ __launch_bounds__(kBlock) void k_count_backward_pairs(QueryParams q, 
     }
 }
 
+template <bool GRID>
+void launch_gauss(uint32_t pack, uint32_t wblocks, hipStream_t s, const QueryParams &q, const GridParams &g,
+                  const Record *rec, const CellBox *box, const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss,
+                  const uint32_t *point_off, const float4 *plan_pos, const float2 *ab, float T, float *moments) {
+    if (pack == 1)
+        hipLaunchKernelGGL((k_backward_gauss<GRID, 1>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, rec, box, spans,
+                           gorder, n_gauss, point_off, plan_pos, ab, T, moments);
+    else if (pack == kPackLarge)
+        hipLaunchKernelGGL((k_backward_gauss<GRID, kPackLarge>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, rec, box,
+                           spans, gorder, n_gauss, point_off, plan_pos, ab, T, moments);
+    else
+        hipLaunchKernelGGL((k_backward_gauss<GRID, kPack>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, rec, box,
+                           spans, gorder, n_gauss, point_off, plan_pos, ab, T, moments);
+}
+
 }  // namespace
 
 hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g, const CellBox *box,
@@ -609,7 +638,8 @@ hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g
 }
 
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
-                           const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
+                           const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, int64_t n_pairs,
+                           const uint32_t *order, const uint32_t *point_off,
                            const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
@@ -635,21 +665,15 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Reco
         prof_end("bwd_stage", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         // few Gaussians: one per wave, so that they still fill the chip
-        const int64_t pack = n_gauss < kPackMinGauss ? 1 : kPack;
-        const uint32_t wblocks = (uint32_t)((n_gauss + pack * kWavesPerBlock - 1) / (pack * kWavesPerBlock));
+        const uint32_t pack = n_gauss < kPackMinGauss ? 1u : (n_pairs >= kLargeBoxCells * n_gauss ? kPackLarge : kPack);
+        const uint32_t wblocks = (uint32_t)((n_gauss + pack * kBwdWaves - 1) / (pack * kBwdWaves));
         prof_begin("bwd_gauss", s);
-        if (grid && pack == 1)
-            hipLaunchKernelGGL((k_backward_gauss<true, 1>), dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans,
-                               gorder, n_gauss, point_off, plan_pos, b.ab, T, b.moments);
-        else if (grid)
-            hipLaunchKernelGGL((k_backward_gauss<true, kPack>), dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box,
-                               spans, gorder, n_gauss, point_off, plan_pos, b.ab, T, b.moments);
-        else if (pack == 1)
-            hipLaunchKernelGGL((k_backward_gauss<false, 1>), dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box, spans,
-                               gorder, n_gauss, point_off, plan_pos, b.ab, T, b.moments);
+        if (grid)
+            launch_gauss<true>(pack, wblocks, s, q, g, rec, box, spans, gorder, n_gauss, point_off, plan_pos, b.ab, T,
+                               b.moments);
         else
-            hipLaunchKernelGGL((k_backward_gauss<false, kPack>), dim3(wblocks), dim3(kBlock), 0, s, q, g, rec, box,
-                               spans, gorder, n_gauss, point_off, plan_pos, b.ab, T, b.moments);
+            launch_gauss<false>(pack, wblocks, s, q, g, rec, box, spans, gorder, n_gauss, point_off, plan_pos, b.ab, T,
+                                b.moments);
         prof_end("bwd_gauss", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {

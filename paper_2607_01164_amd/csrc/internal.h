@@ -367,6 +367,14 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
                                 const PlanResults &pr, hipStream_t s);
 
+// Pairs the forward tests and those passing the cutoff (measurement), into
+// totals[0] and totals[1] (device, 16 bytes); plan_keys and plan_pos are
+// the sorted keys and the positions a forward left in the plan (unused for
+// GRID queries).
+hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const Record *rec,
+                                     const uint32_t *gids, const uint32_t *cell_off, const uint32_t *plan_keys,
+                                     const float4 *plan_pos, float T, unsigned long long *totals, hipStream_t s);
+
 // Gaussians in spatial order: sorted by the cell key of their box's low
 // corner (empty boxes last), so neighbouring work shares cached queries.
 hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g, int shift, uint32_t *keys,
@@ -382,8 +390,10 @@ struct BackwardBuffers {
 hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g, const CellBox *box,
                                       const uint8_t *spans, int64_t n_gauss, const uint32_t *point_off,
                                       unsigned long long *total, hipStream_t s);
+// n_pairs: the index's pair count (it sets how many Gaussians share a wave)
 hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
-                           const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, const uint32_t *order, const uint32_t *point_off,
+                           const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, int64_t n_pairs,
+                           const uint32_t *order, const uint32_t *point_off,
                            const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
                            const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,

@@ -336,34 +336,26 @@ __global__ __launch_bounds__(kBlock) void k_pair_offsets(uint64_t *__restrict__ 
     }
 }
 
-// offsets[k] = number of keys < k. Thread t covers the boundaries before
-// keys 4t .. 4t+3 (and the end, after key n-1), reading its four keys with
-// one 16-byte load where the array is 16-byte aligned.
+// offsets[k] = number of keys < k, for k = 0 .. nkeys: thread k finds the
+// first sorted key >= k by binary search (keys past the end count as
+// nkeys). Every offset is found on its own, so a long run of empty keys
+// costs no more than a short one, and neighbouring threads follow nearly
+// the same search path through the same cache lines.
 __global__ __launch_bounds__(kBlock) void k_key_offsets(const uint32_t *__restrict__ keys, int64_t n,
                                                         uint32_t *__restrict__ off, int64_t nkeys) {
-    const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-    if (i0 > n) return;
-    uint32_t k4[4];
-    if (i0 + 4 <= n && (reinterpret_cast<uintptr_t>(keys) & 15u) == 0) {
-        const uint4 q = *(const uint4 *)(keys + i0);
-        k4[0] = q.x;
-        k4[1] = q.y;
-        k4[2] = q.z;
-        k4[3] = q.w;
-    } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) k4[i] = i0 + i < n ? keys[i0 + i] : 0u;
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k > nkeys) return;
+    uint64_t lo = 0, len = (uint64_t)n;
+    while (len > 0) {
+        const uint64_t half = len >> 1;
+        if ((int64_t)keys[lo + half] < k) {
+            lo += half + 1;
+            len -= half + 1;
+        } else {
+            len = half;
+        }
     }
-    int64_t prev = (i0 == 0) ? -1 : (int64_t)keys[i0 - 1];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t idx = i0 + i;
-        if (idx > n) break;
-        int64_t cur = idx == n ? nkeys : (int64_t)k4[i];
-        cur = cur < nkeys ? cur : nkeys;
-        for (int64_t k = prev + 1; k <= cur; ++k) off[k] = (uint32_t)idx;
-        prev = cur > prev ? cur : prev;
-    }
+    off[k] = (uint32_t)lo;
 }
 
 __global__ void k_fill_u32(uint32_t *p, uint32_t v, int64_t n) {
@@ -492,7 +484,7 @@ hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *
 }
 
 hipError_t key_offsets(const uint32_t *sorted_keys, int64_t n, uint32_t *offsets, int64_t nkeys, hipStream_t s) {
-    const int64_t threads = n / 4 + 1;
+    const int64_t threads = nkeys + 1;
     prof_begin("key_offsets", s);
     hipLaunchKernelGGL(k_key_offsets, dim3((uint32_t)ceil_div(threads, kBlock)), dim3(kBlock), 0, s, sorted_keys, n,
                        offsets, nkeys);

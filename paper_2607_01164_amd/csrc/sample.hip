@@ -24,40 +24,35 @@ namespace {
 // -1/2 log2(e): G = exp(-Q/2) = 2^(Q * kNegHalfLog2e)
 constexpr float kNegHalfLog2e = -0.72134752044448170368f;
 
-__device__ __forceinline__ void accumulate(const Record &r, float px, float py, float pz, float T, float &I,
-                                           float &V) {
+// The samplers run one wave per workgroup. Their waves are independent
+// (each has its own LDS buffer) and the cost of a work item varies by
+// orders of magnitude with the cell's list and queries: a workgroup keeps
+// its LDS until its slowest wave ends, so one-wave workgroups hand a
+// finished wave's slot and LDS straight to new work. Work items are taken
+// in launch order, which the dispatcher deals round-robin over the XCDs:
+// with a fixed block-to-XCD remap, each XCD would own one contiguous
+// stretch of cells, and clustered data would leave most XCDs idle while
+// one works through the dense part.
+constexpr int kSampWaves = 1;
+constexpr int kSampBlock = kSampWaves * kWave;
+
+// Q = |M (p - mu)|^2 of a record at a point, in the one order of float32
+// operations every sampler and the pair counter use.
+__device__ __forceinline__ float cutoff_q(const Record &r, float px, float py, float pz) {
     const float dx = px - r.r0.x, dy = py - r.r0.y, dz = pz - r.r0.z;
     const float u0 = fmaf_(r.r1.x, dx, fmaf_(r.r1.y, dy, r.r1.z * dz));
     const float u1 = fmaf_(r.r2.x, dx, fmaf_(r.r2.y, dy, r.r2.z * dz));
     const float u2 = fmaf_(r.r3.x, dx, fmaf_(r.r3.y, dy, r.r3.z * dz));
-    const float Q = fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
+    return fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
+}
+
+__device__ __forceinline__ void accumulate(const Record &r, float px, float py, float pz, float T, float &I,
+                                           float &V) {
+    const float Q = cutoff_q(r, px, py, pz);
     if (Q <= T) {
         const float a = r.r0.w * exp2_hw(Q * kNegHalfLog2e);
         I += a;
         V = fmaf_(a, r.r1.w, V);
-    }
-}
-
-// Walk a wave-uniform candidate list [j0, j1) for one query per lane, ids
-// and records through the scalar cache, two candidates at a time. The work
-// items of a cell with many queries walk the same list at about the same
-// time on one compute unit and share its records in that cache.
-__device__ __forceinline__ void walk_scalar(const Record *rec, const uint32_t *gids, uint32_t j0, uint32_t j1,
-                                            float px, float py, float pz, float T, float &I, float &V) {
-    ConstU32 *cg = (ConstU32 *)gids;
-    uint32_t j = j0;
-    for (; j + 2 <= j1; j += 2) {
-        const uint32_t g0 = __builtin_amdgcn_readfirstlane(cg[j]);
-        const uint32_t g1 = __builtin_amdgcn_readfirstlane(cg[j + 1]);
-        const Record a = load_record_uniform(rec, g0);
-        const Record b = load_record_uniform(rec, g1);
-        accumulate(a, px, py, pz, T, I, V);
-        accumulate(b, px, py, pz, T, I, V);
-    }
-    if (j < j1) {
-        const uint32_t g0 = __builtin_amdgcn_readfirstlane(cg[j]);
-        const Record a = load_record_uniform(rec, g0);
-        accumulate(a, px, py, pz, T, I, V);
     }
 }
 
@@ -110,12 +105,46 @@ __device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, cons
     }
 }
 
+// R queries per lane against a wave-uniform list [ja, jb), staged in the
+// wave's LDS planes 64 records at a time as in walk_staged: each record
+// read there serves the lane's R queries.
+template <uint32_t R>
+__device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
+                                              uint32_t ja, uint32_t jb, uint32_t lane, float4 *buf,
+                                              const float (&px)[R], const float (&py)[R], const float (&pz)[R],
+                                              float T, float (&I)[R], float (&V)[R]) {
+    uint32_t gnext = 0;
+    if (ja < jb) gnext = gids[ja + lane < jb ? ja + lane : jb - 1];
+    for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
+        const float4 *src = (const float4 *)(rec + gnext);
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq)
+            __builtin_amdgcn_global_load_lds((const void *)(src + qq),
+                                             (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
+        if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_wave_barrier();
+        const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
+        for (uint32_t s = 0; s < cnt; ++s) {
+            Record a;
+            a.r0 = buf[s];
+            a.r1 = buf[kWave + s];
+            a.r2 = buf[2 * kWave + s];
+            a.r3 = buf[3 * kWave + s];
+#pragma unroll
+            for (uint32_t t = 0; t < R; ++t) accumulate(a, px[t], py[t], pz[t], T, I[t], V[t]);
+        }
+        // every lane has read the planes before the next chunk overwrites them
+        __builtin_amdgcn_wave_barrier();
+    }
+}
 
-__global__ __launch_bounds__(kBlock) void k_sample_grid(QueryParams q, GridParams g, const Record *__restrict__ rec,
+
+__global__ __launch_bounds__(kSampBlock) void k_sample_grid(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                         const uint32_t *__restrict__ gids,
                                                         const uint32_t *__restrict__ cell_off, float T, float tau,
                                                         float *__restrict__ out_v, float *__restrict__ out_i) {
-    __shared__ float4 s_grec[kWavesPerBlock][4 * kWave];
+    __shared__ float4 s_grec[kSampWaves][4 * kWave];
     const uint32_t rx = (uint32_t)(q.dims[0] / g.cells[0]);
     const uint32_t ry = (uint32_t)(q.dims[1] / g.cells[1]);
     const uint32_t rz = (uint32_t)(q.dims[2] / g.cells[2]);
@@ -123,7 +152,7 @@ __global__ __launch_bounds__(kBlock) void k_sample_grid(QueryParams q, GridParam
     const uint32_t wpc = (vpc + kWave - 1) / kWave;
     const uint32_t lane = threadIdx.x % kWave;
     const uint64_t wave_id =
-        (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave;
+        (uint64_t)blockIdx.x * kSampWaves + threadIdx.x / kWave;
     const uint64_t cell = wave_id / wpc;
     if (cell >= (uint64_t)g.ncells) return;
     const uint32_t chunk = (uint32_t)(wave_id - cell * wpc);
@@ -191,24 +220,29 @@ __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams
 }
 
 // Work items of the ordered-query sampler: one per cell holding fewer than
-// kDenseMin queries, one per 64 queries of a denser cell. The bucket of
-// queries outside the domain (key ncells) is an item with an empty list.
+// 2 kDenseMin queries, one per kDenseItem queries of a denser cell. The
+// bucket of queries outside the domain (key ncells) is an item with an
+// empty list.
 constexpr uint32_t kDenseMin = 32;
-// From this many queries (five work items of 64) a cell's items walk its
-// candidates through the scalar cache, where the items share the records;
-// fewer items stage the records in LDS instead.
-constexpr uint32_t kScalarWalkMin = 320;
+// A cell of at least 2 kDenseMin queries is dense: lanes are its queries,
+// kDenseR per lane, so each record read from LDS serves kDenseR queries
+// (one per lane leaves the walk bound by LDS reads: four 16-byte broadcast
+// reads per candidate against 16 VALU operations). Its work items take at
+// most kDenseItem queries each, the cell's queries split evenly over them.
+constexpr uint32_t kDenseR = 2;
+constexpr uint32_t kDenseItem = kDenseR * kWave;
 constexpr uint32_t kChunkB = 8;  // queries evaluated together by a sparse-cell item
 constexpr uint32_t kRowsMin = 4;                 // from this many queries a cell uses 4 query rows
 constexpr uint32_t kRowsMax = (kDenseMin + 3) / 4;  // queries per row at most
 
 // Work items per bucket (cell, and the outside bucket last): none for an
-// empty bucket, one for a sparse one, one per 64 queries of a dense one.
+// empty bucket, one for a sparse one, one per kDenseItem queries of a dense
+// one.
 __device__ __forceinline__ uint32_t bucket_items(const uint32_t *point_off, int64_t c, int64_t nbuckets) {
     if (c >= nbuckets) return 0u;
     // the outside bucket (c = nbuckets - 1) has a single key
     const uint32_t n = point_off[c + 1 < nbuckets ? kSub * (c + 1) : kSub * c + 1] - point_off[kSub * c];
-    return n == 0 ? 0u : (n < kDenseMin ? 1u : (n + kWave - 1) / kWave);
+    return n == 0 ? 0u : (n < 2 * kDenseMin ? 1u : (n + kDenseItem - 1) / kDenseItem);
 }
 
 // Buckets are taken kItemGroup at a time (kItemsPerThread per thread).
@@ -269,11 +303,7 @@ __global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restr
 }
 
 __device__ __forceinline__ float eval_a(const Record &r, float px, float py, float pz, float T) {
-    const float dx = px - r.r0.x, dy = py - r.r0.y, dz = pz - r.r0.z;
-    const float u0 = fmaf_(r.r1.x, dx, fmaf_(r.r1.y, dy, r.r1.z * dz));
-    const float u1 = fmaf_(r.r2.x, dx, fmaf_(r.r2.y, dy, r.r2.z * dz));
-    const float u2 = fmaf_(r.r3.x, dx, fmaf_(r.r3.y, dy, r.r3.z * dz));
-    const float Q = fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
+    const float Q = cutoff_q(r, px, py, pz);
     return Q <= T ? r.r0.w * exp2_hw(Q * kNegHalfLog2e) : 0.0f;
 }
 
@@ -398,10 +428,41 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
             write_out(Io, Vo, tau, wvalid && c < ncells, wpid, pa + qi, wx, wy, wz, out_v, out_i, pr);
 }
 
+// A dense cell's work item: queries [qa, qa + qn) of the plan, qn <= 64 R;
+// lane l takes queries qa + l + 64 t, t < R.
+template <uint32_t R>
+__device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t qn, uint32_t ja,
+                                           uint32_t jb, uint32_t c, uint32_t ncells, const QueryParams &q,
+                                           const GridParams &g, const Record *__restrict__ rec,
+                                           const uint32_t *__restrict__ gids, const uint32_t *__restrict__ order,
+                                           float T, float tau, float *__restrict__ out_v, float *__restrict__ out_i,
+                                           const PlanResults &pr, float4 *buf) {
+    float px[R], py[R], pz[R], I[R], V[R];
+    uint32_t pid[R];
+    bool valid[R];
+#pragma unroll
+    for (uint32_t t = 0; t < R; ++t) {
+        px[t] = py[t] = pz[t] = 0.0f;
+        I[t] = V[t] = 0.0f;
+        pid[t] = 0xFFFFFFFFu;
+        valid[t] = false;
+        if (lane + kWave * t < qn) {
+            pid[t] = order[qa + lane + kWave * t];
+            if ((int64_t)pid[t] < q.n) query_position(q, g, pid[t], px[t], py[t], pz[t], valid[t]);
+        }
+    }
+    walk_staged_r<R>(rec, gids, ja, jb, lane, buf, px, py, pz, T, I, V);
+#pragma unroll
+    for (uint32_t t = 0; t < R; ++t)
+        if (lane + kWave * t < qn && (int64_t)pid[t] < q.n)
+            write_out(I[t], V[t], tau, valid[t] && c < ncells, pid[t], qa + lane + kWave * t, px[t], py[t], pz[t],
+                      out_v, out_i, pr);
+}
+
 // One wavefront per item, by the queries n of the cell:
-//  * n >= 64: lanes are queries (64 per item) and walk the list together,
-//    records staged in LDS below kScalarWalkMin queries, through the scalar
-//    cache from there (the cell's items then share them);
+//  * n >= 64: lanes are queries, up to kDenseR each (kDenseItem queries per
+//    item, a cell's queries split evenly over its items), and walk the list
+//    together, the records staged in LDS;
 //  * 4 <= n < 64: query rows x candidate slots (4 x 16 below 32 queries,
 //    8 x 8 from 32), records staged in LDS 64 at a time;
 //  * n < 4: lanes are the cell's candidates (64 at a time) and the queries
@@ -409,10 +470,8 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
 // Every query's sums are reduced in a fixed order.
 // Seven waves per SIMD (at most 72 VGPRs; the compiler keeps a few values in
 // scratch): the row layouts' per-row arrays would otherwise take 83 VGPRs and
-// leave five, and the dense-cell walks need the extra waves to hide their
-// loads (C4 5.76 -> 5.13 ms, C5 166 -> 145 ms; eight waves spill enough to
-// slow the row layouts by a sixth).
-__global__ __launch_bounds__(kBlock, 7) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
+// leave five.
+__global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                          const uint32_t *__restrict__ gids,
                                                          const uint32_t *__restrict__ cell_off,
                                                          const uint32_t *__restrict__ point_off,
@@ -423,10 +482,10 @@ __global__ __launch_bounds__(kBlock, 7) void k_sample_cells(QueryParams q, GridP
                                                          float *__restrict__ out_i, PlanResults pr) {
     // per wave: the records of 64 candidates, as four 1 KiB planes of 16-byte
     // quarters (quarter q of candidate s at [q][s])
-    __shared__ float4 s_rec[kWavesPerBlock][4 * kWave];
+    __shared__ float4 s_rec[kSampWaves][4 * kWave];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t ncells = (uint32_t)g.ncells;
-    const uint64_t w = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave;
+    const uint64_t w = (uint64_t)blockIdx.x * kSampWaves + threadIdx.x / kWave;
     const uint32_t tot = ((ConstU32 *)item_off)[ncells + 1];
     const uint64_t total = tot < (uint64_t)max_items ? tot : (uint64_t)max_items;
     if (w >= total) return;
@@ -441,22 +500,16 @@ __global__ __launch_bounds__(kBlock, 7) void k_sample_cells(QueryParams q, GridP
         jb = ((ConstU32 *)cell_off)[c + 1];
     }
     if (n >= 2 * kDenseMin) {
-        const uint32_t k = pa + chunk * kWave + lane;
-        const bool active = k < pb;
-        uint32_t pid = 0;
-        float px = 0.0f, py = 0.0f, pz = 0.0f;
-        bool valid = false;
-        if (active) {
-            pid = order[k];
-            if ((int64_t)pid < q.n) query_position(q, g, pid, px, py, pz, valid);
-        }
-        float I = 0.0f, V = 0.0f;
-        if (n >= kScalarWalkMin)
-            walk_scalar(rec, gids, ja, jb, px, py, pz, T, I, V);
+        const uint32_t nit = (n + kDenseItem - 1) / kDenseItem;
+        const uint32_t per = (n + nit - 1) / nit;
+        const uint32_t qa = pa + chunk * per;
+        const uint32_t qn = pb - qa < per ? pb - qa : per;
+        float4 *buf = s_rec[threadIdx.x / kWave];
+        if (qn <= (uint32_t)kWave)
+            dense_item<1>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr, buf);
         else
-            walk_staged(rec, gids, ja, jb, lane, s_rec[threadIdx.x / kWave], px, py, pz, T, I, V);
-        if (active && (int64_t)pid < q.n)
-            write_out(I, V, tau, valid && c < ncells, pid, k, px, py, pz, out_v, out_i, pr);
+            dense_item<kDenseR>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr,
+                                buf);
         return;
     }
     if (n >= kRowsMin) {
@@ -513,7 +566,79 @@ __global__ __launch_bounds__(kBlock, 7) void k_sample_cells(QueryParams q, GridP
     }
 }
 
+// Pairs the forward tests and the pairs among them that pass the cutoff,
+// for measurement: thread t takes query t of the grid (x fastest) or the
+// t-th query in plan order, walks its cell's list with the samplers' own
+// float32 test and counts. Summed per block, then into totals[0] (tests)
+// and totals[1] (passing) with one integer atomic each per block (the sums
+// do not depend on their order).
+__global__ __launch_bounds__(kBlock) void k_count_sample_pairs(QueryParams q, GridParams g,
+                                                               const Record *__restrict__ rec,
+                                                               const uint32_t *__restrict__ gids,
+                                                               const uint32_t *__restrict__ cell_off,
+                                                               const uint32_t *__restrict__ plan_keys,
+                                                               const float4 *__restrict__ plan_pos, float T,
+                                                               unsigned long long *totals) {
+    __shared__ unsigned long long lds[2][kWavesPerBlock];
+    const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    unsigned long long tests = 0, hits = 0;
+    if (t < q.n) {
+        int64_t c = -1;
+        float px = 0.0f, py = 0.0f, pz = 0.0f;
+        if (q.kind == 0) {
+            const uint32_t nx = (uint32_t)q.dims[0], ny = (uint32_t)q.dims[1];
+            const uint32_t vx = (uint32_t)(t % nx), vy = (uint32_t)((t / nx) % ny), vz = (uint32_t)(t / ((int64_t)nx * ny));
+            const uint32_t rx = nx / (uint32_t)g.cells[0], ry = ny / (uint32_t)g.cells[1];
+            const uint32_t rz = (uint32_t)q.dims[2] / (uint32_t)g.cells[2];
+            c = (int64_t)(vx / rx) + (int64_t)g.cells[0] * ((int64_t)(vy / ry) + (int64_t)g.cells[1] * (vz / rz));
+            px = voxel_center((int32_t)vx, g.lo[0], q.vsz[0]);
+            py = voxel_center((int32_t)vy, g.lo[1], q.vsz[1]);
+            pz = voxel_center((int32_t)vz, g.lo[2], q.vsz[2]);
+        } else {
+            const uint32_t cc = plan_keys[t] / kSub;
+            if ((int64_t)cc < g.ncells) {
+                c = cc;
+                const float4 p = plan_pos[t];
+                px = p.x;
+                py = p.y;
+                pz = p.z;
+            }
+        }
+        if (c >= 0) {
+            const uint32_t j0 = cell_off[c], j1 = cell_off[c + 1];
+            tests = j1 - j0;
+            for (uint32_t j = j0; j < j1; ++j) hits += cutoff_q(rec[gids[j]], px, py, pz) <= T ? 1u : 0u;
+        }
+    }
+    const uint32_t lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        tests += __shfl_xor(tests, o, kWave);
+        hits += __shfl_xor(hits, o, kWave);
+    }
+    if (lane == 0) {
+        lds[0][wid] = tests;
+        lds[1][wid] = hits;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {
+        unsigned long long s = 0;
+        for (int w = 0; w < kWavesPerBlock; ++w) s += lds[threadIdx.x][w];
+        if (s) atomicAdd(totals + threadIdx.x, s);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const Record *rec,
+                                     const uint32_t *gids, const uint32_t *cell_off, const uint32_t *plan_keys,
+                                     const float4 *plan_pos, float T, unsigned long long *totals, hipStream_t s) {
+    hipError_t e = fill_u32((uint32_t *)totals, 0u, 4, s);
+    if (e != hipSuccess || q.n <= 0) return e;
+    hipLaunchKernelGGL(k_count_sample_pairs, dim3((uint32_t)((q.n + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, q, g,
+                       rec, gids, cell_off, plan_keys, plan_pos, T, totals);
+    return hipGetLastError();
+}
 
 hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids,
                              const RadixPass0 &pass0, hipStream_t s) {
@@ -531,10 +656,10 @@ hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const R
     const int64_t vpc = (int64_t)(q.dims[0] / g.cells[0]) * (q.dims[1] / g.cells[1]) * (q.dims[2] / g.cells[2]);
     const int64_t wpc = (vpc + kWave - 1) / kWave;
     const int64_t waves = g.ncells * wpc;
-    const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    const int64_t blocks = (waves + kSampWaves - 1) / kSampWaves;
     if (blocks <= 0) return hipSuccess;
     prof_begin("sample_grid", s);
-    hipLaunchKernelGGL(k_sample_grid, dim3((uint32_t)blocks), dim3(kBlock), 0, s, q, g, rec, gids, cell_off, T, tau,
+    hipLaunchKernelGGL(k_sample_grid, dim3((uint32_t)blocks), dim3(kSampBlock), 0, s, q, g, rec, gids, cell_off, T, tau,
                        out_v, out_i);
     prof_end("sample_grid", s);
     return hipGetLastError();
@@ -561,8 +686,8 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
     prof_end("cell_items", s);
     if (e != hipSuccess) return e;
     prof_begin("sample_points", s);
-    hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kWavesPerBlock - 1) / kWavesPerBlock)),
-                       dim3(kBlock), 0, s, q, g, rec, gids, cell_off, point_off, order, it.item_off, it.items,
+    hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kSampWaves - 1) / kSampWaves)),
+                       dim3(kSampBlock), 0, s, q, g, rec, gids, cell_off, point_off, order, it.item_off, it.items,
                        it.max_items, T, tau, out_v, out_i, pr);
     prof_end("sample_points", s);
     return hipGetLastError();

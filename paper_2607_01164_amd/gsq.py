@@ -33,7 +33,8 @@ EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_b
             "gs_backward_work_bytes", "gs_sample_backward", "gs_last_error", "gs_version", "gs_profile_enable",
             "gs_profile_select", "gs_profile_reset", "gs_profile_read", "gs_activate", "gs_activate_backward",
             "gs_loss_work_bytes", "gs_loss", "gs_densify_work_bytes", "gs_densify",
-            "gs_sample_gaussian_major_work_bytes", "gs_sample_gaussian_major", "gs_backward_pair_count")
+            "gs_sample_gaussian_major_work_bytes", "gs_sample_gaussian_major", "gs_backward_pair_count",
+            "gs_sample_pair_counts")
 
 
 class GsLibraryMissing(RuntimeError):
@@ -112,6 +113,8 @@ def load_library():
     L.gs_sample_gaussian_major.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, vp, vp, sz, vp, sz, vp]
     L.gs_backward_pair_count.restype = ctypes.c_int
     L.gs_backward_pair_count.argtypes = [P(GsIndex), P(GsQuery), vp, sz, vp, sz, P(i64), vp]
+    L.gs_sample_pair_counts.restype = ctypes.c_int
+    L.gs_sample_pair_counts.argtypes = [P(GsIndex), P(GsQuery), vp, sz, vp, sz, P(i64), P(i64), vp]
     L.gs_backward_work_bytes.restype = sz
     L.gs_backward_work_bytes.argtypes = [P(GsIndex), P(GsQuery)]
     L.gs_sample_backward.restype = ctypes.c_int
@@ -621,6 +624,20 @@ def backward_pair_count(index: Index, query: Query, plan: Optional[torch.Tensor]
                                                ctypes.byref(out), _stream(stream))
     _check(st)
     return int(out.value)
+
+
+def sample_pair_counts(index: Index, query: Query, plan: Optional[torch.Tensor], work: torch.Tensor,
+                       stream=None):
+    """(tests, contributing): the (Gaussian, query) pairs gs_sample tests and
+    those passing the cutoff, for measurement (plan: the one a gs_sample call
+    filled; waits for the counts; overwrites work)."""
+    q = query.c()
+    t, c = ctypes.c_int64(0), ctypes.c_int64(0)
+    st = load_library().gs_sample_pair_counts(ctypes.byref(index.c), ctypes.byref(q), _ptr(plan),
+                                              0 if plan is None else plan.numel(), work.data_ptr(), work.numel(),
+                                              ctypes.byref(t), ctypes.byref(c), _stream(stream))
+    _check(st)
+    return int(t.value), int(c.value)
 
 
 def profile_enable(on: bool = True) -> None:

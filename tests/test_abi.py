@@ -197,6 +197,47 @@ def test_sample_validates_queries():
     assert st == gs.GS_ERR_INVALID_ARGUMENT
 
 
+def test_ordered_queries_reject_grids_of_2_30_cells():
+    """Voxel, point and jitter queries sort 32-bit keys 4 cell + quarter (the
+    outside bucket last): a grid of 2^30 cells or more is refused before any
+    device work, while grid queries may use it."""
+    L = gs.load_library()
+    big = grid((1024, 1024, 1024))
+    ok = grid((1024, 1024, 1023))
+    qp = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 100, None, FAKE)
+    assert L.gs_plan_bytes(ctypes.byref(qp), ctypes.byref(big)) == SIZE_ERR
+    assert L.gs_plan_bytes(ctypes.byref(qp), ctypes.byref(ok)) != SIZE_ERR
+    idx = built_fake_index()
+    idx.grid = big
+    st = L.gs_sample(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(qp), FAKE, FAKE, FAKE, 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"2^30" in L.gs_last_error()
+    qv = gsq.GsQuery(gs.GS_QUERY_VOXELS, (ctypes.c_int32 * 3)(1024, 1024, 1024), 100, FAKE, None)
+    st = L.gs_sample(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(qv), FAKE, FAKE, FAKE, 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"2^30" in L.gs_last_error()
+    qg = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(1024, 1024, 1024), 0, None, None)
+    assert L.gs_plan_bytes(ctypes.byref(qg), ctypes.byref(big)) == 0
+
+
+def test_pair_counts_validate_arguments():
+    L = gs.load_library()
+    t, c = ctypes.c_int64(7), ctypes.c_int64(7)
+    q = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 100, None, FAKE)
+    st = L.gs_sample_pair_counts(ctypes.byref(fake_index()), ctypes.byref(q), FAKE, 1 << 30, FAKE, 1 << 30,
+                                 ctypes.byref(t), ctypes.byref(c), None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"not built" in L.gs_last_error()
+    assert t.value == 0 and c.value == 0
+    idx = built_fake_index()
+    st = L.gs_sample_pair_counts(ctypes.byref(idx), ctypes.byref(q), FAKE, 16, FAKE, 1 << 30, ctypes.byref(t),
+                                 ctypes.byref(c), None)
+    assert st == gs.GS_ERR_WORKSPACE and b"plan" in L.gs_last_error()
+    st = L.gs_sample_pair_counts(ctypes.byref(idx), ctypes.byref(q), FAKE, 1 << 30, FAKE, 8, ctypes.byref(t),
+                                 ctypes.byref(c), None)
+    assert st == gs.GS_ERR_WORKSPACE
+    st = L.gs_sample_pair_counts(ctypes.byref(idx), ctypes.byref(q), FAKE, 1 << 30, FAKE, 1 << 30, None,
+                                 ctypes.byref(c), None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+
+
 def test_backward_validates_arguments():
     L = gs.load_library()
     idx = built_fake_index()
