@@ -4,8 +4,9 @@ TEST INFRASTRUCTURE ONLY: imported by the tests, by the smoke check and by
 the benchmark's CPU-baseline leg, never by the product library. It is an
 independent float64 brute-force implementation (oracle.c) of the paper's
 Eq. 2 and Eq. 3 with the cutoff of Sec. 4.1.1 and the definedness rule of
-Sec. 4.1.3, their exact derivatives (Sec. 4.1.4), and the canonical float32
-cell index (Sec. 4.1.1, Sec. 4.1.2); and (train.c) the training steps on
+Sec. 4.1.3, their exact derivatives (Sec. 4.1.4), the canonical float32
+cell boxes with their block lists (Sec. 4.1.1, Sec. 4.1.2) and the cells each
+Gaussian reaches (an exact float64 minimum of Q over every cell); and (train.c) the training steps on
 either side of the path: the activations of Sec. 4.2 and the losses of
 Sec. 4.2, Eq. 4 and Eq. 5 with their cotangents.
 
@@ -40,10 +41,10 @@ def lib():
         L = ctypes.CDLL(path)
         L.orc_forward.restype = c_int
         L.orc_forward.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, c_int, c_int,
-                                  vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+                                  vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.orc_backward.restype = c_int
         L.orc_backward.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, vp, vp, vp, vp, vp,
-                                   c_i64, vp, c_int, c_int, vp, vp]
+                                   c_i64, vp, c_int, c_int, vp, vp, vp, vp]
         L.orc_support.restype = c_int
         L.orc_support.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, c_i64, vp, c_int, vp]
         L.orc_voxel_centers.restype = c_int
@@ -51,7 +52,10 @@ def lib():
         L.orc_jitter_positions.restype = c_int
         L.orc_jitter_positions.argtypes = [vp, vp, vp, c_i64, vp, vp, vp]
         L.orc_index_boxes.restype = c_i64
-        L.orc_index_boxes.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp, vp, vp]
+        L.orc_index_boxes.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp]
+        L.orc_reached_cells.restype = c_int
+        L.orc_reached_cells.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, ctypes.c_double, c_i64, vp,
+                                        c_int, vp, vp, c_i64]
         L.orc_index.restype = c_int
         L.orc_index.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, vp, c_float, vp, vp, c_i64, vp, vp]
         L.orc_activate.restype = c_int
@@ -63,8 +67,6 @@ def lib():
         L.orc_densify.restype = c_i64
         L.orc_densify.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, vp, vp, vp, vp, vp, c_float,
                                   c_float, c_float, c_i64, c_i64, vp, vp, vp, vp, vp, vp]
-        L.orc_point_order.restype = c_int
-        L.orc_point_order.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp]
         _LIB = L
     return _LIB
 
@@ -105,6 +107,9 @@ def default_threads() -> int:
     return max(1, os.cpu_count() or 1)
 
 
+AMB_KEEP = 8  # ambiguous pairs per point whose a and v the forward keeps one by one
+
+
 class ForwardResult:
     def __init__(self, n):
         self.phi = np.zeros(n)
@@ -114,8 +119,9 @@ class ForwardResult:
         self.namb = np.zeros(n, dtype=np.int32)
         self.i_base = np.zeros(n)
         self.v_base = np.zeros(n)
-        self.amb_a = np.zeros((n, 4))
-        self.amb_v = np.zeros((n, 4))
+        self.amb_a = np.zeros((n, AMB_KEEP))
+        self.amb_v = np.zeros((n, AMB_KEEP))
+        self.amb_tot = np.zeros((n, 3))
         self.b_phi = np.zeros(n)
         self.b_inf = np.zeros(n)
 
@@ -131,17 +137,20 @@ def forward(g, points, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01, prune: boo
     rc = lib().orc_forward(m.shape[0], _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), tau, n, _p(pts),
                            int(prune), threads or default_threads(),
                            _p(r.phi), _p(r.inf), _p(r.defined), _p(r.ncontrib), _p(r.namb), _p(r.i_base),
-                           _p(r.v_base), _p(r.amb_a), _p(r.amb_v), _p(r.b_phi), _p(r.b_inf))
+                           _p(r.v_base), _p(r.amb_a), _p(r.amb_v), _p(r.amb_tot), _p(r.b_phi), _p(r.b_inf))
     if rc != 0:
         raise RuntimeError(f"orc_forward failed ({rc})")
     return r
 
 
 def backward(g, points, phi, inf, g_phi, g_inf, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01,
-             zero_mask=None, select=None, prune: bool = True, threads: int = 0):
+             zero_mask=None, select=None, prune: bool = True, threads: int = 0, pairs: bool = False):
     """Exact gradients (float64) of L = sum gPhi*Phi + gI*I with respect to
     every parameter of the selected Gaussians (all when select is None).
-    Returns (grad, abs_sum), each [nsel, 12] = dmu(3), ds(3), dq(4), dv, dw."""
+    Returns (grad, abs_sum), each [nsel, 12] = dmu(3), ds(3), dq(4), dv, dw,
+    and with pairs=True also each Gaussian's number of intersecting pairs
+    at the defined points [nsel] and the magnitudes of its whitened-frame
+    moment sums [nsel, 9] (see orc_backward)."""
     m, s, q, v, w = _gauss64(g)
     pts = _f64(points).reshape(-1, 3)
     n = pts.shape[0]
@@ -155,12 +164,14 @@ def backward(g, points, phi, inf, g_phi, g_inf, lo=(0, 0, 0), hi=(1, 1, 1), tau:
     nsel = m.shape[0] if sel is None else sel.shape[0]
     grad = np.zeros((nsel, 12))
     ab = np.zeros((nsel, 12))
+    K = np.zeros(nsel, dtype=np.int64)
+    mab = np.zeros((nsel, 9))
     rc = lib().orc_backward(m.shape[0], _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), tau, n, _p(pts),
                             _p(phi), _p(inf), _p(gp), _p(gi), _p(zm), nsel, _p(sel), int(prune),
-                            threads or default_threads(), _p(grad), _p(ab))
+                            threads or default_threads(), _p(grad), _p(ab), _p(K), _p(mab))
     if rc != 0:
         raise RuntimeError(f"orc_backward failed ({rc})")
-    return grad, ab
+    return (grad, ab, K, mab) if pairs else (grad, ab)
 
 
 def support(g, points, select, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01, threads: int = 0):
@@ -218,29 +229,48 @@ def jitter_positions(dims, u, lo=(0, 0, 0), hi=(1, 1, 1), ids=None) -> np.ndarra
     return out
 
 
-SPAN_ROWS = 64
-
-
-def index_boxes(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01, spans: bool = False):
-    """Canonical float32 cell box per Gaussian ([n,6], -1 when empty) and the
-    number of cells it lists; with spans=True also the trimmed flags [n] and
-    the row spans [n, 64] (byte: first | last << 4, offsets from the box's
-    low x; 0x0F for an empty row)."""
+def index_boxes(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01):
+    """Canonical float32 cell box of every Gaussian's cutoff ellipsoid
+    (Sec. 4.1.1): [n, 6] = (x0, y0, z0, x1, y1, z1), inclusive, -1 when
+    empty, and its number of cells."""
     m, s, q, v, w = _gauss(g)
     c = np.asarray(cells, dtype=np.int32).reshape(3)
     lo_, hi_ = _box(lo, hi)
     n = m.shape[0]
     box = np.zeros((n, 6), dtype=np.int32)
     cnt = np.zeros(n, dtype=np.int64)
-    tr = np.zeros(n, dtype=np.uint8)
-    sp = np.zeros((n, SPAN_ROWS), dtype=np.uint8)
-    P = lib().orc_index_boxes(n, _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), _p(c), tau, _p(box), _p(cnt),
-                              _p(tr), _p(sp))
+    P = lib().orc_index_boxes(n, _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), _p(c), tau, _p(box), _p(cnt))
     if P < 0:
         raise ValueError("orc_index_boxes: bad arguments")
-    if spans:
-        return box, cnt, tr.astype(bool), sp
     return box, cnt
+
+
+def reached_cells(g, cells, select=None, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01, margin: float = 0.0,
+                  threads: int = 0):
+    """For the selected Gaussians (all when None): the keys of the index
+    cells holding a point within the cutoff Q <= 2 ln(1/tau), each cell
+    widened by `margin` cell widths (exact float64 minimum of Q over the
+    cell). Returns (counts [nsel], keys concatenated Gaussian after
+    Gaussian, ascending within each)."""
+    m, s, q, v, w = _gauss(g)
+    c = np.asarray(cells, dtype=np.int32).reshape(3)
+    lo_, hi_ = _box(lo, hi)
+    n = m.shape[0]
+    sel = None if select is None else np.ascontiguousarray(select, dtype=np.int64)
+    nsel = n if sel is None else sel.shape[0]
+    cnt = np.zeros(nsel, dtype=np.int64)
+    th = threads or default_threads()
+    rc = lib().orc_reached_cells(n, _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), _p(c), tau, float(margin),
+                                 nsel, _p(sel), th, _p(cnt), None, 0)
+    if rc != 0:
+        raise RuntimeError(f"orc_reached_cells failed ({rc})")
+    total = int(cnt.sum())
+    keys = np.zeros(max(total, 1), dtype=np.uint32)
+    rc = lib().orc_reached_cells(n, _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), _p(c), tau, float(margin),
+                                 nsel, _p(sel), th, _p(cnt), _p(keys), total)
+    if rc != 0:
+        raise RuntimeError(f"orc_reached_cells failed ({rc})")
+    return cnt, keys[:total]
 
 
 def index(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01):
@@ -263,34 +293,32 @@ def index(g, cells, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01):
     return keys[:P], gids[:P], offs
 
 
-def point_order(points, cells, lo=(0, 0, 0), hi=(1, 1, 1)):
-    """Points ordered by (4 cell key + quarter of the cell along x, id);
-    outside points take key 4 ncells. Returns (keys_sorted, order,
-    point_offsets[4 ncells + 2])."""
-    pts = _f32(points).reshape(-1, 3)
-    c = np.asarray(cells, dtype=np.int32).reshape(3)
-    lo_, hi_ = _box(lo, hi)
-    n = pts.shape[0]
-    ncells = int(c[0]) * int(c[1]) * int(c[2])
-    keys = np.zeros(max(n, 1), dtype=np.uint32)
-    order = np.zeros(max(n, 1), dtype=np.uint32)
-    offs = np.zeros(4 * ncells + 2, dtype=np.uint32)
-    rc = lib().orc_point_order(n, _p(pts), _p(lo_), _p(hi_), _p(c), _p(keys), _p(order), _p(offs))
-    if rc != 0:
-        raise RuntimeError("orc_point_order failed")
-    return keys[:n], order[:n], offs
+def point_cells(points, cells, lo=(0, 0, 0), hi=(1, 1, 1)):
+    """float64 cell coordinates t_j = (p_j - lo_j) C_j / (hi_j - lo_j) of
+    each point (its cell is floor(t) clamped to the grid) and whether it lies
+    in the closed domain box."""
+    pts = np.asarray(points, dtype=np.float64).reshape(-1, 3)
+    lo_ = np.asarray(lo, dtype=np.float32).astype(np.float64)
+    hi_ = np.asarray(hi, dtype=np.float32).astype(np.float64)
+    c = np.asarray(cells, dtype=np.float64)
+    t = (pts - lo_) * (c / (hi_ - lo_))
+    inside = np.all((pts >= lo_) & (pts <= hi_), axis=1)
+    return t, inside
 
 
 def accept_forward(ref: ForwardResult, phi_gpu, inf_gpu, tau: float = 0.01, rtol: float = 1e-5,
-                   atol_phi: float = 1e-7, max_amb: int = 4):
+                   atol_phi: float = 1e-7):
     """Element-wise parity verdict for float32 forward outputs against the
     oracle. At a point that is not ambiguous: |Phi - ref| <= rtol |ref| +
     B_Phi + atol and |I - ref| <= rtol ref + B_I, both sides defined or
     undefined alike. At an ambiguous point (a pair within the float32 band of
     the cutoff, or I within 2^-16 tau of tau) the result must match one of the
-    oracle's variants (each ambiguous pair in or out, and either side of the
-    definedness threshold when I is that close to it). Returns (ok_mask,
-    stats)."""
+    oracle's variants: each of its k ambiguous pairs in or out, and either
+    side of the definedness threshold when I is that close to it. With more
+    than AMB_KEEP ambiguous pairs (whose terms are not kept one by one) the
+    result must lie within the hull of those variants instead: I between the
+    sum without and with every ambiguous pair, Phi between the least and the
+    largest of Phi without them and their values. Returns (ok_mask, stats)."""
     phi_gpu = np.asarray(phi_gpu, dtype=np.float64)
     inf_gpu = np.asarray(inf_gpu, dtype=np.float64)
     n = ref.phi.shape[0]
@@ -307,43 +335,41 @@ def accept_forward(ref: ForwardResult, phi_gpu, inf_gpu, tau: float = 0.01, rtol
     ok = close(ref.phi, ref.inf, defined, ref.b_phi, ref.b_inf)
     near_tau = np.abs(ref.inf - tau64) <= band_i
     amb_pt = (ref.namb > 0) | near_tau
-    # variants: every subset of the first min(namb, 4) ambiguous pairs
     idx = np.nonzero(amb_pt & ~ok)[0]
-    too_many = 0
+    bounded = 0
     for p in idx:
         k = int(ref.namb[p])
-        if k > max_amb:
-            # counted and reported, not judged
-            too_many += 1
-            ok[p] = True
+        gp, gi = phi_gpu[p], inf_gpu[p]
+        bphi, binf = ref.b_phi[p], ref.b_inf[p]
+        gdef = not (gp == 0.0 and gi == 0.0)
+        if k > AMB_KEEP:
+            bounded += 1
+            ib, asum = ref.i_base[p], ref.amb_tot[p, 0]
+            if not gdef:
+                ok[p] = ib <= tau64 + band_i
+                continue
+            vals = [ref.amb_tot[p, 1], ref.amb_tot[p, 2]] + ([ref.v_base[p] / ib] if ib > 0 else [])
+            lo_p, hi_p = min(vals), max(vals)
+            tol_p = rtol * max(abs(lo_p), abs(hi_p)) + bphi + atol_phi
+            ok[p] = bool(gi > tau64 - band_i and ib * (1 - rtol) - binf <= gi <= (ib + asum) * (1 + rtol) + binf
+                         and lo_p - tol_p <= gp <= hi_p + tol_p)
             continue
-        good = False
-        for mask in range(1 << k):
-            I = ref.i_base[p] + sum(ref.amb_a[p, j] for j in range(k) if mask >> j & 1)
-            V = ref.v_base[p] + sum(ref.amb_a[p, j] * ref.amb_v[p, j] for j in range(k) if mask >> j & 1)
-            ph = V / I if I > 0 else 0.0
-            for dflag in (True, False):
-                if dflag and not (I > tau64 - band_i):
-                    continue
-                if (not dflag) and not (I <= tau64 + band_i):
-                    continue
-                if dflag:
-                    if abs(phi_gpu[p] - ph) <= rtol * abs(ph) + ref.b_phi[p] + atol_phi and \
-                            abs(inf_gpu[p] - I) <= rtol * I + ref.b_inf[p]:
-                        good = True
-                else:
-                    if phi_gpu[p] == 0.0 and inf_gpu[p] == 0.0:
-                        good = True
-                if good:
-                    break
-            if good:
-                break
-        ok[p] = good
+        bits = ((np.arange(1 << k)[:, None] >> np.arange(k)[None, :]) & 1).astype(np.float64)
+        a = ref.amb_a[p, :k]
+        I = ref.i_base[p] + bits @ a
+        V = ref.v_base[p] + bits @ (a * ref.amb_v[p, :k])
+        if gdef:
+            ph = np.where(I > 0, V / np.where(I > 0, I, 1.0), 0.0)
+            good = (I > tau64 - band_i) & (np.abs(gp - ph) <= rtol * np.abs(ph) + bphi + atol_phi) & \
+                (np.abs(gi - I) <= rtol * I + binf)
+        else:
+            good = I <= tau64 + band_i
+        ok[p] = bool(good.any())
     stats = {
         "n": n,
         "defined": int(defined.sum()),
         "ambiguous": int(amb_pt.sum()),
-        "ambiguous_unchecked": too_many,
+        "ambiguous_bounded": bounded,
         "failed": int((~ok).sum()),
         "used_allowance": int((defined & ok & ((np.abs(phi_gpu - ref.phi) > rtol * np.abs(ref.phi) + atol_phi) |
                                                (np.abs(inf_gpu - ref.inf) > rtol * ref.inf))).sum()),

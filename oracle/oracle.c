@@ -28,9 +28,13 @@
  * (prune = 0) and the tests check both settings agree.
  *
  * The cell index (Sec. 4.1.1 and Sec. 4.1.2: per-Gaussian AABB of the cutoff
- * ellipsoid on a grid of cells, Gaussian-cell pairs ordered by cell) is
- * computed here in float32, in one fixed order of operations with every
- * operation rounded separately, so the GPU index can be compared bit for bit.
+ * ellipsoid on a grid of cells, Gaussian-cell pairs ordered by cell): the
+ * boxes in float32, in one fixed order of operations with every operation
+ * rounded separately, so the GPU's boxes can be compared bit for bit, and
+ * their full cell lists; and, by an exact float64 minimisation of Q over
+ * each cell, the cells every Gaussian reaches. A GPU index may list fewer
+ * cells than the box (the lists only have to hold the Gaussians that can
+ * reach a cell), never fewer than the reached ones.
  *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -shared -fPIC (see build.py).
  */
@@ -46,6 +50,9 @@
 #define ORC_ERR_ARG 1
 #define ORC_ERR_CAPACITY 2
 #define ORC_ERR_NOMEM 3
+
+/* ambiguous pairs of a point whose a and v are kept one by one */
+#define AMB_KEEP 8
 
 /* unit roundoff of float32 */
 #define EPS32 (1.0 / 16777216.0)
@@ -186,13 +193,6 @@ static int culled(const g64 *g, const double d[3], double Tlim)
     return 0;
 }
 
-static int in_box(const float *p, const float lo[3], const float hi[3])
-{
-    for (int j = 0; j < 3; j++)
-        if (!(p[j] >= lo[j]) || !(p[j] <= hi[j])) return 0;
-    return 1;
-}
-
 static int in_box_d(const double *p, const float lo[3], const float hi[3])
 {
     for (int j = 0; j < 3; j++)
@@ -220,7 +220,9 @@ static g64 *prepare_all(int64_t n, const double *mean, const double *scale, cons
  * accept the results that float32 may legitimately produce:
  *   namb          number of pairs with |Q - T| <= T * band_i
  *   i_base/v_base sums over intersecting pairs that are not ambiguous
- *   amb_a/amb_v   a = w G and v of the first 4 ambiguous pairs
+ *   amb_a/amb_v   a = w G and v of the first AMB_KEEP ambiguous pairs
+ *   amb_tot       per point: the sum of a over all its ambiguous pairs and
+ *                 the least and largest v among them (0, 0, 0 when none)
  *   b_phi/b_inf   conditioning allowances sum a_i e_i |v_i - Phi| / I and
  *                 sum a_i e_i over intersecting pairs
  * Any output pointer may be NULL.
@@ -229,7 +231,7 @@ int orc_forward(int64_t n, const double *mean, const double *scale, const double
                 const double *value, const double *weight, const float lo[3], const float hi[3],
                 float tau, int64_t npts, const double *pts, int prune, int nthreads,
                 double *phi, double *inf, int32_t *defined, int32_t *ncontrib, int32_t *namb,
-                double *i_base, double *v_base, double *amb_a, double *amb_v,
+                double *i_base, double *v_base, double *amb_a, double *amb_v, double *amb_tot,
                 double *b_phi, double *b_inf)
 {
     if (n < 0 || npts < 0 || !(tau > 0.0f) || !(tau < 1.0f)) return ORC_ERR_ARG;
@@ -255,7 +257,8 @@ int orc_forward(int64_t n, const double *mean, const double *scale, const double
             const double *pp = pts + 3 * p;
             double I = 0.0, V = 0.0, Ib = 0.0, Vb = 0.0;
             int K = 0, A = 0;
-            double aa[4] = {0, 0, 0, 0}, av[4] = {0, 0, 0, 0};
+            double aa[AMB_KEEP] = {0}, av[AMB_KEEP] = {0};
+            double asum = 0.0, avlo = INFINITY, avhi = -INFINITY;
             cnt = 0;
             int inside = in_box_d(pp, lo, hi);
             if (inside) {
@@ -269,10 +272,14 @@ int orc_forward(int64_t n, const double *mean, const double *scale, const double
                     double Q = whiten(g, d, u);
                     int amb = fabs(Q - T) <= T * g->band;
                     if (amb) {
-                        if (A < 4) {
-                            aa[A] = g->w * exp(-0.5 * Q);
+                        const double a = g->w * exp(-0.5 * Q);
+                        if (A < AMB_KEEP) {
+                            aa[A] = a;
                             av[A] = g->v;
                         }
+                        asum += a;
+                        avlo = g->v < avlo ? g->v : avlo;
+                        avhi = g->v > avhi ? g->v : avhi;
                         A++;
                     }
                     if (Q <= T) {
@@ -320,9 +327,14 @@ int orc_forward(int64_t n, const double *mean, const double *scale, const double
             if (i_base) i_base[p] = Ib;
             if (v_base) v_base[p] = Vb;
             if (amb_a)
-                for (int k = 0; k < 4; k++) amb_a[4 * p + k] = aa[k];
+                for (int k = 0; k < AMB_KEEP; k++) amb_a[AMB_KEEP * p + k] = aa[k];
             if (amb_v)
-                for (int k = 0; k < 4; k++) amb_v[4 * p + k] = av[k];
+                for (int k = 0; k < AMB_KEEP; k++) amb_v[AMB_KEEP * p + k] = av[k];
+            if (amb_tot) {
+                amb_tot[3 * p] = asum;
+                amb_tot[3 * p + 1] = A ? avlo : 0.0;
+                amb_tot[3 * p + 2] = A ? avhi : 0.0;
+            }
             if (b_inf) b_inf[p] = bi;
             if (b_phi) b_phi[p] = def ? bp / I : 0.0;
         }
@@ -360,14 +372,20 @@ int orc_forward(int64_t n, const double *mean, const double *scale, const double
  * abs_out holds the sum over pairs of the absolute per-pair terms, with
  * dL/da counted as the sum of the magnitudes of its parts (see below).
  * Points with zero_mask[p] != 0 contribute nothing (their cotangents are
- * taken as zero). sel == NULL selects every Gaussian.
+ * taken as zero). sel == NULL selects every Gaussian. npairs (optional)
+ * receives each selected Gaussian's number of intersecting pairs at the
+ * defined points taken into account, and mom_abs (optional, [nsel][9])
+ * the sums over those pairs of |dL/dQ| U_k and |dL/dQ| U_m U_k (m <= k:
+ * 00 01 02 11 12 22), with U_k = sum_j |R_jk d_j| / s_k the size of u_k's
+ * parts and |dL/dQ| taken at the size of dL/da's parts: the magnitudes of
+ * the sums an implementation in the whitened frame accumulates.
  */
 int orc_backward(int64_t n, const double *mean, const double *scale, const double *rot,
                  const double *value, const double *weight, const float lo[3], const float hi[3],
                  float tau, int64_t npts, const double *pts, const double *phi, const double *inf,
                  const double *g_phi, const double *g_inf, const uint8_t *zero_mask,
                  int64_t nsel, const int64_t *sel, int prune, int nthreads,
-                 double *grad, double *abs_out)
+                 double *grad, double *abs_out, int64_t *npairs, double *mom_abs)
 {
     if (n < 0 || npts < 0 || !(tau > 0.0f) || !(tau < 1.0f)) return ORC_ERR_ARG;
     if (!sel) nsel = n;
@@ -377,9 +395,11 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
 #pragma omp parallel for schedule(dynamic, 4)
     for (int64_t t = 0; t < nsel; t++) {
         int64_t i = sel ? sel[t] : t;
-        double acc[12], aab[12];
+        double acc[12], aab[12], mab[9];
+        int64_t K = 0;
         memset(acc, 0, sizeof(acc));
         memset(aab, 0, sizeof(aab));
+        memset(mab, 0, sizeof(mab));
         g64 g;
         if (i >= 0 && i < n) prepare(i, mean, scale, rot, value, weight, T, &g);
         else g.valid = 0;
@@ -393,6 +413,7 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
                 double u[3];
                 double Q = whiten(&g, d, u);
                 if (!(Q <= T)) continue;
+                K++;
                 double I = inf[p], Ph = phi[p];
                 double gP = g_phi[p], gI = g_inf[p];
                 double G = exp(-0.5 * Q);
@@ -470,6 +491,15 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
                     acc[k] += term[k] * dLdQv;
                     aab[k] += mag[k] * dLdQm;
                 }
+                /* the sizes of the whitened-frame moments sum |dL/dQ| u and
+                 * sum |dL/dQ| u u^T at the size of u's parts */
+                for (int k = 0; k < 3; k++) mab[k] += dLdQm * U[k];
+                mab[3] += dLdQm * U[0] * U[0];
+                mab[4] += dLdQm * U[0] * U[1];
+                mab[5] += dLdQm * U[0] * U[2];
+                mab[6] += dLdQm * U[1] * U[1];
+                mab[7] += dLdQm * U[1] * U[2];
+                mab[8] += dLdQm * U[2] * U[2];
                 term[10] = gP * a / I;
                 acc[10] += term[10];
                 aab[10] += fabs(term[10]);
@@ -481,6 +511,9 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
             grad[12 * t + k] = acc[k];
             if (abs_out) abs_out[12 * t + k] = aab[k];
         }
+        if (npairs) npairs[t] = K;
+        if (mom_abs)
+            for (int k = 0; k < 9; k++) mom_abs[9 * t + k] = mab[k];
     }
     return ORC_OK;
 }
@@ -651,129 +684,6 @@ static int64_t cell_box(const float *mu, const float *s, const float *q, float v
     return count;
 }
 
-/*
- * Row spans (refinement of the box of Sec. 4.1.1, canonical float64).
- *
- * The cells of a box come in x-rows at fixed (cy, cz). The cutoff
- * ellipsoid E = {p : (p - mu)^T Sigma^-1 (p - mu) <= T'} (T' = RCI^2, the
- * same enlarged cutoff as the box) meets the slab of a row, y in [y0, y1],
- * z in [z0, z1], in a convex set, so the cells of the row it reaches form one
- * run. The span kept for the row is a superset of that run:
- *   - conditioning on (y, z): x | (y, z) is centred on
- *     c(y, z) = mu_x + b_y dy + b_z dz with half-width sqrt((T' - Q2) vc),
- *     where Q2 is the quadratic form of the (y, z) marginal (precision
- *     Sigma_yz^-1), b = Sigma_x,yz Sigma_yz^-1 and vc the conditional variance;
- *   - Q2min = the minimum of Q2 over the slab's rectangle (0 when the centre
- *     lies inside, else the least of the four edge minima); the row is empty
- *     when Q2min > T';
- *   - otherwise x lies in [min c - wm, max c + wm] with wm = sqrt((T' - Q2min) vc)
- *     and the extremes of the linear c taken at the rectangle's corners.
- * The span is clipped to the box. A box is trimmed only when it has at most
- * SPAN_ROWS rows and at most SPAN_NX cells per row; a span is stored as one
- * byte (first and last cell offset from the box's low x, 4 bits each;
- * SPAN_EMPTY for none). Every float64 operation is performed in the order
- * written here.
- */
-#define SPAN_ROWS 64
-#define SPAN_NX 16
-#define SPAN_EMPTY 0x0F
-
-static double rect_qmin(double P00, double P01, double P11, double kz, double ky, double Y0, double Y1,
-                        double Z0, double Z1)
-{
-    if (Y0 <= 0.0 && 0.0 <= Y1 && Z0 <= 0.0 && 0.0 <= Z1) return 0.0;
-    double best = INFINITY;
-    const double Ys[2] = {Y0, Y1}, Zs[2] = {Z0, Z1};
-    for (int e = 0; e < 2; e++) {
-        const double Y = Ys[e];
-        double zs = kz * Y;
-        zs = zs < Z0 ? Z0 : (zs > Z1 ? Z1 : zs);
-        const double v = ((P00 * Y) * Y + 2.0 * ((P01 * Y) * zs)) + (P11 * zs) * zs;
-        best = v < best ? v : best;
-    }
-    for (int e = 0; e < 2; e++) {
-        const double Z = Zs[e];
-        double ys = ky * Z;
-        ys = ys < Y0 ? Y0 : (ys > Y1 ? Y1 : ys);
-        const double v = ((P00 * ys) * ys + 2.0 * ((P01 * ys) * Z)) + (P11 * Z) * Z;
-        best = v < best ? v : best;
-    }
-    return best;
-}
-
-/* Returns 1 and fills span[0 .. ny*nz) and *count when the box is trimmed,
- * 0 when it keeps every cell of its box. */
-static int row_spans(const float *mu, const float *s, const float *q, const int32_t b[6], const float glo[3],
-                     const float ghi[3], const int32_t cells[3], float RCI, uint8_t *span, int64_t *count)
-{
-    const int64_t nx = b[3] - b[0] + 1, ny = b[4] - b[1] + 1, nz = b[5] - b[2] + 1;
-    if (ny * nz > SPAN_ROWS || nx > SPAN_NX) return 0;
-    const double qw = q[0], qx = q[1], qy = q[2], qz = q[3];
-    const double qn = sqrt(((qw * qw + qx * qx) + qy * qy) + qz * qz);
-    const double iq = 1.0 / qn;
-    const double w = qw * iq, x = qx * iq, y = qy * iq, z = qz * iq;
-    double R[3][3];
-    R[0][0] = 1.0 - 2.0 * (y * y + z * z);
-    R[0][1] = 2.0 * (x * y - w * z);
-    R[0][2] = 2.0 * (x * z + w * y);
-    R[1][0] = 2.0 * (x * y + w * z);
-    R[1][1] = 1.0 - 2.0 * (x * x + z * z);
-    R[1][2] = 2.0 * (y * z - w * x);
-    R[2][0] = 2.0 * (x * z - w * y);
-    R[2][1] = 2.0 * (y * z + w * x);
-    R[2][2] = 1.0 - 2.0 * (x * x + y * y);
-    double a[3][3], S[3][3];
-    for (int j = 0; j < 3; j++)
-        for (int m = 0; m < 3; m++) a[j][m] = R[j][m] * (double)s[m];
-    for (int j = 0; j < 3; j++)
-        for (int k = 0; k < 3; k++) S[j][k] = ((a[j][0] * a[k][0]) + (a[j][1] * a[k][1])) + (a[j][2] * a[k][2]);
-    const double det = S[1][1] * S[2][2] - S[1][2] * S[1][2];
-    if (!(det > 0.0) || !isfinite(det)) return 0;
-    const double idet = 1.0 / det;
-    const double by = (S[0][1] * S[2][2] - S[0][2] * S[1][2]) * idet;
-    const double bz = (S[0][2] * S[1][1] - S[0][1] * S[1][2]) * idet;
-    const double vc = S[0][0] - (by * S[0][1] + bz * S[0][2]);
-    if (!(vc > 0.0) || !isfinite(vc)) return 0;
-    const double P00 = S[2][2] * idet, P01 = -S[1][2] * idet, P11 = S[1][1] * idet;
-    const double kz = -(P01 / P11), ky = -(P01 / P00);  /* edge vertices: z = kz y, y = ky z */
-    const double Tq = (double)RCI * (double)RCI;
-    const double icx = (double)cells[0] / ((double)ghi[0] - (double)glo[0]);
-    const double wdy = ((double)ghi[1] - (double)glo[1]) / (double)cells[1];
-    const double wdz = ((double)ghi[2] - (double)glo[2]) / (double)cells[2];
-    int64_t cnt = 0;
-    for (int64_t r = 0; r < ny * nz; r++) {
-        const int64_t cy = b[1] + r % ny, cz = b[2] + r / ny;
-        const double Y0 = ((double)glo[1] + (double)cy * wdy) - (double)mu[1];
-        const double Y1 = ((double)glo[1] + (double)(cy + 1) * wdy) - (double)mu[1];
-        const double Z0 = ((double)glo[2] + (double)cz * wdz) - (double)mu[2];
-        const double Z1 = ((double)glo[2] + (double)(cz + 1) * wdz) - (double)mu[2];
-        const double qmin = rect_qmin(P00, P01, P11, kz, ky, Y0, Y1, Z0, Z1);
-        uint8_t code = SPAN_EMPTY;
-        if (!(qmin > Tq)) {
-            int64_t cl = b[0], ch = b[3];
-            const double wm = sqrt((Tq - qmin) * vc);
-            const double c00 = (double)mu[0] + (by * Y0 + bz * Z0), c01 = (double)mu[0] + (by * Y0 + bz * Z1);
-            const double c10 = (double)mu[0] + (by * Y1 + bz * Z0), c11 = (double)mu[0] + (by * Y1 + bz * Z1);
-            const double m0 = c00 < c01 ? c00 : c01, m1 = c10 < c11 ? c10 : c11;
-            const double M0 = c00 > c01 ? c00 : c01, M1 = c10 > c11 ? c10 : c11;
-            const double cmin = m0 < m1 ? m0 : m1, cmax = M0 > M1 ? M0 : M1;
-            const double fl = floor(((cmin - wm) - (double)glo[0]) * icx);
-            const double fh = floor(((cmax + wm) - (double)glo[0]) * icx);
-            if (isfinite(fl) && isfinite(fh)) {
-                cl = fl < (double)b[0] ? b[0] : (fl > (double)b[3] ? b[3] + 1 : (int64_t)fl);
-                ch = fh > (double)b[3] ? b[3] : (fh < (double)b[0] ? b[0] - 1 : (int64_t)fh);
-            }
-            if (cl <= ch) {
-                code = (uint8_t)((cl - b[0]) | ((ch - b[0]) << 4));
-                cnt += ch - cl + 1;
-            }
-        }
-        span[r] = code;
-    }
-    *count = cnt;
-    return 1;
-}
-
 static void grid_invc(const float lo[3], const float hi[3], const int32_t cells[3], float invc[3])
 {
     for (int j = 0; j < 3; j++) {
@@ -792,16 +702,13 @@ static int grid_ok(const float lo[3], const float hi[3], const int32_t cells[3])
     return nc < ((int64_t)1 << 31);
 }
 
-/* box[n][6] = (cx_lo, cy_lo, cz_lo, cx_hi, cy_hi, cz_hi) or -1, count[n]
- * (cells listed: the trimmed count for a trimmed box), trimmed[n] (1 when
- * the box's rows carry spans), spans[n][SPAN_ROWS] (row spans of trimmed
- * boxes; SPAN_EMPTY for rows past the box and for untrimmed boxes); any
- * output may be NULL. Returns the total number of
- * pairs (or -1 on bad arguments). */
+/* box[n][6] = (cx_lo, cy_lo, cz_lo, cx_hi, cy_hi, cz_hi) or -1 (the cells
+ * of the cutoff ellipsoid's axis-aligned box, Sec. 4.1.1) and count[n] (its
+ * number of cells); either output may be NULL. Returns the total number of
+ * cells over all boxes (or -1 on bad arguments). */
 int64_t orc_index_boxes(int64_t n, const float *mean, const float *scale, const float *rot,
                         const float *value, const float *weight, const float lo[3], const float hi[3],
-                        const int32_t cells[3], float tau, int32_t *box, int64_t *count, uint8_t *trimmed,
-                        uint8_t *spans)
+                        const int32_t cells[3], float tau, int32_t *box, int64_t *count)
 {
     if (n < 0 || !grid_ok(lo, hi, cells) || !(tau > 0.0f) || !(tau < 1.0f)) return -1;
     float invc[3];
@@ -810,26 +717,17 @@ int64_t orc_index_boxes(int64_t n, const float *mean, const float *scale, const 
     int64_t total = 0;
     for (int64_t i = 0; i < n; i++) {
         int32_t b[6];
-        uint8_t sp[SPAN_ROWS];
-        memset(sp, SPAN_EMPTY, sizeof(sp));
         int64_t c = cell_box(mean + 3 * i, scale + 3 * i, rot + 4 * i, value[i], weight[i], lo, invc, cells, RCI, b);
-        int tr = 0;
-        if (c > 0) {
-            int64_t ct = 0;
-            tr = row_spans(mean + 3 * i, scale + 3 * i, rot + 4 * i, b, lo, hi, cells, RCI, sp, &ct);
-            if (tr) c = ct;
-        }
         if (box) memcpy(box + 6 * i, b, sizeof(b));
         if (count) count[i] = c;
-        if (trimmed) trimmed[i] = (uint8_t)tr;
-        if (spans) memcpy(spans + SPAN_ROWS * i, sp, sizeof(sp));
         total += c;
     }
     return total;
 }
 
 /*
- * Gaussian-cell pairs (key = cx + Cx (cy + Cy cz), gid) in lexicographic
+ * Gaussian-cell pairs (key = cx + Cx (cy + Cy cz), gid) of every cell of
+ * every box (Sec. 4.1.2's block intersection lists), in lexicographic
  * (key, gid) order, and cell_offsets[k] = number of pairs with key < k for
  * k = 0..ncells. Written by counting: offsets from per-cell counts, then
  * Gaussians in increasing id append to the lists of the cells in their box.
@@ -844,22 +742,16 @@ int orc_index(int64_t n, const float *mean, const float *scale, const float *rot
     int64_t ncells = (int64_t)cells[0] * cells[1] * cells[2];
     const size_t nn = (size_t)(n > 0 ? n : 1);
     int32_t *box = (int32_t *)malloc(sizeof(int32_t) * 6 * nn);
-    uint8_t *tr = (uint8_t *)malloc(nn);
-    uint8_t *sp = (uint8_t *)malloc((size_t)SPAN_ROWS * nn);
     int64_t *cursor = (int64_t *)calloc((size_t)ncells + 1, sizeof(int64_t));
-    if (!box || !cursor || !tr || !sp) {
+    if (!box || !cursor) {
         free(box);
-        free(tr);
-        free(sp);
         free(cursor);
         return ORC_ERR_NOMEM;
     }
-    int64_t P = orc_index_boxes(n, mean, scale, rot, value, weight, lo, hi, cells, tau, box, NULL, tr, sp);
+    int64_t P = orc_index_boxes(n, mean, scale, rot, value, weight, lo, hi, cells, tau, box, NULL);
     *n_pairs = P;
     if (P > capacity || P >= ((int64_t)1 << 32)) {
         free(box);
-        free(tr);
-        free(sp);
         free(cursor);
         return ORC_ERR_CAPACITY;
     }
@@ -873,16 +765,9 @@ int orc_index(int64_t n, const float *mean, const float *scale, const float *rot
         for (int64_t i = 0; i < n; i++) {
             const int32_t *b = box + 6 * i;
             if (b[0] < 0) continue;
-            const int64_t ny = b[4] - b[1] + 1;
             for (int64_t z = b[2]; z <= b[5]; z++)
-                for (int64_t y = b[1]; y <= b[4]; y++) {
-                    int64_t x0 = b[0], x1 = b[3];
-                    if (tr[i]) {
-                        const uint8_t code = sp[SPAN_ROWS * i + (y - b[1]) + ny * (z - b[2])];
-                        x0 = b[0] + (code & 15);
-                        x1 = b[0] + (code >> 4);
-                    }
-                    for (int64_t x = x0; x <= x1; x++) {
+                for (int64_t y = b[1]; y <= b[4]; y++)
+                    for (int64_t x = b[0]; x <= b[3]; x++) {
                         int64_t key = x + Cx * (y + Cy * z);
                         if (sweep == 0) {
                             cursor[key + 1]++;
@@ -892,73 +777,165 @@ int orc_index(int64_t n, const float *mean, const float *scale, const float *rot
                             gids[at] = (uint32_t)i;
                         }
                     }
-                }
         }
     }
     free(box);
-    free(tr);
-    free(sp);
     free(cursor);
     return ORC_OK;
 }
 
+/* ------------------------------------------------------------------------ */
+/* The cells a Gaussian reaches (Sec. 4.1.1: a block needs a Gaussian in its  */
+/* list exactly when the Gaussian's cutoff region overlaps it).              */
+/* ------------------------------------------------------------------------ */
+
 /*
- * Query ordering for unstructured queries (the library's plan, standing in
- * for the paper's sample BVH): each point's key is 4 cell + j, with the cell
- * key cell = cx + Cx (cy + Cy cz), c_j = clamp(floor(t_j), 0, C_j - 1),
- * t_j = (p_j - lo_j) * invc_j in float32, and j = floor(4 (t_x - c_x)) in
- * [0, 3] the quarter of the cell along x; 4 ncells for a point outside the
- * closed box. order[] lists point ids by (key, id); point_offsets[k] =
- * number of points with key < k, k = 0 .. 4 ncells + 1.
+ * Minimum of the convex quadratic f(d) = d^T A d (A symmetric positive
+ * definite) over the box L <= d <= U, in float64.
+ *
+ * The minimiser lies in the relative interior of exactly one face of the
+ * box (the box itself, one of its 6 facets, 12 edges or 8 vertices). On
+ * the affine hull of a face some coordinates are fixed at a bound and the
+ * others are free; there f is a convex quadratic in the free coordinates
+ * whose minimiser solves A_FF d_F = -A_FX d_X. Every face whose such
+ * minimiser satisfies the free coordinates' bounds gives an attained value
+ * of f on the box, and the face holding the true minimiser is among them,
+ * so the least of those values is the minimum. The free systems have at
+ * most 3 unknowns and are solved by Cramer's rule.
  */
-int orc_point_order(int64_t npts, const float *pts, const float lo[3], const float hi[3],
-                    const int32_t cells[3], uint32_t *keys_out, uint32_t *order, uint32_t *point_offsets)
+static double box_min_quadratic(const double A[3][3], const double L[3], const double U[3])
 {
-    if (npts < 0 || !grid_ok(lo, hi, cells)) return ORC_ERR_ARG;
-    int64_t ncells = (int64_t)cells[0] * cells[1] * cells[2];
-    const int64_t nkeys = 4 * ncells + 1; /* 4 keys per cell, then the outside key */
+    double best = INFINITY;
+    /* state per axis: 0 free, 1 fixed at L, 2 fixed at U */
+    for (int code = 0; code < 27; code++) {
+        int st[3] = {code % 3, (code / 3) % 3, code / 9};
+        int fr[3], nf = 0;
+        double d[3] = {0.0, 0.0, 0.0};
+        for (int j = 0; j < 3; j++) {
+            if (st[j] == 0)
+                fr[nf++] = j;
+            else
+                d[j] = st[j] == 1 ? L[j] : U[j];
+        }
+        /* right-hand side b_F = -A_FX d_X */
+        double b[3] = {0.0, 0.0, 0.0};
+        for (int a = 0; a < nf; a++)
+            for (int j = 0; j < 3; j++)
+                if (st[j] != 0) b[a] -= A[fr[a]][j] * d[j];
+        if (nf == 1) {
+            d[fr[0]] = b[0] / A[fr[0]][fr[0]];
+        } else if (nf == 2) {
+            const double a00 = A[fr[0]][fr[0]], a01 = A[fr[0]][fr[1]], a11 = A[fr[1]][fr[1]];
+            const double det = a00 * a11 - a01 * a01;
+            if (!(det > 0.0)) continue;
+            d[fr[0]] = (b[0] * a11 - a01 * b[1]) / det;
+            d[fr[1]] = (a00 * b[1] - a01 * b[0]) / det;
+        } else if (nf == 3) {
+            /* the unconstrained minimiser d = 0 */
+            d[0] = d[1] = d[2] = 0.0;
+        }
+        int ok = 1;
+        for (int a = 0; a < nf; a++) {
+            const int j = fr[a];
+            if (!(d[j] >= L[j] && d[j] <= U[j])) ok = 0;
+        }
+        if (!ok) continue;
+        double f = 0.0;
+        for (int j = 0; j < 3; j++)
+            for (int k = 0; k < 3; k++) f += d[j] * A[j][k] * d[k];
+        if (f < best) best = f;
+    }
+    return best;
+}
+
+/*
+ * For the selected Gaussians (sel[0..nsel), or all when sel is NULL): the
+ * cells of the index grid that hold a point within the Gaussian's cutoff
+ * Q <= T = 2 ln(1/tau), each cell taken as its box widened by margin cell
+ * widths on every side (margin >= 0; 0 gives the cells the cutoff region
+ * itself overlaps). Q over a cell is minimised exactly in float64
+ * (box_min_quadratic on the inverse covariance A = R S^-2 R^T). Only cells
+ * of the Gaussian's canonical box (orc_index_boxes) are examined; by
+ * Cauchy-Schwarz no point outside the cutoff's own axis-aligned extent is
+ * within the cutoff, and that box holds the extent with a margin.
+ * count[a] = number of such cells of Gaussian sel[a]; when keys is non-NULL
+ * their keys follow Gaussian after Gaussian (in increasing key) in
+ * keys[0 .. sum count), at most capacity of them (ORC_ERR_CAPACITY
+ * beyond). Invalid Gaussians reach no cell.
+ */
+int orc_reached_cells(int64_t n, const float *mean, const float *scale, const float *rot,
+                      const float *value, const float *weight, const float lo[3], const float hi[3],
+                      const int32_t cells[3], float tau, double margin, int64_t nsel, const int64_t *sel,
+                      int nthreads, int64_t *count, uint32_t *keys, int64_t capacity)
+{
+    if (n < 0 || nsel < 0 || !grid_ok(lo, hi, cells) || !(tau > 0.0f) || !(tau < 1.0f) || !(margin >= 0.0))
+        return ORC_ERR_ARG;
+    set_threads(nthreads);
+    const double T = 2.0 * log(1.0 / (double)tau);
     float invc[3];
     grid_invc(lo, hi, cells, invc);
-    uint32_t *key = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(npts > 0 ? npts : 1));
-    int64_t *cursor = (int64_t *)calloc((size_t)nkeys + 1, sizeof(int64_t));
-    if (!key || !cursor) {
-        free(key);
-        free(cursor);
-        return ORC_ERR_NOMEM;
-    }
-    for (int64_t p = 0; p < npts; p++) {
-        const float *pp = pts + 3 * p;
-        int64_t k = 4 * ncells;
-        if (in_box(pp, lo, hi)) {
-            int64_t c[3];
-            float tx = 0.0f;
-            for (int j = 0; j < 3; j++) {
-                volatile float dl = pp[j] - lo[j];
-                volatile float t = dl * invc[j];
-                float f = floorf(t);
-                int64_t ci = (int64_t)f;
-                if (ci < 0) ci = 0;
-                if (ci > cells[j] - 1) ci = cells[j] - 1;
-                c[j] = ci;
-                if (j == 0) tx = t;
+    const float RCI = index_radius(tau);
+    double width[3];
+    for (int j = 0; j < 3; j++) width[j] = ((double)hi[j] - (double)lo[j]) / (double)cells[j];
+    const int64_t m = sel ? nsel : n;
+    int err = 0;
+    for (int pass = 0; pass < (keys ? 2 : 1); pass++) {
+        int64_t *start = NULL;
+        if (pass == 1) {
+            start = (int64_t *)malloc(sizeof(int64_t) * (size_t)(m + 1));
+            if (!start) return ORC_ERR_NOMEM;
+            start[0] = 0;
+            for (int64_t a = 0; a < m; a++) start[a + 1] = start[a] + count[a];
+            if (start[m] > capacity) {
+                free(start);
+                return ORC_ERR_CAPACITY;
             }
-            /* the quarter of the cell along x, floor(4 (t - c)) in float32 */
-            volatile float fr = tx - (float)c[0];
-            float fq = floorf(fr * 4.0f);
-            int64_t qx = fq < 0.0f ? 0 : (fq > 3.0f ? 3 : (int64_t)fq);
-            k = 4 * (c[0] + (int64_t)cells[0] * (c[1] + (int64_t)cells[1] * c[2])) + qx;
         }
-        key[p] = (uint32_t)k;
-        cursor[k + 1]++;
+#pragma omp parallel for schedule(dynamic, 8)
+        for (int64_t a = 0; a < m; a++) {
+            const int64_t i = sel ? sel[a] : a;
+            if (i < 0 || i >= n) {
+#pragma omp atomic write
+                err = 1;
+                continue;
+            }
+            int32_t b[6];
+            int64_t c = cell_box(mean + 3 * i, scale + 3 * i, rot + 4 * i, value[i], weight[i], lo, invc, cells,
+                                 RCI, b);
+            int64_t got = 0;
+            if (c > 0) {
+                const double q[4] = {rot[4 * i], rot[4 * i + 1], rot[4 * i + 2], rot[4 * i + 3]};
+                const double qn = sqrt(q[0] * q[0] + q[1] * q[1] + q[2] * q[2] + q[3] * q[3]);
+                const double qh[4] = {q[0] / qn, q[1] / qn, q[2] / qn, q[3] / qn};
+                double R[3][3], A[3][3];
+                quat_to_rot(qh, R);
+                for (int j = 0; j < 3; j++)
+                    for (int k = 0; k < 3; k++) {
+                        double acc = 0.0;
+                        for (int t = 0; t < 3; t++)
+                            acc += R[j][t] * R[k][t] / ((double)scale[3 * i + t] * (double)scale[3 * i + t]);
+                        A[j][k] = acc;
+                    }
+                for (int64_t z = b[2]; z <= b[5]; z++)
+                    for (int64_t y = b[1]; y <= b[4]; y++)
+                        for (int64_t x = b[0]; x <= b[3]; x++) {
+                            const int64_t cc[3] = {x, y, z};
+                            double L[3], U[3];
+                            for (int j = 0; j < 3; j++) {
+                                L[j] = ((double)lo[j] + ((double)cc[j] - margin) * width[j]) - (double)mean[3 * i + j];
+                                U[j] = ((double)lo[j] + ((double)cc[j] + 1.0 + margin) * width[j]) -
+                                       (double)mean[3 * i + j];
+                            }
+                            if (box_min_quadratic(A, L, U) <= T) {
+                                if (pass == 1) keys[start[a] + got] = (uint32_t)(x + (int64_t)cells[0] *
+                                                                                   (y + (int64_t)cells[1] * z));
+                                got++;
+                            }
+                        }
+            }
+            if (pass == 0) count[a] = got;
+        }
+        free(start);
     }
-    for (int64_t k = 0; k < nkeys; k++) cursor[k + 1] += cursor[k];
-    for (int64_t k = 0; k <= nkeys; k++) point_offsets[k] = (uint32_t)cursor[k];
-    for (int64_t p = 0; p < npts; p++) {
-        int64_t at = cursor[key[p]]++;
-        order[at] = (uint32_t)p;
-        if (keys_out) keys_out[at] = key[p];
-    }
-    free(key);
-    free(cursor);
-    return ORC_OK;
+    return err ? ORC_ERR_ARG : ORC_OK;
 }

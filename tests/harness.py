@@ -124,15 +124,72 @@ class Run:
         return self.points_np if sel is None else self.points_np[sel]
 
 
-def check_index(run: Run):
-    keys, gids, offs = run.index_arrays()
+def gpu_boxes(index, n: int) -> np.ndarray:
+    """The float32 cell boxes the GPU preprocess wrote, read back from the
+    index workspace (the library's layout: a 64-byte record per Gaussian,
+    then at the next 256-byte boundary a 32-byte box per Gaussian,
+    (x0, y0, z0, flag) and (x1, y1, z1, 0), empty when x1 < x0), as
+    [n, 6] = (x0, y0, z0, x1, y1, z1) with -1 for empty boxes."""
+    off = (64 * max(n, 1) + 255) // 256 * 256
+    raw = index.work[off: off + 32 * n].cpu().numpy().view(np.int32).reshape(n, 8)
+    box = np.concatenate([raw[:, 0:3], raw[:, 4:7]], axis=1)
+    box[raw[:, 4] < raw[:, 0]] = -1
+    return box
+
+
+def check_index_arrays(g, cells, lo, hi, tau, keys, gids, offs, boxes, reach_sel=None, label=""):
+    """The GPU index against the oracle, by the properties the paper fixes
+    (Sec. 4.1.1, Sec. 4.1.2):
+      * every Gaussian's float32 cell box equals the oracle's, bit for bit;
+      * the pairs are in strictly increasing (cell key, Gaussian id) order,
+        so no pair repeats, and cell_offsets[k] = #pairs with key < k;
+      * each Gaussian lists only cells of its box, and at least every cell
+        it reaches (the oracle's exact float64 minimum of Q over the cell is
+        within the cutoff), checked for the Gaussians reach_sel (all when
+        None)."""
     t0 = time.time()
-    rk, rg, ro = oracle.index(run.g, run.cells, run.lo, run.hi, run.tau)
-    log(f"  index: P={len(rk)} (oracle {time.time() - t0:.1f}s)")
-    assert len(keys) == len(rk), (len(keys), len(rk))
-    np.testing.assert_array_equal(offs, ro)
-    np.testing.assert_array_equal(keys, rk)
-    np.testing.assert_array_equal(gids, rg)
+    cells = tuple(int(c) for c in cells)
+    ncells = cells[0] * cells[1] * cells[2]
+    rbox, rcnt = oracle.index_boxes(g, cells, lo, hi, tau)
+    np.testing.assert_array_equal(boxes, rbox)
+    P = len(keys)
+    k64, g64 = keys.astype(np.int64), gids.astype(np.int64)
+    assert np.all(k64 < ncells) and np.all(g64 < g.n)
+    code = k64 * (1 << 32) + g64
+    assert np.all(np.diff(code) > 0), "pairs not in strictly increasing (key, gid) order"
+    np.testing.assert_array_equal(offs.astype(np.int64), np.searchsorted(k64, np.arange(ncells + 1), side="left"))
+    cx, cy, cz = k64 % cells[0], (k64 // cells[0]) % cells[1], k64 // (cells[0] * cells[1])
+    b = rbox[g64]
+    inside = (b[:, 0] <= cx) & (cx <= b[:, 3]) & (b[:, 1] <= cy) & (cy <= b[:, 4]) & (b[:, 2] <= cz) & (cz <= b[:, 5])
+    assert inside.all(), f"{int((~inside).sum())} listed cells outside their Gaussian's box"
+    sel = np.arange(g.n) if reach_sel is None else np.asarray(reach_sel, dtype=np.int64)
+    rc, rk = oracle.reached_cells(g, cells, select=sel, lo=lo, hi=hi, tau=tau)
+    want = np.repeat(sel, rc) * ncells + rk.astype(np.int64)
+    have = np.sort(g64 * ncells + k64)
+    pos = np.clip(np.searchsorted(have, want), 0, max(P - 1, 0))
+    found = (have[pos] == want) if P > 0 else np.zeros(len(want), bool)
+    if not found.all():
+        miss = np.nonzero(~found)[0][:10]
+        for m in miss:
+            log(f"    reached but not listed: gaussian {want[m] // ncells} cell {want[m] % ncells}")
+    assert found.all(), f"{int((~found).sum())} reached cells not listed"
+    log(f"  index {label}: P={P}, box cells {int(rcnt.sum())}, reached by {len(sel)} checked Gaussians "
+        f"{int(rc.sum())} (oracle {time.time() - t0:.1f}s)")
+
+
+def check_index(run: Run, reach_sample=None):
+    """check_index_arrays on a Run's index; reach_sample: check the reached
+    cells of that many seeded Gaussians (the 64 with the most box cells
+    among them) instead of all."""
+    keys, gids, offs = run.index_arrays()
+    boxes = gpu_boxes(run.index, run.g.n)
+    sel = None
+    if reach_sample is not None and reach_sample < run.g.n:
+        rbox, rcnt = oracle.index_boxes(run.g, run.cells, run.lo, run.hi, run.tau)
+        big = np.argsort(-rcnt, kind="stable")[:64]
+        rnd = np.random.default_rng(97).choice(run.g.n, size=reach_sample, replace=False)
+        sel = np.unique(np.concatenate([big, rnd]))
+    check_index_arrays(run.g, run.cells, run.lo, run.hi, run.tau, keys, gids, offs, boxes, sel)
 
 
 def check_forward(run: Run, phi, inf, sel=None, label=""):
@@ -177,9 +234,71 @@ def kappa(g: synth.Gaussians) -> np.ndarray:
     return k
 
 
-def grad_tolerance(ref, ab, kap, rtol=1e-4):
+def rot_of(q):
+    """R(q) for the components (w, x, y, z) taken as they are, Hamilton
+    convention (quadratic in q; a unit q gives a rotation)."""
+    w, x, y, z = q
+    return np.array([[1 - 2 * (y * y + z * z), 2 * (x * y - w * z), 2 * (x * z + w * y)],
+                     [2 * (x * y + w * z), 1 - 2 * (x * x + z * z), 2 * (y * z - w * x)],
+                     [2 * (x * z - w * y), 2 * (y * z + w * x), 1 - 2 * (x * x + y * y)]])
+
+
+M2_INDEX = ((0, 0), (0, 1), (0, 2), (1, 1), (1, 2), (2, 2))
+OWN_ROUNDING = 2.0 ** -48
+
+
+def quat_moment_map(scale, rot):
+    """[4, 6]: the linear map from a Gaussian's whitened-frame second moments
+    m2 = sum dL/dQ u u^T (entries 00 01 02 11 12 22, each off-diagonal one
+    standing for both of its places) to dL/dq of the raw quaternion. With
+    d = R S u, dL/dR = sum dL/dQ 2 d (u / s)^T = 2 R S m2 S^-1; then
+    dL/dqhat_i = sum_jk dL/dR_jk dR_jk/dqhat_i (R is quadratic in qhat, so a
+    central difference of step 1 is exact), projected on the tangent of the
+    unit sphere and divided by |q|."""
+    q = np.asarray(rot, np.float64)
+    qn = np.linalg.norm(q)
+    qh = q / qn
+    s = np.asarray(scale, np.float64)
+    R = rot_of(qh)
+    dR = np.stack([(rot_of(qh + e) - rot_of(qh - e)) / 2.0 for e in np.eye(4)])  # [4, 3, 3]
+    out = np.zeros((4, 6))
+    for c, (m, k) in enumerate(M2_INDEX):
+        E = np.zeros((3, 3))
+        E[m, k] = E[k, m] = 1.0
+        G = 2.0 * R @ np.diag(s) @ E @ np.diag(1.0 / s)
+        dqh = np.einsum("ijk,jk->i", dR, G)
+        out[:, c] = (dqh - qh * (qh @ dqh)) / qn
+    return out
+
+
+def grad_tolerance(ref, ab, kap, npairs, mom_abs=None, scale=None, rot=None, rtol=1e-4):
+    """Bar of a float32 gradient against the oracle's float64 one, per
+    element: rtol |ref| plus the float32 error of the sum over the
+    Gaussian's K pairs, measured against the sizes of what is summed. Each
+    term carries the relative error e of G = exp(-Q/2) (e = eps (9 T kappa +
+    8), from the whitening's 18 eps T kappa in Q) and a few roundings of its
+    products: 2 e + 8 eps. The device adds each lane's share of the pairs in
+    turn (at most ceil(K / 64) + 1 additions a lane) and then reduces 64
+    lanes in 6 steps, so the accumulated sums err by at most
+    (ceil(K / 64) + 16) eps of their sizes, to first order. The sizes are the
+    oracle's sums of absolute per-pair terms A; for the quaternion, which
+    the device forms from the whitened-frame moments m2, the sizes of those
+    moments (mom_abs) through the absolute values of the linear map from m2
+    to dL/dq (quat_moment_map), when they are given."""
     e = EPS32 * (9.0 * T64 * kap + 8.0)
-    return rtol * (np.abs(ref) + ab) + 2.0 * e[:, None] * ab
+    depth = np.ceil(np.asarray(npairs, dtype=np.float64) / 64.0) + 16.0
+    f = (2.0 * e + (depth + 8.0) * EPS32)[:, None]
+    tol = rtol * np.abs(ref) + f * ab
+    if mom_abs is not None:
+        for i in range(len(ref)):
+            if not mom_abs[i, 3:9].any():
+                continue  # no pair (or an invalid Gaussian): the bar above, with A = 0
+            L = np.abs(quat_moment_map(scale[i], rot[i]))
+            tol[i, 6:10] = rtol * np.abs(ref[i, 6:10]) + f[i, 0] * (L @ mom_abs[i, 3:9])
+    # the float64 reference's own rounding of its cancelling sums (for a
+    # spherical Gaussian dL/dq is exactly zero, the oracle's sum of its
+    # per-pair terms a few 1e-18)
+    return tol + OWN_ROUNDING * ab
 
 
 def check_backward(run: Run, grads_gpu: np.ndarray, sel, sup, gv_sup, gi_sup, label=""):
@@ -195,9 +314,10 @@ def check_backward(run: Run, grads_gpu: np.ndarray, sel, sup, gv_sup, gi_sup, la
     pts_sup = run.positions(sup)
     phi_sup = run.phi_np[sup].astype(np.float64)
     inf_sup = run.inf_np[sup].astype(np.float64)
-    ref, ab = oracle.backward(run.g, pts_sup, phi_sup, inf_sup, gv_sup, gi_sup, run.lo, run.hi, run.tau, select=sel)
+    ref, ab, K, mab = oracle.backward(run.g, pts_sup, phi_sup, inf_sup, gv_sup, gi_sup, run.lo, run.hi, run.tau,
+                                      select=sel, pairs=True)
     got = grads_gpu[sel]
-    tol = grad_tolerance(ref, ab, kappa(run.g)[sel])
+    tol = grad_tolerance(ref, ab, kappa(run.g)[sel], K, mab, run.g.scale[sel], run.g.rot[sel])
     err = np.abs(got - ref)
     ok = err <= tol
     worst = float(np.max(err / np.maximum(tol, 1e-300)))

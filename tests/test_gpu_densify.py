@@ -251,13 +251,12 @@ def test_rebuilt_index_matches_oracle():
     torch.cuda.synchronize()
     host_g = synth.Gaussians(out.mean[:n].cpu().numpy(), sc.cpu().numpy(), out.rot[:n].cpu().numpy(),
                              va.cpu().numpy(), we.cpu().numpy())
-    rk, rg, ro = oracle.index(host_g, w_.index_cells, (0, 0, 0), (1, 1, 1), TAU)
     P = idx.n_pairs
     log(f"  rebuilt index: {n} Gaussians, {P} pairs")
-    assert P == len(rk)
-    np.testing.assert_array_equal(idx.keys[:P].cpu().numpy().view(np.uint32), rk)
-    np.testing.assert_array_equal(idx.gids[:P].cpu().numpy().view(np.uint32), rg)
-    np.testing.assert_array_equal(idx.cell_offsets.cpu().numpy().view(np.uint32), ro)
+    from harness import check_index_arrays, gpu_boxes
+    check_index_arrays(host_g, w_.index_cells, (0, 0, 0), (1, 1, 1), TAU, idx.keys[:P].cpu().numpy().view(np.uint32),
+                       idx.gids[:P].cpu().numpy().view(np.uint32), idx.cell_offsets.cpu().numpy().view(np.uint32),
+                       gpu_boxes(idx, n), label="rebuilt")
     # the next iteration samples the densified set: forward and backward on
     # new jittered positions, against the oracle
     from harness import Run, check_backward, check_forward, masked_cotangents

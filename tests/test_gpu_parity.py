@@ -15,7 +15,8 @@ import pytest
 
 import oracle
 import synth
-from harness import TAU, Run, check_backward, check_forward, check_index, log, masked_cotangents
+from harness import (TAU, Run, check_backward, check_forward, check_index, check_index_arrays, gpu_boxes, log,
+                     masked_cotangents)
 
 pytestmark = pytest.mark.gpu
 
@@ -233,21 +234,129 @@ def test_index_tile_spanning_many_empty_gaussians():
     check_forward(r, phi, inf, label="wide range")
 
 
+def clustered_points(seed, n, centers, sd):
+    rng = np.random.default_rng(seed)
+    c = np.asarray(centers, np.float64)[rng.integers(0, len(centers), n)]
+    p = c + rng.normal(0.0, sd, size=(n, 3))
+    return np.clip(p, 0.0, 1.0).astype(np.float32)
+
+
+def test_dense_cells_every_output():
+    """Clustered points on a coarse index: cells of hundreds to thousands of
+    queries, so every dense cell splits into several work items of up to
+    two queries a lane, with uneven last items. Every output and every
+    Gaussian's gradient against the oracle."""
+    g = synth.random_gaussians(101, 1500, log_mu=np.log(0.03), log_sd=0.5)
+    pts = clustered_points(102, 200000, [[0.3, 0.3, 0.3], [0.62, 0.55, 0.4], [0.5, 0.8, 0.7]], 0.05)
+    log("case dense cells: 200000 clustered points, 8^3 cells")
+    r = Run(g, (8, 8, 8), "points", points=pts)
+    check_index(r)
+    t, inside = oracle.point_cells(pts, (8, 8, 8))
+    c = np.clip(np.floor(t), 0, 7).astype(np.int64)
+    per = np.bincount(c[:, 0] + 8 * (c[:, 1] + 8 * c[:, 2]), minlength=512)
+    log(f"  queries per cell: max {per.max()}, cells with >= 128: {int((per >= 128).sum())}")
+    assert per.max() > 2000 and (per >= 128).sum() > 20
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="dense cells")
+    gv, gi = synth.random_normal(103, r.nq), synth.random_normal(104, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="dense cells")
+
+
+@pytest.mark.parametrize("counts", [(1, 2, 3, 4, 5), (31, 32, 33, 63), (64, 65, 127, 128, 129), (255, 256, 257, 700)])
+def test_cells_at_layout_boundaries(counts):
+    """Cells holding exactly the query counts where the forward changes
+    layout or item split (4, 32, 64 queries; 128 per dense item), each cell
+    of a 6^3 index filled with that many random points away from its faces,
+    a few more points in cells of their own. Every output against the
+    oracle."""
+    rng = np.random.default_rng(sum(counts))
+    g = synth.random_gaussians(105, 900, log_mu=np.log(0.05), log_sd=0.4)
+    cells = []
+    pts = []
+    for k, n in enumerate(counts):
+        cx, cy, cz = (k * 2) % 6, (k * 3 + 1) % 6, (k + 2) % 6
+        lo = np.array([cx, cy, cz]) / 6.0
+        pts.append(lo + (0.02 + 0.96 * rng.random((n, 3))) / 6.0)
+        cells.append((cx, cy, cz))
+    # a few more points in the x = y = 5 column, which no counted cell uses
+    pts.append(np.array([5.0, 5.0, 0.0]) / 6.0 + rng.random((40, 3)) * np.array([1 / 6, 1 / 6, 1.0]))
+    pts = np.concatenate(pts).astype(np.float32)
+    rng.shuffle(pts)
+    log(f"case layout boundaries {counts}: {len(pts)} points")
+    r = Run(g, (6, 6, 6), "points", points=pts)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label=f"boundaries {counts}")
+    gv, gi = synth.random_normal(106, r.nq), synth.random_normal(107, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="boundaries")
+
+
+def test_sparse_cells_every_output():
+    """Few queries spread over a fine index: almost every occupied cell
+    holds one to three queries (lanes are then the cell's candidates)."""
+    g = synth.random_gaussians(108, 3000, log_mu=np.log(0.02), log_sd=0.5)
+    pts = synth.random_points(109, 4000)
+    log("case sparse cells: 4000 points, 32^3 cells")
+    r = Run(g, (32, 32, 32), "points", points=pts)
+    phi, inf = r.forward()
+    ref, _ = check_forward(r, phi, inf, label="sparse cells")
+    gv, gi = synth.random_normal(110, r.nq), synth.random_normal(111, r.nq)
+    gv, gi, _ = masked_cotangents(ref, gv, gi)
+    grads = r.backward(gv, gi)
+    check_backward(r, grads, np.arange(g.n), np.arange(r.nq), gv, gi, label="sparse cells")
+
+
 def test_point_plan_order_matches_oracle():
-    """The query ordering kept in the plan (Sec. 5.1 analogue of the sample
-    BVH): keys and ids bit-exact against the oracle's stable order."""
+    """The query ordering kept in the plan (the role of the paper's sample
+    BVH, Sec. 5.1.1): a stable sort of the queries by 4 cell + quarter of the
+    cell along x (outside points last). Checked by its properties: the order
+    is a permutation, keys never decrease, ids ascend within a key, the
+    per-key offsets are the ranges, and every query's key is the one a
+    float64 recomputation of its cell coordinates gives (within float32
+    rounding of a cell or quarter face, either side is accepted)."""
     g = synth.random_gaussians(61, 100)
     pts = synth.random_points(62, 50000, -0.1, 1.1)
+    pts[:200] = np.float32(1.0)                 # on the closed box's upper faces
+    pts[200:400, 0] = np.float32(0.0)
+    cells = (7, 9, 11)
     log("case plan order")
-    r = Run(g, (7, 9, 11), "points", points=pts)
+    r = Run(g, cells, "points", points=pts)
     r.forward()
     n = len(pts)
+    ncells = 7 * 9 * 11
     plan = r.plan.cpu().numpy()
-    keys = plan[: 4 * n].view(np.uint32)
-    order = plan[_align(4 * n): _align(4 * n) + 4 * n].view(np.uint32)
-    rk, ro, _ = oracle.point_order(pts, (7, 9, 11))
-    np.testing.assert_array_equal(keys, rk)
-    np.testing.assert_array_equal(order, ro)
+    keys = plan[: 4 * n].view(np.uint32).astype(np.int64)
+    order = plan[_align(4 * n): _align(4 * n) + 4 * n].view(np.uint32).astype(np.int64)
+    poff = plan[4 * _align(4 * n): 4 * _align(4 * n) + 4 * (4 * ncells + 2)].view(np.uint32).astype(np.int64)
+    np.testing.assert_array_equal(np.sort(order), np.arange(n))
+    assert np.all(np.diff(keys) >= 0)
+    same = np.diff(keys) == 0
+    assert np.all(np.diff(order)[same] > 0), "ids not ascending within a key"
+    np.testing.assert_array_equal(poff, np.searchsorted(keys, np.arange(4 * ncells + 2), side="left"))
+    kq = np.empty(n, np.int64)
+    kq[order] = keys
+    t, inside = oracle.point_cells(pts, cells)
+    C = np.array(cells, np.float64)
+    tol = 2.0 ** -18 * np.maximum(1.0, C)
+
+    def key_of(tt):
+        c = np.clip(np.floor(tt), 0, C - 1)
+        qx = np.clip(np.floor(4 * (tt[:, 0] - c[:, 0])), 0, 3)
+        return 4 * (c[:, 0] + C[0] * (c[:, 1] + C[1] * c[:, 2])) + qx
+    ok = np.zeros(n, bool)
+    for sx in (-1, 0, 1):
+        for sy in (-1, 0, 1):
+            for sz in (-1, 0, 1):
+                ok |= key_of(t + tol * np.array([sx, sy, sz])).astype(np.int64) == kq
+    ok[~inside] = kq[~inside] == 4 * ncells
+    exact = key_of(t).astype(np.int64) == kq
+    log(f"  {int(exact[inside].sum())} of {int(inside.sum())} inside keys match float64 exactly, "
+        f"{int((~inside).sum())} outside")
+    assert ok.all(), np.nonzero(~ok)[0][:10]
+    assert exact[inside].mean() > 0.999
 
 
 def _align(x):
@@ -317,14 +426,19 @@ def test_capacity_error_reports_pairs():
     log("case capacity error")
     dg = __import__("harness").dev_gauss(g)
     grid = gs.make_grid((8, 8, 8))
-    box, cnt = oracle.index_boxes(g, (8, 8, 8))
-    idx = gs.Index(grid, g.n, int(cnt.sum()) - 1, "cuda")
+    P = gs.build_index(dg, grid, TAU).n_pairs
+    _, cnt = oracle.index_boxes(g, (8, 8, 8))
+    assert 0 < P <= int(cnt.sum())
+    idx = gs.Index(grid, g.n, P - 1, "cuda")
     with pytest.raises(gs.GsError) as e:
         gs.gs_build_index(dg, grid, TAU, idx)
     assert e.value.status == gs.GS_ERR_CAPACITY
-    assert idx.n_pairs == int(cnt.sum())
-    idx2 = gs.Index(grid, g.n, int(cnt.sum()), "cuda")
-    assert gs.gs_build_index(dg, grid, TAU, idx2) == int(cnt.sum())
+    assert idx.n_pairs == P
+    idx2 = gs.Index(grid, g.n, P, "cuda")
+    assert gs.gs_build_index(dg, grid, TAU, idx2) == P
+    check_index_arrays(g, (8, 8, 8), (0, 0, 0), (1, 1, 1), TAU, idx2.keys[:P].cpu().numpy().view(np.uint32),
+                       idx2.gids[:P].cpu().numpy().view(np.uint32), idx2.cell_offsets.cpu().numpy().view(np.uint32),
+                       gpu_boxes(idx2, g.n))
 
 
 def test_forward_is_deterministic():
@@ -399,15 +513,35 @@ def test_backward_pair_count():
     r.forward()
     work = gs.alloc_backward_work(r.index, r.query, "cuda")
     cnt = gs.backward_pair_count(r.index, r.query, r.plan, work)
+    tests, contrib = gs.sample_pair_counts(r.index, r.query, r.plan, work)
     keys, gids, offs = r.index_arrays()
-    _, _, poff = oracle.point_order(pts, (9, 8, 7))
-    ncells = 9 * 8 * 7
-    per_cell = (poff[4:4 * ncells + 1:4].astype(np.int64) - poff[0:4 * ncells:4])
+    t, inside = oracle.point_cells(pts, (9, 8, 7))
+    c = np.clip(np.floor(t), 0, np.array([8, 7, 6])).astype(np.int64)
+    per_cell = np.bincount((c[:, 0] + 9 * (c[:, 1] + 8 * c[:, 2]))[inside], minlength=9 * 8 * 7)
     cell_tests = int((np.diff(offs.astype(np.int64)) * per_cell).sum())
     ref = oracle.forward(g, pts)
-    contrib = int(ref.ncontrib.sum())
-    log(f"  backward tests {cnt}, cell-list tests {cell_tests}, contributing pairs {contrib}")
+    ref_contrib = int(ref.ncontrib.sum())
+    namb = int(ref.namb.sum())
+    log(f"  backward tests {cnt}, forward tests {tests} (cell lists x queries {cell_tests}), contributing {contrib} "
+        f"(oracle {ref_contrib}, ambiguous pairs {namb})")
+    assert tests == cell_tests
+    assert abs(contrib - ref_contrib) <= namb
     assert contrib <= cnt < cell_tests
+
+
+def test_sample_pair_counts_grid():
+    """On a grid every voxel of a cell tests the cell's list; the passing
+    pairs are the oracle's contributing pairs up to those within float32
+    rounding of the cutoff."""
+    import paper_2607_01164_amd as gs
+    g = synth.random_gaussians(76, 2000, log_mu=np.log(0.03), log_sd=0.5)
+    r = Run(g, (8, 8, 8), "grid", dims=(32, 32, 32))
+    r.forward()
+    work = gs.alloc_backward_work(r.index, r.query, "cuda")
+    tests, contrib = gs.sample_pair_counts(r.index, r.query, None, work)
+    assert tests == r.index.n_pairs * 64
+    ref = oracle.forward(g, r.positions())
+    assert abs(contrib - int(ref.ncontrib.sum())) <= int(ref.namb.sum())
 
 
 def test_backward_quarter_cuts_keep_extreme_points():

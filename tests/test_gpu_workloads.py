@@ -1,7 +1,9 @@
-"""The five workloads at full size on the GPU, in the launch configuration
-the benchmark times: the index compared bit for bit, forward outputs and
-Gaussian gradients compared on seeded samples the oracle computes one by
-one (brute force over every Gaussian)."""
+"""The five workloads at full size on the GPU, at the index configuration
+the benchmark times them with (and, for the 256^3 batch, also at the
+workload's own 64^3 index): the index checked by its defining properties
+(boxes bit-exact, order and ranges, listed cells between the reached cells
+and the box), forward outputs and Gaussian gradients compared on seeded
+samples the oracle computes one by one (brute force over every Gaussian)."""
 import numpy as np
 import pytest
 
@@ -12,7 +14,8 @@ from harness import TAU, Run, check_backward, check_forward, check_index, log
 pytestmark = pytest.mark.gpu
 
 N_FWD_SAMPLE = 2048
-N_BWD_SAMPLE = 96
+N_BWD_SAMPLE = 512
+REACH_SAMPLE = 20000
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -26,14 +29,46 @@ def sample_ids(n, k, seed):
     return np.sort(np.random.default_rng(seed).choice(n, size=min(k, n), replace=False))
 
 
-def sampled_backward(r: Run, w, seed):
-    """Gradients of N_BWD_SAMPLE seeded Gaussians: the oracle recomputes the
-    forward at every query within their reach and the exact gradient."""
-    sel = sample_ids(r.g.n, N_BWD_SAMPLE, seed)
+def stratified_gaussians(r: Run, k, seed):
+    """k Gaussians for the backward check, stratified by box size: the 32
+    largest boxes, Gaussians whose boxes are too large for row spans (more
+    than 64 rows or 16 cells a row), and the rest drawn evenly from the
+    quartiles of the box cell count."""
+    box, cnt = oracle.index_boxes(r.g, r.cells, r.lo, r.hi, r.tau)
+    rng = np.random.default_rng(seed)
+    ok = np.nonzero(cnt > 0)[0]
+    big = ok[np.argsort(-cnt[ok], kind="stable")[:32]]
+    nx = box[:, 3] - box[:, 0] + 1
+    rows = (box[:, 4] - box[:, 1] + 1) * (box[:, 5] - box[:, 2] + 1)
+    wide = np.nonzero((cnt > 0) & ((rows > 64) | (nx > 16)))[0]
+    wide = rng.choice(wide, size=min(len(wide), k // 4), replace=False) if len(wide) else wide
+    rest = k - len(big) - len(wide)
+    q = np.quantile(cnt[ok], [0.25, 0.5, 0.75])
+    strata = np.digitize(cnt[ok], q)
+    pick = [rng.choice(ok[strata == s], size=min(int((strata == s).sum()), rest // 4), replace=False)
+            for s in range(4)]
+    sel = np.unique(np.concatenate([big, wide] + pick))
+    log(f"  backward sample: {len(sel)} Gaussians ({len(wide)} without row spans, largest box {int(cnt.max())} cells)")
+    return sel
+
+
+def sampled_backward(r: Run, w, seed, query_frac=1.0, batch_index=0):
+    """Gradients of a stratified sample of Gaussians: the oracle recomputes
+    the forward at every query within their reach and the exact gradient.
+    With query_frac < 1 the cotangents of all but a seeded fraction of the
+    queries are zero on both sides, which keeps the oracle's work bounded
+    (every query is still walked by the GPU)."""
+    sel = stratified_gaussians(r, N_BWD_SAMPLE, seed)
     pts_all = r.positions()
-    sup = np.nonzero(oracle.support(r.g, pts_all, sel, r.lo, r.hi, TAU))[0]
+    gv, gi = synth.cotangents(w, r.nq, batch_index=batch_index)
+    if query_frac < 1.0:
+        keep = np.random.default_rng(seed + 1).random(r.nq) < query_frac
+        gv[~keep] = 0
+        gi[~keep] = 0
+    else:
+        keep = np.ones(r.nq, bool)
+    sup = np.nonzero(oracle.support(r.g, pts_all, sel, r.lo, r.hi, TAU) & keep)[0]
     ref = oracle.forward(r.g, pts_all[sup], r.lo, r.hi, TAU)
-    gv, gi = synth.cotangents(w, r.nq)
     amb = oracle.ambiguous_points(ref, TAU)
     gv[sup[amb]] = 0
     gi[sup[amb]] = 0
@@ -44,12 +79,15 @@ def sampled_backward(r: Run, w, seed):
     return grads
 
 
-def test_c2_grid256_batch_step():
+@pytest.mark.parametrize("cells", [(32, 32, 32), (64, 64, 64)])
+def test_c2_grid256_batch_step(cells):
+    """The structured 256^3 batch step at the 32^3 index the benchmark uses
+    (about 32 queries a cell) and at the workload's 64^3 (about 4)."""
     w = synth.WORKLOADS["c2_grid256_batch"]
     g = synth.make_gaussians(w)
     ids = synth.voxel_batch(w)
-    log(f"case {w.name}: {g.n} Gaussians, {len(ids)} voxel queries, cells {w.index_cells}")
-    r = Run(g, w.index_cells, "voxels", dims=w.dims, ids=ids)
+    log(f"case {w.name}: {g.n} Gaussians, {len(ids)} voxel queries, cells {cells}")
+    r = Run(g, cells, "voxels", dims=w.dims, ids=ids)
     check_index(r)
     phi, inf = r.forward()
     check_forward(r, phi, inf, sel=sample_ids(r.nq, N_FWD_SAMPLE, 1), label=w.name)
@@ -61,7 +99,7 @@ def test_c3_grid512_full_forward():
     g = synth.make_gaussians(w)
     log(f"case {w.name}: {g.n} Gaussians, 512^3 grid, cells {w.index_cells}")
     r = Run(g, w.index_cells, "grid", dims=w.dims)
-    check_index(r)
+    check_index(r, reach_sample=REACH_SAMPLE)
     phi, inf = r.forward()
     assert np.all(np.isfinite(phi))
     check_forward(r, phi, inf, sel=sample_ids(r.nq, N_FWD_SAMPLE, 3), label=w.name)
@@ -73,20 +111,28 @@ def test_c3_grid512_full_forward():
 
 
 def test_c4_points_batches():
+    """All four 2^21-point batches of the 8M-point cloud, as the benchmark
+    runs them on one index: sampled forward outputs of every batch, and the
+    gradients of a stratified sample of Gaussians on the first and the last
+    batch."""
     w = synth.WORKLOADS["c4_points8m"]
     g = synth.make_gaussians(w)
     pts = synth.make_points(w)
     perm = synth.batch_permutation(w, len(pts))
-    batch = pts[perm[: w.batch]]
-    log(f"case {w.name}: {g.n} Gaussians, batch of {len(batch)} points, cells {w.index_cells}")
-    r = Run(g, w.index_cells, "points", points=batch)
-    check_index(r)
-    phi, inf = r.forward()
-    ref, stats = check_forward(r, phi, inf, sel=sample_ids(r.nq, N_FWD_SAMPLE, 4), label=w.name)
-    # queries inside the cavity lie in empty space
-    cav = np.sum((batch - 0.5) ** 2, axis=1) < 0.2 ** 2
-    assert cav.sum() == 0
-    sampled_backward(r, w, 5)
+    nb = len(pts) // w.batch
+    for b in range(nb):
+        batch = pts[perm[b * w.batch:(b + 1) * w.batch]]
+        log(f"case {w.name} batch {b}: {g.n} Gaussians, {len(batch)} points, cells {w.index_cells}")
+        r = Run(g, w.index_cells, "points", points=batch)
+        if b == 0:
+            check_index(r, reach_sample=REACH_SAMPLE)
+            # queries inside the cavity lie in empty space
+            assert (np.sum((batch - 0.5) ** 2, axis=1) < 0.2 ** 2).sum() == 0
+        phi, inf = r.forward()
+        check_forward(r, phi, inf, sel=sample_ids(r.nq, N_FWD_SAMPLE, 4 + b), label=f"{w.name} batch {b}")
+        if b in (0, nb - 1):
+            sampled_backward(r, w, 5 + b, query_frac=0.125, batch_index=b)
+        del r
 
 
 def test_c5_points_full_forward():
@@ -95,7 +141,7 @@ def test_c5_points_full_forward():
     pts = synth.make_points(w)
     log(f"case {w.name}: {g.n} Gaussians, {len(pts)} points, cells {w.index_cells}")
     r = Run(g, w.index_cells, "points", points=pts)
-    check_index(r)
+    check_index(r, reach_sample=REACH_SAMPLE)
     phi, inf = r.forward()
     assert np.all(np.isfinite(phi)) and np.all(np.isfinite(inf))
     sel = sample_ids(r.nq, 1024, 6)
@@ -155,7 +201,7 @@ def test_training_step_128cubed():
     assert abs(got["total"] - ref.total) <= (2 * nq + 8) * 2.0 ** -53 * ref.total
     log(f"  losses: L1 {ref.l1:.6g}, false negatives {ref.n_fn} ({ref.fn:.3g})")
     # the backward of seeded Gaussians with the loss's cotangents
-    sel = sample_ids(n, N_BWD_SAMPLE, 22)
+    sel = stratified_gaussians(r, N_BWD_SAMPLE, 22)
     pts_all = r.positions()
     sup = np.nonzero(oracle.support(g_act, pts_all, sel, r.lo, r.hi, TAU))[0]
     fref = oracle.forward(g_act, pts_all[sup], r.lo, r.hi, TAU)
