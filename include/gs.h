@@ -225,6 +225,28 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
                              size_t work_bytes, hipStream_t stream);
 
 /*
+ * gs_sample_backward for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving or training loops, harnesses that
+ * forbid hipMalloc. Same arguments, results and errors as
+ * gs_sample_backward (bit-identical outputs), except that its workspace is
+ * a static device array of GS_BACKWARD_NOALLOC_MAX_BYTES inside the
+ * library instead of a caller buffer: no device memory is allocated or
+ * freed. Each GPU the library runs on holds its own copy of that array
+ * from the library's load until the process ends. A call whose workspace
+ * (gs_backward_work_bytes) would exceed it returns GS_ERR_WORKSPACE. Calls
+ * on one GPU share its array, and every call overwrites what the last one
+ * left there (nothing in it needs to start cleared): calls that may
+ * overlap on one GPU (other streams, other host threads) race and must be
+ * ordered by the caller.
+ */
+#define GS_BACKWARD_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+gs_status gs_sample_backward_noalloc(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                                     const void *plan, size_t plan_bytes, const float *value, const float *influence,
+                                     const float *grad_value, const float *grad_influence, float *d_mean,
+                                     float *d_scale, float *d_rot, float *d_value, float *d_weight,
+                                     hipStream_t stream);
+
+/*
  * For measurement: the number of (Gaussian, query) pairs gs_sample_backward
  * tests against the cutoff for this built index, query and plan (the plan
  * a gs_sample call filled; none for GRID queries): per Gaussian, the

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -449,6 +450,40 @@ void prof_end(const char *name, hipStream_t s) {
 
 }  // namespace gs
 
+// Workspace of gs_sample_backward_noalloc: a file-scope device array, one
+// copy per GPU, held until the process ends. Host code never uses the
+// array's name as an address: each device's copy is located once with
+// hipGetSymbolAddress (that device current) and the address kept per device.
+namespace {
+
+constexpr size_t kNoAllocScratchBytes = GS_BACKWARD_NOALLOC_MAX_BYTES;
+__device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Address of the current device's copy of scratch, or null with *err set.
+void *scratch_address(hipError_t *err) {
+    int dev = 0;
+    *err = hipGetDevice(&dev);
+    if (*err != hipSuccess) return nullptr;
+    if (dev < 0 || dev >= kMaxDevices) {
+        *err = hipErrorInvalidDevice;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        *err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (*err != hipSuccess) return nullptr;
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
 extern "C" {
 
 const char *gs_last_error(void) { return g_err.c_str(); }
@@ -711,6 +746,28 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
                            d_scale, d_rot, d_value, d_weight, stream),
            "gs_sample_backward");
     return GS_OK;
+}
+
+gs_status gs_sample_backward_noalloc(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                                     const void *plan, size_t plan_bytes, const float *value, const float *influence,
+                                     const float *grad_value, const float *grad_influence, float *d_mean,
+                                     float *d_scale, float *d_rot, float *d_value, float *d_weight,
+                                     hipStream_t stream) {
+    std::string why;
+    if (!index || index->n_pairs < 0 || !query_valid(query, &why))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample_backward_noalloc: %s",
+                    !index ? "index is null" : (index->n_pairs < 0 ? "the index has not been built" : why.c_str()));
+    const size_t need = bwd_layout(nullptr, index, query).bytes;
+    if (need > kNoAllocScratchBytes)
+        return fail(GS_ERR_WORKSPACE,
+                    "gs_sample_backward_noalloc: needs %zu bytes of workspace, more than its fixed %zu "
+                    "(use gs_sample_backward with a workspace of gs_backward_work_bytes)",
+                    need, kNoAllocScratchBytes);
+    hipError_t e = hipSuccess;
+    void *work = scratch_address(&e);
+    if (!work) return hip_fail(e, "gs_sample_backward_noalloc: locating the static workspace");
+    return gs_sample_backward(gauss, index, query, plan, plan_bytes, value, influence, grad_value, grad_influence,
+                              d_mean, d_scale, d_rot, d_value, d_weight, work, kNoAllocScratchBytes, stream);
 }
 
 // ---------------------------------------------------------------------------

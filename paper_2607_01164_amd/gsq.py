@@ -34,7 +34,7 @@ EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_b
             "gs_profile_select", "gs_profile_reset", "gs_profile_read", "gs_activate", "gs_activate_backward",
             "gs_loss_work_bytes", "gs_loss", "gs_densify_work_bytes", "gs_densify",
             "gs_sample_gaussian_major_work_bytes", "gs_sample_gaussian_major", "gs_backward_pair_count",
-            "gs_sample_pair_counts")
+            "gs_sample_pair_counts", "gs_sample_backward_noalloc")
 
 
 class GsLibraryMissing(RuntimeError):
@@ -120,6 +120,9 @@ def load_library():
     L.gs_sample_backward.restype = ctypes.c_int
     L.gs_sample_backward.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, sz, vp, vp, vp, vp, vp, vp, vp, vp,
                                      vp, vp, sz, vp]
+    L.gs_sample_backward_noalloc.restype = ctypes.c_int
+    L.gs_sample_backward_noalloc.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, sz, vp, vp, vp, vp, vp,
+                                             vp, vp, vp, vp, vp]
     L.gs_last_error.restype = ctypes.c_char_p
     L.gs_last_error.argtypes = []
     L.gs_version.restype = ctypes.c_int
@@ -423,6 +426,30 @@ def gs_sample_backward(gauss: Gaussians, index: Index, query: Query, plan: Optio
         value.data_ptr(), influence.data_ptr(), grad_value.data_ptr(), grad_influence.data_ptr(),
         grads.mean.data_ptr(), grads.scale.data_ptr(), grads.rot.data_ptr(), grads.value.data_ptr(),
         grads.weight.data_ptr(), work.data_ptr(), work.numel(), _stream(stream))
+    _check(st)
+
+
+def gs_sample_backward_noalloc(gauss: Gaussians, index: Index, query: Query, plan: Optional[torch.Tensor],
+                               value: torch.Tensor, influence: torch.Tensor, grad_value: torch.Tensor,
+                               grad_influence: torch.Tensor, grads: Grads, stream=None) -> None:
+    """gs_sample_backward with the library's static workspace (no device
+    allocation; see include/gs.h)."""
+    g = gauss.c()
+    q = query.c()
+    n = query.size()
+    for t, nm in ((value, "value"), (influence, "influence"), (grad_value, "grad_value"),
+                  (grad_influence, "grad_influence")):
+        _dev_f32(t, nm)
+        if t.numel() < n:
+            raise ValueError(f"{nm} needs {n} elements")
+    for t, nm in ((grads.mean, "d_mean"), (grads.scale, "d_scale"), (grads.rot, "d_rot"), (grads.value, "d_value"),
+                  (grads.weight, "d_weight")):
+        _dev_f32(t, nm)
+    st = load_library().gs_sample_backward_noalloc(
+        ctypes.byref(g), ctypes.byref(index.c), ctypes.byref(q), _ptr(plan), 0 if plan is None else plan.numel(),
+        value.data_ptr(), influence.data_ptr(), grad_value.data_ptr(), grad_influence.data_ptr(),
+        grads.mean.data_ptr(), grads.scale.data_ptr(), grads.rot.data_ptr(), grads.value.data_ptr(),
+        grads.weight.data_ptr(), _stream(stream))
     _check(st)
 
 

@@ -238,6 +238,19 @@ def test_pair_counts_validate_arguments():
     assert st == gs.GS_ERR_INVALID_ARGUMENT
 
 
+def test_noalloc_backward_refuses_oversized_work_before_device_work():
+    """The static-workspace backward checks its fixed limit on the host."""
+    L = gs.load_library()
+    idx = built_fake_index(n_gauss=2_000_000)
+    q = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 3_000_000, None, FAKE)
+    st = L.gs_sample_backward_noalloc(ctypes.byref(fake_gauss(2_000_000)), ctypes.byref(idx), ctypes.byref(q), FAKE,
+                                      1 << 40, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == gs.GS_ERR_WORKSPACE and b"fixed" in L.gs_last_error()
+    st = L.gs_sample_backward_noalloc(ctypes.byref(fake_gauss()), ctypes.byref(fake_index()), ctypes.byref(q), FAKE,
+                                      1 << 40, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+
+
 def test_backward_validates_arguments():
     L = gs.load_library()
     idx = built_fake_index()
