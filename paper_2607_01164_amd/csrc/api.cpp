@@ -132,6 +132,7 @@ int gauss_order_bits(const gs_grid *g) { return gauss_order_full_bits(g) - gauss
 struct IndexWork {
     Record *rec;
     CellBox *box;
+    FwdRecord *frec;
     uint8_t *spans;      // [n][kSpanStride] row spans and quarter codes of trimmed boxes
     uint32_t *gorder;    // [n] Gaussians in spatial order
     uint32_t *gkeys;     // [n] their sort keys
@@ -160,6 +161,7 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     w.rec = c.take<Record>((size_t)(n > 0 ? n : 1));
     w.box = c.take<CellBox>((size_t)(n > 0 ? n : 1));
     const size_t n1 = (size_t)(n > 0 ? n : 1);
+    w.frec = c.take<FwdRecord>(n1);
     w.spans = c.take<uint8_t>(n1 * kSpanStride);
     w.gorder = c.take<uint32_t>(n1);
     w.gkeys = c.take<uint32_t>(n1);
@@ -547,7 +549,7 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     IndexWork w = index_layout(index->work, n, grid, index->capacity);
 
     GS_TRY(launch_preprocess(gauss->mean, gauss->scale, gauss->rot, gauss->value, gauss->weight, n, gp,
-                             index_radius(tau), w.rec, w.box, w.spans, w.pair_off, w.pair_sum, stream),
+                             index_radius(tau), w.rec, w.frec, w.box, w.spans, w.pair_off, w.pair_sum, stream),
            "gs_build_index: preprocess");
     {
         // groups past ceil(n / 64) hold only count[n] = 0: their prefix is the total
@@ -659,14 +661,14 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
     IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
     const float T = cutoff_T(index->tau);
     if (query->kind == GS_QUERY_GRID) {
-        GS_TRY(launch_sample_grid(qp, gp, w.rec, index->gids, index->cell_offsets, T, index->tau, out_value,
+        GS_TRY(launch_sample_grid(qp, gp, w.frec, index->gids, index->cell_offsets, T, index->tau, out_value,
                                   out_influence, stream),
                "gs_sample: grid sampler");
         return GS_OK;
     }
     Plan p;
     if ((st = order_queries("gs_sample", qp, gp, nq, plan, plan_bytes, &p, stream)) != GS_OK) return st;
-    GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
+    GS_TRY(launch_sample_points(qp, gp, w.frec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
                                 index->tau, out_value, out_influence, p.res, stream),
            "gs_sample: point sampler");
     return GS_OK;
@@ -958,7 +960,7 @@ gs_status gs_sample_pair_counts(const gs_index *index, const gs_query *query, co
     IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
     unsigned long long *totals = (unsigned long long *)bw.b.moments;
-    GS_TRY(launch_count_sample_pairs(qp, gp, w.rec, index->gids, index->cell_offsets, p.keys, p.res.pos,
+    GS_TRY(launch_count_sample_pairs(qp, gp, w.frec, index->gids, index->cell_offsets, p.keys, p.res.pos,
                                      cutoff_T(index->tau), totals, stream),
            "gs_sample_pair_counts");
     for (int k = 0; k < 2; ++k) {

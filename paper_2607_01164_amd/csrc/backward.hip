@@ -205,6 +205,8 @@ __device__ __forceinline__ float reduce11(const float v[11], uint32_t lane) {
 }
 
 // Queue of contributing pairs of one wave: (u0, u1, u2, Q) and the point.
+// (Loading each lane's (alpha, beta) with its position, so that the queue
+// holds them instead of the point, was slower: 8 more bytes a test.)
 constexpr uint32_t kQueue = 2 * kWave;
 
 __device__ __forceinline__ void drain(const Record &r, const float4 *qu, const uint32_t *qk, uint32_t head,
@@ -225,6 +227,8 @@ __device__ __forceinline__ void drain(const Record &r, const float4 *qu, const u
 // at a time rather than on a fixed eighth of it.
 constexpr int kBwdWaves = 1;
 constexpr int kBwdBlock = kBwdWaves * kWave;
+// Element windows per step of the walk (see the window loop).
+constexpr uint32_t kBwdWindows = 2;
 
 // Gaussians per wavefront: consecutive Gaussians of gorder share a wave, so
 // that their rows are found together. Below kPackMinGauss Gaussians one per
@@ -415,15 +419,18 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
             const uint32_t lb = gend - rb < nrows ? gend - rb : nrows;
             const uint32_t Ea = __builtin_amdgcn_readlane(rbeg, la);
             const uint32_t Eb = lb < (uint32_t)kWave ? __builtin_amdgcn_readlane(rbeg, lb) : E;
-            for (uint32_t e0 = Ea; e0 < Eb; e0 += kWave) {
+            // The element window [e0, e0 + 64): the offset of each lane's row
+            // (ko: element e of the row is point e + ko; grids: x offset xo and
+            // the row's y, z).
+            auto locate = [&](uint32_t e0, uint32_t &ko, uint32_t &xo, float &py, float &pz) {
                 // rbeg rises with the lane (lanes past nrows hold E), so the
                 // rows starting at or before e0 are a prefix of the lanes and
                 // the last of them holds element e0
                 const uint32_t j0 = (uint32_t)__popcll(mask_le_u(rbeg, e0)) - 1u;
                 const uint32_t e = e0 + lane;
-                const uint32_t ko0 = __builtin_amdgcn_readlane(kofs, j0);  // row of element e0
-                uint32_t ko = ko0, xo = 0;
-                float py = 0.0f, pz = 0.0f;
+                ko = __builtin_amdgcn_readlane(kofs, j0);  // row of element e0
+                xo = 0;
+                py = pz = 0.0f;
                 if (GRID) {
                     xo = __builtin_amdgcn_readlane(xofs, j0);
                     py = readlane_f(rpy, j0);
@@ -443,10 +450,15 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
                         pz = nxt ? readlane_f(rpz, j) : pz;
                     }
                 }
+            };
+            // The cutoff test of the window's pairs; contributing ones go to
+            // the queue, which is processed 64 pairs at a time.
+            auto test = [&](uint32_t e0, uint32_t ko, uint32_t xo, float py, float pz, float4 p) {
                 // lanes past the Gaussian's last element read the elements
                 // after it: points of later rows, or past the batch's last
                 // row, whose last point is at most n - 1, up to 63 entries of
                 // the plan's spare tail; their test has no effect
+                const uint32_t e = e0 + lane;
                 const bool valid = e < Eb;
                 const uint32_t k = e + ko;
                 float u0, u1, u2, Q;
@@ -454,12 +466,11 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
                     const float px = g.lo[0] + ((float)(e + xo) + 0.5f) * q.vsz[0];
                     Q = whiten(r, px, py, pz, u0, u1, u2);
                 } else {
-                    const float4 p = plan_pos[k];
                     Q = whiten(r, p.x, p.y, p.z, u0, u1, u2);
                 }
                 const bool hit = valid && Q <= T;
                 const uint64_t mask = mask_le_f(Q, T) & mask_lt_u(e, Eb);
-                if (mask == 0) continue;
+                if (mask == 0) return;
                 if (hit) {
                     const uint32_t pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
@@ -475,6 +486,24 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
                     head = (head + kWave) & (kQueue - 1);
                     cnt -= kWave;
                 }
+            };
+            // Windows are taken two at a time: both positions are loaded
+            // before either is tested, so one load's latency overlaps the
+            // other window's work.
+            for (uint32_t e0 = Ea; e0 < Eb; e0 += kBwdWindows * kWave) {
+                uint32_t koA, xoA, koB = 0, xoB = 0;
+                float pyA, pzA, pyB = 0.0f, pzB = 0.0f;
+                const uint32_t e1 = e0 + kWave;
+                const bool two = kBwdWindows > 1 && e1 < Eb;
+                float4 pA = make_float4(0.0f, 0.0f, 0.0f, 0.0f), pB = pA;
+                locate(e0, koA, xoA, pyA, pzA);
+                if (!GRID) pA = plan_pos[e0 + lane + koA];
+                if (two) {
+                    locate(e1, koB, xoB, pyB, pzB);
+                    if (!GRID) pB = plan_pos[e1 + lane + koB];
+                }
+                test(e0, koA, xoA, pyA, pzA, pA);
+                if (two) test(e1, koB, xoB, pyB, pzB, pB);
             }
         }
     }

@@ -24,6 +24,29 @@ struct alignas(16) Record {
     float4 r0, r1, r2, r3;
 };
 
+// The forward samplers' record, 48 bytes, written with Record:
+//   f0 = (mu_x, mu_y, mu_z, w)
+//   f1 = (U00, U01, U02, v)      U upper triangular with U^T U = M^T M, the
+//   f2 = (U11, U12, U22, 0)      inverse covariance, so Q = |U (p - mu)|^2
+// U (the Cholesky factor of the inverse covariance) takes 6 products and
+// sums where M takes 9, and three 16-byte quarters where M takes four; its
+// float32 rounding bounds Q as M's does (|U| and |M| have the same 2-norm).
+// Formed in float64 and rounded once. Invalid Gaussians get zeros.
+struct alignas(16) FwdRecord {
+    float4 f0, f1, f2;
+};
+constexpr int kFwdQuads = 3;  // 16-byte quarters of a FwdRecord
+
+// Q = |U (p - mu)|^2 in the one order of float32 operations every forward
+// sampler and the pair counter use.
+__device__ __forceinline__ float fwd_q(const FwdRecord &r, float px, float py, float pz) {
+    const float dx = px - r.f0.x, dy = py - r.f0.y, dz = pz - r.f0.z;
+    const float u0 = __builtin_fmaf(r.f1.x, dx, __builtin_fmaf(r.f1.y, dy, r.f1.z * dz));
+    const float u1 = __builtin_fmaf(r.f2.x, dy, r.f2.y * dz);
+    const float u2 = r.f2.z * dz;
+    return __builtin_fmaf(u0, u0, __builtin_fmaf(u1, u1, u2 * u2));
+}
+
 // Cell box of a Gaussian: (x0, y0, z0, trimmed) and (x1, y1, z1, 0),
 // inclusive; an empty box has x1 < x0. When trimmed is 1 the box lists, in
 // each of its (y, z) rows (row r = (y - y0) + ny (z - z0)), only the cells
@@ -276,7 +299,8 @@ struct GridParams {
 // block_sum[b] the sum over elements [64 b, 64 b + 64) of count
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
-                             CellBox *box, uint8_t *spans, uint64_t *count, uint64_t *block_sum, hipStream_t s);
+                             FwdRecord *frec, CellBox *box, uint8_t *spans, uint64_t *count, uint64_t *block_sum,
+                             hipStream_t s);
 // tile_first: ceil(npairs / kSortTile) words of scratch
 hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8_t *spans, int64_t n, int64_t npairs,
                        const GridParams &g,
@@ -342,7 +366,7 @@ __device__ __forceinline__ void query_position(const QueryParams &q, const GridP
 // the first sort digit's tile counts.
 hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids,
                              const RadixPass0 &pass0, hipStream_t s);
-hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
+hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const uint32_t *gids,
                               const uint32_t *cell_off, float T, float tau, float *out_v, float *out_i,
                               hipStream_t s);
 // Work items of the ordered-query sampler (kept in the plan).
@@ -362,7 +386,7 @@ struct PlanResults {
     float2 *out;
 };
 
-hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const uint32_t *gids,
                                 const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
                                 const PlanResults &pr, hipStream_t s);
@@ -371,7 +395,7 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
 // totals[0] and totals[1] (device, 16 bytes); plan_keys and plan_pos are
 // the sorted keys and the positions a forward left in the plan (unused for
 // GRID queries).
-hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const Record *rec,
+hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const FwdRecord *rec,
                                      const uint32_t *gids, const uint32_t *cell_off, const uint32_t *plan_keys,
                                      const float4 *plan_pos, float T, unsigned long long *totals, hipStream_t s);
 

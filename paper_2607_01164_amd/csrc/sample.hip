@@ -3,7 +3,7 @@
 //
 // Grid queries (Sec. 4.1.3, Fig. 4 C): one wavefront per (cell, 64 voxels of
 // the cell); every lane is a voxel and all lanes walk the cell's Gaussian
-// list together. The 64-byte Gaussian records are staged in the wave's LDS
+// list together. The 48-byte Gaussian records are staged in the wave's LDS
 // planes 64 at a time (the paper's shared-memory batches) and read there
 // with one address for all lanes.
 //
@@ -36,34 +36,29 @@ constexpr float kNegHalfLog2e = -0.72134752044448170368f;
 constexpr int kSampWaves = 1;
 constexpr int kSampBlock = kSampWaves * kWave;
 
-// Q = |M (p - mu)|^2 of a record at a point, in the one order of float32
-// operations every sampler and the pair counter use.
-__device__ __forceinline__ float cutoff_q(const Record &r, float px, float py, float pz) {
-    const float dx = px - r.r0.x, dy = py - r.r0.y, dz = pz - r.r0.z;
-    const float u0 = fmaf_(r.r1.x, dx, fmaf_(r.r1.y, dy, r.r1.z * dz));
-    const float u1 = fmaf_(r.r2.x, dx, fmaf_(r.r2.y, dy, r.r2.z * dz));
-    const float u2 = fmaf_(r.r3.x, dx, fmaf_(r.r3.y, dy, r.r3.z * dz));
-    return fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
+// Q of a forward record at a point (fwd_q: Q = |U (p - mu)|^2).
+__device__ __forceinline__ float cutoff_q(const FwdRecord &r, float px, float py, float pz) {
+    return fwd_q(r, px, py, pz);
 }
 
-__device__ __forceinline__ void accumulate(const Record &r, float px, float py, float pz, float T, float &I,
+__device__ __forceinline__ void accumulate(const FwdRecord &r, float px, float py, float pz, float T, float &I,
                                            float &V) {
     const float Q = cutoff_q(r, px, py, pz);
     if (Q <= T) {
-        const float a = r.r0.w * exp2_hw(Q * kNegHalfLog2e);
+        const float a = r.f0.w * exp2_hw(Q * kNegHalfLog2e);
         I += a;
-        V = fmaf_(a, r.r1.w, V);
+        V = fmaf_(a, r.f1.w, V);
     }
 }
 
 // Walk a wave-uniform candidate list [ja, jb) for one query per lane. The
-// list is staged in the wave's LDS planes (buf: 4 planes of kWave float4) 64
+// list is staged in the wave's LDS planes (buf: 3 planes of kWave float4) 64
 // records at a time: lane l copies candidate c0 + l's record from memory
 // straight into LDS (lanes past the list copy its last record), the ids of
 // the next 64 are fetched meanwhile, and every lane then reads each record
 // with the same address (a broadcast). One wait for memory per 64
 // candidates, instead of a dependent id and record load per candidate.
-__device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
+__device__ __forceinline__ void walk_staged(const FwdRecord *__restrict__ rec, const uint32_t *__restrict__ gids,
                                             uint32_t ja, uint32_t jb, uint32_t lane, float4 *buf, float px,
                                             float py, float pz, float T, float &I, float &V) {
     uint32_t gnext = 0;
@@ -71,7 +66,7 @@ __device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, cons
     for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
         const float4 *src = (const float4 *)(rec + gnext);
 #pragma unroll
-        for (int qq = 0; qq < 4; ++qq)
+        for (int qq = 0; qq < kFwdQuads; ++qq)
             __builtin_amdgcn_global_load_lds((const void *)(src + qq),
                                              (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
         if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
@@ -80,24 +75,21 @@ __device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, cons
         const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
         uint32_t s = 0;
         for (; s + 2 <= cnt; s += 2) {
-            Record a, b;
-            a.r0 = buf[s];
-            a.r1 = buf[kWave + s];
-            a.r2 = buf[2 * kWave + s];
-            a.r3 = buf[3 * kWave + s];
-            b.r0 = buf[s + 1];
-            b.r1 = buf[kWave + s + 1];
-            b.r2 = buf[2 * kWave + s + 1];
-            b.r3 = buf[3 * kWave + s + 1];
+            FwdRecord a, b;
+            a.f0 = buf[s];
+            a.f1 = buf[kWave + s];
+            a.f2 = buf[2 * kWave + s];
+            b.f0 = buf[s + 1];
+            b.f1 = buf[kWave + s + 1];
+            b.f2 = buf[2 * kWave + s + 1];
             accumulate(a, px, py, pz, T, I, V);
             accumulate(b, px, py, pz, T, I, V);
         }
         if (s < cnt) {
-            Record a;
-            a.r0 = buf[s];
-            a.r1 = buf[kWave + s];
-            a.r2 = buf[2 * kWave + s];
-            a.r3 = buf[3 * kWave + s];
+            FwdRecord a;
+            a.f0 = buf[s];
+            a.f1 = buf[kWave + s];
+            a.f2 = buf[2 * kWave + s];
             accumulate(a, px, py, pz, T, I, V);
         }
         // every lane has read the planes before the next chunk overwrites them
@@ -109,7 +101,7 @@ __device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, cons
 // wave's LDS planes 64 records at a time as in walk_staged: each record
 // read there serves the lane's R queries.
 template <uint32_t R>
-__device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
+__device__ __forceinline__ void walk_staged_r(const FwdRecord *__restrict__ rec, const uint32_t *__restrict__ gids,
                                               uint32_t ja, uint32_t jb, uint32_t lane, float4 *buf,
                                               const float (&px)[R], const float (&py)[R], const float (&pz)[R],
                                               float T, float (&I)[R], float (&V)[R]) {
@@ -118,7 +110,7 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
     for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
         const float4 *src = (const float4 *)(rec + gnext);
 #pragma unroll
-        for (int qq = 0; qq < 4; ++qq)
+        for (int qq = 0; qq < kFwdQuads; ++qq)
             __builtin_amdgcn_global_load_lds((const void *)(src + qq),
                                              (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
         if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
@@ -126,11 +118,10 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
         __builtin_amdgcn_wave_barrier();
         const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
         for (uint32_t s = 0; s < cnt; ++s) {
-            Record a;
-            a.r0 = buf[s];
-            a.r1 = buf[kWave + s];
-            a.r2 = buf[2 * kWave + s];
-            a.r3 = buf[3 * kWave + s];
+            FwdRecord a;
+            a.f0 = buf[s];
+            a.f1 = buf[kWave + s];
+            a.f2 = buf[2 * kWave + s];
 #pragma unroll
             for (uint32_t t = 0; t < R; ++t) accumulate(a, px[t], py[t], pz[t], T, I[t], V[t]);
         }
@@ -140,11 +131,11 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
 }
 
 
-__global__ __launch_bounds__(kSampBlock) void k_sample_grid(QueryParams q, GridParams g, const Record *__restrict__ rec,
+__global__ __launch_bounds__(kSampBlock) void k_sample_grid(QueryParams q, GridParams g, const FwdRecord *__restrict__ rec,
                                                         const uint32_t *__restrict__ gids,
                                                         const uint32_t *__restrict__ cell_off, float T, float tau,
                                                         float *__restrict__ out_v, float *__restrict__ out_i) {
-    __shared__ float4 s_grec[kSampWaves][4 * kWave];
+    __shared__ float4 s_grec[kSampWaves][kFwdQuads * kWave];
     const uint32_t rx = (uint32_t)(q.dims[0] / g.cells[0]);
     const uint32_t ry = (uint32_t)(q.dims[1] / g.cells[1]);
     const uint32_t rz = (uint32_t)(q.dims[2] / g.cells[2]);
@@ -226,8 +217,8 @@ __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams
 constexpr uint32_t kDenseMin = 32;
 // A cell of at least 2 kDenseMin queries is dense: lanes are its queries,
 // kDenseR per lane, so each record read from LDS serves kDenseR queries
-// (one per lane leaves the walk bound by LDS reads: four 16-byte broadcast
-// reads per candidate against 16 VALU operations). Its work items take at
+// (one per lane leaves the walk bound by LDS reads: three 16-byte broadcast
+// reads per candidate against 13 VALU operations). Its work items take at
 // most kDenseItem queries each, the cell's queries split evenly over them.
 constexpr uint32_t kDenseR = 2;
 constexpr uint32_t kDenseItem = kDenseR * kWave;
@@ -302,9 +293,9 @@ __global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restr
     }
 }
 
-__device__ __forceinline__ float eval_a(const Record &r, float px, float py, float pz, float T) {
+__device__ __forceinline__ float eval_a(const FwdRecord &r, float px, float py, float pz, float T) {
     const float Q = cutoff_q(r, px, py, pz);
-    return Q <= T ? r.r0.w * exp2_hw(Q * kNegHalfLog2e) : 0.0f;
+    return Q <= T ? r.f0.w * exp2_hw(Q * kNegHalfLog2e) : 0.0f;
 }
 
 // sum over the 64 lanes, returned to every lane
@@ -343,7 +334,7 @@ __device__ __forceinline__ float slot_sum(float x) {
 template <uint32_t ROWS>
 __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t pa, uint32_t ja, uint32_t jb,
                                            uint32_t c, uint32_t ncells, const QueryParams &q, const GridParams &g,
-                                           const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
+                                           const FwdRecord *__restrict__ rec, const uint32_t *__restrict__ gids,
                                            const uint32_t *__restrict__ order, float T, float tau,
                                            float *__restrict__ out_v, float *__restrict__ out_i,
                                            const PlanResults &pr, float4 *buf) {
@@ -379,7 +370,7 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
         for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
             const float4 *src = (const float4 *)(rec + gnext);
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq)
+            for (int qq = 0; qq < kFwdQuads; ++qq)
                 __builtin_amdgcn_global_load_lds((const void *)(src + qq),
                                                  (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
             if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
@@ -389,18 +380,17 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
             const uint32_t nstep = left >= (uint32_t)kWave ? kWave / SL : (left + SL - 1) / SL;
             for (uint32_t st = 0; st < nstep; ++st) {
                 const uint32_t sidx = SL * st + sl;
-                Record r;
-                r.r0 = buf[sidx];
-                r.r1 = buf[kWave + sidx];
-                r.r2 = buf[2 * kWave + sidx];
-                r.r3 = buf[3 * kWave + sidx];
-                if (c0 + sidx >= jb) r.r0.w = 0.0f;  // past the list: weight 0
+                FwdRecord r;
+                r.f0 = buf[sidx];
+                r.f1 = buf[kWave + sidx];
+                r.f2 = buf[2 * kWave + sidx];
+                if (c0 + sidx >= jb) r.f0.w = 0.0f;  // past the list: weight 0
 #pragma unroll
                 for (uint32_t t = 0; t < kRowsMax; ++t) {
                     if (t < nt) {
                         const float a = eval_a(r, px[t], py[t], pz[t], T);
                         Ip[t] += a;
-                        Vp[t] = fmaf_(a, r.r1.w, Vp[t]);
+                        Vp[t] = fmaf_(a, r.f1.w, Vp[t]);
                     }
                 }
             }
@@ -433,7 +423,7 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
 template <uint32_t R>
 __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t qn, uint32_t ja,
                                            uint32_t jb, uint32_t c, uint32_t ncells, const QueryParams &q,
-                                           const GridParams &g, const Record *__restrict__ rec,
+                                           const GridParams &g, const FwdRecord *__restrict__ rec,
                                            const uint32_t *__restrict__ gids, const uint32_t *__restrict__ order,
                                            float T, float tau, float *__restrict__ out_v, float *__restrict__ out_i,
                                            const PlanResults &pr, float4 *buf) {
@@ -468,10 +458,9 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
 //  * n < 4: lanes are the cell's candidates (64 at a time) and the queries
 //    are visited in turn, their positions broadcast from SGPRs.
 // Every query's sums are reduced in a fixed order.
-// Seven waves per SIMD (at most 72 VGPRs; the compiler keeps a few values in
-// scratch): the row layouts' per-row arrays would otherwise take 83 VGPRs and
-// leave five.
-__global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
+// Seven waves per SIMD (at most 72 VGPRs, which the row layouts' per-row
+// arrays need; eight would spill them to scratch).
+__global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, GridParams g, const FwdRecord *__restrict__ rec,
                                                          const uint32_t *__restrict__ gids,
                                                          const uint32_t *__restrict__ cell_off,
                                                          const uint32_t *__restrict__ point_off,
@@ -480,9 +469,9 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
                                                          const uint32_t *__restrict__ items, int64_t max_items,
                                                          float T, float tau, float *__restrict__ out_v,
                                                          float *__restrict__ out_i, PlanResults pr) {
-    // per wave: the records of 64 candidates, as four 1 KiB planes of 16-byte
-    // quarters (quarter q of candidate s at [q][s])
-    __shared__ float4 s_rec[kSampWaves][4 * kWave];
+    // per wave: the records of 64 candidates, as three 1 KiB planes of
+    // 16-byte quarters (quarter q of candidate s at [q][s])
+    __shared__ float4 s_rec[kSampWaves][kFwdQuads * kWave];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t ncells = (uint32_t)g.ncells;
     const uint64_t w = (uint64_t)blockIdx.x * kSampWaves + threadIdx.x / kWave;
@@ -534,19 +523,18 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
         for (uint32_t t = 0; t < kChunkB; ++t) Ip[t] = Vp[t] = 0.0f;
         for (uint32_t j0 = ja; j0 < jb; j0 += kWave) {
             const uint32_t j = j0 + lane;
-            Record r;
+            FwdRecord r;
             if (j < jb) {
                 r = rec[gids[j]];
             } else {
-                r.r0 = r.r1 = r.r2 = r.r3 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-                r.r0.w = 0.0f;
+                r.f0 = r.f1 = r.f2 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             }
 #pragma unroll
             for (uint32_t t = 0; t < kChunkB; ++t) {
                 if (t < m) {
                     const float a = eval_a(r, readlane_f(mx, t), readlane_f(my, t), readlane_f(mz, t), T);
                     Ip[t] += a;
-                    Vp[t] = fmaf_(a, r.r1.w, Vp[t]);
+                    Vp[t] = fmaf_(a, r.f1.w, Vp[t]);
                 }
             }
         }
@@ -573,7 +561,7 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
 // and totals[1] (passing) with one integer atomic each per block (the sums
 // do not depend on their order).
 __global__ __launch_bounds__(kBlock) void k_count_sample_pairs(QueryParams q, GridParams g,
-                                                               const Record *__restrict__ rec,
+                                                               const FwdRecord *__restrict__ rec,
                                                                const uint32_t *__restrict__ gids,
                                                                const uint32_t *__restrict__ cell_off,
                                                                const uint32_t *__restrict__ plan_keys,
@@ -630,7 +618,7 @@ __global__ __launch_bounds__(kBlock) void k_count_sample_pairs(QueryParams q, Gr
 
 }  // namespace
 
-hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const Record *rec,
+hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const FwdRecord *rec,
                                      const uint32_t *gids, const uint32_t *cell_off, const uint32_t *plan_keys,
                                      const float4 *plan_pos, float T, unsigned long long *totals, hipStream_t s) {
     hipError_t e = fill_u32((uint32_t *)totals, 0u, 4, s);
@@ -650,7 +638,7 @@ hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t
     return hipGetLastError();
 }
 
-hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
+hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const uint32_t *gids,
                               const uint32_t *cell_off, float T, float tau, float *out_v, float *out_i,
                               hipStream_t s) {
     const int64_t vpc = (int64_t)(q.dims[0] / g.cells[0]) * (q.dims[1] / g.cells[1]) * (q.dims[2] / g.cells[2]);
@@ -665,7 +653,7 @@ hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const R
     return hipGetLastError();
 }
 
-hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const uint32_t *gids,
                                 const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
                                 const PlanResults &pr, hipStream_t s) {
