@@ -44,7 +44,7 @@ def lib():
                                   vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.orc_backward.restype = c_int
         L.orc_backward.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, vp, vp, vp, vp, vp,
-                                   c_i64, vp, c_int, c_int, vp, vp, vp, vp]
+                                   c_i64, vp, c_int, c_int, vp, vp, vp, vp, vp]
         L.orc_support.restype = c_int
         L.orc_support.argtypes = [c_i64, vp, vp, vp, vp, vp, vp, vp, c_float, c_i64, vp, c_i64, vp, c_int, vp]
         L.orc_voxel_centers.restype = c_int
@@ -149,8 +149,9 @@ def backward(g, points, phi, inf, g_phi, g_inf, lo=(0, 0, 0), hi=(1, 1, 1), tau:
     every parameter of the selected Gaussians (all when select is None).
     Returns (grad, abs_sum), each [nsel, 12] = dmu(3), ds(3), dq(4), dv, dw,
     and with pairs=True also each Gaussian's number of intersecting pairs
-    at the defined points [nsel] and the magnitudes of its whitened-frame
-    moment sums [nsel, 9] (see orc_backward)."""
+    at the defined points [nsel], the magnitudes of its triangular-frame
+    moment sums [nsel, 9] and the sums of the absolute exact per-pair terms
+    of dmu, ds, dq [nsel, 10] (see orc_backward)."""
     m, s, q, v, w = _gauss64(g)
     pts = _f64(points).reshape(-1, 3)
     n = pts.shape[0]
@@ -166,12 +167,13 @@ def backward(g, points, phi, inf, g_phi, g_inf, lo=(0, 0, 0), hi=(1, 1, 1), tau:
     ab = np.zeros((nsel, 12))
     K = np.zeros(nsel, dtype=np.int64)
     mab = np.zeros((nsel, 9))
+    tab = np.zeros((nsel, 10))
     rc = lib().orc_backward(m.shape[0], _p(m), _p(s), _p(q), _p(v), _p(w), _p(lo_), _p(hi_), tau, n, _p(pts),
                             _p(phi), _p(inf), _p(gp), _p(gi), _p(zm), nsel, _p(sel), int(prune),
-                            threads or default_threads(), _p(grad), _p(ab), _p(K), _p(mab))
+                            threads or default_threads(), _p(grad), _p(ab), _p(K), _p(mab), _p(tab))
     if rc != 0:
         raise RuntimeError(f"orc_backward failed ({rc})")
-    return (grad, ab, K, mab) if pairs else (grad, ab)
+    return (grad, ab, K, mab, tab) if pairs else (grad, ab)
 
 
 def support(g, points, select, lo=(0, 0, 0), hi=(1, 1, 1), tau: float = 0.01, threads: int = 0):

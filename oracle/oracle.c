@@ -82,6 +82,7 @@ typedef struct {
     double kappa;       /* s_max / s_min */
     double e_rel;       /* float32 relative error allowance of G */
     double band;        /* relative half-width of the ambiguity band in Q */
+    double C[3][3];     /* upper Cholesky factor of R S^-2 R^T: C^T C = M^T M, M = S^-1 R^T */
 } g64;
 
 /* float32 squared norm of the quaternion in the canonical order; a
@@ -162,6 +163,25 @@ static void prepare(int64_t i, const double *mean, const double *scale, const do
         double acc = 0.0;
         for (int k = 0; k < 3; k++) acc += g->R[j][k] * g->R[j][k] * g->s[k] * g->s[k];
         g->sig_diag[j] = acc;
+    }
+    /* Sigma^-1 = R S^-2 R^T and its upper triangular factor (Cholesky, row
+     * by row): |C d|^2 = |S^-1 R^T d|^2 = Q for every d */
+    double A[3][3];
+    for (int j = 0; j < 3; j++)
+        for (int l = 0; l < 3; l++) {
+            double acc = 0.0;
+            for (int k = 0; k < 3; k++) acc += g->R[j][k] * g->R[l][k] / (g->s[k] * g->s[k]);
+            A[j][l] = acc;
+        }
+    for (int r = 0; r < 3; r++) {
+        double dg = A[r][r];
+        for (int m = 0; m < r; m++) dg -= g->C[m][r] * g->C[m][r];
+        g->C[r][r] = sqrt(dg);
+        for (int c = r + 1; c < 3; c++) {
+            double off = A[r][c];
+            for (int m = 0; m < r; m++) off -= g->C[m][r] * g->C[m][c];
+            g->C[r][c] = off / g->C[r][r];
+        }
     }
     g->v = value[i];
     g->w = weight[i];
@@ -375,17 +395,21 @@ int orc_forward(int64_t n, const double *mean, const double *scale, const double
  * taken as zero). sel == NULL selects every Gaussian. npairs (optional)
  * receives each selected Gaussian's number of intersecting pairs at the
  * defined points taken into account, and mom_abs (optional, [nsel][9])
- * the sums over those pairs of |dL/dQ| U_k and |dL/dQ| U_m U_k (m <= k:
- * 00 01 02 11 12 22), with U_k = sum_j |R_jk d_j| / s_k the size of u_k's
- * parts and |dL/dQ| taken at the size of dL/da's parts: the magnitudes of
- * the sums an implementation in the whitened frame accumulates.
+ * the sums over those pairs of |dL/dQ| C_k and |dL/dQ| C_m C_k (m <= k:
+ * 00 01 02 11 12 22), with C_k = sum_j |C_kj d_j| the size of the parts of
+ * c_k = (C d)_k, C the upper Cholesky factor of Sigma^-1 (so |c|^2 = Q),
+ * and |dL/dQ| taken at the size of dL/da's parts: the magnitudes of the
+ * sums an implementation that whitens with the triangular factor
+ * accumulates. term_abs (optional, [nsel][10]) receives the sums over the
+ * pairs of the absolute values of the exact per-pair terms of dmu, ds, dq
+ * for that same |dL/dQ|: what a relative error of G scales.
  */
 int orc_backward(int64_t n, const double *mean, const double *scale, const double *rot,
                  const double *value, const double *weight, const float lo[3], const float hi[3],
                  float tau, int64_t npts, const double *pts, const double *phi, const double *inf,
                  const double *g_phi, const double *g_inf, const uint8_t *zero_mask,
                  int64_t nsel, const int64_t *sel, int prune, int nthreads,
-                 double *grad, double *abs_out, int64_t *npairs, double *mom_abs)
+                 double *grad, double *abs_out, int64_t *npairs, double *mom_abs, double *term_abs)
 {
     if (n < 0 || npts < 0 || !(tau > 0.0f) || !(tau < 1.0f)) return ORC_ERR_ARG;
     if (!sel) nsel = n;
@@ -395,8 +419,9 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
 #pragma omp parallel for schedule(dynamic, 4)
     for (int64_t t = 0; t < nsel; t++) {
         int64_t i = sel ? sel[t] : t;
-        double acc[12], aab[12], mab[9];
+        double acc[12], aab[12], mab[9], tab[10];
         int64_t K = 0;
+        memset(tab, 0, sizeof(tab));
         memset(acc, 0, sizeof(acc));
         memset(aab, 0, sizeof(aab));
         memset(mab, 0, sizeof(mab));
@@ -490,16 +515,22 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
                 for (int k = 0; k < 10; k++) {
                     acc[k] += term[k] * dLdQv;
                     aab[k] += mag[k] * dLdQm;
+                    tab[k] += fabs(term[k]) * dLdQm;
                 }
-                /* the sizes of the whitened-frame moments sum |dL/dQ| u and
-                 * sum |dL/dQ| u u^T at the size of u's parts */
-                for (int k = 0; k < 3; k++) mab[k] += dLdQm * U[k];
-                mab[3] += dLdQm * U[0] * U[0];
-                mab[4] += dLdQm * U[0] * U[1];
-                mab[5] += dLdQm * U[0] * U[2];
-                mab[6] += dLdQm * U[1] * U[1];
-                mab[7] += dLdQm * U[1] * U[2];
-                mab[8] += dLdQm * U[2] * U[2];
+                /* the sizes of the triangular-frame moments sum |dL/dQ| c
+                 * and sum |dL/dQ| c c^T, c = C d, at the size of c's parts */
+                double Cp[3];
+                for (int a_ = 0; a_ < 3; a_++) {
+                    Cp[a_] = 0.0;
+                    for (int b_ = a_; b_ < 3; b_++) Cp[a_] += fabs(g.C[a_][b_] * d[b_]);
+                }
+                for (int k = 0; k < 3; k++) mab[k] += dLdQm * Cp[k];
+                mab[3] += dLdQm * Cp[0] * Cp[0];
+                mab[4] += dLdQm * Cp[0] * Cp[1];
+                mab[5] += dLdQm * Cp[0] * Cp[2];
+                mab[6] += dLdQm * Cp[1] * Cp[1];
+                mab[7] += dLdQm * Cp[1] * Cp[2];
+                mab[8] += dLdQm * Cp[2] * Cp[2];
                 term[10] = gP * a / I;
                 acc[10] += term[10];
                 aab[10] += fabs(term[10]);
@@ -514,6 +545,8 @@ int orc_backward(int64_t n, const double *mean, const double *scale, const doubl
         if (npairs) npairs[t] = K;
         if (mom_abs)
             for (int k = 0; k < 9; k++) mom_abs[9 * t + k] = mab[k];
+        if (term_abs)
+            for (int k = 0; k < 10; k++) term_abs[10 * t + k] = tab[k];
     }
     return ORC_OK;
 }

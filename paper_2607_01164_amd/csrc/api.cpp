@@ -742,7 +742,7 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
     }
     IndexWork w = index_layout(index->work, n, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
-    GS_TRY(launch_backward(qp, gp, w.rec, w.box, w.spans, w.gorder, n, index->n_pairs, p.order, p.point_off, p.res.pos, p.res.out, value,
+    GS_TRY(launch_backward(qp, gp, w.frec, w.box, w.spans, w.gorder, n, index->n_pairs, p.order, p.point_off, p.res.pos, p.res.out, value,
                            influence, grad_value,
                            grad_influence, cutoff_T(index->tau), bw.b, gauss->mean, gauss->scale, gauss->rot, d_mean,
                            d_scale, d_rot, d_value, d_weight, stream),

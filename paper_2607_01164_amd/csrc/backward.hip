@@ -141,23 +141,24 @@ struct Acc {
     float dv, dw;
 };
 
-// Whitened offset u = M (p - mu) and Q = |u|^2, the exponent of paper Eq. 3.
-__device__ __forceinline__ float whiten(const Record &r, float px, float py, float pz, float &u0, float &u1,
+// Whitened offset u = U (p - mu) and Q = |u|^2, the exponent of paper Eq. 3
+// (U the Cholesky factor of the inverse covariance, as the forward uses).
+__device__ __forceinline__ float whiten(const FwdRecord &r, float px, float py, float pz, float &u0, float &u1,
                                         float &u2) {
-    const float dx = px - r.r0.x, dy = py - r.r0.y, dz = pz - r.r0.z;
-    u0 = fmaf_(r.r1.x, dx, fmaf_(r.r1.y, dy, r.r1.z * dz));
-    u1 = fmaf_(r.r2.x, dx, fmaf_(r.r2.y, dy, r.r2.z * dz));
-    u2 = fmaf_(r.r3.x, dx, fmaf_(r.r3.y, dy, r.r3.z * dz));
+    const float dx = px - r.f0.x, dy = py - r.f0.y, dz = pz - r.f0.z;
+    u0 = fmaf_(r.f1.x, dx, fmaf_(r.f1.y, dy, r.f1.z * dz));
+    u1 = fmaf_(r.f2.x, dy, r.f2.y * dz);
+    u2 = r.f2.z * dz;
     return fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
 }
 
 // Partials of one contributing pair (Q <= T), given u, Q and the query's
 // alpha, beta.
-__device__ __forceinline__ void pair_grad(const Record &r, float u0, float u1, float u2, float Q, float al, float be,
+__device__ __forceinline__ void pair_grad(const FwdRecord &r, float u0, float u1, float u2, float Q, float al, float be,
                                           Acc &acc) {
     const float G = exp2_hw(Q * kNegHalfLog2e);
-    const float a = r.r0.w * G;
-    const float dLda = fmaf_(al, r.r1.w, be);
+    const float a = r.f0.w * G;
+    const float dLda = fmaf_(al, r.f1.w, be);
     acc.dv = fmaf_(al, a, acc.dv);
     acc.dw = fmaf_(dLda, G, acc.dw);
     const float c = -0.5f * a * dLda;
@@ -209,7 +210,7 @@ __device__ __forceinline__ float reduce11(const float v[11], uint32_t lane) {
 // holds them instead of the point, was slower: 8 more bytes a test.)
 constexpr uint32_t kQueue = 2 * kWave;
 
-__device__ __forceinline__ void drain(const Record &r, const float4 *qu, const uint32_t *qk, uint32_t head,
+__device__ __forceinline__ void drain(const FwdRecord &r, const float4 *qu, const uint32_t *qk, uint32_t head,
                                       uint32_t cnt, uint32_t lane, const float2 *__restrict__ ab, Acc &acc) {
     if (lane < cnt) {
         const uint32_t slot = (head + lane) & (kQueue - 1);
@@ -242,7 +243,7 @@ constexpr int64_t kLargeBoxCells = 32;
 
 // Partials of the wave's current Gaussian are reduced over the wave and
 // stored: lane k < 12 writes moment k (the 12th is 0).
-__device__ __forceinline__ void finish_gauss(const Record &r, const float4 *qu, const uint32_t *qk, uint32_t head,
+__device__ __forceinline__ void finish_gauss(const FwdRecord &r, const float4 *qu, const uint32_t *qk, uint32_t head,
                                              uint32_t cnt, uint32_t lane, const float2 *__restrict__ ab, Acc &acc,
                                              uint32_t gid, float *__restrict__ moments) {
     if (cnt > 0) {
@@ -279,7 +280,7 @@ __device__ __forceinline__ void acc_zero(Acc &acc) {
 // the spatial order of the index (the cell key of their box corner), so the
 // waves resident at one time work on one region and find its points in L2.
 template <bool GRID, uint32_t PACK>
-__global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, GridParams g, const Record *__restrict__ rec,
+__global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, GridParams g, const FwdRecord *__restrict__ rec,
                                                            const CellBox *__restrict__ box,
                                                            const uint8_t *__restrict__ spans,
                                                            const uint32_t *__restrict__ gorder, int64_t n_gauss,
@@ -334,8 +335,8 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
     // than 1.5 2^-23 (row + 1/2) / nry, which cannot cross it while
     // row < 2^21
     const bool fdiv = wave_max_uniform(mR) < (1u << 21);
-    Record r;
-    r.r0 = r.r1 = r.r2 = r.r3 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    FwdRecord r;
+    r.f0 = r.f1 = r.f2 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     Acc acc;
     acc_zero(acc);
     uint32_t head = 0, cnt = 0;
@@ -412,7 +413,7 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
                 acc_zero(acc);
                 cur = gi;
                 cur_gid = __builtin_amdgcn_readlane(mgid, gi);
-                r = load_record_uniform(rec, cur_gid);
+                r = load_fwd_uniform(rec, cur_gid);
             }
             // its rows in this batch and their elements [Ea, Eb)
             const uint32_t la = gend - gR > rb ? gend - gR - rb : 0u;
@@ -519,7 +520,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
     if (i >= n) return;
     const float *m = moments + (size_t)i * 12;
     const float4 ma = *(const float4 *)m, mb = *(const float4 *)(m + 4), mc = *(const float4 *)(m + 8);
-    const double m1[3] = {ma.x, ma.y, ma.z};
+    const double m1p[3] = {ma.x, ma.y, ma.z};
     const double m2s[6] = {ma.w, mb.x, mb.y, mb.z, mb.w, mc.x};
     const bool any = ma.x != 0.0f || ma.y != 0.0f || ma.z != 0.0f || ma.w != 0.0f || mb.x != 0.0f ||
                      mb.y != 0.0f || mb.z != 0.0f || mb.w != 0.0f || mc.x != 0.0f || mc.y != 0.0f || mc.z != 0.0f;
@@ -542,13 +543,39 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
         R[2][0] = 2.0 * (x * z - w * y);
         R[2][1] = 2.0 * (y * z + w * x);
         R[2][2] = 1.0 - 2.0 * (x * x + y * y);
-        double M2[3][3];
-        M2[0][0] = m2s[0];
-        M2[0][1] = M2[1][0] = m2s[1];
-        M2[0][2] = M2[2][0] = m2s[2];
-        M2[1][1] = m2s[3];
-        M2[1][2] = M2[2][1] = m2s[4];
-        M2[2][2] = m2s[5];
+        // The moments come in the frame of u' = U d (U upper triangular,
+        // U^T U = M^T M with M = S^-1 R^T, the factor the samplers use).
+        // O = M U^-1 is orthogonal and u = M d = O u', so the moments in the
+        // frame of M are m1 = O m1' and m2 = O m2' O^T.
+        double Mm[3][3], A[3][3];
+        for (int k = 0; k < 3; ++k)
+            for (int j = 0; j < 3; ++j) Mm[k][j] = R[j][k] * is[k];
+        for (int j = 0; j < 3; ++j)
+            for (int l = 0; l < 3; ++l) A[j][l] = Mm[0][j] * Mm[0][l] + Mm[1][j] * Mm[1][l] + Mm[2][j] * Mm[2][l];
+        const double u00 = sqrt(A[0][0]);
+        const double u01 = A[0][1] / u00, u02 = A[0][2] / u00;
+        const double u11 = sqrt(A[1][1] - u01 * u01);
+        const double u12 = (A[1][2] - u01 * u02) / u11;
+        const double u22 = sqrt(A[2][2] - u02 * u02 - u12 * u12);
+        const double Ui[3][3] = {{1.0 / u00, -u01 / (u00 * u11), (u01 * u12 - u02 * u11) / (u00 * u11 * u22)},
+                                 {0.0, 1.0 / u11, -u12 / (u11 * u22)},
+                                 {0.0, 0.0, 1.0 / u22}};
+        double O[3][3];
+        for (int k = 0; k < 3; ++k)
+            for (int a = 0; a < 3; ++a) O[k][a] = Mm[k][0] * Ui[0][a] + Mm[k][1] * Ui[1][a] + Mm[k][2] * Ui[2][a];
+        double P2[3][3];
+        P2[0][0] = m2s[0];
+        P2[0][1] = P2[1][0] = m2s[1];
+        P2[0][2] = P2[2][0] = m2s[2];
+        P2[1][1] = m2s[3];
+        P2[1][2] = P2[2][1] = m2s[4];
+        P2[2][2] = m2s[5];
+        double m1[3], OP[3][3], M2[3][3];
+        for (int k = 0; k < 3; ++k) m1[k] = O[k][0] * m1p[0] + O[k][1] * m1p[1] + O[k][2] * m1p[2];
+        for (int k = 0; k < 3; ++k)
+            for (int b = 0; b < 3; ++b) OP[k][b] = O[k][0] * P2[0][b] + O[k][1] * P2[1][b] + O[k][2] * P2[2][b];
+        for (int k = 0; k < 3; ++k)
+            for (int l = 0; l < 3; ++l) M2[k][l] = OP[k][0] * O[l][0] + OP[k][1] * O[l][1] + OP[k][2] * O[l][2];
         for (int j = 0; j < 3; ++j) {
             double acc = 0.0;
             for (int k = 0; k < 3; ++k) acc += R[j][k] * m1[k] * is[k];
@@ -641,7 +668,7 @@ __global__ __launch_bounds__(kBlock) void k_count_backward_pairs(QueryParams q, 
 
 template <bool GRID>
 void launch_gauss(uint32_t pack, uint32_t wblocks, hipStream_t s, const QueryParams &q, const GridParams &g,
-                  const Record *rec, const CellBox *box, const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss,
+                  const FwdRecord *rec, const CellBox *box, const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss,
                   const uint32_t *point_off, const float4 *plan_pos, const float2 *ab, float T, float *moments) {
     if (pack == 1)
         hipLaunchKernelGGL((k_backward_gauss<GRID, 1>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, rec, box, spans,
@@ -666,7 +693,7 @@ hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g
     return hipGetLastError();
 }
 
-hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
+hipError_t launch_backward(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const CellBox *box,
                            const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, int64_t n_pairs,
                            const uint32_t *order, const uint32_t *point_off,
                            const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,

@@ -47,6 +47,19 @@ __device__ __forceinline__ float fwd_q(const FwdRecord &r, float px, float py, f
     return __builtin_fmaf(u0, u0, __builtin_fmaf(u1, u1, u2 * u2));
 }
 
+// A forward record loaded with a wave-uniform address (scalar loads).
+__device__ __forceinline__ FwdRecord load_fwd_uniform(const FwdRecord *rec, uint32_t g) {
+    typedef float f4u __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(4))) const f4u CF4;
+    CF4 *p = (CF4 *)rec + kFwdQuads * (size_t)g;
+    const f4u a = p[0], b = p[1], c = p[2];
+    FwdRecord r;
+    r.f0 = make_float4(a.x, a.y, a.z, a.w);
+    r.f1 = make_float4(b.x, b.y, b.z, b.w);
+    r.f2 = make_float4(c.x, c.y, c.z, c.w);
+    return r;
+}
+
 // Cell box of a Gaussian: (x0, y0, z0, trimmed) and (x1, y1, z1, 0),
 // inclusive; an empty box has x1 < x0. When trimmed is 1 the box lists, in
 // each of its (y, z) rows (row r = (y - y0) + ny (z - z0)), only the cells
@@ -415,7 +428,7 @@ hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g
                                       const uint8_t *spans, int64_t n_gauss, const uint32_t *point_off,
                                       unsigned long long *total, hipStream_t s);
 // n_pairs: the index's pair count (it sets how many Gaussians share a wave)
-hipError_t launch_backward(const QueryParams &q, const GridParams &g, const Record *rec, const CellBox *box,
+hipError_t launch_backward(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const CellBox *box,
                            const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, int64_t n_pairs,
                            const uint32_t *order, const uint32_t *point_off,
                            const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,

@@ -271,30 +271,63 @@ def quat_moment_map(scale, rot):
     return out
 
 
-def grad_tolerance(ref, ab, kap, npairs, mom_abs=None, scale=None, rot=None, rtol=1e-4):
+def moment_map(scale, rot):
+    """[10, 9]: the linear map from a Gaussian's triangular-frame moments
+    m1 = sum dL/dQ c and m2 = sum dL/dQ c c^T (entries 00 01 02 11 12 22,
+    off-diagonal ones standing for both places), c = C d with C the upper
+    Cholesky factor of Sigma^-1 = R S^-2 R^T, to (dL/dmu, dL/ds, dL/dq).
+    u = S^-1 R^T d = O c with O = S^-1 R^T C^-1 orthogonal, so the
+    whitened-frame moments are O m1 and O m2 O^T; then dL/dmu = -2 R S^-1
+    (O m1) = -2 C^T m1, dL/ds_k = -2 (O m2 O^T)_kk / s_k, and dL/dq through
+    quat_moment_map."""
+    q = np.asarray(rot, np.float64)
+    s = np.asarray(scale, np.float64)
+    R = rot_of(q / np.linalg.norm(q))
+    M = np.diag(1.0 / s) @ R.T
+    C = np.linalg.cholesky(M.T @ M).T
+    O = M @ np.linalg.inv(C)
+    L = quat_moment_map(scale, rot)
+    out = np.zeros((10, 9))
+    out[0:3, 0:3] = -2.0 * C.T
+    for c, (m, k) in enumerate(M2_INDEX):
+        E = np.zeros((3, 3))
+        E[m, k] = E[k, m] = 1.0
+        W = O @ E @ O.T
+        out[3:6, 3 + c] = -2.0 * np.diag(W) / s
+        out[6:10, 3 + c] = L @ np.array([W[a, b] for a, b in M2_INDEX])
+    return out
+
+
+def grad_tolerance(ref, ab, kap, npairs, mom_abs=None, term_abs=None, scale=None, rot=None, rtol=1e-4):
     """Bar of a float32 gradient against the oracle's float64 one, per
     element: rtol |ref| plus the float32 error of the sum over the
-    Gaussian's K pairs, measured against the sizes of what is summed. Each
-    term carries the relative error e of G = exp(-Q/2) (e = eps (9 T kappa +
-    8), from the whitening's 18 eps T kappa in Q) and a few roundings of its
-    products: 2 e + 8 eps. The device adds each lane's share of the pairs in
-    turn (at most ceil(K / 64) + 1 additions a lane) and then reduces 64
-    lanes in 6 steps, so the accumulated sums err by at most
-    (ceil(K / 64) + 16) eps of their sizes, to first order. The sizes are the
-    oracle's sums of absolute per-pair terms A; for the quaternion, which
-    the device forms from the whitened-frame moments m2, the sizes of those
-    moments (mom_abs) through the absolute values of the linear map from m2
-    to dL/dq (quat_moment_map), when they are given."""
+    Gaussian's K pairs, measured against the sizes of what is summed. The
+    relative error e of G = exp(-Q/2) (e = eps (9 T kappa + 8), from the
+    whitening's 18 eps T kappa in Q) scales a pair's whole term, so it
+    costs 2 e of the sum of the absolute per-pair terms (term_abs when
+    given, else the sizes A below). The rest is rounding of the sums: the device
+    adds each lane's share of the pairs in turn (at most ceil(K / 64) + 1
+    additions a lane), then reduces 64 lanes in 6 steps, and each term
+    takes a few roundings of its products and of the whitened offset
+    (8 eps), so the sums err by at most (ceil(K / 64) + 24) eps of the
+    sizes of what they add. For dv and dw those sizes are A (the oracle's
+    sums of the per-pair terms at the size of their parts); dL/dmu,
+    dL/ds and dL/dq the device forms from moments summed in the frame of
+    the triangular factor, so for them the sizes of those moments
+    (mom_abs) through the absolute values of the linear map from them
+    (moment_map), or A where that is larger."""
     e = EPS32 * (9.0 * T64 * kap + 8.0)
     depth = np.ceil(np.asarray(npairs, dtype=np.float64) / 64.0) + 16.0
-    f = (2.0 * e + (depth + 8.0) * EPS32)[:, None]
-    tol = rtol * np.abs(ref) + f * ab
+    r = ((depth + 8.0) * EPS32)[:, None]
+    tol = rtol * np.abs(ref) + (2.0 * e[:, None] + r) * ab
     if mom_abs is not None:
         for i in range(len(ref)):
-            if not mom_abs[i, 3:9].any():
+            if not mom_abs[i].any():
                 continue  # no pair (or an invalid Gaussian): the bar above, with A = 0
-            L = np.abs(quat_moment_map(scale[i], rot[i]))
-            tol[i, 6:10] = rtol * np.abs(ref[i, 6:10]) + f[i, 0] * (L @ mom_abs[i, 3:9])
+            J = np.abs(moment_map(scale[i], rot[i]))
+            scaled = ab[i, :10] if term_abs is None else term_abs[i]
+            tol[i, :10] = (rtol * np.abs(ref[i, :10]) + 2.0 * e[i] * scaled +
+                           r[i, 0] * np.maximum(ab[i, :10], J @ mom_abs[i]))
     # the float64 reference's own rounding of its cancelling sums (for a
     # spherical Gaussian dL/dq is exactly zero, the oracle's sum of its
     # per-pair terms a few 1e-18)
@@ -314,10 +347,10 @@ def check_backward(run: Run, grads_gpu: np.ndarray, sel, sup, gv_sup, gi_sup, la
     pts_sup = run.positions(sup)
     phi_sup = run.phi_np[sup].astype(np.float64)
     inf_sup = run.inf_np[sup].astype(np.float64)
-    ref, ab, K, mab = oracle.backward(run.g, pts_sup, phi_sup, inf_sup, gv_sup, gi_sup, run.lo, run.hi, run.tau,
-                                      select=sel, pairs=True)
+    ref, ab, K, mab, tab = oracle.backward(run.g, pts_sup, phi_sup, inf_sup, gv_sup, gi_sup, run.lo, run.hi,
+                                           run.tau, select=sel, pairs=True)
     got = grads_gpu[sel]
-    tol = grad_tolerance(ref, ab, kappa(run.g)[sel], K, mab, run.g.scale[sel], run.g.rot[sel])
+    tol = grad_tolerance(ref, ab, kappa(run.g)[sel], K, mab, tab, run.g.scale[sel], run.g.rot[sel])
     err = np.abs(got - ref)
     ok = err <= tol
     worst = float(np.max(err / np.maximum(tol, 1e-300)))

@@ -180,8 +180,8 @@ def grad_case(seed=5):
     amb = oracle.ambiguous_points(ref, TAU)
     gp[amb] = 0
     gi[amb] = 0
-    grad, ab, K, mab = oracle.backward(g, pts, ref.phi, ref.inf, gp, gi, pairs=True)
-    return g, pts, gp, gi, ref, grad, ab, grad_tolerance(grad, ab, kappa(g), K, mab, g.scale, g.rot)
+    grad, ab, K, mab, tab = oracle.backward(g, pts, ref.phi, ref.inf, gp, gi, pairs=True)
+    return g, pts, gp, gi, ref, grad, ab, grad_tolerance(grad, ab, kappa(g), K, mab, tab, g.scale, g.rot)
 
 
 def octant_case(log_sd=0.6):
@@ -205,8 +205,8 @@ def octant_case(log_sd=0.6):
     gp, gi = np.full(len(pts), 0.1), np.ones(len(pts))
     ref = oracle.forward(g, pts)
     assert np.all(ref.ncontrib == 1) and not oracle.ambiguous_points(ref, TAU).any()
-    grad, ab, K, mab = oracle.backward(g, pts, ref.phi, ref.inf, gp, gi, pairs=True)
-    return g, grad, grad_tolerance(grad, ab, kappa(g), K, mab, g.scale, g.rot)
+    grad, ab, K, mab, tab = oracle.backward(g, pts, ref.phi, ref.inf, gp, gi, pairs=True)
+    return g, grad, grad_tolerance(grad, ab, kappa(g), K, mab, tab, g.scale, g.rot)
 
 
 def test_gradient_bar_accepts_float32_rounding():
@@ -269,3 +269,35 @@ def test_quaternion_moment_map_against_the_oracle():
     m2 = np.array([(c * u[use, m] * u[use, k]).sum() for m, k in M2_INDEX])
     np.testing.assert_allclose(quat_moment_map(g.scale[i], g.rot[i]) @ m2, grad[i, 6:10], rtol=1e-9,
                                atol=1e-12 * np.abs(grad[i, 6:10]).max())
+
+
+def test_triangular_moment_map_against_the_oracle():
+    """The map from triangular-frame moments (c = C d, C the upper Cholesky
+    factor of Sigma^-1) to (dL/dmu, dL/ds, dL/dq) that the gradient bar uses
+    reproduces the oracle's per-pair gradients of columns 0..9 for several
+    Gaussians."""
+    from harness import moment_map, rot_of
+    g, pts, gp, gi, ref, grad, ab, tol = grad_case()
+    T = 2 * np.log(1 / np.float64(np.float32(TAU)))
+    checked = 0
+    for i in range(g.n):
+        q = g.rot[i].astype(np.float64)
+        R = rot_of(q / np.linalg.norm(q))
+        s = g.scale[i].astype(np.float64)
+        M = np.diag(1.0 / s) @ R.T
+        C = np.linalg.cholesky(M.T @ M).T
+        d = pts - g.mean[i].astype(np.float64)
+        c = d @ C.T
+        Q = (c * c).sum(axis=1)
+        use = (Q <= T) & ref.defined.astype(bool)
+        if use.sum() < 5:
+            continue
+        a = float(g.weight[i]) * np.exp(-0.5 * Q[use])
+        dLda = gp[use] * (float(g.value[i]) - ref.phi[use]) / ref.inf[use] + gi[use]
+        w = -0.5 * a * dLda
+        m = np.concatenate([(w[:, None] * c[use]).sum(axis=0),
+                            [(w * c[use, j] * c[use, k]).sum() for j, k in ((0, 0), (0, 1), (0, 2), (1, 1), (1, 2), (2, 2))]])
+        np.testing.assert_allclose(moment_map(g.scale[i], g.rot[i]) @ m, grad[i, :10], rtol=1e-9,
+                                   atol=1e-12 * np.abs(grad[i, :10]).max())
+        checked += 1
+    assert checked >= 10
