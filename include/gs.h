@@ -201,7 +201,11 @@ gs_status gs_sample_gaussian_major(const gs_gaussians *gauss, const gs_index *in
                                    float *out_value, float *out_influence, void *plan, size_t plan_bytes,
                                    void *work, size_t work_bytes, hipStream_t stream);
 
-/* Bytes of backward workspace for an index (built) and a query. */
+/*
+ * Bytes of backward workspace for an index (built) and a query: 48 per
+ * Gaussian and 8 per query (16 for VOXELS, POINTS and JITTER queries), in
+ * 256-byte aligned parts; (size_t)-1 for invalid arguments.
+ */
 size_t gs_backward_work_bytes(const gs_index *index, const gs_query *query);
 
 /*
@@ -217,6 +221,10 @@ size_t gs_backward_work_bytes(const gs_index *index, const gs_query *query);
  * value and influence must be that call's outputs (they are read as given
  * for GRID queries). Every per-Gaussian sum is formed by one wavefront in a
  * fixed order, without atomics: the same inputs give bit-identical results.
+ * Each Gaussian's queries are walked in rows along x (rows of voxels for
+ * GRID queries, rows of index cells in the plan's order otherwise), each
+ * cut to the x-range of the cutoff ellipsoid, enlarged by 2^-7 in Q, over
+ * the row's (y, z) extent: to whole voxels, or to quarters of cells.
  */
 gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
                              const void *plan, size_t plan_bytes, const float *value, const float *influence,
@@ -250,10 +258,10 @@ gs_status gs_sample_backward_noalloc(const gs_gaussians *gauss, const gs_index *
  * For measurement: the number of (Gaussian, query) pairs gs_sample_backward
  * tests against the cutoff for this built index, query and plan (the plan
  * a gs_sample call filled; none for GRID queries): per Gaussian, the
- * queries of its box rows, cut to the row spans of a trimmed box and, for
- * ordered queries, to the quarters of the end cells along x that the row's
- * bound reaches. Uses work (gs_backward_work_bytes() bytes, its contents
- * are overwritten) and waits on the stream for the count.
+ * queries of its rows (see gs_sample_backward), each cut to the row's
+ * x-range: whole voxels for GRID queries, quarters of cells along x
+ * otherwise. Uses work (gs_backward_work_bytes() bytes, its contents are
+ * overwritten) and waits on the stream for the count.
  */
 gs_status gs_backward_pair_count(const gs_index *index, const gs_query *query, const void *plan,
                                  size_t plan_bytes, void *work, size_t work_bytes, int64_t *count,

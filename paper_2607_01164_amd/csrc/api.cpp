@@ -130,9 +130,8 @@ int gauss_order_bits(const gs_grid *g) { return gauss_order_full_bits(g) - gauss
 
 // Index workspace layout.
 struct IndexWork {
-    Record *rec;
-    CellBox *box;
-    FwdRecord *frec;
+    CellBox *box;        // [n] cell boxes (first: the tests read them back)
+    Record *rec;         // [n] evaluation records
     uint8_t *spans;      // [n][kSpanStride] row spans and quarter codes of trimmed boxes
     uint32_t *gorder;    // [n] Gaussians in spatial order
     uint32_t *gkeys;     // [n] their sort keys
@@ -158,10 +157,9 @@ int64_t tile_first_len(int64_t capacity) { return ((capacity > 0 ? capacity : 1)
 IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity) {
     Carver c(base);
     IndexWork w;
-    w.rec = c.take<Record>((size_t)(n > 0 ? n : 1));
-    w.box = c.take<CellBox>((size_t)(n > 0 ? n : 1));
     const size_t n1 = (size_t)(n > 0 ? n : 1);
-    w.frec = c.take<FwdRecord>(n1);
+    w.box = c.take<CellBox>(n1);
+    w.rec = c.take<Record>(n1);
     w.spans = c.take<uint8_t>(n1 * kSpanStride);
     w.gorder = c.take<uint32_t>(n1);
     w.gkeys = c.take<uint32_t>(n1);
@@ -306,6 +304,25 @@ float index_radius(float tau) {
     return (float)(rc * (1.0 + 1.0 / 1024.0));
 }
 
+// The backward's row geometry for a grid and query (see BwdGeom).
+BwdGeom bwd_geom(const GridParams &gp, const QueryParams &qp, float T) {
+    BwdGeom b;
+    b.T2 = (float)((double)T * (1.0 + 1.0 / 128.0));
+    for (int j = 0; j < 2; ++j) {
+        b.cw[j] = (float)(1.0 / (double)gp.invc[j + 1]);
+        b.slack[j] = (float)(std::ldexp(1.0, -18) * (std::fabs((double)gp.lo[j + 1]) + std::fabs((double)gp.hi[j + 1])));
+    }
+    const double ext0 = (double)gp.hi[0] - (double)gp.lo[0];
+    b.ivsz0 = qp.kind == GS_QUERY_GRID ? (float)(1.0 / (double)qp.vsz[0]) : 0.0f;
+    b.xslack = qp.kind == GS_QUERY_GRID
+                   ? (float)(std::ldexp(1.0, -20) * (double)qp.dims[0] *
+                                 (1.0 + (std::fabs((double)gp.lo[0]) + std::fabs((double)gp.hi[0])) / ext0) +
+                             std::ldexp(1.0, -12))
+                   : 0.0f;
+    b.K = (uint32_t)(kSub * gp.cells[0]);
+    return b;
+}
+
 // Backward workspace layout.
 struct BwdWork {
     BackwardBuffers b;
@@ -319,9 +336,8 @@ BwdWork bwd_layout(void *base, const gs_index *index, const gs_query *q) {
     const int64_t nq = query_count(q);
     const size_t mq = (size_t)(nq > 0 ? nq : 1);
     w.b.moments = c.take<float>((size_t)(n > 0 ? n : 1) * 12);
-    (void)q;
     w.b.ab = c.take<float2>(mq);
-    w.b.cot = c.take<float2>(mq);
+    w.b.cot = q->kind != GS_QUERY_GRID ? c.take<float2>(mq) : nullptr;
     w.bytes = c.off;
     return w;
 }
@@ -549,7 +565,7 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     IndexWork w = index_layout(index->work, n, grid, index->capacity);
 
     GS_TRY(launch_preprocess(gauss->mean, gauss->scale, gauss->rot, gauss->value, gauss->weight, n, gp,
-                             index_radius(tau), w.rec, w.frec, w.box, w.spans, w.pair_off, w.pair_sum, stream),
+                             index_radius(tau), w.rec, w.box, w.spans, w.pair_off, w.pair_sum, stream),
            "gs_build_index: preprocess");
     {
         // groups past ceil(n / 64) hold only count[n] = 0: their prefix is the total
@@ -661,14 +677,14 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
     IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
     const float T = cutoff_T(index->tau);
     if (query->kind == GS_QUERY_GRID) {
-        GS_TRY(launch_sample_grid(qp, gp, w.frec, index->gids, index->cell_offsets, T, index->tau, out_value,
+        GS_TRY(launch_sample_grid(qp, gp, w.rec, index->gids, index->cell_offsets, T, index->tau, out_value,
                                   out_influence, stream),
                "gs_sample: grid sampler");
         return GS_OK;
     }
     Plan p;
     if ((st = order_queries("gs_sample", qp, gp, nq, plan, plan_bytes, &p, stream)) != GS_OK) return st;
-    GS_TRY(launch_sample_points(qp, gp, w.frec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
+    GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
                                 index->tau, out_value, out_influence, p.res, stream),
            "gs_sample: point sampler");
     return GS_OK;
@@ -742,10 +758,10 @@ gs_status gs_sample_backward(const gs_gaussians *gauss, const gs_index *index, c
     }
     IndexWork w = index_layout(index->work, n, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
-    GS_TRY(launch_backward(qp, gp, w.frec, w.box, w.spans, w.gorder, n, index->n_pairs, p.order, p.point_off, p.res.pos, p.res.out, value,
-                           influence, grad_value,
-                           grad_influence, cutoff_T(index->tau), bw.b, gauss->mean, gauss->scale, gauss->rot, d_mean,
-                           d_scale, d_rot, d_value, d_weight, stream),
+    const float T = cutoff_T(index->tau);
+    GS_TRY(launch_backward(qp, gp, bwd_geom(gp, qp, T), w.rec, w.box, w.gorder, n, index->n_pairs, p.order,
+                           p.point_off, p.res.pos, p.res.out, value, influence, grad_value, grad_influence, T, bw.b,
+                           gauss->scale, gauss->rot, d_mean, d_scale, d_rot, d_value, d_weight, stream),
            "gs_sample_backward");
     return GS_OK;
 }
@@ -920,7 +936,8 @@ gs_status gs_backward_pair_count(const gs_index *index, const gs_query *query, c
     IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
     unsigned long long *total = (unsigned long long *)bw.b.moments;
-    GS_TRY(launch_count_backward_pairs(qp, gp, w.box, w.spans, index->n_gauss, p.point_off, total, stream),
+    GS_TRY(launch_count_backward_pairs(qp, gp, bwd_geom(gp, qp, cutoff_T(index->tau)), w.rec, w.box,
+                                       index->n_gauss, p.point_off, total, stream),
            "gs_backward_pair_count");
     GS_TRY(hipMemcpyAsync(pc->value, total, sizeof(uint64_t), hipMemcpyDeviceToHost, stream),
            "gs_backward_pair_count: read-back");
@@ -960,7 +977,7 @@ gs_status gs_sample_pair_counts(const gs_index *index, const gs_query *query, co
     IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
     BwdWork bw = bwd_layout(work, index, query);
     unsigned long long *totals = (unsigned long long *)bw.b.moments;
-    GS_TRY(launch_count_sample_pairs(qp, gp, w.frec, index->gids, index->cell_offsets, p.keys, p.res.pos,
+    GS_TRY(launch_count_sample_pairs(qp, gp, w.rec, index->gids, index->cell_offsets, p.keys, p.res.pos,
                                      cutoff_T(index->tau), totals, stream),
            "gs_sample_pair_counts");
     for (int k = 0; k < 2; ++k) {

@@ -8,22 +8,28 @@
 // Gaussian's box, accumulates the partial sums in registers and reduces
 // them across the wave with DPP at the end.
 //
-// The points of a box come as rows: a run of cells along x at fixed (y, z)
-// is contiguous in the plan's cell ordering (for grids, a run of voxels is
-// contiguous in the x-fastest layout). The wave concatenates up to 64 rows
-// and walks them 64 elements per step, so the lanes stay busy across row
-// ends and every load reads whole cache lines. Most tested pairs fail the
-// cutoff; the ones that pass are queued in LDS and processed 64 at a time,
-// so the longer per-pair work runs with every lane busy. Gaussians are
-// visited in the spatial order of the index (the cell key of their box
-// corner), so the waves resident at one time work on one region and find
-// its points in L2.
+// The queries of a Gaussian come as rows along x: for grids a row of
+// voxels at fixed (y, z), contiguous in the x-fastest layout; for ordered
+// queries a row of cells at fixed (y, z), contiguous in the plan's order
+// (by cell, then by quarter of the cell along x). Each row is cut to the
+// x-range of the cutoff ellipsoid over the row's (y, z) extent, computed
+// from the Gaussian's record when the row is set up: whole voxels for
+// grids, quarters of cells for ordered queries. The wave concatenates up to
+// 64 rows and walks them 64 elements per step, so the lanes stay busy
+// across row ends and every load reads whole cache lines. Most tested
+// pairs fail the cutoff; the ones that pass are queued in LDS and
+// processed 64 at a time, so the longer per-pair work runs with every lane
+// busy. Gaussians are visited in the spatial order of the index (the cell
+// key of their box corner), so the waves resident at one time work on one
+// region and find its points in L2.
 //
-// Per pair the partials are kept as 11 moments in the Gaussian's whitened
-// frame u = M (p - mu), M = S^-1 R^T, with c = dL/dQ = -1/2 a dL/da:
+// Per pair the partials are kept as 11 moments in the frame of the
+// record's triangular factor, u = U (p - mu) with U^T U = R S^-2 R^T, and
+// c = dL/dQ = -1/2 a dL/da:
 //   m1 = sum c u (3), m2 = sum c u u^T (6), dv = sum dL/dPhi a / I,
 //   dw = sum dL/da G.
-// A finalize kernel turns them into dL/dmu = -2 M^T m1,
+// A finalize kernel rotates them into the frame of M = S^-1 R^T (O = M U^-1
+// is orthogonal) and turns them into dL/dmu = -2 M^T m1,
 // dL/ds_k = -2 m2_kk / s_k, dL/dR_jk = (2 / s_k) sum_m R_jm s_m m2_mk, and
 // through R(qhat) and qhat = q / |q| into dL/dq.
 // For a defined query with outputs (Phi, I) and cotangents (gPhi, gI):
@@ -50,12 +56,10 @@ __device__ __forceinline__ void alpha_beta(float phi, float inf, float gp, float
     }
 }
 
-// Cotangent staging for ordered queries: (alpha, beta) of the k-th
-// query in plan order, from the forward's (Phi, I) that the plan keeps in
-// that order. The cotangents are first packed in query order as pairs
-// (coalesced), so staging gathers one 8-byte pair per query by id instead
-// of two 4-byte values from two arrays.
-constexpr int kStageItems = 4;  // queries per thread of the point staging
+// Cotangents of ordered queries are first packed in query order as pairs
+// (coalesced), so that staging gathers one 8-byte pair per query by id
+// instead of two 4-byte values from two arrays.
+constexpr int kStageItems = 4;  // queries per thread of the packing
 
 __global__ __launch_bounds__(kBlock) void k_pack_cotangents(int64_t n, const float *__restrict__ gval,
                                                             const float *__restrict__ ginf, bool vec,
@@ -72,56 +76,19 @@ __global__ __launch_bounds__(kBlock) void k_pack_cotangents(int64_t n, const flo
     }
 }
 
-// Thread t stages queries 4t .. 4t+3 with 16-byte loads of their ids and
-// outputs, so the four cotangent gathers of a thread are in flight together.
-__global__ __launch_bounds__(kBlock) void k_stage_points(int64_t n, const uint32_t *__restrict__ order,
-                                                         const float2 *__restrict__ plan_out,
-                                                         const float2 *__restrict__ cot, float2 *__restrict__ ab) {
-    const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kStageItems;
-    if (k0 >= n) return;
-    uint32_t pid[kStageItems];
-    float2 o[kStageItems];
-    if (k0 + kStageItems <= n) {
-        const uint4 p4 = *(const uint4 *)(order + k0);
-        const float4 o01 = *(const float4 *)(plan_out + k0), o23 = *(const float4 *)(plan_out + k0 + 2);
-        pid[0] = p4.x;
-        pid[1] = p4.y;
-        pid[2] = p4.z;
-        pid[3] = p4.w;
-        o[0] = make_float2(o01.x, o01.y);
-        o[1] = make_float2(o01.z, o01.w);
-        o[2] = make_float2(o23.x, o23.y);
-        o[3] = make_float2(o23.z, o23.w);
-    } else {
-#pragma unroll
-        for (int i = 0; i < kStageItems; ++i) {
-            const bool ok = k0 + i < n;
-            pid[i] = ok ? order[k0 + i] : 0u;
-            o[i] = ok ? plan_out[k0 + i] : make_float2(0.0f, 0.0f);
-        }
-    }
-    float2 c[kStageItems];
-#pragma unroll
-    for (int i = 0; i < kStageItems; ++i) {
-        // undefined queries (I = 0) have no gradient: their cotangents are not read
-        const bool need = o[i].y > 0.0f;
-        c[i] = need ? cot[pid[i]] : make_float2(0.0f, 0.0f);
-    }
-    float2 r[kStageItems];
-#pragma unroll
-    for (int i = 0; i < kStageItems; ++i) {
-        float al, be;
-        alpha_beta(o[i].x, o[i].y, c[i].x, c[i].y, al, be);
-        r[i] = make_float2(al, be);
-    }
-    if (k0 + kStageItems <= n) {
-        *(float4 *)(ab + k0) = make_float4(r[0].x, r[0].y, r[1].x, r[1].y);
-        *(float4 *)(ab + k0 + 2) = make_float4(r[2].x, r[2].y, r[3].x, r[3].y);
-    } else {
-#pragma unroll
-        for (int i = 0; i < kStageItems; ++i)
-            if (k0 + i < n) ab[k0 + i] = r[i];
-    }
+// (alpha, beta) of the query at plan index k, from the forward outputs the
+// plan keeps and the packed cotangents.
+__global__ __launch_bounds__(kBlock) void k_stage_plan(int64_t n, const uint32_t *__restrict__ order,
+                                                       const float2 *__restrict__ plan_out,
+                                                       const float2 *__restrict__ cot, float2 *__restrict__ ab) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n) return;
+    const float2 o = plan_out[k];
+    // undefined queries (I = 0) have no gradient: their cotangents are not read
+    const float2 c = o.y > 0.0f ? cot[order[k]] : make_float2(0.0f, 0.0f);
+    float al, be;
+    alpha_beta(o.x, o.y, c.x, c.y, al, be);
+    ab[k] = make_float2(al, be);
 }
 
 __global__ __launch_bounds__(kBlock) void k_stage_grid(int64_t n, const float *__restrict__ value,
@@ -143,7 +110,7 @@ struct Acc {
 
 // Whitened offset u = U (p - mu) and Q = |u|^2, the exponent of paper Eq. 3
 // (U the Cholesky factor of the inverse covariance, as the forward uses).
-__device__ __forceinline__ float whiten(const FwdRecord &r, float px, float py, float pz, float &u0, float &u1,
+__device__ __forceinline__ float whiten(const Record &r, float px, float py, float pz, float &u0, float &u1,
                                         float &u2) {
     const float dx = px - r.f0.x, dy = py - r.f0.y, dz = pz - r.f0.z;
     u0 = fmaf_(r.f1.x, dx, fmaf_(r.f1.y, dy, r.f1.z * dz));
@@ -154,7 +121,7 @@ __device__ __forceinline__ float whiten(const FwdRecord &r, float px, float py, 
 
 // Partials of one contributing pair (Q <= T), given u, Q and the query's
 // alpha, beta.
-__device__ __forceinline__ void pair_grad(const FwdRecord &r, float u0, float u1, float u2, float Q, float al, float be,
+__device__ __forceinline__ void pair_grad(const Record &r, float u0, float u1, float u2, float Q, float al, float be,
                                           Acc &acc) {
     const float G = exp2_hw(Q * kNegHalfLog2e);
     const float a = r.f0.w * G;
@@ -210,7 +177,7 @@ __device__ __forceinline__ float reduce11(const float v[11], uint32_t lane) {
 // holds them instead of the point, was slower: 8 more bytes a test.)
 constexpr uint32_t kQueue = 2 * kWave;
 
-__device__ __forceinline__ void drain(const FwdRecord &r, const float4 *qu, const uint32_t *qk, uint32_t head,
+__device__ __forceinline__ void drain(const Record &r, const float4 *qu, const uint32_t *qk, uint32_t head,
                                       uint32_t cnt, uint32_t lane, const float2 *__restrict__ ab, Acc &acc) {
     if (lane < cnt) {
         const uint32_t slot = (head + lane) & (kQueue - 1);
@@ -243,7 +210,7 @@ constexpr int64_t kLargeBoxCells = 32;
 
 // Partials of the wave's current Gaussian are reduced over the wave and
 // stored: lane k < 12 writes moment k (the 12th is 0).
-__device__ __forceinline__ void finish_gauss(const FwdRecord &r, const float4 *qu, const uint32_t *qk, uint32_t head,
+__device__ __forceinline__ void finish_gauss(const Record &r, const float4 *qu, const uint32_t *qk, uint32_t head,
                                              uint32_t cnt, uint32_t lane, const float2 *__restrict__ ab, Acc &acc,
                                              uint32_t gid, float *__restrict__ moments) {
     if (cnt > 0) {
@@ -264,25 +231,132 @@ __device__ __forceinline__ void acc_zero(Acc &acc) {
     acc.dv = acc.dw = 0.0f;
 }
 
-// PACK consecutive Gaussians of gorder per wavefront. The points of a box
-// come as rows: a run of cells along x at fixed (y, z) is contiguous in the
-// plan's cell ordering (for grids, a run of voxels is contiguous in the
-// x-fastest layout). The rows of the wave's Gaussians are listed one
-// Gaussian after the other and taken 64 at a time, lane l describing row
-// l of the batch, so the loads that find the rows (spans, cell offsets)
-// are issued once for several Gaussians. Within a batch the rows are
-// concatenated; each Gaussian walks its own part 64 elements per step,
-// lane l taking element e0 + l, so the lanes stay busy across row ends and
-// every load reads whole cache lines; a lane finds its row from the row
-// starts with two ballots. The cutoff test is all a non-contributing pair
-// costs; contributing pairs go to a per-wave LDS queue, and every 64
-// queued pairs are processed with all lanes busy. Gaussians are visited in
-// the spatial order of the index (the cell key of their box corner), so the
-// waves resident at one time work on one region and find its points in L2.
+__device__ __forceinline__ float bperm_f(uint32_t src, float v) {
+    return __int_as_float(__builtin_amdgcn_ds_bpermute((int)src, __float_as_int(v)));
+}
+
+// Least value over the rectangle dy in [ay, by], dz in [az, bz] (offsets
+// from the mean) of q2 = (U11 dy + U12 dz)^2 + (U22 dz)^2, the minimum of Q
+// over x at fixed (y, z) for the record's triangular U. q2 is convex: its
+// minimum is at dy = dz = 0 when the rectangle holds it, else on an edge,
+// where it is a quadratic in one variable minimised at its clamped vertex.
+__device__ __forceinline__ float slab_q2min(float U11, float U12, float U22, float ay, float by, float az,
+                                            float bz) {
+    if (ay <= 0.0f && by >= 0.0f && az <= 0.0f && bz >= 0.0f) return 0.0f;
+    const float i11 = __builtin_amdgcn_rcpf(U11);
+    const float iden = __builtin_amdgcn_rcpf(fmaf_(U12, U12, U22 * U22));
+    auto q2 = [&](float dy, float dz) {
+        const float a = fmaf_(U11, dy, U12 * dz), b = U22 * dz;
+        return fmaf_(a, a, b * b);
+    };
+    // fixed dz: best dy = -U12 dz / U11; fixed dy: best dz = -U11 U12 dy / (U12^2 + U22^2)
+    const float ya = fminf(fmaxf(-U12 * az * i11, ay), by), yb = fminf(fmaxf(-U12 * bz * i11, ay), by);
+    const float za = fminf(fmaxf(-U11 * U12 * ay * iden, az), bz), zb = fminf(fmaxf(-U11 * U12 * by * iden, az), bz);
+    return fminf(fminf(q2(ya, az), q2(yb, bz)), fminf(q2(ay, za), q2(by, zb)));
+}
+
+// x-range [xl, xh] of the points of the rectangle (offsets from the mean,
+// as above) with Q <= T2, or false when there are none. At fixed (y, z) Q
+// <= T2 holds for |x - xc| <= sqrt(T2 - q2) / U00 with the centre xc =
+// mu_x - (U01 dy + U02 dz) / U00, linear in (dy, dz): the range spans the
+// centre's extremes at the rectangle's corners, widened by the half-width
+// at the rectangle's least q2, and by a few units of float32 rounding.
+__device__ __forceinline__ bool slab_xrange(const Record &r, float ay, float by, float az, float bz, float T2,
+                                            float &xl, float &xh) {
+    const float q2 = slab_q2min(r.f2.x, r.f2.y, r.f2.z, ay, by, az, bz);
+    if (!(q2 <= T2)) return false;
+    const float iu = __builtin_amdgcn_rcpf(r.f1.x);
+    const float w = __builtin_sqrtf(T2 - q2) * iu;
+    const float c0 = r.f1.y * ay, c1 = r.f1.y * by, c2 = r.f1.z * az, c3 = r.f1.z * bz;
+    const float hi = (fmaxf(c0, c1) + fmaxf(c2, c3)) * iu, lo = (fminf(c0, c1) + fminf(c2, c3)) * iu;
+    const float m = (fabsf(r.f0.x) + fabsf(hi) + fabsf(lo) + w) * 0x1p-20f;
+    xl = r.f0.x - hi - w - m;
+    xh = r.f0.x - lo + w + m;
+    return true;
+}
+
+// Row `row` of a Gaussian's box (lower corner (lx, ly, lz) in cells, nx
+// cells along x, ny along y): for grids voxel row (vy, vz) of the box, for
+// ordered queries the row of cells (cy, cz), y fastest. The row's first
+// element (voxel index, or place in the plan's order), its length, and for
+// grids its first voxel along x and the row's y, z.
+struct RowRun {
+    uint32_t start, len, x0;
+    float py, pz;
+};
+
+template <bool GRID>
+__device__ __forceinline__ RowRun row_run(const Record &r, int32_t lx, int32_t ly, int32_t lz, uint32_t nx,
+                                          uint32_t ny, uint32_t row, uint32_t rx, uint32_t ry, uint32_t rz, bool fdiv,
+                                          const QueryParams &q, const GridParams &g, const BwdGeom &bg,
+                                          const uint32_t *__restrict__ point_off) {
+    RowRun o;
+    o.start = o.len = o.x0 = 0;
+    o.py = o.pz = 0.0f;
+    const uint32_t nry = GRID ? ny * ry : ny;
+    // row -> (yy, zz) by a float reciprocal: (row + 1/2) / nry lies at least
+    // 1/(2 nry) from an integer; v_rcp (1 ulp) and the product err by less
+    // than 1.5 2^-23 (row + 1/2) / nry, which cannot cross it while
+    // row < 2^21
+    uint32_t zz;
+    if (fdiv)
+        zz = (uint32_t)(((float)row + 0.5f) * __builtin_amdgcn_rcpf((float)nry));
+    else
+        zz = row / nry;
+    const uint32_t yy = row - zz * nry;
+    float xl, xh;
+    if (GRID) {
+        (void)rz;
+        const uint32_t vy = (uint32_t)ly * ry + yy, vz = (uint32_t)lz * rz + zz;
+        o.py = g.lo[1] + ((float)vy + 0.5f) * q.vsz[1];
+        o.pz = g.lo[2] + ((float)vz + 0.5f) * q.vsz[2];
+        const float dy = o.py - r.f0.y, dz = o.pz - r.f0.z;
+        if (!slab_xrange(r, dy, dy, dz, dz, bg.T2, xl, xh)) return o;
+        // voxels vx of the box with lo + (vx + 1/2) vsz in [xl, xh]
+        const float vmin = (float)((uint32_t)lx * rx), vmax = (float)(((uint32_t)lx + nx) * rx) - 1.0f;
+        const float a = fminf(fmaxf((xl - g.lo[0]) * bg.ivsz0 - 0.5f - bg.xslack, vmin), vmax + 1.0f);
+        const float b = fminf(fmaxf((xh - g.lo[0]) * bg.ivsz0 - 0.5f + bg.xslack, vmin - 1.0f), vmax);
+        const float v0 = ceilf(a), v1 = floorf(b);
+        if (v1 < v0) return o;
+        o.x0 = (uint32_t)v0;
+        o.len = (uint32_t)(v1 - v0) + 1u;
+        o.start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + o.x0;
+    } else {
+        const uint32_t cy = (uint32_t)ly + yy, cz = (uint32_t)lz + zz;
+        const float y0 = g.lo[1] + (float)cy * bg.cw[0] - bg.slack[0];
+        const float y1 = g.lo[1] + (float)(cy + 1u) * bg.cw[0] + bg.slack[0];
+        const float z0 = g.lo[2] + (float)cz * bg.cw[1] - bg.slack[1];
+        const float z1 = g.lo[2] + (float)(cz + 1u) * bg.cw[1] + bg.slack[1];
+        if (!slab_xrange(r, y0 - r.f0.y, y1 - r.f0.y, z0 - r.f0.z, z1 - r.f0.z, bg.T2, xl, xh)) return o;
+        // quarters of the box's cells with queries whose x can lie in
+        // [xl, xh]: the plan's quarter of x is floor(kSub t), t = (x - lo)
+        // invc in the same float32 operations, monotone in x
+        const float qmin = (float)(kSub * (uint32_t)lx), qmax = (float)(kSub * ((uint32_t)lx + nx)) - 1.0f;
+        const float ql = fminf(fmaxf(floorf((float)kSub * ((xl - g.lo[0]) * g.invc[0])), qmin), qmax);
+        const float qh = fminf(fmaxf(floorf((float)kSub * ((xh - g.lo[0]) * g.invc[0])), qmin), qmax);
+        // the row's quarters are entries base .. base + K of the plan's
+        // offsets, the last one the start of the next row of cells
+        const uint32_t base = (cz * (uint32_t)g.cells[1] + cy) * bg.K;
+        o.start = point_off[base + (uint32_t)ql];
+        o.len = point_off[base + (uint32_t)qh + 1u] - o.start;
+    }
+    return o;
+}
+
+// PACK consecutive Gaussians of gorder per wavefront. The rows of the
+// wave's Gaussians are listed one Gaussian after the other and taken 64 at
+// a time, lane l setting up row l of the batch (its x-range from the
+// Gaussian's record, for ordered queries two offsets of the plan). Within a batch the rows are concatenated; each Gaussian walks
+// its own part 64 elements per step, lane l taking element e0 + l, so the
+// lanes stay busy across row ends and every load reads whole cache lines;
+// a lane finds its row from the row starts with two ballots. The cutoff
+// test is all a non-contributing pair costs; contributing pairs go to a
+// per-wave LDS queue, and every 64 queued pairs are processed with all
+// lanes busy.
 template <bool GRID, uint32_t PACK>
-__global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, GridParams g, const FwdRecord *__restrict__ rec,
+__global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, GridParams g, BwdGeom bg,
+                                                           const Record *__restrict__ rec,
                                                            const CellBox *__restrict__ box,
-                                                           const uint8_t *__restrict__ spans,
                                                            const uint32_t *__restrict__ gorder, int64_t n_gauss,
                                                            const uint32_t *__restrict__ point_off,
                                                            const float4 *__restrict__ plan_pos,
@@ -305,16 +379,19 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
         rz = (uint32_t)(q.dims[2] / g.cells[2]);
     }
     // lane i < nk describes Gaussian i of the wave: id, box, rows
-    uint32_t mgid = 0, mR = 0, mnx = 0, mny = 1, mtrim = 0;
+    uint32_t mgid = 0, mR = 0, mnx = 0, mny = 1;
     int32_t mlx = 0, mly = 0, mlz = 0;
+    Record mrec;
+    mrec.f0 = mrec.f1 = mrec.f2 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     if (lane < nk) {
         mgid = gorder[first + lane];
+        mrec = rec[mgid];
         const CellBox bx = box[mgid];
         if (bx.hi.x >= bx.lo.x) {
             mnx = (uint32_t)(bx.hi.x - bx.lo.x + 1);
             mny = (uint32_t)(bx.hi.y - bx.lo.y + 1);
-            mR = mny * ry * (uint32_t)(bx.hi.z - bx.lo.z + 1) * rz;
-            mtrim = (uint32_t)bx.lo.w;
+            const uint32_t nz = (uint32_t)(bx.hi.z - bx.lo.z + 1);
+            mR = GRID ? mny * ry * nz * rz : mny * nz;
             mlx = bx.lo.x;
             mly = bx.lo.y;
             mlz = bx.lo.z;
@@ -330,12 +407,9 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
     }
     const uint32_t mRend = wave_incl_sum(mR);  // end of Gaussian i's rows in the wave's list
     const uint32_t Rw = __builtin_amdgcn_readlane(mRend, kWave - 1);
-    // row -> (yy, zz) by a float reciprocal: (row + 1/2) / nry lies at least
-    // 1/(2 nry) from an integer; v_rcp (1 ulp) and the product err by less
-    // than 1.5 2^-23 (row + 1/2) / nry, which cannot cross it while
-    // row < 2^21
+    // rows -> (yy, zz) by a float reciprocal below 2^21 rows (see row_run)
     const bool fdiv = wave_max_uniform(mR) < (1u << 21);
-    FwdRecord r;
+    Record r;
     r.f0 = r.f1 = r.f2 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     Acc acc;
     acc_zero(acc);
@@ -348,12 +422,10 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
         uint32_t i = 0;
         for (uint32_t t = 0; t < nk; ++t) i += __builtin_amdgcn_readlane(mRend, t) <= gr ? 1u : 0u;
         const uint32_t src = (i < kWave ? i : 0u) << 2;
-        const uint32_t f_gid = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mgid);
         const uint32_t f_end = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mRend);
         const uint32_t f_R = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mR);
         const uint32_t f_nx = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mnx);
         const uint32_t f_ny = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mny);
-        const uint32_t f_trim = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)mtrim);
         const uint32_t f_lx = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, mlx);
         const uint32_t f_ly = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, mly);
         const uint32_t f_lz = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, mlz);
@@ -361,40 +433,17 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
         float rpy = 0.0f, rpz = 0.0f;
         if (gr < Rw) {
             const uint32_t row = gr - (f_end - f_R);  // row within its Gaussian
-            const uint32_t nry = f_ny * ry;
-            uint32_t zz;
-            if (fdiv)
-                zz = (uint32_t)(((float)row + 0.5f) * __builtin_amdgcn_rcpf((float)nry));
-            else
-                zz = row / nry;
-            const uint32_t yy = row - zz * nry;
-            // the row's run of cells: the whole box row, or its span
-            uint32_t xa = 0, xn = f_nx, qa = 0, qb = 0;
-            if (f_trim) {
-                const size_t at = (size_t)f_gid * kSpanStride + (yy / ry) + f_ny * (zz / rz);
-                const uint32_t code = spans[at];
-                xa = span_first(code);
-                xn = span_len(code);
-                if (!GRID) {
-                    // the quarters of the run's end cells the bound reaches
-                    const uint32_t qc = spans[at + kSpanRows];
-                    qa = qc & 3u;
-                    qb = qc >> 2;
-                }
-            }
-            if (GRID) {
-                const uint32_t vy = f_ly * ry + yy, vz = f_lz * rz + zz;
-                rx0 = (f_lx + xa) * rx;
-                start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + rx0;
-                len = xn * rx;
-                rpy = g.lo[1] + ((float)vy + 0.5f) * q.vsz[1];
-                rpz = g.lo[2] + ((float)vz + 0.5f) * q.vsz[2];
-            } else if (xn > 0) {
-                const uint32_t cy = f_ly + yy, cz = f_lz + zz;
-                const uint32_t kbase = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz) + f_lx;
-                start = point_off[kSub * (kbase + xa) + qa];
-                len = point_off[kSub * (kbase + xa + xn) - qb] - start;
-            }
+            Record fr;
+            fr.f0 = make_float4(bperm_f(src, mrec.f0.x), bperm_f(src, mrec.f0.y), bperm_f(src, mrec.f0.z), 0.0f);
+            fr.f1 = make_float4(bperm_f(src, mrec.f1.x), bperm_f(src, mrec.f1.y), bperm_f(src, mrec.f1.z), 0.0f);
+            fr.f2 = make_float4(bperm_f(src, mrec.f2.x), bperm_f(src, mrec.f2.y), bperm_f(src, mrec.f2.z), 0.0f);
+            const RowRun rr = row_run<GRID>(fr, (int32_t)f_lx, (int32_t)f_ly, (int32_t)f_lz, f_nx, f_ny, row, rx, ry,
+                                            rz, fdiv, q, g, bg, point_off);
+            start = rr.start;
+            len = rr.len;
+            rx0 = rr.x0;
+            rpy = rr.py;
+            rpz = rr.pz;
         }
         const uint32_t nrows = (Rw - rb) < (uint32_t)kWave ? (Rw - rb) : (uint32_t)kWave;
         const uint32_t incl = wave_incl_sum(len);   // end of row l in the batch's concatenation
@@ -413,7 +462,7 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
                 acc_zero(acc);
                 cur = gi;
                 cur_gid = __builtin_amdgcn_readlane(mgid, gi);
-                r = load_fwd_uniform(rec, cur_gid);
+                r = load_record_uniform(rec, cur_gid);
             }
             // its rows in this batch and their elements [Ea, Eb)
             const uint32_t la = gend - gR > rb ? gend - gR - rb : 0u;
@@ -610,13 +659,14 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
     d_weight[i] = mc.z;
 }
 
-// Pairs the backward tests, for measurement: per Gaussian the queries in
-// its box rows, cut to the row spans and end-cell quarters of a trimmed box
-// (grids: the voxels of its box rows). Summed per block, then into *total
-// with one integer atomic per block (the sum does not depend on its order).
-__global__ __launch_bounds__(kBlock) void k_count_backward_pairs(QueryParams q, GridParams g,
-                                                                 const CellBox *__restrict__ box,
-                                                                 const uint8_t *__restrict__ spans, int64_t n_gauss,
+// Pairs the backward tests, for measurement: per Gaussian the elements of
+// its rows, each cut to its x-range as the backward cuts it (row_run).
+// Summed per block, then into *total with one integer atomic per block (the
+// sum does not depend on its order).
+template <bool GRID>
+__global__ __launch_bounds__(kBlock) void k_count_backward_pairs(QueryParams q, GridParams g, BwdGeom bg,
+                                                                 const Record *__restrict__ rec,
+                                                                 const CellBox *__restrict__ box, int64_t n_gauss,
                                                                  const uint32_t *__restrict__ point_off,
                                                                  unsigned long long *total) {
     __shared__ unsigned long long lds[kWavesPerBlock];
@@ -625,32 +675,16 @@ __global__ __launch_bounds__(kBlock) void k_count_backward_pairs(QueryParams q, 
     if (i < n_gauss) {
         const CellBox bx = box[i];
         if (bx.hi.x >= bx.lo.x) {
-            const bool grid = q.kind == 0;
-            const uint32_t rx = grid ? (uint32_t)(q.dims[0] / g.cells[0]) : 1u;
-            const uint32_t ry = grid ? (uint32_t)(q.dims[1] / g.cells[1]) : 1u;
-            const uint32_t rz = grid ? (uint32_t)(q.dims[2] / g.cells[2]) : 1u;
+            const uint32_t rx = GRID ? (uint32_t)(q.dims[0] / g.cells[0]) : 1u;
+            const uint32_t ry = GRID ? (uint32_t)(q.dims[1] / g.cells[1]) : 1u;
+            const uint32_t rz = GRID ? (uint32_t)(q.dims[2] / g.cells[2]) : 1u;
             const uint32_t nx = (uint32_t)(bx.hi.x - bx.lo.x + 1), ny = (uint32_t)(bx.hi.y - bx.lo.y + 1);
             const uint32_t nz = (uint32_t)(bx.hi.z - bx.lo.z + 1);
-            for (uint32_t zz = 0; zz < nz; ++zz)
-                for (uint32_t yy = 0; yy < ny; ++yy) {
-                    uint32_t xa = 0, xn = nx, qa = 0, qb = 0;
-                    if (bx.lo.w) {
-                        const size_t at = (size_t)i * kSpanStride + yy + ny * zz;
-                        xa = span_first(spans[at]);
-                        xn = span_len(spans[at]);
-                        qa = spans[at + kSpanRows] & 3u;
-                        qb = spans[at + kSpanRows] >> 2;
-                    }
-                    if (xn == 0) continue;
-                    if (grid) {
-                        c += (unsigned long long)xn * rx * ry * rz;
-                    } else {
-                        const uint32_t kb = (uint32_t)g.cells[0] * ((uint32_t)bx.lo.y + yy +
-                                                                    (uint32_t)g.cells[1] * ((uint32_t)bx.lo.z + zz)) +
-                                            (uint32_t)bx.lo.x + xa;
-                        c += point_off[kSub * (kb + xn) - qb] - point_off[kSub * kb + qa];
-                    }
-                }
+            const uint32_t R = GRID ? ny * ry * nz * rz : ny * nz;
+            const Record r = rec[i];
+            for (uint32_t row = 0; row < R; ++row)
+                c += row_run<GRID>(r, bx.lo.x, bx.lo.y, bx.lo.z, nx, ny, row, rx, ry, rz, false, q, g, bg, point_off)
+                         .len;
         }
     }
     // block sum in a fixed order, then one atomic per block
@@ -668,40 +702,43 @@ __global__ __launch_bounds__(kBlock) void k_count_backward_pairs(QueryParams q, 
 
 template <bool GRID>
 void launch_gauss(uint32_t pack, uint32_t wblocks, hipStream_t s, const QueryParams &q, const GridParams &g,
-                  const FwdRecord *rec, const CellBox *box, const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss,
+                  const BwdGeom &bg, const Record *rec, const CellBox *box, const uint32_t *gorder, int64_t n_gauss,
                   const uint32_t *point_off, const float4 *plan_pos, const float2 *ab, float T, float *moments) {
     if (pack == 1)
-        hipLaunchKernelGGL((k_backward_gauss<GRID, 1>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, rec, box, spans,
+        hipLaunchKernelGGL((k_backward_gauss<GRID, 1>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, bg, rec, box,
                            gorder, n_gauss, point_off, plan_pos, ab, T, moments);
     else if (pack == kPackLarge)
-        hipLaunchKernelGGL((k_backward_gauss<GRID, kPackLarge>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, rec, box,
-                           spans, gorder, n_gauss, point_off, plan_pos, ab, T, moments);
+        hipLaunchKernelGGL((k_backward_gauss<GRID, kPackLarge>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, bg, rec,
+                           box, gorder, n_gauss, point_off, plan_pos, ab, T, moments);
     else
-        hipLaunchKernelGGL((k_backward_gauss<GRID, kPack>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, rec, box,
-                           spans, gorder, n_gauss, point_off, plan_pos, ab, T, moments);
+        hipLaunchKernelGGL((k_backward_gauss<GRID, kPack>), dim3(wblocks), dim3(kBwdBlock), 0, s, q, g, bg, rec, box,
+                           gorder, n_gauss, point_off, plan_pos, ab, T, moments);
 }
 
 }  // namespace
 
-hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g, const CellBox *box,
-                                      const uint8_t *spans, int64_t n_gauss, const uint32_t *point_off,
-                                      unsigned long long *total, hipStream_t s) {
+hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g, const BwdGeom &bg,
+                                      const Record *rec, const CellBox *box, int64_t n_gauss,
+                                      const uint32_t *point_off, unsigned long long *total, hipStream_t s) {
     hipError_t e = fill_u32((uint32_t *)total, 0u, 2, s);
     if (e != hipSuccess || n_gauss <= 0) return e;
-    hipLaunchKernelGGL(k_count_backward_pairs, dim3((uint32_t)((n_gauss + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
-                       q, g, box, spans, n_gauss, point_off, total);
+    const dim3 grid((uint32_t)((n_gauss + kBlock - 1) / kBlock));
+    if (q.kind == 0)
+        hipLaunchKernelGGL(k_count_backward_pairs<true>, grid, dim3(kBlock), 0, s, q, g, bg, rec, box, n_gauss,
+                           point_off, total);
+    else
+        hipLaunchKernelGGL(k_count_backward_pairs<false>, grid, dim3(kBlock), 0, s, q, g, bg, rec, box, n_gauss,
+                           point_off, total);
     return hipGetLastError();
 }
 
-hipError_t launch_backward(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const CellBox *box,
-                           const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, int64_t n_pairs,
-                           const uint32_t *order, const uint32_t *point_off,
-                           const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,
+hipError_t launch_backward(const QueryParams &q, const GridParams &g, const BwdGeom &bg, const Record *rec,
+                           const CellBox *box, const uint32_t *gorder, int64_t n_gauss, int64_t n_pairs,
+                           const uint32_t *order, const uint32_t *point_off, const float4 *plan_pos,
+                           const float2 *plan_out, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
-                           const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
-                           float *d_mean, float *d_scale, float *d_rot, float *d_value, float *d_weight,
-                           hipStream_t s) {
-    (void)mean;
+                           const BackwardBuffers &b, const float *scale, const float *rot, float *d_mean,
+                           float *d_scale, float *d_rot, float *d_value, float *d_weight, hipStream_t s) {
     if (n_gauss <= 0) return hipSuccess;
     hipError_t e;
     const bool grid = q.kind == 0;
@@ -709,14 +746,15 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const FwdR
     if (q.n > 0) {
         const uint32_t qblocks = (uint32_t)((q.n + kBlock - 1) / kBlock);
         prof_begin("bwd_stage", s);
-        if (grid)
+        if (grid) {
             hipLaunchKernelGGL(k_stage_grid, dim3(qblocks), dim3(kBlock), 0, s, q.n, value, influence, grad_value,
                                grad_influence, b.ab);
-        else {
-            const dim3 sb((uint32_t)((q.n + kBlock * kStageItems - 1) / (kBlock * kStageItems)));
+        } else {
+            const dim3 pb((uint32_t)((q.n + kBlock * kStageItems - 1) / (kBlock * kStageItems)));
             const bool vec = ((uintptr_t)grad_value % 16 == 0) && ((uintptr_t)grad_influence % 16 == 0);
-            hipLaunchKernelGGL(k_pack_cotangents, sb, dim3(kBlock), 0, s, q.n, grad_value, grad_influence, vec, b.cot);
-            hipLaunchKernelGGL(k_stage_points, sb, dim3(kBlock), 0, s, q.n, order, plan_out, b.cot, b.ab);
+            hipLaunchKernelGGL(k_pack_cotangents, pb, dim3(kBlock), 0, s, q.n, grad_value, grad_influence, vec,
+                               b.cot);
+            hipLaunchKernelGGL(k_stage_plan, dim3(qblocks), dim3(kBlock), 0, s, q.n, order, plan_out, b.cot, b.ab);
         }
         prof_end("bwd_stage", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -725,10 +763,10 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const FwdR
         const uint32_t wblocks = (uint32_t)((n_gauss + pack * kBwdWaves - 1) / (pack * kBwdWaves));
         prof_begin("bwd_gauss", s);
         if (grid)
-            launch_gauss<true>(pack, wblocks, s, q, g, rec, box, spans, gorder, n_gauss, point_off, plan_pos, b.ab, T,
+            launch_gauss<true>(pack, wblocks, s, q, g, bg, rec, box, gorder, n_gauss, nullptr, nullptr, b.ab, T,
                                b.moments);
         else
-            launch_gauss<false>(pack, wblocks, s, q, g, rec, box, spans, gorder, n_gauss, point_off, plan_pos, b.ab, T,
+            launch_gauss<false>(pack, wblocks, s, q, g, bg, rec, box, gorder, n_gauss, point_off, plan_pos, b.ab, T,
                                 b.moments);
         prof_end("bwd_gauss", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -29,12 +29,8 @@ namespace {
 constexpr float kNegHalfLog2eG = -0.72134752044448170368f;  // -1/2 log2(e)
 
 __device__ __forceinline__ float eval_pair(const Record &r, float4 p, float T) {
-    const float dx = p.x - r.r0.x, dy = p.y - r.r0.y, dz = p.z - r.r0.z;
-    const float u0 = fmaf_(r.r1.x, dx, fmaf_(r.r1.y, dy, r.r1.z * dz));
-    const float u1 = fmaf_(r.r2.x, dx, fmaf_(r.r2.y, dy, r.r2.z * dz));
-    const float u2 = fmaf_(r.r3.x, dx, fmaf_(r.r3.y, dy, r.r3.z * dz));
-    const float Q = fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
-    return Q <= T ? r.r0.w * exp2_hw(Q * kNegHalfLog2eG) : 0.0f;
+    const float Q = record_q(r, p.x, p.y, p.z);
+    return Q <= T ? r.f0.w * exp2_hw(Q * kNegHalfLog2eG) : 0.0f;
 }
 
 // Position of every query in plan order (the walk below reads them
@@ -66,7 +62,7 @@ __global__ __launch_bounds__(kBlock) void k_forward_gauss(GridParams g, const Re
     const CellBox bx = load_box_uniform(box, gid);
     if (bx.hi.x < bx.lo.x) return;
     const Record r = load_record_uniform(rec, gid);
-    const float v = r.r1.w;
+    const float v = r.f1.w;
     const uint32_t nx = (uint32_t)(bx.hi.x - bx.lo.x + 1), ny = (uint32_t)(bx.hi.y - bx.lo.y + 1);
     const uint32_t R = ny * (uint32_t)(bx.hi.z - bx.lo.z + 1);
     const bool trimmed = bx.lo.w != 0;

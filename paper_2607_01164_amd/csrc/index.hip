@@ -177,8 +177,7 @@ constexpr int kPreBlock = kWave;  // one wave per workgroup: the span walk is pe
 __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restrict__ mean, const float *__restrict__ scale,
                                                        const float *__restrict__ rot, const float *__restrict__ value,
                                                        const float *__restrict__ weight, int64_t n, GridParams g,
-                                                       float rci, Record *__restrict__ rec,
-                                                       FwdRecord *__restrict__ frec, CellBox *__restrict__ box,
+                                                       float rci, Record *__restrict__ rec, CellBox *__restrict__ box,
                                                        uint8_t *__restrict__ spans, uint64_t *__restrict__ count,
                                                        uint64_t *__restrict__ block_sum) {
     // span parameters of the wave's boxes, one array per field (lane stride
@@ -356,8 +355,8 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
     b.hi = make_int4(hi_c[0], hi_c[1], hi_c[2], 0);
     box[i] = b;
 
-    // evaluation record: M = S^-1 R^T formed in float64, rounded once to float32
-    Record r;
+    // evaluation record: the Cholesky factor of the inverse covariance,
+    // formed in float64 and rounded once to float32
     if (valid) {
         const double qn = sqrt((double)q[0] * q[0] + (double)q[1] * q[1] + (double)q[2] * q[2] + (double)q[3] * q[3]);
         const double iq = 1.0 / qn;
@@ -372,19 +371,8 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
         Rd[2][0] = 2.0 * (x * z - w_ * y);
         Rd[2][1] = 2.0 * (y * z + w_ * x);
         Rd[2][2] = 1.0 - 2.0 * (x * x + y * y);
-        float M[3][3];
-#pragma unroll
-        for (int k = 0; k < 3; ++k) {
-            const double is = 1.0 / (double)s[k];
-#pragma unroll
-            for (int j = 0; j < 3; ++j) M[k][j] = (float)(Rd[j][k] * is);
-        }
-        r.r0 = make_float4(mu[0], mu[1], mu[2], w);
-        r.r1 = make_float4(M[0][0], M[0][1], M[0][2], v);
-        r.r2 = make_float4(M[1][0], M[1][1], M[1][2], 0.0f);
-        r.r3 = make_float4(M[2][0], M[2][1], M[2][2], 0.0f);
-        // the forward's factor: the inverse covariance A = R S^-2 R^T and its
-        // Cholesky factor U (upper triangular, A = U^T U), in float64
+        // the inverse covariance A = R S^-2 R^T and its Cholesky factor U
+        // (upper triangular, A = U^T U)
         double A[3][3];
 #pragma unroll
         for (int j = 0; j < 3; ++j)
@@ -400,18 +388,16 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
         const double u11 = sqrt(A[1][1] - u01 * u01);
         const double u12 = (A[1][2] - u01 * u02) / u11;
         const double u22 = sqrt(A[2][2] - u02 * u02 - u12 * u12);
-        FwdRecord f;
-        f.f0 = r.r0;
+        Record f;
+        f.f0 = make_float4(mu[0], mu[1], mu[2], w);
         f.f1 = make_float4((float)u00, (float)u01, (float)u02, v);
         f.f2 = make_float4((float)u11, (float)u12, (float)u22, 0.0f);
-        frec[i] = f;
+        rec[i] = f;
     } else {
-        r.r0 = r.r1 = r.r2 = r.r3 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        FwdRecord f;
+        Record f;
         f.f0 = f.f1 = f.f2 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        frec[i] = f;
+        rec[i] = f;
     }
-    rec[i] = r;
 }
 
 // In-place inclusive max-scan of a tile's kExpandTile marks (kExpandItems
@@ -579,16 +565,15 @@ hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g,
 }
 
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
-                             const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
-                             FwdRecord *frec, CellBox *box, uint8_t *spans, uint64_t *count, uint64_t *block_sum,
+                             const float *weight, int64_t n, const GridParams &g, float rci, Record *rec, CellBox *box, uint8_t *spans, uint64_t *count, uint64_t *block_sum,
                              hipStream_t s) {
     // one thread per Gaussian (thread 0 also writes count[n]): for n a
     // multiple of 64 the launch fits one round of the chip
     const int64_t threads = n > 0 ? n : 1;
     const uint32_t blocks = (uint32_t)((threads + kPreBlock - 1) / kPreBlock);
     prof_begin("preprocess", s);
-    hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kPreBlock), 0, s, mean, scale, rot, value, weight, n, g, rci, rec,
-                       frec, box, spans, count, block_sum);
+    hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kPreBlock), 0, s, mean, scale, rot, value, weight, n, g, rci,
+                       rec, box, spans, count, block_sum);
     prof_end("preprocess", s);
     return hipGetLastError();
 }

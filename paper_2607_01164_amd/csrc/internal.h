@@ -13,33 +13,23 @@ constexpr int kWave = 64;
 constexpr int kBlock = 256;             // threads per workgroup for most kernels
 constexpr int kWavesPerBlock = kBlock / kWave;
 
-// Per-Gaussian evaluation record, 64 bytes, written by the preprocess kernel.
-//   r0 = (mu_x, mu_y, mu_z, w)
-//   r1 = (M00, M01, M02, v)      M = S^-1 R^T, so u = M (p - mu), Q = |u|^2
-//   r2 = (M10, M11, M12, 0)
-//   r3 = (M20, M21, M22, 0)
-// M is formed in float64 and rounded once to float32. Invalid Gaussians get
-// an all-zero record and an empty box, and appear in no cell list.
-struct alignas(16) Record {
-    float4 r0, r1, r2, r3;
-};
-
-// The forward samplers' record, 48 bytes, written with Record:
+// Per-Gaussian evaluation record, 48 bytes, written by the preprocess:
 //   f0 = (mu_x, mu_y, mu_z, w)
-//   f1 = (U00, U01, U02, v)      U upper triangular with U^T U = M^T M, the
-//   f2 = (U11, U12, U22, 0)      inverse covariance, so Q = |U (p - mu)|^2
+//   f1 = (U00, U01, U02, v)      U upper triangular with U^T U = R S^-2 R^T,
+//   f2 = (U11, U12, U22, 0)      the inverse covariance, so Q = |U (p - mu)|^2
 // U (the Cholesky factor of the inverse covariance) takes 6 products and
-// sums where M takes 9, and three 16-byte quarters where M takes four; its
-// float32 rounding bounds Q as M's does (|U| and |M| have the same 2-norm).
-// Formed in float64 and rounded once. Invalid Gaussians get zeros.
-struct alignas(16) FwdRecord {
+// sums where M = S^-1 R^T takes 9, and three 16-byte quarters where M takes
+// four; its float32 rounding bounds Q as M's does (U and M have the same
+// 2-norm). Formed in float64 and rounded once. Invalid Gaussians get zeros,
+// an empty box, and appear in no cell list.
+struct alignas(16) Record {
     float4 f0, f1, f2;
 };
-constexpr int kFwdQuads = 3;  // 16-byte quarters of a FwdRecord
+constexpr int kRecordQuads = 3;  // 16-byte quarters of a Record
 
 // Q = |U (p - mu)|^2 in the one order of float32 operations every forward
 // sampler and the pair counter use.
-__device__ __forceinline__ float fwd_q(const FwdRecord &r, float px, float py, float pz) {
+__device__ __forceinline__ float record_q(const Record &r, float px, float py, float pz) {
     const float dx = px - r.f0.x, dy = py - r.f0.y, dz = pz - r.f0.z;
     const float u0 = __builtin_fmaf(r.f1.x, dx, __builtin_fmaf(r.f1.y, dy, r.f1.z * dz));
     const float u1 = __builtin_fmaf(r.f2.x, dy, r.f2.y * dz);
@@ -47,13 +37,13 @@ __device__ __forceinline__ float fwd_q(const FwdRecord &r, float px, float py, f
     return __builtin_fmaf(u0, u0, __builtin_fmaf(u1, u1, u2 * u2));
 }
 
-// A forward record loaded with a wave-uniform address (scalar loads).
-__device__ __forceinline__ FwdRecord load_fwd_uniform(const FwdRecord *rec, uint32_t g) {
+// A record loaded with a wave-uniform address (scalar loads).
+__device__ __forceinline__ Record load_record_uniform(const Record *rec, uint32_t g) {
     typedef float f4u __attribute__((ext_vector_type(4)));
     typedef __attribute__((address_space(4))) const f4u CF4;
-    CF4 *p = (CF4 *)rec + kFwdQuads * (size_t)g;
+    CF4 *p = (CF4 *)rec + kRecordQuads * (size_t)g;
     const f4u a = p[0], b = p[1], c = p[2];
-    FwdRecord r;
+    Record r;
     r.f0 = make_float4(a.x, a.y, a.z, a.w);
     r.f1 = make_float4(b.x, b.y, b.z, b.w);
     r.f2 = make_float4(c.x, c.y, c.z, c.w);
@@ -91,17 +81,6 @@ typedef int i4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(4))) const f4v ConstF4;
 typedef __attribute__((address_space(4))) const i4v ConstI4;
 typedef __attribute__((address_space(4))) const uint32_t ConstU32;
-
-__device__ __forceinline__ Record load_record_uniform(const Record *rec, uint32_t g) {
-    ConstF4 *p = (ConstF4 *)rec + 4 * (size_t)g;
-    const f4v a = p[0], b = p[1], c = p[2], d = p[3];
-    Record r;
-    r.r0 = make_float4(a.x, a.y, a.z, a.w);
-    r.r1 = make_float4(b.x, b.y, b.z, b.w);
-    r.r2 = make_float4(c.x, c.y, c.z, c.w);
-    r.r3 = make_float4(d.x, d.y, d.z, d.w);
-    return r;
-}
 
 __device__ __forceinline__ CellBox load_box_uniform(const CellBox *box, uint32_t g) {
     ConstI4 *p = (ConstI4 *)box + 2 * (size_t)g;
@@ -311,9 +290,8 @@ struct GridParams {
 // count[0..n] receives the pair count of every Gaussian (count[n] = 0) and
 // block_sum[b] the sum over elements [64 b, 64 b + 64) of count
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
-                             const float *weight, int64_t n, const GridParams &g, float rci, Record *rec,
-                             FwdRecord *frec, CellBox *box, uint8_t *spans, uint64_t *count, uint64_t *block_sum,
-                             hipStream_t s);
+                             const float *weight, int64_t n, const GridParams &g, float rci, Record *rec, CellBox *box, uint8_t *spans,
+                             uint64_t *count, uint64_t *block_sum, hipStream_t s);
 // tile_first: ceil(npairs / kSortTile) words of scratch
 hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8_t *spans, int64_t n, int64_t npairs,
                        const GridParams &g,
@@ -379,7 +357,7 @@ __device__ __forceinline__ void query_position(const QueryParams &q, const GridP
 // the first sort digit's tile counts.
 hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t *keys, uint32_t *ids,
                              const RadixPass0 &pass0, hipStream_t s);
-hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const uint32_t *gids,
+hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                               const uint32_t *cell_off, float T, float tau, float *out_v, float *out_i,
                               hipStream_t s);
 // Work items of the ordered-query sampler (kept in the plan).
@@ -399,7 +377,7 @@ struct PlanResults {
     float2 *out;
 };
 
-hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const uint32_t *gids,
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                                 const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
                                 const PlanResults &pr, hipStream_t s);
@@ -408,7 +386,7 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
 // totals[0] and totals[1] (device, 16 bytes); plan_keys and plan_pos are
 // the sorted keys and the positions a forward left in the plan (unused for
 // GRID queries).
-hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const FwdRecord *rec,
+hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const Record *rec,
                                      const uint32_t *gids, const uint32_t *cell_off, const uint32_t *plan_keys,
                                      const float4 *plan_pos, float T, unsigned long long *totals, hipStream_t s);
 
@@ -418,24 +396,40 @@ hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g,
                              uint32_t *ids, const RadixPass0 &pass0, hipStream_t s);
 
 // Backward (backward.hip).
+//
+// The backward walks each Gaussian's queries by rows along x, each row cut
+// to the x-range of the cutoff ellipsoid over the row's (y, z) extent: for
+// grids a row of voxels; for ordered queries a row of cells, a run of the
+// plan's order, cut to quarters of cells along x.
+
+// Row geometry of the backward (host-computed).
+struct BwdGeom {
+    float T2;          // the cutoff the row bounds use: T (1 + 2^-7)
+    float cw[2];       // ordered queries: y, z extent of a cell, 1 / invc
+    float slack[2];    // widening of a row's y, z extent (float rounding)
+    float ivsz0;       // grids: voxels per unit along x, 1 / vsz[0]
+    float xslack;      // grids: widening of a row's voxel range, in voxels
+    uint32_t K;        // kSub cells[0]: quarters of a row of cells
+};
+
 struct BackwardBuffers {
     float *moments;        // [n_gauss][12]
-    float2 *ab;            // [n] (alpha, beta) per query: plan order (points, voxels) or voxel order (grid)
-    float2 *cot;           // [n] (dL/dPhi, dL/dI) packed in query order (points, voxels)
+    float2 *ab;            // [n] (alpha, beta) per query: plan order (ordered queries) or voxel order (grid)
+    float2 *cot;           // [n] (dL/dPhi, dL/dI) packed in query order (ordered queries)
 };
-// Pairs the backward tests (measurement), into *total (device, 8 bytes).
-hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g, const CellBox *box,
-                                      const uint8_t *spans, int64_t n_gauss, const uint32_t *point_off,
-                                      unsigned long long *total, hipStream_t s);
+// Pairs the backward tests (measurement), into *total (device, 8 bytes);
+// point_off: the plan's offsets (ordered queries).
+hipError_t launch_count_backward_pairs(const QueryParams &q, const GridParams &g, const BwdGeom &bg,
+                                      const Record *rec, const CellBox *box, int64_t n_gauss,
+                                      const uint32_t *point_off, unsigned long long *total, hipStream_t s);
 // n_pairs: the index's pair count (it sets how many Gaussians share a wave)
-hipError_t launch_backward(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const CellBox *box,
-                           const uint8_t *spans, const uint32_t *gorder, int64_t n_gauss, int64_t n_pairs,
-                           const uint32_t *order, const uint32_t *point_off,
-                           const float4 *plan_pos, const float2 *plan_out, const float *value, const float *influence,
+hipError_t launch_backward(const QueryParams &q, const GridParams &g, const BwdGeom &bg, const Record *rec,
+                           const CellBox *box, const uint32_t *gorder, int64_t n_gauss, int64_t n_pairs,
+                           const uint32_t *order, const uint32_t *point_off, const float4 *plan_pos,
+                           const float2 *plan_out, const float *value, const float *influence,
                            const float *grad_value, const float *grad_influence, float T,
-                           const BackwardBuffers &b, const float *mean, const float *scale, const float *rot,
-                           float *d_mean, float *d_scale, float *d_rot, float *d_value, float *d_weight,
-                           hipStream_t s);
+                           const BackwardBuffers &b, const float *scale, const float *rot, float *d_mean,
+                           float *d_scale, float *d_rot, float *d_value, float *d_weight, hipStream_t s);
 
 // Densification (densify.hip).
 size_t densify_work_bytes(int64_t n_in, int64_t nq);

@@ -336,26 +336,58 @@ __global__ __launch_bounds__(kBlock) void k_pair_offsets(uint64_t *__restrict__ 
     }
 }
 
-// offsets[k] = number of keys < k, for k = 0 .. nkeys: thread k finds the
-// first sorted key >= k by binary search (keys past the end count as
-// nkeys). Every offset is found on its own, so a long run of empty keys
-// costs no more than a short one, and neighbouring threads follow nearly
-// the same search path through the same cache lines.
+// offsets[k] = number of keys < k, for k = 0 .. nkeys. Wave w covers keys
+// k0 = 64 w .. k0 + 63. It first bounds all of them at once: lanes 0..31
+// search for the first sorted key >= k0 and lanes 32..63 for the first >= k0
+// + 64, each half probing 32 evenly spaced keys of its interval a step
+// (about log32(n) dependent loads, where a binary search takes log2(n)).
+// Lane l then finds its own key k0 + l by binary search between the two,
+// inside one short stretch of the array that the wave's lanes share. The
+// cost of a wave does not depend on how long runs of empty keys are.
 __global__ __launch_bounds__(kBlock) void k_key_offsets(const uint32_t *__restrict__ keys, int64_t n,
                                                         uint32_t *__restrict__ off, int64_t nkeys) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k > nkeys) return;
-    uint64_t lo = 0, len = (uint64_t)n;
+    const uint32_t lane = threadIdx.x % kWave;
+    const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) - lane;
+    if (k0 > nkeys) return;  // whole waves leave together
+    const bool upper = lane >= 32;
+    const uint32_t l = lane & 31u;
+    const int64_t t = upper ? k0 + 64 : k0;
+    // the first index whose key is >= t lies in [lo, hi]
+    uint64_t lo = 0, hi = (uint64_t)n;
+    while (__ballot(hi > lo) != 0) {
+        const uint64_t len = hi - lo;
+        const uint64_t step = (len + 31) / 32;
+        const uint64_t p = lo + (uint64_t)l * step;
+        const bool less = p < hi && (int64_t)keys[p] < t;
+        const uint64_t m = __ballot(less);
+        const uint32_t cnt = (uint32_t)__popcll(upper ? (m >> 32) : (m & 0xffffffffull));
+        if (hi > lo) {
+            if (cnt == 0) {
+                hi = lo;
+            } else {
+                const uint64_t last = lo + (uint64_t)(cnt - 1) * step;  // its key is < t
+                const uint64_t next = last + step;                       // its key is >= t, if probed
+                lo = last + 1;
+                if (next < hi) hi = next;
+            }
+        }
+    }
+    const uint64_t a = (uint64_t)__shfl((int)(uint32_t)lo, 0, kWave) |
+                       ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(lo >> 32), 0, kWave) << 32);
+    const uint64_t b = (uint64_t)(uint32_t)__shfl((int)(uint32_t)lo, 32, kWave) |
+                       ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(lo >> 32), 32, kWave) << 32);
+    const int64_t k = k0 + lane;
+    uint64_t first = a, len = b - a;
     while (len > 0) {
         const uint64_t half = len >> 1;
-        if ((int64_t)keys[lo + half] < k) {
-            lo += half + 1;
+        if ((int64_t)keys[first + half] < k) {
+            first += half + 1;
             len -= half + 1;
         } else {
             len = half;
         }
     }
-    off[k] = (uint32_t)lo;
+    if (k <= nkeys) off[k] = (uint32_t)first;
 }
 
 __global__ void k_fill_u32(uint32_t *p, uint32_t v, int64_t n) {

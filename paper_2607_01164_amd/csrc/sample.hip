@@ -36,12 +36,12 @@ constexpr float kNegHalfLog2e = -0.72134752044448170368f;
 constexpr int kSampWaves = 1;
 constexpr int kSampBlock = kSampWaves * kWave;
 
-// Q of a forward record at a point (fwd_q: Q = |U (p - mu)|^2).
-__device__ __forceinline__ float cutoff_q(const FwdRecord &r, float px, float py, float pz) {
-    return fwd_q(r, px, py, pz);
+// Q of a forward record at a point (record_q: Q = |U (p - mu)|^2).
+__device__ __forceinline__ float cutoff_q(const Record &r, float px, float py, float pz) {
+    return record_q(r, px, py, pz);
 }
 
-__device__ __forceinline__ void accumulate(const FwdRecord &r, float px, float py, float pz, float T, float &I,
+__device__ __forceinline__ void accumulate(const Record &r, float px, float py, float pz, float T, float &I,
                                            float &V) {
     const float Q = cutoff_q(r, px, py, pz);
     if (Q <= T) {
@@ -58,7 +58,7 @@ __device__ __forceinline__ void accumulate(const FwdRecord &r, float px, float p
 // the next 64 are fetched meanwhile, and every lane then reads each record
 // with the same address (a broadcast). One wait for memory per 64
 // candidates, instead of a dependent id and record load per candidate.
-__device__ __forceinline__ void walk_staged(const FwdRecord *__restrict__ rec, const uint32_t *__restrict__ gids,
+__device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
                                             uint32_t ja, uint32_t jb, uint32_t lane, float4 *buf, float px,
                                             float py, float pz, float T, float &I, float &V) {
     uint32_t gnext = 0;
@@ -66,7 +66,7 @@ __device__ __forceinline__ void walk_staged(const FwdRecord *__restrict__ rec, c
     for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
         const float4 *src = (const float4 *)(rec + gnext);
 #pragma unroll
-        for (int qq = 0; qq < kFwdQuads; ++qq)
+        for (int qq = 0; qq < kRecordQuads; ++qq)
             __builtin_amdgcn_global_load_lds((const void *)(src + qq),
                                              (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
         if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
@@ -75,7 +75,7 @@ __device__ __forceinline__ void walk_staged(const FwdRecord *__restrict__ rec, c
         const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
         uint32_t s = 0;
         for (; s + 2 <= cnt; s += 2) {
-            FwdRecord a, b;
+            Record a, b;
             a.f0 = buf[s];
             a.f1 = buf[kWave + s];
             a.f2 = buf[2 * kWave + s];
@@ -86,7 +86,7 @@ __device__ __forceinline__ void walk_staged(const FwdRecord *__restrict__ rec, c
             accumulate(b, px, py, pz, T, I, V);
         }
         if (s < cnt) {
-            FwdRecord a;
+            Record a;
             a.f0 = buf[s];
             a.f1 = buf[kWave + s];
             a.f2 = buf[2 * kWave + s];
@@ -101,7 +101,7 @@ __device__ __forceinline__ void walk_staged(const FwdRecord *__restrict__ rec, c
 // wave's LDS planes 64 records at a time as in walk_staged: each record
 // read there serves the lane's R queries.
 template <uint32_t R>
-__device__ __forceinline__ void walk_staged_r(const FwdRecord *__restrict__ rec, const uint32_t *__restrict__ gids,
+__device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
                                               uint32_t ja, uint32_t jb, uint32_t lane, float4 *buf,
                                               const float (&px)[R], const float (&py)[R], const float (&pz)[R],
                                               float T, float (&I)[R], float (&V)[R]) {
@@ -110,7 +110,7 @@ __device__ __forceinline__ void walk_staged_r(const FwdRecord *__restrict__ rec,
     for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
         const float4 *src = (const float4 *)(rec + gnext);
 #pragma unroll
-        for (int qq = 0; qq < kFwdQuads; ++qq)
+        for (int qq = 0; qq < kRecordQuads; ++qq)
             __builtin_amdgcn_global_load_lds((const void *)(src + qq),
                                              (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
         if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
@@ -118,7 +118,7 @@ __device__ __forceinline__ void walk_staged_r(const FwdRecord *__restrict__ rec,
         __builtin_amdgcn_wave_barrier();
         const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
         for (uint32_t s = 0; s < cnt; ++s) {
-            FwdRecord a;
+            Record a;
             a.f0 = buf[s];
             a.f1 = buf[kWave + s];
             a.f2 = buf[2 * kWave + s];
@@ -131,11 +131,11 @@ __device__ __forceinline__ void walk_staged_r(const FwdRecord *__restrict__ rec,
 }
 
 
-__global__ __launch_bounds__(kSampBlock) void k_sample_grid(QueryParams q, GridParams g, const FwdRecord *__restrict__ rec,
+__global__ __launch_bounds__(kSampBlock) void k_sample_grid(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                         const uint32_t *__restrict__ gids,
                                                         const uint32_t *__restrict__ cell_off, float T, float tau,
                                                         float *__restrict__ out_v, float *__restrict__ out_i) {
-    __shared__ float4 s_grec[kSampWaves][kFwdQuads * kWave];
+    __shared__ float4 s_grec[kSampWaves][kRecordQuads * kWave];
     const uint32_t rx = (uint32_t)(q.dims[0] / g.cells[0]);
     const uint32_t ry = (uint32_t)(q.dims[1] / g.cells[1]);
     const uint32_t rz = (uint32_t)(q.dims[2] / g.cells[2]);
@@ -293,7 +293,7 @@ __global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restr
     }
 }
 
-__device__ __forceinline__ float eval_a(const FwdRecord &r, float px, float py, float pz, float T) {
+__device__ __forceinline__ float eval_a(const Record &r, float px, float py, float pz, float T) {
     const float Q = cutoff_q(r, px, py, pz);
     return Q <= T ? r.f0.w * exp2_hw(Q * kNegHalfLog2e) : 0.0f;
 }
@@ -334,7 +334,7 @@ __device__ __forceinline__ float slot_sum(float x) {
 template <uint32_t ROWS>
 __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t pa, uint32_t ja, uint32_t jb,
                                            uint32_t c, uint32_t ncells, const QueryParams &q, const GridParams &g,
-                                           const FwdRecord *__restrict__ rec, const uint32_t *__restrict__ gids,
+                                           const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
                                            const uint32_t *__restrict__ order, float T, float tau,
                                            float *__restrict__ out_v, float *__restrict__ out_i,
                                            const PlanResults &pr, float4 *buf) {
@@ -370,7 +370,7 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
         for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
             const float4 *src = (const float4 *)(rec + gnext);
 #pragma unroll
-            for (int qq = 0; qq < kFwdQuads; ++qq)
+            for (int qq = 0; qq < kRecordQuads; ++qq)
                 __builtin_amdgcn_global_load_lds((const void *)(src + qq),
                                                  (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
             if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
@@ -380,7 +380,7 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
             const uint32_t nstep = left >= (uint32_t)kWave ? kWave / SL : (left + SL - 1) / SL;
             for (uint32_t st = 0; st < nstep; ++st) {
                 const uint32_t sidx = SL * st + sl;
-                FwdRecord r;
+                Record r;
                 r.f0 = buf[sidx];
                 r.f1 = buf[kWave + sidx];
                 r.f2 = buf[2 * kWave + sidx];
@@ -423,7 +423,7 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
 template <uint32_t R>
 __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t qn, uint32_t ja,
                                            uint32_t jb, uint32_t c, uint32_t ncells, const QueryParams &q,
-                                           const GridParams &g, const FwdRecord *__restrict__ rec,
+                                           const GridParams &g, const Record *__restrict__ rec,
                                            const uint32_t *__restrict__ gids, const uint32_t *__restrict__ order,
                                            float T, float tau, float *__restrict__ out_v, float *__restrict__ out_i,
                                            const PlanResults &pr, float4 *buf) {
@@ -460,7 +460,7 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
 // Every query's sums are reduced in a fixed order.
 // Seven waves per SIMD (at most 72 VGPRs, which the row layouts' per-row
 // arrays need; eight would spill them to scratch).
-__global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, GridParams g, const FwdRecord *__restrict__ rec,
+__global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                          const uint32_t *__restrict__ gids,
                                                          const uint32_t *__restrict__ cell_off,
                                                          const uint32_t *__restrict__ point_off,
@@ -471,7 +471,7 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
                                                          float *__restrict__ out_i, PlanResults pr) {
     // per wave: the records of 64 candidates, as three 1 KiB planes of
     // 16-byte quarters (quarter q of candidate s at [q][s])
-    __shared__ float4 s_rec[kSampWaves][kFwdQuads * kWave];
+    __shared__ float4 s_rec[kSampWaves][kRecordQuads * kWave];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t ncells = (uint32_t)g.ncells;
     const uint64_t w = (uint64_t)blockIdx.x * kSampWaves + threadIdx.x / kWave;
@@ -523,7 +523,7 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
         for (uint32_t t = 0; t < kChunkB; ++t) Ip[t] = Vp[t] = 0.0f;
         for (uint32_t j0 = ja; j0 < jb; j0 += kWave) {
             const uint32_t j = j0 + lane;
-            FwdRecord r;
+            Record r;
             if (j < jb) {
                 r = rec[gids[j]];
             } else {
@@ -561,7 +561,7 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
 // and totals[1] (passing) with one integer atomic each per block (the sums
 // do not depend on their order).
 __global__ __launch_bounds__(kBlock) void k_count_sample_pairs(QueryParams q, GridParams g,
-                                                               const FwdRecord *__restrict__ rec,
+                                                               const Record *__restrict__ rec,
                                                                const uint32_t *__restrict__ gids,
                                                                const uint32_t *__restrict__ cell_off,
                                                                const uint32_t *__restrict__ plan_keys,
@@ -618,7 +618,7 @@ __global__ __launch_bounds__(kBlock) void k_count_sample_pairs(QueryParams q, Gr
 
 }  // namespace
 
-hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const FwdRecord *rec,
+hipError_t launch_count_sample_pairs(const QueryParams &q, const GridParams &g, const Record *rec,
                                      const uint32_t *gids, const uint32_t *cell_off, const uint32_t *plan_keys,
                                      const float4 *plan_pos, float T, unsigned long long *totals, hipStream_t s) {
     hipError_t e = fill_u32((uint32_t *)totals, 0u, 4, s);
@@ -638,7 +638,7 @@ hipError_t launch_query_keys(const QueryParams &q, const GridParams &g, uint32_t
     return hipGetLastError();
 }
 
-hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const uint32_t *gids,
+hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                               const uint32_t *cell_off, float T, float tau, float *out_v, float *out_i,
                               hipStream_t s) {
     const int64_t vpc = (int64_t)(q.dims[0] / g.cells[0]) * (q.dims[1] / g.cells[1]) * (q.dims[2] / g.cells[2]);
@@ -653,7 +653,7 @@ hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const F
     return hipGetLastError();
 }
 
-hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const FwdRecord *rec, const uint32_t *gids,
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                                 const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
                                 const PlanResults &pr, hipStream_t s) {

@@ -126,12 +126,10 @@ class Run:
 
 def gpu_boxes(index, n: int) -> np.ndarray:
     """The float32 cell boxes the GPU preprocess wrote, read back from the
-    index workspace (the library's layout: a 64-byte record per Gaussian,
-    then at the next 256-byte boundary a 32-byte box per Gaussian,
-    (x0, y0, z0, flag) and (x1, y1, z1, 0), empty when x1 < x0), as
-    [n, 6] = (x0, y0, z0, x1, y1, z1) with -1 for empty boxes."""
-    off = (64 * max(n, 1) + 255) // 256 * 256
-    raw = index.work[off: off + 32 * n].cpu().numpy().view(np.int32).reshape(n, 8)
+    index workspace (the library's layout: at its start a 32-byte box per
+    Gaussian, (x0, y0, z0, flag) and (x1, y1, z1, 0), empty when x1 < x0),
+    as [n, 6] = (x0, y0, z0, x1, y1, z1) with -1 for empty boxes."""
+    raw = index.work[0: 32 * n].cpu().numpy().view(np.int32).reshape(n, 8)
     box = np.concatenate([raw[:, 0:3], raw[:, 4:7]], axis=1)
     box[raw[:, 4] < raw[:, 0]] = -1
     return box
