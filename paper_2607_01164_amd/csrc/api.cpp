@@ -298,7 +298,8 @@ bool gauss_valid(const gs_gaussians *g, std::string *why) {
 
 bool aligned(const void *p) { return ((uintptr_t)p % kAlign) == 0; }
 
-float cutoff_T(float tau) { return (float)(2.0 * std::log(1.0 / (double)tau)); }
+// The cutoff on the records' Q' = Q log2(e) / 2: G >= tau reads Q' <= log2(1/tau).
+float cutoff_T(float tau) { return (float)std::log2(1.0 / (double)tau); }
 float index_radius(float tau) {
     const double rc = std::sqrt(2.0 * std::log(1.0 / (double)tau));
     return (float)(rc * (1.0 + 1.0 / 1024.0));

@@ -24,12 +24,13 @@
 // region and find its points in L2.
 //
 // Per pair the partials are kept as 11 moments in the frame of the
-// record's triangular factor, u = U (p - mu) with U^T U = R S^-2 R^T, and
-// c = dL/dQ = -1/2 a dL/da:
+// record's triangular factor, u = U (p - mu) with U^T U = k^2 R S^-2 R^T
+// (k^2 = log2(e) / 2), and c = dL/dQ = -1/2 a dL/da:
 //   m1 = sum c u (3), m2 = sum c u u^T (6), dv = sum dL/dPhi a / I,
 //   dw = sum dL/da G.
-// A finalize kernel rotates them into the frame of M = S^-1 R^T (O = M U^-1
-// is orthogonal) and turns them into dL/dmu = -2 M^T m1,
+// A finalize kernel rotates them into the frame of M = S^-1 R^T (O = k M
+// U^-1 is orthogonal, u / k = O^T M (p - mu)) and turns them into
+// dL/dmu = -2 M^T m1,
 // dL/ds_k = -2 m2_kk / s_k, dL/dR_jk = (2 / s_k) sum_m R_jm s_m m2_mk, and
 // through R(qhat) and qhat = q / |q| into dL/dq.
 // For a defined query with outputs (Phi, I) and cotangents (gPhi, gI):
@@ -43,7 +44,6 @@ namespace gs {
 
 namespace {
 
-constexpr float kNegHalfLog2e = -0.72134752044448170368f;
 
 __device__ __forceinline__ void alpha_beta(float phi, float inf, float gp, float gi, float &al, float &be) {
     // the forward writes I > tau > 0 at defined points and exactly 0 elsewhere
@@ -108,8 +108,8 @@ struct Acc {
     float dv, dw;
 };
 
-// Whitened offset u = U (p - mu) and Q = |u|^2, the exponent of paper Eq. 3
-// (U the Cholesky factor of the inverse covariance, as the forward uses).
+// Whitened offset u = U (p - mu) with the record's U and Q' = |u|^2 =
+// Q log2(e) / 2, Q the exponent of paper Eq. 3, as the forward forms it.
 __device__ __forceinline__ float whiten(const Record &r, float px, float py, float pz, float &u0, float &u1,
                                         float &u2) {
     const float dx = px - r.f0.x, dy = py - r.f0.y, dz = pz - r.f0.z;
@@ -119,11 +119,11 @@ __device__ __forceinline__ float whiten(const Record &r, float px, float py, flo
     return fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
 }
 
-// Partials of one contributing pair (Q <= T), given u, Q and the query's
-// alpha, beta.
+// Partials of one contributing pair (Q' <= T'), given u, Q' and the
+// query's alpha, beta.
 __device__ __forceinline__ void pair_grad(const Record &r, float u0, float u1, float u2, float Q, float al, float be,
                                           Acc &acc) {
-    const float G = exp2_hw(Q * kNegHalfLog2e);
+    const float G = exp2_hw(-Q);  // Q is Q' = Q log2(e) / 2
     const float a = r.f0.w * G;
     const float dLda = fmaf_(al, r.f1.w, be);
     acc.dv = fmaf_(al, a, acc.dv);
@@ -569,8 +569,10 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
     if (i >= n) return;
     const float *m = moments + (size_t)i * 12;
     const float4 ma = *(const float4 *)m, mb = *(const float4 *)(m + 4), mc = *(const float4 *)(m + 8);
-    const double m1p[3] = {ma.x, ma.y, ma.z};
-    const double m2s[6] = {ma.w, mb.x, mb.y, mb.z, mb.w, mc.x};
+    // moments of u / k, the unscaled factor's frame
+    constexpr double ik = 1.0 / kRecScale, ik2 = ik * ik;
+    const double m1p[3] = {ma.x * ik, ma.y * ik, ma.z * ik};
+    const double m2s[6] = {ma.w * ik2, mb.x * ik2, mb.y * ik2, mb.z * ik2, mb.w * ik2, mc.x * ik2};
     const bool any = ma.x != 0.0f || ma.y != 0.0f || ma.z != 0.0f || ma.w != 0.0f || mb.x != 0.0f ||
                      mb.y != 0.0f || mb.z != 0.0f || mb.w != 0.0f || mc.x != 0.0f || mc.y != 0.0f || mc.z != 0.0f;
     // the parameters are loaded with the moments, whatever these hold
@@ -592,10 +594,11 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
         R[2][0] = 2.0 * (x * z - w * y);
         R[2][1] = 2.0 * (y * z + w * x);
         R[2][2] = 1.0 - 2.0 * (x * x + y * y);
-        // The moments come in the frame of u' = U d (U upper triangular,
-        // U^T U = M^T M with M = S^-1 R^T, the factor the samplers use).
-        // O = M U^-1 is orthogonal and u = M d = O u', so the moments in the
-        // frame of M are m1 = O m1' and m2 = O m2' O^T.
+        // Scaled back by 1/k above, the moments are in the frame of u' = U d
+        // for U upper triangular with U^T U = M^T M, M = S^-1 R^T (the
+        // record's factor over k). O = M U^-1 is orthogonal and u = M d =
+        // O u', so the moments in the frame of M are m1 = O m1' and
+        // m2 = O m2' O^T.
         double Mm[3][3], A[3][3];
         for (int k = 0; k < 3; ++k)
             for (int j = 0; j < 3; ++j) Mm[k][j] = R[j][k] * is[k];

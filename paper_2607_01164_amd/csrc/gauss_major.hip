@@ -26,11 +26,10 @@
 namespace gs {
 namespace {
 
-constexpr float kNegHalfLog2eG = -0.72134752044448170368f;  // -1/2 log2(e)
 
 __device__ __forceinline__ float eval_pair(const Record &r, float4 p, float T) {
     const float Q = record_q(r, p.x, p.y, p.z);
-    return Q <= T ? r.f0.w * exp2_hw(Q * kNegHalfLog2eG) : 0.0f;
+    return Q <= T ? r.f0.w * exp2_hw(-Q) : 0.0f;
 }
 
 // Position of every query in plan order (the walk below reads them

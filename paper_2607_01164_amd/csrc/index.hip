@@ -356,7 +356,7 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
     box[i] = b;
 
     // evaluation record: the Cholesky factor of the inverse covariance,
-    // formed in float64 and rounded once to float32
+    // formed in float64, scaled by kRecScale and rounded once to float32
     if (valid) {
         const double qn = sqrt((double)q[0] * q[0] + (double)q[1] * q[1] + (double)q[2] * q[2] + (double)q[3] * q[3]);
         const double iq = 1.0 / qn;
@@ -390,8 +390,8 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
         const double u22 = sqrt(A[2][2] - u02 * u02 - u12 * u12);
         Record f;
         f.f0 = make_float4(mu[0], mu[1], mu[2], w);
-        f.f1 = make_float4((float)u00, (float)u01, (float)u02, v);
-        f.f2 = make_float4((float)u11, (float)u12, (float)u22, 0.0f);
+        f.f1 = make_float4((float)(kRecScale * u00), (float)(kRecScale * u01), (float)(kRecScale * u02), v);
+        f.f2 = make_float4((float)(kRecScale * u11), (float)(kRecScale * u12), (float)(kRecScale * u22), 0.0f);
         rec[i] = f;
     } else {
         Record f;

@@ -15,20 +15,25 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 
 // Per-Gaussian evaluation record, 48 bytes, written by the preprocess:
 //   f0 = (mu_x, mu_y, mu_z, w)
-//   f1 = (U00, U01, U02, v)      U upper triangular with U^T U = R S^-2 R^T,
-//   f2 = (U11, U12, U22, 0)      the inverse covariance, so Q = |U (p - mu)|^2
-// U (the Cholesky factor of the inverse covariance) takes 6 products and
-// sums where M = S^-1 R^T takes 9, and three 16-byte quarters where M takes
-// four; its float32 rounding bounds Q as M's does (U and M have the same
-// 2-norm). Formed in float64 and rounded once. Invalid Gaussians get zeros,
+//   f1 = (U00, U01, U02, v)      U = kRecScale L, L upper triangular with
+//   f2 = (U11, U12, U22, 0)      L^T L = R S^-2 R^T (the inverse covariance)
+// so that |U (p - mu)|^2 = Q' = Q log2(e) / 2 and G = exp(-Q/2) = 2^-Q'; the
+// cutoff G >= tau reads Q' <= log2(1/tau) (record_T). L, the Cholesky
+// factor of the inverse covariance, takes 6 products and sums where
+// M = S^-1 R^T takes 9, and three 16-byte quarters where M takes four; its
+// float32 rounding bounds Q as M's does (L and M have the same 2-norm).
+// Formed in float64, scaled, and rounded once. Invalid Gaussians get zeros,
 // an empty box, and appear in no cell list.
 struct alignas(16) Record {
     float4 f0, f1, f2;
 };
 constexpr int kRecordQuads = 3;  // 16-byte quarters of a Record
 
-// Q = |U (p - mu)|^2 in the one order of float32 operations every forward
-// sampler and the pair counter use.
+// sqrt(log2(e) / 2), the factor of the record's U
+constexpr double kRecScale = 0.84932180028801904272;
+
+// Q' = |U (p - mu)|^2 = Q log2(e) / 2 in the one order of float32
+// operations every forward sampler and the pair counter use.
 __device__ __forceinline__ float record_q(const Record &r, float px, float py, float pz) {
     const float dx = px - r.f0.x, dy = py - r.f0.y, dz = pz - r.f0.z;
     const float u0 = __builtin_fmaf(r.f1.x, dx, __builtin_fmaf(r.f1.y, dy, r.f1.z * dz));

@@ -21,8 +21,6 @@ namespace gs {
 
 namespace {
 
-// -1/2 log2(e): G = exp(-Q/2) = 2^(Q * kNegHalfLog2e)
-constexpr float kNegHalfLog2e = -0.72134752044448170368f;
 
 // The samplers run one wave per workgroup. Their waves are independent
 // (each has its own LDS buffer) and the cost of a work item varies by
@@ -36,7 +34,7 @@ constexpr float kNegHalfLog2e = -0.72134752044448170368f;
 constexpr int kSampWaves = 1;
 constexpr int kSampBlock = kSampWaves * kWave;
 
-// Q of a forward record at a point (record_q: Q = |U (p - mu)|^2).
+// Q' = Q log2(e) / 2 of a record at a point (record_q), G = 2^-Q'.
 __device__ __forceinline__ float cutoff_q(const Record &r, float px, float py, float pz) {
     return record_q(r, px, py, pz);
 }
@@ -45,10 +43,21 @@ __device__ __forceinline__ void accumulate(const Record &r, float px, float py, 
                                            float &V) {
     const float Q = cutoff_q(r, px, py, pz);
     if (Q <= T) {
-        const float a = r.f0.w * exp2_hw(Q * kNegHalfLog2e);
+        const float a = r.f0.w * exp2_hw(-Q);
         I += a;
         V = fmaf_(a, r.f1.w, V);
     }
+}
+
+// The same sums without a branch: a is selected (0 past the cutoff) and
+// always added, so that a lane's R queries cost one select each (adding 0
+// leaves I and V as they are: both start at +0 and w, v are finite).
+__device__ __forceinline__ void accumulate_sel(const Record &r, float px, float py, float pz, float T, float &I,
+                                               float &V) {
+    const float Q = cutoff_q(r, px, py, pz);
+    const float a = Q <= T ? r.f0.w * exp2_hw(-Q) : 0.0f;
+    I += a;
+    V = fmaf_(a, r.f1.w, V);
 }
 
 // Walk a wave-uniform candidate list [ja, jb) for one query per lane. The
@@ -123,7 +132,7 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
             a.f1 = buf[kWave + s];
             a.f2 = buf[2 * kWave + s];
 #pragma unroll
-            for (uint32_t t = 0; t < R; ++t) accumulate(a, px[t], py[t], pz[t], T, I[t], V[t]);
+            for (uint32_t t = 0; t < R; ++t) accumulate_sel(a, px[t], py[t], pz[t], T, I[t], V[t]);
         }
         // every lane has read the planes before the next chunk overwrites them
         __builtin_amdgcn_wave_barrier();
@@ -295,7 +304,7 @@ __global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restr
 
 __device__ __forceinline__ float eval_a(const Record &r, float px, float py, float pz, float T) {
     const float Q = cutoff_q(r, px, py, pz);
-    return Q <= T ? r.f0.w * exp2_hw(Q * kNegHalfLog2e) : 0.0f;
+    return Q <= T ? r.f0.w * exp2_hw(-Q) : 0.0f;
 }
 
 // sum over the 64 lanes, returned to every lane
