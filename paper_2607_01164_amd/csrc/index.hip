@@ -473,21 +473,31 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
         if (b.hi.x < b.lo.x || base >= (int64_t)tile_cnt) continue;
         const uint64_t gbits = fold ? (uint64_t)(gg - gfirst) << 32 : 0ull;
         const int64_t nx = b.hi.x - b.lo.x + 1, ny = b.hi.y - b.lo.y + 1, nz = b.hi.z - b.lo.z + 1;
+        // rows (y, z) are walked with counters; a row's first cell key is
+        // the key of the box corner plus its offsets (keys fit 32 bits)
+        const uint32_t kcorner = (uint32_t)(b.lo.x + Cx * (b.lo.y + Cy * b.lo.z));
+        const uint32_t kdz = (uint32_t)(Cx * Cy);
         if (b.lo.w) {
             const uint32_t words[16] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w,
                                         c2.x, c2.y, c2.z, c2.w, c3.x, c3.y, c3.z, c3.w};
             const uint32_t nrows = (uint32_t)(ny * nz);
             int64_t start = base;
+            uint32_t yy = 0, krow = kcorner;  // krow: the key of the row's first box cell
             for (uint32_t r = 0; r < nrows && start < (int64_t)tile_cnt; ++r) {
                 const uint32_t code = (words[r >> 2] >> (8 * (r & 3))) & 0xFFu;
                 const uint32_t len = span_len(code);
                 if (len > 0 && start + len > 0) {
                     const int64_t p = start > 0 ? start : 0;
-                    const int64_t cy = b.lo.y + (int64_t)(r % (uint32_t)ny), cz = b.lo.z + (int64_t)(r / (uint32_t)ny);
-                    const int64_t kp = b.lo.x + (int64_t)span_first(code) + (p - start) + Cx * (cy + Cy * cz);
-                    mark[p] = ((uint64_t)(p + 1) << 52) | gbits | (uint64_t)(uint32_t)kp;
+                    const uint32_t kp = krow + span_first(code) + (uint32_t)(p - start);
+                    mark[p] = ((uint64_t)(p + 1) << 52) | gbits | (uint64_t)kp;
                 }
                 start += len;
+                if (++yy == (uint32_t)ny) {
+                    yy = 0;
+                    krow += kdz - (uint32_t)(Cx * (ny - 1));
+                } else {
+                    krow += (uint32_t)Cx;
+                }
             }
         } else {
             // whole rows of nx cells: only those reaching into the tile
@@ -495,12 +505,19 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
             const int64_t r0 = base < 0 ? (-base) / nx : 0;
             int64_t r1 = ((int64_t)tile_cnt - base + nx - 1) / nx;
             r1 = r1 < R ? r1 : R;
+            uint32_t yy = (uint32_t)(r0 % ny);
+            uint32_t krow = kcorner + (uint32_t)Cx * yy + kdz * (uint32_t)(r0 / ny);
             for (int64_t r = r0; r < r1; ++r) {
                 const int64_t start = base + r * nx;
                 const int64_t p = start > 0 ? start : 0;
-                const int64_t cy = b.lo.y + r % ny, cz = b.lo.z + r / ny;
-                const int64_t kp = b.lo.x + (p - start) + Cx * (cy + Cy * cz);
-                mark[p] = ((uint64_t)(p + 1) << 52) | gbits | (uint64_t)(uint32_t)kp;
+                const uint32_t kp = krow + (uint32_t)(p - start);
+                mark[p] = ((uint64_t)(p + 1) << 52) | gbits | (uint64_t)kp;
+                if (++yy == (uint32_t)ny) {
+                    yy = 0;
+                    krow += kdz - (uint32_t)(Cx * (ny - 1));
+                } else {
+                    krow += (uint32_t)Cx;
+                }
             }
         }
     }
