@@ -8,7 +8,10 @@
 
 namespace gs {
 
-constexpr int kExpandItems = 8;
+#ifndef GS_SORT_ITEMS
+#define GS_SORT_ITEMS 8
+#endif
+constexpr int kExpandItems = GS_SORT_ITEMS;
 constexpr int kExpandTile = kBlock * kExpandItems;  // 2048 elements per workgroup
 
 // largest g in [0, n) with off[g] <= x (requires off[0] = 0 <= x)

@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     // output start of every digit in this tile: the exclusive scan of the
     // digit totals plus the tile's place in its digit's row (all loads are
     // issued before the first wait)
-    constexpr int J = kMaxDigits / kBlock;
+    constexpr int J = kMaxDigits > kBlock ? kMaxDigits / kBlock : 1;
     uint32_t loc[J], tpre[J];
 #pragma unroll
     for (int j = 0; j < J; ++j) {

@@ -9,9 +9,17 @@
 
 namespace gs {
 
-constexpr int kSortItems = 8;
+// Build-time tunables: keys per thread of a sort tile (the emit's tile
+// follows) and the widest digit of a pass.
+#ifndef GS_SORT_ITEMS
+#define GS_SORT_ITEMS 8
+#endif
+#ifndef GS_RADIX_BITS
+#define GS_RADIX_BITS 10
+#endif
+constexpr int kSortItems = GS_SORT_ITEMS;
 constexpr int kSortTile = kBlock * kSortItems;  // 2048
-constexpr int kMaxDigitBits = 10;
+constexpr int kMaxDigitBits = GS_RADIX_BITS;
 constexpr int kMaxDigits = 1 << kMaxDigitBits;
 static_assert(kSortTile == kExpandTile, "emit tiles are sort tiles");
 
