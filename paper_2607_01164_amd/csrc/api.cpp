@@ -204,8 +204,8 @@ Plan plan_layout(void *base, int64_t n, int64_t ncells) {
     p.items.item_off = c.take<uint32_t>((size_t)ncells + 2);
     p.items.max_items = ncells + 1 + (n > 0 ? n : 0) / 64 + 1;
     p.items.items = c.take<uint32_t>((size_t)p.items.max_items);
-    p.items.group_sum = c.take<uint32_t>((size_t)item_groups(ncells + 1));
-    p.items.scan_work = c.take<char>(scan_work_bytes(item_groups(ncells + 1), 4));
+    p.items.group_sum = c.take<uint64_t>((size_t)item_groups(ncells + 1) + 1);
+    p.items.scan_work = c.take<char>(scan_work_bytes(item_groups(ncells + 1), 8));
     // 64 spare entries: the backward's lanes past a Gaussian's last point
     // read up to 63 entries beyond the last row of the plan
     p.res.pos = c.take<float4>(m + kWave);

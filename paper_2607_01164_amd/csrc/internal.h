@@ -370,7 +370,7 @@ struct PointItems {
     uint32_t *item_off;   // [ncells + 2]
     uint32_t *items;      // [max_items]
     int64_t max_items;    // ncells + 1 + n / 64 + 1
-    uint32_t *group_sum;  // [item_groups(ncells + 1)] work items per 1024 buckets
+    uint64_t *group_sum;  // [item_groups(ncells + 1) + 1] work items per 1024 buckets, (dense << 32) | sparse
     void *scan_work;      // scan of group_sum
 };
 // groups of 1024 buckets (plus the element after the last bucket)

@@ -237,67 +237,86 @@ constexpr uint32_t kRowsMax = (kDenseMin + 3) / 4;  // queries per row at most
 
 // Work items per bucket (cell, and the outside bucket last): none for an
 // empty bucket, one for a sparse one, one per kDenseItem queries of a dense
-// one.
-__device__ __forceinline__ uint32_t bucket_items(const uint32_t *point_off, int64_t c, int64_t nbuckets) {
-    if (c >= nbuckets) return 0u;
+// one. Dense buckets' items come first in the item list, then the sparse
+// buckets', each class in bucket order: items are taken in launch order,
+// and the long ones started first leave no long item running alone at the
+// end of the launch. The counts travel packed as (dense << 32) | sparse.
+__device__ __forceinline__ uint64_t bucket_items(const uint32_t *point_off, int64_t c, int64_t nbuckets) {
+    if (c >= nbuckets) return 0ull;
     // the outside bucket (c = nbuckets - 1) has a single key
     const uint32_t n = point_off[c + 1 < nbuckets ? kSub * (c + 1) : kSub * c + 1] - point_off[kSub * c];
-    return n == 0 ? 0u : (n < 2 * kDenseMin ? 1u : (n + kDenseItem - 1) / kDenseItem);
+    if (n == 0) return 0ull;
+    if (n < 2 * kDenseMin) return 1ull;
+    return (uint64_t)((n + kDenseItem - 1) / kDenseItem) << 32;
 }
 
 // Buckets are taken kItemGroup at a time (kItemsPerThread per thread).
 constexpr int kItemsPerThread = 4;
 constexpr int kItemGroup = kBlock * kItemsPerThread;  // 1024
-// Up to this many groups, the offsets kernel sums the earlier groups itself;
-// beyond, their sums are scanned by a separate pass.
+// Up to this many groups, the offsets kernel sums the other groups itself;
+// beyond, their sums are scanned by a separate pass (which also writes the
+// total after them).
 constexpr int64_t kInlineGroups = 1024;
 
 __global__ __launch_bounds__(kBlock) void k_item_sums(const uint32_t *__restrict__ point_off, int64_t nbuckets,
-                                                      uint32_t *__restrict__ group_sum) {
-    __shared__ uint32_t lds[kWavesPerBlock];
+                                                      uint64_t *__restrict__ group_sum) {
+    __shared__ uint64_t lds[kWavesPerBlock];
     const int64_t base = (int64_t)blockIdx.x * kItemGroup + (int64_t)threadIdx.x * kItemsPerThread;
-    uint32_t s = 0;
+    uint64_t s = 0;
 #pragma unroll
     for (int i = 0; i < kItemsPerThread; ++i) s += bucket_items(point_off, base + i, nbuckets);
-    uint32_t tot;
+    uint64_t tot;
     (void)block_excl_scan(s, lds, &tot);
     if (threadIdx.x == 0) group_sum[blockIdx.x] = tot;
 }
 
-// item_off[c] for c <= nbuckets (item_off[nbuckets] = the total) and the
-// item list: item_off[c] .. item_off[c] + items(c) - 1 name bucket c.
-// group_sum: the groups' sums, or (scanned) their exclusive prefixes.
+// item_off[c] for c <= nbuckets: the first item of bucket c (item_off[nbuckets]
+// = the total), and the item list: item_off[c] .. item_off[c] + items(c) - 1
+// name bucket c. group_sum: the groups' sums, or (scanned) their exclusive
+// prefixes followed by the total.
 __global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restrict__ point_off, int64_t nbuckets,
-                                                         const uint32_t *__restrict__ group_sum, bool scanned,
-                                                         uint32_t *__restrict__ item_off, uint32_t *__restrict__ items,
-                                                         int64_t max_items) {
-    __shared__ uint32_t lds[kWavesPerBlock];
-    uint32_t prefix;
+                                                         const uint64_t *__restrict__ group_sum, int64_t ngroups,
+                                                         bool scanned, uint32_t *__restrict__ item_off,
+                                                         uint32_t *__restrict__ items, int64_t max_items) {
+    __shared__ uint64_t lds[kWavesPerBlock];
+    uint64_t prefix, total;
     if (scanned) {
         prefix = group_sum[blockIdx.x];
+        total = group_sum[ngroups];
     } else {
-        uint32_t p = 0;
-        for (uint32_t j = threadIdx.x; j < blockIdx.x; j += kBlock) p += group_sum[j];
-        uint32_t tot;
-        (void)block_excl_scan(p, lds, &tot);
-        prefix = tot;
+        uint64_t p = 0, a = 0;
+        for (uint32_t j = threadIdx.x; j < (uint32_t)ngroups; j += kBlock) {
+            const uint64_t v = group_sum[j];
+            a += v;
+            if (j < blockIdx.x) p += v;
+        }
+        uint64_t t;
+        (void)block_excl_scan(p, lds, &t);
+        prefix = t;
+        (void)block_excl_scan(a, lds, &t);
+        total = t;
     }
+    const uint32_t dense_total = (uint32_t)(total >> 32);
     const int64_t base = (int64_t)blockIdx.x * kItemGroup + (int64_t)threadIdx.x * kItemsPerThread;
-    uint32_t v[kItemsPerThread];
-    uint32_t s = 0;
+    uint64_t v[kItemsPerThread];
+    uint64_t s = 0;
 #pragma unroll
     for (int i = 0; i < kItemsPerThread; ++i) {
         v[i] = bucket_items(point_off, base + i, nbuckets);
         s += v[i];
     }
-    uint32_t tot;
-    uint32_t run = block_excl_scan(s, lds, &tot) + prefix;
+    uint64_t tot;
+    uint64_t run = block_excl_scan(s, lds, &tot) + prefix;
 #pragma unroll
     for (int i = 0; i < kItemsPerThread; ++i) {
         const int64_t c = base + i;
-        if (c <= nbuckets) item_off[c] = run;
-        for (uint32_t k = 0; k < v[i]; ++k)
-            if ((int64_t)(run + k) < max_items) items[run + k] = (uint32_t)c;
+        const bool dense = (v[i] >> 32) != 0;
+        const uint32_t first = dense ? (uint32_t)(run >> 32) : dense_total + (uint32_t)run;
+        const uint32_t cnt = dense ? (uint32_t)(v[i] >> 32) : (uint32_t)v[i];
+        if (c < nbuckets) item_off[c] = first;
+        if (c == nbuckets) item_off[c] = dense_total + (uint32_t)total;
+        for (uint32_t k = 0; k < cnt; ++k)
+            if ((int64_t)(first + k) < max_items) items[first + k] = (uint32_t)c;
         run += v[i];
     }
 }
@@ -674,10 +693,11 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
     prof_begin("cell_items", s);
     hipLaunchKernelGGL(k_item_sums, dim3((uint32_t)ngroups), dim3(kBlock), 0, s, point_off, nbuckets, it.group_sum);
     hipError_t e = hipGetLastError();
-    if (e == hipSuccess && scanned) e = exclusive_scan_u32(it.group_sum, it.group_sum, ngroups, it.scan_work, s);
+    if (e == hipSuccess && scanned)
+        e = exclusive_scan_u64_total(it.group_sum, it.group_sum, ngroups, it.group_sum + ngroups, it.scan_work, s);
     if (e == hipSuccess) {
         hipLaunchKernelGGL(k_item_offsets, dim3((uint32_t)ngroups), dim3(kBlock), 0, s, point_off, nbuckets,
-                           it.group_sum, scanned, it.item_off, it.items, it.max_items);
+                           it.group_sum, ngroups, scanned, it.item_off, it.items, it.max_items);
         e = hipGetLastError();
     }
     prof_end("cell_items", s);
