@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_VEC_PEAK_TFLOPS = 157.3   # MI355X vector FP32: 256 CUs x 2.4 GHz x 128 lanes x 2 (packed FMA)
 # Algorithmic work of the samplers: a (Gaussian, point) pair that fails the
-# cutoff costs the test itself, d = p - mu, u = M d, Q = |u|^2 and the
+# cutoff costs the test itself, d = p - mu, u = U d, Q = |u|^2 and the
 # compare, counted as 16 operations; a contributing pair costs 30 flops and
 # one exponential in the forward (the test, a = w exp(-Q/2), I += a,
 # V += a v) and 60 flops and one exponential in the backward (the test, a,
