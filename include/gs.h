@@ -132,7 +132,8 @@ typedef struct gs_query {
 int64_t gs_query_size(const gs_query *query);
 
 /* Bytes of index workspace for n_gauss Gaussians, a grid and a pair
- * capacity (per-Gaussian records and boxes, scan and sort buffers). */
+ * capacity (per-Gaussian records, boxes and row runs, row records of the
+ * large boxes (one per pair of capacity), scan and sort buffers). */
 size_t gs_index_work_bytes(int64_t n_gauss, const gs_grid *grid, int64_t capacity);
 
 /*
@@ -143,14 +144,19 @@ size_t gs_index_work_bytes(int64_t n_gauss, const gs_grid *grid, int64_t capacit
  * Boxes are computed in float32 in one fixed order of operations, so the
  * index is reproducible bit for bit. The half-extent along axis j is
  * r * sqrt(Sigma_jj) with r = sqrt(2 ln(1/tau)) (1 + 2^-10). A box of at
- * most 64 (y, z) rows of at most 16 cells lists, in each row, only the run
- * of cells that the enlarged ellipsoid Q <= r^2 can reach over the row's
- * (y, z) slab, bounded in float64: x conditioned on (y, z) is centred on a
- * line through the mean with half-width sqrt((r^2 - Q2) vc), Q2 the (y, z)
- * marginal's quadratic form and vc the conditional variance; the run covers
+ * most 4096 (y, z) rows lists, in each row, only the run of cells that the
+ * enlarged ellipsoid Q <= r^2 can reach over the row's (y, z) slab, bounded
+ * in float64: x conditioned on (y, z) is centred on a line through the mean
+ * with half-width sqrt((r^2 - Q2) vc), Q2 the (y, z) marginal's quadratic
+ * form and vc the conditional variance; the run covers
  * [min centre - wm, max centre + wm] over the slab's corners, with
  * wm = sqrt((r^2 - min Q2) vc), and is empty when min Q2 > r^2. Every cell
- * holding a point with Q <= 2 ln(1/tau) is still listed.
+ * holding a point with Q <= 2 ln(1/tau) is still listed. Boxes of more than
+ * 64 rows or 16 cells a row keep one record per row with cells in the
+ * workspace, taken from room for `capacity` records in stretches of the
+ * box's row count; a box that finds no room lists every cell of its box.
+ * With a capacity of at least the rows of those boxes, the index (and with
+ * it every result) is reproducible bit for bit.
  * Waits on the stream once, for the pair count. If it exceeds the capacity,
  * returns GS_ERR_CAPACITY with index->n_pairs set to the count needed and the
  * index left unusable.
@@ -188,7 +194,8 @@ size_t gs_sample_gaussian_major_work_bytes(const gs_query *query);
  * B), a variant of gs_sample for VOXELS, POINTS and JITTER queries kept for
  * comparing the two ways of pairing Gaussians with points. The queries are
  * ordered by cell as gs_sample orders them; then one wavefront per Gaussian
- * walks the points of its box (its row spans where trimmed), tests each
+ * walks the points of its box (each row of cells cut to the quarters of
+ * cells the Gaussian's cutoff, enlarged by 2^-7, can reach), tests each
  * against the cutoff and adds w G and w v G to that point's float64 sums
  * with atomic adds; a last pass writes (Phi, I) = (V/I, I) where I > tau
  * and the point lies in the box, (0, 0) elsewhere. The outputs equal

@@ -18,8 +18,8 @@ namespace gs {
 hipError_t launch_loss(int64_t n, const float *value, const float *influence, const float *target,
                        const uint8_t *defined, float tau, float eps, float lambda_fn, float lambda_fp,
                        float *grad_value, float *grad_influence, gs_loss_terms *terms, void *work, hipStream_t s);
-hipError_t launch_sample_gauss_major(const QueryParams &q, const GridParams &g, const Record *rec,
-                                     const CellBox *box, const uint8_t *spans, const uint32_t *gorder,
+hipError_t launch_sample_gauss_major(const QueryParams &q, const GridParams &g, const BwdGeom &bg, const Record *rec,
+                                     const CellBox *box, const uint32_t *gorder,
                                      int64_t n_gauss, const uint32_t *order, const uint32_t *point_off, float T,
                                      float tau, float *out_v, float *out_i, const PlanResults &pr, void *work,
                                      hipStream_t s);
@@ -132,7 +132,9 @@ int gauss_order_bits(const gs_grid *g) { return gauss_order_full_bits(g) - gauss
 struct IndexWork {
     CellBox *box;        // [n] cell boxes (first: the tests read them back)
     Record *rec;         // [n] evaluation records
-    uint8_t *spans;      // [n][kSpanStride] row spans and quarter codes of trimmed boxes
+    uint8_t *lines;      // [n][kLineRows] row-run bytes of the trim-1 boxes
+    uint32_t *rbase;     // [n] first row record of each trim-2 box
+    uint32_t *rtotal;    // row records taken so far (one word)
     uint32_t *gorder;    // [n] Gaussians in spatial order
     uint32_t *gkeys;     // [n] their sort keys
     uint32_t *gsort_k;   // [n] sort scratch
@@ -144,6 +146,7 @@ struct IndexWork {
     uint32_t *tile_first;  // [pair tiles] first Gaussian of every emit tile
     uint32_t *keys_alt;
     uint32_t *gids_alt;
+    RowRec *rows;        // [capacity] row records of the trim-2 boxes (each row has a pair)
     void *radix_work;
     size_t bytes;
 };
@@ -160,7 +163,9 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     const size_t n1 = (size_t)(n > 0 ? n : 1);
     w.box = c.take<CellBox>(n1);
     w.rec = c.take<Record>(n1);
-    w.spans = c.take<uint8_t>(n1 * kSpanStride);
+    w.lines = c.take<uint8_t>(n1 * kLineRows);
+    w.rbase = c.take<uint32_t>(n1);
+    w.rtotal = c.take<uint32_t>(4);
     w.gorder = c.take<uint32_t>(n1);
     w.gkeys = c.take<uint32_t>(n1);
     w.gsort_k = c.take<uint32_t>(n1);
@@ -173,6 +178,7 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     const int64_t cap = capacity > 0 ? capacity : 1;
     w.keys_alt = c.take<uint32_t>((size_t)cap);
     w.gids_alt = c.take<uint32_t>((size_t)cap);
+    w.rows = c.take<RowRec>((size_t)cap);
     w.radix_work = c.take<char>(radix_work_bytes(cap, bits_for(ncells_of(g))));
     w.bytes = c.off;
     return w;
@@ -566,7 +572,8 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     IndexWork w = index_layout(index->work, n, grid, index->capacity);
 
     GS_TRY(launch_preprocess(gauss->mean, gauss->scale, gauss->rot, gauss->value, gauss->weight, n, gp,
-                             index_radius(tau), w.rec, w.box, w.spans, w.pair_off, w.pair_sum, stream),
+                             index_radius(tau), w.rec, w.box, w.lines, w.rows, w.rbase, w.rtotal, index->capacity,
+                             w.pair_off, w.pair_sum, stream),
            "gs_build_index: preprocess");
     {
         // groups past ceil(n / 64) hold only count[n] = 0: their prefix is the total
@@ -615,7 +622,7 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
     // emit where the sort's last pass lands in keys/gids
     uint32_t *ek = odd ? w.keys_alt : index->keys, *ev = odd ? w.gids_alt : index->gids;
     uint32_t *ak = odd ? index->keys : w.keys_alt, *av = odd ? index->gids : w.gids_alt;
-    GS_TRY(launch_emit(w.pair_off, w.box, w.spans, n, (int64_t)P, gp, w.tile_first, ek, ev,
+    GS_TRY(launch_emit(w.pair_off, w.box, w.lines, w.rows, w.rbase, n, (int64_t)P, gp, w.tile_first, ek, ev,
                        radix_pass0(w.radix_work, (int64_t)P, bits), stream),
            "gs_build_index: emit");
     GS_TRY(radix_sort_pairs(ek, ev, ak, av, (int64_t)P, bits, w.radix_work, stream, true), "gs_build_index: sort");
@@ -718,7 +725,8 @@ gs_status gs_sample_gaussian_major(const gs_gaussians *gauss, const gs_index *in
     Plan p;
     if ((st = order_queries("gs_sample_gaussian_major", qp, gp, nq, plan, plan_bytes, &p, stream)) != GS_OK)
         return st;
-    GS_TRY(launch_sample_gauss_major(qp, gp, w.rec, w.box, w.spans, w.gorder, index->n_gauss, p.order, p.point_off,
+    GS_TRY(launch_sample_gauss_major(qp, gp, bwd_geom(gp, qp, cutoff_T(index->tau)), w.rec, w.box, w.gorder,
+                                     index->n_gauss, p.order, p.point_off,
                                      cutoff_T(index->tau), index->tau, out_value, out_influence, p.res, work, stream),
            "gs_sample_gaussian_major");
     return GS_OK;

@@ -120,15 +120,17 @@ __device__ __forceinline__ float whiten(const Record &r, float px, float py, flo
 }
 
 // Partials of one contributing pair (Q' <= T'), given u, Q' and the
-// query's alpha, beta.
+// query's alpha, beta. With a = w G and dL/da = alpha v + beta, the sums
+// kept are sum alpha G (dv / w), sum dL/da G (dw), and the moments of
+// dL/da G u; the weight and the -1/2 of dQ/du (dL/dQ = -a dL/da / 2) are
+// applied once per Gaussian by k_finalize.
 __device__ __forceinline__ void pair_grad(const Record &r, float u0, float u1, float u2, float Q, float al, float be,
                                           Acc &acc) {
     const float G = exp2_hw(-Q);  // Q is Q' = Q log2(e) / 2
-    const float a = r.f0.w * G;
     const float dLda = fmaf_(al, r.f1.w, be);
-    acc.dv = fmaf_(al, a, acc.dv);
-    acc.dw = fmaf_(dLda, G, acc.dw);
-    const float c = -0.5f * a * dLda;
+    const float c = dLda * G;
+    acc.dv = fmaf_(al, G, acc.dv);
+    acc.dw += c;
     const float c0 = c * u0, c1 = c * u1, c2 = c * u2;
     acc.m1[0] += c0;
     acc.m1[1] += c1;
@@ -197,6 +199,10 @@ constexpr int kBwdWaves = 1;
 constexpr int kBwdBlock = kBwdWaves * kWave;
 // Element windows per step of the walk (see the window loop).
 constexpr uint32_t kBwdWindows = 2;
+static_assert(kBwdWindows == 2, "the walk's uniform steps take two windows");
+// Mean row length (elements per row of a Gaussian's part of a batch) from
+// which the walk tracks its row in scalars.
+constexpr uint32_t kLongRow = 128;
 
 // Gaussians per wavefront: consecutive Gaussians of gorder share a wave, so
 // that their rows are found together. Below kPackMinGauss Gaussians one per
@@ -235,46 +241,6 @@ __device__ __forceinline__ float bperm_f(uint32_t src, float v) {
     return __int_as_float(__builtin_amdgcn_ds_bpermute((int)src, __float_as_int(v)));
 }
 
-// Least value over the rectangle dy in [ay, by], dz in [az, bz] (offsets
-// from the mean) of q2 = (U11 dy + U12 dz)^2 + (U22 dz)^2, the minimum of Q
-// over x at fixed (y, z) for the record's triangular U. q2 is convex: its
-// minimum is at dy = dz = 0 when the rectangle holds it, else on an edge,
-// where it is a quadratic in one variable minimised at its clamped vertex.
-__device__ __forceinline__ float slab_q2min(float U11, float U12, float U22, float ay, float by, float az,
-                                            float bz) {
-    if (ay <= 0.0f && by >= 0.0f && az <= 0.0f && bz >= 0.0f) return 0.0f;
-    const float i11 = __builtin_amdgcn_rcpf(U11);
-    const float iden = __builtin_amdgcn_rcpf(fmaf_(U12, U12, U22 * U22));
-    auto q2 = [&](float dy, float dz) {
-        const float a = fmaf_(U11, dy, U12 * dz), b = U22 * dz;
-        return fmaf_(a, a, b * b);
-    };
-    // fixed dz: best dy = -U12 dz / U11; fixed dy: best dz = -U11 U12 dy / (U12^2 + U22^2)
-    const float ya = fminf(fmaxf(-U12 * az * i11, ay), by), yb = fminf(fmaxf(-U12 * bz * i11, ay), by);
-    const float za = fminf(fmaxf(-U11 * U12 * ay * iden, az), bz), zb = fminf(fmaxf(-U11 * U12 * by * iden, az), bz);
-    return fminf(fminf(q2(ya, az), q2(yb, bz)), fminf(q2(ay, za), q2(by, zb)));
-}
-
-// x-range [xl, xh] of the points of the rectangle (offsets from the mean,
-// as above) with Q <= T2, or false when there are none. At fixed (y, z) Q
-// <= T2 holds for |x - xc| <= sqrt(T2 - q2) / U00 with the centre xc =
-// mu_x - (U01 dy + U02 dz) / U00, linear in (dy, dz): the range spans the
-// centre's extremes at the rectangle's corners, widened by the half-width
-// at the rectangle's least q2, and by a few units of float32 rounding.
-__device__ __forceinline__ bool slab_xrange(const Record &r, float ay, float by, float az, float bz, float T2,
-                                            float &xl, float &xh) {
-    const float q2 = slab_q2min(r.f2.x, r.f2.y, r.f2.z, ay, by, az, bz);
-    if (!(q2 <= T2)) return false;
-    const float iu = __builtin_amdgcn_rcpf(r.f1.x);
-    const float w = __builtin_sqrtf(T2 - q2) * iu;
-    const float c0 = r.f1.y * ay, c1 = r.f1.y * by, c2 = r.f1.z * az, c3 = r.f1.z * bz;
-    const float hi = (fmaxf(c0, c1) + fmaxf(c2, c3)) * iu, lo = (fminf(c0, c1) + fminf(c2, c3)) * iu;
-    const float m = (fabsf(r.f0.x) + fabsf(hi) + fabsf(lo) + w) * 0x1p-20f;
-    xl = r.f0.x - hi - w - m;
-    xh = r.f0.x - lo + w + m;
-    return true;
-}
-
 // Row `row` of a Gaussian's box (lower corner (lx, ly, lz) in cells, nx
 // cells along x, ny along y): for grids voxel row (vy, vz) of the box, for
 // ordered queries the row of cells (cy, cz), y fastest. The row's first
@@ -304,8 +270,8 @@ __device__ __forceinline__ RowRun row_run(const Record &r, int32_t lx, int32_t l
     else
         zz = row / nry;
     const uint32_t yy = row - zz * nry;
-    float xl, xh;
     if (GRID) {
+        float xl, xh;
         (void)rz;
         const uint32_t vy = (uint32_t)ly * ry + yy, vz = (uint32_t)lz * rz + zz;
         o.py = g.lo[1] + ((float)vy + 0.5f) * q.vsz[1];
@@ -322,23 +288,7 @@ __device__ __forceinline__ RowRun row_run(const Record &r, int32_t lx, int32_t l
         o.len = (uint32_t)(v1 - v0) + 1u;
         o.start = (uint32_t)q.dims[0] * (vy + (uint32_t)q.dims[1] * vz) + o.x0;
     } else {
-        const uint32_t cy = (uint32_t)ly + yy, cz = (uint32_t)lz + zz;
-        const float y0 = g.lo[1] + (float)cy * bg.cw[0] - bg.slack[0];
-        const float y1 = g.lo[1] + (float)(cy + 1u) * bg.cw[0] + bg.slack[0];
-        const float z0 = g.lo[2] + (float)cz * bg.cw[1] - bg.slack[1];
-        const float z1 = g.lo[2] + (float)(cz + 1u) * bg.cw[1] + bg.slack[1];
-        if (!slab_xrange(r, y0 - r.f0.y, y1 - r.f0.y, z0 - r.f0.z, z1 - r.f0.z, bg.T2, xl, xh)) return o;
-        // quarters of the box's cells with queries whose x can lie in
-        // [xl, xh]: the plan's quarter of x is floor(kSub t), t = (x - lo)
-        // invc in the same float32 operations, monotone in x
-        const float qmin = (float)(kSub * (uint32_t)lx), qmax = (float)(kSub * ((uint32_t)lx + nx)) - 1.0f;
-        const float ql = fminf(fmaxf(floorf((float)kSub * ((xl - g.lo[0]) * g.invc[0])), qmin), qmax);
-        const float qh = fminf(fmaxf(floorf((float)kSub * ((xh - g.lo[0]) * g.invc[0])), qmin), qmax);
-        // the row's quarters are entries base .. base + K of the plan's
-        // offsets, the last one the start of the next row of cells
-        const uint32_t base = (cz * (uint32_t)g.cells[1] + cy) * bg.K;
-        o.start = point_off[base + (uint32_t)ql];
-        o.len = point_off[base + (uint32_t)qh + 1u] - o.start;
+        o.len = plan_row(r, (uint32_t)lx, nx, (uint32_t)ly + yy, (uint32_t)lz + zz, g, bg, point_off, o.start);
     }
     return o;
 }
@@ -537,10 +487,58 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
                     cnt -= kWave;
                 }
             };
+            // The row holding element e, tracked in scalars: its offset kos
+            // and the start nxt of the row after it (lanes past the batch's
+            // rows hold E).
+            uint32_t kos = 0, nxt = 0;
+            auto row_at = [&](uint32_t e) {
+                const uint32_t j = (uint32_t)__popcll(mask_le_u(rbeg, e)) - 1u;
+                kos = __builtin_amdgcn_readlane(kofs, j);
+                nxt = j + 1u < (uint32_t)kWave ? __builtin_amdgcn_readlane(rbeg, j + 1u) : E;
+            };
+            // The test of a window that lies inside one row and before Eb:
+            // every lane is valid and element e0 + l is point e0 + kos + l.
+            auto test_row = [&](uint32_t e0, float4 p) {
+                float u0, u1, u2;
+                const float Q = whiten(r, p.x, p.y, p.z, u0, u1, u2);
+                const uint64_t mask = mask_le_f(Q, T);
+                if (mask == 0) return;
+                if (Q <= T) {
+                    const uint32_t pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                    const uint32_t slot = (head + cnt + pos) & (kQueue - 1);
+                    qu[slot] = make_float4(u0, u1, u2, Q);
+                    qk[slot] = e0 + kos + lane;
+                }
+                cnt += (uint32_t)__popcll(mask);
+                if (cnt >= (uint32_t)kWave) {
+                    __builtin_amdgcn_wave_barrier();
+                    drain(r, qu, qk, head, kWave, lane, ab, acc);
+                    __builtin_amdgcn_wave_barrier();
+                    head = (head + kWave) & (kQueue - 1);
+                    cnt -= kWave;
+                }
+            };
             // Windows are taken two at a time: both positions are loaded
             // before either is tested, so one load's latency overlaps the
-            // other window's work.
+            // other window's work. When the Gaussian's rows are long, a step
+            // whose windows are full and inside one row (most of them then)
+            // skips the per-lane row search and loads from a uniform base;
+            // with short rows the scalar bookkeeping would cost more than it
+            // saves.
+            const bool long_rows = !GRID && Eb - Ea >= kLongRow * (lb - la);
             for (uint32_t e0 = Ea; e0 < Eb; e0 += kBwdWindows * kWave) {
+                if (long_rows) {
+                    if (e0 >= nxt) row_at(e0);
+                    const uint32_t eend = e0 + kBwdWindows * kWave;
+                    if (eend <= nxt && eend <= Eb) {
+                        const float4 *pp = plan_pos + (e0 + kos);
+                        const float4 pA = pp[lane], pB = pp[kWave + lane];
+                        test_row(e0, pA);
+                        test_row(e0 + kWave, pB);
+                        continue;
+                    }
+                }
                 uint32_t koA, xoA, koB = 0, xoB = 0;
                 float pyA, pzA, pyB = 0.0f, pzB = 0.0f;
                 const uint32_t e1 = e0 + kWave;
@@ -561,6 +559,7 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
 }
 
 __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ moments, int64_t n,
+                                                     const Record *__restrict__ rec,
                                                      const float *__restrict__ scale, const float *__restrict__ rot,
                                                      float *__restrict__ d_mean, float *__restrict__ d_scale,
                                                      float *__restrict__ d_rot, float *__restrict__ d_value,
@@ -569,10 +568,12 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
     if (i >= n) return;
     const float *m = moments + (size_t)i * 12;
     const float4 ma = *(const float4 *)m, mb = *(const float4 *)(m + 4), mc = *(const float4 *)(m + 8);
-    // moments of u / k, the unscaled factor's frame
+    // moments of dL/dQ u / k (the unscaled factor's frame): the kernel's
+    // sums of dL/da G u times -w/2, over k
     constexpr double ik = 1.0 / kRecScale, ik2 = ik * ik;
-    const double m1p[3] = {ma.x * ik, ma.y * ik, ma.z * ik};
-    const double m2s[6] = {ma.w * ik2, mb.x * ik2, mb.y * ik2, mb.z * ik2, mb.w * ik2, mc.x * ik2};
+    const double wt = rec[i].f0.w, c1 = -0.5 * wt * ik, c2 = -0.5 * wt * ik2;
+    const double m1p[3] = {ma.x * c1, ma.y * c1, ma.z * c1};
+    const double m2s[6] = {ma.w * c2, mb.x * c2, mb.y * c2, mb.z * c2, mb.w * c2, mc.x * c2};
     const bool any = ma.x != 0.0f || ma.y != 0.0f || ma.z != 0.0f || ma.w != 0.0f || mb.x != 0.0f ||
                      mb.y != 0.0f || mb.z != 0.0f || mb.w != 0.0f || mc.x != 0.0f || mc.y != 0.0f || mc.z != 0.0f;
     // the parameters are loaded with the moments, whatever these hold
@@ -658,7 +659,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(const float *__restrict__ m
         d_scale[3 * i + j] = (float)ds[j];
     }
     for (int k = 0; k < 4; ++k) d_rot[4 * i + k] = (float)dq[k];
-    d_value[i] = mc.y;
+    d_value[i] = (float)(mc.y * wt);
     d_weight[i] = mc.z;
 }
 
@@ -780,8 +781,8 @@ hipError_t launch_backward(const QueryParams &q, const GridParams &g, const BwdG
         if (e != hipSuccess) return e;
     }
     prof_begin("bwd_finalize", s);
-    hipLaunchKernelGGL(k_finalize, dim3(gblocks), dim3(kBlock), 0, s, b.moments, n_gauss, scale, rot, d_mean, d_scale,
-                       d_rot, d_value, d_weight);
+    hipLaunchKernelGGL(k_finalize, dim3(gblocks), dim3(kBlock), 0, s, b.moments, n_gauss, rec, scale, rot, d_mean,
+                       d_scale, d_rot, d_value, d_weight);
     prof_end("bwd_finalize", s);
     return hipGetLastError();
 }

@@ -47,9 +47,8 @@ __global__ __launch_bounds__(kBlock) void k_plan_positions(QueryParams q, GridPa
     acc[2 * k + 1] = 0.0;
 }
 
-__global__ __launch_bounds__(kBlock) void k_forward_gauss(GridParams g, const Record *__restrict__ rec,
+__global__ __launch_bounds__(kBlock) void k_forward_gauss(GridParams g, BwdGeom bg, const Record *__restrict__ rec,
                                                           const CellBox *__restrict__ box,
-                                                          const uint8_t *__restrict__ spans,
                                                           const uint32_t *__restrict__ gorder, int64_t n_gauss,
                                                           const uint32_t *__restrict__ point_off,
                                                           const float4 *__restrict__ pos, float T,
@@ -64,29 +63,15 @@ __global__ __launch_bounds__(kBlock) void k_forward_gauss(GridParams g, const Re
     const float v = r.f1.w;
     const uint32_t nx = (uint32_t)(bx.hi.x - bx.lo.x + 1), ny = (uint32_t)(bx.hi.y - bx.lo.y + 1);
     const uint32_t R = ny * (uint32_t)(bx.hi.z - bx.lo.z + 1);
-    const bool trimmed = bx.lo.w != 0;
     for (uint32_t rb = 0; rb < R; rb += kWave) {
-        // lane l: row rb + l of the box, its first point and length
+        // lane l: row rb + l of the box, its first point and length: the
+        // quarters of its cells the record's cutoff can reach
         const uint32_t row = rb + lane;
         uint32_t start = 0, len = 0;
         if (row < R) {
             const uint32_t zz = row / ny, yy = row - zz * ny;
-            uint32_t xa = 0, xn = nx, qa = 0, qb = 0;
-            if (trimmed) {
-                const size_t at = (size_t)gid * kSpanStride + yy + ny * zz;
-                const uint32_t code = spans[at];
-                xa = span_first(code);
-                xn = span_len(code);
-                const uint32_t qc = spans[at + kSpanRows];  // quarters of the end cells reached
-                qa = qc & 3u;
-                qb = qc >> 2;
-            }
-            if (xn > 0) {
-                const uint32_t cy = (uint32_t)bx.lo.y + yy, cz = (uint32_t)bx.lo.z + zz;
-                const uint32_t kb = (uint32_t)g.cells[0] * (cy + (uint32_t)g.cells[1] * cz) + (uint32_t)bx.lo.x + xa;
-                start = point_off[kSub * kb + qa];
-                len = point_off[kSub * (kb + xn) - qb] - start;
-            }
+            len = plan_row(r, (uint32_t)bx.lo.x, nx, (uint32_t)bx.lo.y + yy, (uint32_t)bx.lo.z + zz, g, bg, point_off,
+                           start);
         }
         const uint32_t nrows = R - rb < (uint32_t)kWave ? R - rb : (uint32_t)kWave;
         const uint32_t incl = wave_incl_sum(len);
@@ -138,8 +123,8 @@ __global__ __launch_bounds__(kBlock) void k_finish_gauss_major(int64_t n, const 
 
 size_t gauss_major_work_bytes(int64_t nq) { return (size_t)(nq > 0 ? nq : 1) * 2 * sizeof(double); }
 
-hipError_t launch_sample_gauss_major(const QueryParams &q, const GridParams &g, const Record *rec,
-                                     const CellBox *box, const uint8_t *spans, const uint32_t *gorder,
+hipError_t launch_sample_gauss_major(const QueryParams &q, const GridParams &g, const BwdGeom &bg, const Record *rec,
+                                     const CellBox *box, const uint32_t *gorder,
                                      int64_t n_gauss, const uint32_t *order, const uint32_t *point_off, float T,
                                      float tau, float *out_v, float *out_i, const PlanResults &pr, void *work,
                                      hipStream_t s) {
@@ -154,7 +139,7 @@ hipError_t launch_sample_gauss_major(const QueryParams &q, const GridParams &g, 
     if (n_gauss > 0) {
         prof_begin("gm_forward", s);
         hipLaunchKernelGGL(k_forward_gauss, dim3((uint32_t)((n_gauss + kWavesPerBlock - 1) / kWavesPerBlock)),
-                           dim3(kBlock), 0, s, g, rec, box, spans, gorder, n_gauss, point_off, pr.pos, T, acc);
+                           dim3(kBlock), 0, s, g, bg, rec, box, gorder, n_gauss, point_off, pr.pos, T, acc);
         prof_end("gm_forward", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }

@@ -55,29 +55,41 @@ __device__ __forceinline__ Record load_record_uniform(const Record *rec, uint32_
     return r;
 }
 
-// Cell box of a Gaussian: (x0, y0, z0, trimmed) and (x1, y1, z1, 0),
-// inclusive; an empty box has x1 < x0. When trimmed is 1 the box lists, in
-// each of its (y, z) rows (row r = (y - y0) + ny (z - z0)), only the cells
-// of the row's span: byte r of the Gaussian's span record holds the first
-// and last cell as offsets from x0 (low and high 4 bits), kSpanEmpty for a
-// row with none.
+// Cell box of a Gaussian: (x0, y0, z0, trim) and (x1, y1, z1, nrec),
+// inclusive; an empty box has x1 < x0. A trimmed box (trim 1 or 2) lists,
+// in each of its (y, z) rows (row r = (y - y0) + ny (z - z0)), only the run
+// of cells that a bound of the cutoff ellipsoid (enlarged like the box)
+// over the row's slab reaches; trim 0 lists every cell of the box. For
+// trim 1 (at most kLineRows rows of at most kLineNx cells) the runs are one
+// byte per row in the Gaussian's line of kLineRows bytes: the first and
+// last cell as offsets from x0 (low and high 4 bits), kRunEmpty for a row
+// with none. For trim 2 they are nrec RowRecs, one per row with cells, in
+// row order, from the Gaussian's record base.
 struct alignas(16) CellBox {
     int4 lo, hi;
 };
-constexpr int kSpanRows = 64;          // rows of a trimmed box at most
-// A trimmed box's line of span data: its kSpanRows span codes, then one
-// quarter code per row: (first quarter of the row's first cell that the
-// bound reaches) | (quarters of its last cell past the bound) << 2, for the
-// query order by quarter of a cell (kSub below).
-constexpr int kSpanStride = 2 * kSpanRows;
-constexpr int kSpanNx = 16;            // cells per row of a trimmed box at most
-constexpr uint32_t kSpanEmpty = 0x0Fu;
+constexpr uint32_t kLineRows = 64;
+constexpr uint32_t kLineNx = 16;
+constexpr uint32_t kRunEmpty = 0x0Fu;
+// Trimmed boxes have at most kTrimRowsMax rows of at most kRecNxMax cells
+// (RowRec's 16-bit fields); larger ones keep every cell.
+constexpr uint32_t kTrimRowsMax = 4096;
+constexpr uint32_t kRecNxMax = 65535;
+// A row with cells of a trim-2 box: the box's cells in earlier rows, the
+// row, and its first cell as an offset from x0 (its length is the next
+// record's pos, or the box's count, minus pos).
+struct RowRec {
+    uint32_t pos;
+    uint16_t row, first;
+};
 
-__device__ __forceinline__ uint32_t span_first(uint32_t code) { return code & 15u; }
-__device__ __forceinline__ uint32_t span_len(uint32_t code) {
+__device__ __forceinline__ uint32_t run_first(uint32_t code) { return code & 15u; }
+__device__ __forceinline__ uint32_t run_len(uint32_t code) {
     const uint32_t a = code & 15u, b = code >> 4;
     return b >= a ? b - a + 1 : 0u;
 }
+
+
 
 // Read-only views in the constant address space: loads through them with a
 // wave-uniform address become scalar loads into SGPRs.
@@ -295,12 +307,13 @@ struct GridParams {
 // count[0..n] receives the pair count of every Gaussian (count[n] = 0) and
 // block_sum[b] the sum over elements [64 b, 64 b + 64) of count
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
-                             const float *weight, int64_t n, const GridParams &g, float rci, Record *rec, CellBox *box, uint8_t *spans,
+                             const float *weight, int64_t n, const GridParams &g, float rci, Record *rec, CellBox *box,
+                             uint8_t *lines, RowRec *rows, uint32_t *rbase, uint32_t *rtotal, int64_t rcap,
                              uint64_t *count, uint64_t *block_sum, hipStream_t s);
 // tile_first: ceil(npairs / kSortTile) words of scratch
-hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8_t *spans, int64_t n, int64_t npairs,
-                       const GridParams &g,
-                       uint32_t *tile_first, uint32_t *keys, uint32_t *gids, const RadixPass0 &pass0, hipStream_t s);
+hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8_t *lines, const RowRec *rows,
+                       const uint32_t *rbase, int64_t n, int64_t npairs, const GridParams &g, uint32_t *tile_first,
+                       uint32_t *keys, uint32_t *gids, const RadixPass0 &pass0, hipStream_t s);
 
 // Sampling (sample.hip).
 // The plan orders the queries by cell and, inside a cell, by the quarter of
@@ -416,6 +429,72 @@ struct BwdGeom {
     float xslack;      // grids: widening of a row's voxel range, in voxels
     uint32_t K;        // kSub cells[0]: quarters of a row of cells
 };
+
+// Least value over the rectangle dy in [ay, by], dz in [az, bz] (offsets
+// from the mean) of q2 = (U11 dy + U12 dz)^2 + (U22 dz)^2, the minimum of Q
+// over x at fixed (y, z) for the record's triangular U. q2 is convex: its
+// minimum is at dy = dz = 0 when the rectangle holds it, else on an edge,
+// where it is a quadratic in one variable minimised at its clamped vertex.
+__device__ __forceinline__ float slab_q2min(float U11, float U12, float U22, float ay, float by, float az,
+                                            float bz) {
+    if (ay <= 0.0f && by >= 0.0f && az <= 0.0f && bz >= 0.0f) return 0.0f;
+    const float i11 = __builtin_amdgcn_rcpf(U11);
+    const float iden = __builtin_amdgcn_rcpf(fmaf_(U12, U12, U22 * U22));
+    auto q2 = [&](float dy, float dz) {
+        const float a = fmaf_(U11, dy, U12 * dz), b = U22 * dz;
+        return fmaf_(a, a, b * b);
+    };
+    // fixed dz: best dy = -U12 dz / U11; fixed dy: best dz = -U11 U12 dy / (U12^2 + U22^2)
+    const float ya = fminf(fmaxf(-U12 * az * i11, ay), by), yb = fminf(fmaxf(-U12 * bz * i11, ay), by);
+    const float za = fminf(fmaxf(-U11 * U12 * ay * iden, az), bz), zb = fminf(fmaxf(-U11 * U12 * by * iden, az), bz);
+    return fminf(fminf(q2(ya, az), q2(yb, bz)), fminf(q2(ay, za), q2(by, zb)));
+}
+
+// x-range [xl, xh] of the points of the rectangle (offsets from the mean,
+// as above) with Q <= T2, or false when there are none. At fixed (y, z) Q
+// <= T2 holds for |x - xc| <= sqrt(T2 - q2) / U00 with the centre xc =
+// mu_x - (U01 dy + U02 dz) / U00, linear in (dy, dz): the range spans the
+// centre's extremes at the rectangle's corners, widened by the half-width
+// at the rectangle's least q2, and by a few units of float32 rounding.
+__device__ __forceinline__ bool slab_xrange(const Record &r, float ay, float by, float az, float bz, float T2,
+                                            float &xl, float &xh) {
+    const float q2 = slab_q2min(r.f2.x, r.f2.y, r.f2.z, ay, by, az, bz);
+    if (!(q2 <= T2)) return false;
+    const float iu = __builtin_amdgcn_rcpf(r.f1.x);
+    const float w = __builtin_sqrtf(T2 - q2) * iu;
+    const float c0 = r.f1.y * ay, c1 = r.f1.y * by, c2 = r.f1.z * az, c3 = r.f1.z * bz;
+    const float hi = (fmaxf(c0, c1) + fmaxf(c2, c3)) * iu, lo = (fminf(c0, c1) + fminf(c2, c3)) * iu;
+    const float m = (fabsf(r.f0.x) + fabsf(hi) + fabsf(lo) + w) * 0x1p-20f;
+    xl = r.f0.x - hi - w - m;
+    xh = r.f0.x - lo + w + m;
+    return true;
+}
+
+// The plan entries [start, start + len) of row (cy, cz) of a box spanning
+// cells lx .. lx + nx - 1 along x whose queries can lie within the cutoff
+// T2 of the record (ordered queries): the row's y, z extent widened by the
+// slack, cut to the x-range of slab_xrange, taken in quarters of cells. The
+// plan's quarter of x is floor(kSub t), t = (x - lo) invc, in the same
+// float32 operations, monotone in x, so every query the range admits is in.
+__device__ __forceinline__ uint32_t plan_row(const Record &r, uint32_t lx, uint32_t nx, uint32_t cy, uint32_t cz,
+                                             const GridParams &g, const BwdGeom &bg,
+                                             const uint32_t *__restrict__ point_off, uint32_t &start) {
+    start = 0;
+    const float y0 = g.lo[1] + (float)cy * bg.cw[0] - bg.slack[0];
+    const float y1 = g.lo[1] + (float)(cy + 1u) * bg.cw[0] + bg.slack[0];
+    const float z0 = g.lo[2] + (float)cz * bg.cw[1] - bg.slack[1];
+    const float z1 = g.lo[2] + (float)(cz + 1u) * bg.cw[1] + bg.slack[1];
+    float xl, xh;
+    if (!slab_xrange(r, y0 - r.f0.y, y1 - r.f0.y, z0 - r.f0.z, z1 - r.f0.z, bg.T2, xl, xh)) return 0;
+    const float qmin = (float)(kSub * lx), qmax = (float)(kSub * (lx + nx)) - 1.0f;
+    const float ql = fminf(fmaxf(floorf((float)kSub * ((xl - g.lo[0]) * g.invc[0])), qmin), qmax);
+    const float qh = fminf(fmaxf(floorf((float)kSub * ((xh - g.lo[0]) * g.invc[0])), qmin), qmax);
+    // the row's quarters are entries base .. base + K of the plan's offsets,
+    // the last one the start of the next row of cells
+    const uint32_t base = (cz * (uint32_t)g.cells[1] + cy) * bg.K;
+    start = point_off[base + (uint32_t)ql];
+    return point_off[base + (uint32_t)qh + 1u] - start;
+}
 
 struct BackwardBuffers {
     float *moments;        // [n_gauss][12]
