@@ -127,7 +127,7 @@ __device__ __forceinline__ float whiten(const Record &r, float px, float py, flo
 __device__ __forceinline__ void pair_grad(const Record &r, float u0, float u1, float u2, float Q, float al, float be,
                                           Acc &acc) {
     const float G = exp2_hw(-Q);  // Q is Q' = Q log2(e) / 2
-    const float dLda = fmaf_(al, r.f1.w, be);
+    const float dLda = fmaf_(al, r.f2.w, be);
     const float c = dLda * G;
     acc.dv = fmaf_(al, G, acc.dv);
     acc.dw += c;

@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kBlock) void k_forward_gauss(GridParams g, BwdGeom 
     const CellBox bx = load_box_uniform(box, gid);
     if (bx.hi.x < bx.lo.x) return;
     const Record r = load_record_uniform(rec, gid);
-    const float v = r.f1.w;
+    const float v = r.f2.w;
     const uint32_t nx = (uint32_t)(bx.hi.x - bx.lo.x + 1), ny = (uint32_t)(bx.hi.y - bx.lo.y + 1);
     const uint32_t R = ny * (uint32_t)(bx.hi.z - bx.lo.z + 1);
     for (uint32_t rb = 0; rb < R; rb += kWave) {

@@ -414,8 +414,8 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
         const double u22 = sqrt(A[2][2] - u02 * u02 - u12 * u12);
         Record f;
         f.f0 = make_float4(mu[0], mu[1], mu[2], w);
-        f.f1 = make_float4((float)(kRecScale * u00), (float)(kRecScale * u01), (float)(kRecScale * u02), v);
-        f.f2 = make_float4((float)(kRecScale * u11), (float)(kRecScale * u12), (float)(kRecScale * u22), 0.0f);
+        f.f1 = make_float4((float)(kRecScale * u00), (float)(kRecScale * u01), (float)(kRecScale * u02), w * v);
+        f.f2 = make_float4((float)(kRecScale * u11), (float)(kRecScale * u12), (float)(kRecScale * u22), v);
         rec[i] = f;
     } else {
         Record f;

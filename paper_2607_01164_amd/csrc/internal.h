@@ -15,9 +15,10 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 
 // Per-Gaussian evaluation record, 48 bytes, written by the preprocess:
 //   f0 = (mu_x, mu_y, mu_z, w)
-//   f1 = (U00, U01, U02, v)      U = kRecScale L, L upper triangular with
-//   f2 = (U11, U12, U22, 0)      L^T L = R S^-2 R^T (the inverse covariance)
+//   f1 = (U00, U01, U02, w v)    U = kRecScale L, L upper triangular with
+//   f2 = (U11, U12, U22, v)      L^T L = R S^-2 R^T (the inverse covariance)
 // so that |U (p - mu)|^2 = Q' = Q log2(e) / 2 and G = exp(-Q/2) = 2^-Q'; the
+// forward adds w G and (w v) G with one FMA each (w v rounded once); the
 // cutoff G >= tau reads Q' <= log2(1/tau) (record_T). L, the Cholesky
 // factor of the inverse covariance, takes 6 products and sums where
 // M = S^-1 R^T takes 9, and three 16-byte quarters where M takes four; its

@@ -43,21 +43,22 @@ __device__ __forceinline__ void accumulate(const Record &r, float px, float py, 
                                            float &V) {
     const float Q = cutoff_q(r, px, py, pz);
     if (Q <= T) {
-        const float a = r.f0.w * exp2_hw(-Q);
-        I += a;
-        V = fmaf_(a, r.f1.w, V);
+        const float G = exp2_hw(-Q);
+        I = fmaf_(r.f0.w, G, I);
+        V = fmaf_(r.f1.w, G, V);
     }
 }
 
-// The same sums without a branch: a is selected (0 past the cutoff) and
-// always added, so that a lane's R queries cost one select each (adding 0
-// leaves I and V as they are: both start at +0 and w, v are finite).
+// The same sums without a branch: G is selected (0 past the cutoff) and
+// always added, so that a lane's R queries cost one select each (adding
+// w 0 and (w v) 0 leaves I and V as they are: both start at +0 and w, v are
+// finite).
 __device__ __forceinline__ void accumulate_sel(const Record &r, float px, float py, float pz, float T, float &I,
                                                float &V) {
     const float Q = cutoff_q(r, px, py, pz);
-    const float a = Q <= T ? r.f0.w * exp2_hw(-Q) : 0.0f;
-    I += a;
-    V = fmaf_(a, r.f1.w, V);
+    const float G = Q <= T ? exp2_hw(-Q) : 0.0f;
+    I = fmaf_(r.f0.w, G, I);
+    V = fmaf_(r.f1.w, G, V);
 }
 
 // Walk a wave-uniform candidate list [ja, jb) for one query per lane. The
@@ -321,9 +322,10 @@ __global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restr
     }
 }
 
-__device__ __forceinline__ float eval_a(const Record &r, float px, float py, float pz, float T) {
+// G of a record at a point, 0 past the cutoff.
+__device__ __forceinline__ float eval_g(const Record &r, float px, float py, float pz, float T) {
     const float Q = cutoff_q(r, px, py, pz);
-    return Q <= T ? r.f0.w * exp2_hw(-Q) : 0.0f;
+    return Q <= T ? exp2_hw(-Q) : 0.0f;
 }
 
 // sum over the 64 lanes, returned to every lane
@@ -412,13 +414,13 @@ __device__ __forceinline__ void query_rows(uint32_t lane, uint32_t n, uint32_t p
                 r.f0 = buf[sidx];
                 r.f1 = buf[kWave + sidx];
                 r.f2 = buf[2 * kWave + sidx];
-                if (c0 + sidx >= jb) r.f0.w = 0.0f;  // past the list: weight 0
+                if (c0 + sidx >= jb) r.f0.w = r.f1.w = 0.0f;  // past the list: weight 0
 #pragma unroll
                 for (uint32_t t = 0; t < kRowsMax; ++t) {
                     if (t < nt) {
-                        const float a = eval_a(r, px[t], py[t], pz[t], T);
-                        Ip[t] += a;
-                        Vp[t] = fmaf_(a, r.f1.w, Vp[t]);
+                        const float G = eval_g(r, px[t], py[t], pz[t], T);
+                        Ip[t] = fmaf_(r.f0.w, G, Ip[t]);
+                        Vp[t] = fmaf_(r.f1.w, G, Vp[t]);
                     }
                 }
             }
@@ -560,9 +562,9 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
 #pragma unroll
             for (uint32_t t = 0; t < kChunkB; ++t) {
                 if (t < m) {
-                    const float a = eval_a(r, readlane_f(mx, t), readlane_f(my, t), readlane_f(mz, t), T);
-                    Ip[t] += a;
-                    Vp[t] = fmaf_(a, r.f1.w, Vp[t]);
+                    const float G = eval_g(r, readlane_f(mx, t), readlane_f(my, t), readlane_f(mz, t), T);
+                    Ip[t] = fmaf_(r.f0.w, G, Ip[t]);
+                    Vp[t] = fmaf_(r.f1.w, G, Vp[t]);
                 }
             }
         }
