@@ -114,6 +114,38 @@ def _dev(torch, np, a, dev="cuda:0"):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
 
+class SidePlans:
+    """Two plans and a side stream: a step's query ordering (gs_plan_queries)
+    runs there while the main stream builds the index and finishes the step
+    before; the planned forward waits for it, and a plan is reused once the
+    backward that read it has run."""
+
+    def __init__(self, gs, torch, query, grid, dev):
+        self.gs, self.torch = gs, torch
+        self.plans = [gs.alloc_plan(query, grid, dev) for _ in range(2)]
+        self.side = torch.cuda.Stream()
+        self.planned = [torch.cuda.Event() for _ in range(2)]
+        self.released = [torch.cuda.Event() for _ in range(2)]
+        for e in self.released:
+            e.record()
+        self.k = 0
+
+    def start(self, query, grid):
+        k = self.k
+        self.side.wait_event(self.released[k])
+        with self.torch.cuda.stream(self.side):
+            self.gs.gs_plan_queries(query, grid, self.plans[k], stream=self.side)
+            self.planned[k].record(self.side)
+        return self.plans[k]
+
+    def wait(self):
+        self.torch.cuda.current_stream().wait_event(self.planned[self.k])
+
+    def release(self):
+        self.released[self.k].record()
+        self.k ^= 1
+
+
 class PointsStep:
     """The unstructured workload's training step: the point cloud in
     `batches` resident batches; each is one iteration of index build,
@@ -153,7 +185,8 @@ class PointsStep:
         probe = gs.build_index(self.dg, self.grid, TAU)
         self.index = gs.Index(self.grid, g.n, int(probe.n_pairs * 1.25) + 4096, dev)
         del probe
-        self.plan = gs.alloc_plan(self.queries[0], self.grid, dev)
+        self.sp = SidePlans(gs, torch, self.queries[0], self.grid, dev)
+        self.plan = self.sp.plans[0]
         self.val = torch.empty(self.n, device=dev)
         self.inf = torch.empty(self.n, device=dev)
         self.grads = gs.Grads.empty(g.n, dev)
@@ -175,9 +208,17 @@ class PointsStep:
                                    self.gi[b], self.grads, self.work)
 
     def iteration(self):
+        """One training iteration: the batch's query ordering on the side
+        stream (into the plan the batch before last has released), the index
+        build on the main stream meanwhile, then the planned forward and the
+        backward."""
+        b = self.b
+        self.plan = self.sp.start(self.queries[b], self.grid)
         self.build()
-        self.forward()
+        self.sp.wait()
+        self.gs.gs_sample_planned(self.dg, self.index, self.queries[b], self.val, self.inf, self.plan)
         self.backward()
+        self.sp.release()
         self.b = (self.b + 1) % self.batches
 
     def step(self):
@@ -224,7 +265,8 @@ class GridBatchStep:
         probe = gs.build_index(self.dg, self.grid, TAU)
         self.index = gs.Index(self.grid, g.n, int(probe.n_pairs * 1.25) + 4096, dev)
         del probe
-        self.plan = gs.alloc_plan(self.query, self.grid, dev)
+        self.sp = SidePlans(gs, torch, self.query, self.grid, dev)
+        self.plan = self.sp.plans[0]
         self.val = torch.empty(self.n, dtype=torch.float32, device=dev)
         self.inf = torch.empty(self.n, dtype=torch.float32, device=dev)
         self.grads = gs.Grads.empty(g.n, dev)
@@ -243,9 +285,14 @@ class GridBatchStep:
                                    self.grads, self.work)
 
     def step(self):
+        """Build + forward + backward, the query ordering on the side stream
+        meanwhile (SidePlans)."""
+        self.plan = self.sp.start(self.query, self.grid)
         self.build()
-        self.forward()
+        self.sp.wait()
+        self.gs.gs_sample_planned(self.dg, self.index, self.query, self.val, self.inf, self.plan)
         self.backward()
+        self.sp.release()
 
     def pair_counts(self):
         self.forward()
@@ -298,7 +345,8 @@ class TrainStep:
         probe = gs.build_index(self.gauss, self.grid, TAU)
         self.index = gs.Index(self.grid, ng, int(probe.n_pairs * 1.25) + 4096, dev)
         del probe
-        self.plan = gs.alloc_plan(self.queries[0], self.grid, dev)
+        self.sp = SidePlans(gs, torch, self.queries[0], self.grid, dev)
+        self.plan = self.sp.plans[0]
         gs.gs_build_index(self.gauss, self.grid, TAU, self.index)
         self.work = gs.alloc_backward_work(self.index, self.queries[0], dev)
         self.it = 0
@@ -344,14 +392,19 @@ class TrainStep:
     def step(self):
         gs, st = self.gs, self.st
         q = self.queries[self.it % self.SETS]
+        # the query ordering on the side stream while activations and the
+        # index build run (SidePlans)
+        self.plan = self.sp.start(q, self.grid)
         self.activate()
         gs.gs_build_index(self.gauss, self.grid, TAU, self.index)
-        gs.gs_sample(self.gauss, self.index, q, self.val, self.inf, self.plan)
+        self.sp.wait()
+        gs.gs_sample_planned(self.gauss, self.index, q, self.val, self.inf, self.plan)
         gs.gs_loss(self.val, self.inf, self.targets[self.it % self.SETS], None, TAU, self.FN_EPS, self.FN_LAMBDA,
                    self.FP_LAMBDA, self.gv, self.gi, self.terms, self.loss_work)
         gs.gs_sample_backward(self.gauss, self.index, q, self.plan, self.val, self.inf, self.gv, self.gi, self.grads,
                               self.work)
         gs.gs_activate_backward(self.raw, self.CAP, self.grads, self.raw_grads)
+        self.sp.release()
         self.it += 1
 
 

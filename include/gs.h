@@ -185,6 +185,23 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
                     float *out_value, float *out_influence, void *plan, size_t plan_bytes,
                     hipStream_t stream);
 
+/*
+ * gs_sample in two parts, so that the query ordering (Sec. 5.1.1's role of
+ * the sample BVH), which needs only the queries and the grid, can run on
+ * another stream while gs_build_index runs: gs_plan_queries fills the
+ * plan's ordering and work items for a query and an index grid (nothing
+ * for GRID queries, whose plan may be null); gs_sample_planned then samples
+ * as gs_sample does, with a plan that gs_plan_queries filled for the same
+ * query and the index's grid, unchanged since (the caller orders the two
+ * streams, e.g. with an event). The outputs and the plan's contents equal
+ * gs_sample's, bit for bit. Plans follow gs_plan_bytes; errors as gs_sample.
+ */
+gs_status gs_plan_queries(const gs_query *query, const gs_grid *grid, void *plan, size_t plan_bytes,
+                          hipStream_t stream);
+gs_status gs_sample_planned(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                            float *out_value, float *out_influence, void *plan, size_t plan_bytes,
+                            hipStream_t stream);
+
 /* Bytes of workspace gs_sample_gaussian_major needs for a query (16 per
  * query; -1 cast to size_t for a GRID or malformed query). */
 size_t gs_sample_gaussian_major_work_bytes(const gs_query *query);

@@ -9,4 +9,4 @@ from .gsq import (GS_ERR_CAPACITY, GS_ERR_HIP, GS_ERR_INVALID_ARGUMENT, GS_ERR_W
                   gs_activate, gs_activate_backward, gs_loss, loss_work_bytes, read_loss_terms, ParamSet,
                   alloc_densify_work, densify_work_bytes, gs_densify, alloc_gaussian_major_work,
                   gaussian_major_work_bytes, gs_sample_gaussian_major, backward_pair_count,
-                  sample_pair_counts, gs_sample_backward_noalloc)
+                  sample_pair_counts, gs_sample_backward_noalloc, gs_plan_queries, gs_sample_planned)

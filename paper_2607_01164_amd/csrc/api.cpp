@@ -658,17 +658,40 @@ static gs_status check_index(const char *fn, const gs_gaussians *gauss, const gs
     return GS_OK;
 }
 
-static gs_status check_query(const char *fn, const gs_index *index, const gs_query *query) {
+static gs_status check_query_grid(const char *fn, const gs_grid *grid, const gs_query *query) {
     std::string why;
     if (!query_valid(query, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "%s: %s", fn, why.c_str());
     if (query->kind == GS_QUERY_GRID)
         for (int j = 0; j < 3; ++j)
-            if (query->dims[j] % index->grid.cells[j] != 0)
+            if (query->dims[j] % grid->cells[j] != 0)
                 return fail(GS_ERR_INVALID_ARGUMENT,
                             "%s: grid query dims must be a multiple of the index cells on every axis", fn);
-    if (query->kind != GS_QUERY_GRID && !ordered_grid_ok(&index->grid))
+    if (query->kind != GS_QUERY_GRID && !ordered_grid_ok(grid))
         return fail(GS_ERR_INVALID_ARGUMENT,
                     "%s: voxel, point and jitter queries need an index grid of fewer than 2^30 cells", fn);
+    return GS_OK;
+}
+
+static gs_status check_query(const char *fn, const gs_index *index, const gs_query *query) {
+    return check_query_grid(fn, &index->grid, query);
+}
+
+// The query ordering and the forward's work items (ordered queries).
+static gs_status plan_queries(const char *who, const QueryParams &qp, const GridParams &gp, int64_t nq, void *plan,
+                              size_t plan_bytes, Plan *out, hipStream_t stream) {
+    gs_status st = order_queries(who, qp, gp, nq, plan, plan_bytes, out, stream);
+    if (st != GS_OK) return st;
+    GS_TRY(launch_cell_items(nq, gp, out->point_off, out->items, stream), "work items");
+    return GS_OK;
+}
+
+// The point sampler over a plan that plan_queries filled.
+static gs_status sample_ordered(const char *who, const gs_index *index, const QueryParams &qp, const GridParams &gp,
+                                const Plan &p, float *out_value, float *out_influence, hipStream_t stream) {
+    IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
+    GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.order, p.point_off, p.items,
+                                cutoff_T(index->tau), index->tau, out_value, out_influence, p.res, stream),
+           who);
     return GS_OK;
 }
 
@@ -691,11 +714,47 @@ gs_status gs_sample(const gs_gaussians *gauss, const gs_index *index, const gs_q
         return GS_OK;
     }
     Plan p;
-    if ((st = order_queries("gs_sample", qp, gp, nq, plan, plan_bytes, &p, stream)) != GS_OK) return st;
-    GS_TRY(launch_sample_points(qp, gp, w.rec, index->gids, index->cell_offsets, p.order, p.point_off, p.items, T,
-                                index->tau, out_value, out_influence, p.res, stream),
-           "gs_sample: point sampler");
-    return GS_OK;
+    if ((st = plan_queries("gs_sample", qp, gp, nq, plan, plan_bytes, &p, stream)) != GS_OK) return st;
+    return sample_ordered("gs_sample: point sampler", index, qp, gp, p, out_value, out_influence, stream);
+}
+
+gs_status gs_plan_queries(const gs_query *query, const gs_grid *grid, void *plan, size_t plan_bytes,
+                          hipStream_t stream) {
+    std::string why;
+    if (!grid_valid(grid, &why)) return fail(GS_ERR_INVALID_ARGUMENT, "gs_plan_queries: %s", why.c_str());
+    gs_status st = check_query_grid("gs_plan_queries", grid, query);
+    if (st != GS_OK) return st;
+    if (query->kind == GS_QUERY_GRID) return GS_OK;
+    const GridParams gp = grid_params(grid);
+    const QueryParams qp = query_params(query, grid);
+    Plan p;
+    return plan_queries("gs_plan_queries", qp, gp, query_count(query), plan, plan_bytes, &p, stream);
+}
+
+gs_status gs_sample_planned(const gs_gaussians *gauss, const gs_index *index, const gs_query *query,
+                            float *out_value, float *out_influence, void *plan, size_t plan_bytes,
+                            hipStream_t stream) {
+    gs_status st = check_index("gs_sample_planned", gauss, index);
+    if (st != GS_OK) return st;
+    if ((st = check_query("gs_sample_planned", index, query)) != GS_OK) return st;
+    const int64_t nq = query_count(query);
+    if (nq > 0 && (!out_value || !out_influence))
+        return fail(GS_ERR_INVALID_ARGUMENT, "gs_sample_planned: output arrays are null");
+    const GridParams gp = grid_params(&index->grid);
+    const QueryParams qp = query_params(query, &index->grid);
+    if (query->kind == GS_QUERY_GRID) {
+        IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
+        GS_TRY(launch_sample_grid(qp, gp, w.rec, index->gids, index->cell_offsets, cutoff_T(index->tau), index->tau,
+                                  out_value, out_influence, stream),
+               "gs_sample_planned: grid sampler");
+        return GS_OK;
+    }
+    const size_t need = plan_layout(nullptr, nq, gp.ncells).bytes;
+    if (!plan || plan_bytes < need || !aligned(plan))
+        return fail(GS_ERR_WORKSPACE, "gs_sample_planned: plan needs %zu bytes, 256-byte aligned (got %zu)", need,
+                    plan_bytes);
+    const Plan p = plan_layout(plan, nq, gp.ncells);
+    return sample_ordered("gs_sample_planned: point sampler", index, qp, gp, p, out_value, out_influence, stream);
 }
 
 size_t gs_sample_gaussian_major_work_bytes(const gs_query *query) {

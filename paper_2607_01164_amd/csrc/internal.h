@@ -396,6 +396,10 @@ struct PlanResults {
     float2 *out;
 };
 
+// The forward's work items from the plan's per-quarter ranges (the query
+// ordering's last step).
+hipError_t launch_cell_items(int64_t nq, const GridParams &g, const uint32_t *point_off, const PointItems &it,
+                             hipStream_t s);
 hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
                                 const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,

@@ -683,11 +683,9 @@ hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const R
     return hipGetLastError();
 }
 
-hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
-                                const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
-                                const PointItems &it, float T, float tau, float *out_v, float *out_i,
-                                const PlanResults &pr, hipStream_t s) {
-    if (q.n <= 0) return hipSuccess;
+hipError_t launch_cell_items(int64_t nq, const GridParams &g, const uint32_t *point_off, const PointItems &it,
+                             hipStream_t s) {
+    if (nq <= 0) return hipSuccess;
     const int64_t nbuckets = g.ncells + 1;  // cells and the outside bucket
     // buckets 0..nbuckets-1 and one empty element after them (its offset is the total)
     const int64_t ngroups = (nbuckets + 1 + kItemGroup - 1) / kItemGroup;
@@ -703,7 +701,14 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
         e = hipGetLastError();
     }
     prof_end("cell_items", s);
-    if (e != hipSuccess) return e;
+    return e;
+}
+
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
+                                const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
+                                const PointItems &it, float T, float tau, float *out_v, float *out_i,
+                                const PlanResults &pr, hipStream_t s) {
+    if (q.n <= 0) return hipSuccess;
     prof_begin("sample_points", s);
     hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kSampWaves - 1) / kSampWaves)),
                        dim3(kSampBlock), 0, s, q, g, rec, gids, cell_off, point_off, order, it.item_off, it.items,

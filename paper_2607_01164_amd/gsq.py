@@ -34,7 +34,7 @@ EXPORTED = ("gs_query_size", "gs_index_work_bytes", "gs_build_index", "gs_plan_b
             "gs_profile_select", "gs_profile_reset", "gs_profile_read", "gs_activate", "gs_activate_backward",
             "gs_loss_work_bytes", "gs_loss", "gs_densify_work_bytes", "gs_densify",
             "gs_sample_gaussian_major_work_bytes", "gs_sample_gaussian_major", "gs_backward_pair_count",
-            "gs_sample_pair_counts", "gs_sample_backward_noalloc")
+            "gs_sample_pair_counts", "gs_sample_backward_noalloc", "gs_plan_queries", "gs_sample_planned")
 
 
 class GsLibraryMissing(RuntimeError):
@@ -107,6 +107,10 @@ def load_library():
     L.gs_plan_bytes.argtypes = [P(GsQuery), P(GsGrid)]
     L.gs_sample.restype = ctypes.c_int
     L.gs_sample.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, vp, vp, sz, vp]
+    L.gs_plan_queries.restype = ctypes.c_int
+    L.gs_plan_queries.argtypes = [P(GsQuery), P(GsGrid), vp, sz, vp]
+    L.gs_sample_planned.restype = ctypes.c_int
+    L.gs_sample_planned.argtypes = [P(GsGaussians), P(GsIndex), P(GsQuery), vp, vp, vp, sz, vp]
     L.gs_sample_gaussian_major_work_bytes.restype = sz
     L.gs_sample_gaussian_major_work_bytes.argtypes = [P(GsQuery)]
     L.gs_sample_gaussian_major.restype = ctypes.c_int
@@ -347,6 +351,32 @@ def gs_sample(gauss: Gaussians, index: Index, query: Query, out_value: torch.Ten
     st = load_library().gs_sample(ctypes.byref(g), ctypes.byref(index.c), ctypes.byref(q), out_value.data_ptr(),
                                   out_influence.data_ptr(), _ptr(plan), 0 if plan is None else plan.numel(),
                                   _stream(stream))
+    _check(st)
+
+
+def gs_plan_queries(query: Query, grid: GsGrid, plan: Optional[torch.Tensor], stream=None) -> None:
+    """The query ordering of gs_sample alone, for gs_sample_planned (it may
+    run on another stream than the index build)."""
+    q = query.c()
+    st = load_library().gs_plan_queries(ctypes.byref(q), ctypes.byref(grid), _ptr(plan),
+                                        0 if plan is None else plan.numel(), _stream(stream))
+    _check(st)
+
+
+def gs_sample_planned(gauss: Gaussians, index: Index, query: Query, out_value: torch.Tensor,
+                      out_influence: torch.Tensor, plan: Optional[torch.Tensor] = None, stream=None) -> None:
+    """gs_sample with a plan that gs_plan_queries filled for this query and
+    the index's grid."""
+    g = gauss.c()
+    q = query.c()
+    n = query.size()
+    for t, nm in ((out_value, "out_value"), (out_influence, "out_influence")):
+        _dev_f32(t, nm)
+        if t.numel() < n:
+            raise ValueError(f"{nm} needs {n} elements")
+    st = load_library().gs_sample_planned(ctypes.byref(g), ctypes.byref(index.c), ctypes.byref(q),
+                                          out_value.data_ptr(), out_influence.data_ptr(), _ptr(plan),
+                                          0 if plan is None else plan.numel(), _stream(stream))
     _check(st)
 
 

@@ -197,6 +197,35 @@ def test_sample_validates_queries():
     assert st == gs.GS_ERR_INVALID_ARGUMENT
 
 
+def test_plan_queries_and_sample_planned_validate_arguments():
+    """The two halves of gs_sample check what gs_sample checks, before any
+    device work; grid queries need no plan."""
+    L = gs.load_library()
+    g = grid((32, 32, 32))
+    qg = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(32, 32, 32), 0, None, None)
+    assert L.gs_plan_queries(ctypes.byref(qg), ctypes.byref(g), None, 0, None) == gs.GS_OK
+    qbad = gsq.GsQuery(gs.GS_QUERY_GRID, (ctypes.c_int32 * 3)(30, 32, 32), 0, None, None)
+    st = L.gs_plan_queries(ctypes.byref(qbad), ctypes.byref(g), None, 0, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"multiple" in L.gs_last_error()
+    qp = gsq.GsQuery(gs.GS_QUERY_POINTS, (ctypes.c_int32 * 3)(0, 0, 0), 100, None, FAKE)
+    st = L.gs_plan_queries(ctypes.byref(qp), ctypes.byref(g), FAKE, 16, None)
+    assert st == gs.GS_ERR_WORKSPACE and b"plan" in L.gs_last_error()
+    st = L.gs_plan_queries(ctypes.byref(qp), ctypes.byref(grid((1024, 1024, 1024))), FAKE, 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"2^30" in L.gs_last_error()
+    st = L.gs_plan_queries(None, ctypes.byref(g), FAKE, 1 << 20, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+    idx = fake_index()  # never built
+    st = L.gs_sample_planned(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(qg), FAKE, FAKE, None, 0, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT and b"not been built" in L.gs_last_error()
+    idx = built_fake_index()
+    st = L.gs_sample_planned(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(qp), FAKE, FAKE, FAKE, 16,
+                             None)
+    assert st == gs.GS_ERR_WORKSPACE and b"plan" in L.gs_last_error()
+    st = L.gs_sample_planned(ctypes.byref(fake_gauss()), ctypes.byref(idx), ctypes.byref(qp), None, FAKE, FAKE,
+                             1 << 20, None)
+    assert st == gs.GS_ERR_INVALID_ARGUMENT
+
+
 def test_ordered_queries_reject_grids_of_2_30_cells():
     """Voxel, point and jitter queries sort 32-bit keys 4 cell + quarter (the
     outside bucket last): a grid of 2^30 cells or more is refused before any
