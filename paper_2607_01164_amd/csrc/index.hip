@@ -476,10 +476,12 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
     __shared__ uint64_t mark[kExpandTile];
     __shared__ uint64_t wmax[kWavesPerBlock];
     // trim-2 boxes of the current 256 Gaussians that reach into the tile:
-    // their records [ja, jb) there, placed by the whole block
-    __shared__ int64_t t_base[kBlock];
-    __shared__ uint32_t t_ja[kBlock], t_jb[kBlock], t_ny[kBlock], t_key[kBlock], t_rb[kBlock];
-    __shared__ uint32_t t_g[kBlock];
+    // their records [ja, jb) there, placed by the whole block (up to
+    // kEmitTasks of them; a box past those places its records itself)
+    constexpr uint32_t kEmitTasks = 64;
+    __shared__ int64_t t_base[kEmitTasks];
+    __shared__ uint32_t t_ja[kEmitTasks], t_jb[kEmitTasks], t_ny[kEmitTasks], t_key[kEmitTasks], t_rb[kEmitTasks];
+    __shared__ uint32_t t_g[kEmitTasks];
     __shared__ uint32_t t_n;
     extern __shared__ uint32_t hist_lds[];  // the first pass's digits, sized at launch
     Pass0Hist hist(hist_lds, pass0);
@@ -561,13 +563,25 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
                     jb = hi;
                 }
                 const uint32_t t = atomicAdd(&t_n, 1u);
-                t_base[t] = base;
-                t_ja[t] = ja;
-                t_jb[t] = jb;
-                t_ny[t] = (uint32_t)ny;
-                t_key[t] = kcorner;
-                t_rb[t] = rb;
-                t_g[t] = (uint32_t)(gg - gfirst);
+                if (t < kEmitTasks) {
+                    t_base[t] = base;
+                    t_ja[t] = ja;
+                    t_jb[t] = jb;
+                    t_ny[t] = (uint32_t)ny;
+                    t_key[t] = kcorner;
+                    t_rb[t] = rb;
+                    t_g[t] = (uint32_t)(gg - gfirst);
+                } else {
+                    for (uint32_t j = ja; j < jb; ++j) {
+                        const RowRec cur = rr[j];
+                        const int64_t start = base + (int64_t)cur.pos;
+                        const uint32_t zz = (uint32_t)cur.row / (uint32_t)ny, yy = (uint32_t)cur.row - zz * (uint32_t)ny;
+                        const int64_t p = start > 0 ? start : 0;
+                        const uint32_t kp =
+                            kcorner + (uint32_t)Cx * yy + kdz * zz + (uint32_t)cur.first + (uint32_t)(p - start);
+                        mark[p] = ((uint64_t)(p + 1) << 52) | gbits | (uint64_t)kp;
+                    }
+                }
             } else {
                 // whole rows of nx cells: only those reaching into the tile
                 const int64_t R = ny * nz;
@@ -593,7 +607,7 @@ __global__ __launch_bounds__(kBlock) void k_emit(const uint64_t *__restrict__ pa
         }();
         __syncthreads();
         // the tasks' records, one per thread
-        const uint32_t nt = t_n;
+        const uint32_t nt = t_n < kEmitTasks ? t_n : kEmitTasks;
         for (uint32_t t = 0; t < nt; ++t) {
             const RowRec *rr = rows + t_rb[t];
             const int64_t base = t_base[t];
