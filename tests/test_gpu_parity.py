@@ -234,6 +234,36 @@ def test_index_tile_spanning_many_empty_gaussians():
     check_forward(r, phi, inf, label="wide range")
 
 
+def test_index_many_row_records_per_tile():
+    """Thin needles along the (y, z) diagonal: boxes of more than 64 rows
+    (row records) listing a few dozen cells each, so that an emit tile meets
+    more such boxes than its task slots and the rest place their own
+    records; the index keeps every reached cell, and the forward matches."""
+    n = 3000
+    rng = np.random.default_rng(95)
+    mean = rng.uniform(0.15, 0.85, size=(n, 3))
+    scale = np.tile(np.array([0.0005, 0.032, 0.0005]), (n, 1)) * rng.uniform(0.9, 1.1, size=(n, 1))
+    # rotation by 45 degrees about x: the long axis along (0, 1, 1)
+    h = np.sin(np.pi / 8)
+    rot = np.tile(np.array([np.cos(np.pi / 8), h, 0.0, 0.0]), (n, 1))
+    f = np.float32
+    g = synth.Gaussians(mean.astype(f), scale.astype(f), rot.astype(f), rng.random(n).astype(f),
+                        rng.uniform(0.2, 1.0, n).astype(f))
+    log("case needles, many row-record boxes per emit tile")
+    box, cnt = oracle.index_boxes(g, (64, 64, 64))
+    rows = (box[:, 4] - box[:, 1] + 1) * (box[:, 5] - box[:, 2] + 1)
+    # a capacity that holds a record for every row of these boxes: the
+    # records then never run out and every box is trimmed
+    r = Run(g, (64, 64, 64), "points", points=synth.random_points(96, 200000), capacity=int(rows.sum()) + 4096)
+    assert (rows > 64).mean() > 0.9, "the needles' boxes should hold more than 64 rows"
+    keys, gids, offs = r.index_arrays()
+    per_box = np.bincount(gids.astype(np.int64), minlength=n)
+    assert per_box.mean() < 32, f"{per_box.mean():.1f} pairs a box: too few boxes per tile"
+    check_index(r)
+    phi, inf = r.forward()
+    check_forward(r, phi, inf, label="needles")
+
+
 def clustered_points(seed, n, centers, sd):
     rng = np.random.default_rng(seed)
     c = np.asarray(centers, np.float64)[rng.integers(0, len(centers), n)]
