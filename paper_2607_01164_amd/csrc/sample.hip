@@ -33,6 +33,7 @@ namespace {
 // one works through the dense part.
 constexpr int kSampWaves = 1;
 constexpr int kSampBlock = kSampWaves * kWave;
+constexpr int kSampPerSimd = 7;  // waves per SIMD the point sampler is compiled for
 
 // Q' = Q log2(e) / 2 of a record at a point (record_q), G = 2^-Q'.
 __device__ __forceinline__ float cutoff_q(const Record &r, float px, float py, float pz) {
@@ -221,34 +222,39 @@ __global__ __launch_bounds__(kBlock) void k_query_keys(QueryParams q, GridParams
 }
 
 // Work items of the ordered-query sampler: one per cell holding fewer than
-// 2 kDenseMin queries, one per kDenseItem queries of a denser cell. The
-// bucket of queries outside the domain (key ncells) is an item with an
-// empty list.
+// 2 kDenseMin queries, one per dense item (64 or 128 queries, see
+// dense_item_queries) of a denser cell. The bucket of queries outside the
+// domain (key ncells) is an item with an empty list.
 constexpr uint32_t kDenseMin = 32;
 // A cell of at least 2 kDenseMin queries is dense: lanes are its queries,
-// kDenseR per lane, so each record read from LDS serves kDenseR queries
-// (one per lane leaves the walk bound by LDS reads: three 16-byte broadcast
-// reads per candidate against 13 VALU operations). Its work items take at
-// most kDenseItem queries each, the cell's queries split evenly over them.
-constexpr uint32_t kDenseR = 2;
-constexpr uint32_t kDenseItem = kDenseR * kWave;
+// one or two per lane, the cell's queries split evenly over its items. Two
+// a lane let each record read from LDS serve two queries (with one, the
+// walk is bound by LDS reads: three 16-byte broadcast reads per candidate
+// against 13 VALU operations), but make half as many items, each twice as
+// long: a launch with few items per wave slot of the chip then ends with
+// long items running alone. Two a lane are taken from kDenseBalance items
+// per wave slot at one a lane (measured: 4.6 per slot, a 2^21-point batch
+// of clustered points, runs 11 % faster with one; 218, 10^8 points, 19 %
+// faster with two).
+constexpr uint32_t kDenseBalance = 32;
 constexpr uint32_t kChunkB = 8;  // queries evaluated together by a sparse-cell item
 constexpr uint32_t kRowsMin = 4;                 // from this many queries a cell uses 4 query rows
 constexpr uint32_t kRowsMax = (kDenseMin + 3) / 4;  // queries per row at most
 
 // Work items per bucket (cell, and the outside bucket last): none for an
-// empty bucket, one for a sparse one, one per kDenseItem queries of a dense
+// empty bucket, one for a sparse one, one per dense_q queries of a dense
 // one. Dense buckets' items come first in the item list, then the sparse
 // buckets', each class in bucket order: items are taken in launch order,
 // and the long ones started first leave no long item running alone at the
 // end of the launch. The counts travel packed as (dense << 32) | sparse.
-__device__ __forceinline__ uint64_t bucket_items(const uint32_t *point_off, int64_t c, int64_t nbuckets) {
+__device__ __forceinline__ uint64_t bucket_items(const uint32_t *point_off, int64_t c, int64_t nbuckets,
+                                                 uint32_t dense_q) {
     if (c >= nbuckets) return 0ull;
     // the outside bucket (c = nbuckets - 1) has a single key
     const uint32_t n = point_off[c + 1 < nbuckets ? kSub * (c + 1) : kSub * c + 1] - point_off[kSub * c];
     if (n == 0) return 0ull;
     if (n < 2 * kDenseMin) return 1ull;
-    return (uint64_t)((n + kDenseItem - 1) / kDenseItem) << 32;
+    return (uint64_t)((n + dense_q - 1) / dense_q) << 32;
 }
 
 // Buckets are taken kItemGroup at a time (kItemsPerThread per thread).
@@ -260,12 +266,12 @@ constexpr int kItemGroup = kBlock * kItemsPerThread;  // 1024
 constexpr int64_t kInlineGroups = 1024;
 
 __global__ __launch_bounds__(kBlock) void k_item_sums(const uint32_t *__restrict__ point_off, int64_t nbuckets,
-                                                      uint64_t *__restrict__ group_sum) {
+                                                      uint32_t dense_q, uint64_t *__restrict__ group_sum) {
     __shared__ uint64_t lds[kWavesPerBlock];
     const int64_t base = (int64_t)blockIdx.x * kItemGroup + (int64_t)threadIdx.x * kItemsPerThread;
     uint64_t s = 0;
 #pragma unroll
-    for (int i = 0; i < kItemsPerThread; ++i) s += bucket_items(point_off, base + i, nbuckets);
+    for (int i = 0; i < kItemsPerThread; ++i) s += bucket_items(point_off, base + i, nbuckets, dense_q);
     uint64_t tot;
     (void)block_excl_scan(s, lds, &tot);
     if (threadIdx.x == 0) group_sum[blockIdx.x] = tot;
@@ -276,7 +282,8 @@ __global__ __launch_bounds__(kBlock) void k_item_sums(const uint32_t *__restrict
 // name bucket c. group_sum: the groups' sums, or (scanned) their exclusive
 // prefixes followed by the total.
 __global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restrict__ point_off, int64_t nbuckets,
-                                                         const uint64_t *__restrict__ group_sum, int64_t ngroups,
+                                                         uint32_t dense_q, const uint64_t *__restrict__ group_sum,
+                                                         int64_t ngroups,
                                                          bool scanned, uint32_t *__restrict__ item_off,
                                                          uint32_t *__restrict__ items, int64_t max_items) {
     __shared__ uint64_t lds[kWavesPerBlock];
@@ -303,7 +310,7 @@ __global__ __launch_bounds__(kBlock) void k_item_offsets(const uint32_t *__restr
     uint64_t s = 0;
 #pragma unroll
     for (int i = 0; i < kItemsPerThread; ++i) {
-        v[i] = bucket_items(point_off, base + i, nbuckets);
+        v[i] = bucket_items(point_off, base + i, nbuckets, dense_q);
         s += v[i];
     }
     uint64_t tot;
@@ -480,9 +487,9 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
 }
 
 // One wavefront per item, by the queries n of the cell:
-//  * n >= 64: lanes are queries, up to kDenseR each (kDenseItem queries per
-//    item, a cell's queries split evenly over its items), and walk the list
-//    together, the records staged in LDS;
+//  * n >= 64: lanes are queries, up to dense_q / 64 each (dense_q
+//    queries per item, a cell's queries split evenly over its items), and
+//    walk the list together, the records staged in LDS;
 //  * 4 <= n < 64: query rows x candidate slots (4 x 16 below 32 queries,
 //    8 x 8 from 32), records staged in LDS 64 at a time;
 //  * n < 4: lanes are the cell's candidates (64 at a time) and the queries
@@ -490,15 +497,16 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
 // Every query's sums are reduced in a fixed order.
 // Seven waves per SIMD (at most 72 VGPRs, which the row layouts' per-row
 // arrays need; eight would spill them to scratch).
-__global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
+__global__ __launch_bounds__(kSampBlock, kSampPerSimd) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
                                                          const uint32_t *__restrict__ gids,
                                                          const uint32_t *__restrict__ cell_off,
                                                          const uint32_t *__restrict__ point_off,
                                                          const uint32_t *__restrict__ order,
                                                          const uint32_t *__restrict__ item_off,
                                                          const uint32_t *__restrict__ items, int64_t max_items,
-                                                         float T, float tau, float *__restrict__ out_v,
-                                                         float *__restrict__ out_i, PlanResults pr) {
+                                                         uint32_t dense_q, float T, float tau,
+                                                         float *__restrict__ out_v, float *__restrict__ out_i,
+                                                         PlanResults pr) {
     // per wave: the records of 64 candidates, as three 1 KiB planes of
     // 16-byte quarters (quarter q of candidate s at [q][s])
     __shared__ float4 s_rec[kSampWaves][kRecordQuads * kWave];
@@ -519,7 +527,7 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
         jb = ((ConstU32 *)cell_off)[c + 1];
     }
     if (n >= 2 * kDenseMin) {
-        const uint32_t nit = (n + kDenseItem - 1) / kDenseItem;
+        const uint32_t nit = (n + dense_q - 1) / dense_q;
         const uint32_t per = (n + nit - 1) / nit;
         const uint32_t qa = pa + chunk * per;
         const uint32_t qn = pb - qa < per ? pb - qa : per;
@@ -527,8 +535,7 @@ __global__ __launch_bounds__(kSampBlock, 7) void k_sample_cells(QueryParams q, G
         if (qn <= (uint32_t)kWave)
             dense_item<1>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr, buf);
         else
-            dense_item<kDenseR>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr,
-                                buf);
+            dense_item<2>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr, buf);
         return;
     }
     if (n >= kRowsMin) {
@@ -683,21 +690,38 @@ hipError_t launch_sample_grid(const QueryParams &q, const GridParams &g, const R
     return hipGetLastError();
 }
 
+// Queries per dense work item for nq ordered queries on the current device:
+// 128 (two a lane) from kDenseBalance items per wave slot of the chip at
+// 64, else 64. The item list and the sampler both take it from nq, so they
+// agree.
+static uint32_t dense_item_queries(int64_t nq) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
+        (void)hipGetLastError();
+        cus = 256;
+    }
+    const int64_t slots = (int64_t)cus * 4 * kSampPerSimd;  // 4 SIMDs a CU
+    return nq / kWave >= (int64_t)kDenseBalance * slots ? 2u * kWave : (uint32_t)kWave;
+}
+
 hipError_t launch_cell_items(int64_t nq, const GridParams &g, const uint32_t *point_off, const PointItems &it,
                              hipStream_t s) {
     if (nq <= 0) return hipSuccess;
+    const uint32_t dense_q = dense_item_queries(nq);
     const int64_t nbuckets = g.ncells + 1;  // cells and the outside bucket
     // buckets 0..nbuckets-1 and one empty element after them (its offset is the total)
     const int64_t ngroups = (nbuckets + 1 + kItemGroup - 1) / kItemGroup;
     const bool scanned = ngroups > kInlineGroups;
     prof_begin("cell_items", s);
-    hipLaunchKernelGGL(k_item_sums, dim3((uint32_t)ngroups), dim3(kBlock), 0, s, point_off, nbuckets, it.group_sum);
+    hipLaunchKernelGGL(k_item_sums, dim3((uint32_t)ngroups), dim3(kBlock), 0, s, point_off, nbuckets, dense_q,
+                       it.group_sum);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && scanned)
         e = exclusive_scan_u64_total(it.group_sum, it.group_sum, ngroups, it.group_sum + ngroups, it.scan_work, s);
     if (e == hipSuccess) {
         hipLaunchKernelGGL(k_item_offsets, dim3((uint32_t)ngroups), dim3(kBlock), 0, s, point_off, nbuckets,
-                           it.group_sum, ngroups, scanned, it.item_off, it.items, it.max_items);
+                           dense_q, it.group_sum, ngroups, scanned, it.item_off, it.items, it.max_items);
         e = hipGetLastError();
     }
     prof_end("cell_items", s);
@@ -712,7 +736,7 @@ hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const
     prof_begin("sample_points", s);
     hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kSampWaves - 1) / kSampWaves)),
                        dim3(kSampBlock), 0, s, q, g, rec, gids, cell_off, point_off, order, it.item_off, it.items,
-                       it.max_items, T, tau, out_v, out_i, pr);
+                       it.max_items, dense_item_queries(q.n), T, tau, out_v, out_i, pr);
     prof_end("sample_points", s);
     return hipGetLastError();
 }

@@ -264,6 +264,38 @@ def test_index_many_row_records_per_tile():
     check_forward(r, phi, inf, label="needles")
 
 
+def test_dense_items_of_two_queries_a_lane():
+    """Launches with many queries give dense cells' work items two queries a
+    lane, smaller ones one (a choice by the launch's query count). A uniform
+    cloud of 2^24 points on 16^3 cells takes two a lane; its halves take one,
+    and every cell stays dense in both (about 4096 and 2048 queries), so the
+    walk visits every query's candidates in the same order: the outputs are
+    bit-identical, and a sample matches the oracle."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 1 << 24
+    # the library's rule: two a lane from 32 items per wave slot (4 SIMDs a
+    # CU, seven waves a SIMD) at one a lane
+    big = 32 * cus * 4 * 7 * 64
+    if not (n >= big > n // 2):
+        pytest.skip(f"{cus} compute units: the rule does not split 2^24 points this way")
+    g = synth.random_gaussians(97, 4096, log_mu=np.log(0.02))
+    pts = synth.random_points(98, n)
+    log(f"case dense items: {g.n} Gaussians, {n} uniform points, cells (16, 16, 16)")
+    r = Run(g, (16, 16, 16), "points", points=pts)
+    phi, inf = r.forward()
+    check_forward(r, phi, inf, sel=np.sort(np.random.default_rng(99).choice(n, 2048, replace=False)),
+                  label="two a lane")
+    del r
+    for h in range(2):
+        part = slice(h * (n // 2), (h + 1) * (n // 2))
+        rh = Run(g, (16, 16, 16), "points", points=pts[part])
+        ph, ih = rh.forward()
+        assert np.array_equal(ph.view(np.uint32), phi[part].view(np.uint32)), f"half {h}: values differ"
+        assert np.array_equal(ih.view(np.uint32), inf[part].view(np.uint32)), f"half {h}: influence differs"
+        del rh
+
+
 def clustered_points(seed, n, centers, sd):
     rng = np.random.default_rng(seed)
     c = np.asarray(centers, np.float64)[rng.integers(0, len(centers), n)]
