@@ -206,11 +206,11 @@ constexpr uint32_t kLongRow = 128;
 
 // Gaussians per wavefront: consecutive Gaussians of gorder share a wave, so
 // that their rows are found together. Below kPackMinGauss Gaussians one per
-// wave (more would leave SIMDs idle); otherwise kPack, or kPackLarge when
-// the boxes list at least kLargeBoxCells cells on average (a wave's cost
-// grows with its Gaussians' boxes, and fewer per wave balance better).
+// wave (more would leave SIMDs idle); otherwise kPack, or kPackLarge (one)
+// when the boxes list at least kLargeBoxCells cells on average (a wave's
+// cost grows with its Gaussians' boxes, and one per wave balances best).
 constexpr uint32_t kPack = 4;
-constexpr uint32_t kPackLarge = 2;
+constexpr uint32_t kPackLarge = 1;
 constexpr int64_t kPackMinGauss = 65536;
 constexpr int64_t kLargeBoxCells = 32;
 
