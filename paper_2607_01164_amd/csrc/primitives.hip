@@ -95,6 +95,7 @@ int digit_bits_for(int bits) {
     return p == 0 ? 0 : (bits + p - 1) / p;
 }
 
+template <int ITEMS>
 __global__ __launch_bounds__(kBlock) void k_radix_upsweep(const uint32_t *__restrict__ keys, int64_t n, int shift,
                                                           uint32_t mask, uint32_t ndig, uint32_t *__restrict__ table,
                                                           uint32_t nb) {
@@ -102,9 +103,9 @@ __global__ __launch_bounds__(kBlock) void k_radix_upsweep(const uint32_t *__rest
     for (uint32_t d = threadIdx.x; d < ndig; d += kBlock) h[d] = 0;
     __syncthreads();
     const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
-    const int64_t base = (int64_t)tile * kSortTile;
+    const int64_t base = (int64_t)tile * (kBlock * ITEMS);
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < ITEMS; ++i) {
         const int64_t idx = base + (int64_t)i * kBlock + threadIdx.x;
         if (idx < n) atomicAdd(&h[(keys[idx] >> shift) & mask], 1u);
     }
@@ -141,18 +142,23 @@ __global__ __launch_bounds__(kBlock) void k_digit_scan(uint32_t *__restrict__ ta
     if (threadIdx.x == 0) digit_tot[blockIdx.x] = carry;
 }
 
-// Stable scatter of one tile of kSortTile keys. Each wave ranks its
-// kSortItems rows of 64 keys in order: lanes holding the same digit are
-// found with one ballot per digit bit, and a per-wave running count per
-// digit in LDS gives each key its rank among earlier keys of the wave.
-// Waves are then combined per digit, the tile is reordered by digit in LDS
-// and written out in runs. LDS: (6 ndig + 2 kSortTile) words, dynamic.
+// Stable scatter of one tile of 64 ITEMS keys. Each wave ranks its ITEMS
+// rows of 64 keys in order: lanes holding the same digit are found with one
+// ballot per digit bit, and a per-wave running count per digit in LDS gives
+// each key its rank among earlier keys of the wave. Waves are then combined
+// per digit, the tile is reordered by digit in LDS and written out in runs.
+// The tile's place in each digit's row of the table is column tile <<
+// col_shift (a first pass counted by the keys' producer in tiles half as
+// long has col_shift 1). LDS: (2 ndig + 2 TILE) words, dynamic.
+template <int ITEMS>
 __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__restrict__ kin,
                                                             const uint32_t *__restrict__ vin,
                                                             uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
                                                             int64_t n, int shift, int dbits,
                                                             const uint32_t *__restrict__ table,
-                                                            const uint32_t *__restrict__ digit_tot, uint32_t nb) {
+                                                            const uint32_t *__restrict__ digit_tot, uint32_t nb,
+                                                            int col_shift) {
+    constexpr int TILE = kBlock * ITEMS;
     extern __shared__ uint32_t lds[];
     __shared__ uint32_t scan_lds[kWavesPerBlock];
     const uint32_t tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -162,15 +168,15 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     const uint32_t tile = xcd_block(blockIdx.x, gridDim.x);
     uint32_t *dstart = lds;                      // [ndig]
     uint32_t *dglob = dstart + ndig;             // [ndig]
-    uint32_t *sk = dglob + ndig;                 // [kSortTile]
-    uint32_t *sv = sk + kSortTile;               // [kSortTile]
+    uint32_t *sk = dglob + ndig;                 // [TILE]
+    uint32_t *sv = sk + TILE;                    // [TILE]
     // the per-wave digit counts share the tile buffers' space: they are all
-    // read before the tile is written there (kWavesPerBlock ndig <= 2 kSortTile)
+    // read before the tile is written there (kWavesPerBlock ndig <= 2 TILE)
     uint32_t *wcnt = sk;                         // [kWavesPerBlock][ndig]
-    const int64_t base = (int64_t)tile * kSortTile + (int64_t)wave * (kWave * kSortItems);
-    uint32_t k[kSortItems], v[kSortItems], r[kSortItems];
+    const int64_t base = (int64_t)tile * TILE + (int64_t)wave * (kWave * ITEMS);
+    uint32_t k[ITEMS], v[ITEMS], r[ITEMS];
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < ITEMS; ++i) {
         const int64_t idx = base + (int64_t)i * kWave + lane;
         const bool ok = idx < n;
         k[i] = ok ? kin[idx] : 0u;
@@ -185,7 +191,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     for (int j = 0; j < J; ++j) {
         const uint32_t d = tid * J + j;
         loc[j] = d < ndig ? digit_tot[d] : 0u;
-        tpre[j] = d < ndig ? table[(size_t)d * nb + tile] : 0u;
+        tpre[j] = d < ndig ? table[(size_t)d * nb + ((size_t)tile << col_shift)] : 0u;
     }
     for (uint32_t d = tid; d < ndig; d += kBlock) {
 #pragma unroll
@@ -209,7 +215,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     uint32_t *mycnt = wcnt + wave * ndig;
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < ITEMS; ++i) {
         const int64_t idx = base + (int64_t)i * kWave + lane;
         const bool ok = idx < n;
         const uint32_t d = (k[i] >> shift) & mask;
@@ -261,9 +267,9 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
         }
     }
     __syncthreads();
-    uint32_t slot[kSortItems];
+    uint32_t slot[ITEMS];
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < ITEMS; ++i) {
         const int64_t idx = base + (int64_t)i * kWave + lane;
         const uint32_t d = (k[i] >> shift) & mask;
         slot[i] = idx < n ? dstart[d] + mycnt[d] + r[i] : 0u;
@@ -271,7 +277,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
     // every counter is read before the tile overwrites their space
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < ITEMS; ++i) {
         const int64_t idx = base + (int64_t)i * kWave + lane;
         if (idx < n) {
             sk[slot[i]] = k[i];
@@ -279,10 +285,10 @@ __global__ __launch_bounds__(kBlock) void k_radix_downsweep(const uint32_t *__re
         }
     }
     __syncthreads();
-    const int64_t tile_n = n - (int64_t)tile * kSortTile;
-    const uint32_t cnt = tile_n < kSortTile ? (uint32_t)tile_n : (uint32_t)kSortTile;
+    const int64_t tile_n = n - (int64_t)tile * TILE;
+    const uint32_t cnt = tile_n < TILE ? (uint32_t)tile_n : (uint32_t)TILE;
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < ITEMS; ++i) {
         const uint32_t slot = (uint32_t)i * kBlock + tid;
         if (slot < cnt) {
             const uint32_t key = sk[slot];
@@ -469,7 +475,9 @@ RadixPass0 radix_pass0(void *work, int64_t n, int bits) {
 // and (k1, v1). The result is in (k0, v0) after an even number of passes
 // and in (k1, v1) after an odd number (radix_passes(bits)). When pass0_ready
 // the producer of the keys has already written the first pass's tile
-// histograms (radix_pass0).
+// histograms (radix_pass0, tiles of kSortTile keys). From kBigSort pairs
+// the passes take tiles of kBigItems keys a thread: half as many tiles,
+// each writing runs twice as long, and half the table to scan.
 hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n, int bits, void *work,
                             hipStream_t s, bool pass0_ready) {
     const RadixLayout L = radix_layout(work, n, bits);
@@ -485,25 +493,44 @@ hipError_t radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *
     }
     const uint32_t ndig = 1u << L.dbits;
     static_assert(kWavesPerBlock * kMaxDigits <= 2 * kSortTile, "the wave counts fit the tile buffers");
-    const size_t lds = ((size_t)2 * ndig + 2 * kSortTile) * 4;
+    static_assert(kBigItems % kSortItems == 0 && kBigItems / kSortItems == 2, "a big tile is two producer tiles");
+    const bool big = n >= kBigSort;
+    const int items = big ? kBigItems : kSortItems;
+    const uint32_t ntiles = (uint32_t)ceil_div(n, (int64_t)kBlock * items);
+    const size_t lds = ((size_t)2 * ndig + 2 * (size_t)kBlock * items) * 4;
     uint32_t *ki = k0, *vi = v0, *ko = k1, *vo = v1;
     for (int p = 0; p < L.passes; ++p) {
         const int shift = p * L.dbits;
         hipError_t e;
-        if (p > 0 || !pass0_ready) {
+        // the table's columns this pass: the producer's tiles (a first pass
+        // it counted) or the sort's own
+        uint32_t ncols = ntiles;
+        int col_shift = 0;
+        if (p == 0 && pass0_ready) {
+            ncols = L.nb;
+            col_shift = big ? 1 : 0;
+        } else {
             prof_begin("radix_upsweep", s);
-            hipLaunchKernelGGL(k_radix_upsweep, dim3(L.nb), dim3(kBlock), 0, s, ki, n, shift, ndig - 1, ndig, L.table,
-                               L.nb);
+            if (big)
+                hipLaunchKernelGGL(k_radix_upsweep<kBigItems>, dim3(ntiles), dim3(kBlock), 0, s, ki, n, shift,
+                                   ndig - 1, ndig, L.table, ncols);
+            else
+                hipLaunchKernelGGL(k_radix_upsweep<kSortItems>, dim3(ntiles), dim3(kBlock), 0, s, ki, n, shift,
+                                   ndig - 1, ndig, L.table, ncols);
             prof_end("radix_upsweep", s);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
         prof_begin("radix_scan", s);
-        hipLaunchKernelGGL(k_digit_scan, dim3(ndig), dim3(kBlock), 0, s, L.table, L.nb, L.digit_tot);
+        hipLaunchKernelGGL(k_digit_scan, dim3(ndig), dim3(kBlock), 0, s, L.table, ncols, L.digit_tot);
         prof_end("radix_scan", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         prof_begin("radix_downsweep", s);
-        hipLaunchKernelGGL(k_radix_downsweep, dim3(L.nb), dim3(kBlock), lds, s, ki, vi, ko, vo, n, shift, L.dbits,
-                           L.table, L.digit_tot, L.nb);
+        if (big)
+            hipLaunchKernelGGL(k_radix_downsweep<kBigItems>, dim3(ntiles), dim3(kBlock), lds, s, ki, vi, ko, vo, n,
+                               shift, L.dbits, L.table, L.digit_tot, ncols, col_shift);
+        else
+            hipLaunchKernelGGL(k_radix_downsweep<kSortItems>, dim3(ntiles), dim3(kBlock), lds, s, ki, vi, ko, vo, n,
+                               shift, L.dbits, L.table, L.digit_tot, ncols, col_shift);
         prof_end("radix_downsweep", s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         uint32_t *tk = ki, *tv = vi;
