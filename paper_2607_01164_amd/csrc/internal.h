@@ -33,8 +33,10 @@ constexpr int kRecordQuads = 3;  // 16-byte quarters of a Record
 // sqrt(log2(e) / 2), the factor of the record's U
 constexpr double kRecScale = 0.84932180028801904272;
 
-// Q' = |U (p - mu)|^2 = Q log2(e) / 2 in the one order of float32
-// operations every forward sampler and the pair counter use.
+// Q' = |U (p - mu)|^2 = Q log2(e) / 2 in float32, as the grid sampler,
+// the forward's sparse and row-layout cells, the Gaussian-major forward and
+// the pair counter form it (the dense cells' walk forms the same Q' from
+// offsets to the cell's centre, see offset_planes).
 __device__ __forceinline__ float record_q(const Record &r, float px, float py, float pz) {
     const float dx = px - r.f0.x, dy = py - r.f0.y, dz = pz - r.f0.z;
     const float u0 = __builtin_fmaf(r.f1.x, dx, __builtin_fmaf(r.f1.y, dy, r.f1.z * dz));
@@ -159,6 +161,9 @@ __device__ __forceinline__ float perm_xor32(float x, uint32_t lane) {
     return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((int)((lane ^ 32u) << 2), __builtin_bit_cast(int, x)));
 }
 
+__device__ __forceinline__ float readfirst_f(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, x)));
+}
 __device__ __forceinline__ float readlane_f(float x, uint32_t l) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), (int)l));
 }

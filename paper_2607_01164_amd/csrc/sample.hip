@@ -50,16 +50,57 @@ __device__ __forceinline__ void accumulate(const Record &r, float px, float py, 
     }
 }
 
-// The same sums without a branch: G is selected (0 past the cutoff) and
-// always added, so that a lane's R queries cost one select each (adding
-// w 0 and (w v) 0 leaves I and V as they are: both start at +0 and w, v are
-// finite).
-__device__ __forceinline__ void accumulate_sel(const Record &r, float px, float py, float pz, float T, float &I,
-                                               float &V) {
-    const float Q = cutoff_q(r, px, py, pz);
+// Records staged for the queries of one cell are rewritten relative to a
+// point o of the cell (its centre): the first quarter of candidate s holds
+// (-c, w) with c = U (mu - o), so that a query at a = p - o has u = U a - c,
+// six FMAs where U (p - mu) takes three subtractions and six operations.
+// Both offsets are at most a cell and a cutoff radius long, so u is formed
+// from terms of its own size plus the cell's extent in units of the
+// Gaussian's scale: the rounding of Q stays well inside the float32 band
+// of the cutoff the oracle allows (measured on the five workloads' Gaussians
+// near their cutoffs: at most 0.15 of it, against 0.07 for U (p - mu)).
+// Lane s rewrites candidate s of the wave's planes. The dense cells' walk
+// takes it: with two queries a lane it is bound by VALU issue (10^8
+// clustered points: the forward 6.6 % faster), and the items of one query a
+// lane take it too so that both give the same bits. The grid cells' walk
+// and the query rows are bound by their LDS reads; the rewrite made them
+// 1-3 % slower, and they keep U (p - mu).
+__device__ __forceinline__ void offset_planes(float4 *buf, uint32_t lane, float ox, float oy, float oz) {
+    const float4 f0 = buf[lane], f1 = buf[kWave + lane], f2 = buf[2 * kWave + lane];
+    const float bx = f0.x - ox, by = f0.y - oy, bz = f0.z - oz;
+    const float c0 = fmaf_(f1.x, bx, fmaf_(f1.y, by, f1.z * bz));
+    const float c1 = fmaf_(f2.x, by, f2.y * bz);
+    const float c2 = f2.z * bz;
+    buf[lane] = make_float4(-c0, -c1, -c2, f0.w);
+}
+
+// Q' of a rewritten record (f0 = (-c, w)) at the offset a = p - o.
+__device__ __forceinline__ float offset_q(const Record &r, float ax, float ay, float az) {
+    const float u0 = fmaf_(r.f1.x, ax, fmaf_(r.f1.y, ay, fmaf_(r.f1.z, az, r.f0.x)));
+    const float u1 = fmaf_(r.f2.x, ay, fmaf_(r.f2.y, az, r.f0.y));
+    const float u2 = fmaf_(r.f2.z, az, r.f0.z);
+    return fmaf_(u0, u0, fmaf_(u1, u1, u2 * u2));
+}
+
+// The sums without a branch: G is selected (0 past the cutoff) and always
+// added, so that a lane's queries cost one select each (adding w 0 and
+// (w v) 0 leaves I and V as they are: both start at +0 and w, v are finite).
+__device__ __forceinline__ void accumulate_off_sel(const Record &r, float ax, float ay, float az, float T, float &I,
+                                                   float &V) {
+    const float Q = offset_q(r, ax, ay, az);
     const float G = Q <= T ? exp2_hw(-Q) : 0.0f;
     I = fmaf_(r.f0.w, G, I);
     V = fmaf_(r.f1.w, G, V);
+}
+
+// The centre of cell c (float32; any point of the cell would do), for a
+// wave-uniform c: kept in scalar registers.
+__device__ __forceinline__ void cell_centre(const GridParams &g, uint32_t c, float &ox, float &oy, float &oz) {
+    const uint32_t nx = (uint32_t)g.cells[0], ny = (uint32_t)g.cells[1];
+    const uint32_t cx = c % nx, cy = (c / nx) % ny, cz = c / (nx * ny);
+    ox = readfirst_f(g.lo[0] + ((float)cx + 0.5f) / g.invc[0]);
+    oy = readfirst_f(g.lo[1] + ((float)cy + 0.5f) / g.invc[1]);
+    oz = readfirst_f(g.lo[2] + ((float)cz + 0.5f) / g.invc[2]);
 }
 
 // Walk a wave-uniform candidate list [ja, jb) for one query per lane. The
@@ -115,7 +156,15 @@ template <uint32_t R>
 __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
                                               uint32_t ja, uint32_t jb, uint32_t lane, float4 *buf,
                                               const float (&px)[R], const float (&py)[R], const float (&pz)[R],
-                                              float T, float (&I)[R], float (&V)[R]) {
+                                              float ox, float oy, float oz, float T, float (&I)[R],
+                                              float (&V)[R]) {
+    float ax[R], ay[R], az[R];
+#pragma unroll
+    for (uint32_t t = 0; t < R; ++t) {
+        ax[t] = px[t] - ox;
+        ay[t] = py[t] - oy;
+        az[t] = pz[t] - oz;
+    }
     uint32_t gnext = 0;
     if (ja < jb) gnext = gids[ja + lane < jb ? ja + lane : jb - 1];
     for (uint32_t c0 = ja; c0 < jb; c0 += kWave) {
@@ -127,6 +176,8 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
         if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
         __builtin_amdgcn_s_waitcnt(0);
         __builtin_amdgcn_wave_barrier();
+        offset_planes(buf, lane, ox, oy, oz);
+        __builtin_amdgcn_wave_barrier();
         const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
         for (uint32_t s = 0; s < cnt; ++s) {
             Record a;
@@ -134,7 +185,7 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
             a.f1 = buf[kWave + s];
             a.f2 = buf[2 * kWave + s];
 #pragma unroll
-            for (uint32_t t = 0; t < R; ++t) accumulate_sel(a, px[t], py[t], pz[t], T, I[t], V[t]);
+            for (uint32_t t = 0; t < R; ++t) accumulate_off_sel(a, ax[t], ay[t], az[t], T, I[t], V[t]);
         }
         // every lane has read the planes before the next chunk overwrites them
         __builtin_amdgcn_wave_barrier();
@@ -478,7 +529,9 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
             if ((int64_t)pid[t] < q.n) query_position(q, g, pid[t], px[t], py[t], pz[t], valid[t]);
         }
     }
-    walk_staged_r<R>(rec, gids, ja, jb, lane, buf, px, py, pz, T, I, V);
+    float ox = 0.0f, oy = 0.0f, oz = 0.0f;
+    if (c < ncells) cell_centre(g, c, ox, oy, oz);
+    walk_staged_r<R>(rec, gids, ja, jb, lane, buf, px, py, pz, ox, oy, oz, T, I, V);
 #pragma unroll
     for (uint32_t t = 0; t < R; ++t)
         if (lane + kWave * t < qn && (int64_t)pid[t] < q.n)
