@@ -56,9 +56,13 @@ __device__ __forceinline__ void accumulate(const Record &r, float px, float py, 
 // six FMAs where U (p - mu) takes three subtractions and six operations.
 // Both offsets are at most a cell and a cutoff radius long, so u is formed
 // from terms of its own size plus the cell's extent in units of the
-// Gaussian's scale: the rounding of Q stays well inside the float32 band
-// of the cutoff the oracle allows (measured on the five workloads' Gaussians
-// near their cutoffs: at most 0.15 of it, against 0.07 for U (p - mu)).
+// Gaussian's scale, and the rounding of Q' grows with that extent: on the
+// five workloads' Gaussians near their cutoffs it stays within 0.15 of the
+// float32 band of the cutoff the oracle allows (0.07 for U (p - mu)), but
+// with cells a few hundred times a Gaussian's largest scale it leaves the
+// band. Such Gaussians are flagged coarse by the preprocess (cell diagonal
+// above kOffsetCells times the largest scale), and a chunk holding one is
+// evaluated as U (p - mu).
 // Lane s rewrites candidate s of the wave's planes. The dense cells' walk
 // takes it: with two queries a lane it is bound by VALU issue (10^8
 // clustered points: the forward 6.6 % faster), and the items of one query a
@@ -85,6 +89,14 @@ __device__ __forceinline__ float offset_q(const Record &r, float ax, float ay, f
 // The sums without a branch: G is selected (0 past the cutoff) and always
 // added, so that a lane's queries cost one select each (adding w 0 and
 // (w v) 0 leaves I and V as they are: both start at +0 and w, v are finite).
+__device__ __forceinline__ void accumulate_sel(const Record &r, float px, float py, float pz, float T, float &I,
+                                               float &V) {
+    const float Q = cutoff_q(r, px, py, pz);
+    const float G = Q <= T ? exp2_hw(-Q) : 0.0f;
+    I = fmaf_(r.f0.w, G, I);
+    V = fmaf_(r.f1.w, G, V);
+}
+
 __device__ __forceinline__ void accumulate_off_sel(const Record &r, float ax, float ay, float az, float T, float &I,
                                                    float &V) {
     const float Q = offset_q(r, ax, ay, az);
@@ -153,8 +165,9 @@ __device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, cons
 // wave's LDS planes 64 records at a time as in walk_staged: each record
 // read there serves the lane's R queries.
 template <uint32_t R>
-__device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, const uint32_t *__restrict__ gids,
-                                              uint32_t ja, uint32_t jb, uint32_t lane, float4 *buf,
+__device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, const uint8_t *__restrict__ coarse,
+                                              const uint32_t *__restrict__ gids, uint32_t ja, uint32_t jb,
+                                              uint32_t lane, float4 *buf,
                                               const float (&px)[R], const float (&py)[R], const float (&pz)[R],
                                               float ox, float oy, float oz, float T, float (&I)[R],
                                               float (&V)[R]) {
@@ -173,19 +186,33 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
         for (int qq = 0; qq < kRecordQuads; ++qq)
             __builtin_amdgcn_global_load_lds((const void *)(src + qq),
                                              (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
+        const uint32_t flag = coarse[gnext];
         if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
         __builtin_amdgcn_s_waitcnt(0);
         __builtin_amdgcn_wave_barrier();
-        offset_planes(buf, lane, ox, oy, oz);
-        __builtin_amdgcn_wave_barrier();
         const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
-        for (uint32_t s = 0; s < cnt; ++s) {
-            Record a;
-            a.f0 = buf[s];
-            a.f1 = buf[kWave + s];
-            a.f2 = buf[2 * kWave + s];
+        if (__ballot(flag != 0) == 0) {
+            // every record of the chunk rewritten to offsets from o
+            offset_planes(buf, lane, ox, oy, oz);
+            __builtin_amdgcn_wave_barrier();
+            for (uint32_t s = 0; s < cnt; ++s) {
+                Record a;
+                a.f0 = buf[s];
+                a.f1 = buf[kWave + s];
+                a.f2 = buf[2 * kWave + s];
 #pragma unroll
-            for (uint32_t t = 0; t < R; ++t) accumulate_off_sel(a, ax[t], ay[t], az[t], T, I[t], V[t]);
+                for (uint32_t t = 0; t < R; ++t) accumulate_off_sel(a, ax[t], ay[t], az[t], T, I[t], V[t]);
+            }
+        } else {
+            // a coarse Gaussian in the chunk: U (p - mu) for all of it
+            for (uint32_t s = 0; s < cnt; ++s) {
+                Record a;
+                a.f0 = buf[s];
+                a.f1 = buf[kWave + s];
+                a.f2 = buf[2 * kWave + s];
+#pragma unroll
+                for (uint32_t t = 0; t < R; ++t) accumulate_sel(a, px[t], py[t], pz[t], T, I[t], V[t]);
+            }
         }
         // every lane has read the planes before the next chunk overwrites them
         __builtin_amdgcn_wave_barrier();
@@ -512,8 +539,9 @@ template <uint32_t R>
 __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t qn, uint32_t ja,
                                            uint32_t jb, uint32_t c, uint32_t ncells, const QueryParams &q,
                                            const GridParams &g, const Record *__restrict__ rec,
-                                           const uint32_t *__restrict__ gids, const uint32_t *__restrict__ order,
-                                           float T, float tau, float *__restrict__ out_v, float *__restrict__ out_i,
+                                           const uint8_t *__restrict__ coarse, const uint32_t *__restrict__ gids,
+                                           const uint32_t *__restrict__ order, float T, float tau,
+                                           float *__restrict__ out_v, float *__restrict__ out_i,
                                            const PlanResults &pr, float4 *buf) {
     float px[R], py[R], pz[R], I[R], V[R];
     uint32_t pid[R];
@@ -531,7 +559,7 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
     }
     float ox = 0.0f, oy = 0.0f, oz = 0.0f;
     if (c < ncells) cell_centre(g, c, ox, oy, oz);
-    walk_staged_r<R>(rec, gids, ja, jb, lane, buf, px, py, pz, ox, oy, oz, T, I, V);
+    walk_staged_r<R>(rec, coarse, gids, ja, jb, lane, buf, px, py, pz, ox, oy, oz, T, I, V);
 #pragma unroll
     for (uint32_t t = 0; t < R; ++t)
         if (lane + kWave * t < qn && (int64_t)pid[t] < q.n)
@@ -551,6 +579,7 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
 // Seven waves per SIMD (at most 72 VGPRs, which the row layouts' per-row
 // arrays need; eight would spill them to scratch).
 __global__ __launch_bounds__(kSampBlock, kSampPerSimd) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
+                                                         const uint8_t *__restrict__ coarse,
                                                          const uint32_t *__restrict__ gids,
                                                          const uint32_t *__restrict__ cell_off,
                                                          const uint32_t *__restrict__ point_off,
@@ -586,9 +615,11 @@ __global__ __launch_bounds__(kSampBlock, kSampPerSimd) void k_sample_cells(Query
         const uint32_t qn = pb - qa < per ? pb - qa : per;
         float4 *buf = s_rec[threadIdx.x / kWave];
         if (qn <= (uint32_t)kWave)
-            dense_item<1>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr, buf);
+            dense_item<1>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, coarse, gids, order, T, tau, out_v, out_i, pr,
+                          buf);
         else
-            dense_item<2>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, gids, order, T, tau, out_v, out_i, pr, buf);
+            dense_item<2>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, coarse, gids, order, T, tau, out_v, out_i, pr,
+                          buf);
         return;
     }
     if (n >= kRowsMin) {
@@ -781,14 +812,15 @@ hipError_t launch_cell_items(int64_t nq, const GridParams &g, const uint32_t *po
     return e;
 }
 
-hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint32_t *gids,
-                                const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint8_t *coarse,
+                                const uint32_t *gids, const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
                                 const PlanResults &pr, hipStream_t s) {
     if (q.n <= 0) return hipSuccess;
     prof_begin("sample_points", s);
     hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kSampWaves - 1) / kSampWaves)),
-                       dim3(kSampBlock), 0, s, q, g, rec, gids, cell_off, point_off, order, it.item_off, it.items,
+                       dim3(kSampBlock), 0, s, q, g, rec, coarse, gids, cell_off, point_off, order, it.item_off,
+                       it.items,
                        it.max_items, dense_item_queries(q.n), T, tau, out_v, out_i, pr);
     prof_end("sample_points", s);
     return hipGetLastError();

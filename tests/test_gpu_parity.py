@@ -296,6 +296,47 @@ def test_dense_items_of_two_queries_a_lane():
         del rh
 
 
+def test_dense_walk_keeps_small_gaussians_in_coarse_cells_exact():
+    """The dense walk forms Q' from offsets to the cell's centre, whose
+    rounding grows with the cell's size in units of the Gaussian's scale;
+    chunks that hold a Gaussian far smaller than the cells (coarse) use
+    U (p - mu). Tiny Gaussians (scales 0.0003-0.0006) in cells of 0.125, a
+    few wide ones that make every point defined, and points on the tiny
+    ones' cutoff surfaces in dense cells: every output within the oracle's
+    bar (a cutoff decision outside the float32 band would move Phi by about
+    1e-3)."""
+    rng = np.random.default_rng(101)
+    nt, per = 3000, 60
+    mean = rng.uniform(0.1, 0.9, size=(nt, 3))
+    scale = 0.0003 * rng.uniform(1.0, 2.0, size=(nt, 3))
+    q = rng.standard_normal((nt, 4))
+    q /= np.linalg.norm(q, axis=1, keepdims=True)
+    # points on each tiny Gaussian's cutoff ellipsoid (Mahalanobis radius
+    # sqrt(T), within 1e-4 of it)
+    T = 2.0 * np.log(1.0 / TAU)
+    w_, x, y, z = q.T
+    R = np.stack([np.stack([1 - 2 * (y * y + z * z), 2 * (x * y - w_ * z), 2 * (x * z + w_ * y)], -1),
+                  np.stack([2 * (x * y + w_ * z), 1 - 2 * (x * x + z * z), 2 * (y * z - w_ * x)], -1),
+                  np.stack([2 * (x * z - w_ * y), 2 * (y * z + w_ * x), 1 - 2 * (x * x + y * y)], -1)], 1)
+    d = rng.standard_normal((nt, per, 3))
+    d /= np.linalg.norm(d, axis=2, keepdims=True)
+    d *= np.sqrt(T) * (1.0 + rng.uniform(-1e-4, 1e-4, size=(nt, per, 1)))
+    pts = (mean[:, None, :] + np.einsum("nij,npj->npi", R, d * scale[:, None, :])).reshape(-1, 3)
+    # wide Gaussians under everything
+    nw = 8
+    wide_mean = rng.uniform(0.2, 0.8, size=(nw, 3))
+    f = np.float32
+    g = synth.Gaussians(np.concatenate([mean, wide_mean]).astype(f),
+                        np.concatenate([scale, np.full((nw, 3), 0.4)]).astype(f),
+                        np.concatenate([q, np.tile([1.0, 0.0, 0.0, 0.0], (nw, 1))]).astype(f),
+                        rng.random(nt + nw).astype(f), np.concatenate([rng.uniform(0.5, 1.0, nt), np.ones(nw)]).astype(f))
+    log(f"case coarse cells: {nt} tiny and {nw} wide Gaussians, {len(pts)} points on cutoff surfaces, cells (8, 8, 8)")
+    r = Run(g, (8, 8, 8), "points", points=pts.astype(f))
+    phi, inf = r.forward()
+    ref, stats = check_forward(r, phi, inf, label="coarse cells")
+    assert stats["defined"] > 0.9 * len(pts)
+
+
 def clustered_points(seed, n, centers, sd):
     rng = np.random.default_rng(seed)
     c = np.asarray(centers, np.float64)[rng.integers(0, len(centers), n)]
