@@ -132,8 +132,9 @@ typedef struct gs_query {
 int64_t gs_query_size(const gs_query *query);
 
 /* Bytes of index workspace for n_gauss Gaussians, a grid and a pair
- * capacity (per-Gaussian records, boxes, row runs and evaluation flags, row records of the
- * large boxes (one per pair of capacity), scan and sort buffers). */
+ * capacity (per-Gaussian records, boxes, row runs and evaluation flags,
+ * row records of the large boxes (one per pair of capacity), scan and sort
+ * buffers). */
 size_t gs_index_work_bytes(int64_t n_gauss, const gs_grid *grid, int64_t capacity);
 
 /*
