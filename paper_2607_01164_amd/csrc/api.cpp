@@ -133,7 +133,7 @@ struct IndexWork {
     CellBox *box;        // [n] cell boxes (first: the tests read them back)
     Record *rec;         // [n] evaluation records
     uint8_t *lines;      // [n][kLineRows] row-run bytes of the trim-1 boxes
-    uint8_t *coarse;     // [n] cells too large for the dense walk's offsets
+    uint8_t *cell_coarse;  // [ncells, 4-byte words] cells holding a Gaussian too small for the offsets
     uint32_t *rbase;     // [n] first row record of each trim-2 box
     uint32_t *rtotal;    // row records taken so far (one word)
     uint32_t *gorder;    // [n] Gaussians in spatial order
@@ -165,7 +165,7 @@ IndexWork index_layout(void *base, int64_t n, const gs_grid *g, int64_t capacity
     w.box = c.take<CellBox>(n1);
     w.rec = c.take<Record>(n1);
     w.lines = c.take<uint8_t>(n1 * kLineRows);
-    w.coarse = c.take<uint8_t>(n1);
+    w.cell_coarse = c.take<uint8_t>((size_t)((ncells_of(g) + 3) / 4) * 4);
     w.rbase = c.take<uint32_t>(n1);
     w.rtotal = c.take<uint32_t>(4);
     w.gorder = c.take<uint32_t>(n1);
@@ -575,7 +575,7 @@ gs_status gs_build_index(const gs_gaussians *gauss, const gs_grid *grid, float t
 
     GS_TRY(launch_preprocess(gauss->mean, gauss->scale, gauss->rot, gauss->value, gauss->weight, n, gp,
                              index_radius(tau), w.rec, w.box, w.lines, w.rows, w.rbase, w.rtotal, index->capacity,
-                             w.coarse, w.pair_off, w.pair_sum, stream),
+                             w.cell_coarse, w.pair_off, w.pair_sum, stream),
            "gs_build_index: preprocess");
     {
         // groups past ceil(n / 64) hold only count[n] = 0: their prefix is the total
@@ -691,7 +691,7 @@ static gs_status plan_queries(const char *who, const QueryParams &qp, const Grid
 static gs_status sample_ordered(const char *who, const gs_index *index, const QueryParams &qp, const GridParams &gp,
                                 const Plan &p, float *out_value, float *out_influence, hipStream_t stream) {
     IndexWork w = index_layout(index->work, index->n_gauss, &index->grid, index->capacity);
-    GS_TRY(launch_sample_points(qp, gp, w.rec, w.coarse, index->gids, index->cell_offsets, p.order, p.point_off, p.items,
+    GS_TRY(launch_sample_points(qp, gp, w.rec, w.cell_coarse, index->gids, index->cell_offsets, p.order, p.point_off, p.items,
                                 cutoff_T(index->tau), index->tau, out_value, out_influence, p.res, stream),
            who);
     return GS_OK;

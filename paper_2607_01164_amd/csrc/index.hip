@@ -218,7 +218,7 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
                                                        float rci, Record *__restrict__ rec, CellBox *__restrict__ box,
                                                        uint8_t *__restrict__ lines, RowRec *__restrict__ rows,
                                                        uint32_t *__restrict__ rbase, uint32_t *__restrict__ rtotal,
-                                                       int64_t rcap, uint8_t *__restrict__ coarse,
+                                                       int64_t rcap, uint8_t *__restrict__ cell_coarse,
                                                        uint64_t *__restrict__ count,
                                                        uint64_t *__restrict__ block_sum) {
     // row-run parameters and boxes of the wave's Gaussians, for the lanes
@@ -423,8 +423,10 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
         f.f0 = f.f1 = f.f2 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         rec[i] = f;
     }
-    // cells too large for the dense walk's offsets (kOffsetCells)
-    {
+    // cells too large for the dense walk's offsets (kOffsetCells): every
+    // cell of the box is marked (such a box is small against the cells;
+    // concurrent marks all write 1)
+    if (valid) {
         double d2 = 0.0;
 #pragma unroll
         for (int j = 0; j < 3; ++j) {
@@ -432,7 +434,11 @@ __global__ __launch_bounds__(kPreBlock) void k_preprocess(const float *__restric
             d2 += h * h;
         }
         const double smax = fmax(fmax((double)s[0], (double)s[1]), (double)s[2]);
-        coarse[i] = valid && sqrt(d2) > kOffsetCells * smax ? 1 : 0;
+        if (sqrt(d2) > kOffsetCells * smax)
+            for (int z = lo_c[2]; z <= hi_c[2]; ++z)
+                for (int y = lo_c[1]; y <= hi_c[1]; ++y)
+                    for (int x = lo_c[0]; x <= hi_c[0]; ++x)
+                        cell_coarse[(int64_t)x + g.cells[0] * ((int64_t)y + (int64_t)g.cells[1] * z)] = 1;
     }
 }
 
@@ -702,16 +708,17 @@ hipError_t launch_gauss_keys(const CellBox *box, int64_t n, const GridParams &g,
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec, CellBox *box,
                              uint8_t *lines, RowRec *rows, uint32_t *rbase, uint32_t *rtotal, int64_t rcap,
-                             uint8_t *coarse, uint64_t *count, uint64_t *block_sum, hipStream_t s) {
+                             uint8_t *cell_coarse, uint64_t *count, uint64_t *block_sum, hipStream_t s) {
     // one thread per Gaussian (thread 0 also writes count[n]): for n a
     // multiple of 64 the launch fits one round of the chip
     const int64_t threads = n > 0 ? n : 1;
     const uint32_t blocks = (uint32_t)((threads + kPreBlock - 1) / kPreBlock);
     prof_begin("preprocess", s);
     hipError_t e = fill_u32(rtotal, 0u, 1, s);
+    if (e == hipSuccess) e = fill_u32((uint32_t *)cell_coarse, 0u, (g.ncells + 3) / 4, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_preprocess, dim3(blocks), dim3(kPreBlock), 0, s, mean, scale, rot, value, weight, n, g, rci,
-                       rec, box, lines, rows, rbase, rtotal, rcap, coarse, count, block_sum);
+                       rec, box, lines, rows, rbase, rtotal, rcap, cell_coarse, count, block_sum);
     prof_end("preprocess", s);
     return hipGetLastError();
 }

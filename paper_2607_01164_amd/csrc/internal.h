@@ -312,17 +312,18 @@ struct GridParams {
 };
 // count[0..n] receives the pair count of every Gaussian (count[n] = 0) and
 // block_sum[b] the sum over elements [64 b, 64 b + 64) of count
-// coarse[i] = 1 when the index's cells are too large against Gaussian i's
-// scales for the dense walk's cell-centre offsets (kOffsetCells).
+// cell_coarse[c] = 1 when cell c's box list may hold a Gaussian too small
+// against the cells for the dense walk's cell-centre offsets (kOffsetCells);
+// ceil(ncells / 4) words, cleared here first.
 hipError_t launch_preprocess(const float *mean, const float *scale, const float *rot, const float *value,
                              const float *weight, int64_t n, const GridParams &g, float rci, Record *rec, CellBox *box,
                              uint8_t *lines, RowRec *rows, uint32_t *rbase, uint32_t *rtotal, int64_t rcap,
-                             uint8_t *coarse, uint64_t *count, uint64_t *block_sum, hipStream_t s);
+                             uint8_t *cell_coarse, uint64_t *count, uint64_t *block_sum, hipStream_t s);
 // A Gaussian is coarse when the cell diagonal passes kOffsetCells times its
-// largest scale: the forward's dense walk then evaluates the chunks that
-// hold it as U (p - mu) (see offset_planes).
+// largest scale: the forward's dense walk then evaluates the cells of its
+// box as U (p - mu) (see offset_planes).
 #ifndef GS_OFFSET_CELLS
-#define GS_OFFSET_CELLS 32.0
+#define GS_OFFSET_CELLS 64.0
 #endif
 constexpr double kOffsetCells = GS_OFFSET_CELLS;
 // tile_first: ceil(npairs / kSortTile) words of scratch
@@ -414,8 +415,9 @@ struct PlanResults {
 // ordering's last step).
 hipError_t launch_cell_items(int64_t nq, const GridParams &g, const uint32_t *point_off, const PointItems &it,
                              hipStream_t s);
-// coarse: the index's per-Gaussian flags (launch_preprocess).
-hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint8_t *coarse,
+// cell_coarse: the index's per-cell flags (launch_preprocess).
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec,
+                                const uint8_t *cell_coarse,
                                 const uint32_t *gids,
                                 const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,

@@ -60,9 +60,9 @@ __device__ __forceinline__ void accumulate(const Record &r, float px, float py, 
 // five workloads' Gaussians near their cutoffs it stays within 0.15 of the
 // float32 band of the cutoff the oracle allows (0.07 for U (p - mu)), but
 // with cells a few hundred times a Gaussian's largest scale it leaves the
-// band. Such Gaussians are flagged coarse by the preprocess (cell diagonal
-// above kOffsetCells times the largest scale), and a chunk holding one is
-// evaluated as U (p - mu).
+// band. The preprocess marks the cells of such Gaussians' boxes (cell
+// diagonal above kOffsetCells times the largest scale), and the dense walk
+// evaluates a marked cell as U (p - mu).
 // Lane s rewrites candidate s of the wave's planes. The dense cells' walk
 // takes it: with two queries a lane it is bound by VALU issue (10^8
 // clustered points: the forward 6.6 % faster), and the items of one query a
@@ -165,7 +165,7 @@ __device__ __forceinline__ void walk_staged(const Record *__restrict__ rec, cons
 // wave's LDS planes 64 records at a time as in walk_staged: each record
 // read there serves the lane's R queries.
 template <uint32_t R>
-__device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, const uint8_t *__restrict__ coarse,
+__device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, bool off,
                                               const uint32_t *__restrict__ gids, uint32_t ja, uint32_t jb,
                                               uint32_t lane, float4 *buf,
                                               const float (&px)[R], const float (&py)[R], const float (&pz)[R],
@@ -186,12 +186,11 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
         for (int qq = 0; qq < kRecordQuads; ++qq)
             __builtin_amdgcn_global_load_lds((const void *)(src + qq),
                                              (__attribute__((address_space(3))) void *)(buf + qq * kWave), 16, 0, 0);
-        const uint32_t flag = coarse[gnext];
         if (c0 + kWave < jb) gnext = gids[c0 + kWave + lane < jb ? c0 + kWave + lane : jb - 1];
         __builtin_amdgcn_s_waitcnt(0);
         __builtin_amdgcn_wave_barrier();
         const uint32_t cnt = jb - c0 < (uint32_t)kWave ? jb - c0 : (uint32_t)kWave;
-        if (__ballot(flag != 0) == 0) {
+        if (off) {
             // every record of the chunk rewritten to offsets from o
             offset_planes(buf, lane, ox, oy, oz);
             __builtin_amdgcn_wave_barrier();
@@ -204,7 +203,7 @@ __device__ __forceinline__ void walk_staged_r(const Record *__restrict__ rec, co
                 for (uint32_t t = 0; t < R; ++t) accumulate_off_sel(a, ax[t], ay[t], az[t], T, I[t], V[t]);
             }
         } else {
-            // a coarse Gaussian in the chunk: U (p - mu) for all of it
+            // a cell that may list a coarse Gaussian: U (p - mu)
             for (uint32_t s = 0; s < cnt; ++s) {
                 Record a;
                 a.f0 = buf[s];
@@ -539,7 +538,7 @@ template <uint32_t R>
 __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t qn, uint32_t ja,
                                            uint32_t jb, uint32_t c, uint32_t ncells, const QueryParams &q,
                                            const GridParams &g, const Record *__restrict__ rec,
-                                           const uint8_t *__restrict__ coarse, const uint32_t *__restrict__ gids,
+                                           bool off, const uint32_t *__restrict__ gids,
                                            const uint32_t *__restrict__ order, float T, float tau,
                                            float *__restrict__ out_v, float *__restrict__ out_i,
                                            const PlanResults &pr, float4 *buf) {
@@ -559,7 +558,7 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
     }
     float ox = 0.0f, oy = 0.0f, oz = 0.0f;
     if (c < ncells) cell_centre(g, c, ox, oy, oz);
-    walk_staged_r<R>(rec, coarse, gids, ja, jb, lane, buf, px, py, pz, ox, oy, oz, T, I, V);
+    walk_staged_r<R>(rec, off, gids, ja, jb, lane, buf, px, py, pz, ox, oy, oz, T, I, V);
 #pragma unroll
     for (uint32_t t = 0; t < R; ++t)
         if (lane + kWave * t < qn && (int64_t)pid[t] < q.n)
@@ -579,7 +578,7 @@ __device__ __forceinline__ void dense_item(uint32_t lane, uint32_t qa, uint32_t 
 // Seven waves per SIMD (at most 72 VGPRs, which the row layouts' per-row
 // arrays need; eight would spill them to scratch).
 __global__ __launch_bounds__(kSampBlock, kSampPerSimd) void k_sample_cells(QueryParams q, GridParams g, const Record *__restrict__ rec,
-                                                         const uint8_t *__restrict__ coarse,
+                                                         const uint8_t *__restrict__ cell_coarse,
                                                          const uint32_t *__restrict__ gids,
                                                          const uint32_t *__restrict__ cell_off,
                                                          const uint32_t *__restrict__ point_off,
@@ -609,16 +608,19 @@ __global__ __launch_bounds__(kSampBlock, kSampPerSimd) void k_sample_cells(Query
         jb = ((ConstU32 *)cell_off)[c + 1];
     }
     if (n >= 2 * kDenseMin) {
+        // offsets from the cell's centre unless the cell may list a Gaussian
+        // too small for them (see offset_planes)
+        const bool off = c >= ncells || __builtin_amdgcn_readfirstlane(cell_coarse[c]) == 0;
         const uint32_t nit = (n + dense_q - 1) / dense_q;
         const uint32_t per = (n + nit - 1) / nit;
         const uint32_t qa = pa + chunk * per;
         const uint32_t qn = pb - qa < per ? pb - qa : per;
         float4 *buf = s_rec[threadIdx.x / kWave];
         if (qn <= (uint32_t)kWave)
-            dense_item<1>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, coarse, gids, order, T, tau, out_v, out_i, pr,
+            dense_item<1>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, off, gids, order, T, tau, out_v, out_i, pr,
                           buf);
         else
-            dense_item<2>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, coarse, gids, order, T, tau, out_v, out_i, pr,
+            dense_item<2>(lane, qa, qn, ja, jb, c, ncells, q, g, rec, off, gids, order, T, tau, out_v, out_i, pr,
                           buf);
         return;
     }
@@ -812,14 +814,14 @@ hipError_t launch_cell_items(int64_t nq, const GridParams &g, const uint32_t *po
     return e;
 }
 
-hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint8_t *coarse,
+hipError_t launch_sample_points(const QueryParams &q, const GridParams &g, const Record *rec, const uint8_t *cell_coarse,
                                 const uint32_t *gids, const uint32_t *cell_off, const uint32_t *order, const uint32_t *point_off,
                                 const PointItems &it, float T, float tau, float *out_v, float *out_i,
                                 const PlanResults &pr, hipStream_t s) {
     if (q.n <= 0) return hipSuccess;
     prof_begin("sample_points", s);
     hipLaunchKernelGGL(k_sample_cells, dim3((uint32_t)((it.max_items + kSampWaves - 1) / kSampWaves)),
-                       dim3(kSampBlock), 0, s, q, g, rec, coarse, gids, cell_off, point_off, order, it.item_off,
+                       dim3(kSampBlock), 0, s, q, g, rec, cell_coarse, gids, cell_off, point_off, order, it.item_off,
                        it.items,
                        it.max_items, dense_item_queries(q.n), T, tau, out_v, out_i, pr);
     prof_end("sample_points", s);
