@@ -322,7 +322,10 @@ hipError_t launch_preprocess(const float *mean, const float *scale, const float 
 // A Gaussian is coarse when the cell diagonal passes kOffsetCells times its
 // largest scale: the forward's dense walk then evaluates the cells of its
 // box as U (p - mu) (see offset_planes).
-constexpr double kOffsetCells = 64.0;
+#ifndef GS_OFFSET_CELLS
+#define GS_OFFSET_CELLS 64.0
+#endif
+constexpr double kOffsetCells = GS_OFFSET_CELLS;
 // tile_first: ceil(npairs / kSortTile) words of scratch
 hipError_t launch_emit(const uint64_t *pair_off, const CellBox *box, const uint8_t *lines, const RowRec *rows,
                        const uint32_t *rbase, int64_t n, int64_t npairs, const GridParams &g, uint32_t *tile_first,
