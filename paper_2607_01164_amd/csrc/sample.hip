@@ -105,6 +105,21 @@ __device__ __forceinline__ void accumulate_off_sel(const Record &r, float ax, fl
     V = fmaf_(r.f1.w, G, V);
 }
 
+// Blocks are dealt round-robin over the 8 XCDs (block b on XCD b % 8). In
+// each window of 8 K blocks the K blocks of XCD x take K consecutive work
+// items, so that the items of one cell (consecutive) share that XCD's L2
+// while the windows still spread every stretch of cells over all XCDs
+// (K = 4: C5's forward 1.6 % faster, C4's unchanged).
+template <uint32_t K>
+__device__ __forceinline__ uint32_t xcd_group(uint32_t b, uint32_t nblocks) {
+    const uint32_t win = 8u * K;
+    const uint32_t full = nblocks - nblocks % win;
+    if (b >= full) return b;
+    const uint32_t r = b % win;
+    return (b - r) + (r & 7u) * K + (r >> 3);
+}
+constexpr uint32_t kXcdItems = 4;
+
 // The centre of cell c (float32; any point of the cell would do), for a
 // wave-uniform c: kept in scalar registers.
 __device__ __forceinline__ void cell_centre(const GridParams &g, uint32_t c, float &ox, float &oy, float &oz) {
@@ -593,7 +608,8 @@ __global__ __launch_bounds__(kSampBlock, kSampPerSimd) void k_sample_cells(Query
     __shared__ float4 s_rec[kSampWaves][kRecordQuads * kWave];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t ncells = (uint32_t)g.ncells;
-    const uint64_t w = (uint64_t)blockIdx.x * kSampWaves + threadIdx.x / kWave;
+    const uint32_t bid = xcd_group<kXcdItems>(blockIdx.x, gridDim.x);
+    const uint64_t w = (uint64_t)bid * kSampWaves + threadIdx.x / kWave;
     const uint32_t tot = ((ConstU32 *)item_off)[ncells + 1];
     const uint64_t total = tot < (uint64_t)max_items ? tot : (uint64_t)max_items;
     if (w >= total) return;
