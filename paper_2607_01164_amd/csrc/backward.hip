@@ -193,10 +193,14 @@ __device__ __forceinline__ void drain(const Record &r, const float4 *qu, const u
 // independent (each has its own LDS queue) and their costs vary with the
 // Gaussians' boxes; a workgroup keeps its LDS until its slowest wave ends.
 // Waves are taken in launch order (dealt round-robin over the XCDs by the
-// dispatcher), so every XCD works on the same stretch of the spatial order
-// at a time rather than on a fixed eighth of it.
+// dispatcher, four consecutive waves to an XCD), so every XCD works on the
+// same stretch of the spatial order at a time rather than on a fixed eighth
+// of it.
 constexpr int kBwdWaves = 1;
 constexpr int kBwdBlock = kBwdWaves * kWave;
+// Four consecutive waves per XCD (xcd_group): neighbouring Gaussians read
+// the same queries through one L2 (C4's backward about 1 % faster).
+constexpr uint32_t kXcdWaves = 4;
 // Element windows per step of the walk (see the window loop).
 constexpr uint32_t kBwdWindows = 2;
 static_assert(kBwdWindows == 2, "the walk's uniform steps take two windows");
@@ -316,7 +320,7 @@ __global__ __launch_bounds__(kBwdBlock) void k_backward_gauss(QueryParams q, Gri
     __shared__ uint32_t s_qk[kBwdWaves][kQueue];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t wib = threadIdx.x / kWave;
-    const uint64_t w = (uint64_t)blockIdx.x * kBwdWaves + wib;
+    const uint64_t w = (uint64_t)xcd_group<kXcdWaves>(blockIdx.x, gridDim.x) * kBwdWaves + wib;
     const uint64_t first = w * PACK;
     if (first >= (uint64_t)n_gauss) return;
     const uint32_t nk = (uint64_t)n_gauss - first < PACK ? (uint32_t)((uint64_t)n_gauss - first) : PACK;

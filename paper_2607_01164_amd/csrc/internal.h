@@ -251,6 +251,20 @@ __device__ __forceinline__ uint32_t xcd_block(uint32_t b, uint32_t nblocks) {
     return (b & 7u) * (full >> 3) + (b >> 3);
 }
 
+// Blocks are dealt round-robin over the 8 XCDs (block b on XCD b % 8). In
+// each window of 8 K blocks the K blocks of XCD x take K consecutive ids,
+// so that neighbouring work shares that XCD's L2 while the windows still
+// spread every stretch of the work over all XCDs. Blocks past the last full
+// window keep their id.
+template <uint32_t K>
+__device__ __forceinline__ uint32_t xcd_group(uint32_t b, uint32_t nblocks) {
+    const uint32_t win = 8u * K;
+    const uint32_t full = nblocks - nblocks % win;
+    if (b >= full) return b;
+    const uint32_t r = b % win;
+    return (b - r) + (r & 7u) * K + (r >> 3);
+}
+
 // --- host side ---------------------------------------------------------------
 
 struct Stream {

@@ -105,19 +105,8 @@ __device__ __forceinline__ void accumulate_off_sel(const Record &r, float ax, fl
     V = fmaf_(r.f1.w, G, V);
 }
 
-// Blocks are dealt round-robin over the 8 XCDs (block b on XCD b % 8). In
-// each window of 8 K blocks the K blocks of XCD x take K consecutive work
-// items, so that the items of one cell (consecutive) share that XCD's L2
-// while the windows still spread every stretch of cells over all XCDs
-// (K = 4: C5's forward 1.6 % faster, C4's unchanged).
-template <uint32_t K>
-__device__ __forceinline__ uint32_t xcd_group(uint32_t b, uint32_t nblocks) {
-    const uint32_t win = 8u * K;
-    const uint32_t full = nblocks - nblocks % win;
-    if (b >= full) return b;
-    const uint32_t r = b % win;
-    return (b - r) + (r & 7u) * K + (r >> 3);
-}
+// Four consecutive work items per XCD (xcd_group): the items of one cell
+// share that XCD's L2 (C5's forward 1.6 % faster, C4's unchanged).
 constexpr uint32_t kXcdItems = 4;
 
 // The centre of cell c (float32; any point of the cell would do), for a
